@@ -1,0 +1,112 @@
+/*
+ * spv_oracle.h -- plain, slow, single-threaded CPU oracle for the SPVConv hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the bench's
+ * CPU-baseline leg may load this library.  It shares no code, header, table or
+ * helper with the HIP library; the two agree only on the documented interface
+ * (argument meaning, layouts and status numbers).
+ *
+ * What it computes (paper: "Searching Efficient 3D Architectures with Sparse
+ * Point-Voxel Convolution", Sec. 3.3):
+ *   spvo_voxelize    Eq. 1 (floor quantization) and Eq. 2 (mean of the point
+ *                    features that fall into each non-empty voxel).
+ *   spvo_kernel_map  the "kernel map" of Sec. 3.2: all active synapses between
+ *                    input and output voxels, outputs restricted to input sites
+ *                    (submanifold, K=3) or to the halved grid (K=2, stride 2).
+ *   spvo_sparse_conv the convolution evaluated on that map (Sec. 3.2, 3.3
+ *                    "Feature Aggregation").
+ *   spvo_devoxelize  trilinear interpolation from the 8 neighbouring voxels
+ *                    (Sec. 3.3 "Sparse Devoxelization"), plus the point-branch
+ *                    MLP and the fusion by addition ("Point Transformation and
+ *                    Feature Fusion").
+ *   spvo_block       the SPVConv block of Fig. 2 composed from the above.
+ *
+ * All pointers are host pointers.  Feature storage dtype: 0 = float32,
+ * 1 = bfloat16 bits, 2 = float16 bits.  Accumulation is fp64; each op rounds its
+ * result once (round to nearest even) into the storage dtype.
+ */
+#ifndef SPV_ORACLE_H
+#define SPV_ORACLE_H
+#include <stdint.h>
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status numbers (identical meaning to the HIP library's) */
+#define SPVO_OK 0
+#define SPVO_ERR_INVALID_ARG 1
+#define SPVO_ERR_CAPACITY 2
+#define SPVO_ERR_RANGE 3
+#define SPVO_ERR_NONFINITE 4
+#define SPVO_ERR_UNSUPPORTED 5
+
+#define SPVO_F32 0
+#define SPVO_BF16 1
+#define SPVO_F16 2
+
+#define SPVO_DEVOX_CENTER 0
+#define SPVO_DEVOX_CORNER 1
+
+/* Voxelize n points (Eq. 1, Eq. 2).  Outputs hold up to n voxels, in ascending
+ * (batch, x, y, z) order.  feat may be NULL (C ignored): then only coordinates,
+ * counts and pt2vox are produced.  coords is [m][4] = (b, x, y, z). */
+int spvo_voxelize(const float* xyz, const int32_t* batch, int64_t n, float voxel_size,
+                  const void* feat, int32_t C, int32_t dtype,
+                  int32_t* coords, void* vfeat, int32_t* counts, int32_t* pt2vox,
+                  int64_t* m_out);
+
+/* Kernel map.  K=3 stride=1: submanifold (outputs = inputs).  K=2 stride=2:
+ * outputs = unique floor(c/2), written to out_coords in ascending order.
+ * Pairs (in, out) grouped by offset k (CSR off[K^3+1]), each group sorted by out. */
+int spvo_kernel_map(const int32_t* in_coords, int64_t m_in, int32_t K, int32_t stride,
+                    int32_t* out_coords, int64_t* m_out,
+                    int32_t* off, int32_t* pairs, int64_t pair_cap, int64_t* total);
+
+/* Sparse conv on a kernel map.  W is [K3][Cin][Cout] in the storage dtype;
+ * scale/shift are float32 [Cout] or NULL (identity); relu 0/1.
+ * transposed=1 uses each pair with its roles swapped (out, in). */
+int spvo_sparse_conv(const void* in, int64_t m_in, int32_t Cin,
+                     const int32_t* off, const int32_t* pairs, int32_t K3, int32_t transposed,
+                     const void* W, const float* scale, const float* shift, int32_t relu,
+                     void* out, int64_t m_out, int32_t Cout, int32_t dtype);
+
+/* Devoxelize from a grid of voxel size voxel_size * 2^stride_log2 (coords in
+ * that grid's units), optionally add the point MLP act(scale*(pfeat @ Wp)+shift).
+ * corner_idx [n][8] / corner_w [n][8] (optional) receive the corner voxel index
+ * (-1 if absent) and the raw trilinear weight of each corner. */
+int spvo_devoxelize(const int32_t* grid_coords, int64_t m, int32_t stride_log2,
+                    const float* xyz, const int32_t* batch, int64_t n, float voxel_size,
+                    int32_t mode, const void* vfeat, int32_t C,
+                    const void* pfeat, int32_t Cp, const void* Wp,
+                    const float* scale_p, const float* shift_p, int32_t relu_p,
+                    void* out, int32_t dtype, int32_t* corner_idx, float* corner_w);
+
+/* SPVConv block: voxelize -> submanifold map -> n_convs x (conv + scale/shift
+ * + ReLU) -> devoxelize + point MLP + add.  Channel count C throughout. */
+typedef struct {
+    int32_t C;
+    int32_t dtype;
+    float voxel_size;
+    int32_t n_convs;            /* 1 or 2 */
+    const void* W[2];           /* [27][C][C] */
+    const float* scale[2];      /* [C] or NULL */
+    const float* shift[2];      /* [C] or NULL */
+    int32_t relu[2];
+    const void* Wp;             /* [C][C] */
+    const float* scale_p;       /* [C] or NULL */
+    const float* shift_p;       /* [C] or NULL */
+    int32_t relu_p;
+    int32_t devox_mode;
+} spvo_block_params;
+
+int spvo_block(const spvo_block_params* p, const float* xyz, const int32_t* batch,
+               int64_t n, const void* feat, void* out, int64_t* m_out);
+
+/* storage conversion helpers exposed for the tests */
+double spvo_decode(const void* buf, int64_t i, int32_t dtype);
+void spvo_round_store(double x, void* buf, int64_t i, int32_t dtype);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,158 @@
+"""Pins for the oracle's kernel map and sparse convolution.
+
+Kernel maps are checked against an all-pairs brute force and closed forms on
+dense blocks; convolutions against torch's dense float64 conv3d /
+conv_transpose3d on the zero-filled grid (a submanifold convolution equals the
+dense one read at the active sites because inactive inputs are zero).
+"""
+import numpy as np
+import pytest
+
+from paper_2007_16100_amd import synth
+from tests import dense_ref
+
+
+def _rand_coords(rng, m, span, batches=1):
+    pts = set()
+    while len(pts) < m:
+        pts.add((int(rng.integers(0, batches)),) + tuple(int(x) for x in rng.integers(-span, span, size=3)))
+    return np.array(sorted(pts), np.int32)
+
+
+def _triples(off, pairs):
+    return [(k, int(pairs[p, 1]), int(pairs[p, 0])) for k in range(len(off) - 1) for p in range(off[k], off[k + 1])]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_kmap_submanifold_allpairs(oracle_lib, seed):
+    rng = np.random.default_rng(seed)
+    c = _rand_coords(rng, 120, 4, batches=2)
+    oc, off, pairs = oracle_lib.kernel_map(c, 3, 1)
+    _, trip = dense_ref.kmap_allpairs(c, 3, 1)
+    assert _triples(off, pairs) == trip  # already sorted by (k, out, in)
+    # centre offset is the identity map
+    np.testing.assert_array_equal(pairs[off[13]:off[14]], np.stack([np.arange(len(c))] * 2, 1))
+    # symmetry: map_{26-k} is map_k with roles swapped
+    for k in range(27):
+        a = {tuple(p) for p in pairs[off[k]:off[k + 1]]}
+        b = {(int(q[1]), int(q[0])) for q in pairs[off[26 - k]:off[27 - k]]}
+        assert a == b
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_kmap_strided_allpairs(oracle_lib, seed):
+    rng = np.random.default_rng(100 + seed)
+    c = _rand_coords(rng, 150, 5, batches=2)
+    oc, off, pairs = oracle_lib.kernel_map(c, 2, 2)
+    roc, trip = dense_ref.kmap_allpairs(c, 2, 2)
+    np.testing.assert_array_equal(oc, roc)
+    assert _triples(off, pairs) == trip
+    # every input appears in exactly one pair; out coords = unique floor(c/2)
+    assert sorted(pairs[:, 0].tolist()) == list(range(len(c)))
+    fl = np.concatenate([c[:, :1], np.floor_divide(c[:, 1:], 2)], 1)
+    np.testing.assert_array_equal(oc, np.unique(fl, axis=0))
+    assert len(oc) <= len(c)
+
+
+@pytest.mark.parametrize("L", [1, 2, 5, 8])
+def test_kmap_dense_block_closed_form(oracle_lib, L):
+    # a fully occupied L^3 block: sum_k |map_k| = (number of (i, j) at distance <= 1 per axis)
+    # = (3L - 2)^3 ; a stride-2 map of a 2L block gives L^3 outputs with 8 children each
+    g = np.stack(np.meshgrid(*[np.arange(L)] * 3, indexing="ij"), -1).reshape(-1, 3) - L // 2
+    c = np.concatenate([np.zeros((len(g), 1), int), g], 1).astype(np.int32)
+    _, off, _ = oracle_lib.kernel_map(c, 3, 1)
+    assert off[-1] == (3 * L - 2) ** 3
+    g2 = np.stack(np.meshgrid(*[np.arange(2 * L)] * 3, indexing="ij"), -1).reshape(-1, 3) - 2 * L
+    c2 = np.concatenate([np.zeros((len(g2), 1), int), g2], 1).astype(np.int32)
+    oc, off, _ = oracle_lib.kernel_map(c2, 2, 2)
+    assert len(oc) == L ** 3 and np.all(np.diff(off) == L ** 3)
+
+
+def test_kmap_errors(oracle_lib):
+    o = oracle_lib
+    c = np.array([[0, 0, 0, 0], [0, 0, 0, 0]], np.int32)
+    with pytest.raises(o.OracleError) as e:
+        o.kernel_map(c)
+    assert e.value.status == o.ERR_INVALID_ARG  # duplicate coordinate
+    with pytest.raises(o.OracleError) as e:
+        o.kernel_map(np.array([[0, 32767, 0, 0]], np.int32))
+    assert e.value.status == o.ERR_RANGE
+    with pytest.raises(o.OracleError) as e:
+        o.kernel_map(np.array([[0, 0, 0, 0]], np.int32), K=3, stride=2)
+    assert e.value.status == o.ERR_UNSUPPORTED
+    with pytest.raises(o.OracleError) as e:
+        o.kernel_map(np.array([[0, 0, 0, 0], [0, 0, 0, 1]], np.int32), pair_cap=3)
+    assert e.value.status == o.ERR_CAPACITY
+    oc, off, pairs = o.kernel_map(np.zeros((0, 4), np.int32))
+    assert off.tolist() == [0] * 28 and pairs.shape == (0, 2)
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_conv_subm_dense(oracle_lib, seed, dtype):
+    rng = np.random.default_rng(200 + seed)
+    c = _rand_coords(rng, 300, 5)
+    Cin, Cout = 7, 5
+    x = synth.normal((len(c), Cin), seed, dtype=dtype)
+    W = synth.conv_weight(27, Cin, Cout, seed + 1, dtype)
+    sc, sh = synth.folded_bn(Cout, seed + 2)
+    _, off, pairs = oracle_lib.kernel_map(c)
+    for scale, shift, relu in [(None, None, False), (sc, sh, True)]:
+        got = oracle_lib.sparse_conv(x, off, pairs, W, len(c), dtype, scale, shift, relu)
+        ref = dense_ref.dense_conv_subm(c, synth.from_storage(x, dtype).astype(np.float64),
+                                        synth.from_storage(W, dtype).astype(np.float64))
+        if scale is not None:
+            ref = ref * sc.astype(np.float64) + sh.astype(np.float64)
+        if relu:
+            ref = np.maximum(ref, 0.0)
+        ulp = 2.0 ** -24 if dtype == "f32" else 2.0 ** -8
+        g = synth.from_storage(got, dtype).astype(np.float64)
+        assert np.all(np.abs(g - ref) <= ulp * np.abs(ref) + 1e-12), np.max(np.abs(g - ref))
+
+
+def test_conv_identity_centre(oracle_lib):
+    rng = np.random.default_rng(5)
+    c = _rand_coords(rng, 200, 4)
+    x = synth.normal((len(c), 8), 1, dtype="bf16")
+    W = np.zeros((27, 8, 8), np.float32)
+    W[13] = np.eye(8)
+    _, off, pairs = oracle_lib.kernel_map(c)
+    got = oracle_lib.sparse_conv(x, off, pairs, synth.to_storage(W, "bf16"), len(c), "bf16")
+    np.testing.assert_array_equal(got, x)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_conv_strided_and_transposed_dense(oracle_lib, seed):
+    rng = np.random.default_rng(300 + seed)
+    c = _rand_coords(rng, 400, 6)
+    Cin, Cout = 6, 9
+    x = synth.normal((len(c), Cin), seed, dtype="f32")
+    W = synth.conv_weight(8, Cin, Cout, seed + 1, "f32")
+    oc, off, pairs = oracle_lib.kernel_map(c, 2, 2)
+    got = oracle_lib.sparse_conv(x, off, pairs, W, len(oc), "f32")
+    ref, dense = dense_ref.dense_conv_down(c, x.astype(np.float64), W.astype(np.float64), oc)
+    np.testing.assert_allclose(got, ref, rtol=1e-6, atol=1e-9)
+    # the dense output is zero away from the coarse set (no inputs there)
+    assert np.count_nonzero(np.abs(dense).sum(0) > 0) <= len(oc)
+    # transposed back onto the fine set with W_T [8][Cout][Cin]
+    WT = synth.conv_weight(8, Cout, Cin, seed + 2, "f32")
+    y = synth.normal((len(oc), Cout), seed + 3, dtype="f32")
+    gotT = oracle_lib.sparse_conv(y, off, pairs, WT, len(c), "f32", transposed=True)
+    refT = dense_ref.dense_conv_transposed(oc, y.astype(np.float64), WT.astype(np.float64), c)
+    np.testing.assert_allclose(gotT, refT, rtol=1e-6, atol=1e-9)
+
+
+def test_conv_errors(oracle_lib):
+    o = oracle_lib
+    c = np.array([[0, 0, 0, 0], [0, 0, 0, 1]], np.int32)
+    _, off, pairs = o.kernel_map(c)
+    x = np.zeros((2, 4), np.float32)
+    W = np.zeros((27, 4, 4), np.float32)
+    bad = pairs.copy()
+    bad[0, 0] = 5
+    with pytest.raises(o.OracleError) as e:
+        o.sparse_conv(x, off, bad, W, 2)
+    assert e.value.status == o.ERR_INVALID_ARG
+    with pytest.raises(o.OracleError) as e:
+        o.sparse_conv(x, off[:10], pairs, np.zeros((9, 4, 4), np.float32), 2)
+    assert e.value.status == o.ERR_UNSUPPORTED
