@@ -1,0 +1,219 @@
+/*
+ * spv.h -- C ABI of libspv.so: the SPVConv hot path on one AMD Instinct MI355X
+ * (gfx950), in hand-written HIP.
+ *
+ * The operations follow the paper "Searching Efficient 3D Architectures with
+ * Sparse Point-Voxel Convolution" (Tang et al., ECCV 2020), Sec. 3.3 and Fig. 2:
+ * a point cloud T = {(p_k, f_k)} is voxelized into a sparse tensor
+ * S = ({(p_m, f_m)}, v) through a GPU hash table, convolved with sparse
+ * convolutions built on kernel maps, and devoxelized back to the points by
+ * trilinear interpolation, where it is fused by addition with a per-point MLP.
+ *
+ * Conventions (all entry points):
+ *  - Tensor pointers are DEVICE pointers, row-major, allocated and owned by the
+ *    caller.  The library never allocates device memory.  Scratch memory (hash
+ *    tables, sort buffers, counters, the device status word) lives in a
+ *    caller-provided workspace `ws` of `ws_bytes` bytes; the size each call needs
+ *    comes from spv_workspace_bytes / spv_block_workspace_bytes.  The workspace
+ *    must be 256-byte aligned and must not be shared by calls that overlap in time.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Every call only
+ *    enqueues work on it and returns; nothing synchronizes unless an optional
+ *    host read-back pointer (`*_host`) is non-NULL.
+ *  - Sizes that only the device knows (the number of voxels m, the number of
+ *    kernel-map pairs) are exchanged through device int64 counters (`*_dev`);
+ *    host-side capacities (`*_cap`) bound every buffer.
+ *  - Host-detectable errors return before any launch with outputs untouched.
+ *    Device-detected errors (non-finite or out-of-range coordinates, exhausted
+ *    capacity) are recorded in the workspace status word: spv_status_check
+ *    (which synchronizes) or any call given a host read-back pointer returns them.
+ *    Each public call clears the status word when it starts.  After a device
+ *    error the contents of the outputs are unspecified (but every access stays
+ *    inside the caller's buffers).
+ *  - Feature storage dtype: SPV_F32, SPV_BF16 or SPV_F16; weights use the
+ *    feature dtype; feature and weight pointers must be 16-byte aligned;
+ *    BatchNorm-style scale/shift vectors are always float32.  bf16/f16 math
+ *    accumulates in fp32 on matrix cores (MFMA).
+ *  - Voxel coordinates are int32 (b, x, y, z) with x, y, z in [-32767, 32766]
+ *    and batch b in [0, 65534]; they are packed into 64-bit hash keys.
+ *    Voxel lists are in ascending (b, x, y, z) order (the canonical order).
+ */
+#ifndef SPV_H
+#define SPV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum spv_status {
+    SPV_OK = 0,
+    SPV_ERR_INVALID_ARG = 1, /* null pointer, bad size, bad voxel size / dtype / K / stride */
+    SPV_ERR_CAPACITY = 2,    /* workspace or output capacity too small */
+    SPV_ERR_RANGE = 3,       /* a voxel coordinate or batch index outside the key range */
+    SPV_ERR_NONFINITE = 4,   /* NaN or Inf in xyz */
+    SPV_ERR_UNSUPPORTED = 5, /* shape / dtype combination not implemented */
+    SPV_ERR_HIP = 6          /* HIP runtime error; see spv_last_hip_error() */
+} spv_status;
+
+typedef enum spv_dtype { SPV_F32 = 0, SPV_BF16 = 1, SPV_F16 = 2 } spv_dtype;
+
+/* Where a voxel's feature sits for trilinear interpolation (Sec. 3.3, "Sparse
+ * Devoxelization"): CENTER = at the voxel centre (q + 1/2) v, CORNER = at q v. */
+typedef enum spv_devox_mode { SPV_DEVOX_CENTER = 0, SPV_DEVOX_CORNER = 1 } spv_devox_mode;
+
+/* Workspace bytes sufficient for spv_voxelize, spv_kernel_map, spv_sparse_conv,
+ * spv_devoxelize and spv_lookup on at most max_points points / voxels. */
+size_t spv_workspace_bytes(int64_t max_points, int32_t max_C);
+
+/*
+ * spv_voxelize -- sparse voxelization (Sec. 3.3, Eq. 1 and Eq. 2).
+ *   p_hat_k = floor(p_k / v) per axis (IEEE single-precision division, floor
+ *   toward -inf); the non-empty voxels are found with a GPU hash table on the
+ *   packed (b, x, y, z) keys; f_m = (1/N_m) sum of the features of the points in
+ *   voxel m (fp32 accumulation, one rounding to dt).
+ * In:  xyz [n][3] f32; batch [n] i32 or NULL (all 0); feat [n][C] (dt) or NULL.
+ * Out: coords [cap][4] i32 (b,x,y,z) in ascending key order; vfeat [cap][C]
+ *      (dt, unused when feat is NULL); counts [cap] i32 = N_m; pt2vox [n] i32;
+ *      m_dev (device int64) = m.  Capacity cap = n suffices since m <= n.
+ *      m_host (host, optional): when non-NULL the call synchronizes, stores m
+ *      and returns any device-detected error.
+ * Errors: SPV_ERR_INVALID_ARG (v <= 0 or non-finite, n < 0, null pointers,
+ *      C <= 0 with feat), SPV_ERR_CAPACITY (ws too small), device-detected
+ *      SPV_ERR_NONFINITE (xyz) and SPV_ERR_RANGE (coordinate / batch range).
+ */
+spv_status spv_voxelize(void* stream, void* ws, size_t ws_bytes,
+                        const float* xyz, const int32_t* batch, int64_t n, float voxel_size,
+                        const void* feat, int32_t C, spv_dtype dt,
+                        int32_t* coords, void* vfeat, int32_t* counts, int32_t* pt2vox,
+                        int64_t* m_dev, int64_t* m_host);
+
+/*
+ * spv_kernel_map -- the kernel map of a sparse convolution (Sec. 3.2: all
+ * active synapses between input and output voxels; Sec. 3.3 "Feature
+ * Aggregation": built with the same GPU hash table as the voxelization).
+ *   K=3, stride=1 (submanifold): outputs = the input voxels; pair (i, j, k) iff
+ *     c_i = c_j + delta_k, delta_k in {-1,0,1}^3, k = 9(dx+1) + 3(dy+1) + (dz+1).
+ *   K=2, stride=2 (downsampling): outputs = the distinct floor(c_i / 2), written
+ *     to out_coords in ascending order; pair iff c_i = 2 c_j + delta_k with
+ *     delta_k in {0,1}^3, k = 4 dx + 2 dy + dz.  The same pairs, used with
+ *     transposed=1 in spv_sparse_conv, give the matching upsampling conv.
+ * In:  in_coords [m_cap][4] i32 (distinct); m_in_dev: device count (NULL = m_cap).
+ * Out: out_coords [m_cap][4] (stride 2 only; may be NULL for stride 1);
+ *      m_out_dev (device int64, may be NULL); off [K^3+1] i32 (CSR by offset,
+ *      device); pairs [pair_cap][2] i32 as (in, out), grouped by k and sorted by
+ *      out within a group.  total_host (optional): synchronizes and stores the
+ *      number of pairs; SPV_ERR_CAPACITY if it exceeds pair_cap (K^3 * m_cap
+ *      always suffices; for stride 2, m_cap does).
+ */
+spv_status spv_kernel_map(void* stream, void* ws, size_t ws_bytes,
+                          const int32_t* in_coords, const int64_t* m_in_dev, int64_t m_cap,
+                          int32_t K, int32_t stride,
+                          int32_t* out_coords, int64_t* m_out_dev,
+                          int32_t* off, int32_t* pairs, int64_t pair_cap, int64_t* total_host);
+
+/*
+ * spv_sparse_conv -- convolution on a kernel map (Sec. 3.2 / 3.3):
+ *   out[j] = act(scale * sum_{(i, j, k)} in[i] @ W[k] + shift)
+ * with act = ReLU when relu != 0.  transposed=1 uses every pair (i, j) with its
+ * roles swapped, which turns a stride-2 map into the upsampling conv onto the
+ * fine voxels.  Output rows with no pair get act(shift).
+ * In:  in [in_rows][Cin] (dt); off [K3+1] / pairs [pair_cap][2] from spv_kernel_map
+ *      (device; pairs past pair_cap and indices outside [0, in_rows) /
+ *      [0, m_out) are ignored); K3 = 27 or 8; W [K3][Cin][Cout] (dt);
+ *      scale/shift [Cout] f32 or NULL.
+ * Out: out [m_out_cap][Cout] (dt); rows < *m_out_dev are written (m_out_dev
+ *      NULL = m_out_cap).
+ * bf16/f16 with Cin % 8 == 0 and Cout % 16 == 0 run on MFMA; other shapes and
+ * f32 run on a vector-ALU kernel with fp32 accumulation.
+ */
+spv_status spv_sparse_conv(void* stream, void* ws, size_t ws_bytes,
+                           const void* in, int64_t in_rows, int32_t Cin,
+                           const int32_t* off, const int32_t* pairs, int64_t pair_cap,
+                           int32_t K3, int32_t transposed,
+                           const void* W, const float* scale, const float* shift, int32_t relu,
+                           void* out, const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout,
+                           spv_dtype dt);
+
+/*
+ * spv_devoxelize -- sparse devoxelization (Sec. 3.3 "Sparse Devoxelization":
+ * trilinear interpolation from the 8 neighbouring voxels) fused with the
+ * point-branch MLP and the fusion by addition ("Point Transformation and
+ * Feature Fusion"):
+ *   out_k = sum_c w_c V[idx_c] / sum_c w_c  +  act(scale_p * (pfeat_k @ Wp) + shift_p)
+ * where the grid has voxel size v * 2^stride_log2 (coordinates in its units),
+ * a = fl32(x / v) * 2^-stride_log2, u = a - 1/2 (CENTER) or a (CORNER),
+ * base = floor(u), t = u - base, corner c = (cx, cy, cz) has index
+ * 4 cx + 2 cy + cz and raw weight prod(c ? t : 1 - t) (fp32, x*y*z order);
+ * absent corners get weight 0 and the rest are renormalized; a point with no
+ * present corner gets 0 from the voxel branch.
+ * In:  grid_coords [m_cap][4] (distinct), m_dev (NULL = m_cap); vfeat [*][C];
+ *      pfeat [n][Cp] and Wp [Cp][C] (both NULL = no point branch).
+ * Out: out [n][C] (dt); corner_idx [n][8] i32 and corner_w [n][8] f32 optional.
+ */
+spv_status spv_devoxelize(void* stream, void* ws, size_t ws_bytes,
+                          const int32_t* grid_coords, const int64_t* m_dev, int64_t m_cap,
+                          int32_t stride_log2,
+                          const float* xyz, const int32_t* batch, int64_t n, float voxel_size,
+                          spv_devox_mode mode,
+                          const void* vfeat, int32_t C,
+                          const void* pfeat, int32_t Cp, const void* Wp,
+                          const float* scale_p, const float* shift_p, int32_t relu_p,
+                          void* out, spv_dtype dt, int32_t* corner_idx, float* corner_w);
+
+/* Parameters of the SPVConv block (Fig. 2): voxel branch = voxelize, n_convs
+ * submanifold 3x3x3 convs C->C, each act(scale * conv + shift); point branch =
+ * act(scale_p * (f @ Wp) + shift_p); fused by addition after devoxelization. */
+typedef struct spv_block_params {
+    int32_t C;
+    spv_dtype dtype;
+    float voxel_size;
+    int32_t n_convs;        /* 1 or 2 */
+    const void* W[2];       /* [27][C][C] (dt), device */
+    const float* scale[2];  /* [C] f32 or NULL */
+    const float* shift[2];  /* [C] f32 or NULL */
+    int32_t relu[2];
+    const void* Wp;         /* [C][C] (dt), device */
+    const float* scale_p;   /* [C] f32 or NULL */
+    const float* shift_p;   /* [C] f32 or NULL */
+    int32_t relu_p;
+    spv_devox_mode devox_mode;
+    /* Optional profiling (NULL = off): n_events >= 7 hipEvent_t handles, created
+     * by the caller, recorded on the stream at the phase boundaries:
+     * [0] start, [1] voxelized, [2] kernel map built, [3] conv plan built and
+     * weights packed, [4] conv 1 done, [5] conv 2 done (same point as [4] when
+     * n_convs == 1), [6] devoxelized (end). */
+    void* const* events;
+    int32_t n_events;
+} spv_block_params;
+
+size_t spv_block_workspace_bytes(int64_t max_points, int32_t C);
+
+/*
+ * spv_block -- one SPVConv block (Sec. 3.3, Fig. 2): the hash table built by the
+ * voxelization is reused by the kernel map and the devoxelization; the kernel
+ * map is built once and shared by the convs.  out [n][C] (dt).  m_host optional
+ * (synchronizes; returns device-detected errors).
+ */
+spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_params* p,
+                     const float* xyz, const int32_t* batch, int64_t n, const void* feat,
+                     void* out, int64_t* m_host);
+
+/* Hash-table lookups (test hook for the voxel hash of Sec. 3.3): builds the
+ * table of table_coords and writes idx[q] = index of qcoords[q] in it, or -1. */
+spv_status spv_lookup(void* stream, void* ws, size_t ws_bytes,
+                      const int32_t* table_coords, const int64_t* m_dev, int64_t m_cap,
+                      const int32_t* qcoords, int64_t q, int32_t* idx);
+
+/* Synchronizes the stream and returns the first device-detected error recorded
+ * in the workspace status word (NONFINITE before RANGE before CAPACITY). */
+spv_status spv_status_check(const void* ws, void* stream);
+
+const char* spv_status_string(spv_status s);
+int spv_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPV_H */

@@ -1,0 +1,409 @@
+// api.hip -- the extern "C" entry points of libspv.so: argument validation,
+// workspace layout and the launch sequences of each operation of the SPVConv
+// hot path (Sec. 3.3 and Fig. 2 of the paper).  No entry point allocates memory
+// or synchronizes unless a host read-back pointer is given.
+#include <math.h>
+#include <string.h>
+
+#include "spv_internal.hpp"
+
+using namespace spv;
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+spv_status hip_check() {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        return SPV_ERR_HIP;
+    }
+    return SPV_OK;
+}
+
+spv_status flags_to_status(uint32_t f) {
+    if (f & kFlagNonfinite) return SPV_ERR_NONFINITE;
+    if (f & kFlagRange) return SPV_ERR_RANGE;
+    if (f & (kFlagCapacity | kFlagTableFull)) return SPV_ERR_CAPACITY;
+    if (f & kFlagDuplicate) return SPV_ERR_INVALID_ARG;
+    return SPV_OK;
+}
+
+// synchronize and return the device status (and optionally the header)
+spv_status sync_status(hipStream_t s, const Header* h, Header* out) {
+    Header tmp;
+    if (hipMemcpyAsync(&tmp, h, sizeof(Header), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return hip_check() == SPV_OK ? SPV_ERR_HIP : SPV_ERR_HIP;
+    if (out) *out = tmp;
+    return flags_to_status(tmp.status);
+}
+
+bool valid_dt(int dt) { return dt == SPV_F32 || dt == SPV_BF16 || dt == SPV_F16; }
+size_t esize(int dt) { return dt == SPV_F32 ? 4 : 2; }
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+bool valid_v(float v) { return isfinite(v) && v > 0.0f; }
+
+// --- workspace layouts (a null base gives the size) -----------------------------
+struct VoxLayout {
+    Header* h;
+    VoxelizeWs w;
+};
+size_t layout_voxelize(void* ws, size_t bytes, int64_t n, VoxLayout& L) {
+    Arena a(ws, bytes);
+    L.h = a.take<Header>(1);
+    plan_voxelize_ws(a, L.w, n);
+    L.w.h = L.h;
+    return a.used;
+}
+
+struct MapLayout {
+    Header* h;
+    KmapWs w;
+};
+size_t layout_kmap(void* ws, size_t bytes, int64_t m_cap, int K, int stride, MapLayout& L) {
+    Arena a(ws, bytes);
+    L.h = a.take<Header>(1);
+    plan_kmap_ws(a, L.w, m_cap, K, stride, true);
+    L.w.h = L.h;
+    return a.used;
+}
+
+struct ConvLayout {
+    Header* h;
+    ConvPlan p;
+    void* wpack;
+};
+size_t layout_conv(void* ws, size_t bytes, int64_t m_out_cap, int K3, int Cin, int Cout, ConvLayout& L) {
+    Arena a(ws, bytes);
+    L.h = a.take<Header>(1);
+    plan_conv_ws(a, L.p, m_out_cap, K3);
+    L.wpack = plan_wpack_ws(a, K3, Cin, Cout > 16 ? Cout : 16);
+    return a.used;
+}
+
+struct DevoxLayout {
+    Header* h;
+    Table t;
+    void* wpack;
+    int32_t* cidx;
+    float* cw;
+};
+size_t layout_devox(void* ws, size_t bytes, int64_t m_cap, int64_t n, int C, int Cp, DevoxLayout& L) {
+    Arena a(ws, bytes);
+    L.h = a.take<Header>(1);
+    uint32_t S = table_capacity(m_cap > 0 ? m_cap : 1);
+    L.t.keys = a.take<uint64_t>(S);
+    L.t.vals = a.take<int32_t>(S);
+    L.t.mask = S - 1;
+    L.wpack = plan_devox_ws(a, C, Cp);
+    int64_t nn = n > 0 ? n : 1;
+    L.cidx = a.take<int32_t>(8 * nn);
+    L.cw = a.take<float>(8 * nn);
+    return a.used;
+}
+
+struct BlockLayout {
+    Header* h;
+    VoxelizeWs vox;
+    KmapWs map;
+    ConvPlan plan;
+    int32_t* coords;
+    int32_t* counts;
+    int32_t* pt2vox;
+    int64_t* m_dev;
+    void* va;
+    void* vb;
+    int32_t* off;
+    int32_t* pairs;
+    int64_t pair_cap;
+    void* wpack_conv[2];
+    void* wpack_mlp;
+    int32_t* cidx;
+    float* cw;
+};
+size_t layout_block(void* ws, size_t bytes, int64_t n, int C, int dt, BlockLayout& L) {
+    Arena a(ws, bytes);
+    const int64_t nn = n > 0 ? n : 1;
+    L.h = a.take<Header>(1);
+    plan_voxelize_ws(a, L.vox, nn);
+    L.vox.h = L.h;
+    L.map.h = L.h;
+    L.map.fine = L.vox.table;  // the voxelization's table serves the kernel map and the devoxelization
+    plan_kmap_ws(a, L.map, nn, 3, 1, false);
+    plan_conv_ws(a, L.plan, nn, 27);
+    L.coords = a.take<int32_t>(4 * nn);
+    L.counts = a.take<int32_t>(nn);
+    L.pt2vox = a.take<int32_t>(nn);
+    L.m_dev = a.take<int64_t>(1);
+    L.va = a.take<char>((size_t)nn * C * esize(dt));
+    L.vb = a.take<char>((size_t)nn * C * esize(dt));
+    L.off = a.take<int32_t>(28);
+    L.pair_cap = 27 * nn;
+    L.pairs = a.take<int32_t>(2 * L.pair_cap);
+    L.wpack_conv[0] = plan_wpack_ws(a, 27, C, C > 16 ? C : 16);
+    L.wpack_conv[1] = plan_wpack_ws(a, 27, C, C > 16 ? C : 16);
+    L.wpack_mlp = plan_devox_ws(a, C, C);
+    L.cidx = a.take<int32_t>(8 * nn);
+    L.cw = a.take<float>(8 * nn);
+    return a.used;
+}
+
+spv_status need(size_t needed, size_t have) { return needed <= have ? SPV_OK : SPV_ERR_CAPACITY; }
+
+}  // namespace
+
+extern "C" {
+
+size_t spv_workspace_bytes(int64_t max_points, int32_t max_C) {
+    if (max_points < 0) max_points = 0;
+    if (max_C < 16) max_C = 16;
+    VoxLayout v;
+    MapLayout m;
+    ConvLayout c;
+    DevoxLayout d;
+    size_t s = layout_voxelize(nullptr, 0, max_points, v);
+    s = std::max(s, layout_kmap(nullptr, 0, max_points, 3, 1, m));
+    s = std::max(s, layout_kmap(nullptr, 0, max_points, 2, 2, m));
+    s = std::max(s, layout_conv(nullptr, 0, max_points, 27, max_C, max_C, c));
+    s = std::max(s, layout_devox(nullptr, 0, max_points, max_points, max_C, max_C, d));
+    return s;
+}
+
+size_t spv_block_workspace_bytes(int64_t max_points, int32_t C) {
+    BlockLayout L;
+    return layout_block(nullptr, 0, max_points < 0 ? 0 : max_points, C < 16 ? 16 : C, SPV_F32, L);
+}
+
+const char* spv_status_string(spv_status s) {
+    switch (s) {
+        case SPV_OK: return "ok";
+        case SPV_ERR_INVALID_ARG: return "invalid argument";
+        case SPV_ERR_CAPACITY: return "capacity too small";
+        case SPV_ERR_RANGE: return "coordinate out of range";
+        case SPV_ERR_NONFINITE: return "non-finite coordinate";
+        case SPV_ERR_UNSUPPORTED: return "unsupported";
+        case SPV_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown";
+}
+
+int spv_last_hip_error(void) { return g_last_hip_error; }
+
+spv_status spv_status_check(const void* ws, void* stream) {
+    if (!ws) return SPV_ERR_INVALID_ARG;
+    return sync_status((hipStream_t)stream, (const Header*)ws, nullptr);
+}
+
+spv_status spv_voxelize(void* stream, void* ws, size_t ws_bytes, const float* xyz, const int32_t* batch, int64_t n,
+                        float voxel_size, const void* feat, int32_t C, spv_dtype dt, int32_t* coords, void* vfeat,
+                        int32_t* counts, int32_t* pt2vox, int64_t* m_dev, int64_t* m_host) {
+    if (!ws || n < 0 || n >= ((int64_t)1 << 31) || !valid_v(voxel_size)) return SPV_ERR_INVALID_ARG;
+    if (n > 0 && (!xyz || !coords || !counts || !pt2vox)) return SPV_ERR_INVALID_ARG;
+    if (feat && (C <= 0 || !vfeat || !valid_dt(dt))) return SPV_ERR_INVALID_ARG;
+    if (((uintptr_t)ws & 255u) != 0) return SPV_ERR_INVALID_ARG;
+    VoxLayout L;
+    if (need(layout_voxelize(nullptr, 0, n, L), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_voxelize(ws, ws_bytes, n, L);
+    if (feat && (!aligned16(feat) || !aligned16(vfeat))) return SPV_ERR_INVALID_ARG;
+    hipStream_t s = (hipStream_t)stream;
+    launch_voxelize(s, L.w, xyz, batch, n, voxel_size, feat, C, dt, coords, vfeat, counts, pt2vox, m_dev);
+    spv_status st = hip_check();
+    if (st || !m_host) return st;
+    Header h;
+    st = sync_status(s, L.h, &h);
+    *m_host = st ? 0 : (h.m > n ? n : h.m);
+    return st;
+}
+
+spv_status spv_lookup(void* stream, void* ws, size_t ws_bytes, const int32_t* table_coords, const int64_t* m_dev,
+                      int64_t m_cap, const int32_t* qcoords, int64_t q, int32_t* idx) {
+    if (!ws || m_cap < 0 || q < 0 || (m_cap > 0 && !table_coords) || (q > 0 && (!qcoords || !idx)))
+        return SPV_ERR_INVALID_ARG;
+    Arena probe(nullptr, 0);
+    probe.take<Header>(1);
+    uint32_t S = table_capacity(m_cap > 0 ? m_cap : 1);
+    probe.take<uint64_t>(S);
+    probe.take<int32_t>(S);
+    if (need(probe.used, ws_bytes)) return SPV_ERR_CAPACITY;
+    Arena a(ws, ws_bytes);
+    Header* h = a.take<Header>(1);
+    Table t{a.take<uint64_t>(S), a.take<int32_t>(S), S - 1};
+    hipStream_t s = (hipStream_t)stream;
+    launch_clear(s, h, t, true);
+    if (m_cap > 0) launch_table_build(s, h, t, table_coords, m_dev, m_cap);
+    launch_table_lookup(s, t, qcoords, q, idx);
+    return hip_check();
+}
+
+spv_status spv_kernel_map(void* stream, void* ws, size_t ws_bytes, const int32_t* in_coords, const int64_t* m_in_dev,
+                          int64_t m_cap, int32_t K, int32_t stride, int32_t* out_coords, int64_t* m_out_dev,
+                          int32_t* off, int32_t* pairs, int64_t pair_cap, int64_t* total_host) {
+    if (!ws || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || !off || pair_cap < 0) return SPV_ERR_INVALID_ARG;
+    if (m_cap > 0 && !in_coords) return SPV_ERR_INVALID_ARG;
+    if (!((K == 3 && stride == 1) || (K == 2 && stride == 2))) return SPV_ERR_UNSUPPORTED;
+    if (stride == 2 && !out_coords) return SPV_ERR_INVALID_ARG;
+    if (pair_cap > 0 && !pairs) return SPV_ERR_INVALID_ARG;
+    MapLayout L;
+    if (need(layout_kmap(nullptr, 0, m_cap, K, stride, L), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_kmap(ws, ws_bytes, m_cap, K, stride, L);
+    hipStream_t s = (hipStream_t)stream;
+    launch_clear_header(s, L.h);
+    launch_kernel_map(s, L.w, true, in_coords, m_in_dev, m_cap, K, stride, out_coords, m_out_dev, off, pairs,
+                      pair_cap);
+    spv_status st = hip_check();
+    if (st || !total_host) return st;
+    const int K3 = K * K * K;
+    int32_t tot = 0;
+    if (hipMemcpyAsync(&tot, off + K3, sizeof(int32_t), hipMemcpyDeviceToHost, s) != hipSuccess) return hip_check();
+    st = sync_status(s, L.h, nullptr);
+    *total_host = tot;
+    if (st == SPV_OK && tot > pair_cap) st = SPV_ERR_CAPACITY;
+    return st;
+}
+
+spv_status spv_sparse_conv(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows, int32_t Cin,
+                           const int32_t* off, const int32_t* pairs, int64_t pair_cap, int32_t K3, int32_t transposed,
+                           const void* W, const float* scale, const float* shift, int32_t relu, void* out,
+                           const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
+    if (!ws || in_rows < 0 || m_out_cap < 0 || m_out_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !off ||
+        !W || pair_cap < 0 || !valid_dt(dt))
+        return SPV_ERR_INVALID_ARG;
+    if (!(K3 == 27 || K3 == 8)) return SPV_ERR_UNSUPPORTED;
+    if ((in_rows > 0 && !in) || (m_out_cap > 0 && !out) || (pair_cap > 0 && !pairs)) return SPV_ERR_INVALID_ARG;
+    if (!aligned16(in) || !aligned16(out) || !aligned16(W)) return SPV_ERR_INVALID_ARG;
+    ConvLayout L;
+    if (need(layout_conv(nullptr, 0, m_out_cap, K3, Cin, Cout, L), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_conv(ws, ws_bytes, m_out_cap, K3, Cin, Cout, L);
+    if (m_out_cap == 0) return SPV_OK;
+    hipStream_t s = (hipStream_t)stream;
+    L.p.m_out_dev = m_out_dev;
+    launch_clear_header(s, L.h);
+    launch_conv_plan(s, L.p, off, pairs, K3, transposed, pair_cap);
+    launch_conv_pack(s, K3, W, L.wpack, Cin, Cout, dt);
+    launch_conv_run(s, L.p, in, Cin, in_rows, W, L.wpack, scale, shift, relu, out, Cout, dt);
+    return hip_check();
+}
+
+spv_status spv_devoxelize(void* stream, void* ws, size_t ws_bytes, const int32_t* grid_coords, const int64_t* m_dev,
+                          int64_t m_cap, int32_t stride_log2, const float* xyz, const int32_t* batch, int64_t n,
+                          float voxel_size, spv_devox_mode mode, const void* vfeat, int32_t C, const void* pfeat,
+                          int32_t Cp, const void* Wp, const float* scale_p, const float* shift_p, int32_t relu_p,
+                          void* out, spv_dtype dt, int32_t* corner_idx, float* corner_w) {
+    if (!ws || n < 0 || n >= ((int64_t)1 << 31) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || C <= 0 ||
+        !valid_dt(dt) || !valid_v(voxel_size) || stride_log2 < 0 || stride_log2 > 15)
+        return SPV_ERR_INVALID_ARG;
+    if (mode != SPV_DEVOX_CENTER && mode != SPV_DEVOX_CORNER) return SPV_ERR_INVALID_ARG;
+    if ((n > 0 && (!xyz || !out)) || (m_cap > 0 && (!grid_coords || !vfeat))) return SPV_ERR_INVALID_ARG;
+    if (pfeat && (Cp <= 0 || !Wp)) return SPV_ERR_INVALID_ARG;
+    if ((corner_idx == nullptr) != (corner_w == nullptr)) return SPV_ERR_INVALID_ARG;
+    if (!aligned16(vfeat) || !aligned16(out) || !aligned16(pfeat) || !aligned16(Wp)) return SPV_ERR_INVALID_ARG;
+    const int cp = pfeat ? Cp : 0;
+    DevoxLayout L;
+    if (need(layout_devox(nullptr, 0, m_cap, n, C, cp, L), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_devox(ws, ws_bytes, m_cap, n, C, cp, L);
+    hipStream_t s = (hipStream_t)stream;
+    launch_clear(s, L.h, L.t, true);
+    if (m_cap > 0) launch_table_build(s, L.h, L.t, grid_coords, m_dev, m_cap);
+    DevoxArgs a;
+    a.table = L.t;
+    a.stride_log2 = stride_log2;
+    a.xyz = xyz;
+    a.batch = batch;
+    a.n = n;
+    a.voxel_size = voxel_size;
+    a.mode = mode;
+    a.vfeat = vfeat;
+    a.C = C;
+    a.pfeat = pfeat;
+    a.Cp = cp;
+    a.Wp = Wp;
+    a.scale_p = scale_p;
+    a.shift_p = shift_p;
+    a.relu_p = relu_p;
+    a.out = out;
+    a.dt = dt;
+    a.corner_idx = corner_idx;
+    a.corner_w = corner_w;
+    a.h = L.h;
+    launch_devox(s, a, L.wpack, L.cidx, L.cw);
+    return hip_check();
+}
+
+spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_params* p, const float* xyz,
+                     const int32_t* batch, int64_t n, const void* feat, void* out, int64_t* m_host) {
+    if (!ws || !p || n < 0 || n >= ((int64_t)1 << 31) || p->C <= 0 || !valid_dt(p->dtype) ||
+        !valid_v(p->voxel_size))
+        return SPV_ERR_INVALID_ARG;
+    if (p->n_convs < 1 || p->n_convs > 2 || !p->Wp) return SPV_ERR_INVALID_ARG;
+    if (p->devox_mode != SPV_DEVOX_CENTER && p->devox_mode != SPV_DEVOX_CORNER) return SPV_ERR_INVALID_ARG;
+    for (int l = 0; l < p->n_convs; ++l)
+        if (!p->W[l] || !aligned16(p->W[l])) return SPV_ERR_INVALID_ARG;
+    if (n > 0 && (!xyz || !feat || !out)) return SPV_ERR_INVALID_ARG;
+    if (!aligned16(feat) || !aligned16(out) || !aligned16(p->Wp)) return SPV_ERR_INVALID_ARG;
+    const int C = p->C, dt = p->dtype;
+    BlockLayout L;
+    if (need(layout_block(nullptr, 0, n, C, dt, L), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_block(ws, ws_bytes, n, C, dt, L);
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t nn = n > 0 ? n : 1;
+    const bool prof = p->events && p->n_events >= 7;
+    auto mark = [&](int i) {
+        if (prof) hipEventRecord((hipEvent_t)p->events[i], s);
+    };
+    mark(0);
+    // voxel branch: Eq. 1-2 into the hashed grid
+    launch_voxelize(s, L.vox, xyz, batch, n, p->voxel_size, feat, C, dt, L.coords, L.va, L.counts, L.pt2vox, L.m_dev);
+    mark(1);
+    // one kernel map for both convs, probing the voxelization's table
+    launch_kernel_map(s, L.map, false, L.coords, L.m_dev, nn, 3, 1, nullptr, nullptr, L.off, L.pairs, L.pair_cap);
+    mark(2);
+    L.plan.m_out_dev = L.m_dev;
+    launch_conv_plan(s, L.plan, L.off, L.pairs, 27, 0, L.pair_cap);
+    for (int l = 0; l < p->n_convs; ++l) launch_conv_pack(s, 27, p->W[l], L.wpack_conv[l], C, C, dt);
+    mark(3);
+    void* cur = L.va;
+    void* nxt = L.vb;
+    for (int l = 0; l < p->n_convs; ++l) {
+        launch_conv_run(s, L.plan, cur, C, nn, p->W[l], L.wpack_conv[l], p->scale[l], p->shift[l], p->relu[l], nxt,
+                        C, dt);
+        void* t = cur;
+        cur = nxt;
+        nxt = t;
+        mark(4 + l);
+    }
+    if (p->n_convs == 1) mark(5);
+    // devoxelize onto the points + point MLP + fusion by addition
+    DevoxArgs a;
+    a.table = L.vox.table;
+    a.stride_log2 = 0;
+    a.xyz = xyz;
+    a.batch = batch;
+    a.n = n;
+    a.voxel_size = p->voxel_size;
+    a.mode = p->devox_mode;
+    a.vfeat = cur;
+    a.C = C;
+    a.pfeat = feat;
+    a.Cp = C;
+    a.Wp = p->Wp;
+    a.scale_p = p->scale_p;
+    a.shift_p = p->shift_p;
+    a.relu_p = p->relu_p;
+    a.out = out;
+    a.dt = dt;
+    a.corner_idx = nullptr;
+    a.corner_w = nullptr;
+    a.h = L.h;
+    launch_devox(s, a, L.wpack_mlp, L.cidx, L.cw);
+    mark(6);
+    spv_status st = hip_check();
+    if (st || !m_host) return st;
+    Header h;
+    st = sync_status(s, L.h, &h);
+    *m_host = st ? 0 : (h.m > n ? n : h.m);
+    return st;
+}
+
+}  // extern "C"

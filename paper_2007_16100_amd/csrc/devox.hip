@@ -1,0 +1,285 @@
+// devox.hip -- sparse devoxelization (Sec. 3.3 "Sparse Devoxelization": trilinear
+// interpolation from the 8 neighbouring voxels, looked up in the voxel hash) fused
+// with the point-branch MLP and the fusion by addition ("Point Transformation and
+// Feature Fusion").
+//
+// MFMA path (bf16/f16): a wave owns 16 points.  Each lane computes two of the
+// 8 corners of one point (hash probes + raw trilinear weights), the weights are
+// renormalized over the present corners with two cross-lane sums, the point MLP
+// runs as a 16 x C x Cp MFMA GEMM with the point rows as the A operand, and the
+// epilogue blends the 8 corner rows into each output element before the single
+// write of the fused result.
+#include "spv_internal.hpp"
+
+namespace spv {
+
+// corner geometry of one point; the float arithmetic is kept in this exact order
+// (no contraction) so corner indices and raw weights are reproducible bit for bit
+struct Corners {
+    int b;
+    int base[3];
+    float t[3];
+    bool ok;
+};
+
+#pragma clang fp contract(off)
+__device__ inline Corners point_corners(const float* xyz, const int32_t* batch, int64_t k, float v, float sfac,
+                                        int mode) {
+    Corners c;
+    c.b = batch ? batch[k] : 0;
+    c.ok = c.b >= 0 && c.b <= kBatchMax;
+#pragma unroll
+    for (int d = 0; d < 3; ++d) {
+        const float x = xyz[3 * k + d];
+        const float a = x / v;  // the same quantity as Eq. 1 before the floor
+        const float fa = floorf(a);
+        c.ok = c.ok && isfinite(x) && isfinite(a) && fa >= (float)kCoordMin && fa <= (float)kCoordMax;
+        const float as = a * sfac;  // exact scaling by 2^-stride_log2
+        const float u = (mode == SPV_DEVOX_CENTER) ? as - 0.5f : as;
+        const float fb = floorf(u);
+        c.base[d] = c.ok ? (int)fb : 0;
+        c.t[d] = c.ok ? u - fb : 0.f;
+    }
+    return c;
+}
+
+__device__ inline float corner_weight(const Corners& c, int cc) {
+    const int cx = (cc >> 2) & 1, cy = (cc >> 1) & 1, cz = cc & 1;
+    const float wx = cx ? c.t[0] : 1.0f - c.t[0];
+    const float wy = cy ? c.t[1] : 1.0f - c.t[1];
+    const float wz = cz ? c.t[2] : 1.0f - c.t[2];
+    float w = wx * wy;
+    w = w * wz;
+    return w;
+}
+#pragma clang fp contract(on)
+
+__device__ inline int32_t corner_lookup(Table t, const Corners& c, int cc) {
+    if (!c.ok) return -1;
+    return table_find(t, pack_key(c.b, c.base[0] + ((cc >> 2) & 1), c.base[1] + ((cc >> 1) & 1), c.base[2] + (cc & 1)));
+}
+
+// ---------------------------------------------------------------------------
+// generic path: corners per point, then one thread per output element
+// ---------------------------------------------------------------------------
+__global__ void k_devox_corners(DevoxArgs a, int32_t* cidx, float* cw) {
+    int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (k >= a.n) return;
+    const float sfac = __builtin_ldexpf(1.0f, -a.stride_log2);
+    Corners c = point_corners(a.xyz, a.batch, k, a.voxel_size, sfac, a.mode);
+    if (!c.ok) raise_flag(a.h, isfinite(a.xyz[3 * k]) && isfinite(a.xyz[3 * k + 1]) && isfinite(a.xyz[3 * k + 2])
+                                   ? kFlagRange
+                                   : kFlagNonfinite);
+#pragma unroll
+    for (int cc = 0; cc < 8; ++cc) {
+        cidx[8 * k + cc] = corner_lookup(a.table, c, cc);
+        cw[8 * k + cc] = c.ok ? corner_weight(c, cc) : 0.f;
+    }
+}
+
+template <int DT>
+__global__ void k_devox_generic(DevoxArgs a, const int32_t* cidx, const float* cw) {
+    int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    int64_t k = t / a.C;
+    int col = (int)(t - k * a.C);
+    if (k >= a.n) return;
+    float den = 0.f, num = 0.f;
+#pragma unroll
+    for (int cc = 0; cc < 8; ++cc) {
+        int32_t i = cidx[8 * k + cc];
+        if (i < 0) continue;
+        float w = cw[8 * k + cc];
+        den += w;
+        num += w * ld_feat<DT>(a.vfeat, (int64_t)i * a.C + col);
+    }
+    float y = den > 0.f ? num / den : 0.f;
+    if (a.pfeat) {
+        float s = 0.f;
+        for (int ci = 0; ci < a.Cp; ++ci)
+            s += ld_feat<DT>(a.pfeat, k * a.Cp + ci) * ld_feat<DT>(a.Wp, (int64_t)ci * a.C + col);
+        if (a.scale_p) s *= a.scale_p[col];
+        if (a.shift_p) s += a.shift_p[col];
+        if (a.relu_p) s = fmaxf(s, 0.f);
+        y += s;
+    }
+    st_feat<DT>(a.out, k * a.C + col, y);
+}
+
+// ---------------------------------------------------------------------------
+// MFMA path
+// ---------------------------------------------------------------------------
+template <int DT, int KCH, int NB>
+__global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __restrict__ wpack) {
+    __shared__ int32_t sidx[4][16][8];
+    __shared__ float sw[4][16][8];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r16 = lane & 15, g = lane >> 4;
+    const int64_t p0 = ((int64_t)blockIdx.x * 4 + wave) * 16;
+    const int64_t k = p0 + r16;
+    const bool kv = k < a.n;
+    const float sfac = __builtin_ldexpf(1.0f, -a.stride_log2);
+
+    // corners 2g and 2g+1 of point r16
+    Corners c;
+    if (kv) c = point_corners(a.xyz, a.batch, k, a.voxel_size, sfac, a.mode);
+    else c.ok = false;
+    if (kv && !c.ok && g == 0)
+        raise_flag(a.h, isfinite(a.xyz[3 * k]) && isfinite(a.xyz[3 * k + 1]) && isfinite(a.xyz[3 * k + 2])
+                            ? kFlagRange
+                            : kFlagNonfinite);
+    int32_t i0 = corner_lookup(a.table, c, 2 * g), i1 = corner_lookup(a.table, c, 2 * g + 1);
+    float w0 = c.ok ? corner_weight(c, 2 * g) : 0.f, w1 = c.ok ? corner_weight(c, 2 * g + 1) : 0.f;
+    if (kv && a.corner_idx) {
+        a.corner_idx[8 * k + 2 * g] = i0;
+        a.corner_idx[8 * k + 2 * g + 1] = i1;
+        a.corner_w[8 * k + 2 * g] = w0;
+        a.corner_w[8 * k + 2 * g + 1] = w1;
+    }
+    float wp = (i0 >= 0 ? w0 : 0.f) + (i1 >= 0 ? w1 : 0.f);
+    wp += __shfl_xor(wp, 16, 64);
+    wp += __shfl_xor(wp, 32, 64);
+    const float inv = wp > 0.f ? 1.0f / wp : 0.f;
+    sidx[wave][r16][2 * g] = i0;
+    sidx[wave][r16][2 * g + 1] = i1;
+    sw[wave][r16][2 * g] = (i0 >= 0) ? w0 * inv : 0.f;
+    sw[wave][r16][2 * g + 1] = (i1 >= 0) ? w1 * inv : 0.f;
+
+    // point MLP on matrix cores
+    f32x4 acc[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (a.pfeat) {
+        const uint16_t* prow = (const uint16_t*)a.pfeat + (kv ? k : 0) * a.Cp + 8 * g;
+#pragma unroll
+        for (int kc = 0; kc < KCH; ++kc) {
+            uint4 av = make_uint4(0, 0, 0, 0);
+            if (kv && kc * 32 + 8 * g < a.Cp) av = *(const uint4*)(prow + kc * 32);
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                acc[nb] = mfma16x16x32<DT>(av, wpack[((int64_t)kc * NB + nb) * 64 + lane], acc[nb]);
+        }
+    }
+    __syncthreads();
+
+    // epilogue: rows 4g..4g+3 of this wave's 16 points, column nb*16 + r16
+    const uint16_t* V = (const uint16_t*)a.vfeat;
+    uint16_t* out = (uint16_t*)a.out;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+        const int col = nb * 16 + r16;
+        const float sc = a.scale_p ? a.scale_p[col] : 1.f;
+        const float sh = a.shift_p ? a.shift_p[col] : 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int row = 4 * g + e;
+            const int64_t kk = p0 + row;
+            if (kk >= a.n) continue;
+            float y = 0.f;
+            if (a.pfeat) {
+                y = acc[nb][e] * sc + sh;
+                if (a.relu_p) y = fmaxf(y, 0.f);
+            }
+            float dv = 0.f;
+#pragma unroll
+            for (int cc = 0; cc < 8; ++cc) {
+                const int32_t i = sidx[wave][row][cc];
+                if (i >= 0) dv += sw[wave][row][cc] * from16<DT>(V[(int64_t)i * a.C + col]);
+            }
+            out[kk * a.C + col] = to16<DT>(y + dv);
+        }
+    }
+}
+
+bool devox_mfma_supported(int C, int Cp, int dt) {
+    if (dt == SPV_F32 || C % 16 != 0) return false;
+    int NB = C / 16;
+    if (!(NB == 1 || NB == 2 || NB == 4 || NB == 6 || NB == 8 || NB == 16)) return false;
+    return Cp == 0 || (Cp % 8 == 0 && Cp <= 256);
+}
+
+void* plan_devox_ws(Arena& a, int C, int Cp) {
+    int KCH = (Cp + 31) / 32, NB = C / 16;
+    if (KCH < 1) KCH = 1;
+    if (NB < 1) NB = 1;
+    return a.take<uint4>((size_t)KCH * NB * 64);
+}
+
+template <int DT, int KCH, int NB>
+static void launch_devox_mfma(hipStream_t s, const DevoxArgs& a, const void* wpack) {
+    int64_t waves = (a.n + 15) / 16;
+    k_devox_mfma<DT, KCH, NB><<<blocks_for(waves, 4), 256, 0, s>>>(a, (const uint4*)wpack);
+}
+
+template <int DT, int NB>
+static void launch_devox_kch(hipStream_t s, const DevoxArgs& a, const void* wpack) {
+    switch ((a.Cp + 31) / 32) {
+        case 0:
+        case 1: launch_devox_mfma<DT, 1, NB>(s, a, wpack); break;
+        case 2: launch_devox_mfma<DT, 2, NB>(s, a, wpack); break;
+        case 3: launch_devox_mfma<DT, 3, NB>(s, a, wpack); break;
+        case 4: launch_devox_mfma<DT, 4, NB>(s, a, wpack); break;
+        case 5: launch_devox_mfma<DT, 5, NB>(s, a, wpack); break;
+        case 6: launch_devox_mfma<DT, 6, NB>(s, a, wpack); break;
+        case 7: launch_devox_mfma<DT, 7, NB>(s, a, wpack); break;
+        case 8: launch_devox_mfma<DT, 8, NB>(s, a, wpack); break;
+    }
+}
+
+template <int DT>
+static void launch_devox_dt(hipStream_t s, const DevoxArgs& a, const void* wpack) {
+    switch (a.C / 16) {
+        case 1: launch_devox_kch<DT, 1>(s, a, wpack); break;
+        case 2: launch_devox_kch<DT, 2>(s, a, wpack); break;
+        case 4: launch_devox_kch<DT, 4>(s, a, wpack); break;
+        case 6: launch_devox_kch<DT, 6>(s, a, wpack); break;
+        case 8: launch_devox_kch<DT, 8>(s, a, wpack); break;
+        case 16: launch_devox_kch<DT, 16>(s, a, wpack); break;
+    }
+}
+
+__global__ void k_pack_wp(const uint16_t* W, int Cin, int Cout, int KCH, int NB, uint4* wpack);
+
+void launch_devox(hipStream_t s, const DevoxArgs& a, void* wpack, int32_t* cidx_tmp, float* cw_tmp) {
+    if (a.n <= 0) return;
+    if (devox_mfma_supported(a.C, a.pfeat ? a.Cp : 0, a.dt)) {
+        if (a.pfeat) {
+            int KCH = (a.Cp + 31) / 32, NB = a.C / 16;
+            int64_t tot = (int64_t)KCH * NB * 64;
+            k_pack_wp<<<blocks_for(tot, 256), 256, 0, s>>>((const uint16_t*)a.Wp, a.Cp, a.C, KCH, NB, (uint4*)wpack);
+        }
+        if (a.dt == SPV_BF16) launch_devox_dt<SPV_BF16>(s, a, wpack);
+        else launch_devox_dt<SPV_F16>(s, a, wpack);
+        return;
+    }
+    int32_t* ci = a.corner_idx ? a.corner_idx : cidx_tmp;
+    float* cw = a.corner_w ? a.corner_w : cw_tmp;
+    k_devox_corners<<<blocks_for(a.n, 256), 256, 0, s>>>(a, ci, cw);
+    unsigned g = blocks_for(a.n * a.C, 256);
+    if (a.dt == SPV_F32) k_devox_generic<SPV_F32><<<g, 256, 0, s>>>(a, ci, cw);
+    else if (a.dt == SPV_BF16) k_devox_generic<SPV_BF16><<<g, 256, 0, s>>>(a, ci, cw);
+    else k_devox_generic<SPV_F16><<<g, 256, 0, s>>>(a, ci, cw);
+}
+
+// the point-MLP weight [Cin][Cout] packed like a single-offset conv weight
+__global__ void k_pack_wp(const uint16_t* W, int Cin, int Cout, int KCH, int NB, uint4* wpack) {
+    int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    int64_t total = (int64_t)KCH * NB * 64;
+    if (t >= total) return;
+    int lane = (int)(t & 63);
+    int64_t f = t >> 6;
+    int nb = (int)(f % NB);
+    int kc = (int)(f / NB);
+    int col = nb * 16 + (lane & 15);
+    int ci0 = kc * 32 + 8 * (lane >> 4);
+    uint32_t w[4];
+    for (int e = 0; e < 4; ++e) {
+        uint32_t lo = 0, hi = 0;
+        int c0 = ci0 + 2 * e, c1 = ci0 + 2 * e + 1;
+        if (c0 < Cin) lo = W[(int64_t)c0 * Cout + col];
+        if (c1 < Cin) hi = W[(int64_t)c1 * Cout + col];
+        w[e] = lo | (hi << 16);
+    }
+    wpack[t] = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+}  // namespace spv

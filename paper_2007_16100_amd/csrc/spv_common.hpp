@@ -1,0 +1,205 @@
+// spv_common.hpp -- device helpers shared by the HIP kernels of libspv.so:
+// packed voxel keys, the open-addressing hash, 16-bit storage conversions,
+// MFMA operand types, the device status word and the workspace arena.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/spv.h"
+
+namespace spv {
+
+// ---------------------------------------------------------------------------
+// packed voxel keys: b:16 | (x + 2^15):16 | (y + 2^15):16 | (z + 2^15):16.
+// The packing is monotone, so key order is (b, x, y, z) lexicographic order.
+// Batch 65535 is reserved, which makes all-ones the empty-slot sentinel.
+// ---------------------------------------------------------------------------
+constexpr uint64_t kEmpty = ~0ull;
+constexpr int kCoordMin = -32767;
+constexpr int kCoordMax = 32766;
+constexpr int kBatchMax = 65534;
+
+__host__ __device__ inline uint64_t pack_key(int b, int x, int y, int z) {
+    return ((uint64_t)(uint32_t)b << 48) | ((uint64_t)(uint32_t)(x + 32768) << 32) |
+           ((uint64_t)(uint32_t)(y + 32768) << 16) | (uint64_t)(uint32_t)(z + 32768);
+}
+__host__ __device__ inline int key_b(uint64_t k) { return (int)(k >> 48); }
+__host__ __device__ inline int key_x(uint64_t k) { return (int)((k >> 32) & 0xFFFF) - 32768; }
+__host__ __device__ inline int key_y(uint64_t k) { return (int)((k >> 16) & 0xFFFF) - 32768; }
+__host__ __device__ inline int key_z(uint64_t k) { return (int)(k & 0xFFFF) - 32768; }
+
+// ---------------------------------------------------------------------------
+// device status word (bit flags); the host reports the most severe one
+// ---------------------------------------------------------------------------
+enum : uint32_t {
+    kFlagNonfinite = 1u << 0,
+    kFlagRange = 1u << 1,
+    kFlagCapacity = 1u << 2,
+    kFlagDuplicate = 1u << 3,  // repeated coordinate where distinct ones are required
+    kFlagTableFull = 1u << 4,
+};
+
+// Workspace header: first 256 bytes of every workspace.
+struct alignas(256) Header {
+    uint32_t status;
+    uint32_t pad;
+    int64_t m;              // unique voxels inserted by the voxelization
+    int64_t aux[4];
+};
+
+__device__ inline void raise_flag(Header* h, uint32_t f) { atomicOr(&h->status, f); }
+
+// ---------------------------------------------------------------------------
+// open-addressing hash with linear probing over 64-bit keys
+// ---------------------------------------------------------------------------
+__host__ __device__ inline uint32_t hash_slot(uint64_t k, uint32_t mask) {
+    // murmur3 64-bit finalizer
+    k ^= k >> 33;
+    k *= 0xff51afd7ed558ccdull;
+    k ^= k >> 33;
+    k *= 0xc4ceb9fe1a85ec53ull;
+    k ^= k >> 33;
+    return (uint32_t)k & mask;
+}
+
+struct Table {
+    uint64_t* keys;
+    int32_t* vals;
+    uint32_t mask;  // capacity - 1 (capacity is a power of two)
+};
+
+// Insert; returns 1 if this call created the entry, 0 if the key was present,
+// -1 if the table is full.  *slot receives the entry's slot.
+__device__ inline int table_insert(Table t, uint64_t key, uint32_t* slot) {
+    uint32_t s = hash_slot(key, t.mask);
+    for (uint32_t i = 0; i <= t.mask; ++i) {
+        uint64_t cur = __hip_atomic_load(&t.keys[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (cur == key) {
+            *slot = s;
+            return 0;
+        }
+        if (cur == kEmpty) {
+            uint64_t prev = atomicCAS((unsigned long long*)&t.keys[s], (unsigned long long)kEmpty,
+                                      (unsigned long long)key);
+            if (prev == kEmpty) {
+                *slot = s;
+                return 1;
+            }
+            if (prev == key) {
+                *slot = s;
+                return 0;
+            }
+        }
+        s = (s + 1) & t.mask;
+    }
+    return -1;
+}
+
+// Lookup after the table is complete (a later kernel); -1 if absent.
+__device__ inline int32_t table_find(Table t, uint64_t key) {
+    uint32_t s = hash_slot(key, t.mask);
+    for (uint32_t i = 0; i <= t.mask; ++i) {
+        uint64_t cur = t.keys[s];
+        if (cur == key) return t.vals[s];
+        if (cur == kEmpty) return -1;
+        s = (s + 1) & t.mask;
+    }
+    return -1;
+}
+
+// slot of a present key (used to set values); -1 if absent
+__device__ inline int64_t table_slot(Table t, uint64_t key) {
+    uint32_t s = hash_slot(key, t.mask);
+    for (uint32_t i = 0; i <= t.mask; ++i) {
+        uint64_t cur = t.keys[s];
+        if (cur == key) return s;
+        if (cur == kEmpty) return -1;
+        s = (s + 1) & t.mask;
+    }
+    return -1;
+}
+
+inline uint32_t table_capacity(int64_t max_keys) {
+    uint64_t c = 1024;
+    while (c < (uint64_t)(2 * max_keys)) c <<= 1;
+    return (uint32_t)c;
+}
+
+// ---------------------------------------------------------------------------
+// 16-bit storage
+// ---------------------------------------------------------------------------
+__device__ inline float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+__device__ inline uint16_t f32_to_bf16(float f) {  // round to nearest even
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);  // quiet NaN
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+__device__ inline float f16_to_f32(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
+__device__ inline uint16_t f32_to_f16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
+
+template <int DT>
+__device__ inline float ld_feat(const void* p, int64_t i) {
+    if constexpr (DT == SPV_F32) return ((const float*)p)[i];
+    else if constexpr (DT == SPV_BF16) return bf16_to_f32(((const uint16_t*)p)[i]);
+    else return f16_to_f32(((const uint16_t*)p)[i]);
+}
+template <int DT>
+__device__ inline void st_feat(void* p, int64_t i, float v) {
+    if constexpr (DT == SPV_F32) ((float*)p)[i] = v;
+    else if constexpr (DT == SPV_BF16) ((uint16_t*)p)[i] = f32_to_bf16(v);
+    else ((uint16_t*)p)[i] = f32_to_f16(v);
+}
+template <int DT>
+__device__ inline uint16_t to16(float v) {
+    if constexpr (DT == SPV_BF16) return f32_to_bf16(v);
+    else return f32_to_f16(v);
+}
+template <int DT>
+__device__ inline float from16(uint32_t h) {
+    if constexpr (DT == SPV_BF16) return bf16_to_f32((uint16_t)h);
+    else return f16_to_f32((uint16_t)h);
+}
+
+// ---------------------------------------------------------------------------
+// MFMA operand types (gfx950: v_mfma_f32_16x16x32_{bf16,f16})
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int DT>
+__device__ inline f32x4 mfma16x16x32(uint4 a, uint4 b, f32x4 c) {
+    if constexpr (DT == SPV_BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                       0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                      0, 0);
+}
+
+// ---------------------------------------------------------------------------
+// host-side workspace arena: sequential 256-byte aligned carving
+// ---------------------------------------------------------------------------
+struct Arena {
+    char* base;
+    size_t cap;
+    size_t used = 0;
+    Arena(void* b, size_t c) : base((char*)b), cap(c) {}
+    template <class T>
+    T* take(size_t count) {
+        size_t off = (used + 255) & ~(size_t)255;
+        used = off + count * sizeof(T);
+        return (base && used <= cap) ? (T*)(base + off) : nullptr;
+    }
+    bool ok() const { return used <= cap; }
+};
+
+inline unsigned blocks_for(int64_t n, int per_block) {
+    int64_t b = (n + per_block - 1) / per_block;
+    return (unsigned)(b < 1 ? 1 : b);
+}
+
+}  // namespace spv

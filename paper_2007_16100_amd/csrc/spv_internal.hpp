@@ -1,0 +1,177 @@
+// spv_internal.hpp -- host-side launchers shared between the translation units of
+// libspv.so.  Every launcher only enqueues kernels on `s`; none synchronizes.
+#pragma once
+
+#include "spv_common.hpp"
+
+namespace spv {
+
+// --- block-level helpers (device) -------------------------------------------
+// exclusive prefix sum of v over the block (blockDim.x threads, multiple of 64);
+// lds must hold blockDim.x/64 + 1 ints.  *total receives the block sum.
+__device__ inline int block_exclusive_scan(int v, int* lds, int* total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        int y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
+    }
+    if (lane == 63) lds[wave] = x;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int run = 0;
+        for (int w = 0; w < nw; ++w) {
+            int t = lds[w];
+            lds[w] = run;
+            run += t;
+        }
+        lds[nw] = run;
+    }
+    __syncthreads();
+    int r = lds[wave] + x - v;
+    *total = lds[nw];
+    __syncthreads();
+    return r;
+}
+
+// --- hash tables (hash_sort_scan.hip) ----------------------------------------
+// Clear the header (status, counters, key statistics) and a table's key slots.
+void launch_clear(hipStream_t s, Header* h, Table t, bool clear_header);
+void launch_clear_header(hipStream_t s, Header* h);
+// Insert coords[0..count) (count = *count_dev or cap) with value = row index;
+// raises kFlagDuplicate on a repeated coordinate, kFlagRange on a coordinate
+// outside the key range.
+void launch_table_build(hipStream_t s, Header* h, Table t, const int32_t* coords, const int64_t* count_dev,
+                        int64_t cap);
+void launch_table_lookup(hipStream_t s, Table t, const int32_t* q, int64_t nq, int32_t* idx);
+
+// --- radix sort of packed voxel keys (hash_sort_scan.hip) ---------------------
+// Sorts keys[0..*count) ascending.  The keys are first compacted (per-field
+// minimum subtracted, fields packed into the fewest bits), then sorted with
+// 8-bit LSD passes; passes beyond the significant bits do nothing.  The result
+// is read back with sorted_key() from whichever buffer holds it.
+struct SortStats {
+    int32_t fmin[4];    // per-field minimum of the keys being sorted (b, x, y, z)
+    int32_t fmax[4];
+    uint32_t fbits[4];  // bit width of each compacted field
+    uint32_t sort_bits; // significant bits of the compacted key
+};
+struct SortBufs {
+    uint64_t* a;       // [cap] input keys / ping
+    uint64_t* b;       // [cap] pong
+    uint32_t* hist;    // [256 * nblocks(cap)]
+    SortStats* st;
+};
+void plan_sort_ws(Arena& a, SortBufs& sb, int64_t cap);
+size_t sort_hist_entries(int64_t cap);
+void launch_sort_keys(hipStream_t s, SortBufs bufs, const int64_t* count_dev, int64_t cap);
+// the sorted key of rank r (decompacted), valid after launch_sort_keys
+__device__ inline uint64_t sorted_key(const SortBufs& sb, int64_t r) {
+    const SortStats* st = sb.st;
+    int passes = (int)((st->sort_bits + 7) / 8);
+    uint64_t ck = (passes & 1) ? sb.b[r] : sb.a[r];
+    uint32_t bz = st->fbits[3], by = st->fbits[2], bx = st->fbits[1];
+    int z = (int)(ck & ((1ull << bz) - 1)) + st->fmin[3];
+    ck >>= bz;
+    int y = (int)(ck & ((1ull << by) - 1)) + st->fmin[2];
+    ck >>= by;
+    int x = (int)(ck & ((1ull << bx) - 1)) + st->fmin[1];
+    ck >>= bx;
+    int b = (int)ck + st->fmin[0];
+    return pack_key(b, x, y, z);
+}
+
+// --- prefix sums with a device-side count (hash_sort_scan.hip) ----------------
+// out[i] = sum_{j<i} in[j] for i in [0, count]; out must hold cap + 1 ints;
+// tmp must hold scan_tmp_entries(cap) ints.
+size_t scan_tmp_entries(int64_t cap);
+void launch_exclusive_scan(hipStream_t s, const int32_t* in, int32_t* out, const int64_t* count_dev, int64_t cap,
+                           int32_t* tmp);
+// single-block exclusive scan of a host-sized array (n small), out[n] = total
+void launch_exclusive_scan_small(hipStream_t s, const uint32_t* in, uint32_t* out, int64_t n);
+
+// --- voxelize (voxelize.hip) ---------------------------------------------------
+struct VoxelizeWs {
+    Header* h;          // assigned by the caller (workspace offset 0)
+    Table table;
+    SortBufs sort;
+    uint64_t* pkey;     // [n] packed key per point (kEmpty if invalid)
+    int32_t* seg;       // [n + 1] CSR offsets of the points of each voxel
+    int32_t* fill;      // [n]
+    int32_t* plist;     // [n] point ids grouped by voxel
+    int32_t* scan_tmp;  // [scan_tmp_entries(n)]
+};
+void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n);
+// coords/counts/pt2vox and (if feat) vfeat; m into h->m and *m_dev
+void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const int32_t* batch, int64_t n,
+                     float voxel_size, const void* feat, int32_t C, int dt, int32_t* coords, void* vfeat,
+                     int32_t* counts, int32_t* pt2vox, int64_t* m_dev);
+
+// --- kernel map (kmap.hip) -----------------------------------------------------
+struct KmapWs {
+    Header* h;          // assigned by the caller
+    Table fine;         // table of the input coords (assigned by the caller when shared)
+    Table coarse;       // stride 2: table of the output coords
+    SortBufs sort;      // stride 2: coarse key sort
+    uint32_t* mask;     // [m_cap] offsets present per output
+    uint32_t* bcnt;     // [K3 * nblk] per-block per-offset counts (k-major)
+    uint32_t* bbase;    // [K3 * nblk + 1]
+    int64_t* m_out;     // device count of outputs
+};
+void plan_kmap_ws(Arena& a, KmapWs& w, int64_t m_cap, int K, int stride, bool own_fine_table);
+// build_fine: clear + insert the input coords into w.fine first (otherwise the
+// table must already map every input coordinate to its row)
+void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const int32_t* in_coords,
+                       const int64_t* m_in_dev, int64_t m_cap, int K, int stride, int32_t* out_coords,
+                       int64_t* m_out_dev, int32_t* off, int32_t* pairs, int64_t pair_cap);
+
+// --- sparse conv (conv.hip) ----------------------------------------------------
+struct ConvPlan {
+    int64_t m_cap;      // output row capacity
+    int K3;
+    uint32_t* mask;     // [m_cap] offsets present per output row
+    uint32_t* umask;    // [nblk16] union of the offsets of each 16-row block
+    uint32_t* ucnt;     // [nblk16 + 1] -> exclusive prefix of popcount(umask)
+    int32_t* table;     // [K3 * nblk16 * 16] input row per (block, present offset, row)
+    const int64_t* m_out_dev;
+};
+void plan_conv_ws(Arena& a, ConvPlan& p, int64_t m_out_cap, int K3);
+void launch_conv_plan(hipStream_t s, const ConvPlan& p, const int32_t* off, const int32_t* pairs, int K3,
+                      int transposed, int64_t pair_bound);
+bool conv_mfma_supported(int Cin, int Cout, int dt);
+void* plan_wpack_ws(Arena& a, int K3, int Cin, int Cout);
+// pack W [K3][Cin][Cout] into MFMA B fragments (no-op when the vector-ALU path runs)
+void launch_conv_pack(hipStream_t s, int K3, const void* W, void* wpack, int Cin, int Cout, int dt);
+// the convolution itself (one kernel); wpack must have been packed from W
+void launch_conv_run(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows, const void* W,
+                     const void* wpack, const float* scale, const float* shift, int relu, void* out, int Cout, int dt);
+
+// --- devoxelize (devox.hip) ----------------------------------------------------
+struct DevoxArgs {
+    Table table;
+    int stride_log2;
+    const float* xyz;
+    const int32_t* batch;
+    int64_t n;
+    float voxel_size;
+    int mode;
+    const void* vfeat;
+    int C;
+    const void* pfeat;
+    int Cp;
+    const void* Wp;
+    const float* scale_p;
+    const float* shift_p;
+    int relu_p;
+    void* out;
+    int dt;
+    int32_t* corner_idx;
+    float* corner_w;
+    Header* h;
+};
+bool devox_mfma_supported(int C, int Cp, int dt);
+void* plan_devox_ws(Arena& a, int C, int Cp);
+void launch_devox(hipStream_t s, const DevoxArgs& a, void* wpack, int32_t* cidx_tmp, float* cw_tmp);
+
+}  // namespace spv

@@ -1,0 +1,185 @@
+// voxelize.hip -- sparse voxelization (Sec. 3.3, Eq. 1 and Eq. 2).
+//
+// 1. every point's key floor(p / v) is inserted into the open-addressing hash;
+//    the thread that creates an entry appends the key to the unique-key list;
+// 2. the m unique keys are radix-sorted into canonical (b, x, y, z) order and the
+//    table values are set to the rank, which also writes the voxel coordinates;
+// 3. every point queries the table for its voxel index (pt2vox) and counts N_m;
+// 4. a counting sort of the points by voxel (prefix sum + fill) lets each voxel
+//    gather and average its own points -- no float atomics, one write per voxel.
+#include "spv_internal.hpp"
+
+namespace spv {
+
+void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n) {
+    int64_t nn = n > 0 ? n : 1;
+    uint32_t S = table_capacity(nn);
+    w.table.keys = a.take<uint64_t>(S);
+    w.table.vals = a.take<int32_t>(S);
+    w.table.mask = S - 1;
+    plan_sort_ws(a, w.sort, nn);
+    w.pkey = a.take<uint64_t>(nn);
+    w.seg = a.take<int32_t>(nn + 1);
+    w.fill = a.take<int32_t>(nn);
+    w.plist = a.take<int32_t>(nn);
+    w.scan_tmp = a.take<int32_t>(scan_tmp_entries(nn));
+}
+
+// Eq. 1 per point, then hash insert.  Invalid points get kEmpty and a status flag.
+__global__ void k_vox_insert(Header* h, Table t, uint64_t* ukeys, uint64_t* pkey, const float* xyz,
+                             const int32_t* batch, int64_t n, float v) {
+    int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (k >= n) return;
+    float p[3] = {xyz[3 * k], xyz[3 * k + 1], xyz[3 * k + 2]};
+    int b = batch ? batch[k] : 0;
+    bool finite = isfinite(p[0]) && isfinite(p[1]) && isfinite(p[2]);
+    bool inrange = b >= 0 && b <= kBatchMax;
+    int q[3] = {0, 0, 0};
+#pragma unroll
+    for (int d = 0; d < 3; ++d) {
+        float a = p[d] / v;  // IEEE single-precision, correctly rounded
+        float f = floorf(a);
+        inrange = inrange && isfinite(a) && f >= (float)kCoordMin && f <= (float)kCoordMax;
+        q[d] = inrange ? (int)f : 0;
+    }
+    if (!finite) {
+        raise_flag(h, kFlagNonfinite);
+        pkey[k] = kEmpty;
+        return;
+    }
+    if (!inrange) {
+        raise_flag(h, kFlagRange);
+        pkey[k] = kEmpty;
+        return;
+    }
+    uint64_t key = pack_key(b, q[0], q[1], q[2]);
+    pkey[k] = key;
+    uint32_t slot;
+    int r = table_insert(t, key, &slot);
+    if (r > 0) {
+        unsigned long long idx = atomicAdd((unsigned long long*)&h->m, 1ull);
+        ukeys[idx] = key;
+    } else if (r < 0) {
+        raise_flag(h, kFlagTableFull);
+    }
+}
+
+// rank -> table value, voxel coordinates, zeroed counters
+__global__ void k_vox_rank(const Header* h, SortBufs sb, Table t, int32_t* coords, int32_t* counts, int32_t* fill,
+                           int64_t cap, int64_t* m_dev) {
+    int64_t m = h->m;
+    if (m > cap) m = cap;
+    int64_t r = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (r == 0 && m_dev) *m_dev = m;
+    if (r >= m) return;
+    uint64_t key = sorted_key(sb, r);
+    int64_t slot = table_slot(t, key);
+    if (slot >= 0) t.vals[slot] = (int32_t)r;
+    coords[4 * r + 0] = key_b(key);
+    coords[4 * r + 1] = key_x(key);
+    coords[4 * r + 2] = key_y(key);
+    coords[4 * r + 3] = key_z(key);
+    counts[r] = 0;
+    fill[r] = 0;
+}
+
+__global__ void k_vox_lookup(Table t, const uint64_t* pkey, int64_t n, int32_t* pt2vox, int32_t* counts) {
+    int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (k >= n) return;
+    uint64_t key = pkey[k];
+    int32_t v = (key == kEmpty) ? -1 : table_find(t, key);
+    pt2vox[k] = v;
+    if (v >= 0) atomicAdd(&counts[v], 1);
+}
+
+__global__ void k_vox_fill(const int32_t* pt2vox, int64_t n, const int32_t* seg, int32_t* fill, int32_t* plist) {
+    int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (k >= n) return;
+    int32_t v = pt2vox[k];
+    if (v < 0) return;
+    int32_t pos = seg[v] + atomicAdd(&fill[v], 1);
+    plist[pos] = (int32_t)k;
+}
+
+// Eq. 2: one thread per (voxel, VEC consecutive channels); sums its points in fp32
+template <int DT, int VEC>
+__global__ void k_vox_mean(const Header* h, int64_t cap, const int32_t* seg, const int32_t* plist, const void* feat,
+                           int C, void* vfeat) {
+    int64_t m = h->m;
+    if (m > cap) m = cap;
+    const int nch = C / VEC;
+    int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    int64_t vox = t / nch;
+    int ch = (int)(t - vox * nch) * VEC;
+    if (vox >= m) return;
+    int32_t lo = seg[vox], hi = seg[vox + 1];
+    float acc[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
+    for (int32_t p = lo; p < hi; ++p) {
+        int64_t row = (int64_t)plist[p] * C + ch;
+        if constexpr (VEC == 8) {
+            uint4 u = *(const uint4*)((const uint16_t*)feat + row);
+            uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                acc[2 * j] += from16<DT>(w[j] & 0xFFFF);
+                acc[2 * j + 1] += from16<DT>(w[j] >> 16);
+            }
+        } else if constexpr (VEC == 4) {
+            float4 f = *(const float4*)((const float*)feat + row);
+            acc[0] += f.x;
+            acc[1] += f.y;
+            acc[2] += f.z;
+            acc[3] += f.w;
+        } else {
+            acc[0] += ld_feat<DT>(feat, row);
+        }
+    }
+    const float N = (float)(hi - lo);
+    int64_t orow = vox * C + ch;
+    if constexpr (VEC == 8) {
+        uint32_t w[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            w[j] = (uint32_t)to16<DT>(acc[2 * j] / N) | ((uint32_t)to16<DT>(acc[2 * j + 1] / N) << 16);
+        *(uint4*)((uint16_t*)vfeat + orow) = make_uint4(w[0], w[1], w[2], w[3]);
+    } else if constexpr (VEC == 4) {
+        *(float4*)((float*)vfeat + orow) = make_float4(acc[0] / N, acc[1] / N, acc[2] / N, acc[3] / N);
+    } else {
+        st_feat<DT>(vfeat, orow, acc[0] / N);
+    }
+}
+
+template <int DT, int VEC>
+static void launch_mean(hipStream_t s, const VoxelizeWs& w, int64_t n, const void* feat, int C, void* vfeat) {
+    int64_t threads = n * (C / VEC);
+    k_vox_mean<DT, VEC><<<blocks_for(threads, 256), 256, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat);
+}
+
+void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const int32_t* batch, int64_t n,
+                     float voxel_size, const void* feat, int32_t C, int dt, int32_t* coords, void* vfeat,
+                     int32_t* counts, int32_t* pt2vox, int64_t* m_dev) {
+    launch_clear(s, w.h, w.table, true);
+    if (n > 0) k_vox_insert<<<blocks_for(n, 256), 256, 0, s>>>(w.h, w.table, w.sort.a, w.pkey, xyz, batch, n, voxel_size);
+    launch_sort_keys(s, w.sort, &w.h->m, n);
+    k_vox_rank<<<blocks_for(n, 256), 256, 0, s>>>(w.h, w.sort, w.table, coords, counts, w.fill, n, m_dev);
+    if (n == 0) return;
+    k_vox_lookup<<<blocks_for(n, 256), 256, 0, s>>>(w.table, w.pkey, n, pt2vox, counts);
+    if (!feat) return;
+    launch_exclusive_scan(s, counts, w.seg, &w.h->m, n, w.scan_tmp);
+    k_vox_fill<<<blocks_for(n, 256), 256, 0, s>>>(pt2vox, n, w.seg, w.fill, w.plist);
+    const bool v16 = (dt != SPV_F32) && (C % 8 == 0), v32 = (dt == SPV_F32) && (C % 4 == 0);
+    if (dt == SPV_F32) {
+        if (v32) launch_mean<SPV_F32, 4>(s, w, n, feat, C, vfeat);
+        else launch_mean<SPV_F32, 1>(s, w, n, feat, C, vfeat);
+    } else if (dt == SPV_BF16) {
+        if (v16) launch_mean<SPV_BF16, 8>(s, w, n, feat, C, vfeat);
+        else launch_mean<SPV_BF16, 1>(s, w, n, feat, C, vfeat);
+    } else {
+        if (v16) launch_mean<SPV_F16, 8>(s, w, n, feat, C, vfeat);
+        else launch_mean<SPV_F16, 1>(s, w, n, feat, C, vfeat);
+    }
+}
+
+}  // namespace spv

@@ -1,0 +1,271 @@
+"""Python binding of libspv.so (ctypes): argument marshalling only.
+
+Every function below forwards to the C entry point of the same name in
+``include/spv.h``; all computation happens in the library's HIP kernels.
+torch supplies device memory (tensor ``data_ptr``) and the stream
+(``torch.cuda.current_stream().cuda_stream``).  Output tensors are allocated
+here with torch when the caller does not pass them.
+
+There is no fallback: if ``libspv.so`` is missing, or the tensors are not on a
+GPU, the call raises.
+"""
+from __future__ import annotations
+
+import ctypes as ct
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libspv.so")
+
+SPV_OK, SPV_ERR_INVALID_ARG, SPV_ERR_CAPACITY, SPV_ERR_RANGE, SPV_ERR_NONFINITE, SPV_ERR_UNSUPPORTED, SPV_ERR_HIP = \
+    range(7)
+SPV_F32, SPV_BF16, SPV_F16 = 0, 1, 2
+SPV_DEVOX_CENTER, SPV_DEVOX_CORNER = 0, 1
+
+_DT = {torch.float32: SPV_F32, torch.bfloat16: SPV_BF16, torch.float16: SPV_F16}
+
+# every symbol include/spv.h declares
+EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_devoxelize",
+           "spv_block_workspace_bytes", "spv_block", "spv_lookup", "spv_status_check", "spv_status_string",
+           "spv_last_hip_error")
+
+
+class SpvError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        msg = lib().spv_status_string(status).decode() if _lib is not None else str(status)
+        super().__init__(f"{what}: {msg} (status {status})")
+
+
+class BlockParams(ct.Structure):
+    _fields_ = [("C", ct.c_int32), ("dtype", ct.c_int32), ("voxel_size", ct.c_float), ("n_convs", ct.c_int32),
+                ("W", ct.c_void_p * 2), ("scale", ct.c_void_p * 2), ("shift", ct.c_void_p * 2),
+                ("relu", ct.c_int32 * 2), ("Wp", ct.c_void_p), ("scale_p", ct.c_void_p), ("shift_p", ct.c_void_p),
+                ("relu_p", ct.c_int32), ("devox_mode", ct.c_int32), ("events", ct.POINTER(ct.c_void_p)),
+                ("n_events", ct.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libspv.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2007_16100_amd.build`")
+        L = ct.CDLL(LIB_PATH)
+        vp, i64, i32, f32, sz = ct.c_void_p, ct.c_int64, ct.c_int32, ct.c_float, ct.c_size_t
+        L.spv_workspace_bytes.argtypes = [i64, i32]
+        L.spv_workspace_bytes.restype = sz
+        L.spv_block_workspace_bytes.argtypes = [i64, i32]
+        L.spv_block_workspace_bytes.restype = sz
+        L.spv_voxelize.argtypes = [vp, vp, sz, vp, vp, i64, f32, vp, i32, i32, vp, vp, vp, vp, vp, vp]
+        L.spv_kernel_map.argtypes = [vp, vp, sz, vp, vp, i64, i32, i32, vp, vp, vp, vp, i64, vp]
+        L.spv_sparse_conv.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i64, i32, i32, vp, vp, vp, i32, vp, vp, i64,
+                                      i32, i32]
+        L.spv_devoxelize.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, vp, i64, f32, i32, vp, i32, vp, i32, vp, vp,
+                                     vp, i32, vp, i32, vp, vp]
+        L.spv_block.argtypes = [vp, vp, sz, ct.POINTER(BlockParams), vp, vp, i64, vp, vp, vp]
+        L.spv_lookup.argtypes = [vp, vp, sz, vp, vp, i64, vp, i64, vp]
+        L.spv_status_check.argtypes = [vp, vp]
+        L.spv_status_string.argtypes = [i32]
+        L.spv_status_string.restype = ct.c_char_p
+        L.spv_last_hip_error.argtypes = []
+        for f in ("spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_devoxelize", "spv_block", "spv_lookup",
+                  "spv_status_check"):
+            getattr(L, f).restype = ct.c_int
+        _lib = L
+    return _lib
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("libspv takes device tensors")
+    if not t.is_contiguous():
+        raise ValueError("libspv takes contiguous tensors")
+    return ct.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ct.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _chk(st: int, what: str):
+    if st != SPV_OK:
+        raise SpvError(st, what)
+
+
+class Workspace:
+    """A caller-owned device workspace (a torch uint8 buffer, 256-byte aligned)."""
+
+    def __init__(self, nbytes: int, device="cuda"):
+        self.nbytes = int(nbytes)
+        self.buf = torch.empty(self.nbytes + 256, dtype=torch.uint8, device=device)
+        off = (-self.buf.data_ptr()) % 256
+        self.ptr = ct.c_void_p(self.buf.data_ptr() + off)
+
+    @classmethod
+    def for_ops(cls, max_points: int, max_C: int, device="cuda"):
+        return cls(lib().spv_workspace_bytes(max_points, max_C), device)
+
+    @classmethod
+    def for_block(cls, max_points: int, C: int, device="cuda"):
+        return cls(lib().spv_block_workspace_bytes(max_points, C), device)
+
+
+def spv_workspace_bytes(max_points: int, max_C: int) -> int:
+    return lib().spv_workspace_bytes(max_points, max_C)
+
+
+def spv_block_workspace_bytes(max_points: int, C: int) -> int:
+    return lib().spv_block_workspace_bytes(max_points, C)
+
+
+def spv_status_check(ws: Workspace) -> int:
+    return lib().spv_status_check(ws.ptr, _stream())
+
+
+@dataclass
+class Voxelized:
+    coords: torch.Tensor    # [cap, 4] int32
+    vfeat: Optional[torch.Tensor]
+    counts: torch.Tensor    # [cap] int32
+    pt2vox: torch.Tensor    # [n] int32
+    m_dev: torch.Tensor     # [1] int64 on device
+    m: Optional[int]        # host copy when synchronized
+
+
+def spv_voxelize(ws: Workspace, xyz: torch.Tensor, voxel_size: float, feat: Optional[torch.Tensor] = None,
+                 batch: Optional[torch.Tensor] = None, sync: bool = True, out: Optional[Voxelized] = None
+                 ) -> Voxelized:
+    n = xyz.shape[0]
+    dev = xyz.device
+    C = feat.shape[1] if feat is not None else 0
+    dt = _DT[feat.dtype] if feat is not None else SPV_F32
+    cap = max(n, 1)
+    if out is None:
+        out = Voxelized(torch.empty((cap, 4), dtype=torch.int32, device=dev),
+                        torch.empty((cap, C), dtype=feat.dtype, device=dev) if feat is not None else None,
+                        torch.empty(cap, dtype=torch.int32, device=dev),
+                        torch.empty(cap, dtype=torch.int32, device=dev),
+                        torch.zeros(1, dtype=torch.int64, device=dev), None)
+    m_host = ct.c_int64(0)
+    st = lib().spv_voxelize(_stream(), ws.ptr, ws.nbytes, _ptr(xyz), _ptr(batch), n, ct.c_float(voxel_size),
+                            _ptr(feat), C, dt, _ptr(out.coords), _ptr(out.vfeat), _ptr(out.counts), _ptr(out.pt2vox),
+                            _ptr(out.m_dev), ct.byref(m_host) if sync else None)
+    _chk(st, "spv_voxelize")
+    out.m = m_host.value if sync else None
+    return out
+
+
+@dataclass
+class KernelMap:
+    out_coords: Optional[torch.Tensor]
+    m_out_dev: torch.Tensor
+    off: torch.Tensor       # [K^3 + 1] int32
+    pairs: torch.Tensor     # [pair_cap, 2] int32 (in, out)
+    total: Optional[int]
+
+
+def spv_kernel_map(ws: Workspace, in_coords: torch.Tensor, K: int = 3, stride: int = 1,
+                   m_in_dev: Optional[torch.Tensor] = None, m_cap: Optional[int] = None,
+                   pair_cap: Optional[int] = None, sync: bool = True) -> KernelMap:
+    dev = in_coords.device
+    m_cap = in_coords.shape[0] if m_cap is None else m_cap
+    K3 = K ** 3
+    if pair_cap is None:
+        pair_cap = max(1, (m_cap if stride == 2 else K3 * m_cap))
+    oc = torch.empty((max(m_cap, 1), 4), dtype=torch.int32, device=dev) if stride == 2 else None
+    km = KernelMap(oc, torch.zeros(1, dtype=torch.int64, device=dev), torch.empty(K3 + 1, dtype=torch.int32, device=dev),
+                   torch.empty((pair_cap, 2), dtype=torch.int32, device=dev), None)
+    tot = ct.c_int64(0)
+    st = lib().spv_kernel_map(_stream(), ws.ptr, ws.nbytes, _ptr(in_coords), _ptr(m_in_dev), m_cap, K, stride,
+                              _ptr(oc), _ptr(km.m_out_dev), _ptr(km.off), _ptr(km.pairs), pair_cap,
+                              ct.byref(tot) if sync else None)
+    if sync:
+        km.total = tot.value
+    _chk(st, "spv_kernel_map")
+    return km
+
+
+def spv_sparse_conv(ws: Workspace, x: torch.Tensor, off: torch.Tensor, pairs: torch.Tensor, W: torch.Tensor,
+                    m_out_cap: int, m_out_dev: Optional[torch.Tensor] = None, scale: Optional[torch.Tensor] = None,
+                    shift: Optional[torch.Tensor] = None, relu: bool = False, transposed: bool = False,
+                    out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    K3, Cin, Cout = W.shape
+    if out is None:
+        out = torch.empty((max(m_out_cap, 1), Cout), dtype=x.dtype, device=x.device)
+    st = lib().spv_sparse_conv(_stream(), ws.ptr, ws.nbytes, _ptr(x), x.shape[0], Cin, _ptr(off), _ptr(pairs),
+                               pairs.shape[0], K3, int(transposed), _ptr(W), _ptr(scale), _ptr(shift), int(relu),
+                               _ptr(out), _ptr(m_out_dev), m_out_cap, Cout, _DT[x.dtype])
+    _chk(st, "spv_sparse_conv")
+    return out
+
+
+def spv_devoxelize(ws: Workspace, grid_coords: torch.Tensor, vfeat: torch.Tensor, xyz: torch.Tensor,
+                   voxel_size: float, stride_log2: int = 0, mode: int = SPV_DEVOX_CENTER,
+                   batch: Optional[torch.Tensor] = None, m_dev: Optional[torch.Tensor] = None,
+                   m_cap: Optional[int] = None, pfeat: Optional[torch.Tensor] = None, Wp: Optional[torch.Tensor] = None,
+                   scale_p: Optional[torch.Tensor] = None, shift_p: Optional[torch.Tensor] = None,
+                   relu_p: bool = False, want_corners: bool = False, out: Optional[torch.Tensor] = None):
+    n = xyz.shape[0]
+    C = vfeat.shape[1]
+    m_cap = grid_coords.shape[0] if m_cap is None else m_cap
+    Cp = pfeat.shape[1] if pfeat is not None else 0
+    if out is None:
+        out = torch.empty((max(n, 1), C), dtype=vfeat.dtype, device=xyz.device)
+    ci = torch.empty((max(n, 1), 8), dtype=torch.int32, device=xyz.device) if want_corners else None
+    cw = torch.empty((max(n, 1), 8), dtype=torch.float32, device=xyz.device) if want_corners else None
+    st = lib().spv_devoxelize(_stream(), ws.ptr, ws.nbytes, _ptr(grid_coords), _ptr(m_dev), m_cap, stride_log2,
+                              _ptr(xyz), _ptr(batch), n, ct.c_float(voxel_size), mode, _ptr(vfeat), C, _ptr(pfeat),
+                              Cp, _ptr(Wp), _ptr(scale_p), _ptr(shift_p), int(relu_p), _ptr(out), _DT[vfeat.dtype],
+                              _ptr(ci), _ptr(cw))
+    _chk(st, "spv_devoxelize")
+    return (out, ci, cw) if want_corners else out
+
+
+def make_block_params(C: int, dtype: torch.dtype, voxel_size: float, convs: Sequence, Wp: torch.Tensor,
+                      scale_p=None, shift_p=None, relu_p: bool = True, mode: int = SPV_DEVOX_CENTER) -> BlockParams:
+    """convs: list of (W [27,C,C], scale|None, shift|None, relu) device tensors (kept alive by the caller)."""
+    p = BlockParams()
+    p.C, p.dtype, p.voxel_size, p.n_convs = C, _DT[dtype], voxel_size, len(convs)
+    for l, (W, sc, sh, r) in enumerate(convs):
+        p.W[l] = W.data_ptr()
+        p.scale[l] = sc.data_ptr() if sc is not None else None
+        p.shift[l] = sh.data_ptr() if sh is not None else None
+        p.relu[l] = int(r)
+    p.Wp = Wp.data_ptr()
+    p.scale_p = scale_p.data_ptr() if scale_p is not None else None
+    p.shift_p = shift_p.data_ptr() if shift_p is not None else None
+    p.relu_p = int(relu_p)
+    p.devox_mode = mode
+    return p
+
+
+def spv_block(ws: Workspace, params: BlockParams, xyz: torch.Tensor, feat: torch.Tensor,
+              batch: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None, sync: bool = False):
+    n, C = feat.shape
+    if out is None:
+        out = torch.empty((max(n, 1), C), dtype=feat.dtype, device=feat.device)
+    m = ct.c_int64(0)
+    st = lib().spv_block(_stream(), ws.ptr, ws.nbytes, ct.byref(params), _ptr(xyz), _ptr(batch), n, _ptr(feat),
+                         _ptr(out), ct.byref(m) if sync else None)
+    _chk(st, "spv_block")
+    return (out, m.value) if sync else out
+
+
+def spv_lookup(ws: Workspace, table_coords: torch.Tensor, qcoords: torch.Tensor,
+               m_dev: Optional[torch.Tensor] = None) -> torch.Tensor:
+    q = qcoords.shape[0]
+    idx = torch.empty(max(q, 1), dtype=torch.int32, device=qcoords.device)
+    st = lib().spv_lookup(_stream(), ws.ptr, ws.nbytes, _ptr(table_coords), _ptr(m_dev), table_coords.shape[0],
+                          _ptr(qcoords), q, _ptr(idx))
+    _chk(st, "spv_lookup")
+    return idx[:q]

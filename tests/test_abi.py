@@ -1,0 +1,80 @@
+"""The C-ABI library loads and exports every symbol include/spv.h declares (no GPU calls)."""
+import ctypes as ct
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "spv.h")
+LIB = os.path.join(ROOT, "paper_2007_16100_amd", "libspv.so")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_][a-z0-9_]*\s*\**\s+(spv_[a-z_0-9]+)\s*\(", src, flags=re.M)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for required in ("spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_devoxelize", "spv_block"):
+        assert required in names
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="libspv.so not built")
+def test_library_exports_every_declared_symbol():
+    lib = ct.CDLL(LIB)
+    missing = [f for f in declared_functions() if not hasattr(lib, f)]
+    assert not missing, missing
+    from paper_2007_16100_amd import spv
+    assert sorted(spv.EXPORTS) == declared_functions()
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="libspv.so not built")
+def test_host_side_validation_without_gpu():
+    """Host-detectable errors return before any HIP call, so they are testable on a CPU-only host."""
+    from paper_2007_16100_amd import spv
+    L = spv.lib()
+    ws = ct.c_void_p(256)  # never dereferenced: validation fails first
+    # non-positive / NaN voxel size
+    for v in (0.0, -1.0, float("nan")):
+        st = L.spv_voxelize(None, ws, 1 << 30, ct.c_void_p(16), None, 4, ct.c_float(v), None, 0, 0,
+                            ct.c_void_p(16), None, ct.c_void_p(16), ct.c_void_p(16), None, None)
+        assert st == spv.SPV_ERR_INVALID_ARG
+    # workspace too small -> capacity
+    st = L.spv_voxelize(None, ws, 16, ct.c_void_p(16), None, 4, ct.c_float(0.1), None, 0, 0, ct.c_void_p(16), None,
+                        ct.c_void_p(16), ct.c_void_p(16), None, None)
+    assert st == spv.SPV_ERR_CAPACITY
+    # unsupported kernel-map geometry
+    st = L.spv_kernel_map(None, ws, 1 << 30, ct.c_void_p(16), None, 4, 3, 2, ct.c_void_p(16), None, ct.c_void_p(16),
+                          ct.c_void_p(16), 100, None)
+    assert st == spv.SPV_ERR_UNSUPPORTED
+    # unsupported conv K3, bad dtype
+    st = L.spv_sparse_conv(None, ws, 1 << 30, ct.c_void_p(16), 4, 8, ct.c_void_p(16), ct.c_void_p(16), 4, 9, 0,
+                           ct.c_void_p(16), None, None, 0, ct.c_void_p(16), None, 4, 16, 1)
+    assert st == spv.SPV_ERR_UNSUPPORTED
+    st = L.spv_sparse_conv(None, ws, 1 << 30, ct.c_void_p(16), 4, 8, ct.c_void_p(16), ct.c_void_p(16), 4, 27, 0,
+                           ct.c_void_p(16), None, None, 0, ct.c_void_p(16), None, 4, 16, 7)
+    assert st == spv.SPV_ERR_INVALID_ARG
+    # misaligned feature pointer
+    st = L.spv_sparse_conv(None, ws, 1 << 30, ct.c_void_p(18), 4, 8, ct.c_void_p(16), ct.c_void_p(16), 4, 27, 0,
+                           ct.c_void_p(16), None, None, 0, ct.c_void_p(16), None, 4, 16, 1)
+    assert st == spv.SPV_ERR_INVALID_ARG
+    # devox: bad mode, stride out of range
+    st = L.spv_devoxelize(None, ws, 1 << 30, ct.c_void_p(16), None, 4, 0, ct.c_void_p(16), None, 4, ct.c_float(0.1),
+                          7, ct.c_void_p(16), 16, None, 0, None, None, None, 0, ct.c_void_p(16), 1, None, None)
+    assert st == spv.SPV_ERR_INVALID_ARG
+    st = L.spv_devoxelize(None, ws, 1 << 30, ct.c_void_p(16), None, 4, 16, ct.c_void_p(16), None, 4,
+                          ct.c_float(0.1), 0, ct.c_void_p(16), 16, None, 0, None, None, None, 0, ct.c_void_p(16), 1,
+                          None, None)
+    assert st == spv.SPV_ERR_INVALID_ARG
+    # block: n_convs out of range
+    p = spv.BlockParams()
+    p.C, p.dtype, p.voxel_size, p.n_convs = 16, 1, 0.1, 3
+    st = L.spv_block(None, ws, 1 << 30, ct.byref(p), ct.c_void_p(16), None, 4, ct.c_void_p(16), ct.c_void_p(16), None)
+    assert st == spv.SPV_ERR_INVALID_ARG
+    assert spv.lib().spv_status_string(3) == b"coordinate out of range"
+    # workspace sizing is monotone and covers the block
+    assert spv.spv_workspace_bytes(1000, 96) < spv.spv_workspace_bytes(100000, 96)
+    assert spv.spv_block_workspace_bytes(121180, 96) > 100 * 1024 * 1024

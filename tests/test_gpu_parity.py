@@ -1,0 +1,333 @@
+"""GPU parity: every HIP entry point (through the C ABI) against the CPU oracle.
+
+Integers (voxel coordinates, counts, point->voxel indices, hash lookups, kernel
+maps, devoxelization corner indices) must match bit for bit.  Floats must
+satisfy the normwise bound max|gpu - oracle| / max|oracle| <= 1e-5 (fp32) or
+2e-2 (bf16 / fp16 storage with fp32 accumulation).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2007_16100_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 2e-2, "f16": 2e-2}
+TD = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
+
+
+@pytest.fixture(scope="module")
+def spv():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2007_16100_amd import spv as s
+    s.lib()
+    return s
+
+
+@pytest.fixture(scope="module")
+def sweep():
+    return synth.lidar_sweep(1002)
+
+
+def dev(a, dtype=None):
+    """numpy (float32 / int32 / uint16 bit patterns) -> device tensor."""
+    if dtype in ("bf16", "f16"):
+        t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(TD[dtype])
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(a))
+    return t.cuda()
+
+
+def host(t, dtype=None):
+    t = t.detach().cpu()
+    if dtype in ("bf16", "f16"):
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()
+
+
+def normwise(g, r, dtype):
+    g = synth.from_storage(g, dtype).astype(np.float64)
+    r = synth.from_storage(r, dtype).astype(np.float64)
+    assert g.shape == r.shape
+    if r.size == 0:
+        return 0.0
+    return float(np.max(np.abs(g - r)) / max(np.max(np.abs(r)), 1e-30))
+
+
+def check_close(g, r, dtype):
+    e = normwise(g, r, dtype)
+    assert e <= TOL[dtype], f"normwise error {e:.3e} > {TOL[dtype]}"
+    return e
+
+
+# ---------------------------------------------------------------------------
+# voxelization
+# ---------------------------------------------------------------------------
+def run_voxelize(spv, xyz, v, feat=None, dtype="f32", batch=None):
+    ws = spv.Workspace.for_ops(max(len(xyz), 1), feat.shape[1] if feat is not None else 16)
+    out = spv.spv_voxelize(ws, dev(xyz), v, None if feat is None else dev(feat, dtype),
+                           None if batch is None else dev(batch))
+    m = out.m
+    return (host(out.coords)[:m], None if feat is None else host(out.vfeat, dtype)[:m], host(out.counts)[:m],
+            host(out.pt2vox)[:len(xyz)], out)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+def test_voxelize_tiny_cube(spv, dtype):
+    xyz = synth.uniform_cube(2000, 1.6, 1001)
+    feat = synth.normal((2000, 16), 1002, dtype=dtype)
+    c, vf, cnt, p2v, _ = run_voxelize(spv, xyz, 0.1, feat, dtype)
+    rc, rvf, rcnt, rp2v = oracle.voxelize(xyz, 0.1, feat, dtype)
+    np.testing.assert_array_equal(c, rc)
+    np.testing.assert_array_equal(cnt, rcnt)
+    np.testing.assert_array_equal(p2v, rp2v)
+    check_close(vf, rvf, dtype)
+
+
+def test_voxelize_sweep_c96(spv, sweep):
+    feat = synth.normal((len(sweep), 96), 1005, dtype="bf16")
+    c, vf, cnt, p2v, _ = run_voxelize(spv, sweep, 0.05, feat, "bf16")
+    rc, rvf, rcnt, rp2v = oracle.voxelize(sweep, 0.05, feat, "bf16")
+    assert len(rc) > 80000
+    np.testing.assert_array_equal(c, rc)
+    np.testing.assert_array_equal(cnt, rcnt)
+    np.testing.assert_array_equal(p2v, rp2v)
+    check_close(vf, rvf, "bf16")
+
+
+@pytest.mark.parametrize("case", ["empty", "one", "one_voxel", "faces", "negative_batch", "odd_c"])
+def test_voxelize_edge_cases(spv, case):
+    rng = np.random.default_rng(77)
+    batch = None
+    C, dtype, v = 8, "bf16", 0.1
+    if case == "empty":
+        xyz = np.zeros((0, 3), np.float32)
+    elif case == "one":
+        xyz = np.array([[0.123, -4.5, 7.0]], np.float32)
+    elif case == "one_voxel":
+        xyz = rng.uniform(0.001, 0.099, size=(20000, 3)).astype(np.float32)
+    elif case == "faces":
+        k = np.arange(-50, 50, dtype=np.float32) * np.float32(v)
+        xyz = np.stack([np.concatenate([k, np.nextafter(k, np.float32(1e9)), np.nextafter(k, np.float32(-1e9))])] * 3,
+                       1).astype(np.float32)
+        xyz[:, 1] = xyz[::-1, 1]
+    elif case == "negative_batch":
+        xyz = rng.uniform(-3000.0, -2990.0, size=(5000, 3)).astype(np.float32)
+        batch = rng.integers(0, 3, size=5000).astype(np.int32)
+    else:  # channel count not a multiple of 8 -> scalar path
+        xyz = rng.uniform(-1, 1, size=(3000, 3)).astype(np.float32)
+        C, dtype = 5, "f32"
+    feat = synth.normal((len(xyz), C), 5, dtype=dtype)
+    c, vf, cnt, p2v, _ = run_voxelize(spv, xyz, v, feat, dtype, batch)
+    rc, rvf, rcnt, rp2v = oracle.voxelize(xyz, v, feat, dtype, batch)
+    np.testing.assert_array_equal(c, rc)
+    np.testing.assert_array_equal(cnt, rcnt)
+    np.testing.assert_array_equal(p2v, rp2v)
+    check_close(vf, rvf, dtype)
+
+
+def test_voxelize_device_errors(spv):
+    xyz = np.zeros((100, 3), np.float32)
+    xyz[17, 1] = np.nan
+    with pytest.raises(spv.SpvError) as e:
+        run_voxelize(spv, xyz, 0.1)
+    assert e.value.status == spv.SPV_ERR_NONFINITE
+    xyz[17, 1] = 5000.0  # floor(5000 / 0.1) = 50000 > 32766
+    with pytest.raises(spv.SpvError) as e:
+        run_voxelize(spv, xyz, 0.1)
+    assert e.value.status == spv.SPV_ERR_RANGE
+    xyz[17, 1] = 0.0
+    with pytest.raises(spv.SpvError) as e:
+        run_voxelize(spv, xyz, 0.1, batch=np.full(100, 65535, np.int32))
+    assert e.value.status == spv.SPV_ERR_RANGE
+
+
+def test_voxelize_deterministic_integers(spv, sweep):
+    a = run_voxelize(spv, sweep, 0.05)
+    b = run_voxelize(spv, sweep, 0.05)
+    for x, y in zip(a[:4], b[:4]):
+        if x is not None:
+            np.testing.assert_array_equal(x, y)
+
+
+def test_lookup(spv, sweep):
+    rc, _, _, _ = oracle.voxelize(sweep, 0.05)
+    rng = np.random.default_rng(3)
+    q = rc[rng.integers(0, len(rc), 20000)].copy()
+    q[::2, 1:] += rng.integers(-1, 2, size=(10000, 3)).astype(np.int32)  # neighbours, present or absent
+    ws = spv.Workspace.for_ops(len(rc), 16)
+    idx = host(spv.spv_lookup(ws, dev(rc), dev(q)))
+    table = {tuple(r): i for i, r in enumerate(rc)}
+    expect = np.array([table.get(tuple(r), -1) for r in q], np.int32)
+    np.testing.assert_array_equal(idx, expect)
+
+
+# ---------------------------------------------------------------------------
+# kernel maps
+# ---------------------------------------------------------------------------
+def run_kmap(spv, coords, K, stride):
+    ws = spv.Workspace.for_ops(len(coords), 16)
+    km = spv.spv_kernel_map(ws, dev(coords), K, stride)
+    oc = host(km.out_coords)[:int(host(km.m_out_dev)[0])] if stride == 2 else None
+    return oc, host(km.off), host(km.pairs)[:km.total], km
+
+
+@pytest.mark.parametrize("K,stride", [(3, 1), (2, 2)])
+def test_kmap_sweep_bitexact(spv, sweep, K, stride):
+    rc, _, _, _ = oracle.voxelize(sweep, 0.05)
+    oc, off, pairs, _ = run_kmap(spv, rc, K, stride)
+    roc, roff, rpairs = oracle.kernel_map(rc, K, stride)
+    np.testing.assert_array_equal(off, roff)
+    np.testing.assert_array_equal(pairs, rpairs)
+    if stride == 2:
+        np.testing.assert_array_equal(oc, roc)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_kmap_random_small(spv, seed):
+    rng = np.random.default_rng(500 + seed)
+    m = int(rng.integers(1, 3000))
+    pts = np.unique(np.concatenate([rng.integers(0, 2, (m, 1)), rng.integers(-12, 12, (m, 3))], 1), axis=0)
+    pts = pts.astype(np.int32)
+    for K, stride in [(3, 1), (2, 2)]:
+        oc, off, pairs, _ = run_kmap(spv, pts, K, stride)
+        roc, roff, rpairs = oracle.kernel_map(pts, K, stride)
+        np.testing.assert_array_equal(off, roff)
+        np.testing.assert_array_equal(pairs, rpairs)
+        if stride == 2:
+            np.testing.assert_array_equal(oc, roc)
+
+
+def test_kmap_duplicate_coords_rejected(spv):
+    pts = np.array([[0, 1, 2, 3], [0, 1, 2, 3]], np.int32)
+    with pytest.raises(spv.SpvError) as e:
+        run_kmap(spv, pts, 3, 1)
+    assert e.value.status == spv.SPV_ERR_INVALID_ARG
+
+
+# ---------------------------------------------------------------------------
+# sparse convolution
+# ---------------------------------------------------------------------------
+def run_conv(spv, x, off, pairs, W, m_out, dtype, scale=None, shift=None, relu=False, transposed=False):
+    ws = spv.Workspace.for_ops(max(m_out, len(x), 1), max(W.shape[1], W.shape[2]))
+    out = spv.spv_sparse_conv(ws, dev(x, dtype), dev(off), dev(pairs), dev(W, dtype), m_out,
+                              scale=None if scale is None else dev(scale), shift=None if shift is None else dev(shift),
+                              relu=relu, transposed=transposed)
+    return host(out, dtype)[:m_out]
+
+
+@pytest.mark.parametrize("cin,cout,dtype,bn", [(32, 32, "bf16", False), (96, 96, "bf16", True),
+                                               (96, 96, "f16", True), (16, 16, "f32", False), (4, 32, "bf16", True),
+                                               (24, 48, "bf16", False), (128, 256, "bf16", True)])
+def test_conv_submanifold_sweep(spv, sweep, cin, cout, dtype, bn):
+    rc, _, _, _ = oracle.voxelize(sweep[::3] if cout >= 256 else sweep, 0.05)
+    _, off, pairs = oracle.kernel_map(rc)
+    x = synth.normal((len(rc), cin), 1003, dtype=dtype)
+    W = synth.conv_weight(27, cin, cout, 1004, dtype)
+    sc, sh = synth.folded_bn(cout, 1005) if bn else (None, None)
+    got = run_conv(spv, x, off, pairs, W, len(rc), dtype, sc, sh, bn)
+    ref = oracle.sparse_conv(x, off, pairs, W, len(rc), dtype, sc, sh, bn)
+    check_close(got, ref, dtype)
+
+
+def test_conv_strided_and_transposed_sweep(spv, sweep):
+    rc, _, _, _ = oracle.voxelize(sweep, 0.05)
+    oc, off, pairs = oracle.kernel_map(rc, 2, 2)
+    x = synth.normal((len(rc), 64), 1006, dtype="bf16")
+    W = synth.conv_weight(8, 64, 128, 1007, "bf16")
+    got = run_conv(spv, x, off, pairs, W, len(oc), "bf16")
+    ref = oracle.sparse_conv(x, off, pairs, W, len(oc), "bf16")
+    check_close(got, ref, "bf16")
+    WT = synth.conv_weight(8, 128, 64, 1008, "bf16")
+    gotT = run_conv(spv, ref, off, pairs, WT, len(rc), "bf16", transposed=True)
+    refT = oracle.sparse_conv(ref, off, pairs, WT, len(rc), "bf16", transposed=True)
+    check_close(gotT, refT, "bf16")
+
+
+def test_conv_deterministic(spv, sweep):
+    rc, _, _, _ = oracle.voxelize(sweep, 0.05)
+    _, off, pairs = oracle.kernel_map(rc)
+    x = synth.normal((len(rc), 32), 11, dtype="bf16")
+    W = synth.conv_weight(27, 32, 32, 12, "bf16")
+    a = run_conv(spv, x, off, pairs, W, len(rc), "bf16")
+    b = run_conv(spv, x, off, pairs, W, len(rc), "bf16")
+    np.testing.assert_array_equal(a, b)
+
+
+# ---------------------------------------------------------------------------
+# devoxelization + point MLP + fusion
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("mode", ["center", "corner"])
+@pytest.mark.parametrize("dtype,C", [("bf16", 96), ("f32", 16), ("f16", 32)])
+def test_devox_sweep(spv, sweep, mode, dtype, C):
+    pts = sweep[::2]
+    rc, _, _, _ = oracle.voxelize(pts, 0.05)
+    vf = synth.normal((len(rc), C), 21, dtype=dtype)
+    pf = synth.normal((len(pts), C), 22, dtype=dtype)
+    Wp = synth.linear_weight(C, C, 23, dtype)
+    sc, sh = synth.folded_bn(C, 24)
+    ws = spv.Workspace.for_ops(len(pts), C)
+    m = spv.SPV_DEVOX_CENTER if mode == "center" else spv.SPV_DEVOX_CORNER
+    out, ci, cw = spv.spv_devoxelize(ws, dev(rc), dev(vf, dtype), dev(pts), 0.05, mode=m, pfeat=dev(pf, dtype),
+                                     Wp=dev(Wp, dtype), scale_p=dev(sc), shift_p=dev(sh), relu_p=True,
+                                     want_corners=True)
+    rout, rci, rcw = oracle.devoxelize(rc, vf, pts, 0.05, mode=mode, pfeat=pf, Wp=Wp, scale_p=sc, shift_p=sh,
+                                       relu_p=True, dtype=dtype, want_corners=True)
+    np.testing.assert_array_equal(host(ci)[:len(pts)], rci)
+    np.testing.assert_array_equal(host(cw)[:len(pts)], rcw)
+    check_close(host(out, dtype)[:len(pts)], rout, dtype)
+
+
+def test_devox_coarse_grid(spv, sweep):
+    pts = sweep[::4]
+    rc, _, _, _ = oracle.voxelize(pts, 0.05)
+    c1, _, _ = oracle.kernel_map(rc, 2, 2)
+    c2, _, _ = oracle.kernel_map(c1, 2, 2)
+    vf = synth.normal((len(c2), 32), 31, dtype="bf16")
+    ws = spv.Workspace.for_ops(len(pts), 32)
+    out = spv.spv_devoxelize(ws, dev(c2), dev(vf, "bf16"), dev(pts), 0.05, stride_log2=2)
+    rout = oracle.devoxelize(c2, vf, pts, 0.05, stride_log2=2, dtype="bf16")
+    check_close(host(out, "bf16")[:len(pts)], rout, "bf16")
+
+
+# ---------------------------------------------------------------------------
+# the SPVConv block
+# ---------------------------------------------------------------------------
+def block_inputs(cfg):
+    if cfg == "tiny":
+        xyz = synth.uniform_cube(2000, 1.6, 1001)
+        C, dtype, v = 16, "f32", 0.1
+        feat = synth.normal((2000, C), 1002, dtype=dtype)
+        convs = [(synth.conv_weight(27, C, C, 1003, dtype), None, None, False)]
+        Wp = synth.linear_weight(C, C, 1004, dtype)
+        return xyz, feat, v, convs, Wp, None, None, dtype
+    xyz = synth.lidar_sweep(1004)
+    C, dtype, v = 96, "bf16", 0.05
+    feat = synth.normal((len(xyz), C), 1005, dtype=dtype)
+    convs = []
+    for l in range(2):
+        sc, sh = synth.folded_bn(C, 1010 + l)
+        convs.append((synth.conv_weight(27, C, C, 1006 + l, dtype), sc, sh, True))
+    Wp = synth.linear_weight(C, C, 1008, dtype)
+    scp, shp = synth.folded_bn(C, 1009)
+    return xyz, feat, v, convs, Wp, scp, shp, dtype
+
+
+@pytest.mark.parametrize("cfg", ["tiny", "sweep_c96"])
+def test_block(spv, cfg):
+    xyz, feat, v, convs, Wp, scp, shp, dtype = block_inputs(cfg)
+    C = feat.shape[1]
+    dconvs = [(dev(W, dtype), None if sc is None else dev(sc), None if sh is None else dev(sh), r)
+              for W, sc, sh, r in convs]
+    dWp = dev(Wp, dtype)
+    dscp = None if scp is None else dev(scp)
+    dshp = None if shp is None else dev(shp)
+    params = spv.make_block_params(C, TD[dtype], v, dconvs, dWp, dscp, dshp, relu_p=True)
+    ws = spv.Workspace.for_block(len(xyz), C)
+    out, m = spv.spv_block(ws, params, dev(xyz), dev(feat, dtype), sync=True)
+    rout, rm = oracle.block(xyz, feat, v, convs, Wp, scp, shp, relu_p=True, dtype=dtype)
+    assert m == rm
+    check_close(host(out, dtype)[:len(xyz)], rout, dtype)
