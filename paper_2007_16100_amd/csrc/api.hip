@@ -26,7 +26,7 @@ spv_status flags_to_status(uint32_t f) {
     if (f & kFlagNonfinite) return SPV_ERR_NONFINITE;
     if (f & kFlagRange) return SPV_ERR_RANGE;
     if (f & (kFlagCapacity | kFlagTableFull)) return SPV_ERR_CAPACITY;
-    if (f & kFlagDuplicate) return SPV_ERR_INVALID_ARG;
+    if (f & (kFlagDuplicate | kFlagUnsorted)) return SPV_ERR_INVALID_ARG;
     return SPV_OK;
 }
 
@@ -75,10 +75,11 @@ struct ConvLayout {
     ConvPlan p;
     void* wpack;
 };
-size_t layout_conv(void* ws, size_t bytes, int64_t m_out_cap, int K3, int Cin, int Cout, ConvLayout& L) {
+size_t layout_conv(void* ws, size_t bytes, int64_t m_out_cap, int K3, int Cin, int Cout, int dt, ConvLayout& L) {
     Arena a(ws, bytes);
     L.h = a.take<Header>(1);
-    plan_conv_ws(a, L.p, m_out_cap, K3);
+    plan_conv_ws(a, L.p, m_out_cap, K3, Cin, Cout, dt);
+    L.p.h = L.h;
     L.wpack = plan_wpack_ws(a, K3, Cin, Cout > 16 ? Cout : 16);
     return a.used;
 }
@@ -132,7 +133,8 @@ size_t layout_block(void* ws, size_t bytes, int64_t n, int C, int dt, BlockLayou
     L.map.h = L.h;
     L.map.fine = L.vox.table;  // the voxelization's table serves the kernel map and the devoxelization
     plan_kmap_ws(a, L.map, nn, 3, 1, false);
-    plan_conv_ws(a, L.plan, nn, 27);
+    plan_conv_ws(a, L.plan, nn, 27, C, C, dt);
+    L.plan.h = L.h;
     L.coords = a.take<int32_t>(4 * nn);
     L.counts = a.take<int32_t>(nn);
     L.pt2vox = a.take<int32_t>(nn);
@@ -166,7 +168,7 @@ size_t spv_workspace_bytes(int64_t max_points, int32_t max_C) {
     size_t s = layout_voxelize(nullptr, 0, max_points, v);
     s = std::max(s, layout_kmap(nullptr, 0, max_points, 3, 1, m));
     s = std::max(s, layout_kmap(nullptr, 0, max_points, 2, 2, m));
-    s = std::max(s, layout_conv(nullptr, 0, max_points, 27, max_C, max_C, c));
+    s = std::max(s, layout_conv(nullptr, 0, max_points, 27, max_C, max_C, SPV_BF16, c));
     s = std::max(s, layout_devox(nullptr, 0, max_points, max_points, max_C, max_C, d));
     return s;
 }
@@ -274,15 +276,16 @@ spv_status spv_sparse_conv(void* stream, void* ws, size_t ws_bytes, const void* 
     if ((in_rows > 0 && !in) || (m_out_cap > 0 && !out) || (pair_cap > 0 && !pairs)) return SPV_ERR_INVALID_ARG;
     if (!aligned16(in) || !aligned16(out) || !aligned16(W)) return SPV_ERR_INVALID_ARG;
     ConvLayout L;
-    if (need(layout_conv(nullptr, 0, m_out_cap, K3, Cin, Cout, L), ws_bytes)) return SPV_ERR_CAPACITY;
-    layout_conv(ws, ws_bytes, m_out_cap, K3, Cin, Cout, L);
+    if (need(layout_conv(nullptr, 0, m_out_cap, K3, Cin, Cout, dt, L), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_conv(ws, ws_bytes, m_out_cap, K3, Cin, Cout, dt, L);
     if (m_out_cap == 0) return SPV_OK;
     hipStream_t s = (hipStream_t)stream;
     L.p.m_out_dev = m_out_dev;
     launch_clear_header(s, L.h);
-    launch_conv_plan(s, L.p, off, pairs, K3, transposed, pair_cap);
+    launch_conv_plan(s, L.p, off, pairs, K3, transposed, pair_cap, in_rows);
     launch_conv_pack(s, K3, W, L.wpack, Cin, Cout, dt);
-    launch_conv_run(s, L.p, in, Cin, in_rows, W, L.wpack, scale, shift, relu, out, Cout, dt);
+    launch_conv_run(s, L.p, in, Cin, in_rows, pairs, pair_cap, transposed, W, L.wpack, scale, shift, relu, out, Cout,
+                    dt);
     return hip_check();
 }
 
@@ -360,14 +363,14 @@ spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_pa
     launch_kernel_map(s, L.map, false, L.coords, L.m_dev, nn, 3, 1, nullptr, nullptr, L.off, L.pairs, L.pair_cap);
     mark(2);
     L.plan.m_out_dev = L.m_dev;
-    launch_conv_plan(s, L.plan, L.off, L.pairs, 27, 0, L.pair_cap);
+    launch_conv_plan(s, L.plan, L.off, L.pairs, 27, 0, L.pair_cap, nn);
     for (int l = 0; l < p->n_convs; ++l) launch_conv_pack(s, 27, p->W[l], L.wpack_conv[l], C, C, dt);
     mark(3);
     void* cur = L.va;
     void* nxt = L.vb;
     for (int l = 0; l < p->n_convs; ++l) {
-        launch_conv_run(s, L.plan, cur, C, nn, p->W[l], L.wpack_conv[l], p->scale[l], p->shift[l], p->relu[l], nxt,
-                        C, dt);
+        launch_conv_run(s, L.plan, cur, C, nn, L.pairs, L.pair_cap, 0, p->W[l], L.wpack_conv[l], p->scale[l],
+                        p->shift[l], p->relu[l], nxt, C, dt);
         void* t = cur;
         cur = nxt;
         nxt = t;

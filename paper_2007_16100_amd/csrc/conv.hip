@@ -1,42 +1,49 @@
 // conv.hip -- sparse convolution on a kernel map (Sec. 3.2 / 3.3):
 //   out[j] = act(scale * sum_{(i, j, k)} in[i] @ W[k] + shift)
 //
-// Output-stationary gather-GEMM on matrix cores.  Output rows are taken in
-// blocks of 16 (one MFMA M-tile); a plan built from the kernel map records, per
-// block, the union of the offsets its rows use and, per (block, offset, row),
-// the input row.  A wave owns R blocks x all output channels in registers
-// (fp32 accumulators) and walks the offsets of its blocks: for each offset the
-// packed weight slice W[k] is loaded once into registers and reused by every
-// block that has the offset, the A operand is gathered straight from the
-// input feature rows (16 bytes per lane, absent rows masked to zero), and
-// v_mfma_f32_16x16x32_{bf16,f16} accumulates.  The epilogue applies the
-// per-channel scale/shift and ReLU and writes each output row exactly once:
-// no atomics, deterministic results.
-#include "spv_internal.hpp"
+// Two matrix-core kernels, both deterministic (no atomics; every output element
+// is summed in ascending offset order) and both writing every output row once:
+//
+// * k_conv_union (3x3x3 maps): a wave owns blocks of 16 output rows with all
+//   output channels, accumulated in registers.  For each of the 27 offsets it
+//   gathers the 16 rows' neighbours (zeros where a neighbour is absent) and
+//   multiplies them by W[k] on v_mfma_f32_16x16x32_{bf16,f16}; blocks whose
+//   rows have no neighbour at that offset skip it.  W[k] is staged once per
+//   workgroup in LDS (asynchronous global->LDS copies two offsets ahead), and
+//   each wave's gathers for the next offset are in flight while the current
+//   one is multiplied.  The cost is MFMA work on absent neighbours: on a LiDAR
+//   sweep the 16-row unions of present offsets are ~3x the pairs.
+//
+// * k_conv_tile (stride-2 and transposed maps, where a 16-row union would be
+//   mostly empty): output rows in tiles of T with an LDS fp32 accumulator; the
+//   pairs of each (tile, offset) are a contiguous slice of the kernel map,
+//   multiplied 16 at a time and added into their output rows.
+//
+// A vector-ALU tile kernel covers fp32 and shapes the MFMA kernels do not take.
+#include "conv_common.hpp"
 
 namespace spv {
 
-constexpr int kRowsPerTile = 16;
 
-void plan_conv_ws(Arena& a, ConvPlan& p, int64_t m_out_cap, int K3) {
+// ---------------------------------------------------------------------------
+// plan
+// ---------------------------------------------------------------------------
+static int conv_tile_rows(int Cin, int Cout, int dt);
+
+// The boundary array is sized for the smallest tile (16 rows) and the neighbour
+// table is reserved for every 3x3x3 plan, so the workspace size does not depend
+// on the channel counts or the dtype.
+void plan_conv_ws(Arena& a, ConvPlan& p, int64_t m_out_cap, int K3, int Cin, int Cout, int dt) {
     p.m_cap = m_out_cap > 0 ? m_out_cap : 1;
     p.K3 = K3;
-    int64_t nb = (p.m_cap + kRowsPerTile - 1) / kRowsPerTile;
-    p.mask = a.take<uint32_t>(p.m_cap);
-    p.umask = a.take<uint32_t>(nb);
-    p.ucnt = a.take<uint32_t>(nb + 1);
-    p.table = a.take<int32_t>((size_t)K3 * nb * kRowsPerTile);
-}
-
-__device__ inline int64_t clamp_rows(const int64_t* d, int64_t cap) {
-    if (!d) return cap;
-    int64_t c = *d;
-    return c < 0 ? 0 : (c > cap ? cap : c);
-}
-
-__global__ void k_plan_zero(uint32_t* mask, int64_t cap) {
-    int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    if (j < cap) mask[j] = 0;
+    p.use_union = union_supported(K3, Cin, Cout, dt) && p.m_cap * K3 * 4 <= (int64_t)0xFFFFE000 ? 1 : 0;
+    p.tile_rows = conv_tile_rows(Cin, Cout, dt);
+    p.ntile_cap = (p.m_cap + p.tile_rows - 1) / p.tile_rows;
+    p.bnd = a.take<int32_t>((size_t)K3 * ((p.m_cap + kChunk - 1) / kChunk + 1));
+    // reserved for every 3x3x3 plan, so that a workspace sized for one dtype / width serves all
+    p.nbr = K3 == 27 ? a.take<int32_t>((size_t)p.m_cap * K3) : nullptr;
+    p.h = nullptr;
+    p.m_out_dev = nullptr;
 }
 
 // the offset k of pair p (off is non-decreasing)
@@ -46,72 +53,101 @@ __device__ inline int pair_offset(const int32_t* soff, int K3, int64_t p) {
     return k;
 }
 
-__global__ void k_plan_mask(const int32_t* off, const int32_t* pairs, int K3, int transposed, int64_t pair_bound,
-                            const int64_t* m_out_dev, int64_t cap, uint32_t* mask) {
-    __shared__ int32_t soff[28];
+// tile of output row j; rows outside [0, m) are placed where they sort
+// (negative rows before tile 0's rows, rows >= m after the last tile)
+__device__ inline int64_t tile_of(int64_t j, int64_t m, int64_t nt, int T) {
+    if (j < 0) return 0;
+    if (j >= m) return nt;
+    return j / T;
+}
+
+// For every offset k and tile t in [0, nt]: bnd[k][t] = first pair of offset k
+// with tile_of(out) >= t.  Each pair writes the entries of the tiles that begin
+// at it; one extra item per offset writes the entries past its last pair.
+__global__ void k_conv_bounds(const int32_t* off, const int32_t* pairs, int K3, int transposed, int64_t pair_bound,
+                              const int64_t* m_out_dev, int64_t cap, int T, int64_t ntc, int32_t* bnd, Header* h) {
+    __shared__ int32_t soff[kMaxK3 + 1];
     if (threadIdx.x <= K3) soff[threadIdx.x] = off[threadIdx.x];
     __syncthreads();
     int64_t total = soff[K3];
     if (total > pair_bound) total = pair_bound;
-    int64_t m = clamp_rows(m_out_dev, cap);
-    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < total; p += (int64_t)gridDim.x * blockDim.x) {
-        int k = pair_offset(soff, K3, p);
-        int64_t j = transposed ? pairs[2 * p] : pairs[2 * p + 1];
-        if (j >= 0 && j < m) atomicOr(&mask[j], 1u << k);
+    if (total < 0) total = 0;
+    const int64_t m = clamp_rows(m_out_dev, cap);
+    const int64_t nt = (m + T - 1) / T;
+    const int osel = transposed ? 0 : 1;  // column of the output row in a pair
+    const int64_t stride = ntc + 1;
+    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < total + K3;
+         p += (int64_t)gridDim.x * blockDim.x) {
+        if (p < total) {
+            const int k = pair_offset(soff, K3, p);
+            const int64_t cur = tile_of(pairs[2 * p + osel], m, nt, T);
+            const int64_t prev = (p == soff[k]) ? -1 : tile_of(pairs[2 * (p - 1) + osel], m, nt, T);
+            if (cur < prev) {
+                raise_flag(h, kFlagUnsorted);
+                continue;
+            }
+            for (int64_t t = prev + 1; t <= cur; ++t) bnd[k * stride + t] = (int32_t)p;
+        } else {
+            const int k = (int)(p - total);
+            int64_t lo = soff[k], hi = soff[k + 1];
+            if (lo > total) lo = total;
+            if (hi > total) hi = total;
+            const int64_t prev = (hi > lo) ? tile_of(pairs[2 * (hi - 1) + osel], m, nt, T) : -1;
+            for (int64_t t = prev + 1; t <= nt; ++t) bnd[k * stride + t] = (int32_t)hi;
+        }
     }
 }
 
-__global__ void k_plan_union(const uint32_t* mask, const int64_t* m_out_dev, int64_t cap, int64_t nblk,
-                             uint32_t* umask, uint32_t* ucnt) {
-    int64_t b = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    if (b >= nblk) return;
-    int64_t m = clamp_rows(m_out_dev, cap);
-    uint32_t u = 0;
-    for (int r = 0; r < kRowsPerTile; ++r) {
-        int64_t j = b * kRowsPerTile + r;
-        if (j < m) u |= mask[j];
+// neighbour table: nbr[j][k] = i + 1 for every pair (i, j) of offset k, 0 elsewhere
+__global__ void k_nbr_clear(int32_t* nbr, const int64_t* m_out_dev, int64_t cap, int K3) {
+    const int64_t n = clamp_rows(m_out_dev, cap) * K3;
+    for (int64_t e = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4; e < n;
+         e += (int64_t)gridDim.x * blockDim.x * 4) {
+        if (e + 4 <= n && ((e & 3) == 0)) {
+            *(int4*)(nbr + e) = make_int4(0, 0, 0, 0);
+        } else {
+            for (int64_t q = e; q < n && q < e + 4; ++q) nbr[q] = 0;
+        }
     }
-    umask[b] = u;
-    ucnt[b] = (uint32_t)__popc(u);
 }
 
-__global__ void k_plan_scatter(const int32_t* off, const int32_t* pairs, int K3, int transposed, int64_t pair_bound,
-                               const int64_t* m_out_dev, int64_t cap, const uint32_t* umask, const uint32_t* ucnt,
-                               int32_t* table) {
-    __shared__ int32_t soff[28];
+__global__ void k_nbr_scatter(const int32_t* off, const int32_t* pairs, int K3, int transposed, int64_t pair_bound,
+                              const int64_t* m_out_dev, int64_t cap, int64_t in_rows, int32_t* nbr) {
+    __shared__ int32_t soff[kMaxK3 + 1];
     if (threadIdx.x <= K3) soff[threadIdx.x] = off[threadIdx.x];
     __syncthreads();
     int64_t total = soff[K3];
     if (total > pair_bound) total = pair_bound;
-    int64_t m = clamp_rows(m_out_dev, cap);
+    const int64_t m = clamp_rows(m_out_dev, cap);
     for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < total; p += (int64_t)gridDim.x * blockDim.x) {
-        int k = pair_offset(soff, K3, p);
-        int64_t i = transposed ? pairs[2 * p + 1] : pairs[2 * p];
-        int64_t j = transposed ? pairs[2 * p] : pairs[2 * p + 1];
-        if (j < 0 || j >= m) continue;
-        int64_t b = j / kRowsPerTile;
-        uint32_t u = umask[b];
-        uint32_t slot = (uint32_t)__popc(u & ((1u << k) - 1u));
-        table[((int64_t)ucnt[b] + slot) * kRowsPerTile + (j % kRowsPerTile)] = (int32_t)i;
+        const int k = pair_offset(soff, K3, p);
+        const int64_t i = transposed ? pairs[2 * p + 1] : pairs[2 * p];
+        const int64_t j = transposed ? pairs[2 * p] : pairs[2 * p + 1];
+        if (i >= 0 && i < in_rows && j >= 0 && j < m) nbr[j * K3 + k] = (int32_t)(i + 1);
     }
 }
 
 void launch_conv_plan(hipStream_t s, const ConvPlan& p, const int32_t* off, const int32_t* pairs, int K3,
-                      int transposed, int64_t pair_bound) {
-    int64_t nblk = (p.m_cap + kRowsPerTile - 1) / kRowsPerTile;
-    unsigned gp = blocks_for(pair_bound, 256);
-    if (gp > 4096) gp = 4096;
-    k_plan_zero<<<blocks_for(p.m_cap, 256), 256, 0, s>>>(p.mask, p.m_cap);
-    k_plan_mask<<<gp, 256, 0, s>>>(off, pairs, K3, transposed, pair_bound, p.m_out_dev, p.m_cap, p.mask);
-    k_plan_union<<<blocks_for(nblk, 256), 256, 0, s>>>(p.mask, p.m_out_dev, p.m_cap, nblk, p.umask, p.ucnt);
-    launch_exclusive_scan_small(s, p.ucnt, p.ucnt, nblk);
-    k_plan_scatter<<<gp, 256, 0, s>>>(off, pairs, K3, transposed, pair_bound, p.m_out_dev, p.m_cap, p.umask, p.ucnt,
-                                      p.table);
+                      int transposed, int64_t pair_bound, int64_t in_rows) {
+    unsigned g = blocks_for(pair_bound + K3, 256);
+    if (g > 2048) g = 2048;
+    if (p.use_union) {
+        unsigned gc = blocks_for(p.m_cap * K3, 1024);
+        if (gc > 2048) gc = 2048;
+        k_nbr_clear<<<gc, 256, 0, s>>>(p.nbr, p.m_out_dev, p.m_cap, K3);
+        k_nbr_scatter<<<g, 256, 0, s>>>(off, pairs, K3, transposed, pair_bound, p.m_out_dev, p.m_cap, in_rows, p.nbr);
+    } else {
+        k_conv_bounds<<<g, 256, 0, s>>>(off, pairs, K3, transposed, pair_bound, p.m_out_dev, p.m_cap, p.tile_rows,
+                                        p.ntile_cap, p.bnd, p.h);
+    }
 }
 
 // ---------------------------------------------------------------------------
-// weight packing into MFMA B-operand fragments:
-// wpack[((k * KCH + kc) * NB + nb) * 64 + lane] = W[k][kc*32 + 8*(lane/16) + e][nb*16 + lane%16], e = 0..7
+// weight packing into MFMA operand fragments:
+// wpack[((k * KCH + kc) * NB + nb) * 64 + lane] holds, for e = 0..7,
+//   W[k][kc*32 + 8*(lane/16) + e][nb*16 + lane%16]
+// i.e. lane l carries output channel nb*16 + l%16 and 8 consecutive input
+// channels: the A operand of D = W^T G^T (or the B operand of D = G W).
 // ---------------------------------------------------------------------------
 __global__ void k_pack_w(const uint16_t* W, int K3, int Cin, int Cout, int KCH, int NB, uint4* wpack) {
     int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
@@ -136,191 +172,462 @@ __global__ void k_pack_w(const uint16_t* W, int K3, int Cin, int Cout, int KCH, 
     wpack[t] = make_uint4(w[0], w[1], w[2], w[3]);
 }
 
+static int conv_kch(int Cin);
+
 void* plan_wpack_ws(Arena& a, int K3, int Cin, int Cout) {
-    int KCH = (Cin + 31) / 32, NB = Cout / 16;
+    int KCH = conv_kch(Cin), NB = (Cout + 15) / 16;
     return a.take<uint4>((size_t)K3 * KCH * NB * 64);
 }
 
 // ---------------------------------------------------------------------------
-// MFMA conv
+// MFMA tile kernel
 // ---------------------------------------------------------------------------
-template <int DT, int KCH, int NB, int R>
-__global__ __launch_bounds__(256) void k_conv_mfma(ConvPlan p, const uint16_t* __restrict__ in, int Cin, int64_t in_rows,
-                                                   const uint4* __restrict__ wpack, const float* __restrict__ scale,
-                                                   const float* __restrict__ shift, int relu,
-                                                   uint16_t* __restrict__ out, int Cout) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int r16 = lane & 15, g = lane >> 4;
-    const int64_t m = clamp_rows(p.m_out_dev, p.m_cap);
-    const int64_t nblk = (m + kRowsPerTile - 1) / kRowsPerTile;
-    const int64_t b0 = ((int64_t)blockIdx.x * 4 + wave) * R;
-    if (b0 >= nblk) return;
-
-    uint32_t U[R], base[R], mrow[R];
-    uint32_t Uall = 0;
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        int64_t b = b0 + r;
-        bool vb = b < nblk;
-        U[r] = vb ? p.umask[b] : 0u;
-        base[r] = vb ? p.ucnt[b] : 0u;
-        int64_t row = b * kRowsPerTile + r16;
-        mrow[r] = (vb && row < m) ? p.mask[row] : 0u;
-        Uall |= U[r];
+// LDS layout (dynamic, in this order):
+//   float acc[T + 1][Cout + 4]        fp32 accumulator of the tile (+ a spill row)
+//   uint4 wslot[NW][KCH*NBW*64]       each wave's weight fragments of the next offset
+//   int2  tab[T/16*K3 + K3]           chunk -> (first pair, offset | pairs << 8)
+//   int   nextk[K3], nchunk
+struct ConvTileSmem {
+    static __host__ __device__ int acc_stride(int Cout) { return Cout + 4; }
+    static __host__ __device__ int tab_entries(int T, int K3) { return T / kChunk * K3 + K3; }
+    static __host__ __device__ size_t acc_bytes(int T, int Cout) { return (size_t)(T + 1) * acc_stride(Cout) * 4; }
+    static __host__ __device__ size_t wslot_bytes(int KCH, int NBW) { return (size_t)KCH * NBW * 64 * 16; }
+    static __host__ __device__ size_t bytes(int T, int Cout, int K3, int KCH, int NBW, int NW) {
+        return acc_bytes(T, Cout) + (size_t)NW * wslot_bytes(KCH, NBW) + (size_t)tab_entries(T, K3) * 8 +
+               (size_t)(K3 + 1) * 4;
     }
-    f32x4 acc[R][NB];
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[r][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+};
 
-    while (Uall) {
-        const int k = __builtin_ctz(Uall);
-        Uall &= Uall - 1;
-        const uint16_t* src[R];
-        bool has[R], ok[R];
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            has[r] = (U[r] >> k) & 1u;
-            int32_t i = -1;
-            if (has[r] && ((mrow[r] >> k) & 1u)) {
-                const uint32_t slot = (uint32_t)__popc(U[r] & ((1u << k) - 1u));
-                i = p.table[((int64_t)base[r] + slot) * kRowsPerTile + r16];
+// Every wave runs a software pipeline over the chunks of its tile: the pair
+// (input row, output row) of chunk c + kPairAhead and the gathered input rows
+// of chunk c + kRowAhead are loaded while chunk c is multiplied.  The chunk
+// loop is unrolled by kPairAhead so that each pipeline slot is a fixed
+// register, and every load writes straight into the slot just consumed (a
+// register copy of a value still in flight would wait for it).  Gathers and
+// pair loads are raw buffer loads: 32-bit offsets from a scalar base, and the
+// hardware range check returns zeros for an absent row.
+//
+// Weights take a separate path.  Vector-memory loads complete in issue order
+// and are waited for by count, so a register load of the next offset's weights
+// would, when waited for, also wait for every gather issued before it.  Instead
+// each wave copies the weight fragments of the next offset straight into its
+// own LDS slot (global_load_lds_dwordx4, one 1 KB fragment block per
+// instruction) when it enters an offset, and at the next offset change waits
+// only until those copies are older than the loads issued since; it then reads
+// the fragments from LDS.  Every pipeline step issues exactly KCH + 1
+// vector-memory loads, which makes that count exact.
+constexpr int kRowAhead = 4;
+constexpr int kPairAhead = 8;
+template <int DT, int KCH, int NBW, int TR>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_conv_tile(ConvPlan p, const uint16_t* __restrict__ in, int Cin,
+                                                    int64_t in_rows, const int32_t* __restrict__ pairs,
+                                                    int64_t pair_bound,
+                                                    const uint4* __restrict__ wpack, int NB,
+                                                    const float* __restrict__ scale, const float* __restrict__ shift,
+                                                    int relu, uint16_t* __restrict__ out, int Cout) {
+    constexpr int kStepLoads = KCH + 1;  // vector-memory loads per pipeline step
+    constexpr int kFrag = KCH * NBW;     // weight fragments per wave and offset
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int T = p.tile_rows, K3 = p.K3;
+    const int nthr = blockDim.x, NW = nthr >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int r16 = lane & 15, g = lane >> 4;
+
+    // tiles of one XCD are contiguous (blocks are dispatched round-robin over the 8 XCDs)
+    const int64_t G = gridDim.x;
+    const int64_t bid = blockIdx.x;
+    const int64_t xq = G / 8, xr = G % 8, x = bid % 8;
+    const int64_t t = x * xq + (x < xr ? x : xr) + bid / 8;
+
+    const int64_t m = clamp_rows(p.m_out_dev, p.m_cap);
+    const int64_t nt = (m + T - 1) / T;
+    if (t >= nt) return;
+    const int64_t row0 = t * T;
+    const int rows = (int)((m - row0) < T ? (m - row0) : T);
+
+    const int ACS = ConvTileSmem::acc_stride(Cout);
+    float* acc = (float*)smem;  // T + 1 rows: row T absorbs the lanes without a pair
+    uint4* wslots = (uint4*)(smem + ConvTileSmem::acc_bytes(T, Cout));
+    uint4* wslot = wslots + (size_t)wave * kFrag * 64;
+    int2* tab = (int2*)(wslots + (size_t)NW * kFrag * 64);
+    int* nextk = (int*)(tab + ConvTileSmem::tab_entries(T, K3));
+    int* s_nchunk = nextk + K3;
+
+    // chunk table of this tile: offsets in ascending order, 16 pairs per chunk
+    if (wave == 0) {
+        const int64_t bs = p.ntile_cap + 1;
+        int lo = 0, n = 0;
+        if (lane < K3) {
+            // clamped into [0, pair_bound): a map that is not a valid kernel map
+            // (unsorted groups, repeated output rows) gives wrong sums, never a
+            // read outside the pair list or the chunk table
+            int64_t l = p.bnd[lane * bs + t], hh = p.bnd[lane * bs + t + 1];
+            l = l < 0 ? 0 : (l > pair_bound ? pair_bound : l);
+            hh = hh < l ? l : (hh > pair_bound ? pair_bound : hh);
+            if (hh - l > T) {
+                raise_flag(p.h, kFlagUnsorted);
+                hh = l + T;
             }
-            ok[r] = i >= 0 && i < in_rows;
-            src[r] = in + (int64_t)(ok[r] ? i : 0) * Cin + 8 * g;
+            lo = (int)l;
+            n = (int)(hh - l);
         }
+        const int nch = (n + kChunk - 1) / kChunk;
+        int incl = nch;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            int y = __shfl_up(incl, d, 64);
+            if (lane >= d) incl += y;
+        }
+        const int start = incl - nch;
+        for (int c = 0; c < nch; ++c) {
+            const int np = (n - c * kChunk) < kChunk ? (n - c * kChunk) : kChunk;
+            tab[start + c] = make_int2(lo + c * kChunk, lane | (np << 8));
+        }
+        const uint64_t has = __ballot(nch > 0);
+        if (lane < K3) {
+            const uint64_t later = has & ~((2ull << lane) - 1ull);
+            nextk[lane] = later ? __builtin_ctzll(later) : -1;
+        }
+        if (lane == 63) *s_nchunk = incl;
+    }
+    // zero the accumulator (and the spill row)
+    for (int e = tid; e < (T + 1) * ACS / 4; e += nthr) ((float4*)acc)[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+    __syncthreads();
+    const int NC = *s_nchunk;
+
+    const uint32_t row_bytes = (uint32_t)Cin * 2u;
+    const __amdgpu_buffer_rsrc_t in_rs = make_rsrc(in, (uint32_t)(in_rows * (int64_t)row_bytes));
+    const __amdgpu_buffer_rsrc_t pr_rs = make_rsrc(pairs, (uint32_t)(pair_bound * 8));
+    const int qin = Cin / 8;                      // 16-byte pieces of an input row
+    const bool ragged = Cin != KCH * 32;          // some pieces of the last K block are padding
+    const int nb0 = wave * NBW;                   // the wave's output channel blocks
+
+    // weight fragments of offset k -> this wave's LDS slot (asynchronous)
+    const uint64_t wbase = (uint64_t)(uintptr_t)wpack + (uint64_t)nb0 * 1024u;
+    const uint32_t wslot_lds = __builtin_amdgcn_readfirstlane(lds_addr(wslot));
+    const uint32_t wlane = (uint32_t)lane * 16u;
+    auto dma_w = [&](int k) {
+        lds_wait();  // the slot's previous contents have been read
+        const uint64_t kb = wbase + (uint64_t)(k * KCH) * (uint64_t)NB * 1024u;
+#pragma unroll
+        for (int kc = 0; kc < KCH; ++kc)
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                lds_dma_x4(kb + (uint64_t)(kc * NB + nb) * 1024u, wlane,
+                           wslot_lds + (uint32_t)((kc * NBW + nb) * 1024));
+    };
+    uint4 wc[KCH][NBW];
+    auto read_w = [&]() {
+#pragma unroll
+        for (int kc = 0; kc < KCH; ++kc)
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) wc[kc][nb] = wslot[(kc * NBW + nb) * 64 + lane];
+    };
+
+    // --- pipeline registers ------------------------------------------------
+    // ps[c % kPairAhead]: raw (in, out) pair of chunk c for lane row r16, valid
+    // iff bit c % kPairAhead of pv; rs[c % kRowAhead]: its gathered row pieces
+    // (zeros for an absent or out-of-range row)
+    i32x2 ps[kPairAhead];
+    uint32_t pv = 0;
+    i32x4 rs[kRowAhead][KCH];
+
+    // chunks past NC (the loop runs whole groups of kPairAhead) are empty:
+    // their loads read past every record and return zeros
+    auto load_pair = [&](int cc, i32x2& dst) -> bool {
+        const int2 te = tab[cc < NC ? cc : NC - 1];
+        const bool valid = cc < NC && r16 < (te.y >> 8);
+        dst = __builtin_amdgcn_raw_buffer_load_b64(pr_rs, valid ? (uint32_t)(te.x + r16) * 8u : kOutOfRange, 0, 0);
+        return valid;
+    };
+    const uint32_t in_rows32 = (uint32_t)in_rows;  // in_rows * row_bytes < 2^32 (checked by the host)
+    auto load_rows = [&](const i32x2& pr, bool valid, i32x4 (&dst)[KCH]) {
+        const uint32_t i = (uint32_t)(TR ? pr.y : pr.x);
+        const uint32_t base = (valid && i < in_rows32) ? i * row_bytes + (uint32_t)g * 16u : kOutOfRange;
 #pragma unroll
         for (int kc = 0; kc < KCH; ++kc) {
-            uint4 bf[NB];
+            uint32_t off = base + kc * 64;
+            if (ragged && kc * 4 + g >= qin) off = kOutOfRange;
+            dst[kc] = __builtin_amdgcn_raw_buffer_load_b128(in_rs, off, 0, 0);
+        }
+    };
+
+    int kcur = -1;
+    int since = kRowAhead;  // pipeline steps since the last weight copy was issued
+    if (NC > 0) {
+        kcur = tab[0].y & 0xFF;
+        dma_w(kcur);
+        vm_wait<0>();
+        read_w();
+        const int kn = nextk[kcur];
+        if (kn >= 0) dma_w(kn);
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) bf[nb] = wpack[((int64_t)(k * KCH + kc) * NB + nb) * 64 + lane];
-            const bool chok = kc * 32 + 8 * g < Cin;
+        for (int j = 0; j < kPairAhead; ++j)
+            if (load_pair(j, ps[j])) pv |= 1u << j;
 #pragma unroll
-            for (int r = 0; r < R; ++r) {
-                if (!has[r]) continue;
-                uint4 a = make_uint4(0, 0, 0, 0);
-                if (ok[r] && chok) a = *(const uint4*)(src[r] + kc * 32);
+        for (int j = 0; j < kRowAhead; ++j) load_rows(ps[j], (pv >> j) & 1u, rs[j]);
+    }
+
+    for (int c0 = 0; c0 < NC; c0 += kPairAhead) {
 #pragma unroll
-                for (int nb = 0; nb < NB; ++nb) acc[r][nb] = mfma16x16x32<DT>(a, bf[nb], acc[r][nb]);
+        for (int u = 0; u < kPairAhead; ++u) {
+            const int c = c0 + u;
+            const int sr = u % kRowAhead;
+            // (a) entering a new offset: its weights were copied one offset ago
+            const int k = c < NC ? __builtin_amdgcn_readfirstlane(tab[c].y & 0xFF) : kcur;
+            if (k != kcur) {
+                // loads issued after that copy: `since` steps of kStepLoads each;
+                // after kRowAhead steps the row waits below have covered it
+                if (since >= kRowAhead) vm_wait<kRowAhead * kStepLoads>();
+                else if (since == 3) vm_wait<3 * kStepLoads>();
+                else if (since == 2) vm_wait<2 * kStepLoads>();
+                else vm_wait<1 * kStepLoads>();
+                read_w();
+                kcur = k;
+                const int kn = nextk[k];
+                if (kn >= 0) {
+                    dma_w(kn);
+                    since = 0;
+                }
             }
+            // (c) this chunk: read the output-row slices, multiply, add, write back
+            const int o = (TR ? ps[u].x : ps[u].y) - (int)row0;
+            const bool live = ((pv >> u) & 1u) && (uint32_t)o < (uint32_t)rows;
+            float4* arow = (float4*)(acc + (live ? o : T) * ACS) + nb0 * 4 + g;
+            float4 av[NBW];
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) av[nb] = arow[nb * 4];
+            f32x4 d[NBW];
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) d[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kc = 0; kc < KCH; ++kc)
+#pragma unroll
+                for (int nb = 0; nb < NBW; ++nb)
+                    d[nb] = mfma16x16x32<DT>(wc[kc][nb], __builtin_bit_cast(uint4, rs[sr][kc]), d[nb]);
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb)
+                arow[nb * 4] = make_float4(av[nb].x + d[nb][0], av[nb].y + d[nb][1], av[nb].z + d[nb][2],
+                                           av[nb].w + d[nb][3]);
+            // (b) refill the consumed slots: rows of chunk c + kRowAhead, pair of chunk c + kPairAhead
+            const int ur = (u + kRowAhead) % kPairAhead;
+            load_rows(ps[ur], (pv >> ur) & 1u, rs[sr]);
+            const bool pnv = load_pair(c + kPairAhead, ps[u]);
+            pv = (pv & ~(1u << u)) | (pnv ? (1u << u) : 0u);
+            ++since;
         }
     }
-    // epilogue: lane holds rows 4g..4g+3 of each 16-row block, column nb*16 + r16
+    vm_wait<0>();  // no weight copy may still target LDS past this point
+    __syncthreads();
+
+    // epilogue: 8 channels per item, one 16-byte store each
+    const int c8n = Cout / 8;
+    for (int e = tid; e < rows * c8n; e += nthr) {
+        const int r = e / c8n, c8 = e - r * c8n;
+        const float4 a0 = *(const float4*)(acc + (size_t)r * ACS + 8 * c8);
+        const float4 a1 = *(const float4*)(acc + (size_t)r * ACS + 8 * c8 + 4);
+        float v[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        uint32_t w[4];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        const int col = nb * 16 + r16;
-        const float sc = scale ? scale[col] : 1.f;
-        const float sh = shift ? shift[col] : 0.f;
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int64_t row = (b0 + r) * kRowsPerTile + 4 * g + e;
-                if (row >= m) continue;
-                float v = acc[r][nb][e] * sc + sh;
-                if (relu) v = fmaxf(v, 0.f);
-                out[row * Cout + col] = to16<DT>(v);
-            }
+        for (int j = 0; j < 8; ++j) {
+            const int col = 8 * c8 + j;
+            float y = v[j] * (scale ? scale[col] : 1.f) + (shift ? shift[col] : 0.f);
+            if (relu) y = fmaxf(y, 0.f);
+            v[j] = y;
         }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w[j] = (uint32_t)to16<DT>(v[2 * j]) | ((uint32_t)to16<DT>(v[2 * j + 1]) << 16);
+        *(uint4*)(out + (row0 + r) * Cout + 8 * c8) = make_uint4(w[0], w[1], w[2], w[3]);
     }
 }
 
 // ---------------------------------------------------------------------------
-// vector-ALU conv (f32, or shapes the MFMA kernel does not take)
+// vector-ALU tile kernel (f32, or shapes the MFMA kernel does not take):
+// 64 output channels per workgroup (grid.y), 4 pair lanes; LDS accumulator
+// [T][64]; a barrier between offsets keeps the updates of one row ordered.
 // ---------------------------------------------------------------------------
 template <int DT>
-__global__ void k_conv_generic(ConvPlan p, const void* in, int Cin, int64_t in_rows, const void* W, const float* scale,
-                               const float* shift, int relu, void* out, int Cout) {
+__global__ __launch_bounds__(256) void k_conv_tile_valu(ConvPlan p, const void* in, int Cin, int64_t in_rows,
+                                                        const int32_t* pairs, int64_t pair_bound, int transposed,
+                                                        const void* W,
+                                                        const float* scale, const float* shift, int relu, void* out,
+                                                        int Cout) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    float* acc = (float*)smem;
+    const int T = p.tile_rows, K3 = p.K3;
+    const int64_t t = blockIdx.x;
     const int64_t m = clamp_rows(p.m_out_dev, p.m_cap);
-    int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    int64_t j = t / Cout;
-    int co = (int)(t - j * Cout);
-    if (j >= m) return;
-    const int64_t b = j / kRowsPerTile;
-    const uint32_t U = p.umask[b], base = p.ucnt[b];
-    uint32_t bits = p.mask[j];
-    float acc = 0.f;
-    while (bits) {
-        const int k = __builtin_ctz(bits);
-        bits &= bits - 1;
-        const uint32_t slot = (uint32_t)__popc(U & ((1u << k) - 1u));
-        const int32_t i = p.table[((int64_t)base + slot) * kRowsPerTile + (j % kRowsPerTile)];
-        if (i < 0 || i >= in_rows) continue;
-        for (int ci = 0; ci < Cin; ++ci)
-            acc += ld_feat<DT>(in, (int64_t)i * Cin + ci) * ld_feat<DT>(W, ((int64_t)k * Cin + ci) * Cout + co);
+    const int64_t nt = (m + T - 1) / T;
+    if (t >= nt) return;
+    const int64_t row0 = t * T;
+    const int rows = (int)((m - row0) < T ? (m - row0) : T);
+    const int cl = threadIdx.x & 63, rl = threadIdx.x >> 6;
+    const int col = blockIdx.y * 64 + cl;
+    const bool cok = col < Cout;
+    for (int e = threadIdx.x; e < T * 64; e += blockDim.x) acc[e] = 0.f;
+    __syncthreads();
+    const int isel = transposed ? 1 : 0;
+    const int64_t bs = p.ntile_cap + 1;
+    for (int k = 0; k < K3; ++k) {
+        int64_t lo = p.bnd[k * bs + t], hi = p.bnd[k * bs + t + 1];
+        lo = lo < 0 ? 0 : (lo > pair_bound ? pair_bound : lo);
+        hi = hi < lo ? lo : (hi > pair_bound ? pair_bound : hi);
+        for (int64_t pi = lo + rl; pi < hi; pi += 4) {
+            const int32_t i = pairs[2 * pi + isel];
+            const int64_t o = (int64_t)pairs[2 * pi + 1 - isel] - row0;
+            if (!cok || o < 0 || o >= rows || i < 0 || i >= in_rows) continue;
+            float s = 0.f;
+            for (int ci = 0; ci < Cin; ++ci)
+                s += ld_feat<DT>(in, (int64_t)i * Cin + ci) * ld_feat<DT>(W, ((int64_t)k * Cin + ci) * Cout + col);
+            acc[o * 64 + cl] += s;
+        }
+        __syncthreads();
     }
-    float v = acc * (scale ? scale[co] : 1.f) + (shift ? shift[co] : 0.f);
-    if (relu) v = fmaxf(v, 0.f);
-    st_feat<DT>(out, j * Cout + co, v);
+    if (!cok) return;
+    const float sc = scale ? scale[col] : 1.f, sh = shift ? shift[col] : 0.f;
+    for (int r = rl; r < rows; r += 4) {
+        float y = acc[r * 64 + cl] * sc + sh;
+        if (relu) y = fmaxf(y, 0.f);
+        st_feat<DT>(out, (row0 + r) * Cout + col, y);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// host dispatch
+// ---------------------------------------------------------------------------
+static int conv_kch(int Cin) {
+    const int k = (Cin + 31) / 32;
+    return k <= 4 ? k : (k <= 6 ? 6 : 8);
+}
+
+// channel blocks per wave of the tile kernel: the largest of 4, 3, 2, 1 that
+// divides Cout / 16 while the wave's weight fragments stay within 12 registers
+// of 16 bytes
+static int conv_nbw(int KCH, int NB) {
+    for (int w = 4; w > 1; --w)
+        if (NB % w == 0 && KCH * w <= 12 && KCH < 6 && NB / w <= 8) return w;
+    return 1;
 }
 
 bool conv_mfma_supported(int Cin, int Cout, int dt) {
-    if (dt == SPV_F32 || Cin % 8 != 0 || Cout % 16 != 0) return false;
-    int KCH = (Cin + 31) / 32, NB = Cout / 16;
-    return KCH <= 8 && (NB == 1 || NB == 2 || NB == 4 || NB == 6 || NB == 8 || NB == 16);
+    if (dt == SPV_F32 || Cin % 8 != 0 || Cout % 16 != 0 || Cin > 256 || Cout > 256) return false;
+    const int NB = Cout / 16;
+    return NB / conv_nbw(conv_kch(Cin), NB) <= 8;  // at most 8 waves per workgroup
 }
 
-template <int DT, int KCH, int NB>
-static void launch_mfma_nb(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows,
-                           const void* wpack, const float* scale, const float* shift, int relu, void* out, int Cout) {
-    constexpr int R = (NB <= 2) ? 8 : (NB <= 6 ? 4 : (NB <= 8 ? 3 : 2));
-    int64_t nblk = (p.m_cap + kRowsPerTile - 1) / kRowsPerTile;
-    int64_t waves = (nblk + R - 1) / R;
-    k_conv_mfma<DT, KCH, NB, R><<<blocks_for(waves, 4), 256, 0, s>>>(p, (const uint16_t*)in, Cin, in_rows,
-                                                                   (const uint4*)wpack, scale, shift, relu,
-                                                                   (uint16_t*)out, Cout);
+static int conv_tile_rows(int Cin, int Cout, int dt) {
+    if (!conv_mfma_supported(Cin, Cout, dt)) return 128;
+    const int KCH = conv_kch(Cin), NB = Cout / 16, NBW = conv_nbw(KCH, NB), NW = NB / NBW;
+    // the largest tile with which two workgroups share a compute unit's 160 KB of LDS
+    for (int T = 128; T > 16; T >>= 1)
+        if (ConvTileSmem::bytes(T, Cout, kMaxK3, KCH, NBW, NW) <= 80 * 1024) return T;
+    return 16;
+}
+
+template <int DT, int KCH, int NBW>
+static void launch_tile3(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows,
+                         const int32_t* pairs, int64_t pair_bound, int transposed, const void* wpack,
+                         const float* scale, const float* shift, int relu, void* out, int Cout) {
+    const int NB = Cout / 16, NW = NB / NBW;
+    const size_t lds = ConvTileSmem::bytes(p.tile_rows, Cout, p.K3, KCH, NBW, NW);
+    const unsigned grid = (unsigned)(p.ntile_cap > 0 ? p.ntile_cap : 1);
+    // opt in to more than 64 KB of dynamic LDS (once per instantiation)
+    static const bool lds_ok = hipFuncSetAttribute((const void*)k_conv_tile<DT, KCH, NBW, 0>,
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                   160 * 1024) == hipSuccess &&
+                               hipFuncSetAttribute((const void*)k_conv_tile<DT, KCH, NBW, 1>,
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                   160 * 1024) == hipSuccess;
+    (void)lds_ok;
+    if (transposed)
+        k_conv_tile<DT, KCH, NBW, 1><<<grid, 64 * NW, lds, s>>>(p, (const uint16_t*)in, Cin, in_rows, pairs,
+                                                                pair_bound, (const uint4*)wpack, NB, scale, shift,
+                                                                relu, (uint16_t*)out, Cout);
+    else
+        k_conv_tile<DT, KCH, NBW, 0><<<grid, 64 * NW, lds, s>>>(p, (const uint16_t*)in, Cin, in_rows, pairs,
+                                                                pair_bound, (const uint4*)wpack, NB, scale, shift,
+                                                                relu, (uint16_t*)out, Cout);
 }
 
 template <int DT, int KCH>
-static void launch_mfma_kch(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows,
-                            const void* wpack, const float* scale, const float* shift, int relu, void* out, int Cout) {
-    switch (Cout / 16) {
-        case 1: launch_mfma_nb<DT, KCH, 1>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
-        case 2: launch_mfma_nb<DT, KCH, 2>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
-        case 4: launch_mfma_nb<DT, KCH, 4>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
-        case 6: launch_mfma_nb<DT, KCH, 6>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
-        case 8: launch_mfma_nb<DT, KCH, 8>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
-        case 16: launch_mfma_nb<DT, KCH, 16>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
+static void launch_tile_kch(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows,
+                            const int32_t* pairs, int64_t pair_bound, int transposed, const void* wpack,
+                            const float* scale, const float* shift, int relu, void* out, int Cout) {
+    switch (conv_nbw(KCH, Cout / 16)) {
+#define SPV_NBW_CASE(W)                                                                                        \
+    case W:                                                                                                    \
+        if constexpr (KCH * W <= 12 && (KCH < 6 || W == 1))                                                   \
+            launch_tile3<DT, KCH, W>(s, p, in, Cin, in_rows, pairs, pair_bound, transposed, wpack, scale, shift, \
+                                     relu, out, Cout);                                                         \
+        break;
+        SPV_NBW_CASE(1)
+        SPV_NBW_CASE(2)
+        SPV_NBW_CASE(3)
+        SPV_NBW_CASE(4)
+#undef SPV_NBW_CASE
     }
 }
 
 template <int DT>
-static void launch_mfma(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows, const void* wpack,
+static void launch_tile(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows,
+                        const int32_t* pairs, int64_t pair_bound, int transposed, const void* wpack,
                         const float* scale, const float* shift, int relu, void* out, int Cout) {
-    switch ((Cin + 31) / 32) {
-        case 1: launch_mfma_kch<DT, 1>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
-        case 2: launch_mfma_kch<DT, 2>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
-        case 3: launch_mfma_kch<DT, 3>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
-        case 4: launch_mfma_kch<DT, 4>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
-        case 5: launch_mfma_kch<DT, 5>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
-        case 6: launch_mfma_kch<DT, 6>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
-        case 7: launch_mfma_kch<DT, 7>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
-        case 8: launch_mfma_kch<DT, 8>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout); break;
+    switch (conv_kch(Cin)) {
+#define SPV_KCH_CASE(K)                                                                                       \
+    case K:                                                                                                   \
+        launch_tile_kch<DT, K>(s, p, in, Cin, in_rows, pairs, pair_bound, transposed, wpack, scale, shift, relu, \
+                               out, Cout);                                                                    \
+        break;
+        SPV_KCH_CASE(1)
+        SPV_KCH_CASE(2)
+        SPV_KCH_CASE(3)
+        SPV_KCH_CASE(4)
+        SPV_KCH_CASE(6)
+        SPV_KCH_CASE(8)
+#undef SPV_KCH_CASE
     }
 }
 
 void launch_conv_pack(hipStream_t s, int K3, const void* W, void* wpack, int Cin, int Cout, int dt) {
     if (!conv_mfma_supported(Cin, Cout, dt)) return;
-    int KCH = (Cin + 31) / 32, NB = Cout / 16;
+    int KCH = conv_kch(Cin), NB = Cout / 16;
     int64_t tot = (int64_t)K3 * KCH * NB * 64;
     k_pack_w<<<blocks_for(tot, 256), 256, 0, s>>>((const uint16_t*)W, K3, Cin, Cout, KCH, NB, (uint4*)wpack);
 }
 
-void launch_conv_run(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows, const void* W,
-                     const void* wpack, const float* scale, const float* shift, int relu, void* out, int Cout,
-                     int dt) {
-    if (conv_mfma_supported(Cin, Cout, dt)) {
-        if (dt == SPV_BF16) launch_mfma<SPV_BF16>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout);
-        else launch_mfma<SPV_F16>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out, Cout);
+// the MFMA kernel addresses the input rows and the pair list with 32-bit buffer offsets
+static bool conv_fits_buffers(int64_t in_rows, int Cin, int64_t pair_bound) {
+    return in_rows * (int64_t)Cin * 2 <= (int64_t)0xFFFFE000 && pair_bound * 8 <= (int64_t)0xFFFFE000;
+}
+
+void launch_conv_run(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows, const int32_t* pairs,
+                     int64_t pair_bound, int transposed, const void* W, const void* wpack, const float* scale,
+                     const float* shift, int relu, void* out, int Cout, int dt) {
+    if (p.use_union && conv_fits_buffers(in_rows, Cin, 0)) {
+        launch_conv_union(s, p, in, Cin, in_rows, Cout, wpack, scale, shift, relu, out, dt);
         return;
     }
-    int64_t threads = p.m_cap * Cout;
-    unsigned g = blocks_for(threads, 256);
-    if (dt == SPV_F32) k_conv_generic<SPV_F32><<<g, 256, 0, s>>>(p, in, Cin, in_rows, W, scale, shift, relu, out, Cout);
+    if (!p.use_union && conv_mfma_supported(Cin, Cout, dt) && conv_fits_buffers(in_rows, Cin, pair_bound)) {
+        if (dt == SPV_BF16)
+            launch_tile<SPV_BF16>(s, p, in, Cin, in_rows, pairs, pair_bound, transposed, wpack, scale, shift, relu,
+                                  out, Cout);
+        else
+            launch_tile<SPV_F16>(s, p, in, Cin, in_rows, pairs, pair_bound, transposed, wpack, scale, shift, relu,
+                                 out, Cout);
+        return;
+    }
+    dim3 grid((unsigned)(p.ntile_cap > 0 ? p.ntile_cap : 1), (unsigned)((Cout + 63) / 64));
+    const size_t lds = (size_t)p.tile_rows * 64 * 4;
+    if (dt == SPV_F32)
+        k_conv_tile_valu<SPV_F32><<<grid, 256, lds, s>>>(p, in, Cin, in_rows, pairs, pair_bound, transposed, W, scale,
+                                                         shift, relu, out, Cout);
     else if (dt == SPV_BF16)
-        k_conv_generic<SPV_BF16><<<g, 256, 0, s>>>(p, in, Cin, in_rows, W, scale, shift, relu, out, Cout);
-    else k_conv_generic<SPV_F16><<<g, 256, 0, s>>>(p, in, Cin, in_rows, W, scale, shift, relu, out, Cout);
+        k_conv_tile_valu<SPV_BF16><<<grid, 256, lds, s>>>(p, in, Cin, in_rows, pairs, pair_bound, transposed, W,
+                                                          scale, shift, relu, out, Cout);
+    else
+        k_conv_tile_valu<SPV_F16><<<grid, 256, lds, s>>>(p, in, Cin, in_rows, pairs, pair_bound, transposed, W,
+                                                         scale, shift, relu, out, Cout);
 }
 
 }  // namespace spv

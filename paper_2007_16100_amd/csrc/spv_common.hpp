@@ -39,6 +39,7 @@ enum : uint32_t {
     kFlagCapacity = 1u << 2,
     kFlagDuplicate = 1u << 3,  // repeated coordinate where distinct ones are required
     kFlagTableFull = 1u << 4,
+    kFlagUnsorted = 1u << 5,   // a kernel-map offset group not sorted by output row
 };
 
 // Workspace header: first 256 bytes of every workspace.

@@ -127,25 +127,37 @@ void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const in
                        int64_t* m_out_dev, int32_t* off, int32_t* pairs, int64_t pair_cap);
 
 // --- sparse conv (conv.hip) ----------------------------------------------------
+// Two MFMA kernels share one plan.
+//  * 3x3x3 maps (K3 = 27): output-stationary blocks of 16 rows with register
+//    accumulators; the plan builds a dense neighbour table nbr[j][k] = i + 1
+//    (0 = no pair) from the kernel map.
+//  * other maps (K3 = 8) and wide shapes: output rows in tiles of `tile_rows`
+//    with an LDS accumulator; the plan records, per offset k and tile t, the
+//    first pair of offset k whose output row lies in tile t or later (the
+//    pairs of one offset are sorted by output row, so those of (tile, offset)
+//    form the range [bnd[k][t], bnd[k][t+1])).
 struct ConvPlan {
     int64_t m_cap;      // output row capacity
     int K3;
-    uint32_t* mask;     // [m_cap] offsets present per output row
-    uint32_t* umask;    // [nblk16] union of the offsets of each 16-row block
-    uint32_t* ucnt;     // [nblk16 + 1] -> exclusive prefix of popcount(umask)
-    int32_t* table;     // [K3 * nblk16 * 16] input row per (block, present offset, row)
+    int use_union;      // 1: neighbour-table kernel, 0: tile kernel (or vector ALU)
+    int tile_rows;      // output rows per tile (power of two)
+    int64_t ntile_cap;  // ceil(m_cap / tile_rows)
+    int32_t* bnd;       // [K3][ntile_cap + 1]
+    int32_t* nbr;       // [m_cap][K3] when use_union
     const int64_t* m_out_dev;
+    Header* h;          // status word (unsorted or out-of-range pairs)
 };
-void plan_conv_ws(Arena& a, ConvPlan& p, int64_t m_out_cap, int K3);
+void plan_conv_ws(Arena& a, ConvPlan& p, int64_t m_out_cap, int K3, int Cin, int Cout, int dt);
 void launch_conv_plan(hipStream_t s, const ConvPlan& p, const int32_t* off, const int32_t* pairs, int K3,
-                      int transposed, int64_t pair_bound);
+                      int transposed, int64_t pair_bound, int64_t in_rows);
 bool conv_mfma_supported(int Cin, int Cout, int dt);
 void* plan_wpack_ws(Arena& a, int K3, int Cin, int Cout);
-// pack W [K3][Cin][Cout] into MFMA B fragments (no-op when the vector-ALU path runs)
+// pack W [K3][Cin][Cout] into MFMA operand fragments (no-op when the vector-ALU path runs)
 void launch_conv_pack(hipStream_t s, int K3, const void* W, void* wpack, int Cin, int Cout, int dt);
 // the convolution itself (one kernel); wpack must have been packed from W
-void launch_conv_run(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows, const void* W,
-                     const void* wpack, const float* scale, const float* shift, int relu, void* out, int Cout, int dt);
+void launch_conv_run(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows, const int32_t* pairs,
+                     int64_t pair_bound, int transposed, const void* W, const void* wpack, const float* scale,
+                     const float* shift, int relu, void* out, int Cout, int dt);
 
 // --- devoxelize (devox.hip) ----------------------------------------------------
 struct DevoxArgs {
