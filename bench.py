@@ -30,6 +30,40 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBPS = 8000.0      # MI355X HBM3E
 
+# Sources of the dominant kernel (the 3x3x3 neighbour-table conv); the committed
+# FETCH_SIZE / WRITE_SIZE summary applies only while their hash is unchanged.
+CONV_SOURCES = ("paper_2007_16100_amd/csrc/conv_union.hip", "paper_2007_16100_amd/csrc/conv_common.hpp")
+CONV_TRAFFIC = "profiles/conv_union_c96_traffic.txt"
+
+
+def conv_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in CONV_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def conv_traffic_bytes():
+    """HBM bytes per conv launch from the committed rocprofv3 counter summary, each
+    counter scaled by what it reads for a plain copy of known size; None when the
+    summary is missing or the kernel source changed since it was taken."""
+    path = os.path.join(ROOT, CONV_TRAFFIC)
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha256") != conv_source_hash():
+        return None
+    cb = float(kv["copy_bytes"])
+    fetch = float(kv["fetch_kib_per_dispatch"]) * cb / float(kv["copy_fetch_kib"])
+    write = float(kv["write_kib_per_dispatch"]) * cb / float(kv["copy_write_kib"])
+    return fetch + write
+
 
 class HipEvents:
     """hipEvent_t handles through the HIP runtime (recorded by libspv on the bench stream)."""
@@ -163,7 +197,7 @@ def main():
     else:
         roof = {"bound": "mfma", "achieved": conv_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": conv_tflops / PEAK_BF16_TFLOPS}
-    roof.update({"traffic": None, "kernel": "k_conv_mfma (3x3x3 submanifold, 96->96, bf16)",
+    roof.update({"traffic": conv_traffic_bytes(), "kernel": "k_conv_union (3x3x3 submanifold, 96->96, bf16)",
                  "alg_bytes_per_launch": B_conv, "eff_flops_per_launch": F_conv,
                  "mfma_frac_eff": conv_tflops / PEAK_BF16_TFLOPS, "avg_launch_us": conv_avg_ms * 1e3})
 

@@ -1,8 +1,19 @@
 // conv_union.hip -- sparse convolution on a 3x3x3 kernel map (Sec. 3.2 / 3.3)
 // with register accumulators: the neighbour-table kernel described in conv.hip.
+#include <type_traits>
+
 #include "conv_common.hpp"
 
 namespace spv {
+
+// f(integral_constant<int, i>) for i = B .. E-1, each i a compile-time constant
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
 
 // ---------------------------------------------------------------------------
 // neighbour-table kernel (3x3x3 maps)
@@ -12,25 +23,40 @@ namespace spv {
 // fragments: lane (r16, g) holds output channels nb*16 + 4g .. 4g+3 of row r16,
 // which is also the order in which they are stored.
 //
-// Step k of the (fully unrolled) offset loop:
-//   wait for the wave's own copies of W[k] and for the barrier (every wave has
-//   copied its share), read the W[k] fragments from LDS buffer k % 3, then
-//   issue the copies of W[k+2] into buffer (k+2) % 3, the neighbour indices of
-//   offset k+2 and the gathered rows of offset k+1, and finally multiply the
-//   rows of offset k.  Every load thus has one or two steps of matrix work to
-//   arrive in, and the compiler's own waits stay exact because every load it
-//   waits for is one it issued (the LDS copies use the compiler's builtin).
+// Step k of the fully unrolled offset loop
+//   (1) writes to LDS buffer (k+2) % 4 this wave's share of W[k+2], loaded
+//       into registers during step k-1, and waits for its LDS writes;
+//   (2) barrier: every wave has written W[k+2] and finished reading the buffer
+//       about to be reused;
+//   (3) loads its share of W[k+3] into registers, the neighbour indices of
+//       offset k+3 and the gathered rows of offset k+2;
+//   (4) multiplies the rows gathered for offset k by W[k], read from LDS buffer
+//       k % 4 one 32-channel slab at a time; blocks without a neighbour at
+//       offset k skip it.
+// Every load has one or two steps of matrix work to arrive in.  All loads are
+// ordinary vector-memory loads the compiler sees, so its waits (which count
+// outstanding loads in issue order) stay exact: with a global->LDS copy in
+// flight it would instead wait for every load at the next use of any of them.
 constexpr int kUnionWaves = 4;
+constexpr int kUK3 = 27;
+constexpr int kWAhead = 3;  // weight loads: steps ahead (ring of kWAhead + 1 LDS buffers)
+constexpr int kNAhead = 3;  // neighbour indices: steps ahead
+constexpr int kRAhead = 1;  // gathered rows: steps ahead
 
 template <int DT, int KCH, int NB, int RB, int FULL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_conv_union(
     const int32_t* __restrict__ nbr, const int64_t* __restrict__ m_out_dev, int64_t m_cap,
     const uint16_t* __restrict__ in, int Cin, int64_t in_rows, const uint4* __restrict__ wpack,
     const float* __restrict__ scale, const float* __restrict__ shift, int relu, uint16_t* __restrict__ out) {
-    constexpr int K3 = 27;
+    constexpr int K3 = kUK3;
     constexpr int FR = KCH * NB;  // 1 KB weight fragments per offset
     constexpr int Cout = NB * 16;
-    __shared__ __align__(16) uint4 wbuf[3][FR * 64];
+    constexpr int NF = (FR + kUnionWaves - 1) / kUnionWaves;  // fragments per wave and offset
+    __shared__ __align__(16) uint4 wb0[FR * 64];
+    __shared__ __align__(16) uint4 wb1[FR * 64];
+    __shared__ __align__(16) uint4 wb2[FR * 64];
+    __shared__ __align__(16) uint4 wb3[FR * 64];
+    auto wbuf = [&](int i) __attribute__((always_inline)) -> uint4* { return i == 0 ? wb0 : (i == 1 ? wb1 : (i == 2 ? wb2 : wb3)); };
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -59,6 +85,55 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
         nboff[b] = row < m ? (uint32_t)(row * K3 * 4) : kOutOfRange;
     }
 
+    // this wave's share of a weight buffer: fragments wave, wave + 4, ...; every
+    // wave handles the same number (surplus ones repeat the last fragment: the
+    // same bytes to the same place)
+    auto frag_of = [&](int j) __attribute__((always_inline)) { return j * kUnionWaves + wave < FR ? j * kUnionWaves + wave : FR - 1; };
+    // (native vector types: HIP's uint4 struct is copied with memcpy, which keeps
+    // an array of them out of registers)
+    const i32x4* wsrc = (const i32x4*)wpack;
+    auto load_w = [&](int k, i32x4 (&wt)[NF]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < NF; ++j) wt[j] = wsrc[((int64_t)k * FR + frag_of(j)) * 64 + lane];
+    };
+    auto store_w = [&](uint4* dst, const i32x4 (&wt)[NF]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < NF; ++j) ((i32x4*)dst)[frag_of(j) * 64 + lane] = wt[j];
+    };
+    auto load_nbr = [&](int k, int (&dst)[RB]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int b = 0; b < RB; ++b)
+            dst[b] = __builtin_amdgcn_raw_buffer_load_b32(nb_rs, nboff[b] + (uint32_t)k * 4u, 0, 0);
+    };
+    auto load_rows = [&](const int (&nb1)[RB], i32x4 (&dst)[RB][KCH]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int b = 0; b < RB; ++b) {
+            const uint32_t i = (uint32_t)(nb1[b] - 1);  // stored as row + 1; 0 = absent
+            const uint32_t base = i < in_rows32 ? i * row_bytes + (uint32_t)g * 16u : kOutOfRange;
+#pragma unroll
+            for (int kc = 0; kc < KCH; ++kc) {
+                uint32_t o = base + kc * 64;
+                if (!FULL && kc * 4 + g >= qin) o = kOutOfRange;
+                dst[b][kc] = __builtin_amdgcn_raw_buffer_load_b128(in_rs, o, 0, 0);
+            }
+        }
+    };
+
+    // prologue: W[0], W[1] into LDS, W[2] in registers, neighbour indices, rows
+    i32x4 wtmp[NF];  // this wave's share of the next weight buffer, between load and LDS write
+#pragma unroll
+    for (int j = 0; j < kWAhead - 1; ++j) {
+        load_w(j, wtmp);
+        store_w(wbuf(j), wtmp);
+    }
+    load_w(kWAhead - 1, wtmp);
+    int ns[kNAhead + 1][RB];         // neighbour indices of offset j in slot j % (kNAhead + 1)
+    i32x4 rs[kRAhead + 1][RB][KCH];  // gathered rows of offset j in slot j % (kRAhead + 1)
+#pragma unroll
+    for (int j = 0; j < kNAhead; ++j) load_nbr(j, ns[j]);
+#pragma unroll
+    for (int j = 0; j < kRAhead; ++j) load_rows(ns[j], rs[j]);
+
     // offsets present in each block (union over its 16 rows), wave-uniform
     uint32_t umask[RB];
 #pragma unroll
@@ -76,78 +151,50 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
         umask[b] = __builtin_amdgcn_readfirstlane(bits);
     }
 
-    // this wave's share of the weight copies: fragments wave, wave + 4, ...
-    auto copy_w = [&](int k, int buf) {
-#pragma unroll
-        for (int f = 0; f < FR; f += kUnionWaves) {
-            if (f + wave < FR)
-                __builtin_amdgcn_global_load_lds(
-                    (const void*)(wpack + ((int64_t)k * FR + f + wave) * 64 + lane),
-                    (__attribute__((address_space(3))) void*)&wbuf[buf][(f + wave) * 64], 16, 0, 0);
-        }
-    };
-    auto load_nbr = [&](int k, int (&dst)[RB]) {
-#pragma unroll
-        for (int b = 0; b < RB; ++b)
-            dst[b] = __builtin_amdgcn_raw_buffer_load_b32(nb_rs, nboff[b] + (uint32_t)k * 4u, 0, 0);
-    };
-    auto load_rows = [&](const int (&nb1)[RB], i32x4 (&dst)[RB][KCH]) {
-#pragma unroll
-        for (int b = 0; b < RB; ++b) {
-            const uint32_t i = (uint32_t)(nb1[b] - 1);  // stored as row + 1; 0 = absent
-            const uint32_t base = i < in_rows32 ? i * row_bytes + (uint32_t)g * 16u : kOutOfRange;
-#pragma unroll
-            for (int kc = 0; kc < KCH; ++kc) {
-                uint32_t o = base + kc * 64;
-                if (!FULL && kc * 4 + g >= qin) o = kOutOfRange;
-                dst[b][kc] = __builtin_amdgcn_raw_buffer_load_b128(in_rs, o, 0, 0);
-            }
-        }
-    };
-
     f32x4 acc[RB][NB];
 #pragma unroll
     for (int b = 0; b < RB; ++b)
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) acc[b][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    int ns[3][RB];        // neighbour indices of offsets k, k+1, k+2 (slot k % 3)
-    i32x4 rs[2][RB][KCH]; // gathered rows of offsets k, k+1 (slot k % 2)
-    copy_w(0, 0);
-    copy_w(1, 1);
-    load_nbr(0, ns[0]);
-    load_nbr(1, ns[1]);
-    load_rows(ns[0], rs[0]);
-
+    static_for<0, K3>([&](auto kk) __attribute__((always_inline)) {
+        constexpr int k = decltype(kk)::value;
+        // (1) this wave's share of W[k+2] into LDS
+        if constexpr (k + kWAhead - 1 < K3) store_w(wbuf((k + kWAhead - 1) % (kWAhead + 1)), wtmp);
+        // (2) a plain barrier after the wave's own LDS writes (a __syncthreads
+        // fence would also wait for every gather in flight)
+        lds_wait();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        // (3) loads of later steps
+        if constexpr (k + kWAhead < K3) load_w(k + kWAhead, wtmp);
+        if constexpr (k + kNAhead < K3) load_nbr(k + kNAhead, ns[(k + kNAhead) % (kNAhead + 1)]);
+        if constexpr (k + kRAhead < K3)
+            load_rows(ns[(k + kRAhead) % (kNAhead + 1)], rs[(k + kRAhead) % (kRAhead + 1)]);
+        // (4) multiply offset k, one 32-channel slab of W[k] at a time
+        const uint4* wk = wbuf(k % (kWAhead + 1));
+        uint32_t present = 0;
 #pragma unroll
-    for (int k = 0; k < K3; ++k) {
-        // every wave's copies of W[k] have landed: at most the loads of the last
-        // step's neighbour indices and rows may still be outstanding
-        vm_wait<RB + KCH * RB>();
-        __syncthreads();
-        uint4 wf[KCH][NB];
+        for (int b = 0; b < RB; ++b) present |= ((umask[b] >> k) & 1u) << b;
+        if (present) {
 #pragma unroll
-        for (int kc = 0; kc < KCH; ++kc)
+            for (int kc = 0; kc < KCH; ++kc) {
+                i32x4 wf[NB];
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) wf[kc][nb] = wbuf[k % 3][(kc * NB + nb) * 64 + lane];
-        asm volatile("" ::: "memory");  // the copies below stay after these reads
-        if (k + 2 < K3) {
-            copy_w(k + 2, (k + 2) % 3);
-            load_nbr(k + 2, ns[(k + 2) % 3]);
-        }
-        if (k + 1 < K3) load_rows(ns[(k + 1) % 3], rs[(k + 1) % 2]);
+                for (int nb = 0; nb < NB; ++nb) wf[nb] = ((const i32x4*)wk)[(kc * NB + nb) * 64 + lane];
 #pragma unroll
-        for (int b = 0; b < RB; ++b) {
-            if ((umask[b] >> k) & 1u) {
+                for (int b = 0; b < RB; ++b) {
+                    if ((present >> b) & 1u) {
 #pragma unroll
-                for (int kc = 0; kc < KCH; ++kc)
-#pragma unroll
-                    for (int nb = 0; nb < NB; ++nb)
-                        acc[b][nb] = mfma16x16x32<DT>(wf[kc][nb], __builtin_bit_cast(uint4, rs[k % 2][b][kc]),
-                                                      acc[b][nb]);
+                        for (int nb = 0; nb < NB; ++nb)
+                            acc[b][nb] = mfma16x16x32<DT>(__builtin_bit_cast(uint4, wf[nb]),
+                                                          __builtin_bit_cast(uint4, rs[k % (kRAhead + 1)][b][kc]),
+                                                          acc[b][nb]);
+                    }
+                }
             }
         }
-    }
+    });
 
     // epilogue: act(scale * acc + shift), 4 channels (8 bytes) per store
     float sc[NB][4], sh[NB][4];
@@ -178,72 +225,49 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
 }
 
 // blocks of 16 rows per wave of the neighbour-table kernel: accumulators
-// (RB*NB), weight fragments (KCH*NB) and two stages of gathered rows
-// (2*RB*KCH), in 16-byte registers, within ~56 of them (two waves per SIMD)
+// (RB*NB), one weight slab (NB) and three stages of gathered rows (3*RB*KCH),
+// in 16-byte registers, within ~52 of them (two waves per SIMD)
 constexpr int union_rb(int KCH, int NB) {
     for (int rb = 4; rb > 1; --rb)
-        if (rb * NB + KCH * NB + 2 * rb * KCH <= 56) return rb;
+        if (rb * NB + NB + (kRAhead + 1) * rb * KCH <= 52) return rb;
     return 1;
 }
 
+// instantiated for square layers C -> C with C in {32, 64, 96, 128} (the widths
+// of the blocks and networks built here); other shapes use the tile kernel
 bool union_supported(int K3, int Cin, int Cout, int dt) {
-    if (K3 != 27 || dt == SPV_F32 || Cin % 8 != 0 || Cout % 16 != 0 || Cin > 128) return false;
-    const int NB = Cout / 16, KCH = (Cin + 31) / 32;
-    if (!(NB == 1 || NB == 2 || NB == 4 || NB == 6 || NB == 8)) return false;
-    return KCH * NB <= 24 && KCH * NB + NB + 2 * KCH <= 56;
-}
-
-template <int DT, int KCH, int NB, int FULL>
-static void launch_union3(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows,
-                          const void* wpack, const float* scale, const float* shift, int relu, void* out) {
-    constexpr int RB = union_rb(KCH, NB);
-    constexpr int64_t rows_wg = (int64_t)kUnionWaves * RB * 16;
-    const unsigned grid = (unsigned)((p.m_cap + rows_wg - 1) / rows_wg);
-    k_conv_union<DT, KCH, NB, RB, FULL><<<grid, 64 * kUnionWaves, 0, s>>>(
-        p.nbr, p.m_out_dev, p.m_cap, (const uint16_t*)in, Cin, in_rows, (const uint4*)wpack, scale, shift, relu,
-        (uint16_t*)out);
-}
-
-template <int DT, int KCH, int NB>
-static void launch_union_nb(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows,
-                            const void* wpack, const float* scale, const float* shift, int relu, void* out) {
-    if (Cin == KCH * 32) launch_union3<DT, KCH, NB, 1>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out);
-    else launch_union3<DT, KCH, NB, 0>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out);
+    if (K3 != 27 || dt == SPV_F32 || Cin != Cout) return false;
+    return Cin == 32 || Cin == 64 || Cin == 96 || Cin == 128;
 }
 
 template <int DT, int KCH>
-static void launch_union_kch(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows, int Cout,
-                             const void* wpack, const float* scale, const float* shift, int relu, void* out) {
-    switch (Cout / 16) {
-#define SPV_NB_CASE(N)                                                                             \
-    case N:                                                                                        \
-        if constexpr (KCH * N <= 24 && KCH * N + N + 2 * KCH <= 56)                                \
-            launch_union_nb<DT, KCH, N>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out);  \
-        break;
-        SPV_NB_CASE(1)
-        SPV_NB_CASE(2)
-        SPV_NB_CASE(4)
-        SPV_NB_CASE(6)
-        SPV_NB_CASE(8)
-#undef SPV_NB_CASE
-    }
+static void launch_union_c(hipStream_t s, const ConvPlan& p, const void* in, int64_t in_rows, const void* wpack,
+                           const float* scale, const float* shift, int relu, void* out) {
+    constexpr int NB = 2 * KCH;  // C = 32 * KCH
+    constexpr int RB = union_rb(KCH, NB);
+    constexpr int64_t rows_wg = (int64_t)kUnionWaves * RB * 16;
+    const unsigned grid = (unsigned)((p.m_cap + rows_wg - 1) / rows_wg);
+    k_conv_union<DT, KCH, NB, RB, 1><<<grid, 64 * kUnionWaves, 0, s>>>(
+        p.nbr, p.m_out_dev, p.m_cap, (const uint16_t*)in, 32 * KCH, in_rows, (const uint4*)wpack, scale, shift, relu,
+        (uint16_t*)out);
 }
 
 template <int DT>
-static void launch_union(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows, int Cout,
+static void launch_union(hipStream_t s, const ConvPlan& p, const void* in, int C, int64_t in_rows,
                          const void* wpack, const float* scale, const float* shift, int relu, void* out) {
-    switch ((Cin + 31) / 32) {
-        case 1: launch_union_kch<DT, 1>(s, p, in, Cin, in_rows, Cout, wpack, scale, shift, relu, out); break;
-        case 2: launch_union_kch<DT, 2>(s, p, in, Cin, in_rows, Cout, wpack, scale, shift, relu, out); break;
-        case 3: launch_union_kch<DT, 3>(s, p, in, Cin, in_rows, Cout, wpack, scale, shift, relu, out); break;
-        case 4: launch_union_kch<DT, 4>(s, p, in, Cin, in_rows, Cout, wpack, scale, shift, relu, out); break;
+    switch (C) {
+        case 32: launch_union_c<DT, 1>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
+        case 64: launch_union_c<DT, 2>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
+        case 96: launch_union_c<DT, 3>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
+        case 128: launch_union_c<DT, 4>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
     }
 }
 
 void launch_conv_union(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows, int Cout,
                        const void* wpack, const float* scale, const float* shift, int relu, void* out, int dt) {
-    if (dt == SPV_BF16) launch_union<SPV_BF16>(s, p, in, Cin, in_rows, Cout, wpack, scale, shift, relu, out);
-    else launch_union<SPV_F16>(s, p, in, Cin, in_rows, Cout, wpack, scale, shift, relu, out);
+    (void)Cout;
+    if (dt == SPV_BF16) launch_union<SPV_BF16>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out);
+    else launch_union<SPV_F16>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out);
 }
 
 }  // namespace spv
