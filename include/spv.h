@@ -121,7 +121,11 @@ spv_status spv_kernel_map(void* stream, void* ws, size_t ws_bytes,
  * fine voxels.  Output rows with no pair get act(shift).
  * In:  in [in_rows][Cin] (dt); off [K3+1] / pairs [pair_cap][2] from spv_kernel_map
  *      (device; pairs past pair_cap and indices outside [0, in_rows) /
- *      [0, m_out) are ignored); K3 = 27 or 8; W [K3][Cin][Cout] (dt);
+ *      [0, m_out) are ignored; within each offset the output rows must
+ *      strictly increase -- a map with a pair out of order, or with two pairs
+ *      for one (output, offset), sets SPV_ERR_INVALID_ARG in the workspace
+ *      status, reported by spv_status_check); K3 = 27 or 8;
+ *      W [K3][Cin][Cout] (dt);
  *      scale/shift [Cout] f32 or NULL.
  * Out: out [m_out_cap][Cout] (dt); rows < *m_out_dev are written (m_out_dev
  *      NULL = m_out_cap).

@@ -80,12 +80,15 @@ __global__ void k_conv_bounds(const int32_t* off, const int32_t* pairs, int K3, 
          p += (int64_t)gridDim.x * blockDim.x) {
         if (p < total) {
             const int k = pair_offset(soff, K3, p);
-            const int64_t cur = tile_of(pairs[2 * p + osel], m, nt, T);
-            const int64_t prev = (p == soff[k]) ? -1 : tile_of(pairs[2 * (p - 1) + osel], m, nt, T);
-            if (cur < prev) {
-                raise_flag(h, kFlagUnsorted);
-                continue;
+            const int64_t j = pairs[2 * p + osel];
+            const int64_t cur = tile_of(j, m, nt, T);
+            int64_t prev = -1;
+            if (p != soff[k]) {
+                const int64_t jp = pairs[2 * (p - 1) + osel];
+                prev = tile_of(jp, m, nt, T);
+                if (j <= jp) raise_flag(h, j < jp ? kFlagUnsorted : kFlagDuplicate);
             }
+            if (cur < prev) continue;
             for (int64_t t = prev + 1; t <= cur; ++t) bnd[k * stride + t] = (int32_t)p;
         } else {
             const int k = (int)(p - total);
@@ -111,8 +114,11 @@ __global__ void k_nbr_clear(int32_t* nbr, const int64_t* m_out_dev, int64_t cap,
     }
 }
 
+// A kernel map holds at most one pair per (output, offset), and each offset's
+// pairs come in increasing output order; a map that breaks either raises a flag
+// (a repeated pair would otherwise overwrite instead of adding).
 __global__ void k_nbr_scatter(const int32_t* off, const int32_t* pairs, int K3, int transposed, int64_t pair_bound,
-                              const int64_t* m_out_dev, int64_t cap, int64_t in_rows, int32_t* nbr) {
+                              const int64_t* m_out_dev, int64_t cap, int64_t in_rows, int32_t* nbr, Header* h) {
     __shared__ int32_t soff[kMaxK3 + 1];
     if (threadIdx.x <= K3) soff[threadIdx.x] = off[threadIdx.x];
     __syncthreads();
@@ -123,6 +129,10 @@ __global__ void k_nbr_scatter(const int32_t* off, const int32_t* pairs, int K3, 
         const int k = pair_offset(soff, K3, p);
         const int64_t i = transposed ? pairs[2 * p + 1] : pairs[2 * p];
         const int64_t j = transposed ? pairs[2 * p] : pairs[2 * p + 1];
+        if (p != soff[k]) {
+            const int64_t jp = transposed ? pairs[2 * (p - 1)] : pairs[2 * (p - 1) + 1];
+            if (j <= jp) raise_flag(h, j < jp ? kFlagUnsorted : kFlagDuplicate);
+        }
         if (i >= 0 && i < in_rows && j >= 0 && j < m) nbr[j * K3 + k] = (int32_t)(i + 1);
     }
 }
@@ -135,7 +145,8 @@ void launch_conv_plan(hipStream_t s, const ConvPlan& p, const int32_t* off, cons
         unsigned gc = blocks_for(p.m_cap * K3, 1024);
         if (gc > 2048) gc = 2048;
         k_nbr_clear<<<gc, 256, 0, s>>>(p.nbr, p.m_out_dev, p.m_cap, K3);
-        k_nbr_scatter<<<g, 256, 0, s>>>(off, pairs, K3, transposed, pair_bound, p.m_out_dev, p.m_cap, in_rows, p.nbr);
+        k_nbr_scatter<<<g, 256, 0, s>>>(off, pairs, K3, transposed, pair_bound, p.m_out_dev, p.m_cap, in_rows, p.nbr,
+                                        p.h);
     } else {
         k_conv_bounds<<<g, 256, 0, s>>>(off, pairs, K3, transposed, pair_bound, p.m_out_dev, p.m_cap, p.tile_rows,
                                         p.ntile_cap, p.bnd, p.h);

@@ -247,6 +247,36 @@ def test_conv_strided_and_transposed_sweep(spv, sweep):
     check_close(gotT, refT, "bf16")
 
 
+@pytest.mark.parametrize("K,cin,cout,dtype", [(3, 32, 32, "bf16"), (3, 16, 16, "f32"), (2, 64, 128, "bf16")])
+@pytest.mark.parametrize("defect", ["none", "swapped", "repeated"])
+def test_conv_rejects_malformed_map(spv, K, cin, cout, dtype, defect):
+    """A map whose offset group is out of output order, or holds one (output,
+    offset) twice, is not a kernel map: the conv reports SPV_ERR_INVALID_ARG."""
+    rng = np.random.default_rng(77)
+    c = np.unique(rng.integers(-6, 6, size=(900, 3)), axis=0).astype(np.int32)
+    rc = np.concatenate([np.zeros((len(c), 1), np.int32), c], axis=1)
+    if K == 3:
+        _, off, pairs = oracle.kernel_map(rc)
+        m_out = len(rc)
+    else:
+        oc, off, pairs = oracle.kernel_map(rc, 2, 2)
+        m_out = len(oc)
+    pairs = pairs.copy()
+    g = int(np.argmax(np.diff(off)))  # the largest offset group
+    p = int(off[g]) + 5
+    assert off[g + 1] - off[g] > 10
+    if defect == "swapped":
+        pairs[[p, p + 1]] = pairs[[p + 1, p]]
+    elif defect == "repeated":
+        pairs[p] = pairs[p - 1]
+    x = synth.normal((len(rc), cin), 5, dtype=dtype)
+    W = synth.conv_weight(K ** 3, cin, cout, 6, dtype)
+    ws = spv.Workspace.for_ops(max(m_out, len(rc)), max(cin, cout))
+    spv.spv_sparse_conv(ws, dev(x, dtype), dev(off), dev(pairs), dev(W, dtype), m_out)
+    st = spv.spv_status_check(ws)
+    assert st == (spv.SPV_OK if defect == "none" else spv.SPV_ERR_INVALID_ARG)
+
+
 def test_conv_deterministic(spv, sweep):
     rc, _, _, _ = oracle.voxelize(sweep, 0.05)
     _, off, pairs = oracle.kernel_map(rc)
