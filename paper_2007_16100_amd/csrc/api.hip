@@ -65,7 +65,7 @@ struct MapLayout {
 size_t layout_kmap(void* ws, size_t bytes, int64_t m_cap, int K, int stride, MapLayout& L) {
     Arena a(ws, bytes);
     L.h = a.take<Header>(1);
-    plan_kmap_ws(a, L.w, m_cap, K, stride, true);
+    plan_kmap_ws(a, L.w, m_cap, K, stride, true, true);
     L.w.h = L.h;
     return a.used;
 }
@@ -132,9 +132,10 @@ size_t layout_block(void* ws, size_t bytes, int64_t n, int C, int dt, BlockLayou
     L.vox.h = L.h;
     L.map.h = L.h;
     L.map.fine = L.vox.table;  // the voxelization's table serves the kernel map and the devoxelization
-    plan_kmap_ws(a, L.map, nn, 3, 1, false);
+    plan_kmap_ws(a, L.map, nn, 3, 1, false, false);
     plan_conv_ws(a, L.plan, nn, 27, C, C, dt);
     L.plan.h = L.h;
+    L.map.nbr = L.plan.nbr;  // the map's neighbour table is the 3x3x3 conv's plan
     L.coords = a.take<int32_t>(4 * nn);
     L.counts = a.take<int32_t>(nn);
     L.pt2vox = a.take<int32_t>(nn);
@@ -359,11 +360,17 @@ spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_pa
     // voxel branch: Eq. 1-2 into the hashed grid
     launch_voxelize(s, L.vox, xyz, batch, n, p->voxel_size, feat, C, dt, L.coords, L.va, L.counts, L.pt2vox, L.m_dev);
     mark(1);
-    // one kernel map for both convs, probing the voxelization's table
-    launch_kernel_map(s, L.map, false, L.coords, L.m_dev, nn, 3, 1, nullptr, nullptr, L.off, L.pairs, L.pair_cap);
-    mark(2);
+    // one kernel map for both convs, probing the voxelization's table; the
+    // neighbour-table conv needs only the table, the other kernels the pairs
     L.plan.m_out_dev = L.m_dev;
-    launch_conv_plan(s, L.plan, L.off, L.pairs, 27, 0, L.pair_cap, nn);
+    if (L.plan.use_union) {
+        launch_kernel_map_nbr(s, L.map, L.coords, L.m_dev, nn, L.plan.nbr);
+        mark(2);
+    } else {
+        launch_kernel_map(s, L.map, false, L.coords, L.m_dev, nn, 3, 1, nullptr, nullptr, L.off, L.pairs, L.pair_cap);
+        mark(2);
+        launch_conv_plan(s, L.plan, L.off, L.pairs, 27, 0, L.pair_cap, nn);
+    }
     for (int l = 0; l < p->n_convs; ++l) launch_conv_pack(s, 27, p->W[l], L.wpack_conv[l], C, C, dt);
     mark(3);
     void* cur = L.va;

@@ -62,13 +62,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r16 = lane & 15, g = lane >> 4;
 
-    // workgroups of one XCD take consecutive row ranges (round-robin dispatch over 8 XCDs)
-    const int64_t G = gridDim.x, bid = blockIdx.x;
-    const int64_t xq = G / 8, xr = G % 8, x = bid % 8;
-    const int64_t wg = x * xq + (x < xr ? x : xr) + bid / 8;
-
+    // Workgroups are dispatched round-robin over the 8 XCDs (workgroup b to XCD
+    // b % 8).  The row tiles that exist (from the live row count, not the
+    // capacity the grid was sized for) are split into 8 consecutive ranges, one
+    // per XCD, so neighbouring tiles share an L2 and every XCD gets work.
     const int64_t m = clamp_rows(m_out_dev, m_cap);
-    if (wg * (kUnionWaves * RB * 16) >= m) return;  // the whole workgroup
+    constexpr int64_t rows_wg = kUnionWaves * RB * 16;
+    const int64_t bid = blockIdx.x, x = bid % 8, seq = bid / 8;
+    const int64_t ga = (m + rows_wg - 1) / rows_wg, xq = ga / 8, xr = ga % 8;
+    if (seq >= xq + (x < xr ? 1 : 0)) return;  // the whole workgroup
+    const int64_t wg = x * xq + (x < xr ? x : xr) + seq;
     const int64_t blk0 = (wg * kUnionWaves + wave) * RB;
 
     const __amdgpu_buffer_rsrc_t nb_rs = make_rsrc(nbr, (uint32_t)(m * K3 * 4));
@@ -105,16 +108,41 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
         for (int b = 0; b < RB; ++b)
             dst[b] = __builtin_amdgcn_raw_buffer_load_b32(nb_rs, nboff[b] + (uint32_t)k * 4u, 0, 0);
     };
-    auto load_rows = [&](const int (&nb1)[RB], i32x4 (&dst)[RB][KCH]) __attribute__((always_inline)) {
+    // offsets present in each block (union over its 16 rows), wave-uniform
+    uint32_t umask[RB];
+#pragma unroll
+    for (int b = 0; b < RB; ++b) {
+        uint32_t bits = 0;
+#pragma unroll
+        for (int k = 0; k < K3; k += 4) {
+            if (k + g < K3) {
+                const int v = __builtin_amdgcn_raw_buffer_load_b32(nb_rs, nboff[b] + (uint32_t)(k + g) * 4u, 0, 0);
+                bits |= (v > 0 ? 1u : 0u) << (k + g);
+            }
+        }
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) bits |= __shfl_xor(bits, d, 64);
+        umask[b] = __builtin_amdgcn_readfirstlane(bits);
+    }
+    // gathered rows of offset kr: nothing is fetched for a block without a
+    // neighbour at kr (its registers keep stale values the multiply skips) or
+    // for a lane whose row has none (zeros)
+    auto load_rows = [&](int kr, const int (&nb1)[RB], i32x4 (&dst)[RB][KCH]) __attribute__((always_inline)) {
 #pragma unroll
         for (int b = 0; b < RB; ++b) {
+            if (!((umask[b] >> kr) & 1u)) continue;
             const uint32_t i = (uint32_t)(nb1[b] - 1);  // stored as row + 1; 0 = absent
-            const uint32_t base = i < in_rows32 ? i * row_bytes + (uint32_t)g * 16u : kOutOfRange;
+            const bool have = i < in_rows32;
 #pragma unroll
-            for (int kc = 0; kc < KCH; ++kc) {
-                uint32_t o = base + kc * 64;
-                if (!FULL && kc * 4 + g >= qin) o = kOutOfRange;
-                dst[b][kc] = __builtin_amdgcn_raw_buffer_load_b128(in_rs, o, 0, 0);
+            for (int kc = 0; kc < KCH; ++kc) dst[b][kc] = i32x4{0, 0, 0, 0};
+            if (have) {
+                const uint32_t base = i * row_bytes + (uint32_t)g * 16u;
+#pragma unroll
+                for (int kc = 0; kc < KCH; ++kc) {
+                    uint32_t o = base + kc * 64;
+                    if (!FULL && kc * 4 + g >= qin) o = kOutOfRange;
+                    dst[b][kc] = __builtin_amdgcn_raw_buffer_load_b128(in_rs, o, 0, 0);
+                }
             }
         }
     };
@@ -132,24 +160,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
 #pragma unroll
     for (int j = 0; j < kNAhead; ++j) load_nbr(j, ns[j]);
 #pragma unroll
-    for (int j = 0; j < kRAhead; ++j) load_rows(ns[j], rs[j]);
-
-    // offsets present in each block (union over its 16 rows), wave-uniform
-    uint32_t umask[RB];
-#pragma unroll
-    for (int b = 0; b < RB; ++b) {
-        uint32_t bits = 0;
-#pragma unroll
-        for (int k = 0; k < K3; k += 4) {
-            if (k + g < K3) {
-                const int v = __builtin_amdgcn_raw_buffer_load_b32(nb_rs, nboff[b] + (uint32_t)(k + g) * 4u, 0, 0);
-                bits |= (v > 0 ? 1u : 0u) << (k + g);
-            }
-        }
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) bits |= __shfl_xor(bits, d, 64);
-        umask[b] = __builtin_amdgcn_readfirstlane(bits);
-    }
+    for (int j = 0; j < kRAhead; ++j) load_rows(j, ns[j], rs[j]);
 
     f32x4 acc[RB][NB];
 #pragma unroll
@@ -170,7 +181,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
         if constexpr (k + kWAhead < K3) load_w(k + kWAhead, wtmp);
         if constexpr (k + kNAhead < K3) load_nbr(k + kNAhead, ns[(k + kNAhead) % (kNAhead + 1)]);
         if constexpr (k + kRAhead < K3)
-            load_rows(ns[(k + kRAhead) % (kNAhead + 1)], rs[(k + kRAhead) % (kRAhead + 1)]);
+            load_rows(k + kRAhead, ns[(k + kRAhead) % (kNAhead + 1)], rs[(k + kRAhead) % (kRAhead + 1)]);
         // (4) multiply offset k, one 32-channel slab of W[k] at a time
         const uint4* wk = wbuf(k % (kWAhead + 1));
         uint32_t present = 0;
@@ -246,7 +257,8 @@ static void launch_union_c(hipStream_t s, const ConvPlan& p, const void* in, int
     constexpr int NB = 2 * KCH;  // C = 32 * KCH
     constexpr int RB = union_rb(KCH, NB);
     constexpr int64_t rows_wg = (int64_t)kUnionWaves * RB * 16;
-    const unsigned grid = (unsigned)((p.m_cap + rows_wg - 1) / rows_wg);
+    // a multiple of 8 workgroups: the kernel spreads the live tiles over the 8 XCDs
+    const unsigned grid = (unsigned)(((p.m_cap + rows_wg - 1) / rows_wg + 7) / 8 * 8);
     k_conv_union<DT, KCH, NB, RB, 1><<<grid, 64 * kUnionWaves, 0, s>>>(
         p.nbr, p.m_out_dev, p.m_cap, (const uint16_t*)in, 32 * KCH, in_rows, (const uint4*)wpack, scale, shift, relu,
         (uint16_t*)out);

@@ -106,95 +106,194 @@ __global__ void k_devox_generic(DevoxArgs a, const int32_t* cidx, const float* c
 }
 
 // ---------------------------------------------------------------------------
-// MFMA path
+// MFMA path: a wave owns PB blocks of 16 points.
+//  1. corner probes of all its points issued together (lane (r16, g) takes
+//     corners 2g, 2g+1 of point r16 of each block), weights renormalized over
+//     the present corners, kept in LDS;
+//  2. point MLP D = Wp^T P^T on matrix cores (Wp fragments staged once per
+//     workgroup in LDS): lane (r16, g) ends with channels nb*16 + 4g .. 4g+3 of
+//     point r16, activated and parked in an LDS row tile;
+//  3. blend: one lane per (point, 8-channel chunk) gathers that chunk of the 8
+//     corner voxels (16-byte loads), adds the MLP row chunk and writes the
+//     fused 16 bytes once.
 // ---------------------------------------------------------------------------
+constexpr int kDevoxPB = 4;  // 16-point blocks per wave
+
 template <int DT, int KCH, int NB>
 __global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __restrict__ wpack) {
-    __shared__ int32_t sidx[4][16][8];
-    __shared__ float sw[4][16][8];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    constexpr int PB = kDevoxPB;
+    constexpr int C = NB * 16;
+    constexpr int NCH = C / 8;  // 16-byte chunks per output row
+    __shared__ __align__(16) uint4 wl[KCH * NB * 64];
+    __shared__ __align__(16) int32_t sidx[4][PB * 16][8];
+    __shared__ __align__(16) float sw[4][PB * 16][8];
+    __shared__ __align__(16) float ys[4][16][C + 4];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r16 = lane & 15, g = lane >> 4;
-    const int64_t p0 = ((int64_t)blockIdx.x * 4 + wave) * 16;
-    const int64_t k = p0 + r16;
-    const bool kv = k < a.n;
+    const int64_t p0 = ((int64_t)blockIdx.x * 4 + wave) * (PB * 16);
     const float sfac = __builtin_ldexpf(1.0f, -a.stride_log2);
+    const bool mlp = a.pfeat != nullptr;
 
-    // corners 2g and 2g+1 of point r16
-    Corners c;
-    if (kv) c = point_corners(a.xyz, a.batch, k, a.voxel_size, sfac, a.mode);
-    else c.ok = false;
-    if (kv && !c.ok && g == 0)
-        raise_flag(a.h, isfinite(a.xyz[3 * k]) && isfinite(a.xyz[3 * k + 1]) && isfinite(a.xyz[3 * k + 2])
-                            ? kFlagRange
-                            : kFlagNonfinite);
-    int32_t i0 = corner_lookup(a.table, c, 2 * g), i1 = corner_lookup(a.table, c, 2 * g + 1);
-    float w0 = c.ok ? corner_weight(c, 2 * g) : 0.f, w1 = c.ok ? corner_weight(c, 2 * g + 1) : 0.f;
-    if (kv && a.corner_idx) {
-        a.corner_idx[8 * k + 2 * g] = i0;
-        a.corner_idx[8 * k + 2 * g + 1] = i1;
-        a.corner_w[8 * k + 2 * g] = w0;
-        a.corner_w[8 * k + 2 * g + 1] = w1;
+    // Wp fragments into LDS (the whole workgroup)
+    if (mlp) {
+        for (int f = threadIdx.x; f < KCH * NB * 64; f += blockDim.x) wl[f] = wpack[f];
     }
-    float wp = (i0 >= 0 ? w0 : 0.f) + (i1 >= 0 ? w1 : 0.f);
-    wp += __shfl_xor(wp, 16, 64);
-    wp += __shfl_xor(wp, 32, 64);
-    const float inv = wp > 0.f ? 1.0f / wp : 0.f;
-    sidx[wave][r16][2 * g] = i0;
-    sidx[wave][r16][2 * g + 1] = i1;
-    sw[wave][r16][2 * g] = (i0 >= 0) ? w0 * inv : 0.f;
-    sw[wave][r16][2 * g + 1] = (i1 >= 0) ? w1 * inv : 0.f;
 
-    // point MLP on matrix cores
-    f32x4 acc[NB];
+    // 1. corners: probes of the wave's PB blocks together
+    Corners cn[PB];
+    uint64_t key[2 * PB];
+    bool act[2 * PB];
+    int32_t idx[2 * PB];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (a.pfeat) {
-        const uint16_t* prow = (const uint16_t*)a.pfeat + (kv ? k : 0) * a.Cp + 8 * g;
+    for (int b = 0; b < PB; ++b) {
+        const int64_t k = p0 + b * 16 + r16;
+        if (k < a.n) cn[b] = point_corners(a.xyz, a.batch, k, a.voxel_size, sfac, a.mode);
+        else cn[b].ok = false;
+        if (k < a.n && !cn[b].ok && g == 0)
+            raise_flag(a.h, isfinite(a.xyz[3 * k]) && isfinite(a.xyz[3 * k + 1]) && isfinite(a.xyz[3 * k + 2])
+                                ? kFlagRange
+                                : kFlagNonfinite);
 #pragma unroll
-        for (int kc = 0; kc < KCH; ++kc) {
-            uint4 av = make_uint4(0, 0, 0, 0);
-            if (kv && kc * 32 + 8 * g < a.Cp) av = *(const uint4*)(prow + kc * 32);
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-                acc[nb] = mfma16x16x32<DT>(av, wpack[((int64_t)kc * NB + nb) * 64 + lane], acc[nb]);
+        for (int h = 0; h < 2; ++h) {
+            const int cc = 2 * g + h;
+            act[2 * b + h] = cn[b].ok;
+            key[2 * b + h] = pack_key(cn[b].b, cn[b].base[0] + ((cc >> 2) & 1), cn[b].base[1] + ((cc >> 1) & 1),
+                                      cn[b].base[2] + (cc & 1));
         }
     }
-    __syncthreads();
+    table_find_n<2 * PB>(a.table, key, act, idx);
+#pragma unroll
+    for (int b = 0; b < PB; ++b) {
+        const int64_t k = p0 + b * 16 + r16;
+        const int32_t i0 = idx[2 * b], i1 = idx[2 * b + 1];
+        const float w0 = cn[b].ok ? corner_weight(cn[b], 2 * g) : 0.f;
+        const float w1 = cn[b].ok ? corner_weight(cn[b], 2 * g + 1) : 0.f;
+        if (k < a.n && a.corner_idx) {
+            a.corner_idx[8 * k + 2 * g] = i0;
+            a.corner_idx[8 * k + 2 * g + 1] = i1;
+            a.corner_w[8 * k + 2 * g] = w0;
+            a.corner_w[8 * k + 2 * g + 1] = w1;
+        }
+        float wp = (i0 >= 0 ? w0 : 0.f) + (i1 >= 0 ? w1 : 0.f);
+        wp += __shfl_xor(wp, 16, 64);
+        wp += __shfl_xor(wp, 32, 64);
+        const float inv = wp > 0.f ? 1.0f / wp : 0.f;
+        sidx[wave][b * 16 + r16][2 * g] = i0;
+        sidx[wave][b * 16 + r16][2 * g + 1] = i1;
+        sw[wave][b * 16 + r16][2 * g] = (i0 >= 0) ? w0 * inv : 0.f;
+        sw[wave][b * 16 + r16][2 * g + 1] = (i1 >= 0) ? w1 * inv : 0.f;
+    }
 
-    // epilogue: rows 4g..4g+3 of this wave's 16 points, column nb*16 + r16
+    __syncthreads();  // Wp fragments in LDS
+
     const uint16_t* V = (const uint16_t*)a.vfeat;
     uint16_t* out = (uint16_t*)a.out;
+    // point rows for the MLP: B operand, lane (r16, g) = point r16, channels kc*32 + 8g ..
+    auto load_p = [&](int b, i32x4v (&pv)[KCH]) __attribute__((always_inline)) {
+        const int64_t k = p0 + b * 16 + r16;
+        const uint16_t* prow = (const uint16_t*)a.pfeat + (k < a.n ? k : 0) * a.Cp + 8 * g;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        const int col = nb * 16 + r16;
-        const float sc = a.scale_p ? a.scale_p[col] : 1.f;
-        const float sh = a.shift_p ? a.shift_p[col] : 0.f;
+        for (int kc = 0; kc < KCH; ++kc) {
+            pv[kc] = i32x4v{0, 0, 0, 0};
+            if (mlp && k < a.n && kc * 32 + 8 * g < a.Cp) pv[kc] = *(const i32x4v*)(prow + kc * 32);
+        }
+    };
+    i32x4v pv[2][KCH];
+    load_p(0, pv[0]);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int row = 4 * g + e;
-            const int64_t kk = p0 + row;
-            if (kk >= a.n) continue;
-            float y = 0.f;
-            if (a.pfeat) {
-                y = acc[nb][e] * sc + sh;
-                if (a.relu_p) y = fmaxf(y, 0.f);
+    for (int b = 0; b < PB; ++b) {
+        if (b + 1 < PB) load_p(b + 1, pv[(b + 1) & 1]);
+        f32x4 acc[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (mlp) {
+#pragma unroll
+            for (int kc = 0; kc < KCH; ++kc) {
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+                    acc[nb] = mfma16x16x32<DT>(wl[(kc * NB + nb) * 64 + lane], __builtin_bit_cast(uint4, pv[b & 1][kc]),
+                                               acc[nb]);
             }
-            float dv = 0.f;
+        }
+        // 2. activated MLP rows of block b into the wave's row tile
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (mlp) {
+                const int col = nb * 16 + 4 * g;
+                float sc[4], sh[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {  // (scale / shift need only 4-byte alignment)
+                    sc[e] = a.scale_p ? a.scale_p[col + e] : 1.f;
+                    sh[e] = a.shift_p ? a.shift_p[col + e] : 0.f;
+                }
+                y.x = acc[nb][0] * sc[0] + sh[0];
+                y.y = acc[nb][1] * sc[1] + sh[1];
+                y.z = acc[nb][2] * sc[2] + sh[2];
+                y.w = acc[nb][3] * sc[3] + sh[3];
+                if (a.relu_p) {
+                    y.x = fmaxf(y.x, 0.f);
+                    y.y = fmaxf(y.y, 0.f);
+                    y.z = fmaxf(y.z, 0.f);
+                    y.w = fmaxf(y.w, 0.f);
+                }
+            }
+            *(float4*)&ys[wave][r16][nb * 16 + 4 * g] = y;
+        }
+        __builtin_amdgcn_wave_barrier();
+        // 3. blend: tasks (point, chunk) of block b
+#pragma unroll
+        for (int j = 0; j < (16 * NCH + 63) / 64; ++j) {
+            const int t = lane + 64 * j;
+            if (t >= 16 * NCH) break;
+            const int pt = t / NCH, ch = t - pt * NCH;
+            const int64_t k = p0 + b * 16 + pt;
+            const i32x4v ia = *(const i32x4v*)&sidx[wave][b * 16 + pt][0];
+            const i32x4v ib = *(const i32x4v*)&sidx[wave][b * 16 + pt][4];
+            const float4 wa = *(const float4*)&sw[wave][b * 16 + pt][0];
+            const float4 wb = *(const float4*)&sw[wave][b * 16 + pt][4];
+            const int32_t ci[8] = {ia.x, ia.y, ia.z, ia.w, ib.x, ib.y, ib.z, ib.w};
+            const float cw[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
+            uint4 v[8];
 #pragma unroll
             for (int cc = 0; cc < 8; ++cc) {
-                const int32_t i = sidx[wave][row][cc];
-                if (i >= 0) dv += sw[wave][row][cc] * from16<DT>(V[(int64_t)i * a.C + col]);
+                v[cc] = make_uint4(0, 0, 0, 0);
+                if (ci[cc] >= 0) v[cc] = *(const uint4*)(V + (int64_t)ci[cc] * C + ch * 8);
             }
-            out[kk * a.C + col] = to16<DT>(y + dv);
+            float dv[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) dv[e] = 0.f;
+#pragma unroll
+            for (int cc = 0; cc < 8; ++cc) {
+                if (ci[cc] < 0) continue;
+                const uint32_t u[4] = {v[cc].x, v[cc].y, v[cc].z, v[cc].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    dv[2 * e] += cw[cc] * from16<DT>(u[e] & 0xFFFF);
+                    dv[2 * e + 1] += cw[cc] * from16<DT>(u[e] >> 16);
+                }
+            }
+            const float4 y0 = *(const float4*)&ys[wave][pt][ch * 8];
+            const float4 y1 = *(const float4*)&ys[wave][pt][ch * 8 + 4];
+            const float yy[8] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w};
+            uint32_t o[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                o[e] = (uint32_t)to16<DT>(yy[2 * e] + dv[2 * e]) | ((uint32_t)to16<DT>(yy[2 * e + 1] + dv[2 * e + 1]) << 16);
+            if (k < a.n) *(uint4*)(out + k * C + ch * 8) = make_uint4(o[0], o[1], o[2], o[3]);
         }
+        __builtin_amdgcn_wave_barrier();
     }
 }
 
+// 16-bit features, C in {16, 32, 64, 96, 128} and Cp <= 128 (LDS: the Wp
+// fragments plus each wave's row tile); everything else takes the generic path
 bool devox_mfma_supported(int C, int Cp, int dt) {
     if (dt == SPV_F32 || C % 16 != 0) return false;
     int NB = C / 16;
-    if (!(NB == 1 || NB == 2 || NB == 4 || NB == 6 || NB == 8 || NB == 16)) return false;
-    return Cp == 0 || (Cp % 8 == 0 && Cp <= 256);
+    if (!(NB == 1 || NB == 2 || NB == 4 || NB == 6 || NB == 8)) return false;
+    return Cp == 0 || (Cp % 8 == 0 && Cp <= 128);
 }
 
 void* plan_devox_ws(Arena& a, int C, int Cp) {
@@ -206,22 +305,18 @@ void* plan_devox_ws(Arena& a, int C, int Cp) {
 
 template <int DT, int KCH, int NB>
 static void launch_devox_mfma(hipStream_t s, const DevoxArgs& a, const void* wpack) {
-    int64_t waves = (a.n + 15) / 16;
+    int64_t waves = (a.n + 16 * kDevoxPB - 1) / (16 * kDevoxPB);
     k_devox_mfma<DT, KCH, NB><<<blocks_for(waves, 4), 256, 0, s>>>(a, (const uint4*)wpack);
 }
 
 template <int DT, int NB>
 static void launch_devox_kch(hipStream_t s, const DevoxArgs& a, const void* wpack) {
-    switch ((a.Cp + 31) / 32) {
+    switch (a.pfeat ? (a.Cp + 31) / 32 : 0) {
         case 0:
         case 1: launch_devox_mfma<DT, 1, NB>(s, a, wpack); break;
         case 2: launch_devox_mfma<DT, 2, NB>(s, a, wpack); break;
         case 3: launch_devox_mfma<DT, 3, NB>(s, a, wpack); break;
         case 4: launch_devox_mfma<DT, 4, NB>(s, a, wpack); break;
-        case 5: launch_devox_mfma<DT, 5, NB>(s, a, wpack); break;
-        case 6: launch_devox_mfma<DT, 6, NB>(s, a, wpack); break;
-        case 7: launch_devox_mfma<DT, 7, NB>(s, a, wpack); break;
-        case 8: launch_devox_mfma<DT, 8, NB>(s, a, wpack); break;
     }
 }
 
@@ -233,7 +328,6 @@ static void launch_devox_dt(hipStream_t s, const DevoxArgs& a, const void* wpack
         case 4: launch_devox_kch<DT, 4>(s, a, wpack); break;
         case 6: launch_devox_kch<DT, 6>(s, a, wpack); break;
         case 8: launch_devox_kch<DT, 8>(s, a, wpack); break;
-        case 16: launch_devox_kch<DT, 16>(s, a, wpack); break;
     }
 }
 

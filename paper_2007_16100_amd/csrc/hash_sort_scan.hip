@@ -76,24 +76,22 @@ void launch_table_lookup(hipStream_t s, Table t, const int32_t* q, int64_t nq, i
 constexpr int kSortThreads = 256;
 constexpr int kSortItems = 8;
 constexpr int kSortTile = kSortThreads * kSortItems;
+constexpr int kSortParts = 256;            // partial records of the stand-alone min / max kernel
+constexpr uint32_t kFusedSortBlocks = 1024;  // up to this many tiles a scatter block scans the histograms itself
 
 size_t sort_hist_entries(int64_t cap) { return (size_t)256 * blocks_for(cap, kSortTile); }
+size_t sort_part_records(int64_t cap) {
+    const size_t b = blocks_for(cap, kAppendThreads);
+    return b > (size_t)kSortParts ? b : (size_t)kSortParts;
+}
 
 void plan_sort_ws(Arena& a, SortBufs& sb, int64_t cap) {
     int64_t c = cap > 0 ? cap : 1;
     sb.a = a.take<uint64_t>(c);
     sb.b = a.take<uint64_t>(c);
     sb.hist = a.take<uint32_t>(sort_hist_entries(c));
+    sb.part = a.take<int32_t>(8 * sort_part_records(c));
     sb.st = a.take<SortStats>(1);
-}
-
-__global__ void k_sort_reset(SortStats* st) {
-    if (threadIdx.x < 4) {
-        st->fmin[threadIdx.x] = 0x7fffffff;
-        st->fmax[threadIdx.x] = (int32_t)0x80000000;
-        st->fbits[threadIdx.x] = 0;
-    }
-    if (threadIdx.x == 0) st->sort_bits = 0;
 }
 
 __device__ inline int64_t clamp_count(const int64_t* count_dev, int64_t cap) {
@@ -101,19 +99,38 @@ __device__ inline int64_t clamp_count(const int64_t* count_dev, int64_t cap) {
     return c < 0 ? 0 : (c > cap ? cap : c);
 }
 
-__global__ void k_sort_minmax(SortStats* h, const uint64_t* keys, const int64_t* count_dev, int64_t cap) {
-    int64_t count = clamp_count(count_dev, cap);
+__global__ __launch_bounds__(256) void k_sort_minmax(int32_t* part, const uint64_t* keys, const int64_t* count_dev,
+                                                     int64_t cap) {
+    const int64_t count = clamp_count(count_dev, cap);
     int mn[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
     int mx[4] = {(int)0x80000000, (int)0x80000000, (int)0x80000000, (int)0x80000000};
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count; i += (int64_t)gridDim.x * blockDim.x) {
-        uint64_t k = keys[i];
-        int f[4] = {key_b(k), key_x(k), key_y(k), key_z(k)};
+        const uint64_t k = keys[i];
+        const int f[4] = {key_b(k), key_x(k), key_y(k), key_z(k)};
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
             mn[d] = min(mn[d], f[d]);
             mx[d] = max(mx[d], f[d]);
         }
     }
+    block_minmax_record(mn, mx, part + 8 * blockIdx.x);
+}
+
+// reduce the partial records into the per-field minimum and bit widths
+__global__ __launch_bounds__(256) void k_sort_stats(SortStats* st, const int32_t* part, uint32_t nparts,
+                                                    const int64_t* count_dev, int64_t cap) {
+    int mn[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
+    int mx[4] = {(int)0x80000000, (int)0x80000000, (int)0x80000000, (int)0x80000000};
+    for (uint32_t r = threadIdx.x; r < nparts; r += blockDim.x) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            mn[d] = min(mn[d], part[8 * r + d]);
+            mx[d] = max(mx[d], part[8 * r + 4 + d]);
+        }
+    }
+    __shared__ int32_t red[8];
+    if (threadIdx.x < 8) red[threadIdx.x] = threadIdx.x < 4 ? 0x7fffffff : (int)0x80000000;
+    __syncthreads();
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
 #pragma unroll
@@ -125,58 +142,78 @@ __global__ void k_sort_minmax(SortStats* h, const uint64_t* keys, const int64_t*
     if ((threadIdx.x & 63) == 0) {
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
-            atomicMin(&h->fmin[d], mn[d]);
-            atomicMax(&h->fmax[d], mx[d]);
+            atomicMin(&red[d], mn[d]);  // LDS atomics: a few per block
+            atomicMax(&red[4 + d], mx[d]);
         }
     }
-}
-
-__device__ inline uint32_t bitwidth(uint32_t range) { return range ? 32u - __clz(range) : 0u; }
-
-__global__ void k_sort_compact(SortStats* h, uint64_t* keys, const int64_t* count_dev, int64_t cap) {
-    int64_t count = clamp_count(count_dev, cap);
-    int32_t mn[4];
-    uint32_t w[4];
-#pragma unroll
-    for (int d = 0; d < 4; ++d) {
-        mn[d] = h->fmin[d];
-        w[d] = (count > 0) ? bitwidth((uint32_t)(h->fmax[d] - h->fmin[d])) : 0u;
-    }
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        for (int d = 0; d < 4; ++d) h->fbits[d] = w[d];
-        h->sort_bits = w[0] + w[1] + w[2] + w[3];
-    }
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count; i += (int64_t)gridDim.x * blockDim.x) {
-        uint64_t k = keys[i];
-        uint64_t ck = (uint64_t)(uint32_t)(key_b(k) - mn[0]);
-        ck = (ck << w[1]) | (uint64_t)(uint32_t)(key_x(k) - mn[1]);
-        ck = (ck << w[2]) | (uint64_t)(uint32_t)(key_y(k) - mn[2]);
-        ck = (ck << w[3]) | (uint64_t)(uint32_t)(key_z(k) - mn[3]);
-        keys[i] = ck;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const bool nonempty = clamp_count(count_dev, cap) > 0;
+        uint32_t bits = 0;
+        for (int d = 0; d < 4; ++d) {
+            const uint32_t range = nonempty ? (uint32_t)(red[4 + d] - red[d]) : 0u;
+            const uint32_t w = range ? 32u - __clz(range) : 0u;
+            st->fmin[d] = nonempty ? red[d] : 0;
+            st->fmax[d] = nonempty ? red[4 + d] : 0;
+            st->fbits[d] = w;
+            bits += w;
+        }
+        st->sort_bits = bits;
     }
 }
 
-__global__ __launch_bounds__(kSortThreads) void k_radix_hist(const SortStats* h, SortBufs sb, const int64_t* count_dev,
+// Histogram of one 8-bit digit per tile.  Pass 0 first replaces every key by
+// its compacted form (per-field minimum subtracted, fields packed into their
+// bit widths) in place; it runs even when there is nothing to sort so that the
+// buffer read back always holds compacted keys.
+__global__ __launch_bounds__(kSortThreads) void k_radix_hist(const SortStats* st, SortBufs sb, const int64_t* count_dev,
                                                              int64_t cap, int pass) {
     const uint32_t nblk = gridDim.x;
-    if ((uint32_t)(8 * pass) >= h->sort_bits) return;
-    const uint64_t* src = (pass & 1) ? sb.b : sb.a;
+    if (pass > 0 && (uint32_t)(8 * pass) >= st->sort_bits) return;
+    uint64_t* src = (pass & 1) ? sb.b : sb.a;
     __shared__ uint32_t hist[256];
     hist[threadIdx.x] = 0;
-    __syncthreads();
-    int64_t count = clamp_count(count_dev, cap);
-    int64_t base = (int64_t)blockIdx.x * kSortTile;
+    const int64_t count = clamp_count(count_dev, cap);
+    const int64_t base = (int64_t)blockIdx.x * kSortTile;
+    uint64_t key[kSortItems];
+#pragma unroll
     for (int r = 0; r < kSortItems; ++r) {
-        int64_t i = base + r * kSortThreads + threadIdx.x;
-        if (i < count) atomicAdd(&hist[(src[i] >> (8 * pass)) & 0xFF], 1u);
+        const int64_t i = base + r * kSortThreads + threadIdx.x;
+        key[r] = i < count ? src[i] : 0ull;
+    }
+    if (pass == 0) {
+        int32_t mn[4];
+        uint32_t w[4];
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            mn[d] = st->fmin[d];
+            w[d] = st->fbits[d];
+        }
+#pragma unroll
+        for (int r = 0; r < kSortItems; ++r) {
+            const int64_t i = base + r * kSortThreads + threadIdx.x;
+            const uint64_t k = key[r];
+            uint64_t ck = (uint64_t)(uint32_t)(key_b(k) - mn[0]);
+            ck = (ck << w[1]) | (uint64_t)(uint32_t)(key_x(k) - mn[1]);
+            ck = (ck << w[2]) | (uint64_t)(uint32_t)(key_y(k) - mn[2]);
+            ck = (ck << w[3]) | (uint64_t)(uint32_t)(key_z(k) - mn[3]);
+            key[r] = ck;
+            if (i < count) src[i] = ck;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+        const int64_t i = base + r * kSortThreads + threadIdx.x;
+        if (i < count) atomicAdd(&hist[(key[r] >> (8 * pass)) & 0xFF], 1u);
     }
     __syncthreads();
     sb.hist[threadIdx.x * nblk + blockIdx.x] = hist[threadIdx.x];
 }
 
-// exclusive scan of the digit-major histogram by one block
-__global__ __launch_bounds__(1024) void k_radix_scan(const SortStats* h, uint32_t* hist, uint32_t n, int pass) {
-    if ((uint32_t)(8 * pass) >= h->sort_bits) return;
+// exclusive scan of the digit-major histogram by one block (many-tile sorts)
+__global__ __launch_bounds__(1024) void k_radix_scan(const SortStats* st, uint32_t* hist, uint32_t n, int pass) {
+    if ((uint32_t)(8 * pass) >= st->sort_bits) return;
     __shared__ int lds[17];
     uint32_t per = (n + blockDim.x - 1) / blockDim.x;
     uint32_t lo = threadIdx.x * per, hi = min(n, lo + per);
@@ -191,41 +228,67 @@ __global__ __launch_bounds__(1024) void k_radix_scan(const SortStats* h, uint32_
     }
 }
 
-__global__ __launch_bounds__(kSortThreads) void k_radix_scatter(const SortStats* h, SortBufs sb,
-                                                                const int64_t* count_dev, int64_t cap, int pass) {
+// Stable scatter of one tile by one digit.  With `fused`, the block derives its
+// digit offsets from the raw histograms (thread d: all tiles' counts of digit d,
+// those of earlier tiles, then a scan over the digits); otherwise k_radix_scan
+// has already turned the histograms into offsets.
+__global__ __launch_bounds__(kSortThreads) void k_radix_scatter(const SortStats* st, SortBufs sb,
+                                                                const int64_t* count_dev, int64_t cap, int pass,
+                                                                int fused) {
     const uint32_t nblk = gridDim.x;
-    if ((uint32_t)(8 * pass) >= h->sort_bits) return;
+    if ((uint32_t)(8 * pass) >= st->sort_bits) return;
     const uint64_t* src = (pass & 1) ? sb.b : sb.a;
     uint64_t* dst = (pass & 1) ? sb.a : sb.b;
     __shared__ uint32_t run[256];
     __shared__ uint32_t wcnt[kSortThreads / 64][256];
     __shared__ uint32_t woff[kSortThreads / 64][256];
+    __shared__ int lds[kSortThreads / 64 + 1];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    run[t] = sb.hist[t * nblk + blockIdx.x];
+    const int64_t count = clamp_count(count_dev, cap);
+    const int64_t base = (int64_t)blockIdx.x * kSortTile;
+    uint64_t keys[kSortItems];
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+        const int64_t i = base + r * kSortThreads + t;
+        keys[r] = i < count ? src[i] : 0ull;
+    }
+    if (fused) {
+        const uint32_t* hd = sb.hist + (size_t)t * nblk;
+        uint32_t tot = 0, pre = 0;
+#pragma unroll 8
+        for (uint32_t b = 0; b < nblk; ++b) {
+            const uint32_t v = hd[b];
+            tot += v;
+            pre += (b < blockIdx.x) ? v : 0u;
+        }
+        int all;
+        run[t] = (uint32_t)block_exclusive_scan((int)tot, lds, &all) + pre;
+    } else {
+        run[t] = sb.hist[t * nblk + blockIdx.x];
+    }
     for (int w = 0; w < kSortThreads / 64; ++w) wcnt[w][t] = 0;
     __syncthreads();
-    int64_t count = clamp_count(count_dev, cap);
-    int64_t base = (int64_t)blockIdx.x * kSortTile;
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
     for (int r = 0; r < kSortItems; ++r) {
-        int64_t i = base + r * kSortThreads + t;
-        bool valid = i < count;
-        uint64_t key = valid ? src[i] : 0;
-        uint32_t d = (uint32_t)(key >> (8 * pass)) & 0xFF;
+        const int64_t i = base + r * kSortThreads + t;
+        const bool valid = i < count;
+        const uint64_t key = keys[r];
+        const uint32_t d = (uint32_t)(key >> (8 * pass)) & 0xFF;
         // lanes of this wave holding the same digit
         uint64_t peers = __ballot(valid);
 #pragma unroll
         for (int b = 0; b < 8; ++b) {
-            uint64_t bal = __ballot((d >> b) & 1);
+            const uint64_t bal = __ballot((d >> b) & 1);
             peers &= ((d >> b) & 1) ? bal : ~bal;
         }
-        uint32_t rank = (uint32_t)__popcll(peers & lt);
+        const uint32_t rank = (uint32_t)__popcll(peers & lt);
         if (valid && rank == 0) wcnt[wave][d] = (uint32_t)__popcll(peers);
         __syncthreads();
         {
             uint32_t b0 = run[t];
             for (int w = 0; w < kSortThreads / 64; ++w) {
-                uint32_t c = wcnt[w][t];
+                const uint32_t c = wcnt[w][t];
                 woff[w][t] = b0;
                 b0 += c;
                 wcnt[w][t] = 0;
@@ -237,18 +300,21 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_scatter(const SortStats*
     }
 }
 
-void launch_sort_keys(hipStream_t s, SortBufs sb, const int64_t* count_dev, int64_t cap) {
+void launch_sort_keys(hipStream_t s, SortBufs sb, const int64_t* count_dev, int64_t cap, uint32_t nparts) {
     if (cap <= 0) cap = 1;
-    SortStats* h = sb.st;
-    k_sort_reset<<<1, 64, 0, s>>>(h);
-    unsigned g = blocks_for(cap, 256 * 4);
-    k_sort_minmax<<<g, 256, 0, s>>>(h, sb.a, count_dev, cap);
-    k_sort_compact<<<g, 256, 0, s>>>(h, sb.a, count_dev, cap);
-    unsigned nblk = blocks_for(cap, kSortTile);
+    if (nparts == 0) {
+        unsigned g = blocks_for(cap, 256 * 4);
+        if (g > (unsigned)kSortParts) g = kSortParts;
+        k_sort_minmax<<<g, 256, 0, s>>>(sb.part, sb.a, count_dev, cap);
+        nparts = g;
+    }
+    k_sort_stats<<<1, 256, 0, s>>>(sb.st, sb.part, nparts, count_dev, cap);
+    const unsigned nblk = blocks_for(cap, kSortTile);
+    const int fused = nblk <= kFusedSortBlocks ? 1 : 0;
     for (int pass = 0; pass < 8; ++pass) {
-        k_radix_hist<<<nblk, kSortThreads, 0, s>>>(h, sb, count_dev, cap, pass);
-        k_radix_scan<<<1, 1024, 0, s>>>(h, sb.hist, 256 * nblk, pass);
-        k_radix_scatter<<<nblk, kSortThreads, 0, s>>>(h, sb, count_dev, cap, pass);
+        k_radix_hist<<<nblk, kSortThreads, 0, s>>>(sb.st, sb, count_dev, cap, pass);
+        if (!fused) k_radix_scan<<<1, 1024, 0, s>>>(sb.st, sb.hist, 256 * nblk, pass);
+        k_radix_scatter<<<nblk, kSortThreads, 0, s>>>(sb.st, sb, count_dev, cap, pass, fused);
     }
 }
 
@@ -258,6 +324,7 @@ void launch_sort_keys(hipStream_t s, SortBufs sb, const int64_t* count_dev, int6
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 8;
 constexpr int kScanTile = kScanThreads * kScanItems;
+constexpr unsigned kScanFusedTiles = 4096;  // up to this many tiles: two kernels, no separate scan of the sums
 
 size_t scan_tmp_entries(int64_t cap) { return (size_t)blocks_for(cap + 1, kScanTile) + 1; }
 
@@ -306,9 +373,59 @@ __global__ void k_scan_add(int32_t* out, const int64_t* count_dev, int64_t cap, 
     if (i <= count) out[i] += tmp[i / kScanTile];
 }
 
+// tile sums only (first kernel of the two-kernel scan)
+__global__ __launch_bounds__(kScanThreads) void k_scan_sums(const int32_t* in, const int64_t* count_dev, int64_t cap,
+                                                            int32_t* tmp) {
+    __shared__ int lds[kScanThreads / 64 + 1];
+    const int64_t count = count_dev ? clamp_count(count_dev, cap) : cap;
+    const int64_t base = (int64_t)blockIdx.x * kScanTile;
+    int s = 0;
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+        const int64_t i = base + j * kScanThreads + threadIdx.x;
+        s += (i < count) ? in[i] : 0;
+    }
+    int tot;
+    block_exclusive_scan(s, lds, &tot);
+    if (threadIdx.x == 0) tmp[blockIdx.x] = tot;
+}
+
+// every tile adds up the sums of the tiles before it, then scans itself
+__global__ __launch_bounds__(kScanThreads) void k_scan_apply(const int32_t* in, int32_t* out, const int64_t* count_dev,
+                                                             int64_t cap, const int32_t* tmp) {
+    __shared__ int lds[kScanThreads / 64 + 1];
+    const int64_t count = count_dev ? clamp_count(count_dev, cap) : cap;
+    int pre = 0;
+    for (uint32_t b = threadIdx.x; b < blockIdx.x; b += blockDim.x) pre += tmp[b];
+    int prefix;
+    block_exclusive_scan(pre, lds, &prefix);
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    int v[kScanItems];
+    int s = 0;
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+        const int64_t i = base + j;
+        v[j] = (i < count) ? in[i] : 0;
+        s += v[j];
+    }
+    int tot;
+    int run = block_exclusive_scan(s, lds, &tot) + prefix;
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+        const int64_t i = base + j;
+        if (i <= count) out[i] = run;
+        run += v[j];
+    }
+}
+
 void launch_exclusive_scan(hipStream_t s, const int32_t* in, int32_t* out, const int64_t* count_dev, int64_t cap,
                            int32_t* tmp) {
     unsigned nb = blocks_for(cap + 1, kScanTile);
+    if (nb <= kScanFusedTiles) {
+        k_scan_sums<<<nb, kScanThreads, 0, s>>>(in, count_dev, cap, tmp);
+        k_scan_apply<<<nb, kScanThreads, 0, s>>>(in, out, count_dev, cap, tmp);
+        return;
+    }
     k_scan_tiles<<<nb, kScanThreads, 0, s>>>(in, out, count_dev, cap, tmp);
     k_scan_totals<<<1, 1024, 0, s>>>(tmp, nb);
     k_scan_add<<<blocks_for(cap + 1, 256), 256, 0, s>>>(out, count_dev, cap, tmp);

@@ -3,23 +3,31 @@
 // built with the same GPU hash table as the voxelization).
 //
 // Outputs: CSR by offset k -- off[K^3+1] and pairs (in, out), each offset's
-// pairs sorted by out.  Two passes over the outputs, 256 per block:
-//   pass 1: probe the K^3 neighbour coordinates of each output, keep a bit mask
-//           of the present offsets, count per (offset, block) with wave ballots;
-//   scan:   one exclusive scan over the offset-major (offset, block) counts gives
-//           every block its write position inside every offset's segment;
-//   pass 2: re-probe only the present offsets and write the pairs, the rank
-//           inside the block coming from the same ballots -> deterministic,
+// pairs sorted by out.
+//
+// Submanifold 3x3x3 maps (outputs = inputs), blocks of 64 output voxels:
+//   pass 1: the dense neighbour table nbr[j][k] = i + 1 (0 = no voxel), one
+//           hash probe per (voxel, offset) with a wave's probes issued together,
+//           and per-(offset, block) pair counts from wave ballots;
+//   scan:   one exclusive scan over the offset-major (offset, block) counts
+//           gives every block its write position inside every offset's segment;
+//   pass 2: reads the table back and writes the pairs at their final, sorted
+//           positions (rank inside the block from ballots) -> deterministic,
 //           already-sorted output without atomics.
-// Stride 2: the output voxels are the distinct floor(c/2), deduplicated in a
-// second hash table and radix-sorted into canonical order first.
+// The 3x3x3 convolution consumes the neighbour table directly, so a block that
+// only needs the convolution stops after pass 1.
+// Stride 2 (K = 2): the output voxels are the distinct floor(c/2), deduplicated
+// in a second hash table and radix-sorted into canonical order; then a probe /
+// count pass and a write pass over 256 outputs per block as above.
 #include "spv_internal.hpp"
 
 namespace spv {
 
 constexpr int kMapThreads = 256;
+constexpr int kNbrVox = 64;  // output voxels per block of the 3x3x3 passes (one per lane)
+constexpr int kNbrProbes = 7;  // offsets per wave: wave w takes k = w, w + 4, ..., < 27
 
-void plan_kmap_ws(Arena& a, KmapWs& w, int64_t m_cap, int K, int stride, bool own_fine_table) {
+void plan_kmap_ws(Arena& a, KmapWs& w, int64_t m_cap, int K, int stride, bool own_fine_table, bool own_nbr) {
     int64_t mc = m_cap > 0 ? m_cap : 1;
     const int K3 = K * K * K;
     if (own_fine_table) {
@@ -37,11 +45,13 @@ void plan_kmap_ws(Arena& a, KmapWs& w, int64_t m_cap, int K, int stride, bool ow
     } else {
         w.coarse = Table{nullptr, nullptr, 0};
     }
-    size_t nblk = blocks_for(mc, kMapThreads);
+    size_t nblk = blocks_for(mc, K == 3 ? kNbrVox : kMapThreads);
     w.mask = a.take<uint32_t>(mc);
     w.bcnt = a.take<uint32_t>(K3 * nblk);
     w.bbase = a.take<uint32_t>(K3 * nblk + 1);
+    w.scan_tmp = a.take<int32_t>(scan_tmp_entries((int64_t)K3 * nblk));
     w.m_out = a.take<int64_t>(2);
+    w.nbr = (K == 3 && own_nbr) ? a.take<int32_t>((size_t)mc * 27) : nullptr;
 }
 
 __device__ inline int64_t count_or_cap(const int64_t* d, int64_t cap) {
@@ -72,23 +82,37 @@ __global__ void k_map_same_count(const int64_t* m_in_dev, int64_t cap, int64_t* 
 
 __global__ void k_map_zero_i64(int64_t* p) { *p = 0; }
 
-// stride 2: coarse keys into the coarse table; creators append to the key list
-__global__ void k_map_coarse_insert(Header* h, Table coarse, uint64_t* ukeys, int64_t* cnt, const int32_t* in_coords,
-                                    const int64_t* m_in_dev, int64_t cap) {
-    int64_t m = count_or_cap(m_in_dev, cap);
-    int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    if (i >= m) return;
-    const int32_t* c = in_coords + 4 * i;
-    // floor(c / 2) via arithmetic shift
-    uint64_t key = pack_key(c[0], c[1] >> 1, c[2] >> 1, c[3] >> 1);
-    uint32_t slot;
-    int r = table_insert(coarse, key, &slot);
-    if (r > 0) {
-        unsigned long long idx = atomicAdd((unsigned long long*)cnt, 1ull);
-        ukeys[idx] = key;
-    } else if (r < 0) {
-        raise_flag(h, kFlagTableFull);
+// stride 2: coarse keys into the coarse table; each block appends the keys it
+// created to the key list and records their per-field min / max for the sort
+__global__ __launch_bounds__(kAppendThreads) void k_map_coarse_insert(Header* h, Table coarse, SortBufs sb,
+                                                                      int64_t* cnt, const int32_t* in_coords,
+                                                                      const int64_t* m_in_dev, int64_t cap) {
+    const int64_t m = count_or_cap(m_in_dev, cap);
+    const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    bool created = false;
+    uint64_t key = kEmpty;
+    int f[4] = {0, 0, 0, 0};
+    if (i < m) {
+        const int32_t* c = in_coords + 4 * i;
+        // floor(c / 2) via arithmetic shift
+        f[0] = c[0];
+        f[1] = c[1] >> 1;
+        f[2] = c[2] >> 1;
+        f[3] = c[3] >> 1;
+        key = pack_key(f[0], f[1], f[2], f[3]);
+        uint32_t slot;
+        const int r = table_insert(coarse, key, &slot);
+        created = r > 0;
+        if (r < 0) raise_flag(h, kFlagTableFull);
     }
+    int mn[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
+    int mx[4] = {(int)0x80000000, (int)0x80000000, (int)0x80000000, (int)0x80000000};
+    if (created) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) mn[d] = mx[d] = f[d];
+    }
+    block_append(created, key, sb.a, cnt);
+    block_minmax_record(mn, mx, sb.part + 8 * blockIdx.x);
 }
 
 __global__ void k_map_coarse_rank(SortBufs sb, Table coarse, const int64_t* cnt, int64_t cap, int32_t* out_coords,
@@ -197,6 +221,85 @@ __global__ __launch_bounds__(kMapThreads) void k_map_write(Header* h, Table fine
     }
 }
 
+// pass 1 of a submanifold 3x3x3 map (see the file comment); bcnt may be null
+__global__ __launch_bounds__(256) void k_map_nbr3(Table fine, const int32_t* coords, const int64_t* m_out,
+                                                  int64_t cap, int32_t* nbr, uint32_t* bcnt) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t m = count_or_cap(m_out, cap);
+    const int64_t j = (int64_t)blockIdx.x * kNbrVox + lane;
+    const bool valid = j < m;
+    int c[4] = {0, 0, 0, 0};
+    if (valid) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) c[d] = coords[4 * j + d];
+    }
+    uint64_t key[kNbrProbes];
+    bool act[kNbrProbes];
+    int32_t res[kNbrProbes];
+#pragma unroll
+    for (int q = 0; q < kNbrProbes; ++q) {
+        const int k = wave + 4 * q;
+        int dx, dy, dz;
+        offset_delta<3>(k, dx, dy, dz);
+        // the centre offset of a submanifold map is the voxel itself
+        act[q] = valid && k < 27 && k != 13;
+        key[q] = pack_key(c[0], c[1] + dx, c[2] + dy, c[3] + dz);
+    }
+    table_find_n<kNbrProbes>(fine, key, act, res);
+    const uint32_t nblk = gridDim.x;
+#pragma unroll
+    for (int q = 0; q < kNbrProbes; ++q) {
+        const int k = wave + 4 * q;
+        if (k >= 27) break;
+        const int32_t i = (k == 13) ? (int32_t)j : res[q];
+        const bool present = valid && i >= 0;
+        if (valid) nbr[j * 27 + k] = present ? i + 1 : 0;
+        if (bcnt) {
+            const uint64_t bal = __ballot(present);
+            if (lane == 0) bcnt[k * nblk + blockIdx.x] = (uint32_t)__popcll(bal);
+        }
+    }
+}
+
+// pass 2 of a submanifold 3x3x3 map: pairs from the neighbour table
+__global__ __launch_bounds__(256) void k_map_pairs3(Header* h, const int32_t* nbr, const int64_t* m_out, int64_t cap,
+                                                    const uint32_t* bbase, int32_t* off, int32_t* pairs,
+                                                    int64_t pair_cap) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t nblk = gridDim.x;
+    if (blockIdx.x == 0) {
+        for (int k = threadIdx.x; k <= 27; k += blockDim.x) off[k] = (int32_t)bbase[k * nblk];
+    }
+    const int64_t m = count_or_cap(m_out, cap);
+    const int64_t j = (int64_t)blockIdx.x * kNbrVox + lane;
+    const bool valid = j < m;
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+    for (int q = 0; q < kNbrProbes; ++q) {
+        const int k = wave + 4 * q;
+        if (k >= 27) break;
+        const int32_t e = valid ? nbr[j * 27 + k] : 0;
+        const uint64_t bal = __ballot(e != 0);
+        if (e != 0) {
+            const int64_t pos = (int64_t)bbase[k * nblk + blockIdx.x] + __popcll(bal & lt);
+            if (pos < pair_cap) {
+                pairs[2 * pos] = e - 1;
+                pairs[2 * pos + 1] = (int32_t)j;
+            } else {
+                raise_flag(h, kFlagCapacity);
+            }
+        }
+    }
+}
+
+void launch_kernel_map_nbr(hipStream_t s, const KmapWs& w, const int32_t* coords, const int64_t* m_dev,
+                           int64_t m_cap, int32_t* nbr) {
+    const int64_t mc = m_cap > 0 ? m_cap : 1;
+    k_map_nbr3<<<blocks_for(mc, kNbrVox), 256, 0, s>>>(w.fine, coords, m_dev, mc, nbr, nullptr);
+}
+
 void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const int32_t* in_coords,
                        const int64_t* m_in_dev, int64_t m_cap, int K, int stride, int32_t* out_coords,
                        int64_t* m_out_dev, int32_t* off, int32_t* pairs, int64_t pair_cap) {
@@ -208,26 +311,26 @@ void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const in
         launch_table_build(s, w.h, w.fine, in_coords, m_in_dev, m_cap);
     }
     const int32_t* oc = in_coords;
-    if (stride == 1) {
-        k_map_same_count<<<1, 1, 0, s>>>(m_in_dev, m_cap, w.m_out, m_out_dev);
-    } else {
+    if (stride == 2) {
         launch_clear(s, w.h, w.coarse, false);
         k_map_zero_i64<<<1, 1, 0, s>>>(w.m_out + 1);
-        k_map_coarse_insert<<<nblk, kMapThreads, 0, s>>>(w.h, w.coarse, w.sort.a, w.m_out + 1, in_coords, m_in_dev,
-                                                         m_cap);
-        launch_sort_keys(s, w.sort, w.m_out + 1, mc);
+        const unsigned nins = blocks_for(mc, kAppendThreads);
+        k_map_coarse_insert<<<nins, kAppendThreads, 0, s>>>(w.h, w.coarse, w.sort, w.m_out + 1, in_coords, m_in_dev,
+                                                            mc);
+        launch_sort_keys(s, w.sort, w.m_out + 1, mc, nins);
         k_map_coarse_rank<<<nblk, kMapThreads, 0, s>>>(w.sort, w.coarse, w.m_out + 1, mc, out_coords, w.m_out,
                                                        m_out_dev);
         oc = out_coords;
     }
     if (K == 3) {
-        k_map_mask<3, 1><<<nblk, kMapThreads, 0, s>>>(w.fine, oc, w.m_out, mc, w.mask, w.bcnt);
-        launch_exclusive_scan_small(s, w.bcnt, w.bbase, (int64_t)K3 * nblk);
-        k_map_write<3, 1><<<nblk, kMapThreads, 0, s>>>(w.h, w.fine, oc, w.m_out, mc, w.mask, w.bbase, off, pairs,
-                                                       pair_cap);
+        const unsigned nb3 = blocks_for(mc, kNbrVox);
+        k_map_same_count<<<1, 1, 0, s>>>(m_in_dev, m_cap, w.m_out, m_out_dev);
+        k_map_nbr3<<<nb3, 256, 0, s>>>(w.fine, in_coords, w.m_out, mc, w.nbr, w.bcnt);
+        launch_exclusive_scan(s, (const int32_t*)w.bcnt, (int32_t*)w.bbase, nullptr, (int64_t)27 * nb3, w.scan_tmp);
+        k_map_pairs3<<<nb3, 256, 0, s>>>(w.h, w.nbr, w.m_out, mc, w.bbase, off, pairs, pair_cap);
     } else {
         k_map_mask<2, 2><<<nblk, kMapThreads, 0, s>>>(w.fine, oc, w.m_out, mc, w.mask, w.bcnt);
-        launch_exclusive_scan_small(s, w.bcnt, w.bbase, (int64_t)K3 * nblk);
+        launch_exclusive_scan(s, (const int32_t*)w.bcnt, (int32_t*)w.bbase, nullptr, (int64_t)K3 * nblk, w.scan_tmp);
         k_map_write<2, 2><<<nblk, kMapThreads, 0, s>>>(w.h, w.fine, oc, w.m_out, mc, w.mask, w.bbase, off, pairs,
                                                        pair_cap);
     }

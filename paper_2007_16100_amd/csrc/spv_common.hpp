@@ -53,26 +53,34 @@ struct alignas(256) Header {
 __device__ inline void raise_flag(Header* h, uint32_t f) { atomicOr(&h->status, f); }
 
 // ---------------------------------------------------------------------------
-// open-addressing hash with linear probing over 64-bit keys
+// open-addressing hash with linear probing over 64-bit keys.  A probe sequence
+// starts at the first slot of a 4-slot bucket (a 32-byte aligned run of keys)
+// and continues linearly, wrapping at the end of the table; lookups read one
+// whole bucket (4 keys + 4 values) per round, so almost every lookup costs a
+// single memory round trip.
 // ---------------------------------------------------------------------------
+typedef unsigned long long u64x2 __attribute__((ext_vector_type(2)));
+typedef int i32x4v __attribute__((ext_vector_type(4)));
+
 __host__ __device__ inline uint32_t hash_slot(uint64_t k, uint32_t mask) {
-    // murmur3 64-bit finalizer
+    // murmur3 64-bit finalizer, scaled to a bucket's first slot
     k ^= k >> 33;
     k *= 0xff51afd7ed558ccdull;
     k ^= k >> 33;
     k *= 0xc4ceb9fe1a85ec53ull;
     k ^= k >> 33;
-    return (uint32_t)k & mask;
+    return ((uint32_t)k << 2) & mask;
 }
 
 struct Table {
-    uint64_t* keys;
-    int32_t* vals;
-    uint32_t mask;  // capacity - 1 (capacity is a power of two)
+    uint64_t* keys;  // [capacity], 256-byte aligned
+    int32_t* vals;   // [capacity], 256-byte aligned
+    uint32_t mask;   // capacity - 1 (capacity is a power of two, >= 1024)
 };
 
 // Insert; returns 1 if this call created the entry, 0 if the key was present,
-// -1 if the table is full.  *slot receives the entry's slot.
+// -1 if the table is full.  *slot receives the entry's slot.  Slots are claimed
+// strictly in probe order, so a lookup may stop at the first empty slot.
 __device__ inline int table_insert(Table t, uint64_t key, uint32_t* slot) {
     uint32_t s = hash_slot(key, t.mask);
     for (uint32_t i = 0; i <= t.mask; ++i) {
@@ -98,28 +106,91 @@ __device__ inline int table_insert(Table t, uint64_t key, uint32_t* slot) {
     return -1;
 }
 
+// One bucket of a probe: keys s..s+3 (s a multiple of 4) and their values.
+struct Bucket {
+    u64x2 k01, k23;
+    i32x4v v;
+};
+__device__ inline Bucket load_bucket(Table t, uint32_t s) {
+    Bucket b;
+    b.k01 = *(const u64x2*)(t.keys + s);
+    b.k23 = *(const u64x2*)(t.keys + s + 2);
+    b.v = *(const i32x4v*)(t.vals + s);
+    return b;
+}
+// settle a lookup from one bucket: 1 = found (*pos = slot offset 0..3),
+// 0 = absent (an empty slot came first), -1 = continue with the next bucket
+__device__ inline int bucket_match(const Bucket& b, uint64_t key, int* pos) {
+    const uint64_t k[4] = {b.k01.x, b.k01.y, b.k23.x, b.k23.y};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        if (k[e] == key) {
+            *pos = e;
+            return 1;
+        }
+        if (k[e] == kEmpty) return 0;
+    }
+    return -1;
+}
+__device__ inline int32_t bucket_val(const Bucket& b, int e) {
+    return e == 0 ? b.v.x : e == 1 ? b.v.y : e == 2 ? b.v.z : b.v.w;
+}
+
+// slot of a present key, -1 if absent; the probe starts at bucket slot s
+__device__ inline int64_t table_slot_from(Table t, uint64_t key, uint32_t s) {
+    for (uint32_t i = 0; i <= t.mask; i += 4) {
+        const Bucket b = load_bucket(t, s);
+        int e = 0;
+        const int r = bucket_match(b, key, &e);
+        if (r > 0) return (int64_t)(s + e);
+        if (r == 0) return -1;
+        s = (s + 4) & t.mask;
+    }
+    return -1;
+}
+
 // Lookup after the table is complete (a later kernel); -1 if absent.
 __device__ inline int32_t table_find(Table t, uint64_t key) {
     uint32_t s = hash_slot(key, t.mask);
-    for (uint32_t i = 0; i <= t.mask; ++i) {
-        uint64_t cur = t.keys[s];
-        if (cur == key) return t.vals[s];
-        if (cur == kEmpty) return -1;
-        s = (s + 1) & t.mask;
+    for (uint32_t i = 0; i <= t.mask; i += 4) {
+        const Bucket b = load_bucket(t, s);
+        int e = 0;
+        const int r = bucket_match(b, key, &e);
+        if (r > 0) return bucket_val(b, e);
+        if (r == 0) return -1;
+        s = (s + 4) & t.mask;
     }
     return -1;
 }
 
 // slot of a present key (used to set values); -1 if absent
-__device__ inline int64_t table_slot(Table t, uint64_t key) {
-    uint32_t s = hash_slot(key, t.mask);
-    for (uint32_t i = 0; i <= t.mask; ++i) {
-        uint64_t cur = t.keys[s];
-        if (cur == key) return s;
-        if (cur == kEmpty) return -1;
-        s = (s + 1) & t.mask;
+__device__ inline int64_t table_slot(Table t, uint64_t key) { return table_slot_from(t, key, hash_slot(key, t.mask)); }
+
+// NP lookups whose first buckets are read together (one round trip for all of
+// them); the rare key not settled by its first bucket continues on its own.
+// Inactive entries (act[p] false) read bucket 0 and return -1.
+template <int NP>
+__device__ inline void table_find_n(Table t, const uint64_t (&key)[NP], const bool (&act)[NP], int32_t (&res)[NP]) {
+    uint32_t s[NP];
+    Bucket b[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        s[p] = act[p] ? hash_slot(key[p], t.mask) : 0u;
+        b[p] = load_bucket(t, s[p]);
     }
-    return -1;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        int e = 0;
+        const int r = act[p] ? bucket_match(b[p], key[p], &e) : 0;
+        if (r > 0) {
+            res[p] = bucket_val(b[p], e);
+        } else if (r == 0) {
+            res[p] = -1;
+        } else {
+            const int64_t sl = table_slot_from(t, key[p], (s[p] + 4) & t.mask);
+            res[p] = sl >= 0 ? t.vals[sl] : -1;
+        }
+    }
 }
 
 inline uint32_t table_capacity(int64_t max_keys) {

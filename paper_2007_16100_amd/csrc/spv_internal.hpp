@@ -35,6 +35,47 @@ __device__ inline int block_exclusive_scan(int v, int* lds, int* total) {
     return r;
 }
 
+// Threads per block of the kernels that append new keys to a list.
+constexpr int kAppendThreads = 1024;
+
+// Appends `key` for every thread with `take` set to list[*counter ...] with one
+// counter atomic per block (order inside the list is unspecified).  Every thread
+// of the block must call it.
+__device__ inline void block_append(bool take, uint64_t key, uint64_t* list, int64_t* counter) {
+    __shared__ int lds[kAppendThreads / 64 + 1];
+    __shared__ unsigned long long base;
+    int tot;
+    const int r = block_exclusive_scan(take ? 1 : 0, lds, &tot);
+    if (threadIdx.x == 0) base = tot ? atomicAdd((unsigned long long*)counter, (unsigned long long)tot) : 0ull;
+    __syncthreads();
+    if (take) list[base + (unsigned long long)r] = key;
+}
+
+// The block's per-field minimum / maximum (4 + 4 ints) into rec[0..8).  Every
+// thread of the block must call it; neutral values come from threads without keys.
+__device__ inline void block_minmax_record(int (&mn)[4], int (&mx)[4], int32_t* rec) {
+    __shared__ int32_t red[8];
+    if (threadIdx.x < 8) red[threadIdx.x] = threadIdx.x < 4 ? 0x7fffffff : (int32_t)0x80000000;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            mn[d] = min(mn[d], __shfl_xor(mn[d], o, 64));
+            mx[d] = max(mx[d], __shfl_xor(mx[d], o, 64));
+        }
+    }
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            atomicMin(&red[d], mn[d]);  // LDS
+            atomicMax(&red[4 + d], mx[d]);
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < 8) rec[threadIdx.x] = red[threadIdx.x];
+}
+
 // --- hash tables (hash_sort_scan.hip) ----------------------------------------
 // Clear the header (status, counters, key statistics) and a table's key slots.
 void launch_clear(hipStream_t s, Header* h, Table t, bool clear_header);
@@ -47,10 +88,12 @@ void launch_table_build(hipStream_t s, Header* h, Table t, const int32_t* coords
 void launch_table_lookup(hipStream_t s, Table t, const int32_t* q, int64_t nq, int32_t* idx);
 
 // --- radix sort of packed voxel keys (hash_sort_scan.hip) ---------------------
-// Sorts keys[0..*count) ascending.  The keys are first compacted (per-field
-// minimum subtracted, fields packed into the fewest bits), then sorted with
-// 8-bit LSD passes; passes beyond the significant bits do nothing.  The result
-// is read back with sorted_key() from whichever buffer holds it.
+// Sorts keys a[0..*count) ascending.  The per-field minima and maxima come from
+// partial records (4 minima + 4 maxima each) written by the producer of the keys
+// (nparts of them) or, with nparts = 0, by the sort itself; the keys are then
+// compacted (minimum subtracted, fields packed into the fewest bits) and sorted
+// with stable 8-bit LSD passes; passes beyond the significant bits do nothing.
+// The result is read back with sorted_key() from whichever buffer holds it.
 struct SortStats {
     int32_t fmin[4];    // per-field minimum of the keys being sorted (b, x, y, z)
     int32_t fmax[4];
@@ -61,11 +104,14 @@ struct SortBufs {
     uint64_t* a;       // [cap] input keys / ping
     uint64_t* b;       // [cap] pong
     uint32_t* hist;    // [256 * nblocks(cap)]
+    int32_t* part;     // [sort_part_records(cap)][8] partial min / max records
     SortStats* st;
 };
 void plan_sort_ws(Arena& a, SortBufs& sb, int64_t cap);
 size_t sort_hist_entries(int64_t cap);
-void launch_sort_keys(hipStream_t s, SortBufs bufs, const int64_t* count_dev, int64_t cap);
+// records a producer with blocks of kAppendThreads over cap items may write
+size_t sort_part_records(int64_t cap);
+void launch_sort_keys(hipStream_t s, SortBufs bufs, const int64_t* count_dev, int64_t cap, uint32_t nparts);
 // the sorted key of rank r (decompacted), valid after launch_sort_keys
 __device__ inline uint64_t sorted_key(const SortBufs& sb, int64_t r) {
     const SortStats* st = sb.st;
@@ -114,17 +160,24 @@ struct KmapWs {
     Table fine;         // table of the input coords (assigned by the caller when shared)
     Table coarse;       // stride 2: table of the output coords
     SortBufs sort;      // stride 2: coarse key sort
-    uint32_t* mask;     // [m_cap] offsets present per output
+    uint32_t* mask;     // [m_cap] offsets present per output (stride 2)
     uint32_t* bcnt;     // [K3 * nblk] per-block per-offset counts (k-major)
     uint32_t* bbase;    // [K3 * nblk + 1]
+    int32_t* scan_tmp;  // [scan_tmp_entries(K3 * nblk)]
     int64_t* m_out;     // device count of outputs
+    int32_t* nbr;       // K = 3: [m_cap][27] neighbour table i + 1 (0 = none)
 };
-void plan_kmap_ws(Arena& a, KmapWs& w, int64_t m_cap, int K, int stride, bool own_fine_table);
+// own_nbr: reserve the 3x3x3 neighbour table here (otherwise the caller assigns w.nbr)
+void plan_kmap_ws(Arena& a, KmapWs& w, int64_t m_cap, int K, int stride, bool own_fine_table, bool own_nbr);
 // build_fine: clear + insert the input coords into w.fine first (otherwise the
 // table must already map every input coordinate to its row)
 void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const int32_t* in_coords,
                        const int64_t* m_in_dev, int64_t m_cap, int K, int stride, int32_t* out_coords,
                        int64_t* m_out_dev, int32_t* off, int32_t* pairs, int64_t pair_cap);
+// submanifold 3x3x3 neighbour table only (pass 1, no pairs): nbr[j][k] = i + 1,
+// 0 where offset k of voxel j holds no voxel; w.fine must map every coordinate
+void launch_kernel_map_nbr(hipStream_t s, const KmapWs& w, const int32_t* coords, const int64_t* m_dev,
+                           int64_t m_cap, int32_t* nbr);
 
 // --- sparse conv (conv.hip) ----------------------------------------------------
 // Two MFMA kernels share one plan.

@@ -25,43 +25,51 @@ void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n) {
     w.scan_tmp = a.take<int32_t>(scan_tmp_entries(nn));
 }
 
-// Eq. 1 per point, then hash insert.  Invalid points get kEmpty and a status flag.
-__global__ void k_vox_insert(Header* h, Table t, uint64_t* ukeys, uint64_t* pkey, const float* xyz,
-                             const int32_t* batch, int64_t n, float v) {
-    int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    if (k >= n) return;
-    float p[3] = {xyz[3 * k], xyz[3 * k + 1], xyz[3 * k + 2]};
-    int b = batch ? batch[k] : 0;
-    bool finite = isfinite(p[0]) && isfinite(p[1]) && isfinite(p[2]);
-    bool inrange = b >= 0 && b <= kBatchMax;
+// Eq. 1 per point, then hash insert.  Invalid points get kEmpty and a status
+// flag.  The block appends the keys it created to the unique-key list (one
+// counter atomic per block) and records their per-field min / max for the sort.
+__global__ __launch_bounds__(kAppendThreads) void k_vox_insert(Header* h, Table t, SortBufs sb, uint64_t* pkey,
+                                                               const float* xyz, const int32_t* batch, int64_t n,
+                                                               float v) {
+    const int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    bool created = false;
+    uint64_t key = kEmpty;
     int q[3] = {0, 0, 0};
+    int b = 0;
+    if (k < n) {
+        const float p[3] = {xyz[3 * k], xyz[3 * k + 1], xyz[3 * k + 2]};
+        b = batch ? batch[k] : 0;
+        const bool finite = isfinite(p[0]) && isfinite(p[1]) && isfinite(p[2]);
+        bool inrange = b >= 0 && b <= kBatchMax;
 #pragma unroll
-    for (int d = 0; d < 3; ++d) {
-        float a = p[d] / v;  // IEEE single-precision, correctly rounded
-        float f = floorf(a);
-        inrange = inrange && isfinite(a) && f >= (float)kCoordMin && f <= (float)kCoordMax;
-        q[d] = inrange ? (int)f : 0;
+        for (int d = 0; d < 3; ++d) {
+            const float a = p[d] / v;  // IEEE single-precision, correctly rounded
+            const float f = floorf(a);
+            inrange = inrange && isfinite(a) && f >= (float)kCoordMin && f <= (float)kCoordMax;
+            q[d] = inrange ? (int)f : 0;
+        }
+        if (!finite) {
+            raise_flag(h, kFlagNonfinite);
+        } else if (!inrange) {
+            raise_flag(h, kFlagRange);
+        } else {
+            key = pack_key(b, q[0], q[1], q[2]);
+            uint32_t slot;
+            const int r = table_insert(t, key, &slot);
+            created = r > 0;
+            if (r < 0) raise_flag(h, kFlagTableFull);
+        }
+        pkey[k] = key;
     }
-    if (!finite) {
-        raise_flag(h, kFlagNonfinite);
-        pkey[k] = kEmpty;
-        return;
+    int mn[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
+    int mx[4] = {(int)0x80000000, (int)0x80000000, (int)0x80000000, (int)0x80000000};
+    if (created) {
+        const int f[4] = {b, q[0], q[1], q[2]};
+#pragma unroll
+        for (int d = 0; d < 4; ++d) mn[d] = mx[d] = f[d];
     }
-    if (!inrange) {
-        raise_flag(h, kFlagRange);
-        pkey[k] = kEmpty;
-        return;
-    }
-    uint64_t key = pack_key(b, q[0], q[1], q[2]);
-    pkey[k] = key;
-    uint32_t slot;
-    int r = table_insert(t, key, &slot);
-    if (r > 0) {
-        unsigned long long idx = atomicAdd((unsigned long long*)&h->m, 1ull);
-        ukeys[idx] = key;
-    } else if (r < 0) {
-        raise_flag(h, kFlagTableFull);
-    }
+    block_append(created, key, sb.a, &h->m);
+    block_minmax_record(mn, mx, sb.part + 8 * blockIdx.x);
 }
 
 // rank -> table value, voxel coordinates, zeroed counters
@@ -161,8 +169,9 @@ void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const
                      float voxel_size, const void* feat, int32_t C, int dt, int32_t* coords, void* vfeat,
                      int32_t* counts, int32_t* pt2vox, int64_t* m_dev) {
     launch_clear(s, w.h, w.table, true);
-    if (n > 0) k_vox_insert<<<blocks_for(n, 256), 256, 0, s>>>(w.h, w.table, w.sort.a, w.pkey, xyz, batch, n, voxel_size);
-    launch_sort_keys(s, w.sort, &w.h->m, n);
+    const unsigned nins = n > 0 ? blocks_for(n, kAppendThreads) : 0u;
+    if (n > 0) k_vox_insert<<<nins, kAppendThreads, 0, s>>>(w.h, w.table, w.sort, w.pkey, xyz, batch, n, voxel_size);
+    launch_sort_keys(s, w.sort, &w.h->m, n, nins);
     k_vox_rank<<<blocks_for(n, 256), 256, 0, s>>>(w.h, w.sort, w.table, coords, counts, w.fill, n, m_dev);
     if (n == 0) return;
     k_vox_lookup<<<blocks_for(n, 256), 256, 0, s>>>(w.table, w.pkey, n, pt2vox, counts);

@@ -311,6 +311,26 @@ def test_devox_sweep(spv, sweep, mode, dtype, C):
     check_close(host(out, dtype)[:len(pts)], rout, dtype)
 
 
+@pytest.mark.parametrize("C,Cp,n", [(16, 0, 1000), (64, 24, 3001), (128, 128, 2047), (256, 96, 1500), (32, 8, 1)])
+def test_devox_shapes(spv, C, Cp, n):
+    """Channel widths with and without a point branch, partial 32-channel slabs
+    of the point MLP, widths past the matrix-core kernel and ragged point counts."""
+    rng = np.random.default_rng(C + Cp + n)
+    pts = rng.uniform(-1.0, 1.0, size=(n, 3)).astype(np.float32)
+    rc, _, _, _ = oracle.voxelize(pts, 0.1)
+    vf = synth.normal((len(rc), C), 31, dtype="bf16")
+    pf = synth.normal((n, Cp), 32, dtype="bf16") if Cp else None
+    Wp = synth.linear_weight(Cp, C, 33, "bf16") if Cp else None
+    sc, sh = synth.folded_bn(C, 34)
+    ws = spv.Workspace.for_ops(n, max(C, Cp))
+    out = spv.spv_devoxelize(ws, dev(rc), dev(vf, "bf16"), dev(pts), 0.1,
+                             pfeat=None if pf is None else dev(pf, "bf16"), Wp=None if Wp is None else dev(Wp, "bf16"),
+                             scale_p=dev(sc) if Cp else None, shift_p=dev(sh) if Cp else None, relu_p=bool(Cp))
+    ref = oracle.devoxelize(rc, vf, pts, 0.1, pfeat=pf, Wp=Wp, scale_p=sc if Cp else None,
+                            shift_p=sh if Cp else None, relu_p=bool(Cp), dtype="bf16")
+    check_close(host(out, "bf16")[:n], ref, "bf16")
+
+
 def test_devox_coarse_grid(spv, sweep):
     pts = sweep[::4]
     rc, _, _, _ = oracle.voxelize(pts, 0.05)
