@@ -77,7 +77,7 @@ constexpr int kSortThreads = 256;
 constexpr int kSortItems = 8;
 constexpr int kSortTile = kSortThreads * kSortItems;
 constexpr int kSortParts = 256;            // partial records of the stand-alone min / max kernel
-constexpr uint32_t kFusedSortBlocks = 1024;  // up to this many tiles a scatter block scans the histograms itself
+constexpr uint32_t kFusedSortBlocks = 256;  // up to this many tiles a scatter block scans the histograms itself
 
 size_t sort_hist_entries(int64_t cap) { return (size_t)256 * blocks_for(cap, kSortTile); }
 size_t sort_part_records(int64_t cap) {
@@ -162,10 +162,22 @@ __global__ __launch_bounds__(256) void k_sort_stats(SortStats* st, const int32_t
     }
 }
 
+// lanes of this wave whose `valid` digit d equals this lane's (8 ballots)
+__device__ inline uint64_t digit_peers(uint32_t d, bool valid) {
+    uint64_t peers = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+        const uint64_t bal = __ballot((d >> b) & 1);
+        peers &= ((d >> b) & 1) ? bal : ~bal;
+    }
+    return peers;
+}
+
 // Histogram of one 8-bit digit per tile.  Pass 0 first replaces every key by
 // its compacted form (per-field minimum subtracted, fields packed into their
 // bit widths) in place; it runs even when there is nothing to sort so that the
-// buffer read back always holds compacted keys.
+// buffer read back always holds compacted keys.  Lanes of a wave holding the
+// same digit are counted by one LDS add of their leader.
 __global__ __launch_bounds__(kSortThreads) void k_radix_hist(const SortStats* st, SortBufs sb, const int64_t* count_dev,
                                                              int64_t cap, int pass) {
     const uint32_t nblk = gridDim.x;
@@ -173,6 +185,8 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_hist(const SortStats* st
     uint64_t* src = (pass & 1) ? sb.b : sb.a;
     __shared__ uint32_t hist[256];
     hist[threadIdx.x] = 0;
+    const int lane = threadIdx.x & 63;
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     const int64_t count = clamp_count(count_dev, cap);
     const int64_t base = (int64_t)blockIdx.x * kSortTile;
     uint64_t key[kSortItems];
@@ -205,44 +219,50 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_hist(const SortStats* st
 #pragma unroll
     for (int r = 0; r < kSortItems; ++r) {
         const int64_t i = base + r * kSortThreads + threadIdx.x;
-        if (i < count) atomicAdd(&hist[(key[r] >> (8 * pass)) & 0xFF], 1u);
+        const bool valid = i < count;
+        const uint32_t d = (uint32_t)(key[r] >> (8 * pass)) & 0xFF;
+        const uint64_t peers = digit_peers(d, valid);
+        if (valid && (peers & lt) == 0) atomicAdd(&hist[d], (uint32_t)__popcll(peers));
     }
     __syncthreads();
-    sb.hist[threadIdx.x * nblk + blockIdx.x] = hist[threadIdx.x];
+    sb.hist[(size_t)blockIdx.x * 256 + threadIdx.x] = hist[threadIdx.x];  // tile-major
 }
 
-// exclusive scan of the digit-major histogram by one block (many-tile sorts)
-__global__ __launch_bounds__(1024) void k_radix_scan(const SortStats* st, uint32_t* hist, uint32_t n, int pass) {
+// Many-tile sorts: one block turns the tile-major histograms into write offsets
+// in place (thread d walks digit d over the tiles, then the digit totals are
+// scanned and added).
+__global__ __launch_bounds__(256) void k_radix_scan(const SortStats* st, uint32_t* hist, uint32_t nblk, int pass) {
     if ((uint32_t)(8 * pass) >= st->sort_bits) return;
-    __shared__ int lds[17];
-    uint32_t per = (n + blockDim.x - 1) / blockDim.x;
-    uint32_t lo = threadIdx.x * per, hi = min(n, lo + per);
-    int s = 0;
-    for (uint32_t i = lo; i < hi; ++i) s += (int)hist[i];
-    int tot;
-    int run = block_exclusive_scan(s, lds, &tot);
-    for (uint32_t i = lo; i < hi; ++i) {
-        uint32_t v = hist[i];
-        hist[i] = (uint32_t)run;
-        run += (int)v;
+    __shared__ int lds[5];
+    const int t = threadIdx.x;
+    uint32_t run = 0;
+    for (uint32_t b = 0; b < nblk; ++b) {
+        const uint32_t v = hist[(size_t)b * 256 + t];
+        hist[(size_t)b * 256 + t] = run;
+        run += v;
     }
+    int all;
+    const uint32_t dbase = (uint32_t)block_exclusive_scan((int)run, lds, &all);
+    for (uint32_t b = 0; b < nblk; ++b) hist[(size_t)b * 256 + t] += dbase;
 }
 
 // Stable scatter of one tile by one digit.  With `fused`, the block derives its
 // digit offsets from the raw histograms (thread d: all tiles' counts of digit d,
 // those of earlier tiles, then a scan over the digits); otherwise k_radix_scan
-// has already turned the histograms into offsets.
+// has already turned the histograms into offsets.  Inside the tile, items are
+// ranked in (round, wave, lane) order -- the index order -- from per-wave digit
+// groups: counts of every (round, wave, digit) first, then one running sum per
+// digit over them, then every item is written.
 __global__ __launch_bounds__(kSortThreads) void k_radix_scatter(const SortStats* st, SortBufs sb,
                                                                 const int64_t* count_dev, int64_t cap, int pass,
                                                                 int fused) {
+    constexpr int NWV = kSortThreads / 64;
     const uint32_t nblk = gridDim.x;
     if ((uint32_t)(8 * pass) >= st->sort_bits) return;
     const uint64_t* src = (pass & 1) ? sb.b : sb.a;
     uint64_t* dst = (pass & 1) ? sb.a : sb.b;
-    __shared__ uint32_t run[256];
-    __shared__ uint32_t wcnt[kSortThreads / 64][256];
-    __shared__ uint32_t woff[kSortThreads / 64][256];
-    __shared__ int lds[kSortThreads / 64 + 1];
+    __shared__ uint32_t cnt[kSortItems][NWV][256];  // counts, then write offsets
+    __shared__ int lds[NWV + 1];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int64_t count = clamp_count(count_dev, cap);
     const int64_t base = (int64_t)blockIdx.x * kSortTile;
@@ -252,51 +272,54 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_scatter(const SortStats*
         const int64_t i = base + r * kSortThreads + t;
         keys[r] = i < count ? src[i] : 0ull;
     }
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r)
+#pragma unroll
+        for (int w = 0; w < NWV; ++w) cnt[r][w][t] = 0;
+    uint32_t run;
     if (fused) {
-        const uint32_t* hd = sb.hist + (size_t)t * nblk;
         uint32_t tot = 0, pre = 0;
 #pragma unroll 8
         for (uint32_t b = 0; b < nblk; ++b) {
-            const uint32_t v = hd[b];
+            const uint32_t v = sb.hist[(size_t)b * 256 + t];  // coalesced over the digits
             tot += v;
             pre += (b < blockIdx.x) ? v : 0u;
         }
         int all;
-        run[t] = (uint32_t)block_exclusive_scan((int)tot, lds, &all) + pre;
+        run = (uint32_t)block_exclusive_scan((int)tot, lds, &all) + pre;
     } else {
-        run[t] = sb.hist[t * nblk + blockIdx.x];
+        run = sb.hist[(size_t)blockIdx.x * 256 + t];
+        __syncthreads();
     }
-    for (int w = 0; w < kSortThreads / 64; ++w) wcnt[w][t] = 0;
-    __syncthreads();
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    uint32_t rank[kSortItems];
 #pragma unroll
     for (int r = 0; r < kSortItems; ++r) {
         const int64_t i = base + r * kSortThreads + t;
         const bool valid = i < count;
-        const uint64_t key = keys[r];
-        const uint32_t d = (uint32_t)(key >> (8 * pass)) & 0xFF;
-        // lanes of this wave holding the same digit
-        uint64_t peers = __ballot(valid);
+        const uint32_t d = (uint32_t)(keys[r] >> (8 * pass)) & 0xFF;
+        const uint64_t peers = digit_peers(d, valid);
+        rank[r] = (uint32_t)__popcll(peers & lt);
+        if (valid && rank[r] == 0) cnt[r][wave][d] = (uint32_t)__popcll(peers);
+    }
+    __syncthreads();
+    // thread t owns digit t: running offsets over (round, wave) in index order
 #pragma unroll
-        for (int b = 0; b < 8; ++b) {
-            const uint64_t bal = __ballot((d >> b) & 1);
-            peers &= ((d >> b) & 1) ? bal : ~bal;
+    for (int r = 0; r < kSortItems; ++r)
+#pragma unroll
+        for (int w = 0; w < NWV; ++w) {
+            const uint32_t c = cnt[r][w][t];
+            cnt[r][w][t] = run;
+            run += c;
         }
-        const uint32_t rank = (uint32_t)__popcll(peers & lt);
-        if (valid && rank == 0) wcnt[wave][d] = (uint32_t)__popcll(peers);
-        __syncthreads();
-        {
-            uint32_t b0 = run[t];
-            for (int w = 0; w < kSortThreads / 64; ++w) {
-                const uint32_t c = wcnt[w][t];
-                woff[w][t] = b0;
-                b0 += c;
-                wcnt[w][t] = 0;
-            }
-            run[t] = b0;
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+        const int64_t i = base + r * kSortThreads + t;
+        if (i < count) {
+            const uint32_t d = (uint32_t)(keys[r] >> (8 * pass)) & 0xFF;
+            dst[cnt[r][wave][d] + rank[r]] = keys[r];
         }
-        __syncthreads();
-        if (valid) dst[woff[wave][d] + rank] = key;
     }
 }
 
@@ -313,7 +336,7 @@ void launch_sort_keys(hipStream_t s, SortBufs sb, const int64_t* count_dev, int6
     const int fused = nblk <= kFusedSortBlocks ? 1 : 0;
     for (int pass = 0; pass < 8; ++pass) {
         k_radix_hist<<<nblk, kSortThreads, 0, s>>>(sb.st, sb, count_dev, cap, pass);
-        if (!fused) k_radix_scan<<<1, 1024, 0, s>>>(sb.st, sb.hist, 256 * nblk, pass);
+        if (!fused) k_radix_scan<<<1, 256, 0, s>>>(sb.st, sb.hist, nblk, pass);
         k_radix_scatter<<<nblk, kSortThreads, 0, s>>>(sb.st, sb, count_dev, cap, pass, fused);
     }
 }

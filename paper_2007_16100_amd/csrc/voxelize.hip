@@ -109,7 +109,18 @@ __global__ void k_vox_fill(const int32_t* pt2vox, int64_t n, const int32_t* seg,
     plist[pos] = (int32_t)k;
 }
 
-// Eq. 2: one thread per (voxel, VEC consecutive channels); sums its points in fp32
+// fp64 -> fp32 rounding to odd: a following round-to-nearest-even to a format
+// with at most 22 fraction bits then rounds the fp64 value exactly once
+__device__ inline float f64_to_f32_odd(double d) {
+    float f = __double2float_rz(d);
+    if ((double)f != d) f = __uint_as_float(__float_as_uint(f) | 1u);
+    return f;
+}
+
+// Eq. 2: one thread per (voxel, VEC consecutive channels).  The points are
+// summed in fp64 -- exact for 16-bit features of ordinary range, so the result
+// does not depend on the order in which they were grouped -- and the mean is
+// rounded once to the storage type.
 template <int DT, int VEC>
 __global__ void k_vox_mean(const Header* h, int64_t cap, const int32_t* seg, const int32_t* plist, const void* feat,
                            int C, void* vfeat) {
@@ -121,9 +132,9 @@ __global__ void k_vox_mean(const Header* h, int64_t cap, const int32_t* seg, con
     int ch = (int)(t - vox * nch) * VEC;
     if (vox >= m) return;
     int32_t lo = seg[vox], hi = seg[vox + 1];
-    float acc[VEC];
+    double acc[VEC];
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
+    for (int j = 0; j < VEC; ++j) acc[j] = 0.0;
     for (int32_t p = lo; p < hi; ++p) {
         int64_t row = (int64_t)plist[p] * C + ch;
         if constexpr (VEC == 8) {
@@ -131,31 +142,34 @@ __global__ void k_vox_mean(const Header* h, int64_t cap, const int32_t* seg, con
             uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                acc[2 * j] += from16<DT>(w[j] & 0xFFFF);
-                acc[2 * j + 1] += from16<DT>(w[j] >> 16);
+                acc[2 * j] += (double)from16<DT>(w[j] & 0xFFFF);
+                acc[2 * j + 1] += (double)from16<DT>(w[j] >> 16);
             }
         } else if constexpr (VEC == 4) {
             float4 f = *(const float4*)((const float*)feat + row);
-            acc[0] += f.x;
-            acc[1] += f.y;
-            acc[2] += f.z;
-            acc[3] += f.w;
+            acc[0] += (double)f.x;
+            acc[1] += (double)f.y;
+            acc[2] += (double)f.z;
+            acc[3] += (double)f.w;
         } else {
-            acc[0] += ld_feat<DT>(feat, row);
+            acc[0] += (double)ld_feat<DT>(feat, row);
         }
     }
-    const float N = (float)(hi - lo);
+    const double N = (double)(hi - lo);
     int64_t orow = vox * C + ch;
     if constexpr (VEC == 8) {
         uint32_t w[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            w[j] = (uint32_t)to16<DT>(acc[2 * j] / N) | ((uint32_t)to16<DT>(acc[2 * j + 1] / N) << 16);
+            w[j] = (uint32_t)to16<DT>(f64_to_f32_odd(acc[2 * j] / N)) |
+                   ((uint32_t)to16<DT>(f64_to_f32_odd(acc[2 * j + 1] / N)) << 16);
         *(uint4*)((uint16_t*)vfeat + orow) = make_uint4(w[0], w[1], w[2], w[3]);
     } else if constexpr (VEC == 4) {
-        *(float4*)((float*)vfeat + orow) = make_float4(acc[0] / N, acc[1] / N, acc[2] / N, acc[3] / N);
+        *(float4*)((float*)vfeat + orow) =
+            make_float4((float)(acc[0] / N), (float)(acc[1] / N), (float)(acc[2] / N), (float)(acc[3] / N));
     } else {
-        st_feat<DT>(vfeat, orow, acc[0] / N);
+        if constexpr (DT == SPV_F32) st_feat<DT>(vfeat, orow, (float)(acc[0] / N));
+        else st_feat<DT>(vfeat, orow, f64_to_f32_odd(acc[0] / N));
     }
 }
 

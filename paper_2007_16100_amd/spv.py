@@ -233,19 +233,27 @@ def spv_devoxelize(ws: Workspace, grid_coords: torch.Tensor, vfeat: torch.Tensor
 
 def make_block_params(C: int, dtype: torch.dtype, voxel_size: float, convs: Sequence, Wp: torch.Tensor,
                       scale_p=None, shift_p=None, relu_p: bool = True, mode: int = SPV_DEVOX_CENTER) -> BlockParams:
-    """convs: list of (W [27,C,C], scale|None, shift|None, relu) device tensors (kept alive by the caller)."""
+    """convs: list of (W [27,C,C], scale|None, shift|None, relu) device tensors.
+
+    The struct holds raw device pointers; it also keeps references to every
+    tensor it points into, so they stay allocated as long as the struct lives."""
+    def ptr(t):
+        return None if t is None else _ptr(t).value
     p = BlockParams()
     p.C, p.dtype, p.voxel_size, p.n_convs = C, _DT[dtype], voxel_size, len(convs)
+    keep = [Wp, scale_p, shift_p]
     for l, (W, sc, sh, r) in enumerate(convs):
-        p.W[l] = W.data_ptr()
-        p.scale[l] = sc.data_ptr() if sc is not None else None
-        p.shift[l] = sh.data_ptr() if sh is not None else None
+        p.W[l] = ptr(W)
+        p.scale[l] = ptr(sc)
+        p.shift[l] = ptr(sh)
         p.relu[l] = int(r)
-    p.Wp = Wp.data_ptr()
-    p.scale_p = scale_p.data_ptr() if scale_p is not None else None
-    p.shift_p = shift_p.data_ptr() if shift_p is not None else None
+        keep += [W, sc, sh]
+    p.Wp = ptr(Wp)
+    p.scale_p = ptr(scale_p)
+    p.shift_p = ptr(shift_p)
     p.relu_p = int(relu_p)
     p.devox_mode = mode
+    p._keep = keep
     return p
 
 

@@ -129,6 +129,31 @@ def test_voxelize_edge_cases(spv, case):
     check_close(vf, rvf, dtype)
 
 
+def test_voxelize_many_tiles(spv):
+    """Over 524k distinct voxels: the sort's offsets come from the separate
+    histogram scan instead of the scatter's own."""
+    rng = np.random.default_rng(4242)
+    xyz = rng.uniform(-60.0, 60.0, size=(700_000, 3)).astype(np.float32)
+    xyz[::7] = xyz[1::7][: len(xyz[::7])]  # some shared voxels
+    c, vf, cnt, p2v, _ = run_voxelize(spv, xyz, 0.05, synth.normal((len(xyz), 8), 9, dtype="bf16"), "bf16")
+    rc, rvf, rcnt, rp2v = oracle.voxelize(xyz, 0.05, synth.normal((len(xyz), 8), 9, dtype="bf16"), "bf16")
+    assert len(rc) > 524288
+    np.testing.assert_array_equal(c, rc)
+    np.testing.assert_array_equal(cnt, rcnt)
+    np.testing.assert_array_equal(p2v, rp2v)
+    check_close(vf, rvf, "bf16")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+def test_voxelize_mean_bit_exact(spv, sweep, dtype):
+    """The scatter-mean sums in fp64 (exact for these features) and rounds once,
+    as the oracle does, so voxel features agree bit for bit."""
+    feat = synth.normal((len(sweep), 32), 1011, dtype=dtype)
+    _, vf, _, _, _ = run_voxelize(spv, sweep, 0.05, feat, dtype)
+    _, rvf, _, _ = oracle.voxelize(sweep, 0.05, feat, dtype)
+    np.testing.assert_array_equal(vf, rvf)
+
+
 def test_voxelize_device_errors(spv):
     xyz = np.zeros((100, 3), np.float32)
     xyz[17, 1] = np.nan
@@ -381,3 +406,37 @@ def test_block(spv, cfg):
     rout, rm = oracle.block(xyz, feat, v, convs, Wp, scp, shp, relu_p=True, dtype=dtype)
     assert m == rm
     check_close(host(out, dtype)[:len(xyz)], rout, dtype)
+
+
+def test_block_graph_replay(spv, sweep):
+    """spv_block captured into a graph: every replay, with eager work and
+    synchronization between them, reproduces the eager result bit for bit."""
+    C = 32
+    xyz = sweep
+    feat = synth.normal((len(xyz), C), 61, dtype="bf16")
+    convs = []
+    for l in range(2):
+        sc, sh = synth.folded_bn(C, 62 + l)
+        convs.append((dev(synth.conv_weight(27, C, C, 64 + l, "bf16"), "bf16"), dev(sc), dev(sh), True))
+    scp, shp = synth.folded_bn(C, 66)
+    params = spv.make_block_params(C, torch.bfloat16, 0.05, convs, dev(synth.linear_weight(C, C, 67, "bf16"), "bf16"),
+                                   dev(scp), dev(shp), relu_p=True)
+    d_xyz, d_feat = dev(xyz), dev(feat, "bf16")
+    ws = spv.Workspace.for_block(len(xyz), C)
+    out = torch.empty((len(xyz), C), dtype=torch.bfloat16, device="cuda")
+    spv.spv_block(ws, params, d_xyz, d_feat, out=out)
+    torch.cuda.synchronize()
+    ref = out.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        spv.spv_block(ws, params, d_xyz, d_feat, out=out)
+    torch.cuda.synchronize()
+    scratch = torch.empty_like(out)
+    for i in range(3):
+        out.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), ref.view(torch.int16)), f"replay {i}"
+        spv.spv_block(ws, params, d_xyz, d_feat, out=scratch)  # eager work between replays
+        torch.cuda.synchronize()
+        assert torch.equal(scratch.view(torch.int16), ref.view(torch.int16)), f"eager after replay {i}"
