@@ -18,45 +18,35 @@ __device__ __forceinline__ void static_for(F&& f) {
 // ---------------------------------------------------------------------------
 // neighbour-table kernel (3x3x3 maps)
 // ---------------------------------------------------------------------------
-// Workgroup = 4 waves; wave w owns RB blocks of 16 output rows and all output
-// channels (NB blocks of 16).  The accumulators of a block are D = W^T G^T
-// fragments: lane (r16, g) holds output channels nb*16 + 4g .. 4g+3 of row r16,
-// which is also the order in which they are stored.
+// One workgroup of NW waves per CU; wave w owns RB blocks of 16 output rows and
+// all output channels (NB blocks of 16).  The accumulators of a block are
+// D = W^T G^T fragments: lane (r16, g) holds output channels nb*16 + 4g .. 4g+3
+// of row r16, which is also the order in which they are stored.
 //
-// Step k of the fully unrolled offset loop
-//   (1) writes to LDS buffer (k+2) % 4 this wave's share of W[k+2], loaded
-//       into registers during step k-1, and waits for its LDS writes;
-//   (2) barrier: every wave has written W[k+2] and finished reading the buffer
-//       about to be reused;
-//   (3) loads its share of W[k+3] into registers, the neighbour indices of
-//       offset k+3 and the gathered rows of offset k+2;
-//   (4) multiplies the rows gathered for offset k by W[k], read from LDS buffer
-//       k % 4 one 32-channel slab at a time; blocks without a neighbour at
-//       offset k skip it.
-// Every load has one or two steps of matrix work to arrive in.  All loads are
-// ordinary vector-memory loads the compiler sees, so its waits (which count
-// outstanding loads in issue order) stay exact: with a global->LDS copy in
-// flight it would instead wait for every load at the next use of any of them.
-constexpr int kUnionWaves = 4;
+// The 27 offsets run in phases of PH: at the start of a phase the workgroup
+// copies W of the phase's offsets into LDS (one barrier before, one after);
+// inside a phase the waves never synchronize and load no weights, each one
+// streaming its own rows:
+//   step k: loads the neighbour indices of offset k+3 and gathers the rows of
+//           offset k+1 (a block with no neighbour at that offset loads
+//           nothing; a lane whose row has none gets zeros), then multiplies the
+//           rows gathered for offset k by W[k] one 32-channel slab at a time,
+//           skipping blocks without a neighbour at k.
+// All loads are ordinary vector-memory loads the compiler sees, so its waits
+// (which count outstanding loads in issue order) stay exact.
 constexpr int kUK3 = 27;
-constexpr int kWAhead = 3;  // weight loads: steps ahead (ring of kWAhead + 1 LDS buffers)
 constexpr int kNAhead = 3;  // neighbour indices: steps ahead
 constexpr int kRAhead = 1;  // gathered rows: steps ahead
 
-template <int DT, int KCH, int NB, int RB, int FULL>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_conv_union(
+template <int DT, int KCH, int NB, int RB, int NW, int PH>
+__global__ __launch_bounds__(64 * NW) void k_conv_union(
     const int32_t* __restrict__ nbr, const int64_t* __restrict__ m_out_dev, int64_t m_cap,
     const uint16_t* __restrict__ in, int Cin, int64_t in_rows, const uint4* __restrict__ wpack,
     const float* __restrict__ scale, const float* __restrict__ shift, int relu, uint16_t* __restrict__ out) {
     constexpr int K3 = kUK3;
     constexpr int FR = KCH * NB;  // 1 KB weight fragments per offset
     constexpr int Cout = NB * 16;
-    constexpr int NF = (FR + kUnionWaves - 1) / kUnionWaves;  // fragments per wave and offset
-    __shared__ __align__(16) uint4 wb0[FR * 64];
-    __shared__ __align__(16) uint4 wb1[FR * 64];
-    __shared__ __align__(16) uint4 wb2[FR * 64];
-    __shared__ __align__(16) uint4 wb3[FR * 64];
-    auto wbuf = [&](int i) __attribute__((always_inline)) -> uint4* { return i == 0 ? wb0 : (i == 1 ? wb1 : (i == 2 ? wb2 : wb3)); };
+    __shared__ __align__(16) uint4 wl[PH * FR * 64];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -67,18 +57,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
     // capacity the grid was sized for) are split into 8 consecutive ranges, one
     // per XCD, so neighbouring tiles share an L2 and every XCD gets work.
     const int64_t m = clamp_rows(m_out_dev, m_cap);
-    constexpr int64_t rows_wg = kUnionWaves * RB * 16;
+    constexpr int64_t rows_wg = (int64_t)NW * RB * 16;
     const int64_t bid = blockIdx.x, x = bid % 8, seq = bid / 8;
     const int64_t ga = (m + rows_wg - 1) / rows_wg, xq = ga / 8, xr = ga % 8;
     if (seq >= xq + (x < xr ? 1 : 0)) return;  // the whole workgroup
     const int64_t wg = x * xq + (x < xr ? x : xr) + seq;
-    const int64_t blk0 = (wg * kUnionWaves + wave) * RB;
+    const int64_t blk0 = (wg * NW + wave) * RB;
 
     const __amdgpu_buffer_rsrc_t nb_rs = make_rsrc(nbr, (uint32_t)(m * K3 * 4));
     const uint32_t row_bytes = (uint32_t)Cin * 2u;
     const __amdgpu_buffer_rsrc_t in_rs = make_rsrc(in, (uint32_t)(in_rows * (int64_t)row_bytes));
     const uint32_t in_rows32 = (uint32_t)in_rows;
-    const int qin = Cin / 8;
 
     // nbr byte offset of (row of block b, offset 0) for this lane; rows past m read zeros
     uint32_t nboff[RB];
@@ -87,27 +76,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
         const int64_t row = (blk0 + b) * 16 + r16;
         nboff[b] = row < m ? (uint32_t)(row * K3 * 4) : kOutOfRange;
     }
-
-    // this wave's share of a weight buffer: fragments wave, wave + 4, ...; every
-    // wave handles the same number (surplus ones repeat the last fragment: the
-    // same bytes to the same place)
-    auto frag_of = [&](int j) __attribute__((always_inline)) { return j * kUnionWaves + wave < FR ? j * kUnionWaves + wave : FR - 1; };
-    // (native vector types: HIP's uint4 struct is copied with memcpy, which keeps
-    // an array of them out of registers)
-    const i32x4* wsrc = (const i32x4*)wpack;
-    auto load_w = [&](int k, i32x4 (&wt)[NF]) __attribute__((always_inline)) {
-#pragma unroll
-        for (int j = 0; j < NF; ++j) wt[j] = wsrc[((int64_t)k * FR + frag_of(j)) * 64 + lane];
-    };
-    auto store_w = [&](uint4* dst, const i32x4 (&wt)[NF]) __attribute__((always_inline)) {
-#pragma unroll
-        for (int j = 0; j < NF; ++j) ((i32x4*)dst)[frag_of(j) * 64 + lane] = wt[j];
-    };
-    auto load_nbr = [&](int k, int (&dst)[RB]) __attribute__((always_inline)) {
-#pragma unroll
-        for (int b = 0; b < RB; ++b)
-            dst[b] = __builtin_amdgcn_raw_buffer_load_b32(nb_rs, nboff[b] + (uint32_t)k * 4u, 0, 0);
-    };
     // offsets present in each block (union over its 16 rows), wave-uniform
     uint32_t umask[RB];
 #pragma unroll
@@ -124,9 +92,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
         for (int d = 1; d < 64; d <<= 1) bits |= __shfl_xor(bits, d, 64);
         umask[b] = __builtin_amdgcn_readfirstlane(bits);
     }
-    // gathered rows of offset kr: nothing is fetched for a block without a
-    // neighbour at kr (its registers keep stale values the multiply skips) or
-    // for a lane whose row has none (zeros)
+
+    auto load_nbr = [&](int k, int (&dst)[RB]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int b = 0; b < RB; ++b)
+            dst[b] = __builtin_amdgcn_raw_buffer_load_b32(nb_rs, nboff[b] + (uint32_t)k * 4u, 0, 0);
+    };
+    // gathered rows of offset kr (16-byte chunks g + 4 kc of row i)
     auto load_rows = [&](int kr, const int (&nb1)[RB], i32x4 (&dst)[RB][KCH]) __attribute__((always_inline)) {
 #pragma unroll
         for (int b = 0; b < RB; ++b) {
@@ -138,23 +110,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
             if (have) {
                 const uint32_t base = i * row_bytes + (uint32_t)g * 16u;
 #pragma unroll
-                for (int kc = 0; kc < KCH; ++kc) {
-                    uint32_t o = base + kc * 64;
-                    if (!FULL && kc * 4 + g >= qin) o = kOutOfRange;
-                    dst[b][kc] = __builtin_amdgcn_raw_buffer_load_b128(in_rs, o, 0, 0);
-                }
+                for (int kc = 0; kc < KCH; ++kc)
+                    dst[b][kc] = __builtin_amdgcn_raw_buffer_load_b128(in_rs, base + (uint32_t)kc * 64u, 0, 0);
             }
         }
     };
 
-    // prologue: W[0], W[1] into LDS, W[2] in registers, neighbour indices, rows
-    i32x4 wtmp[NF];  // this wave's share of the next weight buffer, between load and LDS write
-#pragma unroll
-    for (int j = 0; j < kWAhead - 1; ++j) {
-        load_w(j, wtmp);
-        store_w(wbuf(j), wtmp);
-    }
-    load_w(kWAhead - 1, wtmp);
     int ns[kNAhead + 1][RB];         // neighbour indices of offset j in slot j % (kNAhead + 1)
     i32x4 rs[kRAhead + 1][RB][KCH];  // gathered rows of offset j in slot j % (kRAhead + 1)
 #pragma unroll
@@ -168,22 +129,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) acc[b][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    const i32x4* wsrc = (const i32x4*)wpack;
     static_for<0, K3>([&](auto kk) __attribute__((always_inline)) {
         constexpr int k = decltype(kk)::value;
-        // (1) this wave's share of W[k+2] into LDS
-        if constexpr (k + kWAhead - 1 < K3) store_w(wbuf((k + kWAhead - 1) % (kWAhead + 1)), wtmp);
-        // (2) a plain barrier after the wave's own LDS writes (a __syncthreads
-        // fence would also wait for every gather in flight)
-        lds_wait();
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-        // (3) loads of later steps
-        if constexpr (k + kWAhead < K3) load_w(k + kWAhead, wtmp);
+        if constexpr (k % PH == 0) {
+            // a new phase: once every wave is done with the previous weights,
+            // copy W[k .. k+PH) into LDS
+            constexpr int nf = (K3 - k < PH ? K3 - k : PH) * FR;
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            for (int f = wave; f < nf; f += NW)
+                ((i32x4*)wl)[f * 64 + lane] = wsrc[((int64_t)k * FR + f) * 64 + lane];
+            lds_wait();
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+        }
         if constexpr (k + kNAhead < K3) load_nbr(k + kNAhead, ns[(k + kNAhead) % (kNAhead + 1)]);
         if constexpr (k + kRAhead < K3)
             load_rows(k + kRAhead, ns[(k + kRAhead) % (kNAhead + 1)], rs[(k + kRAhead) % (kRAhead + 1)]);
-        // (4) multiply offset k, one 32-channel slab of W[k] at a time
-        const uint4* wk = wbuf(k % (kWAhead + 1));
+        const i32x4* wk = (const i32x4*)wl + (k % PH) * FR * 64;
         uint32_t present = 0;
 #pragma unroll
         for (int b = 0; b < RB; ++b) present |= ((umask[b] >> k) & 1u) << b;
@@ -192,7 +156,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
             for (int kc = 0; kc < KCH; ++kc) {
                 i32x4 wf[NB];
 #pragma unroll
-                for (int nb = 0; nb < NB; ++nb) wf[nb] = ((const i32x4*)wk)[(kc * NB + nb) * 64 + lane];
+                for (int nb = 0; nb < NB; ++nb) wf[nb] = wk[(kc * NB + nb) * 64 + lane];
 #pragma unroll
                 for (int b = 0; b < RB; ++b) {
                     if ((present >> b) & 1u) {
@@ -235,15 +199,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
     }
 }
 
-// blocks of 16 rows per wave of the neighbour-table kernel: accumulators
-// (RB*NB), one weight slab (NB) and three stages of gathered rows (3*RB*KCH),
-// in 16-byte registers, within ~52 of them (two waves per SIMD)
-constexpr int union_rb(int KCH, int NB) {
-    for (int rb = 4; rb > 1; --rb)
-        if (rb * NB + NB + (kRAhead + 1) * rb * KCH <= 52) return rb;
-    return 1;
-}
-
 // instantiated for square layers C -> C with C in {32, 64, 96, 128} (the widths
 // of the blocks and networks built here); other shapes use the tile kernel
 bool union_supported(int K3, int Cin, int Cout, int dt) {
@@ -251,15 +206,20 @@ bool union_supported(int K3, int Cin, int Cout, int dt) {
     return Cin == 32 || Cin == 64 || Cin == 96 || Cin == 128;
 }
 
+// Launch shape per width: 12 waves of 2 blocks (384 rows per workgroup, about
+// one workgroup per CU on ~10^5-voxel scans), phases of as many offsets as fit
+// in 128 KB of LDS.
 template <int DT, int KCH>
 static void launch_union_c(hipStream_t s, const ConvPlan& p, const void* in, int64_t in_rows, const void* wpack,
                            const float* scale, const float* shift, int relu, void* out) {
     constexpr int NB = 2 * KCH;  // C = 32 * KCH
-    constexpr int RB = union_rb(KCH, NB);
-    constexpr int64_t rows_wg = (int64_t)kUnionWaves * RB * 16;
+    constexpr int RB = 2, NW = 12;
+    constexpr int FR = KCH * NB;
+    constexpr int PH = (128 / FR) < kUK3 ? (128 / FR) : kUK3;  // 27, 14, 7, 4 for C = 32, 64, 96, 128
+    constexpr int64_t rows_wg = (int64_t)NW * RB * 16;
     // a multiple of 8 workgroups: the kernel spreads the live tiles over the 8 XCDs
     const unsigned grid = (unsigned)(((p.m_cap + rows_wg - 1) / rows_wg + 7) / 8 * 8);
-    k_conv_union<DT, KCH, NB, RB, 1><<<grid, 64 * kUnionWaves, 0, s>>>(
+    k_conv_union<DT, KCH, NB, RB, NW, PH><<<grid, 64 * NW, 0, s>>>(
         p.nbr, p.m_out_dev, p.m_cap, (const uint16_t*)in, 32 * KCH, in_rows, (const uint4*)wpack, scale, shift, relu,
         (uint16_t*)out);
 }
