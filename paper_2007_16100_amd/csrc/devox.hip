@@ -23,14 +23,13 @@ struct Corners {
 };
 
 #pragma clang fp contract(off)
-__device__ inline Corners point_corners(const float* xyz, const int32_t* batch, int64_t k, float v, float sfac,
-                                        int mode) {
+__device__ inline Corners corners_of(const float (&p)[3], int b, float v, float sfac, int mode) {
     Corners c;
-    c.b = batch ? batch[k] : 0;
+    c.b = b;
     c.ok = c.b >= 0 && c.b <= kBatchMax;
 #pragma unroll
     for (int d = 0; d < 3; ++d) {
-        const float x = xyz[3 * k + d];
+        const float x = p[d];
         const float a = x / v;  // the same quantity as Eq. 1 before the floor
         const float fa = floorf(a);
         c.ok = c.ok && isfinite(x) && isfinite(a) && fa >= (float)kCoordMin && fa <= (float)kCoordMax;
@@ -41,6 +40,11 @@ __device__ inline Corners point_corners(const float* xyz, const int32_t* batch, 
         c.t[d] = c.ok ? u - fb : 0.f;
     }
     return c;
+}
+__device__ inline Corners point_corners(const float* xyz, const int32_t* batch, int64_t k, float v, float sfac,
+                                        int mode) {
+    const float p[3] = {xyz[3 * k], xyz[3 * k + 1], xyz[3 * k + 2]};
+    return corners_of(p, batch ? batch[k] : 0, v, sfac, mode);
 }
 
 __device__ inline float corner_weight(const Corners& c, int cc) {
@@ -128,6 +132,7 @@ __global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __
     __shared__ __align__(16) int32_t sidx[4][PB * 16][8];
     __shared__ __align__(16) float sw[4][PB * 16][8];
     __shared__ __align__(16) float ys[4][16][C + 4];
+    __shared__ float ssc[C], ssh[C];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r16 = lane & 15, g = lane >> 4;
@@ -135,12 +140,27 @@ __global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __
     const float sfac = __builtin_ldexpf(1.0f, -a.stride_log2);
     const bool mlp = a.pfeat != nullptr;
 
-    // Wp fragments into LDS (the whole workgroup)
+    // Wp fragments, scale and shift into LDS (the whole workgroup)
     if (mlp) {
         for (int f = threadIdx.x; f < KCH * NB * 64; f += blockDim.x) wl[f] = wpack[f];
+        for (int c = threadIdx.x; c < C; c += blockDim.x) {
+            ssc[c] = a.scale_p ? a.scale_p[c] : 1.f;
+            ssh[c] = a.shift_p ? a.shift_p[c] : 0.f;
+        }
     }
 
-    // 1. corners: probes of the wave's PB blocks together
+    // 1. corners: coordinates of the wave's points loaded together, then the
+    // probes of all its blocks together
+    float px[PB][3];
+    int pb[PB];
+#pragma unroll
+    for (int b = 0; b < PB; ++b) {
+        const int64_t k = p0 + b * 16 + r16;
+        const int64_t kc = k < a.n ? k : 0;
+#pragma unroll
+        for (int d = 0; d < 3; ++d) px[b][d] = a.xyz[3 * kc + d];
+        pb[b] = a.batch ? a.batch[kc] : 0;
+    }
     Corners cn[PB];
     uint64_t key[2 * PB];
     bool act[2 * PB];
@@ -148,12 +168,11 @@ __global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __
 #pragma unroll
     for (int b = 0; b < PB; ++b) {
         const int64_t k = p0 + b * 16 + r16;
-        if (k < a.n) cn[b] = point_corners(a.xyz, a.batch, k, a.voxel_size, sfac, a.mode);
-        else cn[b].ok = false;
+        cn[b] = corners_of(px[b], pb[b], a.voxel_size, sfac, a.mode);
+        if (k >= a.n) cn[b].ok = false;
         if (k < a.n && !cn[b].ok && g == 0)
-            raise_flag(a.h, isfinite(a.xyz[3 * k]) && isfinite(a.xyz[3 * k + 1]) && isfinite(a.xyz[3 * k + 2])
-                                ? kFlagRange
-                                : kFlagNonfinite);
+            raise_flag(a.h, isfinite(px[b][0]) && isfinite(px[b][1]) && isfinite(px[b][2]) ? kFlagRange
+                                                                                        : kFlagNonfinite);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int cc = 2 * g + h;
@@ -224,9 +243,9 @@ __global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __
                 const int col = nb * 16 + 4 * g;
                 float sc[4], sh[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {  // (scale / shift need only 4-byte alignment)
-                    sc[e] = a.scale_p ? a.scale_p[col + e] : 1.f;
-                    sh[e] = a.shift_p ? a.shift_p[col + e] : 0.f;
+                for (int e = 0; e < 4; ++e) {
+                    sc[e] = ssc[col + e];
+                    sh[e] = ssh[col + e];
                 }
                 y.x = acc[nb][0] * sc[0] + sh[0];
                 y.y = acc[nb][1] * sc[1] + sh[1];
@@ -242,36 +261,47 @@ __global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __
             *(float4*)&ys[wave][r16][nb * 16 + 4 * g] = y;
         }
         __builtin_amdgcn_wave_barrier();
-        // 3. blend: tasks (point, chunk) of block b
+        // 3. blend: tasks (point, chunk) of block b; the corner rows of all of
+        // a lane's tasks are requested before any of them is used
+        constexpr int NT = (16 * NCH + 63) / 64;
+        int32_t ci[NT][8];
+        float cw[NT][8];
+        uint4 v[NT][8];
 #pragma unroll
-        for (int j = 0; j < (16 * NCH + 63) / 64; ++j) {
+        for (int j = 0; j < NT; ++j) {
             const int t = lane + 64 * j;
-            if (t >= 16 * NCH) break;
-            const int pt = t / NCH, ch = t - pt * NCH;
-            const int64_t k = p0 + b * 16 + pt;
+            const int pt = (t < 16 * NCH ? t : 0) / NCH, ch = (t < 16 * NCH ? t : 0) % NCH;
             const i32x4v ia = *(const i32x4v*)&sidx[wave][b * 16 + pt][0];
             const i32x4v ib = *(const i32x4v*)&sidx[wave][b * 16 + pt][4];
             const float4 wa = *(const float4*)&sw[wave][b * 16 + pt][0];
             const float4 wb = *(const float4*)&sw[wave][b * 16 + pt][4];
-            const int32_t ci[8] = {ia.x, ia.y, ia.z, ia.w, ib.x, ib.y, ib.z, ib.w};
-            const float cw[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
-            uint4 v[8];
+            const int32_t ii[8] = {ia.x, ia.y, ia.z, ia.w, ib.x, ib.y, ib.z, ib.w};
+            const float ww[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
 #pragma unroll
             for (int cc = 0; cc < 8; ++cc) {
-                v[cc] = make_uint4(0, 0, 0, 0);
-                if (ci[cc] >= 0) v[cc] = *(const uint4*)(V + (int64_t)ci[cc] * C + ch * 8);
+                ci[j][cc] = t < 16 * NCH ? ii[cc] : -1;
+                cw[j][cc] = ww[cc];
+                v[j][cc] = make_uint4(0, 0, 0, 0);
+                if (ci[j][cc] >= 0) v[j][cc] = *(const uint4*)(V + (int64_t)ci[j][cc] * C + ch * 8);
             }
+        }
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+            const int t = lane + 64 * j;
+            if (t >= 16 * NCH) break;
+            const int pt = t / NCH, ch = t - pt * NCH;
+            const int64_t k = p0 + b * 16 + pt;
             float dv[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) dv[e] = 0.f;
 #pragma unroll
             for (int cc = 0; cc < 8; ++cc) {
-                if (ci[cc] < 0) continue;
-                const uint32_t u[4] = {v[cc].x, v[cc].y, v[cc].z, v[cc].w};
+                if (ci[j][cc] < 0) continue;
+                const uint32_t u[4] = {v[j][cc].x, v[j][cc].y, v[j][cc].z, v[j][cc].w};
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    dv[2 * e] += cw[cc] * from16<DT>(u[e] & 0xFFFF);
-                    dv[2 * e + 1] += cw[cc] * from16<DT>(u[e] >> 16);
+                    dv[2 * e] += cw[j][cc] * from16<DT>(u[e] & 0xFFFF);
+                    dv[2 * e + 1] += cw[j][cc] * from16<DT>(u[e] >> 16);
                 }
             }
             const float4 y0 = *(const float4*)&ys[wave][pt][ch * 8];

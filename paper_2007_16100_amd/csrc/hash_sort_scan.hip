@@ -323,6 +323,68 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_scatter(const SortStats*
     }
 }
 
+// Passes 4.. (compacted keys wider than 32 bits: coordinate ranges of whole
+// cities or many batches) by one workgroup over all the keys: for each pass a
+// histogram, a scan of the 256 digit counts, then a stable scatter chunk by
+// chunk (a digit's keys keep their order inside a chunk by (wave, lane) and
+// across chunks by the running offsets).  Exits at once for keys of at most 32
+// bits, the usual case, so the host always launches it.
+constexpr int kWideThreads = 1024;
+__global__ __launch_bounds__(kWideThreads) void k_radix_wide(const SortStats* st, SortBufs sb,
+                                                             const int64_t* count_dev, int64_t cap) {
+    constexpr int NWV = kWideThreads / 64;
+    const uint32_t bits = st->sort_bits;
+    if (bits <= 32) return;
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t run[256];
+    __shared__ uint32_t wcnt[NWV][256];
+    __shared__ int lds[NWV + 1];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int64_t count = clamp_count(count_dev, cap);
+    const int passes = (int)((bits + 7) / 8);
+    for (int pass = 4; pass < passes; ++pass) {
+        const uint64_t* src = (pass & 1) ? sb.b : sb.a;
+        uint64_t* dst = (pass & 1) ? sb.a : sb.b;
+        if (t < 256) hist[t] = 0;
+        __syncthreads();
+        for (int64_t i = t; i < count; i += kWideThreads) atomicAdd(&hist[(src[i] >> (8 * pass)) & 0xFF], 1u);
+        __syncthreads();
+        {
+            const int v = t < 256 ? (int)hist[t] : 0;
+            int tot;
+            const int ex = block_exclusive_scan(v, lds, &tot);
+            if (t < 256) run[t] = (uint32_t)ex;
+        }
+        __syncthreads();
+        for (int64_t c0 = 0; c0 < count; c0 += kWideThreads) {
+            const int64_t i = c0 + t;
+            const bool valid = i < count;
+            const uint64_t key = valid ? src[i] : 0ull;
+            const uint32_t d = (uint32_t)(key >> (8 * pass)) & 0xFF;
+            for (int w = 0; w < NWV; ++w)
+                if (t < 256) wcnt[w][t] = 0;
+            __syncthreads();
+            const uint64_t peers = digit_peers(d, valid);
+            const uint32_t rank = (uint32_t)__popcll(peers & lt);
+            if (valid && rank == 0) wcnt[wave][d] = (uint32_t)__popcll(peers);
+            __syncthreads();
+            if (t < 256) {
+                uint32_t b0 = run[t];
+                for (int w = 0; w < NWV; ++w) {
+                    const uint32_t c = wcnt[w][t];
+                    wcnt[w][t] = b0;
+                    b0 += c;
+                }
+                run[t] = b0;
+            }
+            __syncthreads();
+            if (valid) dst[wcnt[wave][d] + rank] = key;
+            __syncthreads();
+        }
+    }
+}
+
 void launch_sort_keys(hipStream_t s, SortBufs sb, const int64_t* count_dev, int64_t cap, uint32_t nparts) {
     if (cap <= 0) cap = 1;
     if (nparts == 0) {
@@ -334,11 +396,12 @@ void launch_sort_keys(hipStream_t s, SortBufs sb, const int64_t* count_dev, int6
     k_sort_stats<<<1, 256, 0, s>>>(sb.st, sb.part, nparts, count_dev, cap);
     const unsigned nblk = blocks_for(cap, kSortTile);
     const int fused = nblk <= kFusedSortBlocks ? 1 : 0;
-    for (int pass = 0; pass < 8; ++pass) {
+    for (int pass = 0; pass < 4; ++pass) {
         k_radix_hist<<<nblk, kSortThreads, 0, s>>>(sb.st, sb, count_dev, cap, pass);
         if (!fused) k_radix_scan<<<1, 256, 0, s>>>(sb.st, sb.hist, nblk, pass);
         k_radix_scatter<<<nblk, kSortThreads, 0, s>>>(sb.st, sb, count_dev, cap, pass, fused);
     }
+    k_radix_wide<<<1, kWideThreads, 0, s>>>(sb.st, sb, count_dev, cap);
 }
 
 // ---------------------------------------------------------------------------

@@ -221,9 +221,12 @@ __global__ __launch_bounds__(kMapThreads) void k_map_write(Header* h, Table fine
     }
 }
 
-// pass 1 of a submanifold 3x3x3 map (see the file comment); bcnt may be null
+// pass 1 of a submanifold 3x3x3 map (see the file comment); bcnt may be null.
+// The block's 64 rows of the table are assembled in LDS and written out as one
+// contiguous run.
 __global__ __launch_bounds__(256) void k_map_nbr3(Table fine, const int32_t* coords, const int64_t* m_out,
                                                   int64_t cap, int32_t* nbr, uint32_t* bcnt) {
+    __shared__ int32_t tile[kNbrVox * 27];  // row stride 27 words: conflict-free per-lane writes
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t m = count_or_cap(m_out, cap);
@@ -254,12 +257,16 @@ __global__ __launch_bounds__(256) void k_map_nbr3(Table fine, const int32_t* coo
         if (k >= 27) break;
         const int32_t i = (k == 13) ? (int32_t)j : res[q];
         const bool present = valid && i >= 0;
-        if (valid) nbr[j * 27 + k] = present ? i + 1 : 0;
+        tile[lane * 27 + k] = present ? i + 1 : 0;
         if (bcnt) {
             const uint64_t bal = __ballot(present);
             if (lane == 0) bcnt[k * nblk + blockIdx.x] = (uint32_t)__popcll(bal);
         }
     }
+    __syncthreads();
+    const int64_t j0 = (int64_t)blockIdx.x * kNbrVox;
+    const int rows = m - j0 < kNbrVox ? (int)(m - j0) : kNbrVox;
+    for (int e = threadIdx.x; e < rows * 27; e += blockDim.x) nbr[j0 * 27 + e] = tile[e];
 }
 
 // pass 2 of a submanifold 3x3x3 map: pairs from the neighbour table

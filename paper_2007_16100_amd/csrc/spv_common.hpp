@@ -167,11 +167,13 @@ __device__ inline int32_t table_find(Table t, uint64_t key) {
 __device__ inline int64_t table_slot(Table t, uint64_t key) { return table_slot_from(t, key, hash_slot(key, t.mask)); }
 
 // NP lookups whose first buckets are read together (one round trip for all of
-// them); the rare key not settled by its first bucket continues on its own.
-// Inactive entries (act[p] false) read bucket 0 and return -1.
+// them), then the second buckets of the ones not yet settled (one more round);
+// the rare key settled by neither continues on its own.  Inactive entries
+// (act[p] false) read bucket 0 and return -1.
 template <int NP>
 __device__ inline void table_find_n(Table t, const uint64_t (&key)[NP], const bool (&act)[NP], int32_t (&res)[NP]) {
     uint32_t s[NP];
+    int st[NP];  // 1 found, 0 absent, -1 open
     Bucket b[NP];
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
@@ -181,14 +183,24 @@ __device__ inline void table_find_n(Table t, const uint64_t (&key)[NP], const bo
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
         int e = 0;
-        const int r = act[p] ? bucket_match(b[p], key[p], &e) : 0;
-        if (r > 0) {
-            res[p] = bucket_val(b[p], e);
-        } else if (r == 0) {
-            res[p] = -1;
-        } else {
-            const int64_t sl = table_slot_from(t, key[p], (s[p] + 4) & t.mask);
-            res[p] = sl >= 0 ? t.vals[sl] : -1;
+        st[p] = act[p] ? bucket_match(b[p], key[p], &e) : 0;
+        res[p] = st[p] > 0 ? bucket_val(b[p], e) : -1;
+        if (st[p] < 0) s[p] = (s[p] + 4) & t.mask;
+    }
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+        if (st[p] < 0) b[p] = load_bucket(t, s[p]);
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        if (st[p] < 0) {
+            int e = 0;
+            const int r = bucket_match(b[p], key[p], &e);
+            if (r > 0) {
+                res[p] = bucket_val(b[p], e);
+            } else if (r < 0) {
+                const int64_t sl = table_slot_from(t, key[p], (s[p] + 4) & t.mask);
+                res[p] = sl >= 0 ? t.vals[sl] : -1;
+            }
         }
     }
 }

@@ -154,6 +154,20 @@ def test_voxelize_mean_bit_exact(spv, sweep, dtype):
     np.testing.assert_array_equal(vf, rvf)
 
 
+def test_voxelize_wide_keys(spv):
+    """Coordinates spanning nearly the whole key range (48 significant bits once
+    compacted): the sort's passes past 32 bits run."""
+    rng = np.random.default_rng(4343)
+    xyz = rng.uniform(-1600.0, 1600.0, size=(20_000, 3)).astype(np.float32)
+    batch = rng.integers(0, 4, size=len(xyz)).astype(np.int32)
+    c, vf, cnt, p2v, _ = run_voxelize(spv, xyz, 0.05, synth.normal((len(xyz), 8), 3, dtype="bf16"), "bf16", batch)
+    rc, rvf, rcnt, rp2v = oracle.voxelize(xyz, 0.05, synth.normal((len(xyz), 8), 3, dtype="bf16"), "bf16", batch)
+    np.testing.assert_array_equal(c, rc)
+    np.testing.assert_array_equal(cnt, rcnt)
+    np.testing.assert_array_equal(p2v, rp2v)
+    np.testing.assert_array_equal(vf, rvf)
+
+
 def test_voxelize_device_errors(spv):
     xyz = np.zeros((100, 3), np.float32)
     xyz[17, 1] = np.nan
