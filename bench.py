@@ -124,7 +124,21 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline leg")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 256 MiB device-to-device copy three times (the reference for scaling "
+                         "the FETCH_SIZE / WRITE_SIZE counters to bytes)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        nbytes = 256 << 20
+        x = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+        y = torch.empty_like(x)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": nbytes, "repeats": 3}))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the SPVConv hot path here runs on a single MI355X); "
               f"--gpus {args.gpus} is not supported", file=sys.stderr)
