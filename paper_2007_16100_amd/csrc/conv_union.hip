@@ -24,7 +24,8 @@ __device__ __forceinline__ void static_for(F&& f) {
 // of row r16, which is also the order in which they are stored.
 //
 // The 27 offsets run in phases of PH: at the start of a phase the workgroup
-// copies W of the phase's offsets into LDS (one barrier before, one after);
+// copies W of the phase's offsets into LDS with global->LDS loads (one barrier
+// before, one wait for every load of the wave and one barrier after);
 // inside a phase the waves never synchronize and load no weights, each one
 // streaming its own rows:
 //   step k: loads the neighbour indices of offset k+3 and gathers the rows of
@@ -32,8 +33,9 @@ __device__ __forceinline__ void static_for(F&& f) {
 //           nothing; a lane whose row has none gets zeros), then multiplies the
 //           rows gathered for offset k by W[k] one 32-channel slab at a time,
 //           skipping blocks without a neighbour at k.
-// All loads are ordinary vector-memory loads the compiler sees, so its waits
-// (which count outstanding loads in issue order) stay exact.
+// All other loads are ordinary vector-memory loads the compiler sees, so its
+// waits (which count outstanding loads in issue order) stay exact: the weight
+// copies it does not see are all complete (vmcnt 0) before the phase starts.
 constexpr int kUK3 = 27;
 constexpr int kNAhead = 3;  // neighbour indices: steps ahead
 constexpr int kRAhead = 1;  // gathered rows: steps ahead
@@ -135,12 +137,16 @@ __global__ __launch_bounds__(64 * NW) void k_conv_union(
         if constexpr (k % PH == 0) {
             // a new phase: once every wave is done with the previous weights,
             // copy W[k .. k+PH) into LDS
+            // (global->LDS copies, all issued before one wait: a copy through
+            // registers would wait for each fragment -- and every gather in
+            // flight -- in turn)
             constexpr int nf = (K3 - k < PH ? K3 - k : PH) * FR;
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
+            const uint64_t gw = (uint64_t)(wsrc + (int64_t)k * FR * 64);
             for (int f = wave; f < nf; f += NW)
-                ((i32x4*)wl)[f * 64 + lane] = wsrc[((int64_t)k * FR + f) * 64 + lane];
-            lds_wait();
+                lds_dma_x4(gw + (uint64_t)f * 1024u, (uint32_t)lane * 16u, lds_addr(wl + f * 64));
+            vm_wait<0>();
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
         }
