@@ -6,6 +6,8 @@ A step = one spv_block call: voxelize (Eq. 1-2, hash) -> submanifold kernel map 
 MLP 96->96 + BN + ReLU + add.  Inputs are resident in HBM before timing starts.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu]
+    python bench.py --sizes      # block phases on batches of 1, 4, 16, 64 sweeps (GB/s vs n)
+    python bench.py --configs    # map build and conv alone: 32->32 k3, 64->128 k2s2, 128->64 transposed
 
 Prints ONE JSON line.  `value` is the sparse-conv throughput in TFLOP/s on its
 effective FLOPs (2 * Cin * Cout * sum_k |map_k|, MACs over active synapses only),
@@ -100,6 +102,192 @@ def make_workload(seed=1004, C=96):
     return xyz, feat, convs, Wp, scp, shp
 
 
+def table_slots(n):
+    """Hash-table capacity the library uses for n keys (power of two >= 2n, at least 1024)."""
+    c = 1024
+    while c < 2 * n:
+        c <<= 1
+    return c
+
+
+def phase_bytes(n, m, pairs, C, nconv=2):
+    """Algorithmic bytes per phase of the block: compulsory reads of inputs plus writes of
+    outputs, each gathered row counted once, plus one write of the hash table (12 B/slot)."""
+    S = table_slots(n)
+    return {
+        # xyz + features in; coords, counts, pt2vox, voxel features out; table written once
+        "voxelize": 12 * n + 2 * C * n + 16 * m + 4 * m + 4 * n + 2 * C * m + 12 * S,
+        # coords in, table read once, 27-entry neighbour table out
+        "kernel_map": 16 * m + 12 * S + 108 * m,
+        # input rows + output rows + the map (8 B per pair) + weights, per conv
+        "conv": 2 * C * m + 2 * C * m + 8 * pairs + 27 * C * C * 2,
+        # xyz + point features + voxel features + table + output
+        "devox_mlp_add": 12 * n + 2 * C * n + 2 * C * m + 12 * S + 2 * C * n,
+    }
+
+
+def time_block(spv, ws, params, d_xyz, d_feat, out, steps, warm, batch=None):
+    """Per-phase HIP-event times (ms) of `steps` block calls after `warm` untimed ones."""
+    n_ev = 7
+    evs = [HipEvents(n_ev) for _ in range(steps)]
+    for _ in range(warm):
+        spv.spv_block(ws, params, d_xyz, d_feat, batch=batch, out=out)
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        params.events = ct.cast(evs[s].arr, ct.POINTER(ct.c_void_p))
+        params.n_events = n_ev
+        spv.spv_block(ws, params, d_xyz, d_feat, batch=batch, out=out)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    params.events = None
+    params.n_events = 0
+    names = ["voxelize", "kernel_map", "conv_plan", "conv1", "conv2", "devox_mlp_add"]
+    ph = {k: [e.ms(i, i + 1) for e in evs] for i, k in enumerate(names)}
+    ph["block"] = [e.ms(0, 6) for e in evs]
+    return ph, wall
+
+
+def block_graph_ms(spv, ws, params, d_xyz, d_feat, out, steps):
+    """Mean time (ms) of one block call captured into a graph and replayed `steps` times."""
+    import torch
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        spv.spv_block(ws, params, d_xyz, d_feat, out=out)
+    for _ in range(3):
+        g.replay()
+    torch.cuda.synchronize()
+    ga, gb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ga.record()
+    for _ in range(steps):
+        g.replay()
+    gb.record()
+    torch.cuda.synchronize()
+    return ga.elapsed_time(gb) / steps
+
+
+def sizes_mode(args):
+    """The block on batches of 1, 4, 16 and 64 independent sweeps (batch index in the key),
+    one JSON line per batch: per-phase median time and GB/s of algorithmic bytes."""
+    import torch
+    from paper_2007_16100_amd import spv, synth
+    C, v = 96, 0.05
+    dev = torch.device("cuda:0")
+    batches = [int(b) for b in args.batches.split(",")]
+    sweeps = []
+    for i in range(max(batches)):
+        sweeps.append(synth.lidar_sweep(2000 + i))
+        if (i + 1) % 8 == 0:
+            print(f"# generated {i + 1} sweeps", file=sys.stderr, flush=True)
+    _, _, convs, Wp, scp, shp = make_workload(C=C)
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    d_convs = [(bf(W), torch.from_numpy(sc).to(dev), torch.from_numpy(sh).to(dev), r) for W, sc, sh, r in convs]
+    params = spv.make_block_params(C, torch.bfloat16, v, d_convs, bf(Wp), torch.from_numpy(scp).to(dev),
+                                   torch.from_numpy(shp).to(dev), relu_p=True)
+    for B in batches:
+        xyz = np.concatenate(sweeps[:B])
+        bt = np.concatenate([np.full(len(sweeps[i]), i, np.int32) for i in range(B)])
+        n = len(xyz)
+        feat = synth.normal((n, C), 2100 + B, dtype="bf16")
+        d_xyz, d_bt, d_feat = torch.from_numpy(xyz).to(dev), torch.from_numpy(bt).to(dev), bf(feat)
+        ws2 = spv.Workspace.for_ops(n, C)
+        vox = spv.spv_voxelize(ws2, d_xyz, v, batch=d_bt)
+        km = spv.spv_kernel_map(ws2, vox.coords[:vox.m].contiguous())
+        m, pairs = vox.m, km.total
+        del ws2, vox, km
+        ws = spv.Workspace.for_block(n, C)
+        out = torch.empty((n, C), dtype=torch.bfloat16, device=dev)
+        ph, _ = time_block(spv, ws, params, d_xyz, d_feat, out, args.steps, args.warmup, batch=d_bt)
+        pb = phase_bytes(n, m, pairs, C)
+        med = {k: float(np.median(x)) for k, x in ph.items()}
+        conv_ms = float(np.median(ph["conv1"] + ph["conv2"]))
+        gbps = {k: pb[k] / (med[k] * 1e-3) / 1e9 for k in ("voxelize", "kernel_map", "devox_mlp_add")}
+        gbps["conv"] = pb["conv"] / (conv_ms * 1e-3) / 1e9
+        print(json.dumps({"sweeps": B, "points": n, "voxels": m, "kernel_map_pairs": pairs, "C": C,
+                          "phases_ms_median": med, "alg_bytes": pb, "GBps": gbps,
+                          "hbm_frac": {k: x / PEAK_HBM_GBPS for k, x in gbps.items()},
+                          "conv_TFLOPs": 2.0 * C * C * pairs / (conv_ms * 1e-3) / 1e12}), flush=True)
+        del ws, out, d_xyz, d_bt, d_feat
+        torch.cuda.empty_cache()
+
+
+def configs_mode(args):
+    """Map build and conv alone on the sweep: a submanifold 3x3x3 conv 32->32 (seed 1002), and
+    the stride-2 map with a k2s2 conv 64->128 and its transposed 128->64 (seed 1003).  One JSON
+    line per op: median HIP-event time, algorithmic bytes / FLOPs and both roofline fractions."""
+    import torch
+    from paper_2007_16100_amd import spv, synth
+    dev = torch.device("cuda:0")
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(args.steps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            ts.append((a, b))
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) for a, b in ts]))
+
+    def report(op, ms, nbytes, flops=0.0, **kw):
+        gbps = nbytes / (ms * 1e-3) / 1e9
+        tf = flops / (ms * 1e-3) / 1e12
+        print(json.dumps({"op": op, "ms_median": ms, "alg_bytes": nbytes, "GBps": gbps,
+                          "hbm_frac": gbps / PEAK_HBM_GBPS, "eff_flops": flops, "TFLOPs": tf,
+                          "mfma_frac": tf / PEAK_BF16_TFLOPS, **kw}), flush=True)
+
+    for seed in (1002, 1003):
+        xyz = synth.lidar_sweep(seed)
+        d_xyz = torch.from_numpy(xyz).to(dev)
+        ws = spv.Workspace.for_ops(len(xyz), 128)
+        vox = spv.spv_voxelize(ws, d_xyz, 0.05)
+        m = vox.m
+        coords = vox.coords[:m].contiguous()
+        wsm = spv.Workspace.for_ops(len(xyz), 128)
+        if seed == 1002:
+            km = spv.spv_kernel_map(wsm, coords)
+            P = km.total
+            ms = timed(lambda: spv.spv_kernel_map(wsm, coords, sync=False))
+            report("kernel_map k3 s1", ms, 16 * m + 12 * table_slots(m) + 8 * P + 4 * 28, voxels=m, pairs=P)
+            C = 32
+            x = bf(synth.normal((m, C), seed + 1, dtype="bf16"))
+            W = bf(synth.conv_weight(27, C, C, seed + 2, "bf16"))
+            out = torch.empty((m, C), dtype=torch.bfloat16, device=dev)
+            ms = timed(lambda: spv.spv_sparse_conv(wsm, x, km.off, km.pairs, W, m, out=out))
+            report("conv k3 32->32", ms, 2 * C * m * 2 + 8 * P + 27 * C * C * 2, 2.0 * C * C * P, voxels=m, pairs=P)
+        else:
+            km = spv.spv_kernel_map(wsm, coords, K=2, stride=2)
+            mc = int(km.m_out_dev.item())
+            P = km.total
+            ms = timed(lambda: spv.spv_kernel_map(wsm, coords, K=2, stride=2, sync=False))
+            report("kernel_map k2 s2", ms, 16 * m + 16 * mc + 12 * table_slots(m) + 8 * P + 4 * 9,
+                   voxels=m, coarse_voxels=mc, pairs=P)
+            x = bf(synth.normal((m, 64), seed + 1, dtype="bf16"))
+            W = bf(synth.conv_weight(8, 64, 128, seed + 2, "bf16"))
+            WT = bf(synth.conv_weight(8, 128, 64, seed + 3, "bf16"))
+            y = torch.empty((mc, 128), dtype=torch.bfloat16, device=dev)
+            z = torch.empty((m, 64), dtype=torch.bfloat16, device=dev)
+            ms = timed(lambda: spv.spv_sparse_conv(wsm, x, km.off, km.pairs, W, mc, m_out_dev=km.m_out_dev, out=y))
+            report("conv k2s2 64->128", ms, 2 * 64 * m + 2 * 128 * mc + 8 * P + 8 * 64 * 128 * 2,
+                   2.0 * 64 * 128 * P, voxels=m, coarse_voxels=mc, pairs=P)
+            ms = timed(lambda: spv.spv_sparse_conv(wsm, y, km.off, km.pairs, WT, m, transposed=True, out=z))
+            report("conv k2s2 transposed 128->64", ms, 2 * 128 * mc + 2 * 64 * m + 8 * P + 8 * 64 * 128 * 2,
+                   2.0 * 64 * 128 * P, voxels=m, coarse_voxels=mc, pairs=P)
+        del ws, wsm
+        torch.cuda.empty_cache()
+
+
 def cpu_baseline(xyz, convs, C, v=0.05):
     """The oracle, as it stands, on one full 96->96 conv layer of the workload (one thread)."""
     import oracle
@@ -127,7 +315,18 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy three times (the reference for scaling "
                          "the FETCH_SIZE / WRITE_SIZE counters to bytes)")
+    ap.add_argument("--no-graph", action="store_true", help="skip the graph-replay timing of the block")
+    ap.add_argument("--sizes", action="store_true", help="block phases on batches of sweeps (GB/s against n)")
+    ap.add_argument("--batches", default="1,4,16,64", help="sweeps per batch for --sizes")
+    ap.add_argument("--configs", action="store_true",
+                    help="map build and conv alone at the 32->32 and 64<->128 (k2s2, transposed) shapes")
     args = ap.parse_args()
+    if args.sizes:
+        sizes_mode(args)
+        return
+    if args.configs:
+        configs_mode(args)
+        return
     if args.copy_calibration:
         import torch
         nbytes = 256 << 20
@@ -170,32 +369,15 @@ def main():
     m, pairs_total = vox.m, km.total
     del ws2, vox, km
 
-    n_ev = 7
     steps, warm = args.steps, args.warmup
-    evs = [HipEvents(n_ev) for _ in range(steps)]
-    params_plain = params
-    for _ in range(warm):
-        spv.spv_block(ws, params_plain, d_xyz, d_feat, out=out)
-    torch.cuda.synchronize()
-
-    t0 = time.perf_counter()
-    for s in range(steps):
-        params.events = ct.cast(evs[s].arr, ct.POINTER(ct.c_void_p))
-        params.n_events = n_ev
-        spv.spv_block(ws, params, d_xyz, d_feat, out=out)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    params.events = None
-    params.n_events = 0
-
-    phase_names = ["voxelize", "kernel_map", "conv_plan", "conv1", "conv2", "devox_mlp_add"]
-    ph = {k: [] for k in phase_names}
-    block_ms = []
-    for e in evs:
-        for i, k in enumerate(phase_names):
-            ph[k].append(e.ms(i, i + 1))
-        block_ms.append(e.ms(0, 6))
+    ph, wall = time_block(spv, ws, params, d_xyz, d_feat, out, steps, warm)
+    block_ms = ph.pop("block")
     med = {k: float(np.median(vv)) for k, vv in ph.items()}
+    p10 = {k: float(np.percentile(vv, 10)) for k, vv in ph.items()}
+    p90 = {k: float(np.percentile(vv, 90)) for k, vv in ph.items()}
+
+    # the same block captured once into a graph and replayed (no events inside)
+    graph_ms = None if args.no_graph else block_graph_ms(spv, ws, params, d_xyz, d_feat, out, steps)
     conv_ms = [a for k in ("conv1", "conv2") for a in ph[k]]
     conv_avg_ms = float(np.mean(conv_ms))
     F_conv = 2.0 * C * C * pairs_total
@@ -233,7 +415,12 @@ def main():
                                "voxel 0.05 m, bf16 storage / fp32 accumulation",
                    "points": n, "voxels": m, "kernel_map_pairs": pairs_total, "C": C, "seed": 1004},
         "block_ms_median": float(np.median(block_ms)),
+        "block_ms_p10": float(np.percentile(block_ms, 10)),
+        "block_ms_p90": float(np.percentile(block_ms, 90)),
+        "block_ms_graph_replay": graph_ms,
         "phases_ms_median": med,
+        "phases_ms_p10": p10,
+        "phases_ms_p90": p90,
         "roofline": roof,
     }
     if not args.no_cpu:

@@ -79,7 +79,7 @@ constexpr int kSortTile = kSortThreads * kSortItems;
 constexpr int kSortParts = 256;            // partial records of the stand-alone min / max kernel
 constexpr uint32_t kFusedSortBlocks = 256;  // up to this many tiles a scatter block scans the histograms itself
 
-size_t sort_hist_entries(int64_t cap) { return (size_t)256 * blocks_for(cap, kSortTile); }
+size_t sort_hist_entries(int64_t cap) { return (size_t)256 * blocks_for(cap, kSortTile) + 1; }
 size_t sort_part_records(int64_t cap) {
     const size_t b = blocks_for(cap, kAppendThreads);
     return b > (size_t)kSortParts ? b : (size_t)kSortParts;
@@ -92,6 +92,7 @@ void plan_sort_ws(Arena& a, SortBufs& sb, int64_t cap) {
     sb.hist = a.take<uint32_t>(sort_hist_entries(c));
     sb.part = a.take<int32_t>(8 * sort_part_records(c));
     sb.st = a.take<SortStats>(1);
+    sb.scan_tmp = a.take<int32_t>(scan_tmp_entries((int64_t)sort_hist_entries(c)));
 }
 
 __device__ inline int64_t clamp_count(const int64_t* count_dev, int64_t cap) {
@@ -179,7 +180,7 @@ __device__ inline uint64_t digit_peers(uint32_t d, bool valid) {
 // buffer read back always holds compacted keys.  Lanes of a wave holding the
 // same digit are counted by one LDS add of their leader.
 __global__ __launch_bounds__(kSortThreads) void k_radix_hist(const SortStats* st, SortBufs sb, const int64_t* count_dev,
-                                                             int64_t cap, int pass) {
+                                                             int64_t cap, int pass, int digit_major) {
     const uint32_t nblk = gridDim.x;
     if (pass > 0 && (uint32_t)(8 * pass) >= st->sort_bits) return;
     uint64_t* src = (pass & 1) ? sb.b : sb.a;
@@ -225,31 +226,15 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_hist(const SortStats* st
         if (valid && (peers & lt) == 0) atomicAdd(&hist[d], (uint32_t)__popcll(peers));
     }
     __syncthreads();
-    sb.hist[(size_t)blockIdx.x * 256 + threadIdx.x] = hist[threadIdx.x];  // tile-major
-}
-
-// Many-tile sorts: one block turns the tile-major histograms into write offsets
-// in place (thread d walks digit d over the tiles, then the digit totals are
-// scanned and added).
-__global__ __launch_bounds__(256) void k_radix_scan(const SortStats* st, uint32_t* hist, uint32_t nblk, int pass) {
-    if ((uint32_t)(8 * pass) >= st->sort_bits) return;
-    __shared__ int lds[5];
-    const int t = threadIdx.x;
-    uint32_t run = 0;
-    for (uint32_t b = 0; b < nblk; ++b) {
-        const uint32_t v = hist[(size_t)b * 256 + t];
-        hist[(size_t)b * 256 + t] = run;
-        run += v;
-    }
-    int all;
-    const uint32_t dbase = (uint32_t)block_exclusive_scan((int)run, lds, &all);
-    for (uint32_t b = 0; b < nblk; ++b) hist[(size_t)b * 256 + t] += dbase;
+    if (digit_major) sb.hist[(size_t)threadIdx.x * nblk + blockIdx.x] = hist[threadIdx.x];
+    else sb.hist[(size_t)blockIdx.x * 256 + threadIdx.x] = hist[threadIdx.x];  // tile-major (coalesced)
 }
 
 // Stable scatter of one tile by one digit.  With `fused`, the block derives its
-// digit offsets from the raw histograms (thread d: all tiles' counts of digit d,
-// those of earlier tiles, then a scan over the digits); otherwise k_radix_scan
-// has already turned the histograms into offsets.  Inside the tile, items are
+// digit offsets from the raw tile-major histograms (thread d: all tiles' counts
+// of digit d, those of earlier tiles, then a scan over the digits); otherwise
+// the histograms are digit-major and an exclusive scan over all of them has
+// already turned them into write offsets.  Inside the tile, items are
 // ranked in (round, wave, lane) order -- the index order -- from per-wave digit
 // groups: counts of every (round, wave, digit) first, then one running sum per
 // digit over them, then every item is written.
@@ -288,7 +273,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_scatter(const SortStats*
         int all;
         run = (uint32_t)block_exclusive_scan((int)tot, lds, &all) + pre;
     } else {
-        run = sb.hist[(size_t)blockIdx.x * 256 + t];
+        run = sb.hist[(size_t)t * nblk + blockIdx.x];
         __syncthreads();
     }
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -323,68 +308,6 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_scatter(const SortStats*
     }
 }
 
-// Passes 4.. (compacted keys wider than 32 bits: coordinate ranges of whole
-// cities or many batches) by one workgroup over all the keys: for each pass a
-// histogram, a scan of the 256 digit counts, then a stable scatter chunk by
-// chunk (a digit's keys keep their order inside a chunk by (wave, lane) and
-// across chunks by the running offsets).  Exits at once for keys of at most 32
-// bits, the usual case, so the host always launches it.
-constexpr int kWideThreads = 1024;
-__global__ __launch_bounds__(kWideThreads) void k_radix_wide(const SortStats* st, SortBufs sb,
-                                                             const int64_t* count_dev, int64_t cap) {
-    constexpr int NWV = kWideThreads / 64;
-    const uint32_t bits = st->sort_bits;
-    if (bits <= 32) return;
-    __shared__ uint32_t hist[256];
-    __shared__ uint32_t run[256];
-    __shared__ uint32_t wcnt[NWV][256];
-    __shared__ int lds[NWV + 1];
-    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    const int64_t count = clamp_count(count_dev, cap);
-    const int passes = (int)((bits + 7) / 8);
-    for (int pass = 4; pass < passes; ++pass) {
-        const uint64_t* src = (pass & 1) ? sb.b : sb.a;
-        uint64_t* dst = (pass & 1) ? sb.a : sb.b;
-        if (t < 256) hist[t] = 0;
-        __syncthreads();
-        for (int64_t i = t; i < count; i += kWideThreads) atomicAdd(&hist[(src[i] >> (8 * pass)) & 0xFF], 1u);
-        __syncthreads();
-        {
-            const int v = t < 256 ? (int)hist[t] : 0;
-            int tot;
-            const int ex = block_exclusive_scan(v, lds, &tot);
-            if (t < 256) run[t] = (uint32_t)ex;
-        }
-        __syncthreads();
-        for (int64_t c0 = 0; c0 < count; c0 += kWideThreads) {
-            const int64_t i = c0 + t;
-            const bool valid = i < count;
-            const uint64_t key = valid ? src[i] : 0ull;
-            const uint32_t d = (uint32_t)(key >> (8 * pass)) & 0xFF;
-            for (int w = 0; w < NWV; ++w)
-                if (t < 256) wcnt[w][t] = 0;
-            __syncthreads();
-            const uint64_t peers = digit_peers(d, valid);
-            const uint32_t rank = (uint32_t)__popcll(peers & lt);
-            if (valid && rank == 0) wcnt[wave][d] = (uint32_t)__popcll(peers);
-            __syncthreads();
-            if (t < 256) {
-                uint32_t b0 = run[t];
-                for (int w = 0; w < NWV; ++w) {
-                    const uint32_t c = wcnt[w][t];
-                    wcnt[w][t] = b0;
-                    b0 += c;
-                }
-                run[t] = b0;
-            }
-            __syncthreads();
-            if (valid) dst[wcnt[wave][d] + rank] = key;
-            __syncthreads();
-        }
-    }
-}
-
 void launch_sort_keys(hipStream_t s, SortBufs sb, const int64_t* count_dev, int64_t cap, uint32_t nparts) {
     if (cap <= 0) cap = 1;
     if (nparts == 0) {
@@ -396,12 +319,18 @@ void launch_sort_keys(hipStream_t s, SortBufs sb, const int64_t* count_dev, int6
     k_sort_stats<<<1, 256, 0, s>>>(sb.st, sb.part, nparts, count_dev, cap);
     const unsigned nblk = blocks_for(cap, kSortTile);
     const int fused = nblk <= kFusedSortBlocks ? 1 : 0;
-    for (int pass = 0; pass < 4; ++pass) {
-        k_radix_hist<<<nblk, kSortThreads, 0, s>>>(sb.st, sb, count_dev, cap, pass);
-        if (!fused) k_radix_scan<<<1, 256, 0, s>>>(sb.st, sb.hist, nblk, pass);
+    // the significant bits are known on the device only: every pass a 64-bit key
+    // may need is launched, and passes beyond them exit at once
+    for (int pass = 0; pass < 8; ++pass) {
+        k_radix_hist<<<nblk, kSortThreads, 0, s>>>(sb.st, sb, count_dev, cap, pass, !fused);
+        if (!fused) {
+            // digit-major histograms -> write offsets (a pass past the significant
+            // bits scans stale counts that its scatter then ignores)
+            int32_t* h = (int32_t*)sb.hist;
+            launch_exclusive_scan(s, h, h, nullptr, (int64_t)256 * nblk, sb.scan_tmp);
+        }
         k_radix_scatter<<<nblk, kSortThreads, 0, s>>>(sb.st, sb, count_dev, cap, pass, fused);
     }
-    k_radix_wide<<<1, kWideThreads, 0, s>>>(sb.st, sb, count_dev, cap);
 }
 
 // ---------------------------------------------------------------------------

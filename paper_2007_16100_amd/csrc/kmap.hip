@@ -100,6 +100,11 @@ __global__ __launch_bounds__(kAppendThreads) void k_map_coarse_insert(Header* h,
         f[2] = c[2] >> 1;
         f[3] = c[3] >> 1;
         key = pack_key(f[0], f[1], f[2], f[3]);
+    }
+    // sorted fine voxels: neighbours in z often share a coarse voxel, and a lane
+    // whose key equals the previous lane's leaves the insert to its run's head
+    const uint64_t prev_key = __shfl_up(key, 1, 64);
+    if (key != kEmpty && ((threadIdx.x & 63) == 0 || prev_key != key)) {
         uint32_t slot;
         const int r = table_insert(coarse, key, &slot);
         created = r > 0;

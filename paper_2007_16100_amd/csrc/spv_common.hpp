@@ -81,25 +81,21 @@ struct Table {
 // Insert; returns 1 if this call created the entry, 0 if the key was present,
 // -1 if the table is full.  *slot receives the entry's slot.  Slots are claimed
 // strictly in probe order, so a lookup may stop at the first empty slot.
+// Every probe step is one compare-and-swap (empty -> key): on a table this
+// sparse the first slot is usually empty or already holds the key, and a CAS
+// settles both in one round trip, where a load first would take two.
 __device__ inline int table_insert(Table t, uint64_t key, uint32_t* slot) {
     uint32_t s = hash_slot(key, t.mask);
     for (uint32_t i = 0; i <= t.mask; ++i) {
-        uint64_t cur = __hip_atomic_load(&t.keys[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (cur == key) {
+        const uint64_t prev = atomicCAS((unsigned long long*)&t.keys[s], (unsigned long long)kEmpty,
+                                        (unsigned long long)key);
+        if (prev == kEmpty) {
+            *slot = s;
+            return 1;
+        }
+        if (prev == key) {
             *slot = s;
             return 0;
-        }
-        if (cur == kEmpty) {
-            uint64_t prev = atomicCAS((unsigned long long*)&t.keys[s], (unsigned long long)kEmpty,
-                                      (unsigned long long)key);
-            if (prev == kEmpty) {
-                *slot = s;
-                return 1;
-            }
-            if (prev == key) {
-                *slot = s;
-                return 0;
-            }
         }
         s = (s + 1) & t.mask;
     }

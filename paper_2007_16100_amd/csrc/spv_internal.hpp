@@ -106,6 +106,7 @@ struct SortBufs {
     uint32_t* hist;    // [256 * nblocks(cap)]
     int32_t* part;     // [sort_part_records(cap)][8] partial min / max records
     SortStats* st;
+    int32_t* scan_tmp; // scan partials for the many-tile offsets
 };
 void plan_sort_ws(Arena& a, SortBufs& sb, int64_t cap);
 size_t sort_hist_entries(int64_t cap);

@@ -26,8 +26,10 @@ void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n) {
 }
 
 // Eq. 1 per point, then hash insert.  Invalid points get kEmpty and a status
-// flag.  The block appends the keys it created to the unique-key list (one
-// counter atomic per block) and records their per-field min / max for the sort.
+// flag.  Consecutive returns of a sweep often share a voxel: a lane whose key
+// equals the previous lane's leaves the insert to the head of its run.  The
+// block appends the keys it created to the unique-key list (one counter atomic
+// per block) and records their per-field min / max for the sort.
 __global__ __launch_bounds__(kAppendThreads) void k_vox_insert(Header* h, Table t, SortBufs sb, uint64_t* pkey,
                                                                const float* xyz, const int32_t* batch, int64_t n,
                                                                float v) {
@@ -54,12 +56,15 @@ __global__ __launch_bounds__(kAppendThreads) void k_vox_insert(Header* h, Table 
             raise_flag(h, kFlagRange);
         } else {
             key = pack_key(b, q[0], q[1], q[2]);
-            uint32_t slot;
-            const int r = table_insert(t, key, &slot);
-            created = r > 0;
-            if (r < 0) raise_flag(h, kFlagTableFull);
         }
         pkey[k] = key;
+    }
+    const uint64_t prev_key = __shfl_up(key, 1, 64);
+    if (key != kEmpty && ((threadIdx.x & 63) == 0 || prev_key != key)) {
+        uint32_t slot;
+        const int r = table_insert(t, key, &slot);
+        created = r > 0;
+        if (r < 0) raise_flag(h, kFlagTableFull);
     }
     int mn[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
     int mx[4] = {(int)0x80000000, (int)0x80000000, (int)0x80000000, (int)0x80000000};

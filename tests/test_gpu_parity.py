@@ -130,8 +130,8 @@ def test_voxelize_edge_cases(spv, case):
 
 
 def test_voxelize_many_tiles(spv):
-    """Over 524k distinct voxels: the sort's offsets come from the separate
-    histogram scan instead of the scatter's own."""
+    """Over 524k distinct voxels: the sort's offsets come from a multi-tile scan
+    of digit-major histograms instead of the scatter's own."""
     rng = np.random.default_rng(4242)
     xyz = rng.uniform(-60.0, 60.0, size=(700_000, 3)).astype(np.float32)
     xyz[::7] = xyz[1::7][: len(xyz[::7])]  # some shared voxels
@@ -162,6 +162,24 @@ def test_voxelize_wide_keys(spv):
     batch = rng.integers(0, 4, size=len(xyz)).astype(np.int32)
     c, vf, cnt, p2v, _ = run_voxelize(spv, xyz, 0.05, synth.normal((len(xyz), 8), 3, dtype="bf16"), "bf16", batch)
     rc, rvf, rcnt, rp2v = oracle.voxelize(xyz, 0.05, synth.normal((len(xyz), 8), 3, dtype="bf16"), "bf16", batch)
+    np.testing.assert_array_equal(c, rc)
+    np.testing.assert_array_equal(cnt, rcnt)
+    np.testing.assert_array_equal(p2v, rp2v)
+    np.testing.assert_array_equal(vf, rvf)
+
+
+def test_voxelize_wide_keys_many_tiles(spv):
+    """Keys past 32 significant bits (4 batches over +-1600 m) and over 524k of
+    them: every pass of the sort runs over more than 256 tiles, with scanned offsets."""
+    rng = np.random.default_rng(4444)
+    xyz = rng.uniform(-1600.0, 1600.0, size=(600_000, 3)).astype(np.float32)
+    xyz[::5] = xyz[1::5][: len(xyz[::5])]  # some shared voxels
+    batch = rng.integers(0, 4, size=len(xyz)).astype(np.int32)
+    batch[::5] = batch[1::5][: len(batch[::5])]
+    feat = synth.normal((len(xyz), 8), 5, dtype="bf16")
+    c, vf, cnt, p2v, _ = run_voxelize(spv, xyz, 0.05, feat, "bf16", batch)
+    rc, rvf, rcnt, rp2v = oracle.voxelize(xyz, 0.05, feat, "bf16", batch)
+    assert len(xyz) > 256 * 2048 and len(rc) > 400_000  # more than 256 sort tiles
     np.testing.assert_array_equal(c, rc)
     np.testing.assert_array_equal(cnt, rcnt)
     np.testing.assert_array_equal(p2v, rp2v)
