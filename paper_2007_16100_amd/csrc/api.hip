@@ -356,9 +356,38 @@ spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_pa
     auto mark = [&](int i) {
         if (prof) hipEventRecord((hipEvent_t)p->events[i], s);
     };
+    // devoxelization arguments (its MLP weight is packed by the prologue)
+    DevoxArgs a;
+    a.table = L.vox.table;
+    a.stride_log2 = 0;
+    a.xyz = xyz;
+    a.batch = batch;
+    a.n = n;
+    a.voxel_size = p->voxel_size;
+    a.mode = p->devox_mode;
+    a.vfeat = nullptr;  // set once the convs have run
+    a.C = C;
+    a.pfeat = feat;
+    a.Cp = C;
+    a.Wp = p->Wp;
+    a.scale_p = p->scale_p;
+    a.shift_p = p->shift_p;
+    a.relu_p = p->relu_p;
+    a.out = out;
+    a.dt = dt;
+    a.corner_idx = nullptr;
+    a.corner_w = nullptr;
+    a.h = L.h;
     mark(0);
+    // one launch clears the voxel table and packs every weight of the block
+    PackJob jobs[kMaxPackJobs];
+    int njobs = 0;
+    for (int l = 0; l < p->n_convs; ++l) jobs[njobs++] = conv_pack_job(27, p->W[l], L.wpack_conv[l], C, C, dt);
+    jobs[njobs++] = devox_pack_job(a, L.wpack_mlp);
+    launch_block_prologue(s, L.h, L.vox.table, jobs, njobs);
     // voxel branch: Eq. 1-2 into the hashed grid
-    launch_voxelize(s, L.vox, xyz, batch, n, p->voxel_size, feat, C, dt, L.coords, L.va, L.counts, L.pt2vox, L.m_dev);
+    launch_voxelize(s, L.vox, xyz, batch, n, p->voxel_size, feat, C, dt, L.coords, L.va, L.counts, L.pt2vox, L.m_dev,
+                    true);
     mark(1);
     // one kernel map for both convs, probing the voxelization's table; the
     // neighbour-table conv needs only the table, the other kernels the pairs
@@ -371,7 +400,6 @@ spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_pa
         mark(2);
         launch_conv_plan(s, L.plan, L.off, L.pairs, 27, 0, L.pair_cap, nn);
     }
-    for (int l = 0; l < p->n_convs; ++l) launch_conv_pack(s, 27, p->W[l], L.wpack_conv[l], C, C, dt);
     mark(3);
     void* cur = L.va;
     void* nxt = L.vb;
@@ -385,28 +413,8 @@ spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_pa
     }
     if (p->n_convs == 1) mark(5);
     // devoxelize onto the points + point MLP + fusion by addition
-    DevoxArgs a;
-    a.table = L.vox.table;
-    a.stride_log2 = 0;
-    a.xyz = xyz;
-    a.batch = batch;
-    a.n = n;
-    a.voxel_size = p->voxel_size;
-    a.mode = p->devox_mode;
     a.vfeat = cur;
-    a.C = C;
-    a.pfeat = feat;
-    a.Cp = C;
-    a.Wp = p->Wp;
-    a.scale_p = p->scale_p;
-    a.shift_p = p->shift_p;
-    a.relu_p = p->relu_p;
-    a.out = out;
-    a.dt = dt;
-    a.corner_idx = nullptr;
-    a.corner_w = nullptr;
-    a.h = L.h;
-    launch_devox(s, a, L.wpack_mlp, L.cidx, L.cw);
+    launch_devox(s, a, L.wpack_mlp, L.cidx, L.cw, true);
     mark(6);
     spv_status st = hip_check();
     if (st || !m_host) return st;

@@ -160,28 +160,57 @@ void launch_conv_plan(hipStream_t s, const ConvPlan& p, const int32_t* off, cons
 // i.e. lane l carries output channel nb*16 + l%16 and 8 consecutive input
 // channels: the A operand of D = W^T G^T (or the B operand of D = G W).
 // ---------------------------------------------------------------------------
-__global__ void k_pack_w(const uint16_t* W, int K3, int Cin, int Cout, int KCH, int NB, uint4* wpack) {
-    int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    int64_t total = (int64_t)K3 * KCH * NB * 64;
-    if (t >= total) return;
-    int lane = (int)(t & 63);
+// fragment t of the packing (t = ((k * KCH + kc) * NB + nb) * 64 + lane)
+__device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int Cout, int KCH, int NB, int64_t t) {
+    const int lane = (int)(t & 63);
     int64_t f = t >> 6;
-    int nb = (int)(f % NB);
+    const int nb = (int)(f % NB);
     f /= NB;
-    int kc = (int)(f % KCH);
-    int k = (int)(f / KCH);
-    int col = nb * 16 + (lane & 15);
-    int ci0 = kc * 32 + 8 * (lane >> 4);
+    const int kc = (int)(f % KCH);
+    const int k = (int)(f / KCH);
+    const int col = nb * 16 + (lane & 15);
+    const int ci0 = kc * 32 + 8 * (lane >> 4);
     uint32_t w[4];
     for (int e = 0; e < 4; ++e) {
         uint32_t lo = 0, hi = 0;
-        int c0 = ci0 + 2 * e, c1 = ci0 + 2 * e + 1;
+        const int c0 = ci0 + 2 * e, c1 = ci0 + 2 * e + 1;
         if (c0 < Cin) lo = W[((int64_t)k * Cin + c0) * Cout + col];
         if (c1 < Cin) hi = W[((int64_t)k * Cin + c1) * Cout + col];
         w[e] = lo | (hi << 16);
     }
-    wpack[t] = make_uint4(w[0], w[1], w[2], w[3]);
+    return make_uint4(w[0], w[1], w[2], w[3]);
 }
+
+__global__ void k_pack_w(const uint16_t* W, int K3, int Cin, int Cout, int KCH, int NB, uint4* wpack) {
+    const int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (t >= (int64_t)K3 * KCH * NB * 64) return;
+    wpack[t] = pack_fragment(W, Cin, Cout, KCH, NB, t);
+}
+
+struct PrologueArgs {
+    Header* h;
+    uint64_t* keys;
+    uint32_t nslots;
+    int njobs;
+    PackJob job[kMaxPackJobs];
+};
+
+// table + header clear and weight packing of a block call, grid-stride
+__global__ __launch_bounds__(256) void k_block_prologue(PrologueArgs a) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        a.h->status = 0;
+        a.h->m = 0;
+        for (int i = 0; i < 4; ++i) a.h->aux[i] = 0;
+    }
+    const int64_t t0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = t0; i < (int64_t)a.nslots; i += stride) a.keys[i] = kEmpty;
+    for (int j = 0; j < a.njobs; ++j) {
+        const PackJob& q = a.job[j];
+        for (int64_t t = t0; t < q.total; t += stride) q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.KCH, q.NB, t);
+    }
+}
+
 
 static int conv_kch(int Cin);
 
@@ -605,6 +634,30 @@ void launch_conv_pack(hipStream_t s, int K3, const void* W, void* wpack, int Cin
     int KCH = conv_kch(Cin), NB = Cout / 16;
     int64_t tot = (int64_t)K3 * KCH * NB * 64;
     k_pack_w<<<blocks_for(tot, 256), 256, 0, s>>>((const uint16_t*)W, K3, Cin, Cout, KCH, NB, (uint4*)wpack);
+}
+
+PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int dt) {
+    PackJob q{(const uint16_t*)W, (uint4*)wpack, K3, Cin, Cout, 0, 0, 0};
+    if (!conv_mfma_supported(Cin, Cout, dt)) return q;
+    q.KCH = conv_kch(Cin);
+    q.NB = Cout / 16;
+    q.total = (int64_t)K3 * q.KCH * q.NB * 64;
+    return q;
+}
+
+void launch_block_prologue(hipStream_t s, Header* h, Table t, const PackJob* jobs, int njobs) {
+    PrologueArgs a;
+    a.h = h;
+    a.keys = t.keys;
+    a.nslots = t.mask + 1;
+    a.njobs = 0;
+    int64_t work = a.nslots;
+    for (int j = 0; j < njobs && a.njobs < kMaxPackJobs; ++j)
+        if (jobs[j].total > 0) {
+            a.job[a.njobs++] = jobs[j];
+            work += jobs[j].total;
+        }
+    k_block_prologue<<<blocks_for(work, 256 * 2), 256, 0, s>>>(a);
 }
 
 // the MFMA kernel addresses the input rows and the pair list with 32-bit buffer offsets

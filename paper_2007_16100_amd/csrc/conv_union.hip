@@ -212,14 +212,14 @@ bool union_supported(int K3, int Cin, int Cout, int dt) {
     return Cin == 32 || Cin == 64 || Cin == 96 || Cin == 128;
 }
 
-// Launch shape per width: 12 waves of 2 blocks (384 rows per workgroup, about
-// one workgroup per CU on ~10^5-voxel scans), phases of as many offsets as fit
-// in 128 KB of LDS.
+// Launch shape per width: 11 waves of 2 blocks (352 rows per workgroup: a
+// ~9*10^4-voxel scan gives ~250 workgroups, one round over the 256 CUs with
+// nearly every CU busy), phases of as many offsets as fit in 128 KB of LDS.
 template <int DT, int KCH>
 static void launch_union_c(hipStream_t s, const ConvPlan& p, const void* in, int64_t in_rows, const void* wpack,
                            const float* scale, const float* shift, int relu, void* out) {
     constexpr int NB = 2 * KCH;  // C = 32 * KCH
-    constexpr int RB = 2, NW = 12;
+    constexpr int RB = 2, NW = 11;
     constexpr int FR = KCH * NB;
     constexpr int PH = (128 / FR) < kUK3 ? (128 / FR) : kUK3;  // 27, 14, 7, 4 for C = 32, 64, 96, 128
     constexpr int64_t rows_wg = (int64_t)NW * RB * 16;

@@ -363,10 +363,21 @@ static void launch_devox_dt(hipStream_t s, const DevoxArgs& a, const void* wpack
 
 __global__ void k_pack_wp(const uint16_t* W, int Cin, int Cout, int KCH, int NB, uint4* wpack);
 
-void launch_devox(hipStream_t s, const DevoxArgs& a, void* wpack, int32_t* cidx_tmp, float* cw_tmp) {
+// the point-MLP weight [Cp][C] packed like a single-offset conv weight, when
+// the MFMA kernel runs with point features
+PackJob devox_pack_job(const DevoxArgs& a, void* wpack) {
+    PackJob q{(const uint16_t*)a.Wp, (uint4*)wpack, 1, a.Cp, a.C, 0, 0, 0};
+    if (a.n <= 0 || !a.pfeat || !devox_mfma_supported(a.C, a.Cp, a.dt)) return q;
+    q.KCH = (a.Cp + 31) / 32;
+    q.NB = a.C / 16;
+    q.total = (int64_t)q.KCH * q.NB * 64;
+    return q;
+}
+
+void launch_devox(hipStream_t s, const DevoxArgs& a, void* wpack, int32_t* cidx_tmp, float* cw_tmp, bool wp_packed) {
     if (a.n <= 0) return;
     if (devox_mfma_supported(a.C, a.pfeat ? a.Cp : 0, a.dt)) {
-        if (a.pfeat) {
+        if (a.pfeat && !wp_packed) {
             int KCH = (a.Cp + 31) / 32, NB = a.C / 16;
             int64_t tot = (int64_t)KCH * NB * 64;
             k_pack_wp<<<blocks_for(tot, 256), 256, 0, s>>>((const uint16_t*)a.Wp, a.Cp, a.C, KCH, NB, (uint4*)wpack);

@@ -153,7 +153,8 @@ void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n);
 // coords/counts/pt2vox and (if feat) vfeat; m into h->m and *m_dev
 void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const int32_t* batch, int64_t n,
                      float voxel_size, const void* feat, int32_t C, int dt, int32_t* coords, void* vfeat,
-                     int32_t* counts, int32_t* pt2vox, int64_t* m_dev);
+                     int32_t* counts, int32_t* pt2vox, int64_t* m_dev,
+                     bool table_cleared = false);
 
 // --- kernel map (kmap.hip) -----------------------------------------------------
 struct KmapWs {
@@ -208,6 +209,19 @@ bool conv_mfma_supported(int Cin, int Cout, int dt);
 void* plan_wpack_ws(Arena& a, int K3, int Cin, int Cout);
 // pack W [K3][Cin][Cout] into MFMA operand fragments (no-op when the vector-ALU path runs)
 void launch_conv_pack(hipStream_t s, int K3, const void* W, void* wpack, int Cin, int Cout, int dt);
+// One weight packing into MFMA operand fragments, as a job for the block prologue
+// (total = 0: nothing to pack, the layer runs on a kernel that reads W itself).
+struct PackJob {
+    const uint16_t* W;  // [K3][Cin][Cout]
+    uint4* wpack;
+    int K3, Cin, Cout, KCH, NB;
+    int64_t total;      // fragments * 64 lanes
+};
+PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int dt);
+// The first kernel of a block call: clears the voxel table and the status
+// header, and packs up to kMaxPackJobs weights, in one grid-stride launch.
+constexpr int kMaxPackJobs = 3;
+void launch_block_prologue(hipStream_t s, Header* h, Table t, const PackJob* jobs, int njobs);
 // the convolution itself (one kernel); wpack must have been packed from W
 void launch_conv_run(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows, const int32_t* pairs,
                      int64_t pair_bound, int transposed, const void* W, const void* wpack, const float* scale,
@@ -238,6 +252,9 @@ struct DevoxArgs {
 };
 bool devox_mfma_supported(int C, int Cp, int dt);
 void* plan_devox_ws(Arena& a, int C, int Cp);
-void launch_devox(hipStream_t s, const DevoxArgs& a, void* wpack, int32_t* cidx_tmp, float* cw_tmp);
+// wp_packed: the point-MLP weight is already in wpack (a block prologue packed it)
+void launch_devox(hipStream_t s, const DevoxArgs& a, void* wpack, int32_t* cidx_tmp, float* cw_tmp,
+                  bool wp_packed = false);
+PackJob devox_pack_job(const DevoxArgs& a, void* wpack);
 
 }  // namespace spv

@@ -186,8 +186,8 @@ static void launch_mean(hipStream_t s, const VoxelizeWs& w, int64_t n, const voi
 
 void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const int32_t* batch, int64_t n,
                      float voxel_size, const void* feat, int32_t C, int dt, int32_t* coords, void* vfeat,
-                     int32_t* counts, int32_t* pt2vox, int64_t* m_dev) {
-    launch_clear(s, w.h, w.table, true);
+                     int32_t* counts, int32_t* pt2vox, int64_t* m_dev, bool table_cleared) {
+    if (!table_cleared) launch_clear(s, w.h, w.table, true);
     const unsigned nins = n > 0 ? blocks_for(n, kAppendThreads) : 0u;
     if (n > 0) k_vox_insert<<<nins, kAppendThreads, 0, s>>>(w.h, w.table, w.sort, w.pkey, xyz, batch, n, voxel_size);
     launch_sort_keys(s, w.sort, &w.h->m, n, nins);
