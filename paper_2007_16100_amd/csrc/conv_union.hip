@@ -29,13 +29,14 @@ __device__ __forceinline__ void static_for(F&& f) {
 // inside a phase the waves never synchronize and load no weights, each one
 // streaming its own rows:
 //   step k: loads the neighbour indices of offset k+3 and gathers the rows of
-//           offset k+1 (a block with no neighbour at that offset loads
-//           nothing; a lane whose row has none gets zeros), then multiplies the
-//           rows gathered for offset k by W[k] one 32-channel slab at a time,
-//           skipping blocks without a neighbour at k.
-// All other loads are ordinary vector-memory loads the compiler sees, so its
-// waits (which count outstanding loads in issue order) stay exact: the weight
-// copies it does not see are all complete (vmcnt 0) before the phase starts.
+//           offset k+1 (a block with no neighbour at that offset, or a lane
+//           whose row has none, reads zeros from outside the buffer), then
+//           multiplies the rows gathered for offset k by W[k] one 32-channel
+//           slab at a time, skipping blocks without a neighbour at k.
+// All other loads are ordinary vector-memory loads the compiler sees, the same
+// number every step, so its waits (which count outstanding loads in issue
+// order) stay exact and a step waits for its own rows only: the weight copies
+// it does not see are all complete (vmcnt 0) before the phase starts.
 constexpr int kUK3 = 27;
 constexpr int kNAhead = 3;  // neighbour indices: steps ahead
 constexpr int kRAhead = 1;  // gathered rows: steps ahead
@@ -101,20 +102,20 @@ __global__ __launch_bounds__(64 * NW) void k_conv_union(
             dst[b] = __builtin_amdgcn_raw_buffer_load_b32(nb_rs, nboff[b] + (uint32_t)k * 4u, 0, 0);
     };
     // gathered rows of offset kr (16-byte chunks g + 4 kc of row i)
+    // Every step issues the same RB * KCH loads, so the compiler's vmcnt waits
+    // are exact and a step waits for its own rows only, never for the rows it
+    // prefetches: a block without a neighbour at kr, or a lane whose row has
+    // none, loads from an out-of-range offset, which returns zeros and touches
+    // no memory.
     auto load_rows = [&](int kr, const int (&nb1)[RB], i32x4 (&dst)[RB][KCH]) __attribute__((always_inline)) {
 #pragma unroll
         for (int b = 0; b < RB; ++b) {
-            if (!((umask[b] >> kr) & 1u)) continue;
             const uint32_t i = (uint32_t)(nb1[b] - 1);  // stored as row + 1; 0 = absent
-            const bool have = i < in_rows32;
+            const bool have = ((umask[b] >> kr) & 1u) && i < in_rows32;
+            const uint32_t base = have ? i * row_bytes + (uint32_t)g * 16u : kOutOfRange;
 #pragma unroll
-            for (int kc = 0; kc < KCH; ++kc) dst[b][kc] = i32x4{0, 0, 0, 0};
-            if (have) {
-                const uint32_t base = i * row_bytes + (uint32_t)g * 16u;
-#pragma unroll
-                for (int kc = 0; kc < KCH; ++kc)
-                    dst[b][kc] = __builtin_amdgcn_raw_buffer_load_b128(in_rs, base + (uint32_t)kc * 64u, 0, 0);
-            }
+            for (int kc = 0; kc < KCH; ++kc)
+                dst[b][kc] = __builtin_amdgcn_raw_buffer_load_b128(in_rs, base + (uint32_t)kc * 64u, 0, 0);
         }
     };
 
