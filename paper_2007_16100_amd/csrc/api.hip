@@ -282,9 +282,9 @@ spv_status spv_sparse_conv(void* stream, void* ws, size_t ws_bytes, const void* 
     if (m_out_cap == 0) return SPV_OK;
     hipStream_t s = (hipStream_t)stream;
     L.p.m_out_dev = m_out_dev;
-    launch_clear_header(s, L.h);
-    launch_conv_plan(s, L.p, off, pairs, K3, transposed, pair_cap, in_rows);
-    launch_conv_pack(s, K3, W, L.wpack, Cin, Cout, dt);
+    // the plan clears the status header first and packs W in one of its launches
+    launch_conv_plan(s, L.p, off, pairs, K3, transposed, pair_cap, in_rows,
+                     conv_pack_job(K3, W, L.wpack, Cin, Cout, dt), true);
     launch_conv_run(s, L.p, in, Cin, in_rows, pairs, pair_cap, transposed, W, L.wpack, scale, shift, relu, out, Cout,
                     dt);
     return hip_check();
@@ -398,7 +398,7 @@ spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_pa
     } else {
         launch_kernel_map(s, L.map, false, L.coords, L.m_dev, nn, 3, 1, nullptr, nullptr, L.off, L.pairs, L.pair_cap);
         mark(2);
-        launch_conv_plan(s, L.plan, L.off, L.pairs, 27, 0, L.pair_cap, nn);
+        launch_conv_plan(s, L.plan, L.off, L.pairs, 27, 0, L.pair_cap, nn, PackJob{});
     }
     mark(3);
     void* cur = L.va;

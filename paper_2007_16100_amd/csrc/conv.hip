@@ -61,11 +61,40 @@ __device__ inline int64_t tile_of(int64_t j, int64_t m, int64_t nt, int T) {
     return j / T;
 }
 
+// fragment t of the packing (t = ((k * KCH + kc) * NB + nb) * 64 + lane)
+__device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int Cout, int KCH, int NB, int64_t t) {
+    const int lane = (int)(t & 63);
+    int64_t f = t >> 6;
+    const int nb = (int)(f % NB);
+    f /= NB;
+    const int kc = (int)(f % KCH);
+    const int k = (int)(f / KCH);
+    const int col = nb * 16 + (lane & 15);
+    const int ci0 = kc * 32 + 8 * (lane >> 4);
+    uint32_t w[4];
+    for (int e = 0; e < 4; ++e) {
+        uint32_t lo = 0, hi = 0;
+        const int c0 = ci0 + 2 * e, c1 = ci0 + 2 * e + 1;
+        if (c0 < Cin) lo = W[((int64_t)k * Cin + c0) * Cout + col];
+        if (c1 < Cin) hi = W[((int64_t)k * Cin + c1) * Cout + col];
+        w[e] = lo | (hi << 16);
+    }
+    return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// a weight packing run alongside another kernel's work (grid-stride)
+__device__ inline void pack_job_run(const PackJob& q) {
+    for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < q.total; t += (int64_t)gridDim.x * blockDim.x)
+        q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.KCH, q.NB, t);
+}
+
 // For every offset k and tile t in [0, nt]: bnd[k][t] = first pair of offset k
 // with tile_of(out) >= t.  Each pair writes the entries of the tiles that begin
 // at it; one extra item per offset writes the entries past its last pair.
 __global__ void k_conv_bounds(const int32_t* off, const int32_t* pairs, int K3, int transposed, int64_t pair_bound,
-                              const int64_t* m_out_dev, int64_t cap, int T, int64_t ntc, int32_t* bnd, Header* h) {
+                              const int64_t* m_out_dev, int64_t cap, int T, int64_t ntc, int32_t* bnd, Header* h,
+                              PackJob pk) {
+    pack_job_run(pk);
     __shared__ int32_t soff[kMaxK3 + 1];
     if (threadIdx.x <= K3) soff[threadIdx.x] = off[threadIdx.x];
     __syncthreads();
@@ -83,7 +112,7 @@ __global__ void k_conv_bounds(const int32_t* off, const int32_t* pairs, int K3, 
             const int64_t j = pairs[2 * p + osel];
             const int64_t cur = tile_of(j, m, nt, T);
             int64_t prev = -1;
-            if (p != soff[k]) {
+            if (p > 0 && p != soff[k]) {
                 const int64_t jp = pairs[2 * (p - 1) + osel];
                 prev = tile_of(jp, m, nt, T);
                 if (j <= jp) raise_flag(h, j < jp ? kFlagUnsorted : kFlagDuplicate);
@@ -95,14 +124,24 @@ __global__ void k_conv_bounds(const int32_t* off, const int32_t* pairs, int K3, 
             int64_t lo = soff[k], hi = soff[k + 1];
             if (lo > total) lo = total;
             if (hi > total) hi = total;
+            if (lo < 0) lo = 0;
+            if (hi < 0) hi = 0;
             const int64_t prev = (hi > lo) ? tile_of(pairs[2 * (hi - 1) + osel], m, nt, T) : -1;
             for (int64_t t = prev + 1; t <= nt; ++t) bnd[k * stride + t] = (int32_t)hi;
         }
     }
 }
 
-// neighbour table: nbr[j][k] = i + 1 for every pair (i, j) of offset k, 0 elsewhere
-__global__ void k_nbr_clear(int32_t* nbr, const int64_t* m_out_dev, int64_t cap, int K3) {
+// neighbour table: nbr[j][k] = i + 1 for every pair (i, j) of offset k, 0 elsewhere.
+// The clearing launch also clears the status header (h, when given) and runs
+// the layer's weight packing; the scatter that follows may then raise flags.
+__global__ void k_nbr_clear(int32_t* nbr, const int64_t* m_out_dev, int64_t cap, int K3, Header* h, PackJob pk) {
+    if (h && blockIdx.x == 0 && threadIdx.x == 0) {
+        h->status = 0;
+        h->m = 0;
+        for (int i = 0; i < 4; ++i) h->aux[i] = 0;
+    }
+    pack_job_run(pk);
     const int64_t n = clamp_rows(m_out_dev, cap) * K3;
     for (int64_t e = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4; e < n;
          e += (int64_t)gridDim.x * blockDim.x * 4) {
@@ -129,7 +168,7 @@ __global__ void k_nbr_scatter(const int32_t* off, const int32_t* pairs, int K3, 
         const int k = pair_offset(soff, K3, p);
         const int64_t i = transposed ? pairs[2 * p + 1] : pairs[2 * p];
         const int64_t j = transposed ? pairs[2 * p] : pairs[2 * p + 1];
-        if (p != soff[k]) {
+        if (p > 0 && p != soff[k]) {
             const int64_t jp = transposed ? pairs[2 * (p - 1)] : pairs[2 * (p - 1) + 1];
             if (j <= jp) raise_flag(h, j < jp ? kFlagUnsorted : kFlagDuplicate);
         }
@@ -138,18 +177,19 @@ __global__ void k_nbr_scatter(const int32_t* off, const int32_t* pairs, int K3, 
 }
 
 void launch_conv_plan(hipStream_t s, const ConvPlan& p, const int32_t* off, const int32_t* pairs, int K3,
-                      int transposed, int64_t pair_bound, int64_t in_rows) {
+                      int transposed, int64_t pair_bound, int64_t in_rows, const PackJob& pk, bool clear_header) {
     unsigned g = blocks_for(pair_bound + K3, 256);
     if (g > 2048) g = 2048;
     if (p.use_union) {
         unsigned gc = blocks_for(p.m_cap * K3, 1024);
         if (gc > 2048) gc = 2048;
-        k_nbr_clear<<<gc, 256, 0, s>>>(p.nbr, p.m_out_dev, p.m_cap, K3);
+        k_nbr_clear<<<gc, 256, 0, s>>>(p.nbr, p.m_out_dev, p.m_cap, K3, clear_header ? p.h : nullptr, pk);
         k_nbr_scatter<<<g, 256, 0, s>>>(off, pairs, K3, transposed, pair_bound, p.m_out_dev, p.m_cap, in_rows, p.nbr,
                                         p.h);
     } else {
+        if (clear_header) launch_clear_header(s, p.h);
         k_conv_bounds<<<g, 256, 0, s>>>(off, pairs, K3, transposed, pair_bound, p.m_out_dev, p.m_cap, p.tile_rows,
-                                        p.ntile_cap, p.bnd, p.h);
+                                        p.ntile_cap, p.bnd, p.h, pk);
     }
 }
 
@@ -160,27 +200,6 @@ void launch_conv_plan(hipStream_t s, const ConvPlan& p, const int32_t* off, cons
 // i.e. lane l carries output channel nb*16 + l%16 and 8 consecutive input
 // channels: the A operand of D = W^T G^T (or the B operand of D = G W).
 // ---------------------------------------------------------------------------
-// fragment t of the packing (t = ((k * KCH + kc) * NB + nb) * 64 + lane)
-__device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int Cout, int KCH, int NB, int64_t t) {
-    const int lane = (int)(t & 63);
-    int64_t f = t >> 6;
-    const int nb = (int)(f % NB);
-    f /= NB;
-    const int kc = (int)(f % KCH);
-    const int k = (int)(f / KCH);
-    const int col = nb * 16 + (lane & 15);
-    const int ci0 = kc * 32 + 8 * (lane >> 4);
-    uint32_t w[4];
-    for (int e = 0; e < 4; ++e) {
-        uint32_t lo = 0, hi = 0;
-        const int c0 = ci0 + 2 * e, c1 = ci0 + 2 * e + 1;
-        if (c0 < Cin) lo = W[((int64_t)k * Cin + c0) * Cout + col];
-        if (c1 < Cin) hi = W[((int64_t)k * Cin + c1) * Cout + col];
-        w[e] = lo | (hi << 16);
-    }
-    return make_uint4(w[0], w[1], w[2], w[3]);
-}
-
 __global__ void k_pack_w(const uint16_t* W, int K3, int Cin, int Cout, int KCH, int NB, uint4* wpack) {
     const int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
     if (t >= (int64_t)K3 * KCH * NB * 64) return;

@@ -203,8 +203,13 @@ struct ConvPlan {
     Header* h;          // status word (unsorted or out-of-range pairs)
 };
 void plan_conv_ws(Arena& a, ConvPlan& p, int64_t m_out_cap, int K3, int Cin, int Cout, int dt);
+struct PackJob;
+// plans the conv on a kernel map (neighbour table or tile bounds), runs the
+// weight packing pk (total = 0: none) in one of its launches and, with
+// clear_header, first clears the status header the plan may raise flags in
 void launch_conv_plan(hipStream_t s, const ConvPlan& p, const int32_t* off, const int32_t* pairs, int K3,
-                      int transposed, int64_t pair_bound, int64_t in_rows);
+                      int transposed, int64_t pair_bound, int64_t in_rows, const PackJob& pk,
+                      bool clear_header = false);
 bool conv_mfma_supported(int Cin, int Cout, int dt);
 void* plan_wpack_ws(Arena& a, int K3, int Cin, int Cout);
 // pack W [K3][Cin][Cout] into MFMA operand fragments (no-op when the vector-ALU path runs)
