@@ -17,8 +17,9 @@
 // The 3x3x3 convolution consumes the neighbour table directly, so a block that
 // only needs the convolution stops after pass 1.
 // Stride 2 (K = 2): the output voxels are the distinct floor(c/2), deduplicated
-// in a second hash table and radix-sorted into canonical order; then a probe /
-// count pass and a write pass over 256 outputs per block as above.
+// in a second hash table and radix-sorted into canonical order; then the pairs
+// are a stable partition of the inputs by coordinate parity (a count pass, one
+// scan, a write pass with one coarse-table lookup per input).
 #include "spv_internal.hpp"
 
 namespace spv {
@@ -46,7 +47,6 @@ void plan_kmap_ws(Arena& a, KmapWs& w, int64_t m_cap, int K, int stride, bool ow
         w.coarse = Table{nullptr, nullptr, 0};
     }
     size_t nblk = blocks_for(mc, K == 3 ? kNbrVox : kMapThreads);
-    w.mask = a.take<uint32_t>(mc);
     w.bcnt = a.take<uint32_t>(K3 * nblk);
     w.bbase = a.take<uint32_t>(K3 * nblk + 1);
     w.scan_tmp = a.take<int32_t>(scan_tmp_entries((int64_t)K3 * nblk));
@@ -138,91 +138,70 @@ __global__ void k_map_coarse_rank(SortBufs sb, Table coarse, const int64_t* cnt,
     out_coords[4 * r + 3] = key_z(key);
 }
 
-// pass 1: offset masks + per-(offset, block) counts
-template <int K, int S>
-__global__ __launch_bounds__(kMapThreads) void k_map_mask(Table fine, const int32_t* out_coords, const int64_t* m_out,
-                                                          int64_t cap, uint32_t* mask, uint32_t* bcnt) {
-    constexpr int K3 = K * K * K;
-    __shared__ uint32_t cnt[K3];
-    for (int k = threadIdx.x; k < K3; k += blockDim.x) cnt[k] = 0;
+// Stride 2 (K = 2): input voxel i is in exactly one pair, (i, j, k) with j the
+// index of floor(c_i / 2) and k = 4 (x & 1) + 2 (y & 1) + (z & 1).  Inside one
+// parity class, c -> floor(c / 2) is increasing, so offset k's pairs are the
+// class-k inputs in input order, already sorted by output: the map is a stable
+// partition of the inputs by parity (per-block class counts, one scan, then
+// every input written at its place).  No table of the inputs is needed.
+__device__ inline int parity_k(const int32_t* c) { return ((c[1] & 1) << 2) | ((c[2] & 1) << 1) | (c[3] & 1); }
+
+__global__ __launch_bounds__(kMapThreads) void k_s2_count(const int32_t* in_coords, const int64_t* m_in_dev,
+                                                          int64_t cap, uint32_t* bcnt) {
+    __shared__ uint32_t cnt[8];
+    if (threadIdx.x < 8) cnt[threadIdx.x] = 0;
     __syncthreads();
-    int64_t m = count_or_cap(m_out, cap);
-    int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    bool valid = j < m;
-    uint32_t bits = 0;
-    if (valid) {
-        const int32_t* c = out_coords + 4 * j;
-#pragma unroll
-        for (int k = 0; k < K3; ++k) {
-            int dx, dy, dz;
-            offset_delta<K>(k, dx, dy, dz);
-            if (K == 3 && k == 13) {
-                bits |= 1u << k;  // an output of a submanifold map is its own centre neighbour
-                continue;
-            }
-            int32_t i = table_find(fine, pack_key(c[0], S * c[1] + dx, S * c[2] + dy, S * c[3] + dz));
-            if (i >= 0) bits |= 1u << k;
-        }
-        mask[j] = bits;
-    }
+    const int64_t m = count_or_cap(m_in_dev, cap);
+    const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    const int k = i < m ? parity_k(in_coords + 4 * i) : -1;
     const int lane = threadIdx.x & 63;
 #pragma unroll
-    for (int k = 0; k < K3; ++k) {
-        uint64_t bal = __ballot((bits >> k) & 1);
-        if (lane == 0 && bal) atomicAdd(&cnt[k], (uint32_t)__popcll(bal));
+    for (int q = 0; q < 8; ++q) {
+        const uint64_t bal = __ballot(k == q);
+        if (lane == 0 && bal) atomicAdd(&cnt[q], (uint32_t)__popcll(bal));
     }
     __syncthreads();
-    for (int k = threadIdx.x; k < K3; k += blockDim.x) bcnt[k * gridDim.x + blockIdx.x] = cnt[k];
+    if (threadIdx.x < 8) bcnt[threadIdx.x * gridDim.x + blockIdx.x] = cnt[threadIdx.x];  // offset-major
 }
 
-// pass 2: pairs at their final, sorted positions
-template <int K, int S>
-__global__ __launch_bounds__(kMapThreads) void k_map_write(Header* h, Table fine, const int32_t* out_coords,
-                                                           const int64_t* m_out, int64_t cap, const uint32_t* mask,
-                                                           const uint32_t* bbase, int32_t* off, int32_t* pairs,
-                                                           int64_t pair_cap) {
-    constexpr int K3 = K * K * K;
+__global__ __launch_bounds__(kMapThreads) void k_s2_write(Header* h, Table coarse, const int32_t* in_coords,
+                                                          const int64_t* m_in_dev, int64_t cap, const uint32_t* bbase,
+                                                          int32_t* off, int32_t* pairs, int64_t pair_cap) {
     constexpr int NW = kMapThreads / 64;
-    __shared__ uint32_t wtot[NW][K3];
+    __shared__ uint32_t wtot[NW][8];
     const uint32_t nblk = gridDim.x;
     if (blockIdx.x == 0) {
-        for (int k = threadIdx.x; k <= K3; k += blockDim.x) off[k] = (int32_t)bbase[k * nblk];
+        for (int k = threadIdx.x; k <= 8; k += blockDim.x) off[k] = (int32_t)bbase[k * nblk];
     }
-    int64_t m = count_or_cap(m_out, cap);
-    int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    bool valid = j < m;
-    uint32_t bits = valid ? mask[j] : 0u;
+    const int64_t m = count_or_cap(m_in_dev, cap);
+    const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    const bool valid = i < m;
+    int c[4] = {0, 0, 0, 0};
+    if (valid) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) c[d] = in_coords[4 * i + d];
+    }
+    const int k = valid ? parity_k(c) : -1;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    uint32_t rank[K3];
+    uint32_t rank = 0;
 #pragma unroll
-    for (int k = 0; k < K3; ++k) {
-        uint64_t bal = __ballot((bits >> k) & 1);
-        rank[k] = (uint32_t)__popcll(bal & lt);
-        if (lane == 0) wtot[wave][k] = (uint32_t)__popcll(bal);
+    for (int q = 0; q < 8; ++q) {
+        const uint64_t bal = __ballot(k == q);
+        if (k == q) rank = (uint32_t)__popcll(bal & lt);
+        if (lane == 0) wtot[wave][q] = (uint32_t)__popcll(bal);
     }
     __syncthreads();
     if (!valid) return;
-    const int32_t* c = out_coords + 4 * j;
-#pragma unroll
-    for (int k = 0; k < K3; ++k) {
-        if (!((bits >> k) & 1)) continue;
-        uint32_t pos = bbase[k * nblk + blockIdx.x] + rank[k];
-        for (int w = 0; w < wave; ++w) pos += wtot[w][k];
-        int32_t i;
-        if (K == 3 && k == 13) {
-            i = (int32_t)j;
-        } else {
-            int dx, dy, dz;
-            offset_delta<K>(k, dx, dy, dz);
-            i = table_find(fine, pack_key(c[0], S * c[1] + dx, S * c[2] + dy, S * c[3] + dz));
-        }
-        if ((int64_t)pos < pair_cap) {
-            pairs[2 * (int64_t)pos] = i;
-            pairs[2 * (int64_t)pos + 1] = (int32_t)j;
-        } else {
-            raise_flag(h, kFlagCapacity);
-        }
+    uint32_t pos = bbase[k * nblk + blockIdx.x] + rank;
+    for (int w = 0; w < wave; ++w) pos += wtot[w][k];
+    // floor(c / 2) by arithmetic shift, as the coarse keys were made
+    const int32_t j = table_find(coarse, pack_key(c[0], c[1] >> 1, c[2] >> 1, c[3] >> 1));
+    if ((int64_t)pos < pair_cap) {
+        pairs[2 * (int64_t)pos] = (int32_t)i;
+        pairs[2 * (int64_t)pos + 1] = j;
+    } else {
+        raise_flag(h, kFlagCapacity);
     }
 }
 
@@ -318,11 +297,10 @@ void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const in
     const int64_t mc = m_cap > 0 ? m_cap : 1;
     const unsigned nblk = blocks_for(mc, kMapThreads);
     const int K3 = K * K * K;
-    if (build_fine) {
+    if (build_fine && K == 3) {  // a stride-2 map needs no table of its inputs
         launch_clear(s, w.h, w.fine, false);
         launch_table_build(s, w.h, w.fine, in_coords, m_in_dev, m_cap);
     }
-    const int32_t* oc = in_coords;
     if (stride == 2) {
         launch_clear(s, w.h, w.coarse, false);
         k_map_zero_i64<<<1, 1, 0, s>>>(w.m_out + 1);
@@ -332,7 +310,6 @@ void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const in
         launch_sort_keys(s, w.sort, w.m_out + 1, mc, nins);
         k_map_coarse_rank<<<nblk, kMapThreads, 0, s>>>(w.sort, w.coarse, w.m_out + 1, mc, out_coords, w.m_out,
                                                        m_out_dev);
-        oc = out_coords;
     }
     if (K == 3) {
         const unsigned nb3 = blocks_for(mc, kNbrVox);
@@ -341,10 +318,9 @@ void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const in
         launch_exclusive_scan(s, (const int32_t*)w.bcnt, (int32_t*)w.bbase, nullptr, (int64_t)27 * nb3, w.scan_tmp);
         k_map_pairs3<<<nb3, 256, 0, s>>>(w.h, w.nbr, w.m_out, mc, w.bbase, off, pairs, pair_cap);
     } else {
-        k_map_mask<2, 2><<<nblk, kMapThreads, 0, s>>>(w.fine, oc, w.m_out, mc, w.mask, w.bcnt);
+        k_s2_count<<<nblk, kMapThreads, 0, s>>>(in_coords, m_in_dev, mc, w.bcnt);
         launch_exclusive_scan(s, (const int32_t*)w.bcnt, (int32_t*)w.bbase, nullptr, (int64_t)K3 * nblk, w.scan_tmp);
-        k_map_write<2, 2><<<nblk, kMapThreads, 0, s>>>(w.h, w.fine, oc, w.m_out, mc, w.mask, w.bbase, off, pairs,
-                                                       pair_cap);
+        k_s2_write<<<nblk, kMapThreads, 0, s>>>(w.h, w.coarse, in_coords, m_in_dev, mc, w.bbase, off, pairs, pair_cap);
     }
 }
 

@@ -162,7 +162,6 @@ struct KmapWs {
     Table fine;         // table of the input coords (assigned by the caller when shared)
     Table coarse;       // stride 2: table of the output coords
     SortBufs sort;      // stride 2: coarse key sort
-    uint32_t* mask;     // [m_cap] offsets present per output (stride 2)
     uint32_t* bcnt;     // [K3 * nblk] per-block per-offset counts (k-major)
     uint32_t* bbase;    // [K3 * nblk + 1]
     int32_t* scan_tmp;  // [scan_tmp_entries(K3 * nblk)]
