@@ -252,9 +252,9 @@ spv_status spv_kernel_map(void* stream, void* ws, size_t ws_bytes, const int32_t
     if (need(layout_kmap(nullptr, 0, m_cap, K, stride, L), ws_bytes)) return SPV_ERR_CAPACITY;
     layout_kmap(ws, ws_bytes, m_cap, K, stride, L);
     hipStream_t s = (hipStream_t)stream;
-    launch_clear_header(s, L.h);
+    // the map's first launch clears the status header
     launch_kernel_map(s, L.w, true, in_coords, m_in_dev, m_cap, K, stride, out_coords, m_out_dev, off, pairs,
-                      pair_cap);
+                      pair_cap, true);
     spv_status st = hip_check();
     if (st || !total_host) return st;
     const int K3 = K * K * K;

@@ -8,31 +8,39 @@ namespace spv {
 // ---------------------------------------------------------------------------
 // table clear / build / lookup
 // ---------------------------------------------------------------------------
-__global__ void k_clear(Header* h, uint64_t* keys, uint32_t nslots, int clear_header) {
-    if (clear_header && blockIdx.x == 0 && threadIdx.x == 0) {
-        h->status = 0;
-        h->m = 0;
-        for (int i = 0; i < 4; ++i) h->aux[i] = 0;
+__global__ void k_clear(Header* h, uint64_t* keys, uint32_t nslots, int clear_header, int64_t* zero64) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        if (clear_header) {
+            h->status = 0;
+            h->m = 0;
+            for (int i = 0; i < 4; ++i) h->aux[i] = 0;
+        }
+        if (zero64) *zero64 = 0;
     }
     for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < nslots; i += gridDim.x * blockDim.x) keys[i] = kEmpty;
 }
 
-void launch_clear(hipStream_t s, Header* h, Table t, bool clear_header) {
+void launch_clear(hipStream_t s, Header* h, Table t, bool clear_header, int64_t* zero64) {
     uint32_t n = t.mask + 1;
     unsigned g = blocks_for(n, 256 * 4);
-    k_clear<<<g, 256, 0, s>>>(h, t.keys, n, clear_header ? 1 : 0);
+    k_clear<<<g, 256, 0, s>>>(h, t.keys, n, clear_header ? 1 : 0, zero64);
 }
 
-void launch_clear_header(hipStream_t s, Header* h) { k_clear<<<1, 64, 0, s>>>(h, nullptr, 0, 1); }
+void launch_clear_header(hipStream_t s, Header* h) { k_clear<<<1, 64, 0, s>>>(h, nullptr, 0, 1, nullptr); }
 
 __device__ inline bool coord_ok(const int32_t* c) {
     return c[0] >= 0 && c[0] <= kBatchMax && c[1] >= kCoordMin && c[1] <= kCoordMax && c[2] >= kCoordMin &&
            c[2] <= kCoordMax && c[3] >= kCoordMin && c[3] <= kCoordMax;
 }
 
-__global__ void k_table_build(Header* h, Table t, const int32_t* coords, const int64_t* count_dev, int64_t cap) {
+__global__ void k_table_build(Header* h, Table t, const int32_t* coords, const int64_t* count_dev, int64_t cap,
+                              int64_t* count_out, int64_t* count_out2) {
     int64_t count = count_dev ? *count_dev : cap;
     if (count > cap) count = cap;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {  // the count, for kernels that take it from here
+        if (count_out) *count_out = count;
+        if (count_out2) *count_out2 = count;
+    }
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count; i += (int64_t)gridDim.x * blockDim.x) {
         const int32_t* c = coords + 4 * i;
         if (!coord_ok(c)) {
@@ -52,8 +60,8 @@ __global__ void k_table_build(Header* h, Table t, const int32_t* coords, const i
 }
 
 void launch_table_build(hipStream_t s, Header* h, Table t, const int32_t* coords, const int64_t* count_dev,
-                        int64_t cap) {
-    k_table_build<<<blocks_for(cap, 256), 256, 0, s>>>(h, t, coords, count_dev, cap);
+                        int64_t cap, int64_t* count_out, int64_t* count_out2) {
+    k_table_build<<<blocks_for(cap, 256), 256, 0, s>>>(h, t, coords, count_dev, cap, count_out, count_out2);
 }
 
 __global__ void k_table_lookup(Table t, const int32_t* q, int64_t nq, int32_t* idx) {

@@ -80,8 +80,6 @@ __global__ void k_map_same_count(const int64_t* m_in_dev, int64_t cap, int64_t* 
     if (m_out_user) *m_out_user = m;
 }
 
-__global__ void k_map_zero_i64(int64_t* p) { *p = 0; }
-
 // stride 2: coarse keys into the coarse table; each block appends the keys it
 // created to the key list and records their per-field min / max for the sort
 __global__ __launch_bounds__(kAppendThreads) void k_map_coarse_insert(Header* h, Table coarse, SortBufs sb,
@@ -293,17 +291,21 @@ void launch_kernel_map_nbr(hipStream_t s, const KmapWs& w, const int32_t* coords
 
 void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const int32_t* in_coords,
                        const int64_t* m_in_dev, int64_t m_cap, int K, int stride, int32_t* out_coords,
-                       int64_t* m_out_dev, int32_t* off, int32_t* pairs, int64_t pair_cap) {
+                       int64_t* m_out_dev, int32_t* off, int32_t* pairs, int64_t pair_cap, bool clear_header) {
     const int64_t mc = m_cap > 0 ? m_cap : 1;
     const unsigned nblk = blocks_for(mc, kMapThreads);
     const int K3 = K * K * K;
-    if (build_fine && K == 3) {  // a stride-2 map needs no table of its inputs
-        launch_clear(s, w.h, w.fine, false);
-        launch_table_build(s, w.h, w.fine, in_coords, m_in_dev, m_cap);
+    const bool fine = build_fine && K == 3;  // a stride-2 map needs no table of its inputs
+    if (fine) {
+        // the table build also hands the output count (= the input count) on
+        launch_clear(s, w.h, w.fine, clear_header);
+        launch_table_build(s, w.h, w.fine, in_coords, m_in_dev, m_cap, w.m_out, m_out_dev);
+    } else if (clear_header && stride != 2) {
+        launch_clear_header(s, w.h);
     }
     if (stride == 2) {
-        launch_clear(s, w.h, w.coarse, false);
-        k_map_zero_i64<<<1, 1, 0, s>>>(w.m_out + 1);
+        // coarse table, status header and the coarse key counter in one launch
+        launch_clear(s, w.h, w.coarse, clear_header, w.m_out + 1);
         const unsigned nins = blocks_for(mc, kAppendThreads);
         k_map_coarse_insert<<<nins, kAppendThreads, 0, s>>>(w.h, w.coarse, w.sort, w.m_out + 1, in_coords, m_in_dev,
                                                             mc);
@@ -313,7 +315,7 @@ void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const in
     }
     if (K == 3) {
         const unsigned nb3 = blocks_for(mc, kNbrVox);
-        k_map_same_count<<<1, 1, 0, s>>>(m_in_dev, m_cap, w.m_out, m_out_dev);
+        if (!fine) k_map_same_count<<<1, 1, 0, s>>>(m_in_dev, m_cap, w.m_out, m_out_dev);
         k_map_nbr3<<<nb3, 256, 0, s>>>(w.fine, in_coords, w.m_out, mc, w.nbr, w.bcnt);
         launch_exclusive_scan(s, (const int32_t*)w.bcnt, (int32_t*)w.bbase, nullptr, (int64_t)27 * nb3, w.scan_tmp);
         k_map_pairs3<<<nb3, 256, 0, s>>>(w.h, w.nbr, w.m_out, mc, w.bbase, off, pairs, pair_cap);

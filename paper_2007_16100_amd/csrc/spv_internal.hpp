@@ -78,13 +78,16 @@ __device__ inline void block_minmax_record(int (&mn)[4], int (&mx)[4], int32_t* 
 
 // --- hash tables (hash_sort_scan.hip) ----------------------------------------
 // Clear the header (status, counters, key statistics) and a table's key slots.
-void launch_clear(hipStream_t s, Header* h, Table t, bool clear_header);
+// empties the table; clear_header also clears the status header; zero64 (when
+// given) is set to 0 in the same launch
+void launch_clear(hipStream_t s, Header* h, Table t, bool clear_header, int64_t* zero64 = nullptr);
 void launch_clear_header(hipStream_t s, Header* h);
 // Insert coords[0..count) (count = *count_dev or cap) with value = row index;
 // raises kFlagDuplicate on a repeated coordinate, kFlagRange on a coordinate
 // outside the key range.
+// count_out / count_out2 (when given) receive the clamped count in the same launch
 void launch_table_build(hipStream_t s, Header* h, Table t, const int32_t* coords, const int64_t* count_dev,
-                        int64_t cap);
+                        int64_t cap, int64_t* count_out = nullptr, int64_t* count_out2 = nullptr);
 void launch_table_lookup(hipStream_t s, Table t, const int32_t* q, int64_t nq, int32_t* idx);
 
 // --- radix sort of packed voxel keys (hash_sort_scan.hip) ---------------------
@@ -172,9 +175,10 @@ struct KmapWs {
 void plan_kmap_ws(Arena& a, KmapWs& w, int64_t m_cap, int K, int stride, bool own_fine_table, bool own_nbr);
 // build_fine: clear + insert the input coords into w.fine first (otherwise the
 // table must already map every input coordinate to its row)
+// clear_header: the map's first launch also clears the status header
 void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const int32_t* in_coords,
                        const int64_t* m_in_dev, int64_t m_cap, int K, int stride, int32_t* out_coords,
-                       int64_t* m_out_dev, int32_t* off, int32_t* pairs, int64_t pair_cap);
+                       int64_t* m_out_dev, int32_t* off, int32_t* pairs, int64_t pair_cap, bool clear_header = false);
 // submanifold 3x3x3 neighbour table only (pass 1, no pairs): nbr[j][k] = i + 1,
 // 0 where offset k of voxel j holds no voxel; w.fine must map every coordinate
 void launch_kernel_map_nbr(hipStream_t s, const KmapWs& w, const int32_t* coords, const int64_t* m_dev,
