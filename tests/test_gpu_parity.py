@@ -258,6 +258,25 @@ def test_kmap_random_small(spv, seed):
             np.testing.assert_array_equal(oc, roc)
 
 
+@pytest.mark.parametrize("K,stride", [(3, 1), (2, 2)])
+def test_kmap_large_batched(spv, K, stride):
+    """~400k voxels in 4 batches over a wide range (coarse keys past 32 bits):
+    the stride-2 parity partition and the submanifold map over more than 256
+    count tiles, against the oracle exactly."""
+    rng = np.random.default_rng(4545)
+    c = rng.integers(-1500, 1500, size=(420_000, 3))
+    c[1::3] = c[::3][: len(c[1::3])] + rng.integers(-1, 2, size=(len(c[1::3]), 3))  # local clusters
+    b = rng.integers(0, 4, size=(len(c), 1))
+    pts = np.unique(np.concatenate([b, c], 1), axis=0).astype(np.int32)
+    assert len(pts) > 256 * 256
+    oc, off, pairs, _ = run_kmap(spv, pts, K, stride)
+    roc, roff, rpairs = oracle.kernel_map(pts, K, stride)
+    np.testing.assert_array_equal(off, roff)
+    np.testing.assert_array_equal(pairs, rpairs)
+    if stride == 2:
+        np.testing.assert_array_equal(oc, roc)
+
+
 def test_kmap_duplicate_coords_rejected(spv):
     pts = np.array([[0, 1, 2, 3], [0, 1, 2, 3]], np.int32)
     with pytest.raises(spv.SpvError) as e:
