@@ -86,6 +86,8 @@ constexpr int kSortItems = 8;
 constexpr int kSortTile = kSortThreads * kSortItems;
 constexpr int kSortParts = 256;            // partial records of the stand-alone min / max kernel
 constexpr uint32_t kFusedSortBlocks = 256;  // up to this many tiles a scatter block scans the histograms itself
+constexpr uint32_t kFusedStatsParts = 1024;  // up to this many min / max records the pass-0 blocks reduce them
+constexpr uint64_t kFusedStatsReads = 1u << 20;  // ... if all blocks together read at most this many records
 
 size_t sort_hist_entries(int64_t cap) { return (size_t)256 * blocks_for(cap, kSortTile) + 1; }
 size_t sort_part_records(int64_t cap) {
@@ -126,8 +128,10 @@ __global__ __launch_bounds__(256) void k_sort_minmax(int32_t* part, const uint64
 }
 
 // reduce the partial records into the per-field minimum and bit widths
-__global__ __launch_bounds__(256) void k_sort_stats(SortStats* st, const int32_t* part, uint32_t nparts,
-                                                    const int64_t* count_dev, int64_t cap) {
+// The sort's statistics from the producers' min / max records, by one block
+// (any size, a multiple of 64 threads): every thread gets them in *out.
+__device__ inline void reduce_sort_stats(const int32_t* part, uint32_t nparts, const int64_t* count_dev, int64_t cap,
+                                         SortStats* out) {
     int mn[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
     int mx[4] = {(int)0x80000000, (int)0x80000000, (int)0x80000000, (int)0x80000000};
     for (uint32_t r = threadIdx.x; r < nparts; r += blockDim.x) {
@@ -138,6 +142,7 @@ __global__ __launch_bounds__(256) void k_sort_stats(SortStats* st, const int32_t
         }
     }
     __shared__ int32_t red[8];
+    __shared__ SortStats res;
     if (threadIdx.x < 8) red[threadIdx.x] = threadIdx.x < 4 ? 0x7fffffff : (int)0x80000000;
     __syncthreads();
 #pragma unroll
@@ -162,13 +167,22 @@ __global__ __launch_bounds__(256) void k_sort_stats(SortStats* st, const int32_t
         for (int d = 0; d < 4; ++d) {
             const uint32_t range = nonempty ? (uint32_t)(red[4 + d] - red[d]) : 0u;
             const uint32_t w = range ? 32u - __clz(range) : 0u;
-            st->fmin[d] = nonempty ? red[d] : 0;
-            st->fmax[d] = nonempty ? red[4 + d] : 0;
-            st->fbits[d] = w;
+            res.fmin[d] = nonempty ? red[d] : 0;
+            res.fmax[d] = nonempty ? red[4 + d] : 0;
+            res.fbits[d] = w;
             bits += w;
         }
-        st->sort_bits = bits;
+        res.sort_bits = bits;
     }
+    __syncthreads();
+    *out = res;
+}
+
+__global__ __launch_bounds__(256) void k_sort_stats(SortStats* st, const int32_t* part, uint32_t nparts,
+                                                    const int64_t* count_dev, int64_t cap) {
+    SortStats r;
+    reduce_sort_stats(part, nparts, count_dev, cap, &r);
+    if (threadIdx.x == 0) *st = r;
 }
 
 // lanes of this wave whose `valid` digit d equals this lane's (8 ballots)
@@ -187,10 +201,19 @@ __device__ inline uint64_t digit_peers(uint32_t d, bool valid) {
 // bit widths) in place; it runs even when there is nothing to sort so that the
 // buffer read back always holds compacted keys.  Lanes of a wave holding the
 // same digit are counted by one LDS add of their leader.
-__global__ __launch_bounds__(kSortThreads) void k_radix_hist(const SortStats* st, SortBufs sb, const int64_t* count_dev,
-                                                             int64_t cap, int pass, int digit_major) {
+// With fused_parts > 0 (pass 0 only) the block first reduces the producers'
+// fused_parts min / max records itself (block 0 also stores the result for the
+// later kernels), in place of a separate statistics launch.
+__global__ __launch_bounds__(kSortThreads) void k_radix_hist(SortStats* st, SortBufs sb, const int64_t* count_dev,
+                                                             int64_t cap, int pass, int digit_major,
+                                                             uint32_t fused_parts) {
     const uint32_t nblk = gridDim.x;
     if (pass > 0 && (uint32_t)(8 * pass) >= st->sort_bits) return;
+    SortStats lst;
+    if (fused_parts) {
+        reduce_sort_stats(sb.part, fused_parts, count_dev, cap, &lst);
+        if (blockIdx.x == 0 && threadIdx.x == 0) *st = lst;
+    }
     uint64_t* src = (pass & 1) ? sb.b : sb.a;
     __shared__ uint32_t hist[256];
     hist[threadIdx.x] = 0;
@@ -209,8 +232,8 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_hist(const SortStats* st
         uint32_t w[4];
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
-            mn[d] = st->fmin[d];
-            w[d] = st->fbits[d];
+            mn[d] = fused_parts ? lst.fmin[d] : st->fmin[d];
+            w[d] = fused_parts ? lst.fbits[d] : st->fbits[d];
         }
 #pragma unroll
         for (int r = 0; r < kSortItems; ++r) {
@@ -324,13 +347,15 @@ void launch_sort_keys(hipStream_t s, SortBufs sb, const int64_t* count_dev, int6
         k_sort_minmax<<<g, 256, 0, s>>>(sb.part, sb.a, count_dev, cap);
         nparts = g;
     }
-    k_sort_stats<<<1, 256, 0, s>>>(sb.st, sb.part, nparts, count_dev, cap);
     const unsigned nblk = blocks_for(cap, kSortTile);
+    // few records: every pass-0 histogram block reduces them itself
+    const uint32_t fused_parts = (nparts <= kFusedStatsParts && (uint64_t)nblk * nparts <= kFusedStatsReads) ? nparts : 0u;
+    if (!fused_parts) k_sort_stats<<<1, 256, 0, s>>>(sb.st, sb.part, nparts, count_dev, cap);
     const int fused = nblk <= kFusedSortBlocks ? 1 : 0;
     // the significant bits are known on the device only: every pass a 64-bit key
     // may need is launched, and passes beyond them exit at once
     for (int pass = 0; pass < 8; ++pass) {
-        k_radix_hist<<<nblk, kSortThreads, 0, s>>>(sb.st, sb, count_dev, cap, pass, !fused);
+        k_radix_hist<<<nblk, kSortThreads, 0, s>>>(sb.st, sb, count_dev, cap, pass, !fused, pass == 0 ? fused_parts : 0u);
         if (!fused) {
             // digit-major histograms -> write offsets (a pass past the significant
             // bits scans stale counts that its scatter then ignores)

@@ -72,6 +72,8 @@ __host__ __device__ inline uint32_t hash_slot(uint64_t k, uint32_t mask) {
     return ((uint32_t)k << 2) & mask;
 }
 
+constexpr uint32_t kNoSlot = 0xFFFFFFFFu;  // "no table slot"
+
 struct Table {
     uint64_t* keys;  // [capacity], 256-byte aligned
     int32_t* vals;   // [capacity], 256-byte aligned

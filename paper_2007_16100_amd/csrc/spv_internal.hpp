@@ -146,7 +146,7 @@ struct VoxelizeWs {
     Header* h;          // assigned by the caller (workspace offset 0)
     Table table;
     SortBufs sort;
-    uint64_t* pkey;     // [n] packed key per point (kEmpty if invalid)
+    uint32_t* pslot;    // [n] table slot of each point's key (kNoSlot if invalid)
     int32_t* seg;       // [n + 1] CSR offsets of the points of each voxel
     int32_t* fill;      // [n]
     int32_t* plist;     // [n] point ids grouped by voxel

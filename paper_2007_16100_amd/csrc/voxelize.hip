@@ -4,7 +4,8 @@
 //    the thread that creates an entry appends the key to the unique-key list;
 // 2. the m unique keys are radix-sorted into canonical (b, x, y, z) order and the
 //    table values are set to the rank, which also writes the voxel coordinates;
-// 3. every point queries the table for its voxel index (pt2vox) and counts N_m;
+// 3. every point reads its voxel index (pt2vox) at the table slot its insert
+//    found, and counts N_m;
 // 4. a counting sort of the points by voxel (prefix sum + fill) lets each voxel
 //    gather and average its own points -- no float atomics, one write per voxel.
 #include "spv_internal.hpp"
@@ -18,7 +19,7 @@ void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n) {
     w.table.vals = a.take<int32_t>(S);
     w.table.mask = S - 1;
     plan_sort_ws(a, w.sort, nn);
-    w.pkey = a.take<uint64_t>(nn);
+    w.pslot = a.take<uint32_t>(nn);
     w.seg = a.take<int32_t>(nn + 1);
     w.fill = a.take<int32_t>(nn);
     w.plist = a.take<int32_t>(nn);
@@ -30,7 +31,7 @@ void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n) {
 // equals the previous lane's leaves the insert to the head of its run.  The
 // block appends the keys it created to the unique-key list (one counter atomic
 // per block) and records their per-field min / max for the sort.
-__global__ __launch_bounds__(kAppendThreads) void k_vox_insert(Header* h, Table t, SortBufs sb, uint64_t* pkey,
+__global__ __launch_bounds__(kAppendThreads) void k_vox_insert(Header* h, Table t, SortBufs sb, uint32_t* pslot,
                                                                const float* xyz, const int32_t* batch, int64_t n,
                                                                float v) {
     const int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
@@ -57,15 +58,25 @@ __global__ __launch_bounds__(kAppendThreads) void k_vox_insert(Header* h, Table 
         } else {
             key = pack_key(b, q[0], q[1], q[2]);
         }
-        pkey[k] = key;
     }
+    // runs of equal keys inside the wave: the head inserts, the others take its
+    // slot (every lane between a head and a later lane of its run has its key)
+    const int lane = threadIdx.x & 63;
     const uint64_t prev_key = __shfl_up(key, 1, 64);
-    if (key != kEmpty && ((threadIdx.x & 63) == 0 || prev_key != key)) {
-        uint32_t slot;
+    const bool head = key != kEmpty && (lane == 0 || prev_key != key);
+    uint32_t slot = kNoSlot;
+    if (head) {
         const int r = table_insert(t, key, &slot);
         created = r > 0;
-        if (r < 0) raise_flag(h, kFlagTableFull);
+        if (r < 0) {
+            raise_flag(h, kFlagTableFull);
+            slot = kNoSlot;
+        }
     }
+    const uint64_t heads = __ballot(head) & (~0ull >> (63 - lane));  // heads at lanes <= this one
+    const int src = heads ? 63 - __clzll(heads) : lane;
+    const uint32_t run_slot = __shfl(slot, src, 64);
+    if (k < n) pslot[k] = key == kEmpty ? kNoSlot : run_slot;
     int mn[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
     int mx[4] = {(int)0x80000000, (int)0x80000000, (int)0x80000000, (int)0x80000000};
     if (created) {
@@ -96,11 +107,12 @@ __global__ void k_vox_rank(const Header* h, SortBufs sb, Table t, int32_t* coord
     fill[r] = 0;
 }
 
-__global__ void k_vox_lookup(Table t, const uint64_t* pkey, int64_t n, int32_t* pt2vox, int32_t* counts) {
+// every point's voxel index, read at the table slot its insert found
+__global__ void k_vox_lookup(Table t, const uint32_t* pslot, int64_t n, int32_t* pt2vox, int32_t* counts) {
     int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
     if (k >= n) return;
-    uint64_t key = pkey[k];
-    int32_t v = (key == kEmpty) ? -1 : table_find(t, key);
+    const uint32_t ps = pslot[k];
+    int32_t v = (ps == kNoSlot) ? -1 : t.vals[ps];
     pt2vox[k] = v;
     if (v >= 0) atomicAdd(&counts[v], 1);
 }
@@ -189,11 +201,11 @@ void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const
                      int32_t* counts, int32_t* pt2vox, int64_t* m_dev, bool table_cleared) {
     if (!table_cleared) launch_clear(s, w.h, w.table, true);
     const unsigned nins = n > 0 ? blocks_for(n, kAppendThreads) : 0u;
-    if (n > 0) k_vox_insert<<<nins, kAppendThreads, 0, s>>>(w.h, w.table, w.sort, w.pkey, xyz, batch, n, voxel_size);
+    if (n > 0) k_vox_insert<<<nins, kAppendThreads, 0, s>>>(w.h, w.table, w.sort, w.pslot, xyz, batch, n, voxel_size);
     launch_sort_keys(s, w.sort, &w.h->m, n, nins);
     k_vox_rank<<<blocks_for(n, 256), 256, 0, s>>>(w.h, w.sort, w.table, coords, counts, w.fill, n, m_dev);
     if (n == 0) return;
-    k_vox_lookup<<<blocks_for(n, 256), 256, 0, s>>>(w.table, w.pkey, n, pt2vox, counts);
+    k_vox_lookup<<<blocks_for(n, 256), 256, 0, s>>>(w.table, w.pslot, n, pt2vox, counts);
     if (!feat) return;
     launch_exclusive_scan(s, counts, w.seg, &w.h->m, n, w.scan_tmp);
     k_vox_fill<<<blocks_for(n, 256), 256, 0, s>>>(pt2vox, n, w.seg, w.fill, w.plist);
