@@ -378,6 +378,11 @@ spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_pa
     a.corner_idx = nullptr;
     a.corner_w = nullptr;
     a.h = L.h;
+    if (L.plan.use_union) {  // the map's neighbour table gives every point's corners
+        a.pt2vox = L.pt2vox;
+        a.grid_coords = L.coords;
+        a.nbr = L.plan.nbr;
+    }
     mark(0);
     // one launch clears the voxel table and packs every weight of the block
     PackJob jobs[kMaxPackJobs];

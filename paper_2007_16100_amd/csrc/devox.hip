@@ -181,7 +181,39 @@ __global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __
                                       cn[b].base[2] + (cc & 1));
         }
     }
-    table_find_n<2 * PB>(a.table, key, act, idx);
+    if (a.nbr) {
+        // the grid is the points' own voxelization with its 3x3x3 neighbour
+        // table: every corner lies in the neighbourhood of the point's voxel j,
+        // so corner c is entry 9(dx+1) + 3(dy+1) + (dz+1) of row j, with
+        // d = base + c - (voxel j's coordinates) in {-1, 0, 1} per axis
+        int32_t j[PB];
+#pragma unroll
+        for (int b = 0; b < PB; ++b) {
+            const int64_t k = p0 + b * 16 + r16;
+            j[b] = (cn[b].ok && k < a.n) ? a.pt2vox[k] : -1;
+        }
+        int own[PB][3];
+#pragma unroll
+        for (int b = 0; b < PB; ++b)
+#pragma unroll
+            for (int d = 0; d < 3; ++d) own[b][d] = j[b] >= 0 ? a.grid_coords[4 * (int64_t)j[b] + 1 + d] : 0;
+#pragma unroll
+        for (int b = 0; b < PB; ++b) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int cc = 2 * g + h;
+                const int dx = cn[b].base[0] + ((cc >> 2) & 1) - own[b][0];
+                const int dy = cn[b].base[1] + ((cc >> 1) & 1) - own[b][1];
+                const int dz = cn[b].base[2] + (cc & 1) - own[b][2];
+                const bool in = j[b] >= 0 && dx >= -1 && dx <= 1 && dy >= -1 && dy <= 1 && dz >= -1 && dz <= 1;
+                idx[2 * b + h] = in ? a.nbr[27 * (int64_t)j[b] + 9 * (dx + 1) + 3 * (dy + 1) + (dz + 1)] - 1 : -1;
+                // outside the neighbourhood (not expected): the hash decides
+                if (act[2 * b + h] && !in) idx[2 * b + h] = table_find(a.table, key[2 * b + h]);
+            }
+        }
+    } else {
+        table_find_n<2 * PB>(a.table, key, act, idx);
+    }
 #pragma unroll
     for (int b = 0; b < PB; ++b) {
         const int64_t k = p0 + b * 16 + r16;

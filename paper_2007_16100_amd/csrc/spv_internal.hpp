@@ -257,6 +257,13 @@ struct DevoxArgs {
     int32_t* corner_idx;
     float* corner_w;
     Header* h;
+    // optional, when the grid is the points' own voxelization at stride 1:
+    // each point's voxel (pt2vox), the grid's coordinates and its 3x3x3
+    // neighbour table (nbr[j][k] = i + 1); corners are then read from the
+    // table instead of probed
+    const int32_t* pt2vox = nullptr;
+    const int32_t* grid_coords = nullptr;
+    const int32_t* nbr = nullptr;
 };
 bool devox_mfma_supported(int C, int Cp, int dt);
 void* plan_devox_ws(Arena& a, int C, int Cp);

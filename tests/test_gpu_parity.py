@@ -459,6 +459,48 @@ def test_block(spv, cfg):
     check_close(host(out, dtype)[:len(xyz)], rout, dtype)
 
 
+@pytest.mark.parametrize("mode", ["center", "corner"])
+@pytest.mark.parametrize("C", [32, 96])
+def test_block_equals_stand_alone_ops(spv, sweep, mode, C):
+    """The block reads every point's interpolation corners from the kernel map's
+    neighbour table; the stand-alone devoxelization probes the hash for them.
+    Everything else runs the same kernels, so the block's output equals the
+    stand-alone chain (voxelize, map, 2 convs, devoxelize + MLP) bit for bit;
+    both agree with the oracle's block."""
+    dt = "bf16"
+    xyz = sweep
+    feat = synth.normal((len(xyz), C), 71, dtype=dt)
+    convs = []
+    for l in range(2):
+        sc, sh = synth.folded_bn(C, 72 + l)
+        convs.append((synth.conv_weight(27, C, C, 74 + l, dt), sc, sh, True))
+    Wp = synth.linear_weight(C, C, 76, dt)
+    scp, shp = synth.folded_bn(C, 77)
+    m_code = spv.SPV_DEVOX_CENTER if mode == "center" else spv.SPV_DEVOX_CORNER
+    dconvs = [(dev(W, dt), dev(sc), dev(sh), r) for W, sc, sh, r in convs]
+    d_xyz, d_feat, d_Wp, d_scp, d_shp = dev(xyz), dev(feat, dt), dev(Wp, dt), dev(scp), dev(shp)
+    params = spv.make_block_params(C, torch.bfloat16, 0.05, dconvs, d_Wp, d_scp, d_shp, relu_p=True, mode=m_code)
+    out, m = spv.spv_block(spv.Workspace.for_block(len(xyz), C), params, d_xyz, d_feat, sync=True)
+    # the same pipeline through the stand-alone entry points
+    ws = spv.Workspace.for_ops(len(xyz), C)
+    vox = spv.spv_voxelize(ws, d_xyz, 0.05, d_feat)
+    assert vox.m == m
+    coords = vox.coords[:m].contiguous()
+    km = spv.spv_kernel_map(spv.Workspace.for_ops(len(xyz), C), coords)
+    x = vox.vfeat[:m].contiguous()
+    for W, sc, sh, r in dconvs:
+        x = spv.spv_sparse_conv(spv.Workspace.for_ops(len(xyz), C), x, km.off, km.pairs, W, m, scale=sc, shift=sh,
+                                relu=r)[:m].contiguous()
+    ref = spv.spv_devoxelize(spv.Workspace.for_ops(len(xyz), C), coords, x, d_xyz, 0.05, mode=m_code, pfeat=d_feat,
+                             Wp=d_Wp, scale_p=d_scp, shift_p=d_shp, relu_p=True)
+    ref = ref[0] if isinstance(ref, tuple) else ref
+    torch.cuda.synchronize()
+    assert torch.equal(out[:len(xyz)].view(torch.int16), ref[:len(xyz)].view(torch.int16))
+    rout, rm = oracle.block(xyz, feat, 0.05, convs, Wp, scp, shp, relu_p=True, dtype=dt, mode=mode)
+    assert rm == m
+    check_close(host(out, dt)[:len(xyz)], rout, dt)
+
+
 def test_block_graph_replay(spv, sweep):
     """spv_block captured into a graph: every replay, with eager work and
     synchronization between them, reproduces the eager result bit for bit."""
