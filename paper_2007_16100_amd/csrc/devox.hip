@@ -123,7 +123,8 @@ __global__ void k_devox_generic(DevoxArgs a, const int32_t* cidx, const float* c
 // ---------------------------------------------------------------------------
 constexpr int kDevoxPB = 4;  // 16-point blocks per wave
 
-template <int DT, int KCH, int NB>
+// NBR: corners read from the grid's neighbour table (a.nbr), else probed
+template <int DT, int KCH, int NB, bool NBR>
 __global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __restrict__ wpack) {
     constexpr int PB = kDevoxPB;
     constexpr int C = NB * 16;
@@ -181,7 +182,7 @@ __global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __
                                       cn[b].base[2] + (cc & 1));
         }
     }
-    if (a.nbr) {
+    if constexpr (NBR) {
         // the grid is the points' own voxelization with its 3x3x3 neighbour
         // table: every corner lies in the neighbourhood of the point's voxel j,
         // so corner c is entry 9(dx+1) + 3(dy+1) + (dz+1) of row j, with
@@ -368,7 +369,10 @@ void* plan_devox_ws(Arena& a, int C, int Cp) {
 template <int DT, int KCH, int NB>
 static void launch_devox_mfma(hipStream_t s, const DevoxArgs& a, const void* wpack) {
     int64_t waves = (a.n + 16 * kDevoxPB - 1) / (16 * kDevoxPB);
-    k_devox_mfma<DT, KCH, NB><<<blocks_for(waves, 4), 256, 0, s>>>(a, (const uint4*)wpack);
+    if (a.nbr && a.pt2vox && a.grid_coords)
+        k_devox_mfma<DT, KCH, NB, true><<<blocks_for(waves, 4), 256, 0, s>>>(a, (const uint4*)wpack);
+    else
+        k_devox_mfma<DT, KCH, NB, false><<<blocks_for(waves, 4), 256, 0, s>>>(a, (const uint4*)wpack);
 }
 
 template <int DT, int NB>
