@@ -260,6 +260,15 @@ def configs_mode(args):
         if seed == 1002:
             km = spv.spv_kernel_map(wsm, coords)
             P = km.total
+            # Sec. 4.3's resource model on this scan: |map_k| per offset and the MACs
+            # of the block's two 96->96 convs and of a 32->32 conv
+            from paper_2007_16100_amd import mapstats
+            ms = mapstats.MapStats()
+            sizes = ms.add("s1k3", km.off)
+            total_macs, per_layer = mapstats.conv_macs([("s1k3", 96, 96), ("s1k3", 96, 96), ("s1k3", 32, 32)], ms)
+            print(json.dumps({"op": "kernel_map k3 s1 statistics", "map_sizes": [int(x) for x in sizes],
+                              "macs_layers": ["96->96", "96->96", "32->32"], "macs": per_layer,
+                              "macs_total": total_macs}), flush=True)
             ms = timed(lambda: spv.spv_kernel_map(wsm, coords, sync=False))
             report("kernel_map k3 s1", ms, 16 * m + 12 * table_slots(m) + 8 * P + 4 * 28, voxels=m, pairs=P)
             C = 32
@@ -272,6 +281,9 @@ def configs_mode(args):
             km = spv.spv_kernel_map(wsm, coords, K=2, stride=2)
             mc = int(km.m_out_dev.item())
             P = km.total
+            from paper_2007_16100_amd import mapstats
+            print(json.dumps({"op": "kernel_map k2 s2 statistics",
+                              "map_sizes": [int(x) for x in mapstats.map_sizes(km.off)]}), flush=True)
             ms = timed(lambda: spv.spv_kernel_map(wsm, coords, K=2, stride=2, sync=False))
             report("kernel_map k2 s2", ms, 16 * m + 16 * mc + 12 * table_slots(m) + 8 * P + 4 * 9,
                    voxels=m, coarse_voxels=mc, pairs=P)
