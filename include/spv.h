@@ -60,8 +60,16 @@ typedef enum spv_status {
 typedef enum spv_dtype { SPV_F32 = 0, SPV_BF16 = 1, SPV_F16 = 2 } spv_dtype;
 
 /* Where a voxel's feature sits for trilinear interpolation (Sec. 3.3, "Sparse
- * Devoxelization"): CENTER = at the voxel centre (q + 1/2) v, CORNER = at q v. */
-typedef enum spv_devox_mode { SPV_DEVOX_CENTER = 0, SPV_DEVOX_CORNER = 1 } spv_devox_mode;
+ * Devoxelization"): CENTER = at the voxel centre (q + 1/2) v, CORNER = at q v.
+ * NEAREST is the nearest-voxel interpolation the paper weighs trilinear
+ * against: a point takes the feature of the voxel that contains it (at the
+ * grid's stride), or 0 if the grid lacks that voxel -- CORNER's corners with
+ * all of the weight on corner 0. */
+typedef enum spv_devox_mode {
+    SPV_DEVOX_CENTER = 0,
+    SPV_DEVOX_CORNER = 1,
+    SPV_DEVOX_NEAREST = 2
+} spv_devox_mode;
 
 /* Workspace bytes sufficient for spv_voxelize, spv_kernel_map, spv_sparse_conv,
  * spv_devoxelize and spv_lookup on at most max_points points / voxels. */

@@ -22,7 +22,7 @@ _LIB = os.path.join(_HERE, "libspv_oracle.so")
 
 OK, ERR_INVALID_ARG, ERR_CAPACITY, ERR_RANGE, ERR_NONFINITE, ERR_UNSUPPORTED = 0, 1, 2, 3, 4, 5
 DT = {"f32": 0, "bf16": 1, "f16": 2}
-MODE = {"center": 0, "corner": 1}
+MODE = {"center": 0, "corner": 1, "nearest": 2}
 
 
 def build(force: bool = True) -> str:

@@ -404,7 +404,8 @@ int spvo_devoxelize(const int32_t* grid_coords, int64_t m, int32_t stride_log2,
     if (n < 0 || n >= ((int64_t)1 << 31) || m < 0 || C <= 0 || !valid_dtype(dtype))
         return SPVO_ERR_INVALID_ARG;
     if (!valid_voxel_size(voxel_size) || stride_log2 < 0 || stride_log2 > 15) return SPVO_ERR_INVALID_ARG;
-    if (mode != SPVO_DEVOX_CENTER && mode != SPVO_DEVOX_CORNER) return SPVO_ERR_INVALID_ARG;
+    if (mode != SPVO_DEVOX_CENTER && mode != SPVO_DEVOX_CORNER && mode != SPVO_DEVOX_NEAREST)
+        return SPVO_ERR_INVALID_ARG;
     if (n > 0 && (!xyz || !out)) return SPVO_ERR_INVALID_ARG;
     if (m > 0 && (!grid_coords || !vfeat)) return SPVO_ERR_INVALID_ARG;
     if (pfeat && (Cp <= 0 || !Wp)) return SPVO_ERR_INVALID_ARG;
@@ -433,7 +434,8 @@ int spvo_devoxelize(const int32_t* grid_coords, int64_t m, int32_t stride_log2,
             float u = (mode == SPVO_DEVOX_CENTER) ? as - 0.5f : as;
             float fb = floorf(u);
             base[d] = (int32_t)fb;
-            t[d] = u - fb;
+            /* NEAREST: the voxel containing the point takes all the weight (corner 0) */
+            t[d] = (mode == SPVO_DEVOX_NEAREST) ? 0.0f : u - fb;
         }
         double den = 0.0;
         for (int32_t c = 0; c < C; ++c) num[c] = 0.0;

@@ -46,6 +46,7 @@ extern "C" {
 
 #define SPVO_DEVOX_CENTER 0
 #define SPVO_DEVOX_CORNER 1
+#define SPVO_DEVOX_NEAREST 2 /* the point's own voxel only (the interpolation the paper sets trilinear against) */
 
 /* Voxelize n points (Eq. 1, Eq. 2).  Outputs hold up to n voxels, in ascending
  * (batch, x, y, z) order.  feat may be NULL (C ignored): then only coordinates,

@@ -298,7 +298,7 @@ spv_status spv_devoxelize(void* stream, void* ws, size_t ws_bytes, const int32_t
     if (!ws || n < 0 || n >= ((int64_t)1 << 31) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || C <= 0 ||
         !valid_dt(dt) || !valid_v(voxel_size) || stride_log2 < 0 || stride_log2 > 15)
         return SPV_ERR_INVALID_ARG;
-    if (mode != SPV_DEVOX_CENTER && mode != SPV_DEVOX_CORNER) return SPV_ERR_INVALID_ARG;
+    if (mode != SPV_DEVOX_CENTER && mode != SPV_DEVOX_CORNER && mode != SPV_DEVOX_NEAREST) return SPV_ERR_INVALID_ARG;
     if ((n > 0 && (!xyz || !out)) || (m_cap > 0 && (!grid_coords || !vfeat))) return SPV_ERR_INVALID_ARG;
     if (pfeat && (Cp <= 0 || !Wp)) return SPV_ERR_INVALID_ARG;
     if ((corner_idx == nullptr) != (corner_w == nullptr)) return SPV_ERR_INVALID_ARG;
@@ -341,7 +341,8 @@ spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_pa
         !valid_v(p->voxel_size))
         return SPV_ERR_INVALID_ARG;
     if (p->n_convs < 1 || p->n_convs > 2 || !p->Wp) return SPV_ERR_INVALID_ARG;
-    if (p->devox_mode != SPV_DEVOX_CENTER && p->devox_mode != SPV_DEVOX_CORNER) return SPV_ERR_INVALID_ARG;
+    if (p->devox_mode != SPV_DEVOX_CENTER && p->devox_mode != SPV_DEVOX_CORNER && p->devox_mode != SPV_DEVOX_NEAREST)
+        return SPV_ERR_INVALID_ARG;
     for (int l = 0; l < p->n_convs; ++l)
         if (!p->W[l] || !aligned16(p->W[l])) return SPV_ERR_INVALID_ARG;
     if (n > 0 && (!xyz || !feat || !out)) return SPV_ERR_INVALID_ARG;

@@ -37,7 +37,8 @@ __device__ inline Corners corners_of(const float (&p)[3], int b, float v, float 
         const float u = (mode == SPV_DEVOX_CENTER) ? as - 0.5f : as;
         const float fb = floorf(u);
         c.base[d] = c.ok ? (int)fb : 0;
-        c.t[d] = c.ok ? u - fb : 0.f;
+        // NEAREST: the voxel containing the point (corner 0) takes all the weight
+        c.t[d] = (c.ok && mode != SPV_DEVOX_NEAREST) ? u - fb : 0.f;
     }
     return c;
 }

@@ -24,7 +24,7 @@ LIB_PATH = os.path.join(_HERE, "libspv.so")
 SPV_OK, SPV_ERR_INVALID_ARG, SPV_ERR_CAPACITY, SPV_ERR_RANGE, SPV_ERR_NONFINITE, SPV_ERR_UNSUPPORTED, SPV_ERR_HIP = \
     range(7)
 SPV_F32, SPV_BF16, SPV_F16 = 0, 1, 2
-SPV_DEVOX_CENTER, SPV_DEVOX_CORNER = 0, 1
+SPV_DEVOX_CENTER, SPV_DEVOX_CORNER, SPV_DEVOX_NEAREST = 0, 1, 2
 
 _DT = {torch.float32: SPV_F32, torch.bfloat16: SPV_BF16, torch.float16: SPV_F16}
 

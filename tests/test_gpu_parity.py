@@ -366,7 +366,10 @@ def test_conv_deterministic(spv, sweep):
 # ---------------------------------------------------------------------------
 # devoxelization + point MLP + fusion
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("mode", ["center", "corner"])
+MODE_CODE = {"center": 0, "corner": 1, "nearest": 2}  # spv_devox_mode
+
+
+@pytest.mark.parametrize("mode", ["center", "corner", "nearest"])
 @pytest.mark.parametrize("dtype,C", [("bf16", 96), ("f32", 16), ("f16", 32)])
 def test_devox_sweep(spv, sweep, mode, dtype, C):
     pts = sweep[::2]
@@ -376,7 +379,7 @@ def test_devox_sweep(spv, sweep, mode, dtype, C):
     Wp = synth.linear_weight(C, C, 23, dtype)
     sc, sh = synth.folded_bn(C, 24)
     ws = spv.Workspace.for_ops(len(pts), C)
-    m = spv.SPV_DEVOX_CENTER if mode == "center" else spv.SPV_DEVOX_CORNER
+    m = MODE_CODE[mode]
     out, ci, cw = spv.spv_devoxelize(ws, dev(rc), dev(vf, dtype), dev(pts), 0.05, mode=m, pfeat=dev(pf, dtype),
                                      Wp=dev(Wp, dtype), scale_p=dev(sc), shift_p=dev(sh), relu_p=True,
                                      want_corners=True)
@@ -459,7 +462,7 @@ def test_block(spv, cfg):
     check_close(host(out, dtype)[:len(xyz)], rout, dtype)
 
 
-@pytest.mark.parametrize("mode", ["center", "corner"])
+@pytest.mark.parametrize("mode", ["center", "corner", "nearest"])
 @pytest.mark.parametrize("C", [32, 96])
 def test_block_equals_stand_alone_ops(spv, sweep, mode, C):
     """The block reads every point's interpolation corners from the kernel map's
@@ -476,7 +479,7 @@ def test_block_equals_stand_alone_ops(spv, sweep, mode, C):
         convs.append((synth.conv_weight(27, C, C, 74 + l, dt), sc, sh, True))
     Wp = synth.linear_weight(C, C, 76, dt)
     scp, shp = synth.folded_bn(C, 77)
-    m_code = spv.SPV_DEVOX_CENTER if mode == "center" else spv.SPV_DEVOX_CORNER
+    m_code = MODE_CODE[mode]
     dconvs = [(dev(W, dt), dev(sc), dev(sh), r) for W, sc, sh, r in convs]
     d_xyz, d_feat, d_Wp, d_scp, d_shp = dev(xyz), dev(feat, dt), dev(Wp, dt), dev(scp), dev(shp)
     params = spv.make_block_params(C, torch.bfloat16, 0.05, dconvs, d_Wp, d_scp, d_shp, relu_p=True, mode=m_code)

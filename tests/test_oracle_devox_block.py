@@ -103,6 +103,44 @@ def test_devox_coarse_stride(oracle_lib):
     np.testing.assert_allclose(got, ref, rtol=2e-6, atol=2e-6)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_devox_nearest_is_own_voxel(oracle_lib, dtype):
+    """NEAREST (the interpolation the paper sets trilinear against, Sec. 3.3):
+    every point gets exactly its own voxel's feature -- the voxel the
+    voxelization assigned it (pt2vox) -- and the raw corner weights are
+    (1, 0, ..., 0)."""
+    rng = np.random.default_rng(31)
+    xyz = rng.uniform(-0.8, 0.8, size=(1500, 3)).astype(np.float32)
+    v = 0.1
+    coords, _, _, p2v = oracle_lib.voxelize(xyz, v)
+    vf = synth.normal((len(coords), 7), 32, dtype=dtype)
+    out, ci, cw = oracle_lib.devoxelize(coords, vf, xyz, v, mode="nearest", dtype=dtype, want_corners=True)
+    np.testing.assert_array_equal(out, vf[p2v])
+    np.testing.assert_array_equal(ci[:, 0], p2v)
+    np.testing.assert_array_equal(cw, np.eye(8, dtype=np.float32)[np.zeros(len(xyz), int)])
+
+
+def test_devox_nearest_coarse_and_absent(oracle_lib):
+    """At stride 2 a point takes the feature of voxel floor(c / 2) of its own
+    voxel c; a point whose voxel the grid lacks gets 0."""
+    rng = np.random.default_rng(33)
+    xyz = rng.uniform(-1.0, 1.0, size=(900, 3)).astype(np.float32)
+    v = 0.1
+    fine, _, _, p2v = oracle_lib.voxelize(xyz, v)
+    coarse, _, _ = oracle_lib.kernel_map(fine, 2, 2)
+    keep = np.ones(len(coarse), bool)
+    keep[::5] = False  # a grid without every fifth coarse voxel
+    grid = coarse[keep]
+    vf = synth.normal((len(grid), 4), 34, dtype="f32")
+    out = oracle_lib.devoxelize(grid, vf, xyz, v, stride_log2=1, mode="nearest")
+    index = {tuple(c): i for i, c in enumerate(grid.tolist())}
+    for k in range(len(xyz)):
+        c = fine[p2v[k]]
+        key = (int(c[0]), int(c[1]) >> 1, int(c[2]) >> 1, int(c[3]) >> 1)
+        want = vf[index[key]] if key in index else np.zeros(4, np.float32)
+        np.testing.assert_array_equal(out[k], want)
+
+
 def test_devox_mlp_fusion(oracle_lib):
     rng = np.random.default_rng(21)
     xyz = rng.uniform(-0.5, 0.5, size=(300, 3)).astype(np.float32)
