@@ -48,13 +48,15 @@ def lib():
         L.spvo_voxelize.argtypes = [vp, vp, i64, f32, vp, i32, i32, vp, vp, vp, vp, vp]
         L.spvo_kernel_map.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, i64, vp]
         L.spvo_sparse_conv.argtypes = [vp, i64, i32, vp, vp, i32, i32, vp, vp, vp, i32, vp, i64, i32, i32]
+        L.spvo_sparse_conv_res.argtypes = [vp, i64, i32, vp, vp, i32, i32, vp, vp, vp, vp, i32, vp, i64, i32, i32]
         L.spvo_devoxelize.argtypes = [vp, i64, i32, vp, vp, i64, f32, i32, vp, i32, vp, i32, vp, vp, vp, i32,
                                       vp, i32, vp, vp]
         L.spvo_block.argtypes = [vp, vp, vp, i64, vp, vp, vp]
         L.spvo_decode.argtypes = [vp, i64, i32]
         L.spvo_decode.restype = ct.c_double
         L.spvo_round_store.argtypes = [ct.c_double, vp, i64, i32]
-        for f in ("spvo_voxelize", "spvo_kernel_map", "spvo_sparse_conv", "spvo_devoxelize", "spvo_block"):
+        for f in ("spvo_voxelize", "spvo_kernel_map", "spvo_sparse_conv", "spvo_sparse_conv_res", "spvo_devoxelize",
+                  "spvo_block"):
             getattr(L, f).restype = ct.c_int
         _lib = L
     return _lib
@@ -117,7 +119,8 @@ def kernel_map(in_coords, K=3, stride=1, pair_cap=None):
     return oc, off[:K3 + 1], pairs[:total.value]
 
 
-def sparse_conv(x, off, pairs, W, m_out, dtype="f32", scale=None, shift=None, relu=False, transposed=False):
+def sparse_conv(x, off, pairs, W, m_out, dtype="f32", scale=None, shift=None, relu=False, transposed=False,
+                res=None):
     x = np.ascontiguousarray(x, dtype=_sdt(dtype))
     W = np.ascontiguousarray(W, dtype=_sdt(dtype))
     K3, Cin, Cout = W.shape
@@ -126,8 +129,9 @@ def sparse_conv(x, off, pairs, W, m_out, dtype="f32", scale=None, shift=None, re
     scale = None if scale is None else np.ascontiguousarray(scale, dtype=np.float32)
     shift = None if shift is None else np.ascontiguousarray(shift, dtype=np.float32)
     out = np.zeros((max(m_out, 1), Cout), _sdt(dtype))
-    st = lib().spvo_sparse_conv(_p(x), x.shape[0], Cin, _p(off), _p(pairs), K3, int(transposed), _p(W),
-                                _p(scale), _p(shift), int(relu), _p(out), m_out, Cout, DT[dtype])
+    res = None if res is None else np.ascontiguousarray(res, dtype=_sdt(dtype)).reshape(m_out, Cout)
+    st = lib().spvo_sparse_conv_res(_p(x), x.shape[0], Cin, _p(off), _p(pairs), K3, int(transposed), _p(W),
+                                    _p(scale), _p(shift), _p(res), int(relu), _p(out), m_out, Cout, DT[dtype])
     _chk(st, "sparse_conv")
     return out[:m_out]
 
@@ -163,12 +167,13 @@ class _BlockParams(ct.Structure):
     _fields_ = [("C", ct.c_int32), ("dtype", ct.c_int32), ("voxel_size", ct.c_float), ("n_convs", ct.c_int32),
                 ("W", ct.c_void_p * 2), ("scale", ct.c_void_p * 2), ("shift", ct.c_void_p * 2),
                 ("relu", ct.c_int32 * 2), ("Wp", ct.c_void_p), ("scale_p", ct.c_void_p), ("shift_p", ct.c_void_p),
-                ("relu_p", ct.c_int32), ("devox_mode", ct.c_int32)]
+                ("relu_p", ct.c_int32), ("devox_mode", ct.c_int32), ("residual", ct.c_int32)]
 
 
 def block(xyz, feat, voxel_size, convs, Wp, scale_p=None, shift_p=None, relu_p=True, dtype="f32", batch=None,
-          mode="center"):
-    """SPVConv block.  convs: list of (W [27,C,C], scale|None, shift|None, relu)."""
+          mode="center", residual=False):
+    """SPVConv block.  convs: list of (W [27,C,C], scale|None, shift|None, relu).  residual: the last
+    conv adds the block's voxel input before its activation (a residual block, Sec. 3.3)."""
     xyz = np.ascontiguousarray(xyz, dtype=np.float32)
     feat = np.ascontiguousarray(feat, dtype=_sdt(dtype))
     n, C = feat.shape
@@ -193,6 +198,7 @@ def block(xyz, feat, voxel_size, convs, Wp, scale_p=None, shift_p=None, relu_p=T
     p.shift_p = arr(shift_p, np.float32)
     p.relu_p = int(relu_p)
     p.devox_mode = MODE[mode]
+    p.residual = int(residual)
     batch = None if batch is None else np.ascontiguousarray(batch, dtype=np.int32)
     out = np.zeros((max(n, 1), C), _sdt(dtype))
     m = ct.c_int64(0)

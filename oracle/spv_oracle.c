@@ -344,10 +344,13 @@ int spvo_kernel_map(const int32_t* in_coords, int64_t m_in, int32_t K, int32_t s
 /* sparse convolution on the map                                              */
 /* ------------------------------------------------------------------------- */
 
-int spvo_sparse_conv(const void* in, int64_t m_in, int32_t Cin,
-                     const int32_t* off, const int32_t* pairs, int32_t K3, int32_t transposed,
-                     const void* W, const float* scale, const float* shift, int32_t relu,
-                     void* out, int64_t m_out, int32_t Cout, int32_t dtype) {
+/* res (NULL = none) is a residual input [m_out][Cout] of the storage type,
+ * added after scale and shift and before the activation (the identity branch
+ * of a residual block, Sec. 3.3 "Feature Aggregation"). */
+int spvo_sparse_conv_res(const void* in, int64_t m_in, int32_t Cin,
+                         const int32_t* off, const int32_t* pairs, int32_t K3, int32_t transposed,
+                         const void* W, const float* scale, const float* shift, const void* res, int32_t relu,
+                         void* out, int64_t m_out, int32_t Cout, int32_t dtype) {
     if (m_in < 0 || m_out < 0 || Cin <= 0 || Cout <= 0 || !off || !W || !valid_dtype(dtype))
         return SPVO_ERR_INVALID_ARG;
     if (!(K3 == 27 || K3 == 8)) return SPVO_ERR_UNSUPPORTED;
@@ -383,12 +386,21 @@ int spvo_sparse_conv(const void* in, int64_t m_in, int32_t Cin,
             double y = acc[j * Cout + co];
             if (scale) y *= (double)scale[co];
             if (shift) y += (double)shift[co];
+            if (res) y += spvo_decode(res, j * Cout + co, dtype);
             if (relu && y < 0.0) y = 0.0;
             spvo_round_store(y, out, j * Cout + co, dtype);
         }
     free(w);
     free(acc);
     return SPVO_OK;
+}
+
+int spvo_sparse_conv(const void* in, int64_t m_in, int32_t Cin,
+                     const int32_t* off, const int32_t* pairs, int32_t K3, int32_t transposed,
+                     const void* W, const float* scale, const float* shift, int32_t relu,
+                     void* out, int64_t m_out, int32_t Cout, int32_t dtype) {
+    return spvo_sparse_conv_res(in, m_in, Cin, off, pairs, K3, transposed, W, scale, shift, NULL, relu, out, m_out,
+                                Cout, dtype);
 }
 
 /* ------------------------------------------------------------------------- */
@@ -498,13 +510,18 @@ int spvo_block(const spvo_block_params* p, const float* xyz, const int32_t* batc
     int64_t m = 0, mo = 0, total = 0;
     int st = spvo_voxelize(xyz, batch, n, p->voxel_size, feat, C, p->dtype, coords, va, counts, pt2vox, &m);
     if (!st) st = spvo_kernel_map(coords, m, 3, 1, NULL, &mo, off, pairs, (int64_t)nn * 27, &total);
+    /* residual: the last conv adds the block's voxel input x before its activation */
+    void* x = p->residual ? malloc(nn * (size_t)C * es) : NULL;
+    if (x && !st) memcpy(x, va, (size_t)(m > 0 ? m : 1) * (size_t)C * es);
     for (int l = 0; l < p->n_convs && !st; ++l) {
-        st = spvo_sparse_conv(va, m, C, off, pairs, 27, 0, p->W[l], p->scale[l], p->shift[l], p->relu[l],
-                              vb, m, C, p->dtype);
+        const void* res = (x && l == p->n_convs - 1) ? x : NULL;
+        st = spvo_sparse_conv_res(va, m, C, off, pairs, 27, 0, p->W[l], p->scale[l], p->shift[l], res, p->relu[l],
+                                  vb, m, C, p->dtype);
         void* t = va;
         va = vb;
         vb = t;
     }
+    free(x);
     if (!st)
         st = spvo_devoxelize(coords, m, 0, xyz, batch, n, p->voxel_size, p->devox_mode, va, C, feat, C, p->Wp,
                              p->scale_p, p->shift_p, p->relu_p, out, p->dtype, NULL, NULL);

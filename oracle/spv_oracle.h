@@ -70,6 +70,12 @@ int spvo_sparse_conv(const void* in, int64_t m_in, int32_t Cin,
                      const int32_t* off, const int32_t* pairs, int32_t K3, int32_t transposed,
                      const void* W, const float* scale, const float* shift, int32_t relu,
                      void* out, int64_t m_out, int32_t Cout, int32_t dtype);
+/* the same with a residual input res [m_out][Cout] (NULL = none), added after
+ * scale and shift and before the activation */
+int spvo_sparse_conv_res(const void* in, int64_t m_in, int32_t Cin,
+                         const int32_t* off, const int32_t* pairs, int32_t K3, int32_t transposed,
+                         const void* W, const float* scale, const float* shift, const void* res, int32_t relu,
+                         void* out, int64_t m_out, int32_t Cout, int32_t dtype);
 
 /* Devoxelize from a grid of voxel size voxel_size * 2^stride_log2 (coords in
  * that grid's units), optionally add the point MLP act(scale*(pfeat @ Wp)+shift).
@@ -98,6 +104,7 @@ typedef struct {
     const float* shift_p;       /* [C] or NULL */
     int32_t relu_p;
     int32_t devox_mode;
+    int32_t residual; /* nonzero: the last conv adds the block's voxel input before its activation */
 } spvo_block_params;
 
 int spvo_block(const spvo_block_params* p, const float* xyz, const int32_t* batch,

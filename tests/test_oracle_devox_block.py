@@ -185,8 +185,9 @@ def test_golden_mac_ratios(oracle_lib):
     assert int(rows["devox_neighbours"][0]) == 8
 
 
-def _dense_block_config1(xyz, feat, v, W, Wp):
-    """The tiny fp32 block computed densely: numpy scatter-mean, torch conv3d, grid_sample."""
+def _dense_block_config1(xyz, feat, v, W, Wp, residual=False, relu=False):
+    """The tiny fp32 block computed densely: numpy scatter-mean, torch conv3d, grid_sample.
+    residual / relu: the conv's output plus the voxel input, then max(., 0)."""
     q = dense_ref.quantize(xyz, v)
     o = q.min(0) - 2
     shape = q.max(0) - o + 3
@@ -199,7 +200,12 @@ def _dense_block_config1(xyz, feat, v, W, Wp):
     mask = cnt > 0
     mean = np.where(mask, s / np.maximum(cnt, 1), 0.0)
     w = torch.from_numpy(np.ascontiguousarray(W.reshape(3, 3, 3, *W.shape[1:]).transpose(4, 3, 0, 1, 2)))
-    conv = F.conv3d(torch.from_numpy(mean)[None], w, padding=1)[0].numpy() * mask  # submanifold: active sites only
+    conv = F.conv3d(torch.from_numpy(mean)[None], w, padding=1)[0].numpy()
+    if residual:
+        conv = conv + mean
+    if relu:
+        conv = np.maximum(conv, 0.0)
+    conv = conv * mask  # submanifold: active sites only
     a = (xyz / np.float32(v)).astype(np.float64) - 0.5 - o
     gn = 2.0 * a / (np.array(shape, np.float64) - 1.0) - 1.0
     grid = torch.from_numpy(gn[:, ::-1].copy()).reshape(1, 1, 1, -1, 3)
@@ -218,3 +224,18 @@ def test_block_config1_dense(oracle_lib):
     assert m == 1944
     ref = _dense_block_config1(xyz, feat.astype(np.float64), 0.1, W.astype(np.float64), Wp.astype(np.float64))
     np.testing.assert_allclose(out, ref, rtol=1e-5, atol=1e-5)
+
+
+def test_block_config1_dense_residual(oracle_lib):
+    """A residual block (Sec. 3.3): the conv's output plus the block's voxel
+    input, then ReLU, against the dense pipeline with the same identity branch."""
+    xyz = synth.uniform_cube(2000, 1.6, 1001)
+    feat = synth.normal((2000, 16), 1002)
+    W = synth.conv_weight(27, 16, 16, 1003, "f32")
+    Wp = synth.linear_weight(16, 16, 1004, "f32")
+    out, m = oracle_lib.block(xyz, feat, 0.1, [(W, None, None, True)], Wp, relu_p=True, residual=True)
+    ref = _dense_block_config1(xyz, feat.astype(np.float64), 0.1, W.astype(np.float64), Wp.astype(np.float64),
+                               residual=True, relu=True)
+    np.testing.assert_allclose(out, ref, rtol=1e-5, atol=1e-5)
+    plain, _ = oracle_lib.block(xyz, feat, 0.1, [(W, None, None, True)], Wp, relu_p=True)
+    assert np.abs(out - plain).max() > 1e-2  # the identity branch changes the result

@@ -156,3 +156,27 @@ def test_conv_errors(oracle_lib):
     with pytest.raises(o.OracleError) as e:
         o.sparse_conv(x, off[:10], pairs, np.zeros((9, 4, 4), np.float32), 2)
     assert e.value.status == o.ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_conv_residual_input(oracle_lib, dtype):
+    """The residual input is added after scale/shift and before the activation:
+    zero weights return it (exactly, or its ReLU); otherwise the sum of the plain
+    conv and the input, rounded once."""
+    rng = np.random.default_rng(61)
+    c = np.unique(rng.integers(-5, 5, size=(500, 3)), axis=0).astype(np.int32)
+    rc = np.concatenate([np.zeros((len(c), 1), np.int32), c], 1)
+    _, off, pairs = oracle_lib.kernel_map(rc)
+    m, C = len(rc), 12
+    x = synth.normal((m, C), 62, dtype=dtype)
+    r = synth.normal((m, C), 63, dtype=dtype)
+    zero = np.zeros((27, C, C), synth.to_storage(np.zeros(1, np.float32), dtype).dtype)
+    np.testing.assert_array_equal(oracle_lib.sparse_conv(x, off, pairs, zero, m, dtype, res=r), r)
+    rr = synth.from_storage(r, dtype)
+    got = synth.from_storage(oracle_lib.sparse_conv(x, off, pairs, zero, m, dtype, relu=True, res=r), dtype)
+    np.testing.assert_array_equal(got, np.maximum(rr, 0.0))
+    W = synth.conv_weight(27, C, C, 64, "f32")
+    plain = oracle_lib.sparse_conv(synth.from_storage(x, dtype), off, pairs, W, m, "f32")
+    withr = oracle_lib.sparse_conv(synth.from_storage(x, dtype), off, pairs, W, m, "f32",
+                                   res=rr.astype(np.float32))
+    np.testing.assert_allclose(withr, plain.astype(np.float64) + rr, rtol=1e-6, atol=1e-6)
