@@ -191,6 +191,11 @@ typedef struct spv_block_params {
     const float* shift_p;   /* [C] f32 or NULL */
     int32_t relu_p;
     spv_devox_mode devox_mode;
+    /* Residual block (Sec. 3.3: the voxel branch aggregates with residual
+     * sparse-convolution blocks): nonzero makes the last conv add the block's
+     * voxel input x (the voxelized point features) to its output after scale
+     * and shift and before its ReLU: y = act(scale * conv(.) + shift + x). */
+    int32_t residual;
     /* Optional profiling (NULL = off): n_events >= 7 hipEvent_t handles, created
      * by the caller, recorded on the stream at the phase boundaries:
      * [0] start, [1] voxelized, [2] kernel map built, [3] conv plan built and

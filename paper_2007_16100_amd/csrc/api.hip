@@ -116,6 +116,7 @@ struct BlockLayout {
     int64_t* m_dev;
     void* va;
     void* vb;
+    void* vc;
     int32_t* off;
     int32_t* pairs;
     int64_t pair_cap;
@@ -142,6 +143,7 @@ size_t layout_block(void* ws, size_t bytes, int64_t n, int C, int dt, BlockLayou
     L.m_dev = a.take<int64_t>(1);
     L.va = a.take<char>((size_t)nn * C * esize(dt));
     L.vb = a.take<char>((size_t)nn * C * esize(dt));
+    L.vc = a.take<char>((size_t)nn * C * esize(dt));  // a residual block's last output (its input stays in va)
     L.off = a.take<int32_t>(28);
     L.pair_cap = 27 * nn;
     L.pairs = a.take<int32_t>(2 * L.pair_cap);
@@ -410,7 +412,15 @@ spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_pa
     void* cur = L.va;
     void* nxt = L.vb;
     for (int l = 0; l < p->n_convs; ++l) {
-        launch_conv_run(s, L.plan, cur, C, nn, L.pairs, L.pair_cap, 0, p->W[l], L.wpack_conv[l], p->scale[l],
+        ConvPlan plan = L.plan;
+        const bool res = p->residual && l == p->n_convs - 1;
+        if (res) {
+            // the last conv of a residual block adds the block's voxel input
+            // (still in va) and writes a buffer that aliases neither
+            plan.res = L.va;
+            nxt = (cur == L.vb) ? L.vc : L.vb;
+        }
+        launch_conv_run(s, plan, cur, C, nn, L.pairs, L.pair_cap, 0, p->W[l], L.wpack_conv[l], p->scale[l],
                         p->shift[l], p->relu[l], nxt, C, dt);
         void* t = cur;
         cur = nxt;

@@ -487,11 +487,21 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))) voi
         const float4 a0 = *(const float4*)(acc + (size_t)r * ACS + 8 * c8);
         const float4 a1 = *(const float4*)(acc + (size_t)r * ACS + 8 * c8 + 4);
         float v[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        float rv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        if (p.res) {
+            const uint4 u = *(const uint4*)((const uint16_t*)p.res + (row0 + r) * Cout + 8 * c8);
+            const uint32_t uu[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                rv[2 * j] = from16<DT>(uu[j] & 0xFFFF);
+                rv[2 * j + 1] = from16<DT>(uu[j] >> 16);
+            }
+        }
         uint32_t w[4];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int col = 8 * c8 + j;
-            float y = v[j] * (scale ? scale[col] : 1.f) + (shift ? shift[col] : 0.f);
+            float y = v[j] * (scale ? scale[col] : 1.f) + (shift ? shift[col] : 0.f) + rv[j];
             if (relu) y = fmaxf(y, 0.f);
             v[j] = y;
         }
@@ -547,6 +557,7 @@ __global__ __launch_bounds__(256) void k_conv_tile_valu(ConvPlan p, const void* 
     const float sc = scale ? scale[col] : 1.f, sh = shift ? shift[col] : 0.f;
     for (int r = rl; r < rows; r += 4) {
         float y = acc[r * 64 + cl] * sc + sh;
+        if (p.res) y += ld_feat<DT>(p.res, (row0 + r) * Cout + col);
         if (relu) y = fmaxf(y, 0.f);
         st_feat<DT>(out, (row0 + r) * Cout + col, y);
     }

@@ -45,7 +45,8 @@ template <int DT, int KCH, int NB, int RB, int NW, int PH>
 __global__ __launch_bounds__(64 * NW) void k_conv_union(
     const int32_t* __restrict__ nbr, const int64_t* __restrict__ m_out_dev, int64_t m_cap,
     const uint16_t* __restrict__ in, int Cin, int64_t in_rows, const uint4* __restrict__ wpack,
-    const float* __restrict__ scale, const float* __restrict__ shift, int relu, uint16_t* __restrict__ out) {
+    const float* __restrict__ scale, const float* __restrict__ shift, int relu, const uint16_t* __restrict__ res,
+    uint16_t* __restrict__ out) {
     constexpr int K3 = kUK3;
     constexpr int FR = KCH * NB;  // 1 KB weight fragments per offset
     constexpr int Cout = NB * 16;
@@ -193,10 +194,17 @@ __global__ __launch_bounds__(64 * NW) void k_conv_union(
         if (row >= m) continue;
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-            float y[4];
+            float y[4], rv[4] = {0.f, 0.f, 0.f, 0.f};
+            if (res) {  // the residual input, same layout as the output
+                const uint2 u = *(const uint2*)(res + row * Cout + nb * 16 + 4 * g);
+                rv[0] = from16<DT>(u.x & 0xFFFF);
+                rv[1] = from16<DT>(u.x >> 16);
+                rv[2] = from16<DT>(u.y & 0xFFFF);
+                rv[3] = from16<DT>(u.y >> 16);
+            }
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                y[e] = acc[b][nb][e] * sc[nb][e] + sh[nb][e];
+                y[e] = acc[b][nb][e] * sc[nb][e] + sh[nb][e] + rv[e];
                 if (relu) y[e] = fmaxf(y[e], 0.f);
             }
             const uint32_t lo = (uint32_t)to16<DT>(y[0]) | ((uint32_t)to16<DT>(y[1]) << 16);
@@ -228,7 +236,7 @@ static void launch_union_c(hipStream_t s, const ConvPlan& p, const void* in, int
     const unsigned grid = (unsigned)(((p.m_cap + rows_wg - 1) / rows_wg + 7) / 8 * 8);
     k_conv_union<DT, KCH, NB, RB, NW, PH><<<grid, 64 * NW, 0, s>>>(
         p.nbr, p.m_out_dev, p.m_cap, (const uint16_t*)in, 32 * KCH, in_rows, (const uint4*)wpack, scale, shift, relu,
-        (uint16_t*)out);
+        (const uint16_t*)p.res, (uint16_t*)out);
 }
 
 template <int DT>

@@ -204,6 +204,9 @@ struct ConvPlan {
     int32_t* nbr;       // [m_cap][K3] when use_union
     const int64_t* m_out_dev;
     Header* h;          // status word (unsorted or out-of-range pairs)
+    // residual input [m][Cout] of the storage type (nullptr = none), added after
+    // scale and shift and before the activation; it must not alias the output
+    const void* res = nullptr;
 };
 void plan_conv_ws(Arena& a, ConvPlan& p, int64_t m_out_cap, int K3, int Cin, int Cout, int dt);
 struct PackJob;

@@ -45,7 +45,8 @@ class BlockParams(ct.Structure):
     _fields_ = [("C", ct.c_int32), ("dtype", ct.c_int32), ("voxel_size", ct.c_float), ("n_convs", ct.c_int32),
                 ("W", ct.c_void_p * 2), ("scale", ct.c_void_p * 2), ("shift", ct.c_void_p * 2),
                 ("relu", ct.c_int32 * 2), ("Wp", ct.c_void_p), ("scale_p", ct.c_void_p), ("shift_p", ct.c_void_p),
-                ("relu_p", ct.c_int32), ("devox_mode", ct.c_int32), ("events", ct.POINTER(ct.c_void_p)),
+                ("relu_p", ct.c_int32), ("devox_mode", ct.c_int32), ("residual", ct.c_int32),
+                ("events", ct.POINTER(ct.c_void_p)),
                 ("n_events", ct.c_int32)]
 
 
@@ -232,7 +233,8 @@ def spv_devoxelize(ws: Workspace, grid_coords: torch.Tensor, vfeat: torch.Tensor
 
 
 def make_block_params(C: int, dtype: torch.dtype, voxel_size: float, convs: Sequence, Wp: torch.Tensor,
-                      scale_p=None, shift_p=None, relu_p: bool = True, mode: int = SPV_DEVOX_CENTER) -> BlockParams:
+                      scale_p=None, shift_p=None, relu_p: bool = True, mode: int = SPV_DEVOX_CENTER,
+                      residual: bool = False) -> BlockParams:
     """convs: list of (W [27,C,C], scale|None, shift|None, relu) device tensors.
 
     The struct holds raw device pointers; it also keeps references to every
@@ -253,6 +255,7 @@ def make_block_params(C: int, dtype: torch.dtype, voxel_size: float, convs: Sequ
     p.shift_p = ptr(shift_p)
     p.relu_p = int(relu_p)
     p.devox_mode = mode
+    p.residual = int(residual)
     p._keep = keep
     return p
 

@@ -504,6 +504,32 @@ def test_block_equals_stand_alone_ops(spv, sweep, mode, C):
     check_close(host(out, dt)[:len(xyz)], rout, dt)
 
 
+@pytest.mark.parametrize("C,dtype,nconv", [(16, "f32", 1), (16, "f32", 2), (48, "bf16", 2), (96, "bf16", 2)])
+def test_block_residual(spv, sweep, C, dtype, nconv):
+    """Residual blocks (Sec. 3.3): the last conv adds the block's voxel input
+    before its ReLU -- through the vector-ALU (f32), tile (C = 48) and
+    neighbour-table (C = 96) conv kernels -- against the oracle's residual block."""
+    xyz = sweep[::2] if C != 96 else sweep
+    v = 0.05
+    feat = synth.normal((len(xyz), C), 81, dtype=dtype)
+    convs = []
+    for l in range(nconv):
+        sc, sh = synth.folded_bn(C, 82 + l)
+        convs.append((synth.conv_weight(27, C, C, 84 + l, dtype), sc, sh, True))
+    Wp = synth.linear_weight(C, C, 86, dtype)
+    dconvs = [(dev(W, dtype), dev(sc), dev(sh), r) for W, sc, sh, r in convs]
+    params = spv.make_block_params(C, TD[dtype], v, dconvs, dev(Wp, dtype), None, None, relu_p=True, residual=True)
+    ws = spv.Workspace.for_block(len(xyz), C)
+    out, m = spv.spv_block(ws, params, dev(xyz), dev(feat, dtype), sync=True)
+    rout, rm = oracle.block(xyz, feat, v, convs, Wp, relu_p=True, dtype=dtype, residual=True)
+    assert m == rm
+    got = host(out, dtype)[:len(xyz)]
+    check_close(got, rout, dtype)
+    plain, _ = oracle.block(xyz, feat, v, convs, Wp, relu_p=True, dtype=dtype)
+    diff = np.abs(synth.from_storage(rout, dtype) - synth.from_storage(plain, dtype)).max()
+    assert diff > 0.05  # the identity branch matters here
+
+
 def test_block_graph_replay(spv, sweep):
     """spv_block captured into a graph: every replay, with eager work and
     synchronization between them, reproduces the eager result bit for bit."""
