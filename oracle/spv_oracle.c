@@ -271,7 +271,7 @@ int spvo_kernel_map(const int32_t* in_coords, int64_t m_in, int32_t K, int32_t s
     if (m_in < 0 || m_in >= ((int64_t)1 << 31) || !off || !total || !m_out || pair_cap < 0)
         return SPVO_ERR_INVALID_ARG;
     if (m_in > 0 && !in_coords) return SPVO_ERR_INVALID_ARG;
-    if (!((K == 3 && stride == 1) || (K == 2 && stride == 2))) return SPVO_ERR_UNSUPPORTED;
+    if (!((K == 3 && (stride == 1 || stride == 2)) || (K == 2 && stride == 2))) return SPVO_ERR_UNSUPPORTED;
     if (stride == 2 && !out_coords) return SPVO_ERR_INVALID_ARG;
     if (!coords_in_range(in_coords, m_in)) return SPVO_ERR_RANGE;
 

@@ -56,9 +56,11 @@ int spvo_voxelize(const float* xyz, const int32_t* batch, int64_t n, float voxel
                   int32_t* coords, void* vfeat, int32_t* counts, int32_t* pt2vox,
                   int64_t* m_out);
 
-/* Kernel map.  K=3 stride=1: submanifold (outputs = inputs).  K=2 stride=2:
- * outputs = unique floor(c/2), written to out_coords in ascending order.
- * Pairs (in, out) grouped by offset k (CSR off[K^3+1]), each group sorted by out. */
+/* Kernel map.  K=3 stride=1: submanifold (outputs = inputs).  Stride 2 (K=2 or
+ * K=3): outputs = unique floor(c/2), written to out_coords in ascending order;
+ * (in, out) is a pair of offset k iff in = 2 out + delta_k (delta in {0,1}^3 for
+ * K=2, {-1,0,1}^3 for K=3).  Pairs (in, out) grouped by offset k (CSR
+ * off[K^3+1]), each group sorted by out. */
 int spvo_kernel_map(const int32_t* in_coords, int64_t m_in, int32_t K, int32_t stride,
                     int32_t* out_coords, int64_t* m_out,
                     int32_t* off, int32_t* pairs, int64_t pair_cap, int64_t* total);

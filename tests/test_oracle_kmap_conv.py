@@ -7,6 +7,7 @@ dense one read at the active sites because inactive inputs are zero).
 """
 import numpy as np
 import pytest
+import torch
 
 from paper_2007_16100_amd import synth
 from tests import dense_ref
@@ -180,3 +181,48 @@ def test_conv_residual_input(oracle_lib, dtype):
     withr = oracle_lib.sparse_conv(synth.from_storage(x, dtype), off, pairs, W, m, "f32",
                                    res=rr.astype(np.float32))
     np.testing.assert_allclose(withr, plain.astype(np.float64) + rr, rtol=1e-6, atol=1e-6)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_kmap_k3_stride2_allpairs(oracle_lib, seed):
+    """K=3 stride 2: (i, j, k) is a pair iff c_i - 2 c'_j is offset k's delta in
+    {-1,0,1}^3, with c' the distinct floor(c / 2) -- checked against every
+    (input, output) pair of a small set."""
+    rng = np.random.default_rng(700 + seed)
+    m = 160
+    pts = np.unique(np.concatenate([rng.integers(0, 2, (m, 1)), rng.integers(-6, 6, (m, 3))], 1),
+                    axis=0).astype(np.int32)
+    oc, off, pairs = oracle_lib.kernel_map(pts, 3, 2)
+    want_oc = np.unique(np.concatenate([pts[:, :1], pts[:, 1:] >> 1], 1), axis=0)
+    np.testing.assert_array_equal(oc, want_oc)
+    want = []
+    for k in range(27):
+        d = np.array([k // 9 - 1, (k // 3) % 3 - 1, k % 3 - 1])
+        for j, o in enumerate(oc):
+            for i, c in enumerate(pts):
+                if c[0] == o[0] and np.array_equal(c[1:] - 2 * o[1:], d):
+                    want.append((k, i, j))
+    got = [(k, int(pairs[p, 0]), int(pairs[p, 1])) for k in range(27) for p in range(off[k], off[k + 1])]
+    assert got == want  # grouped by offset, each group in output (then input) order
+
+
+def test_conv_k3_stride2_dense(oracle_lib):
+    """A conv on the K=3 stride-2 map equals the dense conv3d with stride 2 and
+    padding 1 at the active coarse sites (inputs zero elsewhere)."""
+    rng = np.random.default_rng(710)
+    pts = np.unique(rng.integers(-6, 6, (350, 3)), axis=0).astype(np.int32)
+    rc = np.concatenate([np.zeros((len(pts), 1), np.int32), pts], 1)
+    oc, off, pairs = oracle_lib.kernel_map(rc, 3, 2)
+    Cin, Cout = 5, 7
+    x = synth.normal((len(rc), Cin), 711)
+    W = synth.conv_weight(27, Cin, Cout, 712, "f32")
+    got = oracle_lib.sparse_conv(x, off, pairs, W, len(oc), "f32")
+    sh = 8  # an even shift keeps floor(c / 2) aligned with the stride-2 grid
+    q = pts + sh
+    dense = np.zeros((Cin, 20, 20, 20))
+    dense[:, q[:, 0], q[:, 1], q[:, 2]] = x.T
+    w = torch.from_numpy(W.astype(np.float64).reshape(3, 3, 3, Cin, Cout).transpose(4, 3, 0, 1, 2).copy())
+    y = torch.nn.functional.conv3d(torch.from_numpy(dense)[None], w, stride=2, padding=1)[0].numpy()
+    o = oc[:, 1:] + sh // 2
+    ref = y[:, o[:, 0], o[:, 1], o[:, 2]].T
+    np.testing.assert_allclose(got, ref, rtol=1e-5, atol=1e-5)
