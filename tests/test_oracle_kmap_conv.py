@@ -79,7 +79,7 @@ def test_kmap_errors(oracle_lib):
         o.kernel_map(np.array([[0, 32767, 0, 0]], np.int32))
     assert e.value.status == o.ERR_RANGE
     with pytest.raises(o.OracleError) as e:
-        o.kernel_map(np.array([[0, 0, 0, 0]], np.int32), K=3, stride=2)
+        o.kernel_map(np.array([[0, 0, 0, 0]], np.int32), K=2, stride=1)
     assert e.value.status == o.ERR_UNSUPPORTED
     with pytest.raises(o.OracleError) as e:
         o.kernel_map(np.array([[0, 0, 0, 0], [0, 0, 0, 1]], np.int32), pair_cap=3)
