@@ -107,13 +107,17 @@ spv_status spv_voxelize(void* stream, void* ws, size_t ws_bytes,
  *     to out_coords in ascending order; pair iff c_i = 2 c_j + delta_k with
  *     delta_k in {0,1}^3, k = 4 dx + 2 dy + dz.  The same pairs, used with
  *     transposed=1 in spv_sparse_conv, give the matching upsampling conv.
+ *   K=3, stride=2 (downsampling with a 3x3x3 kernel, Sec. 3.2's strided sparse
+ *     convolution): the same outputs as K=2; pair iff c_i = 2 c_j + delta_k with
+ *     delta_k in {-1,0,1}^3, k = 9(dx+1) + 3(dy+1) + (dz+1).  An input is in at
+ *     most 8 pairs (2 per odd coordinate), so pair_cap = 8 m_cap suffices.
  * In:  in_coords [m_cap][4] i32 (distinct); m_in_dev: device count (NULL = m_cap).
  * Out: out_coords [m_cap][4] (stride 2 only; may be NULL for stride 1);
  *      m_out_dev (device int64, may be NULL); off [K^3+1] i32 (CSR by offset,
  *      device); pairs [pair_cap][2] i32 as (in, out), grouped by k and sorted by
  *      out within a group.  total_host (optional): synchronizes and stores the
  *      number of pairs; SPV_ERR_CAPACITY if it exceeds pair_cap (K^3 * m_cap
- *      always suffices; for stride 2, m_cap does).
+ *      always suffices; for K=2 stride 2, m_cap does).
  */
 spv_status spv_kernel_map(void* stream, void* ws, size_t ws_bytes,
                           const int32_t* in_coords, const int64_t* m_in_dev, int64_t m_cap,

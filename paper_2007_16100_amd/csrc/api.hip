@@ -171,6 +171,7 @@ size_t spv_workspace_bytes(int64_t max_points, int32_t max_C) {
     size_t s = layout_voxelize(nullptr, 0, max_points, v);
     s = std::max(s, layout_kmap(nullptr, 0, max_points, 3, 1, m));
     s = std::max(s, layout_kmap(nullptr, 0, max_points, 2, 2, m));
+    s = std::max(s, layout_kmap(nullptr, 0, max_points, 3, 2, m));
     s = std::max(s, layout_conv(nullptr, 0, max_points, 27, max_C, max_C, SPV_BF16, c));
     s = std::max(s, layout_devox(nullptr, 0, max_points, max_points, max_C, max_C, d));
     return s;
@@ -247,7 +248,7 @@ spv_status spv_kernel_map(void* stream, void* ws, size_t ws_bytes, const int32_t
                           int32_t* off, int32_t* pairs, int64_t pair_cap, int64_t* total_host) {
     if (!ws || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || !off || pair_cap < 0) return SPV_ERR_INVALID_ARG;
     if (m_cap > 0 && !in_coords) return SPV_ERR_INVALID_ARG;
-    if (!((K == 3 && stride == 1) || (K == 2 && stride == 2))) return SPV_ERR_UNSUPPORTED;
+    if (!((K == 3 && (stride == 1 || stride == 2)) || (K == 2 && stride == 2))) return SPV_ERR_UNSUPPORTED;
     if (stride == 2 && !out_coords) return SPV_ERR_INVALID_ARG;
     if (pair_cap > 0 && !pairs) return SPV_ERR_INVALID_ARG;
     MapLayout L;

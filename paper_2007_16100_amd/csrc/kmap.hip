@@ -16,10 +16,13 @@
 //           already-sorted output without atomics.
 // The 3x3x3 convolution consumes the neighbour table directly, so a block that
 // only needs the convolution stops after pass 1.
-// Stride 2 (K = 2): the output voxels are the distinct floor(c/2), deduplicated
-// in a second hash table and radix-sorted into canonical order; then the pairs
-// are a stable partition of the inputs by coordinate parity (a count pass, one
-// scan, a write pass with one coarse-table lookup per input).
+// Stride 2: the output voxels are the distinct floor(c/2), deduplicated in a
+// second hash table and radix-sorted into canonical order.  K = 2: the pairs are
+// a stable partition of the inputs by coordinate parity (a count pass, one scan,
+// a write pass with one coarse-table lookup per input).  K = 3: the same three
+// passes as the submanifold map, run over the output voxels, with output C
+// probing the input table at 2C + delta (a probe outside the key range is
+// absent: no input can sit there).
 #include "spv_internal.hpp"
 
 namespace spv {
@@ -203,9 +206,11 @@ __global__ __launch_bounds__(kMapThreads) void k_s2_write(Header* h, Table coars
     }
 }
 
-// pass 1 of a submanifold 3x3x3 map (see the file comment); bcnt may be null.
+// pass 1 of a 3x3x3 map (see the file comment); bcnt may be null.  S2: coords
+// are the stride-2 outputs and offset k of output C probes 2C + delta_k.
 // The block's 64 rows of the table are assembled in LDS and written out as one
 // contiguous run.
+template <bool S2>
 __global__ __launch_bounds__(256) void k_map_nbr3(Table fine, const int32_t* coords, const int64_t* m_out,
                                                   int64_t cap, int32_t* nbr, uint32_t* bcnt) {
     __shared__ int32_t tile[kNbrVox * 27];  // row stride 27 words: conflict-free per-lane writes
@@ -227,9 +232,15 @@ __global__ __launch_bounds__(256) void k_map_nbr3(Table fine, const int32_t* coo
         const int k = wave + 4 * q;
         int dx, dy, dz;
         offset_delta<3>(k, dx, dy, dz);
-        // the centre offset of a submanifold map is the voxel itself
-        act[q] = valid && k < 27 && k != 13;
-        key[q] = pack_key(c[0], c[1] + dx, c[2] + dy, c[3] + dz);
+        if constexpr (S2) {
+            const int x = 2 * c[1] + dx, y = 2 * c[2] + dy, z = 2 * c[3] + dz;
+            act[q] = valid && k < 27 && in_key_range(x) && in_key_range(y) && in_key_range(z);
+            key[q] = pack_key(c[0], x, y, z);
+        } else {
+            // the centre offset of a submanifold map is the voxel itself
+            act[q] = valid && k < 27 && k != 13;
+            key[q] = pack_key(c[0], c[1] + dx, c[2] + dy, c[3] + dz);
+        }
     }
     table_find_n<kNbrProbes>(fine, key, act, res);
     const uint32_t nblk = gridDim.x;
@@ -237,7 +248,7 @@ __global__ __launch_bounds__(256) void k_map_nbr3(Table fine, const int32_t* coo
     for (int q = 0; q < kNbrProbes; ++q) {
         const int k = wave + 4 * q;
         if (k >= 27) break;
-        const int32_t i = (k == 13) ? (int32_t)j : res[q];
+        const int32_t i = (!S2 && k == 13) ? (int32_t)j : res[q];
         const bool present = valid && i >= 0;
         tile[lane * 27 + k] = present ? i + 1 : 0;
         if (bcnt) {
@@ -286,7 +297,7 @@ __global__ __launch_bounds__(256) void k_map_pairs3(Header* h, const int32_t* nb
 void launch_kernel_map_nbr(hipStream_t s, const KmapWs& w, const int32_t* coords, const int64_t* m_dev,
                            int64_t m_cap, int32_t* nbr) {
     const int64_t mc = m_cap > 0 ? m_cap : 1;
-    k_map_nbr3<<<blocks_for(mc, kNbrVox), 256, 0, s>>>(w.fine, coords, m_dev, mc, nbr, nullptr);
+    k_map_nbr3<false><<<blocks_for(mc, kNbrVox), 256, 0, s>>>(w.fine, coords, m_dev, mc, nbr, nullptr);
 }
 
 void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const int32_t* in_coords,
@@ -295,17 +306,20 @@ void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const in
     const int64_t mc = m_cap > 0 ? m_cap : 1;
     const unsigned nblk = blocks_for(mc, kMapThreads);
     const int K3 = K * K * K;
-    const bool fine = build_fine && K == 3;  // a stride-2 map needs no table of its inputs
+    const bool fine = build_fine && K == 3;  // a K = 2 map needs no table of its inputs
     if (fine) {
-        // the table build also hands the output count (= the input count) on
+        // a submanifold map's table build also hands the output count (= the
+        // input count) on
         launch_clear(s, w.h, w.fine, clear_header);
-        launch_table_build(s, w.h, w.fine, in_coords, m_in_dev, m_cap, w.m_out, m_out_dev);
+        launch_table_build(s, w.h, w.fine, in_coords, m_in_dev, m_cap, stride == 1 ? w.m_out : nullptr,
+                           stride == 1 ? m_out_dev : nullptr);
     } else if (clear_header && stride != 2) {
         launch_clear_header(s, w.h);
     }
     if (stride == 2) {
-        // coarse table, status header and the coarse key counter in one launch
-        launch_clear(s, w.h, w.coarse, clear_header, w.m_out + 1);
+        // coarse table, status header (unless cleared above) and the coarse key
+        // counter in one launch
+        launch_clear(s, w.h, w.coarse, clear_header && !fine, w.m_out + 1);
         const unsigned nins = blocks_for(mc, kAppendThreads);
         k_map_coarse_insert<<<nins, kAppendThreads, 0, s>>>(w.h, w.coarse, w.sort, w.m_out + 1, in_coords, m_in_dev,
                                                             mc);
@@ -315,8 +329,12 @@ void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const in
     }
     if (K == 3) {
         const unsigned nb3 = blocks_for(mc, kNbrVox);
-        if (!fine) k_map_same_count<<<1, 1, 0, s>>>(m_in_dev, m_cap, w.m_out, m_out_dev);
-        k_map_nbr3<<<nb3, 256, 0, s>>>(w.fine, in_coords, w.m_out, mc, w.nbr, w.bcnt);
+        if (stride == 2) {
+            k_map_nbr3<true><<<nb3, 256, 0, s>>>(w.fine, out_coords, w.m_out, mc, w.nbr, w.bcnt);
+        } else {
+            if (!fine) k_map_same_count<<<1, 1, 0, s>>>(m_in_dev, m_cap, w.m_out, m_out_dev);
+            k_map_nbr3<false><<<nb3, 256, 0, s>>>(w.fine, in_coords, w.m_out, mc, w.nbr, w.bcnt);
+        }
         launch_exclusive_scan(s, (const int32_t*)w.bcnt, (int32_t*)w.bbase, nullptr, (int64_t)27 * nb3, w.scan_tmp);
         k_map_pairs3<<<nb3, 256, 0, s>>>(w.h, w.nbr, w.m_out, mc, w.bbase, off, pairs, pair_cap);
     } else {

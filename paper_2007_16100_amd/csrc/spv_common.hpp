@@ -20,6 +20,7 @@ constexpr uint64_t kEmpty = ~0ull;
 constexpr int kCoordMin = -32767;
 constexpr int kCoordMax = 32766;
 constexpr int kBatchMax = 65534;
+__host__ __device__ inline bool in_key_range(int c) { return c >= kCoordMin && c <= kCoordMax; }
 
 __host__ __device__ inline uint64_t pack_key(int b, int x, int y, int z) {
     return ((uint64_t)(uint32_t)b << 48) | ((uint64_t)(uint32_t)(x + 32768) << 32) |

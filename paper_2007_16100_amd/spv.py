@@ -182,7 +182,8 @@ def spv_kernel_map(ws: Workspace, in_coords: torch.Tensor, K: int = 3, stride: i
     m_cap = in_coords.shape[0] if m_cap is None else m_cap
     K3 = K ** 3
     if pair_cap is None:
-        pair_cap = max(1, (m_cap if stride == 2 else K3 * m_cap))
+        # K=2 s2: each input in one pair; K=3 s2: at most 2 outputs per odd axis
+        pair_cap = max(1, m_cap if K == 2 else (8 * m_cap if stride == 2 else K3 * m_cap))
     oc = torch.empty((max(m_cap, 1), 4), dtype=torch.int32, device=dev) if stride == 2 else None
     km = KernelMap(oc, torch.zeros(1, dtype=torch.int64, device=dev), torch.empty(K3 + 1, dtype=torch.int32, device=dev),
                    torch.empty((pair_cap, 2), dtype=torch.int32, device=dev), None)

@@ -47,7 +47,7 @@ def test_host_side_validation_without_gpu():
                         ct.c_void_p(16), ct.c_void_p(16), None, None)
     assert st == spv.SPV_ERR_CAPACITY
     # unsupported kernel-map geometry
-    st = L.spv_kernel_map(None, ws, 1 << 30, ct.c_void_p(16), None, 4, 3, 2, ct.c_void_p(16), None, ct.c_void_p(16),
+    st = L.spv_kernel_map(None, ws, 1 << 30, ct.c_void_p(16), None, 4, 2, 1, ct.c_void_p(16), None, ct.c_void_p(16),
                           ct.c_void_p(16), 100, None)
     assert st == spv.SPV_ERR_UNSUPPORTED
     # unsupported conv K3, bad dtype

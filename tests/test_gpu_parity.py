@@ -232,7 +232,7 @@ def run_kmap(spv, coords, K, stride):
     return oc, host(km.off), host(km.pairs)[:km.total], km
 
 
-@pytest.mark.parametrize("K,stride", [(3, 1), (2, 2)])
+@pytest.mark.parametrize("K,stride", [(3, 1), (2, 2), (3, 2)])
 def test_kmap_sweep_bitexact(spv, sweep, K, stride):
     rc, _, _, _ = oracle.voxelize(sweep, 0.05)
     oc, off, pairs, _ = run_kmap(spv, rc, K, stride)
@@ -249,7 +249,7 @@ def test_kmap_random_small(spv, seed):
     m = int(rng.integers(1, 3000))
     pts = np.unique(np.concatenate([rng.integers(0, 2, (m, 1)), rng.integers(-12, 12, (m, 3))], 1), axis=0)
     pts = pts.astype(np.int32)
-    for K, stride in [(3, 1), (2, 2)]:
+    for K, stride in [(3, 1), (2, 2), (3, 2)]:
         oc, off, pairs, _ = run_kmap(spv, pts, K, stride)
         roc, roff, rpairs = oracle.kernel_map(pts, K, stride)
         np.testing.assert_array_equal(off, roff)
@@ -258,7 +258,7 @@ def test_kmap_random_small(spv, seed):
             np.testing.assert_array_equal(oc, roc)
 
 
-@pytest.mark.parametrize("K,stride", [(3, 1), (2, 2)])
+@pytest.mark.parametrize("K,stride", [(3, 1), (2, 2), (3, 2)])
 def test_kmap_large_batched(spv, K, stride):
     """~400k voxels in 4 batches over a wide range (coarse keys past 32 bits):
     the stride-2 parity partition and the submanifold map over more than 256
@@ -275,6 +275,24 @@ def test_kmap_large_batched(spv, K, stride):
     np.testing.assert_array_equal(pairs, rpairs)
     if stride == 2:
         np.testing.assert_array_equal(oc, roc)
+
+
+def test_kmap_k3_stride2_key_range_edges(spv):
+    """3x3x3 stride-2 probes 2C + delta reach one step past the coordinate range
+    at both ends (2 * -16384 - 1 and 2 * 16383 + 1): they must find nothing
+    rather than wrap onto a stored key."""
+    e = []
+    for b in (0, 3):
+        for x in (-32767, -32766, -32765, 32764, 32765, 32766):
+            for y in (-32767, 0, 1, 32766):
+                for z in (-32767, -1, 32765, 32766):
+                    e.append((b, x, y, z))
+    pts = np.array(sorted(set(e)), np.int32)
+    oc, off, pairs, _ = run_kmap(spv, pts, 3, 2)
+    roc, roff, rpairs = oracle.kernel_map(pts, 3, 2)
+    np.testing.assert_array_equal(oc, roc)
+    np.testing.assert_array_equal(off, roff)
+    np.testing.assert_array_equal(pairs, rpairs)
 
 
 def test_kmap_duplicate_coords_rejected(spv):
@@ -321,6 +339,24 @@ def test_conv_strided_and_transposed_sweep(spv, sweep):
     gotT = run_conv(spv, ref, off, pairs, WT, len(rc), "bf16", transposed=True)
     refT = oracle.sparse_conv(ref, off, pairs, WT, len(rc), "bf16", transposed=True)
     check_close(gotT, refT, "bf16")
+
+
+@pytest.mark.parametrize("cin,cout,dtype", [(32, 64, "bf16"), (64, 128, "bf16"), (16, 16, "f32"), (96, 96, "f16")])
+def test_conv_k3_stride2_and_transposed_sweep(spv, sweep, cin, cout, dtype):
+    """Strided 3x3x3 conv on the K=3 stride-2 map (GPU-built, bit-exact against the
+    oracle's map) and the transposed conv back onto the fine voxels."""
+    rc, _, _, _ = oracle.voxelize(sweep, 0.05)
+    oc, off, pairs, _ = run_kmap(spv, rc, 3, 2)
+    x = synth.normal((len(rc), cin), 1016, dtype=dtype)
+    W = synth.conv_weight(27, cin, cout, 1017, dtype)
+    sc, sh = synth.folded_bn(cout, 1018)
+    got = run_conv(spv, x, off, pairs, W, len(oc), dtype, sc, sh, True)
+    ref = oracle.sparse_conv(x, off, pairs, W, len(oc), dtype, sc, sh, True)
+    check_close(got, ref, dtype)
+    WT = synth.conv_weight(27, cout, cin, 1019, dtype)
+    gotT = run_conv(spv, ref, off, pairs, WT, len(rc), dtype, transposed=True)
+    refT = oracle.sparse_conv(ref, off, pairs, WT, len(rc), dtype, transposed=True)
+    check_close(gotT, refT, dtype)
 
 
 @pytest.mark.parametrize("K,cin,cout,dtype", [(3, 32, 32, "bf16"), (3, 16, 16, "f32"), (2, 64, 128, "bf16")])
