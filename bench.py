@@ -219,7 +219,8 @@ def sizes_mode(args):
 
 def configs_mode(args):
     """Map build and conv alone on the sweep: a submanifold 3x3x3 conv 32->32 (seed 1002), and
-    the stride-2 map with a k2s2 conv 64->128 and its transposed 128->64 (seed 1003).  One JSON
+    the stride-2 maps (K = 2 and K = 3) with a strided conv 64->128 and its transposed 128->64
+    on each (seed 1003).  One JSON
     line per op: median HIP-event time, algorithmic bytes / FLOPs and both roofline fractions."""
     import torch
     from paper_2007_16100_amd import spv, synth
@@ -298,6 +299,23 @@ def configs_mode(args):
             ms = timed(lambda: spv.spv_sparse_conv(wsm, y, km.off, km.pairs, WT, m, transposed=True, out=z))
             report("conv k2s2 transposed 128->64", ms, 2 * 128 * mc + 2 * 64 * m + 8 * P + 8 * 64 * 128 * 2,
                    2.0 * 64 * 128 * P, voxels=m, coarse_voxels=mc, pairs=P)
+            # the 3x3x3 stride-2 map (same coarse voxels; probes of the fine table) and its convs
+            km3 = spv.spv_kernel_map(wsm, coords, K=3, stride=2)
+            P3 = km3.total
+            print(json.dumps({"op": "kernel_map k3 s2 statistics",
+                              "map_sizes": [int(x) for x in mapstats.map_sizes(km3.off)]}), flush=True)
+            ms = timed(lambda: spv.spv_kernel_map(wsm, coords, K=3, stride=2, sync=False))
+            report("kernel_map k3 s2", ms, 16 * m + 16 * mc + 24 * table_slots(m) + 8 * P3 + 4 * 28,
+                   voxels=m, coarse_voxels=mc, pairs=P3)
+            W3 = bf(synth.conv_weight(27, 64, 128, seed + 4, "bf16"))
+            W3T = bf(synth.conv_weight(27, 128, 64, seed + 5, "bf16"))
+            ms = timed(lambda: spv.spv_sparse_conv(wsm, x, km3.off, km3.pairs, W3, mc, m_out_dev=km3.m_out_dev,
+                                                   out=y))
+            report("conv k3s2 64->128", ms, 2 * 64 * m + 2 * 128 * mc + 8 * P3 + 27 * 64 * 128 * 2,
+                   2.0 * 64 * 128 * P3, voxels=m, coarse_voxels=mc, pairs=P3)
+            ms = timed(lambda: spv.spv_sparse_conv(wsm, y, km3.off, km3.pairs, W3T, m, transposed=True, out=z))
+            report("conv k3s2 transposed 128->64", ms, 2 * 128 * mc + 2 * 64 * m + 8 * P3 + 27 * 64 * 128 * 2,
+                   2.0 * 64 * 128 * P3, voxels=m, coarse_voxels=mc, pairs=P3)
         del ws, wsm
         torch.cuda.empty_cache()
 

@@ -285,6 +285,11 @@ spv_status spv_sparse_conv(void* stream, void* ws, size_t ws_bytes, const void* 
     if (m_out_cap == 0) return SPV_OK;
     hipStream_t s = (hipStream_t)stream;
     L.p.m_out_dev = m_out_dev;
+    // A transposed map gives an output few of the 27 offsets (a transposed
+    // stride-2 map at most 8, 2-3 on a sweep), which the neighbour-table kernel
+    // would still step through for every block: the tile kernel, which only
+    // visits pairs, takes it.
+    if (transposed) L.p.use_union = 0;
     // the plan clears the status header first and packs W in one of its launches
     launch_conv_plan(s, L.p, off, pairs, K3, transposed, pair_cap, in_rows,
                      conv_pack_job(K3, W, L.wpack, Cin, Cout, dt), true);

@@ -8,16 +8,18 @@
 //   output channels, accumulated in registers.  For each of the 27 offsets it
 //   gathers the 16 rows' neighbours (zeros where a neighbour is absent) and
 //   multiplies them by W[k] on v_mfma_f32_16x16x32_{bf16,f16}; blocks whose
-//   rows have no neighbour at that offset skip it.  W[k] is staged once per
-//   workgroup in LDS (asynchronous global->LDS copies two offsets ahead), and
-//   each wave's gathers for the next offset are in flight while the current
-//   one is multiplied.  The cost is MFMA work on absent neighbours: on a LiDAR
-//   sweep the 16-row unions of present offsets are ~3x the pairs.
+//   rows have no neighbour at that offset skip it.  The weights of a phase of
+//   offsets are staged per workgroup in LDS (global->LDS copies), and each
+//   wave's gathers for the next offset are in flight while the current one is
+//   multiplied.  The cost is MFMA work on absent neighbours: on a LiDAR sweep
+//   the 16-row unions of present offsets are ~3x the pairs.  Widths C_in,
+//   C_out in {32, 64, 96, 128}; submanifold and strided 3x3x3 maps.
 //
-// * k_conv_tile (stride-2 and transposed maps, where a 16-row union would be
-//   mostly empty): output rows in tiles of T with an LDS fp32 accumulator; the
-//   pairs of each (tile, offset) are a contiguous slice of the kernel map,
-//   multiplied 16 at a time and added into their output rows.
+// * k_conv_tile (K = 2 maps, transposed maps -- where a 16-row union would be
+//   mostly empty -- and the other widths): output rows in tiles of T with an
+//   LDS fp32 accumulator; the pairs of each (tile, offset) are a contiguous
+//   slice of the kernel map, multiplied 16 at a time and added into their
+//   output rows.
 //
 // A vector-ALU tile kernel covers fp32 and shapes the MFMA kernels do not take.
 #include "conv_common.hpp"

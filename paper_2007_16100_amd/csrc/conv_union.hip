@@ -214,23 +214,26 @@ __global__ __launch_bounds__(64 * NW) void k_conv_union(
     }
 }
 
-// instantiated for square layers C -> C with C in {32, 64, 96, 128} (the widths
-// of the blocks and networks built here); other shapes use the tile kernel
+// instantiated for C_in, C_out in {32, 64, 96, 128} (the widths of the blocks
+// and networks built here, square layers and the channel changes between
+// stages); other shapes use the tile kernel
 bool union_supported(int K3, int Cin, int Cout, int dt) {
-    if (K3 != 27 || dt == SPV_F32 || Cin != Cout) return false;
-    return Cin == 32 || Cin == 64 || Cin == 96 || Cin == 128;
+    if (K3 != 27 || dt == SPV_F32) return false;
+    const auto width_ok = [](int c) { return c == 32 || c == 64 || c == 96 || c == 128; };
+    return width_ok(Cin) && width_ok(Cout);
 }
 
 // Launch shape per width: 11 waves of 2 blocks (352 rows per workgroup: a
 // ~9*10^4-voxel scan gives ~250 workgroups, one round over the 256 CUs with
 // nearly every CU busy), phases of as many offsets as fit in 128 KB of LDS.
-template <int DT, int KCH>
+// 128 -> 128 takes one block per wave: two would not fit the 168 registers a
+// wave has at 11 waves per workgroup.
+template <int DT, int KCH, int NB>
 static void launch_union_c(hipStream_t s, const ConvPlan& p, const void* in, int64_t in_rows, const void* wpack,
                            const float* scale, const float* shift, int relu, void* out) {
-    constexpr int NB = 2 * KCH;  // C = 32 * KCH
-    constexpr int RB = 2, NW = 11;
     constexpr int FR = KCH * NB;
-    constexpr int PH = (128 / FR) < kUK3 ? (128 / FR) : kUK3;  // 27, 14, 7, 4 for C = 32, 64, 96, 128
+    constexpr int RB = FR >= 32 ? 1 : 2, NW = 11;
+    constexpr int PH = (128 / FR) < kUK3 ? (128 / FR) : kUK3;  // 27, 14, 7, 4 for C -> C = 32, 64, 96, 128
     constexpr int64_t rows_wg = (int64_t)NW * RB * 16;
     // a multiple of 8 workgroups: the kernel spreads the live tiles over the 8 XCDs
     const unsigned grid = (unsigned)(((p.m_cap + rows_wg - 1) / rows_wg + 7) / 8 * 8);
@@ -239,22 +242,32 @@ static void launch_union_c(hipStream_t s, const ConvPlan& p, const void* in, int
         (const uint16_t*)p.res, (uint16_t*)out);
 }
 
+template <int DT, int KCH>
+static void launch_union_cin(hipStream_t s, const ConvPlan& p, const void* in, int Cout, int64_t in_rows,
+                             const void* wpack, const float* scale, const float* shift, int relu, void* out) {
+    switch (Cout) {
+        case 32: launch_union_c<DT, KCH, 2>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
+        case 64: launch_union_c<DT, KCH, 4>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
+        case 96: launch_union_c<DT, KCH, 6>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
+        case 128: launch_union_c<DT, KCH, 8>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
+    }
+}
+
 template <int DT>
-static void launch_union(hipStream_t s, const ConvPlan& p, const void* in, int C, int64_t in_rows,
+static void launch_union(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int Cout, int64_t in_rows,
                          const void* wpack, const float* scale, const float* shift, int relu, void* out) {
-    switch (C) {
-        case 32: launch_union_c<DT, 1>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
-        case 64: launch_union_c<DT, 2>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
-        case 96: launch_union_c<DT, 3>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
-        case 128: launch_union_c<DT, 4>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
+    switch (Cin) {
+        case 32: launch_union_cin<DT, 1>(s, p, in, Cout, in_rows, wpack, scale, shift, relu, out); break;
+        case 64: launch_union_cin<DT, 2>(s, p, in, Cout, in_rows, wpack, scale, shift, relu, out); break;
+        case 96: launch_union_cin<DT, 3>(s, p, in, Cout, in_rows, wpack, scale, shift, relu, out); break;
+        case 128: launch_union_cin<DT, 4>(s, p, in, Cout, in_rows, wpack, scale, shift, relu, out); break;
     }
 }
 
 void launch_conv_union(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows, int Cout,
                        const void* wpack, const float* scale, const float* shift, int relu, void* out, int dt) {
-    (void)Cout;
-    if (dt == SPV_BF16) launch_union<SPV_BF16>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out);
-    else launch_union<SPV_F16>(s, p, in, Cin, in_rows, wpack, scale, shift, relu, out);
+    if (dt == SPV_BF16) launch_union<SPV_BF16>(s, p, in, Cin, Cout, in_rows, wpack, scale, shift, relu, out);
+    else launch_union<SPV_F16>(s, p, in, Cin, Cout, in_rows, wpack, scale, shift, relu, out);
 }
 
 }  // namespace spv

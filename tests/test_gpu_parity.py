@@ -315,7 +315,10 @@ def run_conv(spv, x, off, pairs, W, m_out, dtype, scale=None, shift=None, relu=F
 
 @pytest.mark.parametrize("cin,cout,dtype,bn", [(32, 32, "bf16", False), (96, 96, "bf16", True),
                                                (96, 96, "f16", True), (16, 16, "f32", False), (4, 32, "bf16", True),
-                                               (24, 48, "bf16", False), (128, 256, "bf16", True)])
+                                               (24, 48, "bf16", False), (128, 256, "bf16", True),
+                                               (32, 64, "bf16", True), (64, 128, "f16", False),
+                                               (128, 64, "bf16", True), (96, 32, "bf16", False),
+                                               (128, 128, "bf16", True), (64, 96, "f16", True)])
 def test_conv_submanifold_sweep(spv, sweep, cin, cout, dtype, bn):
     rc, _, _, _ = oracle.voxelize(sweep[::3] if cout >= 256 else sweep, 0.05)
     _, off, pairs = oracle.kernel_map(rc)
