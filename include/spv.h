@@ -153,6 +153,30 @@ spv_status spv_sparse_conv(void* stream, void* ws, size_t ws_bytes,
                            spv_dtype dt);
 
 /*
+ * spv_sparse_conv_sliced -- spv_sparse_conv with shared, channel-sliced weights
+ * (Sec. 4.2 "Weight Sharing": a candidate layer of the super network with C_in
+ * input and C_out output channels uses the first C_in input and the first C_out
+ * output channels of the layer's full weight tensor, and its normalization the
+ * first C_out entries of the full scale / shift).
+ *   out[j] = act(scale[:Cout] * sum_{(i, j, k)} in[i] @ W[k][:Cin][:Cout] + shift[:Cout])
+ * In:  W [K3][Cin_full][Cout_full] (dt), the full tensor (not a copy of the
+ *      slice); scale/shift: the full [Cout_full] f32 vectors or NULL (only the
+ *      first Cout entries are read); every other argument as in spv_sparse_conv
+ *      (in [in_rows][Cin] and out [m_out_cap][Cout] are dense at the sliced
+ *      widths).
+ * Errors: as spv_sparse_conv, plus SPV_ERR_INVALID_ARG when Cin > Cin_full or
+ *      Cout > Cout_full.  Cin_full = Cin and Cout_full = Cout is spv_sparse_conv.
+ */
+spv_status spv_sparse_conv_sliced(void* stream, void* ws, size_t ws_bytes,
+                                  const void* in, int64_t in_rows, int32_t Cin,
+                                  const int32_t* off, const int32_t* pairs, int64_t pair_cap,
+                                  int32_t K3, int32_t transposed,
+                                  const void* W, int32_t Cin_full, int32_t Cout_full,
+                                  const float* scale, const float* shift, int32_t relu,
+                                  void* out, const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout,
+                                  spv_dtype dt);
+
+/*
  * spv_devoxelize -- sparse devoxelization (Sec. 3.3 "Sparse Devoxelization":
  * trilinear interpolation from the 8 neighbouring voxels) fused with the
  * point-branch MLP and the fusion by addition ("Point Transformation and

@@ -136,6 +136,21 @@ def sparse_conv(x, off, pairs, W, m_out, dtype="f32", scale=None, shift=None, re
     return out[:m_out]
 
 
+def sparse_conv_sliced(x, off, pairs, W_full, m_out, Cout, dtype="f32", scale=None, shift=None, relu=False,
+                       transposed=False):
+    """Weight sharing in the super network (Sec. 4.2): a layer run at C_in input and
+    Cout output channels (C_in = x's width) uses the first C_in and the first Cout
+    channels of the full weight tensor W_full [K3][Cin_full][Cout_full], and the
+    first Cout entries of the full normalization scale / shift."""
+    W_full = np.asarray(W_full)
+    Cin = np.asarray(x).shape[1]
+    if Cin > W_full.shape[1] or Cout > W_full.shape[2]:
+        raise OracleError(ERR_INVALID_ARG, "sparse_conv_sliced")
+    return sparse_conv(x, off, pairs, W_full[:, :Cin, :Cout], m_out, dtype,
+                       None if scale is None else np.asarray(scale)[:Cout],
+                       None if shift is None else np.asarray(shift)[:Cout], relu, transposed)
+
+
 def devoxelize(grid_coords, vfeat, xyz, voxel_size, stride_log2=0, mode="center", batch=None, pfeat=None,
                Wp=None, scale_p=None, shift_p=None, relu_p=False, dtype="f32", want_corners=False):
     grid_coords = np.ascontiguousarray(grid_coords, dtype=np.int32).reshape(-1, 4)

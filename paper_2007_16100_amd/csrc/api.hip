@@ -269,12 +269,15 @@ spv_status spv_kernel_map(void* stream, void* ws, size_t ws_bytes, const int32_t
     return st;
 }
 
-spv_status spv_sparse_conv(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows, int32_t Cin,
-                           const int32_t* off, const int32_t* pairs, int64_t pair_cap, int32_t K3, int32_t transposed,
-                           const void* W, const float* scale, const float* shift, int32_t relu, void* out,
-                           const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
+// Cin_full / Cout_full: W's stored shape [K3][Cin_full][Cout_full], of which the
+// leading Cin x Cout block of every offset is used
+static spv_status sparse_conv_call(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows,
+                                   int32_t Cin, const int32_t* off, const int32_t* pairs, int64_t pair_cap, int32_t K3,
+                                   int32_t transposed, const void* W, int32_t Cin_full, int32_t Cout_full,
+                                   const float* scale, const float* shift, int32_t relu, void* out,
+                                   const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
     if (!ws || in_rows < 0 || m_out_cap < 0 || m_out_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !off ||
-        !W || pair_cap < 0 || !valid_dt(dt))
+        !W || pair_cap < 0 || !valid_dt(dt) || Cin > Cin_full || Cout > Cout_full)
         return SPV_ERR_INVALID_ARG;
     if (!(K3 == 27 || K3 == 8)) return SPV_ERR_UNSUPPORTED;
     if ((in_rows > 0 && !in) || (m_out_cap > 0 && !out) || (pair_cap > 0 && !pairs)) return SPV_ERR_INVALID_ARG;
@@ -285,6 +288,8 @@ spv_status spv_sparse_conv(void* stream, void* ws, size_t ws_bytes, const void* 
     if (m_out_cap == 0) return SPV_OK;
     hipStream_t s = (hipStream_t)stream;
     L.p.m_out_dev = m_out_dev;
+    L.p.w_ldc = Cout_full;
+    L.p.w_ldk = (int64_t)Cin_full * Cout_full;
     // A transposed map gives an output few of the 27 offsets (a transposed
     // stride-2 map at most 8, 2-3 on a sweep), which the neighbour-table kernel
     // would still step through for every block: the tile kernel, which only
@@ -292,10 +297,27 @@ spv_status spv_sparse_conv(void* stream, void* ws, size_t ws_bytes, const void* 
     if (transposed) L.p.use_union = 0;
     // the plan clears the status header first and packs W in one of its launches
     launch_conv_plan(s, L.p, off, pairs, K3, transposed, pair_cap, in_rows,
-                     conv_pack_job(K3, W, L.wpack, Cin, Cout, dt), true);
+                     conv_pack_job(K3, W, L.wpack, Cin, Cout, dt, L.p.w_ldc, L.p.w_ldk), true);
     launch_conv_run(s, L.p, in, Cin, in_rows, pairs, pair_cap, transposed, W, L.wpack, scale, shift, relu, out, Cout,
                     dt);
     return hip_check();
+}
+
+spv_status spv_sparse_conv(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows, int32_t Cin,
+                           const int32_t* off, const int32_t* pairs, int64_t pair_cap, int32_t K3, int32_t transposed,
+                           const void* W, const float* scale, const float* shift, int32_t relu, void* out,
+                           const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
+    return sparse_conv_call(stream, ws, ws_bytes, in, in_rows, Cin, off, pairs, pair_cap, K3, transposed, W, Cin, Cout,
+                            scale, shift, relu, out, m_out_dev, m_out_cap, Cout, dt);
+}
+
+spv_status spv_sparse_conv_sliced(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows,
+                                  int32_t Cin, const int32_t* off, const int32_t* pairs, int64_t pair_cap, int32_t K3,
+                                  int32_t transposed, const void* W, int32_t Cin_full, int32_t Cout_full,
+                                  const float* scale, const float* shift, int32_t relu, void* out,
+                                  const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
+    return sparse_conv_call(stream, ws, ws_bytes, in, in_rows, Cin, off, pairs, pair_cap, K3, transposed, W, Cin_full,
+                            Cout_full, scale, shift, relu, out, m_out_dev, m_out_cap, Cout, dt);
 }
 
 spv_status spv_devoxelize(void* stream, void* ws, size_t ws_bytes, const int32_t* grid_coords, const int64_t* m_dev,

@@ -64,7 +64,9 @@ __device__ inline int64_t tile_of(int64_t j, int64_t m, int64_t nt, int T) {
 }
 
 // fragment t of the packing (t = ((k * KCH + kc) * NB + nb) * 64 + lane)
-__device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int Cout, int KCH, int NB, int64_t t) {
+// W[k][c][col] sits at W[k * ldk + c * ldc + col] (ldc = Cout, ldk = Cin * Cout
+// for a dense [K3][Cin][Cout] tensor; larger for a channel slice of a wider one)
+__device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int ldc, int64_t ldk, int KCH, int NB, int64_t t) {
     const int lane = (int)(t & 63);
     int64_t f = t >> 6;
     const int nb = (int)(f % NB);
@@ -77,8 +79,8 @@ __device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int Cout, int 
     for (int e = 0; e < 4; ++e) {
         uint32_t lo = 0, hi = 0;
         const int c0 = ci0 + 2 * e, c1 = ci0 + 2 * e + 1;
-        if (c0 < Cin) lo = W[((int64_t)k * Cin + c0) * Cout + col];
-        if (c1 < Cin) hi = W[((int64_t)k * Cin + c1) * Cout + col];
+        if (c0 < Cin) lo = W[(int64_t)k * ldk + (int64_t)c0 * ldc + col];
+        if (c1 < Cin) hi = W[(int64_t)k * ldk + (int64_t)c1 * ldc + col];
         w[e] = lo | (hi << 16);
     }
     return make_uint4(w[0], w[1], w[2], w[3]);
@@ -87,7 +89,7 @@ __device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int Cout, int 
 // a weight packing run alongside another kernel's work (grid-stride)
 __device__ inline void pack_job_run(const PackJob& q) {
     for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < q.total; t += (int64_t)gridDim.x * blockDim.x)
-        q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.KCH, q.NB, t);
+        q.wpack[t] = pack_fragment(q.W, q.Cin, q.ldc, q.ldk, q.KCH, q.NB, t);
 }
 
 // For every offset k and tile t in [0, nt]: bnd[k][t] = first pair of offset k
@@ -202,12 +204,6 @@ void launch_conv_plan(hipStream_t s, const ConvPlan& p, const int32_t* off, cons
 // i.e. lane l carries output channel nb*16 + l%16 and 8 consecutive input
 // channels: the A operand of D = W^T G^T (or the B operand of D = G W).
 // ---------------------------------------------------------------------------
-__global__ void k_pack_w(const uint16_t* W, int K3, int Cin, int Cout, int KCH, int NB, uint4* wpack) {
-    const int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    if (t >= (int64_t)K3 * KCH * NB * 64) return;
-    wpack[t] = pack_fragment(W, Cin, Cout, KCH, NB, t);
-}
-
 struct PrologueArgs {
     Header* h;
     uint64_t* keys;
@@ -228,7 +224,8 @@ __global__ __launch_bounds__(256) void k_block_prologue(PrologueArgs a) {
     for (int64_t i = t0; i < (int64_t)a.nslots; i += stride) a.keys[i] = kEmpty;
     for (int j = 0; j < a.njobs; ++j) {
         const PackJob& q = a.job[j];
-        for (int64_t t = t0; t < q.total; t += stride) q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.KCH, q.NB, t);
+        for (int64_t t = t0; t < q.total; t += stride)
+            q.wpack[t] = pack_fragment(q.W, q.Cin, q.ldc, q.ldk, q.KCH, q.NB, t);
     }
 }
 
@@ -540,6 +537,7 @@ __global__ __launch_bounds__(256) void k_conv_tile_valu(ConvPlan p, const void* 
     __syncthreads();
     const int isel = transposed ? 1 : 0;
     const int64_t bs = p.ntile_cap + 1;
+    const int64_t ldc = p.w_ldc > 0 ? p.w_ldc : Cout, ldk = p.w_ldk > 0 ? p.w_ldk : (int64_t)Cin * Cout;
     for (int k = 0; k < K3; ++k) {
         int64_t lo = p.bnd[k * bs + t], hi = p.bnd[k * bs + t + 1];
         lo = lo < 0 ? 0 : (lo > pair_bound ? pair_bound : lo);
@@ -550,7 +548,7 @@ __global__ __launch_bounds__(256) void k_conv_tile_valu(ConvPlan p, const void* 
             if (!cok || o < 0 || o >= rows || i < 0 || i >= in_rows) continue;
             float s = 0.f;
             for (int ci = 0; ci < Cin; ++ci)
-                s += ld_feat<DT>(in, (int64_t)i * Cin + ci) * ld_feat<DT>(W, ((int64_t)k * Cin + ci) * Cout + col);
+                s += ld_feat<DT>(in, (int64_t)i * Cin + ci) * ld_feat<DT>(W, k * ldk + ci * ldc + col);
             acc[o * 64 + cl] += s;
         }
         __syncthreads();
@@ -661,15 +659,9 @@ static void launch_tile(hipStream_t s, const ConvPlan& p, const void* in, int Ci
     }
 }
 
-void launch_conv_pack(hipStream_t s, int K3, const void* W, void* wpack, int Cin, int Cout, int dt) {
-    if (!conv_mfma_supported(Cin, Cout, dt)) return;
-    int KCH = conv_kch(Cin), NB = Cout / 16;
-    int64_t tot = (int64_t)K3 * KCH * NB * 64;
-    k_pack_w<<<blocks_for(tot, 256), 256, 0, s>>>((const uint16_t*)W, K3, Cin, Cout, KCH, NB, (uint4*)wpack);
-}
-
-PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int dt) {
-    PackJob q{(const uint16_t*)W, (uint4*)wpack, K3, Cin, Cout, 0, 0, 0};
+PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int dt, int ldc, int64_t ldk) {
+    PackJob q{(const uint16_t*)W, (uint4*)wpack, K3, Cin, Cout, 0, 0, 0, ldc > 0 ? ldc : Cout,
+              ldk > 0 ? ldk : (int64_t)Cin * Cout};
     if (!conv_mfma_supported(Cin, Cout, dt)) return q;
     q.KCH = conv_kch(Cin);
     q.NB = Cout / 16;

@@ -207,6 +207,10 @@ struct ConvPlan {
     // residual input [m][Cout] of the storage type (nullptr = none), added after
     // scale and shift and before the activation; it must not alias the output
     const void* res = nullptr;
+    // W strides in elements for the vector-ALU kernel, which reads W itself
+    // (0: a dense [K3][Cin][Cout] tensor)
+    int w_ldc = 0;
+    int64_t w_ldk = 0;
 };
 void plan_conv_ws(Arena& a, ConvPlan& p, int64_t m_out_cap, int K3, int Cin, int Cout, int dt);
 struct PackJob;
@@ -218,17 +222,19 @@ void launch_conv_plan(hipStream_t s, const ConvPlan& p, const int32_t* off, cons
                       bool clear_header = false);
 bool conv_mfma_supported(int Cin, int Cout, int dt);
 void* plan_wpack_ws(Arena& a, int K3, int Cin, int Cout);
-// pack W [K3][Cin][Cout] into MFMA operand fragments (no-op when the vector-ALU path runs)
-void launch_conv_pack(hipStream_t s, int K3, const void* W, void* wpack, int Cin, int Cout, int dt);
 // One weight packing into MFMA operand fragments, as a job for the block prologue
 // (total = 0: nothing to pack, the layer runs on a kernel that reads W itself).
 struct PackJob {
-    const uint16_t* W;  // [K3][Cin][Cout]
+    const uint16_t* W;  // W[k][c][col] at W[k * ldk + c * ldc + col]
     uint4* wpack;
     int K3, Cin, Cout, KCH, NB;
     int64_t total;      // fragments * 64 lanes
+    int ldc;            // elements between input channels (Cout when dense)
+    int64_t ldk;        // elements between offsets (Cin * Cout when dense)
 };
-PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int dt);
+// ldc / ldk <= 0: W is a dense [K3][Cin][Cout] tensor; otherwise the leading
+// Cin x Cout block of each offset of a wider tensor (a channel slice)
+PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int dt, int ldc = 0, int64_t ldk = 0);
 // The first kernel of a block call: clears the voxel table and the status
 // header, and packs up to kMaxPackJobs weights, in one grid-stride launch.
 constexpr int kMaxPackJobs = 3;

@@ -29,7 +29,8 @@ SPV_DEVOX_CENTER, SPV_DEVOX_CORNER, SPV_DEVOX_NEAREST = 0, 1, 2
 _DT = {torch.float32: SPV_F32, torch.bfloat16: SPV_BF16, torch.float16: SPV_F16}
 
 # every symbol include/spv.h declares
-EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_devoxelize",
+EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced",
+           "spv_devoxelize",
            "spv_block_workspace_bytes", "spv_block", "spv_lookup", "spv_status_check", "spv_status_string",
            "spv_last_hip_error")
 
@@ -69,6 +70,8 @@ def lib():
         L.spv_kernel_map.argtypes = [vp, vp, sz, vp, vp, i64, i32, i32, vp, vp, vp, vp, i64, vp]
         L.spv_sparse_conv.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i64, i32, i32, vp, vp, vp, i32, vp, vp, i64,
                                       i32, i32]
+        L.spv_sparse_conv_sliced.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i64, i32, i32, vp, i32, i32, vp, vp,
+                                             i32, vp, vp, i64, i32, i32]
         L.spv_devoxelize.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, vp, i64, f32, i32, vp, i32, vp, i32, vp, vp,
                                      vp, i32, vp, i32, vp, vp]
         L.spv_block.argtypes = [vp, vp, sz, ct.POINTER(BlockParams), vp, vp, i64, vp, vp, vp]
@@ -77,8 +80,8 @@ def lib():
         L.spv_status_string.argtypes = [i32]
         L.spv_status_string.restype = ct.c_char_p
         L.spv_last_hip_error.argtypes = []
-        for f in ("spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_devoxelize", "spv_block", "spv_lookup",
-                  "spv_status_check"):
+        for f in ("spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced", "spv_devoxelize",
+                  "spv_block", "spv_lookup", "spv_status_check"):
             getattr(L, f).restype = ct.c_int
         _lib = L
     return _lib
@@ -208,6 +211,26 @@ def spv_sparse_conv(ws: Workspace, x: torch.Tensor, off: torch.Tensor, pairs: to
                                pairs.shape[0], K3, int(transposed), _ptr(W), _ptr(scale), _ptr(shift), int(relu),
                                _ptr(out), _ptr(m_out_dev), m_out_cap, Cout, _DT[x.dtype])
     _chk(st, "spv_sparse_conv")
+    return out
+
+
+def spv_sparse_conv_sliced(ws: Workspace, x: torch.Tensor, off: torch.Tensor, pairs: torch.Tensor,
+                           W_full: torch.Tensor, Cin: int, Cout: int, m_out_cap: int,
+                           m_out_dev: Optional[torch.Tensor] = None, scale: Optional[torch.Tensor] = None,
+                           shift: Optional[torch.Tensor] = None, relu: bool = False, transposed: bool = False,
+                           out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The conv with the first Cin x Cout channels of the full weight W_full [K3][Cin_full][Cout_full]
+    (and the first Cout entries of the full scale / shift)."""
+    K3, Cin_full, Cout_full = W_full.shape
+    if x.shape[1] != Cin:
+        raise ValueError(f"x has {x.shape[1]} channels, the slice takes {Cin}")
+    if out is None:
+        out = torch.empty((max(m_out_cap, 1), Cout), dtype=x.dtype, device=x.device)
+    st = lib().spv_sparse_conv_sliced(_stream(), ws.ptr, ws.nbytes, _ptr(x), x.shape[0], Cin, _ptr(off), _ptr(pairs),
+                                      pairs.shape[0], K3, int(transposed), _ptr(W_full), Cin_full, Cout_full,
+                                      _ptr(scale), _ptr(shift), int(relu), _ptr(out), _ptr(m_out_dev), m_out_cap, Cout,
+                                      _DT[x.dtype])
+    _chk(st, "spv_sparse_conv_sliced")
     return out
 
 

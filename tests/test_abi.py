@@ -57,6 +57,13 @@ def test_host_side_validation_without_gpu():
     st = L.spv_sparse_conv(None, ws, 1 << 30, ct.c_void_p(16), 4, 8, ct.c_void_p(16), ct.c_void_p(16), 4, 27, 0,
                            ct.c_void_p(16), None, None, 0, ct.c_void_p(16), None, 4, 16, 7)
     assert st == spv.SPV_ERR_INVALID_ARG
+    # a weight slice wider than the stored tensor
+    st = L.spv_sparse_conv_sliced(None, ws, 1 << 30, ct.c_void_p(16), 4, 64, ct.c_void_p(16), ct.c_void_p(16), 4, 27,
+                                  0, ct.c_void_p(16), 32, 64, None, None, 0, ct.c_void_p(16), None, 4, 32, 1)
+    assert st == spv.SPV_ERR_INVALID_ARG
+    st = L.spv_sparse_conv_sliced(None, ws, 1 << 30, ct.c_void_p(16), 4, 32, ct.c_void_p(16), ct.c_void_p(16), 4, 27,
+                                  0, ct.c_void_p(16), 32, 32, None, None, 0, ct.c_void_p(16), None, 4, 48, 1)
+    assert st == spv.SPV_ERR_INVALID_ARG
     # misaligned feature pointer
     st = L.spv_sparse_conv(None, ws, 1 << 30, ct.c_void_p(18), 4, 8, ct.c_void_p(16), ct.c_void_p(16), 4, 27, 0,
                            ct.c_void_p(16), None, None, 0, ct.c_void_p(16), None, 4, 16, 1)

@@ -362,6 +362,52 @@ def test_conv_k3_stride2_and_transposed_sweep(spv, sweep, cin, cout, dtype):
     check_close(gotT, refT, dtype)
 
 
+@pytest.mark.parametrize("K,full,cin,cout,dtype,transposed", [
+    (3, (128, 128), 96, 64, "bf16", False),   # neighbour-table kernel
+    (3, (128, 128), 64, 96, "f16", False),
+    (3, (128, 128), 32, 32, "bf16", False),
+    (3, (128, 128), 48, 80, "bf16", False),   # tile kernel (80 outputs)
+    (3, (40, 24), 16, 24, "f32", False),      # vector ALU
+    (2, (128, 128), 64, 96, "bf16", False),   # stride-2 tile kernel
+    (2, (128, 96), 96, 48, "bf16", True),     # transposed
+])
+def test_conv_sliced_weights(spv, sweep, K, full, cin, cout, dtype, transposed):
+    """Channel-sliced weight sharing (Sec. 4.2): a (cin, cout) candidate reads the first
+    channels of the full weight tensor and BN vectors in place."""
+    rc, _, _, _ = oracle.voxelize(sweep, 0.05)
+    if K == 3:
+        _, off, pairs = oracle.kernel_map(rc)
+        m_in = m_out = len(rc)
+    else:
+        oc, off, pairs = oracle.kernel_map(rc, 2, 2)
+        m_in, m_out = (len(oc), len(rc)) if transposed else (len(rc), len(oc))
+    Wf = synth.conv_weight(K ** 3, full[0], full[1], 1030, dtype)
+    sc, sh = synth.folded_bn(full[1], 1031)
+    x = synth.normal((m_in, cin), 1032, dtype=dtype)
+    ws = spv.Workspace.for_ops(max(m_in, m_out), 128)
+    got = spv.spv_sparse_conv_sliced(ws, dev(x, dtype), dev(off), dev(pairs), dev(Wf, dtype), cin, cout, m_out,
+                                     scale=dev(sc), shift=dev(sh), relu=True, transposed=transposed)
+    got = host(got, dtype)[:m_out]
+    ref = oracle.sparse_conv_sliced(x, off, pairs, Wf, m_out, cout, dtype, sc, sh, True, transposed)
+    check_close(got, ref, dtype)
+    # the same layer from a dense copy of the slice, through spv_sparse_conv: identical bits
+    Ws = np.ascontiguousarray(Wf[:, :cin, :cout])
+    dense = spv.spv_sparse_conv(ws, dev(x, dtype), dev(off), dev(pairs), dev(Ws, dtype), m_out,
+                                scale=dev(np.ascontiguousarray(sc[:cout])), shift=dev(np.ascontiguousarray(sh[:cout])),
+                                relu=True, transposed=transposed)
+    np.testing.assert_array_equal(got, host(dense, dtype)[:m_out])
+
+
+def test_conv_sliced_rejects_wider_slice(spv):
+    ws = spv.Workspace.for_ops(16, 32)
+    c = np.array([[0, 0, 0, 0], [0, 0, 0, 1]], np.int32)
+    _, off, pairs = oracle.kernel_map(c)
+    Wf = np.zeros((27, 32, 32), np.float32)
+    with pytest.raises(spv.SpvError) as e:
+        spv.spv_sparse_conv_sliced(ws, dev(np.zeros((2, 32), np.float32)), dev(off), dev(pairs), dev(Wf), 32, 48, 2)
+    assert e.value.status == spv.SPV_ERR_INVALID_ARG
+
+
 @pytest.mark.parametrize("K,cin,cout,dtype", [(3, 32, 32, "bf16"), (3, 16, 16, "f32"), (2, 64, 128, "bf16")])
 @pytest.mark.parametrize("defect", ["none", "swapped", "repeated"])
 def test_conv_rejects_malformed_map(spv, K, cin, cout, dtype, defect):

@@ -226,3 +226,33 @@ def test_conv_k3_stride2_dense(oracle_lib):
     o = oc[:, 1:] + sh // 2
     ref = y[:, o[:, 0], o[:, 1], o[:, 2]].T
     np.testing.assert_allclose(got, ref, rtol=1e-5, atol=1e-5)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("cin,cout,transposed", [(5, 3, False), (8, 8, False), (2, 7, True), (1, 1, False)])
+def test_conv_sliced_equals_zero_padded_full(oracle_lib, dtype, cin, cout, transposed):
+    """Weight sharing (Sec. 4.2): a layer at (cin, cout) of a (8, 8) super-layer equals
+    the full layer run on inputs zero-padded to 8 channels, read at its first cout
+    outputs -- bit for bit, since the padded terms add exact zeros before the one
+    rounding.  A slice taken from the wrong end or with a wrong stride fails this."""
+    rng = np.random.default_rng(71)
+    c = _rand_coords(rng, 250, 4)
+    if transposed:
+        oc, off, pairs = oracle_lib.kernel_map(c, 2, 2)
+        m_in, m_out, K3 = len(oc), len(c), 8
+    else:
+        _, off, pairs = oracle_lib.kernel_map(c)
+        m_in, m_out, K3 = len(c), len(c), 27
+    Wf = synth.conv_weight(K3, 8, 8, 72, dtype)
+    sc, sh = synth.folded_bn(8, 73)
+    x = synth.normal((m_in, cin), 74, dtype=dtype)
+    xpad = np.zeros((m_in, 8), x.dtype)
+    xpad[:, :cin] = x
+    got = oracle_lib.sparse_conv_sliced(x, off, pairs, Wf, m_out, cout, dtype, sc, sh, True, transposed)
+    full = oracle_lib.sparse_conv(xpad, off, pairs, Wf, m_out, dtype, sc, sh, True, transposed)
+    np.testing.assert_array_equal(got, full[:, :cout])
+    # the largest candidate is the full layer
+    np.testing.assert_array_equal(
+        oracle_lib.sparse_conv_sliced(xpad, off, pairs, Wf, m_out, 8, dtype, sc, sh, True, transposed), full)
+    with pytest.raises(oracle_lib.OracleError):
+        oracle_lib.sparse_conv_sliced(x, off, pairs, Wf, m_out, 9, dtype)
