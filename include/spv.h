@@ -159,22 +159,59 @@ spv_status spv_sparse_conv(void* stream, void* ws, size_t ws_bytes,
  * output channels of the layer's full weight tensor, and its normalization the
  * first C_out entries of the full scale / shift).
  *   out[j] = act(scale[:Cout] * sum_{(i, j, k)} in[i] @ W[k][:Cin][:Cout] + shift[:Cout])
+ * With res non-NULL the layer also adds a residual input before the activation:
+ *   out[j] = act(scale * conv + shift + res[j])
+ * (the second conv of a residual block adds its shortcut, Sec. 3.3; a conv
+ * over concatenated inputs [a; b] is W_a a + W_b b: the conv of b takes the
+ * conv of a, scaled and unshifted, as res).
  * In:  W [K3][Cin_full][Cout_full] (dt), the full tensor (not a copy of the
- *      slice); scale/shift: the full [Cout_full] f32 vectors or NULL (only the
- *      first Cout entries are read); every other argument as in spv_sparse_conv
- *      (in [in_rows][Cin] and out [m_out_cap][Cout] are dense at the sliced
- *      widths).
- * Errors: as spv_sparse_conv, plus SPV_ERR_INVALID_ARG when Cin > Cin_full or
- *      Cout > Cout_full.  Cin_full = Cin and Cout_full = Cout is spv_sparse_conv.
+ *      slice; 16-byte aligned).  W may also point at input-channel row r0 of
+ *      the full tensor (W_full + r0 * Cout_full; Cin_full still the full count,
+ *      which sets the stride between offsets): the slice is then input channels
+ *      r0 .. r0 + Cin - 1, and the caller guarantees r0 + Cin <= Cin_full;
+ *      scale/shift: the full [Cout_full] f32 vectors or NULL (only the first
+ *      Cout entries are read); res [m_out_cap][Cout] (dt, 16-byte aligned, not
+ *      the output) or NULL; every other argument as in spv_sparse_conv (in
+ *      [in_rows][Cin] and out [m_out_cap][Cout] are dense at the sliced widths).
+ * Errors: as spv_sparse_conv, plus SPV_ERR_INVALID_ARG when Cin > Cin_full,
+ *      Cout > Cout_full or res aliases out.  Cin_full = Cin, Cout_full = Cout
+ *      and res = NULL is spv_sparse_conv.
  */
 spv_status spv_sparse_conv_sliced(void* stream, void* ws, size_t ws_bytes,
                                   const void* in, int64_t in_rows, int32_t Cin,
                                   const int32_t* off, const int32_t* pairs, int64_t pair_cap,
                                   int32_t K3, int32_t transposed,
                                   const void* W, int32_t Cin_full, int32_t Cout_full,
-                                  const float* scale, const float* shift, int32_t relu,
+                                  const float* scale, const float* shift, const void* res, int32_t relu,
                                   void* out, const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout,
                                   spv_dtype dt);
+
+/*
+ * spv_linear -- a pointwise linear layer on feature rows:
+ *   res_after_act = 0:  out[i] = act(scale * (in[i] @ W) + shift + res[i])
+ *   res_after_act = 1:  out[i] = act(scale * (in[i] @ W) + shift) + res[i]
+ * The point branch's MLP with the fusion by addition (Sec. 3.3 "Point
+ * Transformation and Feature Fusion": res = the devoxelized voxel features, added
+ * after the activation); the 1x1 shortcut of a residual block; a classifier
+ * (scale NULL, shift = bias, no activation).  fp32 accumulation, one rounding.
+ * In:  in [m_cap][Cin] (dt, 16-byte aligned); m_dev: device row count (NULL =
+ *      m_cap); W [Cin_full][Cout_full] (dt) of which the leading Cin x Cout block
+ *      is used (channel slicing as in spv_sparse_conv_sliced; W may point at a
+ *      later row of a wider tensor); scale/shift f32 [>= Cout] or NULL;
+ *      res [m_cap][Cout] (dt, 16-byte aligned, not the output) or NULL.
+ * Out: out [m_cap][Cout] (dt, 16-byte aligned, not the input); rows < *m_dev.
+ * bf16/f16 with Cin % 8 == 0, ceil(Cin / 32) in {1, 2, 3, 4, 8} and Cout in
+ * {16, 32, 64, 96, 128, 256} run on MFMA; other shapes and f32 on a vector-ALU
+ * kernel.  The workspace from spv_workspace_bytes(., max(Cin, Cout)) suffices.
+ * Errors: SPV_ERR_INVALID_ARG (sizes, Cin > Cin_full, Cout > Cout_full, null or
+ *      misaligned pointers, aliasing), SPV_ERR_CAPACITY (ws too small).
+ */
+spv_status spv_linear(void* stream, void* ws, size_t ws_bytes,
+                      const void* in, const int64_t* m_dev, int64_t m_cap, int32_t Cin,
+                      const void* W, int32_t Cin_full, int32_t Cout_full,
+                      const float* scale, const float* shift, int32_t relu,
+                      const void* res, int32_t res_after_act,
+                      void* out, int32_t Cout, spv_dtype dt);
 
 /*
  * spv_devoxelize -- sparse devoxelization (Sec. 3.3 "Sparse Devoxelization":

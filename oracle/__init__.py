@@ -52,11 +52,12 @@ def lib():
         L.spvo_devoxelize.argtypes = [vp, i64, i32, vp, vp, i64, f32, i32, vp, i32, vp, i32, vp, vp, vp, i32,
                                       vp, i32, vp, vp]
         L.spvo_block.argtypes = [vp, vp, vp, i64, vp, vp, vp]
+        L.spvo_linear.argtypes = [vp, i64, i32, vp, vp, vp, vp, i32, i32, vp, i32, i32]
         L.spvo_decode.argtypes = [vp, i64, i32]
         L.spvo_decode.restype = ct.c_double
         L.spvo_round_store.argtypes = [ct.c_double, vp, i64, i32]
         for f in ("spvo_voxelize", "spvo_kernel_map", "spvo_sparse_conv", "spvo_sparse_conv_res", "spvo_devoxelize",
-                  "spvo_block"):
+                  "spvo_block", "spvo_linear"):
             getattr(L, f).restype = ct.c_int
         _lib = L
     return _lib
@@ -149,6 +150,25 @@ def sparse_conv_sliced(x, off, pairs, W_full, m_out, Cout, dtype="f32", scale=No
     return sparse_conv(x, off, pairs, W_full[:, :Cin, :Cout], m_out, dtype,
                        None if scale is None else np.asarray(scale)[:Cout],
                        None if shift is None else np.asarray(shift)[:Cout], relu, transposed)
+
+
+def linear(x, W, dtype="f32", scale=None, shift=None, relu=False, res=None, res_after_act=False):
+    """Pointwise linear layer (the point MLP of Sec. 3.3, a 1x1 shortcut, a classifier):
+    act(scale * (x @ W) + shift + res), or act(...) + res with res_after_act."""
+    x = np.ascontiguousarray(x, dtype=_sdt(dtype))
+    W = np.ascontiguousarray(W, dtype=_sdt(dtype))
+    m, Cin = x.shape
+    Cout = W.shape[1]
+    if W.shape[0] != Cin:
+        raise OracleError(ERR_INVALID_ARG, "linear")
+    scale = None if scale is None else np.ascontiguousarray(scale, dtype=np.float32)
+    shift = None if shift is None else np.ascontiguousarray(shift, dtype=np.float32)
+    res = None if res is None else np.ascontiguousarray(res, dtype=_sdt(dtype)).reshape(m, Cout)
+    out = np.zeros((max(m, 1), Cout), _sdt(dtype))
+    st = lib().spvo_linear(_p(x), m, Cin, _p(W), _p(scale), _p(shift), _p(res), int(res_after_act), int(relu), _p(out),
+                           Cout, DT[dtype])
+    _chk(st, "linear")
+    return out[:m]
 
 
 def devoxelize(grid_coords, vfeat, xyz, voxel_size, stride_log2=0, mode="center", batch=None, pfeat=None,

@@ -404,6 +404,48 @@ int spvo_sparse_conv(const void* in, int64_t m_in, int32_t Cin,
 }
 
 /* ------------------------------------------------------------------------- */
+/* pointwise linear layer                                                     */
+/* ------------------------------------------------------------------------- */
+
+/* out[i] = act(scale * (in[i] @ W) + shift [+ res[i]]) [+ res[i]]: the point
+ * branch's MLP (Sec. 3.3 "Point Transformation and Feature Fusion": linear, then
+ * normalization and activation, then fusion by addition -- res after act), a 1x1
+ * shortcut of a residual block (res before act), or a classifier (shift = bias). */
+int spvo_linear(const void* in, int64_t m, int32_t Cin, const void* W, const float* scale, const float* shift,
+                const void* res, int32_t res_after_act, int32_t relu, void* out, int32_t Cout, int32_t dtype) {
+    if (m < 0 || Cin <= 0 || Cout <= 0 || !W || !valid_dtype(dtype)) return SPVO_ERR_INVALID_ARG;
+    if (m > 0 && (!in || !out)) return SPVO_ERR_INVALID_ARG;
+    double* w = (double*)malloc((size_t)Cin * Cout * sizeof(double));
+    double* acc = (double*)malloc((size_t)Cout * sizeof(double));
+    if (!w || !acc) {
+        free(w);
+        free(acc);
+        return SPVO_ERR_CAPACITY;
+    }
+    for (int64_t t = 0; t < (int64_t)Cin * Cout; ++t) w[t] = spvo_decode(W, t, dtype);
+    for (int64_t i = 0; i < m; ++i) {
+        for (int32_t co = 0; co < Cout; ++co) acc[co] = 0.0;
+        for (int32_t ci = 0; ci < Cin; ++ci) {
+            const double x = spvo_decode(in, i * Cin + ci, dtype);
+            for (int32_t co = 0; co < Cout; ++co) acc[co] += x * w[(int64_t)ci * Cout + co];
+        }
+        for (int32_t co = 0; co < Cout; ++co) {
+            double y = acc[co];
+            if (scale) y *= (double)scale[co];
+            if (shift) y += (double)shift[co];
+            const double r = res ? spvo_decode(res, i * Cout + co, dtype) : 0.0;
+            if (!res_after_act) y += r;
+            if (relu && y < 0.0) y = 0.0;
+            if (res_after_act) y += r;
+            spvo_round_store(y, out, i * Cout + co, dtype);
+        }
+    }
+    free(w);
+    free(acc);
+    return SPVO_OK;
+}
+
+/* ------------------------------------------------------------------------- */
 /* devoxelize (trilinear over 8 neighbour voxels) + point MLP + add           */
 /* ------------------------------------------------------------------------- */
 

@@ -79,6 +79,12 @@ int spvo_sparse_conv_res(const void* in, int64_t m_in, int32_t Cin,
                          const void* W, const float* scale, const float* shift, const void* res, int32_t relu,
                          void* out, int64_t m_out, int32_t Cout, int32_t dtype);
 
+/* Pointwise linear layer: out[i] = act(scale * (in[i] @ W) + shift + res[i]) with
+ * res_after_act = 0, act(scale * (in[i] @ W) + shift) + res[i] with 1.  W is
+ * [Cin][Cout] (storage dtype); scale/shift f32 [Cout] or NULL; res [m][Cout] or NULL. */
+int spvo_linear(const void* in, int64_t m, int32_t Cin, const void* W, const float* scale, const float* shift,
+                const void* res, int32_t res_after_act, int32_t relu, void* out, int32_t Cout, int32_t dtype);
+
 /* Devoxelize from a grid of voxel size voxel_size * 2^stride_log2 (coords in
  * that grid's units), optionally add the point MLP act(scale*(pfeat @ Wp)+shift).
  * corner_idx [n][8] / corner_w [n][8] (optional) receive the corner voxel index

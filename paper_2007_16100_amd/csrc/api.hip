@@ -84,6 +84,12 @@ size_t layout_conv(void* ws, size_t bytes, int64_t m_out_cap, int K3, int Cin, i
     return a.used;
 }
 
+size_t layout_linear(void* ws, size_t bytes, int Cin, int Cout, void** wpack) {
+    Arena a(ws, bytes);
+    *wpack = plan_linear_ws(a, Cin, Cout);
+    return a.used;
+}
+
 struct DevoxLayout {
     Header* h;
     Table t;
@@ -173,6 +179,8 @@ size_t spv_workspace_bytes(int64_t max_points, int32_t max_C) {
     s = std::max(s, layout_kmap(nullptr, 0, max_points, 2, 2, m));
     s = std::max(s, layout_kmap(nullptr, 0, max_points, 3, 2, m));
     s = std::max(s, layout_conv(nullptr, 0, max_points, 27, max_C, max_C, SPV_BF16, c));
+    void* wl = nullptr;
+    s = std::max(s, layout_linear(nullptr, 0, max_C, max_C, &wl));
     s = std::max(s, layout_devox(nullptr, 0, max_points, max_points, max_C, max_C, d));
     return s;
 }
@@ -274,20 +282,22 @@ spv_status spv_kernel_map(void* stream, void* ws, size_t ws_bytes, const int32_t
 static spv_status sparse_conv_call(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows,
                                    int32_t Cin, const int32_t* off, const int32_t* pairs, int64_t pair_cap, int32_t K3,
                                    int32_t transposed, const void* W, int32_t Cin_full, int32_t Cout_full,
-                                   const float* scale, const float* shift, int32_t relu, void* out,
+                                   const float* scale, const float* shift, const void* res, int32_t relu, void* out,
                                    const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
     if (!ws || in_rows < 0 || m_out_cap < 0 || m_out_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !off ||
         !W || pair_cap < 0 || !valid_dt(dt) || Cin > Cin_full || Cout > Cout_full)
         return SPV_ERR_INVALID_ARG;
     if (!(K3 == 27 || K3 == 8)) return SPV_ERR_UNSUPPORTED;
     if ((in_rows > 0 && !in) || (m_out_cap > 0 && !out) || (pair_cap > 0 && !pairs)) return SPV_ERR_INVALID_ARG;
-    if (!aligned16(in) || !aligned16(out) || !aligned16(W)) return SPV_ERR_INVALID_ARG;
+    if (!aligned16(in) || !aligned16(out) || !aligned16(W) || !aligned16(res) || (res && res == out))
+        return SPV_ERR_INVALID_ARG;
     ConvLayout L;
     if (need(layout_conv(nullptr, 0, m_out_cap, K3, Cin, Cout, dt, L), ws_bytes)) return SPV_ERR_CAPACITY;
     layout_conv(ws, ws_bytes, m_out_cap, K3, Cin, Cout, dt, L);
     if (m_out_cap == 0) return SPV_OK;
     hipStream_t s = (hipStream_t)stream;
     L.p.m_out_dev = m_out_dev;
+    L.p.res = res;
     L.p.w_ldc = Cout_full;
     L.p.w_ldk = (int64_t)Cin_full * Cout_full;
     // A transposed map gives an output few of the 27 offsets (a transposed
@@ -308,16 +318,36 @@ spv_status spv_sparse_conv(void* stream, void* ws, size_t ws_bytes, const void* 
                            const void* W, const float* scale, const float* shift, int32_t relu, void* out,
                            const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
     return sparse_conv_call(stream, ws, ws_bytes, in, in_rows, Cin, off, pairs, pair_cap, K3, transposed, W, Cin, Cout,
-                            scale, shift, relu, out, m_out_dev, m_out_cap, Cout, dt);
+                            scale, shift, nullptr, relu, out, m_out_dev, m_out_cap, Cout, dt);
 }
 
 spv_status spv_sparse_conv_sliced(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows,
                                   int32_t Cin, const int32_t* off, const int32_t* pairs, int64_t pair_cap, int32_t K3,
                                   int32_t transposed, const void* W, int32_t Cin_full, int32_t Cout_full,
-                                  const float* scale, const float* shift, int32_t relu, void* out,
+                                  const float* scale, const float* shift, const void* res, int32_t relu, void* out,
                                   const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
     return sparse_conv_call(stream, ws, ws_bytes, in, in_rows, Cin, off, pairs, pair_cap, K3, transposed, W, Cin_full,
-                            Cout_full, scale, shift, relu, out, m_out_dev, m_out_cap, Cout, dt);
+                            Cout_full, scale, shift, res, relu, out, m_out_dev, m_out_cap, Cout, dt);
+}
+
+spv_status spv_linear(void* stream, void* ws, size_t ws_bytes, const void* in, const int64_t* m_dev, int64_t m_cap,
+                      int32_t Cin, const void* W, int32_t Cin_full, int32_t Cout_full, const float* scale,
+                      const float* shift, int32_t relu, const void* res, int32_t res_after_act, void* out,
+                      int32_t Cout, spv_dtype dt) {
+    if (!ws || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !W || !valid_dt(dt) ||
+        Cin > Cin_full || Cout > Cout_full)
+        return SPV_ERR_INVALID_ARG;
+    if (m_cap > 0 && (!in || !out)) return SPV_ERR_INVALID_ARG;
+    if (!aligned16(in) || !aligned16(out) || !aligned16(res) || (res && res == out) || in == out)
+        return SPV_ERR_INVALID_ARG;
+    void* wpack = nullptr;
+    if (need(layout_linear(nullptr, 0, Cin, Cout, &wpack), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_linear(ws, ws_bytes, Cin, Cout, &wpack);
+    if (m_cap == 0) return SPV_OK;
+    LinearArgs a{in, m_dev, m_cap, Cin, Cout, (int)dt, W, Cout_full, scale, shift, relu, res, res_after_act ? 1 : 0,
+                 out};
+    launch_linear((hipStream_t)stream, a, wpack);
+    return hip_check();
 }
 
 spv_status spv_devoxelize(void* stream, void* ws, size_t ws_bytes, const int32_t* grid_coords, const int64_t* m_dev,

@@ -204,6 +204,15 @@ void launch_conv_plan(hipStream_t s, const ConvPlan& p, const int32_t* off, cons
 // i.e. lane l carries output channel nb*16 + l%16 and 8 consecutive input
 // channels: the A operand of D = W^T G^T (or the B operand of D = G W).
 // ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_pack_job(PackJob q) { pack_job_run(q); }
+
+void launch_pack_job(hipStream_t s, const PackJob& q) {
+    if (q.total <= 0) return;
+    int64_t g = (q.total + 255) / 256;
+    if (g > 1024) g = 1024;
+    k_pack_job<<<(unsigned)g, 256, 0, s>>>(q);
+}
+
 struct PrologueArgs {
     Header* h;
     uint64_t* keys;

@@ -235,6 +235,29 @@ struct PackJob {
 // ldc / ldk <= 0: W is a dense [K3][Cin][Cout] tensor; otherwise the leading
 // Cin x Cout block of each offset of a wider tensor (a channel slice)
 PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int dt, int ldc = 0, int64_t ldk = 0);
+// the weight packing q as a launch of its own
+void launch_pack_job(hipStream_t s, const PackJob& q);
+
+// --- pointwise linear layer (linear.hip) -----------------------------------------
+struct LinearArgs {
+    const void* in;          // [m][Cin]
+    const int64_t* m_dev;    // device row count (nullptr = m_cap)
+    int64_t m_cap;
+    int Cin, Cout, dt;
+    const void* W;           // W[ci][co] at W[ci * ldw + co]
+    int ldw;
+    const float* scale;      // [Cout] or nullptr
+    const float* shift;      // [Cout] or nullptr
+    int relu;
+    const void* res;         // [m][Cout] or nullptr
+    int res_after;           // 1: res added after the activation
+    void* out;               // [m][Cout]
+};
+bool linear_mfma_supported(int Cin, int Cout, int dt);
+void* plan_linear_ws(Arena& a, int Cin, int Cout);
+// packs W into wpack (MFMA path) and runs the layer
+void launch_linear(hipStream_t s, const LinearArgs& a, void* wpack);
+
 // The first kernel of a block call: clears the voxel table and the status
 // header, and packs up to kMaxPackJobs weights, in one grid-stride launch.
 constexpr int kMaxPackJobs = 3;

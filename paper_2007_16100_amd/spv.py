@@ -30,7 +30,7 @@ _DT = {torch.float32: SPV_F32, torch.bfloat16: SPV_BF16, torch.float16: SPV_F16}
 
 # every symbol include/spv.h declares
 EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced",
-           "spv_devoxelize",
+           "spv_linear", "spv_devoxelize",
            "spv_block_workspace_bytes", "spv_block", "spv_lookup", "spv_status_check", "spv_status_string",
            "spv_last_hip_error")
 
@@ -71,7 +71,8 @@ def lib():
         L.spv_sparse_conv.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i64, i32, i32, vp, vp, vp, i32, vp, vp, i64,
                                       i32, i32]
         L.spv_sparse_conv_sliced.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i64, i32, i32, vp, i32, i32, vp, vp,
-                                             i32, vp, vp, i64, i32, i32]
+                                             vp, i32, vp, vp, i64, i32, i32]
+        L.spv_linear.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, i32, i32, vp, vp, i32, vp, i32, vp, i32, i32]
         L.spv_devoxelize.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, vp, i64, f32, i32, vp, i32, vp, i32, vp, vp,
                                      vp, i32, vp, i32, vp, vp]
         L.spv_block.argtypes = [vp, vp, sz, ct.POINTER(BlockParams), vp, vp, i64, vp, vp, vp]
@@ -80,8 +81,8 @@ def lib():
         L.spv_status_string.argtypes = [i32]
         L.spv_status_string.restype = ct.c_char_p
         L.spv_last_hip_error.argtypes = []
-        for f in ("spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced", "spv_devoxelize",
-                  "spv_block", "spv_lookup", "spv_status_check"):
+        for f in ("spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced", "spv_linear",
+                  "spv_devoxelize", "spv_block", "spv_lookup", "spv_status_check"):
             getattr(L, f).restype = ct.c_int
         _lib = L
     return _lib
@@ -218,19 +219,47 @@ def spv_sparse_conv_sliced(ws: Workspace, x: torch.Tensor, off: torch.Tensor, pa
                            W_full: torch.Tensor, Cin: int, Cout: int, m_out_cap: int,
                            m_out_dev: Optional[torch.Tensor] = None, scale: Optional[torch.Tensor] = None,
                            shift: Optional[torch.Tensor] = None, relu: bool = False, transposed: bool = False,
-                           out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """The conv with the first Cin x Cout channels of the full weight W_full [K3][Cin_full][Cout_full]
-    (and the first Cout entries of the full scale / shift)."""
+                           out: Optional[torch.Tensor] = None, res: Optional[torch.Tensor] = None,
+                           cin_offset: int = 0, in_rows: Optional[int] = None) -> torch.Tensor:
+    """The conv with input channels cin_offset .. cin_offset+Cin and the first Cout output
+    channels of the full weight W_full [K3][Cin_full][Cout_full] (and the first Cout entries of
+    the full scale / shift); res: a residual input added before the activation."""
     K3, Cin_full, Cout_full = W_full.shape
     if x.shape[1] != Cin:
         raise ValueError(f"x has {x.shape[1]} channels, the slice takes {Cin}")
+    if cin_offset < 0 or cin_offset + Cin > Cin_full:
+        raise ValueError("input-channel slice outside the weight")
     if out is None:
         out = torch.empty((max(m_out_cap, 1), Cout), dtype=x.dtype, device=x.device)
-    st = lib().spv_sparse_conv_sliced(_stream(), ws.ptr, ws.nbytes, _ptr(x), x.shape[0], Cin, _ptr(off), _ptr(pairs),
-                                      pairs.shape[0], K3, int(transposed), _ptr(W_full), Cin_full, Cout_full,
-                                      _ptr(scale), _ptr(shift), int(relu), _ptr(out), _ptr(m_out_dev), m_out_cap, Cout,
+    wp = ct.c_void_p(_ptr(W_full).value + cin_offset * Cout_full * W_full.element_size())
+    st = lib().spv_sparse_conv_sliced(_stream(), ws.ptr, ws.nbytes, _ptr(x), x.shape[0] if in_rows is None else in_rows,
+                                      Cin, _ptr(off), _ptr(pairs), pairs.shape[0], K3, int(transposed), wp,
+                                      Cin_full, Cout_full, _ptr(scale),
+                                      _ptr(shift), _ptr(res), int(relu), _ptr(out), _ptr(m_out_dev), m_out_cap, Cout,
                                       _DT[x.dtype])
     _chk(st, "spv_sparse_conv_sliced")
+    return out
+
+
+def spv_linear(ws: Workspace, x: torch.Tensor, W: torch.Tensor, Cout: Optional[int] = None,
+               m_dev: Optional[torch.Tensor] = None, m_cap: Optional[int] = None,
+               scale: Optional[torch.Tensor] = None, shift: Optional[torch.Tensor] = None, relu: bool = False,
+               res: Optional[torch.Tensor] = None, res_after_act: bool = False, cin_offset: int = 0,
+               out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """act(scale * (x @ W[cin_offset : cin_offset + Cin, :Cout]) + shift [+ res]) [+ res]."""
+    Cin = x.shape[1]
+    Cin_full, Cout_full = W.shape
+    Cout = Cout_full if Cout is None else Cout
+    if cin_offset < 0 or cin_offset + Cin > Cin_full:
+        raise ValueError("input-channel slice outside the weight")
+    m_cap = x.shape[0] if m_cap is None else m_cap
+    if out is None:
+        out = torch.empty((max(m_cap, 1), Cout), dtype=x.dtype, device=x.device)
+    wp = ct.c_void_p(_ptr(W).value + cin_offset * Cout_full * W.element_size())
+    st = lib().spv_linear(_stream(), ws.ptr, ws.nbytes, _ptr(x), _ptr(m_dev), m_cap, Cin, wp, Cin_full - cin_offset,
+                          Cout_full, _ptr(scale), _ptr(shift), int(relu), _ptr(res), int(res_after_act), _ptr(out),
+                          Cout, _DT[x.dtype])
+    _chk(st, "spv_linear")
     return out
 
 

@@ -57,13 +57,30 @@ def test_host_side_validation_without_gpu():
     st = L.spv_sparse_conv(None, ws, 1 << 30, ct.c_void_p(16), 4, 8, ct.c_void_p(16), ct.c_void_p(16), 4, 27, 0,
                            ct.c_void_p(16), None, None, 0, ct.c_void_p(16), None, 4, 16, 7)
     assert st == spv.SPV_ERR_INVALID_ARG
-    # a weight slice wider than the stored tensor
+    # a weight slice wider than the stored tensor; a residual that is the output
     st = L.spv_sparse_conv_sliced(None, ws, 1 << 30, ct.c_void_p(16), 4, 64, ct.c_void_p(16), ct.c_void_p(16), 4, 27,
-                                  0, ct.c_void_p(16), 32, 64, None, None, 0, ct.c_void_p(16), None, 4, 32, 1)
+                                  0, ct.c_void_p(16), 32, 64, None, None, None, 0, ct.c_void_p(16), None, 4, 32, 1)
     assert st == spv.SPV_ERR_INVALID_ARG
     st = L.spv_sparse_conv_sliced(None, ws, 1 << 30, ct.c_void_p(16), 4, 32, ct.c_void_p(16), ct.c_void_p(16), 4, 27,
-                                  0, ct.c_void_p(16), 32, 32, None, None, 0, ct.c_void_p(16), None, 4, 48, 1)
+                                  0, ct.c_void_p(16), 32, 32, None, None, None, 0, ct.c_void_p(16), None, 4, 48, 1)
     assert st == spv.SPV_ERR_INVALID_ARG
+    st = L.spv_sparse_conv_sliced(None, ws, 1 << 30, ct.c_void_p(16), 4, 32, ct.c_void_p(16), ct.c_void_p(16), 4, 27,
+                                  0, ct.c_void_p(16), 32, 32, None, None, ct.c_void_p(32), 0, ct.c_void_p(32), None, 4,
+                                  32, 1)
+    assert st == spv.SPV_ERR_INVALID_ARG
+    # linear: slice wider than W, misaligned rows, output aliasing the input
+    st = L.spv_linear(None, ws, 1 << 30, ct.c_void_p(16), None, 4, 64, ct.c_void_p(16), 32, 32, None, None, 0, None,
+                      0, ct.c_void_p(48), 32, 1)
+    assert st == spv.SPV_ERR_INVALID_ARG
+    st = L.spv_linear(None, ws, 1 << 30, ct.c_void_p(18), None, 4, 32, ct.c_void_p(16), 32, 32, None, None, 0, None,
+                      0, ct.c_void_p(48), 32, 1)
+    assert st == spv.SPV_ERR_INVALID_ARG
+    st = L.spv_linear(None, ws, 1 << 30, ct.c_void_p(16), None, 4, 32, ct.c_void_p(16), 32, 32, None, None, 0, None,
+                      0, ct.c_void_p(16), 32, 1)
+    assert st == spv.SPV_ERR_INVALID_ARG
+    st = L.spv_linear(None, ws, 16, ct.c_void_p(16), None, 4, 32, ct.c_void_p(16), 32, 32, None, None, 0, None,
+                      0, ct.c_void_p(48), 32, 1)
+    assert st == spv.SPV_ERR_CAPACITY
     # misaligned feature pointer
     st = L.spv_sparse_conv(None, ws, 1 << 30, ct.c_void_p(18), 4, 8, ct.c_void_p(16), ct.c_void_p(16), 4, 27, 0,
                            ct.c_void_p(16), None, None, 0, ct.c_void_p(16), None, 4, 16, 1)

@@ -647,3 +647,66 @@ def test_block_graph_replay(spv, sweep):
         spv.spv_block(ws, params, d_xyz, d_feat, out=scratch)  # eager work between replays
         torch.cuda.synchronize()
         assert torch.equal(scratch.view(torch.int16), ref.view(torch.int16)), f"eager after replay {i}"
+
+
+# ---------------------------------------------------------------------------
+# pointwise linear layer and the split of a conv over concatenated inputs
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("cin,cout,dtype", [(32, 64, "bf16"), (96, 256, "bf16"), (256, 128, "f16"),
+                                            (128, 96, "bf16"), (8, 16, "bf16"), (96, 19, "bf16"), (40, 24, "f32")])
+@pytest.mark.parametrize("mode", ["plain", "res_before", "res_after"])
+def test_linear(spv, cin, cout, dtype, mode):
+    """Rows past the live count (m_dev < m_cap) are left alone; 16-row blocks with a ragged tail."""
+    m_cap, m = 20011, 19997
+    x = synth.normal((m_cap, cin), 1040, dtype=dtype)
+    W = synth.linear_weight(cin, cout, 1041, dtype)
+    sc, sh = synth.folded_bn(cout, 1042)
+    res = synth.normal((m_cap, cout), 1043, dtype=dtype) if mode != "plain" else None
+    after = mode == "res_after"
+    ws = spv.Workspace.for_ops(16, max(cin, cout))
+    out = torch.full((m_cap, cout), 7.0, dtype=TD[dtype], device="cuda")
+    spv.spv_linear(ws, dev(x, dtype), dev(W, dtype), m_dev=torch.tensor([m], dtype=torch.int64, device="cuda"),
+                   scale=dev(sc), shift=dev(sh), relu=True, res=None if res is None else dev(res, dtype),
+                   res_after_act=after, out=out)
+    got = host(out, dtype)
+    ref = oracle.linear(x[:m], W, dtype, sc, sh, True, None if res is None else res[:m], after)
+    check_close(got[:m], ref, dtype)
+    assert np.all(synth.from_storage(got[m:], dtype) == 7.0)
+
+
+def test_linear_input_channel_offset(spv):
+    """The rows cin_offset .. of a wider weight (one part of a concatenated input)."""
+    x = synth.normal((5000, 64), 1044, dtype="bf16")
+    W = synth.linear_weight(192, 128, 1045, "bf16")
+    ws = spv.Workspace.for_ops(16, 192)
+    got = host(spv.spv_linear(ws, dev(x, "bf16"), dev(W, "bf16"), cin_offset=128), "bf16")
+    ref = oracle.linear(x, np.ascontiguousarray(W[128:]), "bf16")
+    check_close(got, ref, "bf16")
+
+
+@pytest.mark.parametrize("ca,cb,cout,transposed", [(96, 32, 96, False), (128, 64, 128, False),
+                                                   (256, 128, 256, False), (64, 32, 64, True)])
+def test_conv_concat_split(spv, sweep, ca, cb, cout, transposed):
+    """A conv over the concatenation [a; b] (a decoder's skip connection) as two sliced convs,
+    W_a a scaled into a residual and W_b b + shift + that residual, against the oracle's conv on
+    the concatenated features with the full weight."""
+    rc, _, _, _ = oracle.voxelize(sweep[::2], 0.05)
+    if transposed:
+        oc, off, pairs = oracle.kernel_map(rc, 2, 2)
+        m_in, m_out, K3 = len(oc), len(rc), 8
+    else:
+        _, off, pairs = oracle.kernel_map(rc)
+        m_in = m_out = len(rc)
+        K3 = 27
+    a = synth.normal((m_in, ca), 1046, dtype="bf16")
+    b = synth.normal((m_in, cb), 1047, dtype="bf16")
+    W = synth.conv_weight(K3, ca + cb, cout, 1048, "bf16")
+    sc, sh = synth.folded_bn(cout, 1049)
+    ref = oracle.sparse_conv(np.concatenate([a, b], 1), off, pairs, W, m_out, "bf16", sc, sh, True, transposed)
+    ws = spv.Workspace.for_ops(max(m_in, m_out), 256)
+    d_off, d_pairs, d_W = dev(off), dev(pairs), dev(W, "bf16")
+    part = spv.spv_sparse_conv_sliced(ws, dev(a, "bf16"), d_off, d_pairs, d_W, ca, cout, m_out, scale=dev(sc),
+                                      transposed=transposed)
+    got = spv.spv_sparse_conv_sliced(ws, dev(b, "bf16"), d_off, d_pairs, d_W, cb, cout, m_out, scale=dev(sc),
+                                     shift=dev(sh), relu=True, transposed=transposed, res=part, cin_offset=ca)
+    check_close(host(got, "bf16")[:m_out], ref, "bf16")
