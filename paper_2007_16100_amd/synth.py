@@ -184,3 +184,72 @@ def folded_bn(c: int, seed: int):
     scale = rng.uniform(0.5, 1.5, size=c).astype(np.float32)
     shift = rng.normal(0.0, 0.1, size=c).astype(np.float32)
     return scale, shift
+
+
+# ---------------------------------------------------------------------------
+# an SPVCNN-style network: point features and random-init parameters
+# ---------------------------------------------------------------------------
+# channel widths: stem, four encoder stages, four decoder stages
+SPVCNN_WIDTHS = (32, 32, 64, 128, 256, 256, 128, 96, 96)
+SPVCNN_IN = 4        # x, y, z, intensity
+SPVCNN_CLASSES = 19
+
+
+def point_features(xyz: np.ndarray, seed: int, dtype: str = "f32") -> np.ndarray:
+    """Per-point input features [n][4]: the coordinates and an intensity ~ U(0, 1)."""
+    rng = np.random.default_rng(seed)
+    f = np.concatenate([np.asarray(xyz, np.float32), rng.uniform(0.0, 1.0, (len(xyz), 1)).astype(np.float32)], 1)
+    return to_storage(f, dtype)
+
+
+def spvcnn_params(seed: int, dtype: str, widths=SPVCNN_WIDTHS, c_in: int = SPVCNN_IN,
+                  classes: int = SPVCNN_CLASSES) -> dict:
+    """Random-init parameters by layer name; each entry is (W, scale, shift), scale / shift the
+    folded BatchNorm of that layer (the classifier's scale is None and its shift is the bias).
+
+    stem.0 / stem.1      3x3x3 convs c_in -> w0 -> w0
+    down.s               2x2x2 stride-2 conv w[s-1] -> w[s-1]               (s = 1..4)
+    enc.s.r.{a,b,sc}     residual block r of stage s (r = 0: w[s-1] -> w[s], r = 1: w[s] -> w[s]);
+                         a, b: 3x3x3 convs; sc: 1x1 shortcut when the width changes
+    up.u                 2x2x2 transposed conv w[3+u] -> w[4+u]             (u = 1..4)
+    dec.u.r.{a,b,sc}     residual blocks after the skip concatenation [up output; encoder x_{4-u}]
+                         (r = 0: w[4+u] + w[4-u] -> w[4+u], r = 1: w[4+u] -> w[4+u])
+    point.0 .. point.3   point-branch MLPs c_in -> w0, w0 -> w4, w4 -> w6, w6 -> w8
+    head                 linear w8 -> classes with a bias
+    """
+    w = widths
+    P = {}
+    sd = [seed]
+
+    def nxt():
+        sd[0] += 1
+        return sd[0]
+
+    def conv(name, K3, cin, cout):
+        P[name] = (conv_weight(K3, cin, cout, nxt(), dtype),) + folded_bn(cout, nxt())
+
+    def lin(name, cin, cout):
+        P[name] = (linear_weight(cin, cout, nxt(), dtype),) + folded_bn(cout, nxt())
+
+    def res(name, cin, cout):
+        conv(name + ".a", 27, cin, cout)
+        conv(name + ".b", 27, cout, cout)
+        if cin != cout:
+            lin(name + ".sc", cin, cout)
+
+    conv("stem.0", 27, c_in, w[0])
+    conv("stem.1", 27, w[0], w[0])
+    for s in range(1, 5):
+        conv(f"down.{s}", 8, w[s - 1], w[s - 1])
+        res(f"enc.{s}.0", w[s - 1], w[s])
+        res(f"enc.{s}.1", w[s], w[s])
+    for u in range(1, 5):
+        conv(f"up.{u}", 8, w[3 + u], w[4 + u])
+        res(f"dec.{u}.0", w[4 + u] + w[4 - u], w[4 + u])
+        res(f"dec.{u}.1", w[4 + u], w[4 + u])
+    for i, (cin, cout) in enumerate([(c_in, w[0]), (w[0], w[4]), (w[4], w[6]), (w[6], w[8])]):
+        lin(f"point.{i}", cin, cout)
+    rng = np.random.default_rng(nxt())
+    P["head"] = (linear_weight(w[8], classes, nxt(), dtype), None,
+                 rng.normal(0.0, 0.1, size=classes).astype(np.float32))
+    return P
