@@ -1,0 +1,176 @@
+"""SPVCNN-style encoder-decoder forward on the libspv C ABI.
+
+The backbone of the paper's appendix A.1: MinkowskiNet-style residual sparse-conv
+blocks (a U-Net with four stride-2 stages and four transposed stages with skip
+connections) wrapped by four SPVConv point branches (Sec. 3.3).  The first
+module voxelizes the points and devoxelizes after the stem; the second
+voxelizes again and devoxelizes after the four downsampling stages; the last two
+each wrap two upsampling stages.  Every devoxelization is fused with the point
+branch's MLP by addition; a linear head gives per-point class scores.
+
+Every step runs in libspv's kernels; this module only sequences the calls and
+holds the device buffers:
+
+* plan: voxelization at stride 1, the four stride-2 maps (which give the
+  coordinate sets of strides 2..16) and the five submanifold maps, one
+  synchronization per stride to size what follows exactly;
+* a conv over a skip concatenation [t; x] runs as two sliced convs,
+  W_t t (scaled, unshifted) handed as the residual input of W_x x + shift;
+  the 1x1 shortcut over it likewise as two linear layers;
+* a devoxelization whose point MLP the fused kernel does not take on matrix
+  cores (C or C_p above 128) runs as a devoxelization plus a linear layer that
+  adds it after the activation.
+Layer names and widths follow ``synth.spvcnn_params``.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict, List, Optional
+
+import numpy as np
+import torch
+
+from . import spv
+
+_TORCH = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}
+
+
+def voxel_size_at(v: float, s: int) -> float:
+    """Voxel size of stride 2^s: the float32 voxel size scaled by 2^s (exact in float32), so
+    that voxelizing at stride 2^s gives the cascaded stride-2 coordinates."""
+    return float(np.float32(v) * np.float32(2.0 ** s))
+
+
+@dataclass
+class Plan:
+    coords: List[torch.Tensor]      # [m_s][4] per stride 2^s, s = 0..4
+    m: List[int]
+    down: List[Optional[spv.KernelMap]]   # down[s]: stride 2^(s-1) -> 2^s (s = 1..4)
+    subm: List[spv.KernelMap]
+
+
+class SPVCNN:
+    def __init__(self, params: Dict[str, tuple], dtype: str = "bf16", voxel_size: float = 0.05,
+                 mode: int = spv.SPV_DEVOX_CENTER, device: str = "cuda"):
+        self.dt = _TORCH[dtype]
+        self.v = voxel_size
+        self.mode = mode
+        self.device = device
+        self.P = {}
+        for name, (W, sc, sh) in params.items():
+            self.P[name] = (self._dev(W), None if sc is None else torch.from_numpy(np.asarray(sc)).to(device),
+                            None if sh is None else torch.from_numpy(np.asarray(sh)).to(device))
+        self.ws = None
+
+    def _dev(self, a):
+        a = np.ascontiguousarray(a)
+        if self.dt == torch.float32:
+            return torch.from_numpy(a.astype(np.float32)).to(self.device)
+        return torch.from_numpy(a.view(np.int16)).view(self.dt).to(self.device)
+
+    def _workspace(self, n):
+        need = spv.spv_workspace_bytes(max(n, 1), 256)
+        if self.ws is None or self.ws.nbytes < need:
+            self.ws = spv.Workspace(need, self.device)
+        return self.ws
+
+    # -- plan ----------------------------------------------------------------
+    def plan(self, xyz: torch.Tensor, batch: Optional[torch.Tensor] = None, feat: Optional[torch.Tensor] = None):
+        ws = self._workspace(xyz.shape[0])
+        vox = spv.spv_voxelize(ws, xyz, self.v, feat, batch)
+        m = [vox.m]
+        coords = [vox.coords[: vox.m]]
+        down: List[Optional[spv.KernelMap]] = [None]
+        for s in range(1, 5):
+            km = spv.spv_kernel_map(ws, coords[s - 1], K=2, stride=2)
+            ms = int(km.m_out_dev.item())
+            down.append(km)
+            m.append(ms)
+            coords.append(km.out_coords[:ms])
+        subm = [spv.spv_kernel_map(ws, c, sync=False) for c in coords]
+        return Plan(coords, m, down, subm), vox
+
+    # -- layers --------------------------------------------------------------
+    def _conv(self, x, name, km, m_out, relu=True, transposed=False, res=None, cin_offset=0, cout=None,
+              shift=True):
+        W, sc, sh = self.P[name]
+        Cout = W.shape[2] if cout is None else cout
+        return spv.spv_sparse_conv_sliced(self.ws, x, km.off, km.pairs, W, x.shape[1], Cout, m_out, scale=sc,
+                                          shift=sh if shift else None, relu=relu, transposed=transposed, res=res,
+                                          cin_offset=cin_offset)
+
+    def _lin(self, x, name, relu=False, res=None, res_after=False, cin_offset=0, shift=True):
+        W, sc, sh = self.P[name]
+        return spv.spv_linear(self.ws, x, W, scale=sc, shift=sh if shift else None, relu=relu, res=res,
+                              res_after_act=res_after, cin_offset=cin_offset)
+
+    def _resblock(self, parts, name, km):
+        """Residual block over the concatenation of `parts` (one tensor: no concatenation)."""
+        m = parts[0].shape[0]
+        offs = np.cumsum([0] + [p.shape[1] for p in parts[:-1]])
+
+        def over_parts(layer, last_kw):
+            r = None
+            for i, (p, o) in enumerate(zip(parts, offs)):
+                final = i == len(parts) - 1
+                r = layer(p, int(o), r, final, last_kw if final else {})
+            return r
+
+        h = over_parts(lambda p, o, r, final, kw: self._conv(p, name + ".a", km, m, relu=final, res=r,
+                                                             cin_offset=o, shift=final), {})
+        if name + ".sc" in self.P:
+            s = over_parts(lambda p, o, r, final, kw: self._lin(p, name + ".sc", res=r, cin_offset=o, shift=final),
+                           {})
+        else:
+            s = parts[0]
+        return self._conv(h, name + ".b", km, m, res=s)
+
+    def _fuse(self, plan, vfeat, s, z, name, xyz, batch):
+        W, sc, sh = self.P[name]
+        C, Cp = vfeat.shape[1], z.shape[1]
+        fused = self.dt != torch.float32 and C % 16 == 0 and C // 16 in (1, 2, 4, 6, 8) and Cp % 8 == 0 and Cp <= 128
+        if fused:
+            return spv.spv_devoxelize(self.ws, plan.coords[s], vfeat, xyz, self.v, s, self.mode, batch, pfeat=z, Wp=W,
+                                      scale_p=sc, shift_p=sh, relu_p=True)
+        d = spv.spv_devoxelize(self.ws, plan.coords[s], vfeat, xyz, self.v, s, self.mode, batch)
+        return spv.spv_linear(self.ws, z, W, scale=sc, shift=sh, relu=True, res=d, res_after_act=True)
+
+    def _revoxelize(self, xyz, z, s, batch, m):
+        vox = spv.spv_voxelize(self.ws, xyz, voxel_size_at(self.v, s), z, batch, sync=False)
+        return vox.vfeat[:m], vox
+
+    # -- forward -------------------------------------------------------------
+    def forward(self, xyz: torch.Tensor, feat: torch.Tensor, batch: Optional[torch.Tensor] = None,
+                trace: Optional[dict] = None) -> torch.Tensor:
+        plan, vox = self.plan(xyz, batch, feat)
+        m = plan.m
+        x = vox.vfeat[: m[0]]
+        x = self._conv(x, "stem.0", plan.subm[0], m[0])
+        x = self._conv(x, "stem.1", plan.subm[0], m[0])
+        skips = [x]
+        z = self._fuse(plan, x, 0, feat, "point.0", xyz, batch)
+
+        x, _ = self._revoxelize(xyz, z, 0, batch, m[0])
+        for s in range(1, 5):
+            x = self._conv(x, f"down.{s}", plan.down[s], m[s])
+            x = self._resblock([x], f"enc.{s}.0", plan.subm[s])
+            x = self._resblock([x], f"enc.{s}.1", plan.subm[s])
+            skips.append(x)
+        z = self._fuse(plan, x, 4, z, "point.1", xyz, batch)
+
+        def up(y, u):
+            t = self._conv(y, f"up.{u}", plan.down[5 - u], m[4 - u], transposed=True)
+            y = self._resblock([t, skips[4 - u]], f"dec.{u}.0", plan.subm[4 - u])
+            return self._resblock([y], f"dec.{u}.1", plan.subm[4 - u])
+
+        y, vox4 = self._revoxelize(xyz, z, 4, batch, m[4])
+        y = up(up(y, 1), 2)
+        z = self._fuse(plan, y, 2, z, "point.2", xyz, batch)
+        y, vox2 = self._revoxelize(xyz, z, 2, batch, m[2])
+        y = up(up(y, 3), 4)
+        z = self._fuse(plan, y, 0, z, "point.3", xyz, batch)
+        W, _, bias = self.P["head"]
+        out = spv.spv_linear(self.ws, z, W, shift=bias)
+        if trace is not None:
+            trace.update(plan=plan, revox=[vox4, vox2], z3=z, y4=y, skips=skips)
+        return out
