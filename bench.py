@@ -320,6 +320,64 @@ def configs_mode(args):
         torch.cuda.empty_cache()
 
 
+def spvcnn_flops(P, plan, n):
+    """Effective FLOPs of one network forward (Sec. 4.3: active synapses only): per layer
+    2 * C_in * C_out times its kernel-map pairs (convs) or rows (1x1 shortcuts, point MLPs,
+    head)."""
+    pairs = lambda km: int(km.off[-1].item())
+    units = {}
+    for name in P:
+        parts = name.split(".")
+        if parts[0] == "stem":
+            units[name] = pairs(plan.subm[0])
+        elif parts[0] == "down":
+            units[name] = pairs(plan.down[int(parts[1])])
+        elif parts[0] == "up":
+            units[name] = pairs(plan.down[5 - int(parts[1])])
+        elif parts[0] in ("enc", "dec"):
+            s = int(parts[1]) if parts[0] == "enc" else 4 - int(parts[1])
+            units[name] = plan.m[s] if parts[3] == "sc" else pairs(plan.subm[s])
+        else:  # point MLPs and the head run on every point
+            units[name] = n
+    return sum(2.0 * P[k][0].shape[-2] * P[k][0].shape[-1] * u for k, u in units.items())
+
+
+def spvcnn_mode(args):
+    """The SPVCNN-style encoder-decoder forward on a batch of 4 sweeps (seeds 1005-1008, batch
+    index in the key), bf16: wall-clock per forward (synchronized, the plan's per-stride count
+    read-backs included) and effective conv + linear TFLOP/s."""
+    import torch
+    from paper_2007_16100_amd import synth
+    from paper_2007_16100_amd.spvcnn import SPVCNN
+    sw = [synth.lidar_sweep(1005 + i) for i in range(4)]
+    xyz = np.concatenate(sw)
+    batch = np.concatenate([np.full(len(a), i, np.int32) for i, a in enumerate(sw)])
+    feat = synth.point_features(xyz, 9001, "bf16")
+    P = synth.spvcnn_params(9002, "bf16")
+    net = SPVCNN(P, "bf16", 0.05)
+    d_xyz = torch.from_numpy(xyz).cuda()
+    d_b = torch.from_numpy(batch).cuda()
+    d_f = torch.from_numpy(feat.view(np.int16)).view(torch.bfloat16).cuda()
+    tr = {}
+    net.forward(d_xyz, d_f, d_b, trace=tr)
+    torch.cuda.synchronize()
+    F = spvcnn_flops(P, tr["plan"], len(xyz))
+    for _ in range(args.warmup):
+        net.forward(d_xyz, d_f, d_b)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(args.steps):
+        t0 = time.perf_counter()
+        net.forward(d_xyz, d_f, d_b)
+        torch.cuda.synchronize()
+        ts.append(time.perf_counter() - t0)
+    ms = float(np.median(ts)) * 1e3
+    print(json.dumps({"op": "spvcnn forward, 4 sweeps", "points": int(len(xyz)), "voxels_per_stride": tr["plan"].m,
+                      "ms_median": ms, "ms_p10": float(np.percentile(ts, 10)) * 1e3,
+                      "ms_p90": float(np.percentile(ts, 90)) * 1e3, "points_per_s": len(xyz) / (ms * 1e-3),
+                      "eff_flops": F, "TFLOPs": F / (ms * 1e-3) / 1e12, "steps": args.steps}), flush=True)
+
+
 def cpu_baseline(xyz, convs, C, v=0.05):
     """The oracle, as it stands, on one full 96->96 conv layer of the workload (one thread)."""
     import oracle
@@ -352,7 +410,12 @@ def main():
     ap.add_argument("--batches", default="1,4,16,64", help="sweeps per batch for --sizes")
     ap.add_argument("--configs", action="store_true",
                     help="map build and conv alone at the 32->32 and 64<->128 (k2s2, transposed) shapes")
+    ap.add_argument("--spvcnn", action="store_true",
+                    help="the SPVCNN-style encoder-decoder forward on a batch of 4 sweeps")
     args = ap.parse_args()
+    if args.spvcnn:
+        spvcnn_mode(args)
+        return
     if args.sizes:
         sizes_mode(args)
         return

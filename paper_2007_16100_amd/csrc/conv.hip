@@ -66,7 +66,8 @@ __device__ inline int64_t tile_of(int64_t j, int64_t m, int64_t nt, int T) {
 // fragment t of the packing (t = ((k * KCH + kc) * NB + nb) * 64 + lane)
 // W[k][c][col] sits at W[k * ldk + c * ldc + col] (ldc = Cout, ldk = Cin * Cout
 // for a dense [K3][Cin][Cout] tensor; larger for a channel slice of a wider one)
-__device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int ldc, int64_t ldk, int KCH, int NB, int64_t t) {
+__device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int Cout, int ldc, int64_t ldk, int KCH, int NB,
+                                     int64_t t) {
     const int lane = (int)(t & 63);
     int64_t f = t >> 6;
     const int nb = (int)(f % NB);
@@ -79,8 +80,9 @@ __device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int ldc, int64
     for (int e = 0; e < 4; ++e) {
         uint32_t lo = 0, hi = 0;
         const int c0 = ci0 + 2 * e, c1 = ci0 + 2 * e + 1;
-        if (c0 < Cin) lo = W[(int64_t)k * ldk + (int64_t)c0 * ldc + col];
-        if (c1 < Cin) hi = W[(int64_t)k * ldk + (int64_t)c1 * ldc + col];
+        // zeros past the last input channel and past the last output column
+        if (c0 < Cin && col < Cout) lo = W[(int64_t)k * ldk + (int64_t)c0 * ldc + col];
+        if (c1 < Cin && col < Cout) hi = W[(int64_t)k * ldk + (int64_t)c1 * ldc + col];
         w[e] = lo | (hi << 16);
     }
     return make_uint4(w[0], w[1], w[2], w[3]);
@@ -89,7 +91,7 @@ __device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int ldc, int64
 // a weight packing run alongside another kernel's work (grid-stride)
 __device__ inline void pack_job_run(const PackJob& q) {
     for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < q.total; t += (int64_t)gridDim.x * blockDim.x)
-        q.wpack[t] = pack_fragment(q.W, q.Cin, q.ldc, q.ldk, q.KCH, q.NB, t);
+        q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.ldc, q.ldk, q.KCH, q.NB, t);
 }
 
 // For every offset k and tile t in [0, nt]: bnd[k][t] = first pair of offset k
@@ -234,7 +236,7 @@ __global__ __launch_bounds__(256) void k_block_prologue(PrologueArgs a) {
     for (int j = 0; j < a.njobs; ++j) {
         const PackJob& q = a.job[j];
         for (int64_t t = t0; t < q.total; t += stride)
-            q.wpack[t] = pack_fragment(q.W, q.Cin, q.ldc, q.ldk, q.KCH, q.NB, t);
+            q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.ldc, q.ldk, q.KCH, q.NB, t);
     }
 }
 
@@ -586,6 +588,9 @@ static int conv_kch(int Cin) {
 static int conv_nbw(int KCH, int NB) {
     for (int w = 4; w > 1; --w)
         if (NB % w == 0 && KCH * w <= 12 && KCH < 6 && NB / w <= 8) return w;
+    // wide inputs and outputs (e.g. 256 -> 256): two blocks per wave where one
+    // each would take more than 8 waves
+    if (KCH >= 6 && NB > 8 && NB % 2 == 0 && NB / 2 <= 8) return 2;
     return 1;
 }
 
@@ -636,7 +641,7 @@ static void launch_tile_kch(hipStream_t s, const ConvPlan& p, const void* in, in
     switch (conv_nbw(KCH, Cout / 16)) {
 #define SPV_NBW_CASE(W)                                                                                        \
     case W:                                                                                                    \
-        if constexpr (KCH * W <= 12 && (KCH < 6 || W == 1))                                                   \
+        if constexpr ((KCH * W <= 12 && (KCH < 6 || W == 1)) || (KCH >= 6 && W == 2))                         \
             launch_tile3<DT, KCH, W>(s, p, in, Cin, in_rows, pairs, pair_bound, transposed, wpack, scale, shift, \
                                      relu, out, Cout);                                                         \
         break;

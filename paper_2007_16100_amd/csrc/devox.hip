@@ -356,7 +356,7 @@ __global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __
 bool devox_mfma_supported(int C, int Cp, int dt) {
     if (dt == SPV_F32 || C % 16 != 0) return false;
     int NB = C / 16;
-    if (!(NB == 1 || NB == 2 || NB == 4 || NB == 6 || NB == 8)) return false;
+    if (!(NB == 1 || NB == 2 || NB == 4 || NB == 6 || NB == 8 || NB == 16)) return false;
     return Cp == 0 || (Cp % 8 == 0 && Cp <= 128);
 }
 
@@ -395,6 +395,7 @@ static void launch_devox_dt(hipStream_t s, const DevoxArgs& a, const void* wpack
         case 4: launch_devox_kch<DT, 4>(s, a, wpack); break;
         case 6: launch_devox_kch<DT, 6>(s, a, wpack); break;
         case 8: launch_devox_kch<DT, 8>(s, a, wpack); break;
+        case 16: launch_devox_kch<DT, 16>(s, a, wpack); break;
     }
 }
 

@@ -6,7 +6,9 @@
 // devoxelized voxel features; the 1x1 shortcut of a residual block is the first;
 // a classifier is shift = bias, no activation.
 //
-// MFMA path (bf16/f16, C_in % 8 == 0, C_out in 16 * {1, 2, 4, 6, 8, 16}):
+// MFMA path (bf16/f16, C_in % 8 == 0, ceil(C_out / 16) in {1, 2, 4, 6, 8, 16};
+// a C_out that is not a multiple of 16 -- a classifier's -- computes zero
+// columns up to the next multiple and stores only the real ones):
 // the packed W (the conv's operand fragments, one offset) and scale / shift are
 // staged in LDS once per workgroup; each wave then takes blocks of 16 rows in
 // turn (grid-stride), multiplies them on v_mfma_f32_16x16x32 with W^T as the A
@@ -18,19 +20,19 @@ namespace spv {
 
 constexpr int kLinWaves = 4;
 
-template <int DT, int KCH, int NB>
+template <int DT, int KCH, int NB, bool RAGGED>
 __global__ __launch_bounds__(64 * kLinWaves) void k_linear_mfma(
     const uint16_t* __restrict__ in, int Cin, const int64_t* __restrict__ m_dev, int64_t m_cap,
     const uint4* __restrict__ wpack, const float* __restrict__ scale, const float* __restrict__ shift, int relu,
-    const uint16_t* __restrict__ res, int res_after, uint16_t* __restrict__ out) {
+    const uint16_t* __restrict__ res, int res_after, uint16_t* __restrict__ out, int Cout) {
     constexpr int C = NB * 16;
     constexpr int FR = KCH * NB;
     __shared__ __align__(16) uint4 wl[FR * 64];
     __shared__ float ssc[C], ssh[C];
     for (int f = threadIdx.x; f < FR * 64; f += blockDim.x) wl[f] = wpack[f];
     for (int c = threadIdx.x; c < C; c += blockDim.x) {
-        ssc[c] = scale ? scale[c] : 1.f;
-        ssh[c] = shift ? shift[c] : 0.f;
+        ssc[c] = (scale && c < Cout) ? scale[c] : 1.f;
+        ssh[c] = (shift && c < Cout) ? shift[c] : 0.f;
     }
     __syncthreads();
 
@@ -66,11 +68,17 @@ __global__ __launch_bounds__(64 * kLinWaves) void k_linear_mfma(
             const int c = nb * 16 + 4 * g;
             float rv[4] = {0.f, 0.f, 0.f, 0.f};
             if (res) {
-                const uint2 u = *(const uint2*)(res + row * C + c);
-                rv[0] = from16<DT>(u.x & 0xFFFF);
-                rv[1] = from16<DT>(u.x >> 16);
-                rv[2] = from16<DT>(u.y & 0xFFFF);
-                rv[3] = from16<DT>(u.y >> 16);
+                if constexpr (RAGGED) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (c + e < Cout) rv[e] = from16<DT>(res[row * Cout + c + e]);
+                } else {
+                    const uint2 u = *(const uint2*)(res + row * C + c);
+                    rv[0] = from16<DT>(u.x & 0xFFFF);
+                    rv[1] = from16<DT>(u.x >> 16);
+                    rv[2] = from16<DT>(u.y & 0xFFFF);
+                    rv[3] = from16<DT>(u.y >> 16);
+                }
             }
             float y[4];
 #pragma unroll
@@ -80,9 +88,15 @@ __global__ __launch_bounds__(64 * kLinWaves) void k_linear_mfma(
                 if (relu) y[e] = fmaxf(y[e], 0.f);
                 if (res_after) y[e] += rv[e];
             }
-            const uint32_t lo = (uint32_t)to16<DT>(y[0]) | ((uint32_t)to16<DT>(y[1]) << 16);
-            const uint32_t hi = (uint32_t)to16<DT>(y[2]) | ((uint32_t)to16<DT>(y[3]) << 16);
-            *(uint2*)(out + row * C + c) = make_uint2(lo, hi);
+            if constexpr (RAGGED) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (c + e < Cout) out[row * Cout + c + e] = to16<DT>(y[e]);
+            } else {
+                const uint32_t lo = (uint32_t)to16<DT>(y[0]) | ((uint32_t)to16<DT>(y[1]) << 16);
+                const uint32_t hi = (uint32_t)to16<DT>(y[2]) | ((uint32_t)to16<DT>(y[3]) << 16);
+                *(uint2*)(out + row * C + c) = make_uint2(lo, hi);
+            }
         }
     }
 }
@@ -114,11 +128,12 @@ __global__ __launch_bounds__(256) void k_linear_valu(const void* __restrict__ in
 static int linear_kch(int Cin) { return (Cin + 31) / 32; }
 
 bool linear_mfma_supported(int Cin, int Cout, int dt) {
-    if (dt == SPV_F32 || Cin % 8 != 0 || Cout % 16 != 0) return false;
-    const int KCH = linear_kch(Cin), NB = Cout / 16;
+    if (dt == SPV_F32 || Cin % 8 != 0) return false;
+    const int KCH = linear_kch(Cin), NB = (Cout + 15) / 16;
     const bool kch_ok = KCH == 1 || KCH == 2 || KCH == 3 || KCH == 4 || KCH == 8;
     const bool nb_ok = NB == 1 || NB == 2 || NB == 4 || NB == 6 || NB == 8 || NB == 16;
-    return kch_ok && nb_ok;
+    // ragged widths (not a multiple of 16) are built for classifier sizes only
+    return kch_ok && nb_ok && (Cout % 16 == 0 || NB <= 2);
 }
 
 void* plan_linear_ws(Arena& a, int Cin, int Cout) {
@@ -132,14 +147,19 @@ static void launch_lin(hipStream_t s, const LinearArgs& a, const void* wpack) {
     int64_t grid = (blocks16 + kLinWaves - 1) / kLinWaves;
     if (grid > 1024) grid = 1024;
     if (grid < 1) grid = 1;
-    k_linear_mfma<DT, KCH, NB><<<(unsigned)grid, 64 * kLinWaves, 0, s>>>(
-        (const uint16_t*)a.in, a.Cin, a.m_dev, a.m_cap, (const uint4*)wpack, a.scale, a.shift, a.relu,
-        (const uint16_t*)a.res, a.res_after, (uint16_t*)a.out);
+    if (a.Cout == NB * 16)
+        k_linear_mfma<DT, KCH, NB, false><<<(unsigned)grid, 64 * kLinWaves, 0, s>>>(
+            (const uint16_t*)a.in, a.Cin, a.m_dev, a.m_cap, (const uint4*)wpack, a.scale, a.shift, a.relu,
+            (const uint16_t*)a.res, a.res_after, (uint16_t*)a.out, a.Cout);
+    else if constexpr (NB <= 2)
+        k_linear_mfma<DT, KCH, NB, true><<<(unsigned)grid, 64 * kLinWaves, 0, s>>>(
+            (const uint16_t*)a.in, a.Cin, a.m_dev, a.m_cap, (const uint4*)wpack, a.scale, a.shift, a.relu,
+            (const uint16_t*)a.res, a.res_after, (uint16_t*)a.out, a.Cout);
 }
 
 template <int DT, int KCH>
 static void launch_lin_nb(hipStream_t s, const LinearArgs& a, const void* wpack) {
-    switch (a.Cout / 16) {
+    switch ((a.Cout + 15) / 16) {
         case 1: launch_lin<DT, KCH, 1>(s, a, wpack); break;
         case 2: launch_lin<DT, KCH, 2>(s, a, wpack); break;
         case 4: launch_lin<DT, KCH, 4>(s, a, wpack); break;
@@ -163,7 +183,7 @@ static void launch_lin_dt(hipStream_t s, const LinearArgs& a, const void* wpack)
 void launch_linear(hipStream_t s, const LinearArgs& a, void* wpack) {
     if (a.m_cap <= 0) return;
     if (linear_mfma_supported(a.Cin, a.Cout, a.dt)) {
-        const int KCH = linear_kch(a.Cin), NB = a.Cout / 16;
+        const int KCH = linear_kch(a.Cin), NB = (a.Cout + 15) / 16;
         PackJob q{(const uint16_t*)a.W, (uint4*)wpack, 1, a.Cin, a.Cout, KCH, NB, (int64_t)KCH * NB * 64, a.ldw,
                   (int64_t)a.Cin * a.ldw};
         launch_pack_job(s, q);

@@ -48,7 +48,7 @@ struct alignas(256) Header {
     uint32_t status;
     uint32_t pad;
     int64_t m;              // unique voxels inserted by the voxelization
-    int64_t aux[4];
+    int64_t aux[4];         // [0]: voxels the scatter-mean sums with a whole workgroup
 };
 
 __device__ inline void raise_flag(Header* h, uint32_t f) { atomicOr(&h->status, f); }

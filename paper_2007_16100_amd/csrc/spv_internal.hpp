@@ -150,6 +150,7 @@ struct VoxelizeWs {
     int32_t* seg;       // [n + 1] CSR offsets of the points of each voxel
     int32_t* fill;      // [n]
     int32_t* plist;     // [n] point ids grouped by voxel
+    int32_t* longv;     // [n] voxels whose mean takes a whole workgroup (count in h->aux[0])
     int32_t* scan_tmp;  // [scan_tmp_entries(n)]
 };
 void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n);

@@ -23,6 +23,7 @@ void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n) {
     w.seg = a.take<int32_t>(nn + 1);
     w.fill = a.take<int32_t>(nn);
     w.plist = a.take<int32_t>(nn);
+    w.longv = a.take<int32_t>(nn);
     w.scan_tmp = a.take<int32_t>(scan_tmp_entries(nn));
 }
 
@@ -137,43 +138,33 @@ __device__ inline float f64_to_f32_odd(double d) {
 // Eq. 2: one thread per (voxel, VEC consecutive channels).  The points are
 // summed in fp64 -- exact for 16-bit features of ordinary range, so the result
 // does not depend on the order in which they were grouped -- and the mean is
-// rounded once to the storage type.
+// rounded once to the storage type.  A voxel of more than `run` points (a
+// coarse grid near the sensor holds up to ~10^3) would keep one thread on a
+// long chain of dependent loads: its first thread appends it to `longv` (count
+// in h->aux[0]) and k_vox_mean_long sums it with a whole workgroup.
 template <int DT, int VEC>
-__global__ void k_vox_mean(const Header* h, int64_t cap, const int32_t* seg, const int32_t* plist, const void* feat,
-                           int C, void* vfeat) {
-    int64_t m = h->m;
-    if (m > cap) m = cap;
-    const int nch = C / VEC;
-    int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    int64_t vox = t / nch;
-    int ch = (int)(t - vox * nch) * VEC;
-    if (vox >= m) return;
-    int32_t lo = seg[vox], hi = seg[vox + 1];
-    double acc[VEC];
+__device__ inline void mean_add(double (&acc)[VEC], const void* feat, int64_t row) {
+    if constexpr (VEC == 8) {
+        uint4 u = *(const uint4*)((const uint16_t*)feat + row);
+        uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) acc[j] = 0.0;
-    for (int32_t p = lo; p < hi; ++p) {
-        int64_t row = (int64_t)plist[p] * C + ch;
-        if constexpr (VEC == 8) {
-            uint4 u = *(const uint4*)((const uint16_t*)feat + row);
-            uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                acc[2 * j] += (double)from16<DT>(w[j] & 0xFFFF);
-                acc[2 * j + 1] += (double)from16<DT>(w[j] >> 16);
-            }
-        } else if constexpr (VEC == 4) {
-            float4 f = *(const float4*)((const float*)feat + row);
-            acc[0] += (double)f.x;
-            acc[1] += (double)f.y;
-            acc[2] += (double)f.z;
-            acc[3] += (double)f.w;
-        } else {
-            acc[0] += (double)ld_feat<DT>(feat, row);
+        for (int j = 0; j < 4; ++j) {
+            acc[2 * j] += (double)from16<DT>(w[j] & 0xFFFF);
+            acc[2 * j + 1] += (double)from16<DT>(w[j] >> 16);
         }
+    } else if constexpr (VEC == 4) {
+        float4 f = *(const float4*)((const float*)feat + row);
+        acc[0] += (double)f.x;
+        acc[1] += (double)f.y;
+        acc[2] += (double)f.z;
+        acc[3] += (double)f.w;
+    } else {
+        acc[0] += (double)ld_feat<DT>(feat, row);
     }
-    const double N = (double)(hi - lo);
-    int64_t orow = vox * C + ch;
+}
+
+template <int DT, int VEC>
+__device__ inline void mean_store(const double (&acc)[VEC], double N, void* vfeat, int64_t orow) {
     if constexpr (VEC == 8) {
         uint32_t w[4];
 #pragma unroll
@@ -191,9 +182,75 @@ __global__ void k_vox_mean(const Header* h, int64_t cap, const int32_t* seg, con
 }
 
 template <int DT, int VEC>
+__global__ void k_vox_mean(Header* h, int64_t cap, const int32_t* seg, const int32_t* plist, const void* feat,
+                           int C, void* vfeat, int run, int32_t* longv) {
+    int64_t m = h->m;
+    if (m > cap) m = cap;
+    const int nch = C / VEC;
+    int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    int64_t vox = t / nch;
+    int ch = (int)(t - vox * nch) * VEC;
+    if (vox >= m) return;
+    int32_t lo = seg[vox], hi = seg[vox + 1];
+    if (hi - lo > run) {
+        if (ch == 0) longv[atomicAdd((unsigned long long*)&h->aux[0], 1ull)] = (int32_t)vox;
+        return;
+    }
+    double acc[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) acc[j] = 0.0;
+    for (int32_t p = lo; p < hi; ++p) mean_add<DT, VEC>(acc, feat, (int64_t)plist[p] * C + ch);
+    mean_store<DT, VEC>(acc, (double)(hi - lo), vfeat, vox * C + ch);
+}
+
+// the long voxels: thread (slice, chunk) sums every slices-th point of the
+// voxel for one VEC-channel chunk; the slices' partial sums are then added in
+// slice order by the chunk's first thread (fixed order, and exact as above)
+constexpr int kMeanLongThreads = 512;
+template <int DT, int VEC>
+__global__ __launch_bounds__(kMeanLongThreads) void k_vox_mean_long(const Header* h, int64_t cap, const int32_t* seg,
+                                                                    const int32_t* plist, const void* feat, int C,
+                                                                    void* vfeat, const int32_t* longv) {
+    __shared__ double red[kMeanLongThreads][VEC];
+    int64_t nl = h->aux[0];
+    if (nl > cap) nl = cap;
+    const int nch = C / VEC;
+    const int slices = kMeanLongThreads / nch;  // >= 2: the host takes this path only then
+    const int tch = threadIdx.x % nch, sl = threadIdx.x / nch;
+    for (int64_t e = blockIdx.x; e < nl; e += gridDim.x) {
+        const int32_t vox = longv[e];
+        const int32_t lo = seg[vox], hi = seg[vox + 1];
+        double acc[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) acc[j] = 0.0;
+        if (sl < slices)
+            for (int32_t p = lo + sl; p < hi; p += slices) mean_add<DT, VEC>(acc, feat, (int64_t)plist[p] * C + tch * VEC);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) red[threadIdx.x][j] = acc[j];
+        __syncthreads();
+        if (sl == 0) {
+            for (int q = 1; q < slices; ++q)
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) acc[j] += red[q * nch + tch][j];
+            mean_store<DT, VEC>(acc, (double)(hi - lo), vfeat, (int64_t)vox * C + tch * VEC);
+        }
+        __syncthreads();
+    }
+}
+
+constexpr int kMeanRun = 32;  // points a single thread sums
+
+template <int DT, int VEC>
 static void launch_mean(hipStream_t s, const VoxelizeWs& w, int64_t n, const void* feat, int C, void* vfeat) {
-    int64_t threads = n * (C / VEC);
-    k_vox_mean<DT, VEC><<<blocks_for(threads, 256), 256, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat);
+    const int64_t threads = n * (C / VEC);
+    const bool split = C / VEC <= kMeanLongThreads / 2;
+    k_vox_mean<DT, VEC><<<blocks_for(threads, 256), 256, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat,
+                                                                 split ? kMeanRun : INT32_MAX, w.longv);
+    if (split) {
+        const int64_t g = n < 1024 ? (n > 0 ? n : 1) : 1024;
+        k_vox_mean_long<DT, VEC><<<(unsigned)g, kMeanLongThreads, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat,
+                                                                          w.longv);
+    }
 }
 
 void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const int32_t* batch, int64_t n,

@@ -18,8 +18,8 @@ holds the device buffers:
   W_t t (scaled, unshifted) handed as the residual input of W_x x + shift;
   the 1x1 shortcut over it likewise as two linear layers;
 * a devoxelization whose point MLP the fused kernel does not take on matrix
-  cores (C or C_p above 128) runs as a devoxelization plus a linear layer that
-  adds it after the activation.
+  cores (C_p above 128) runs as a devoxelization plus a linear layer that adds
+  it after the activation.
 Layer names and widths follow ``synth.spvcnn_params``.
 """
 from __future__ import annotations
@@ -56,8 +56,18 @@ class SPVCNN:
         self.v = voxel_size
         self.mode = mode
         self.device = device
+        # the input channels are padded with zeros to a multiple of 8 (the matrix cores' K
+        # granularity is 8 16-bit values per lane): the stem conv and the first point MLP get
+        # zero weight rows for them, which adds exact zeros
+        self.c_in = params["stem.0"][0].shape[1]
+        self.c_pad = self.c_in if self.dt == torch.float32 else (self.c_in + 7) // 8 * 8
         self.P = {}
         for name, (W, sc, sh) in params.items():
+            if name in ("stem.0", "point.0") and self.c_pad != self.c_in:
+                W = np.asarray(W)
+                pad = [(0, 0)] * W.ndim
+                pad[-2] = (0, self.c_pad - self.c_in)
+                W = np.pad(W, pad)
             self.P[name] = (self._dev(W), None if sc is None else torch.from_numpy(np.asarray(sc)).to(device),
                             None if sh is None else torch.from_numpy(np.asarray(sh)).to(device))
         self.ws = None
@@ -128,7 +138,8 @@ class SPVCNN:
     def _fuse(self, plan, vfeat, s, z, name, xyz, batch):
         W, sc, sh = self.P[name]
         C, Cp = vfeat.shape[1], z.shape[1]
-        fused = self.dt != torch.float32 and C % 16 == 0 and C // 16 in (1, 2, 4, 6, 8) and Cp % 8 == 0 and Cp <= 128
+        fused = self.dt != torch.float32 and C % 16 == 0 and C // 16 in (1, 2, 4, 6, 8, 16) and Cp % 8 == 0 and \
+            Cp <= 128
         if fused:
             return spv.spv_devoxelize(self.ws, plan.coords[s], vfeat, xyz, self.v, s, self.mode, batch, pfeat=z, Wp=W,
                                       scale_p=sc, shift_p=sh, relu_p=True)
@@ -142,6 +153,10 @@ class SPVCNN:
     # -- forward -------------------------------------------------------------
     def forward(self, xyz: torch.Tensor, feat: torch.Tensor, batch: Optional[torch.Tensor] = None,
                 trace: Optional[dict] = None) -> torch.Tensor:
+        if feat.shape[1] != self.c_pad:
+            f = torch.zeros((feat.shape[0], self.c_pad), dtype=feat.dtype, device=feat.device)
+            f[:, : feat.shape[1]] = feat
+            feat = f
         plan, vox = self.plan(xyz, batch, feat)
         m = plan.m
         x = vox.vfeat[: m[0]]

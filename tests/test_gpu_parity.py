@@ -154,6 +154,18 @@ def test_voxelize_mean_bit_exact(spv, sweep, dtype):
     np.testing.assert_array_equal(vf, rvf)
 
 
+@pytest.mark.parametrize("dtype,C", [("bf16", 256), ("bf16", 8), ("f16", 96), ("f32", 12), ("bf16", 5)])
+def test_voxelize_coarse_long_runs(spv, sweep, dtype, C):
+    """At 0.8 m voxels a sweep's voxels hold up to ~10^3 points; those over 32 are summed
+    by a whole workgroup (point slices, then the slices in order).  The fp64 sums are
+    exact for these features, so the means still match the oracle bit for bit."""
+    feat = synth.normal((len(sweep), C), 1012, dtype=dtype)
+    _, vf, cnt, _, _ = run_voxelize(spv, sweep, 0.8, feat, dtype)
+    assert cnt.max() > 500 and (cnt > 32).sum() > 100
+    _, rvf, _, _ = oracle.voxelize(sweep, 0.8, feat, dtype)
+    np.testing.assert_array_equal(vf, rvf)
+
+
 def test_voxelize_wide_keys(spv):
     """Coordinates spanning nearly the whole key range (48 significant bits once
     compacted): the sort's passes past 32 bits run."""
@@ -318,7 +330,8 @@ def run_conv(spv, x, off, pairs, W, m_out, dtype, scale=None, shift=None, relu=F
                                                (24, 48, "bf16", False), (128, 256, "bf16", True),
                                                (32, 64, "bf16", True), (64, 128, "f16", False),
                                                (128, 64, "bf16", True), (96, 32, "bf16", False),
-                                               (128, 128, "bf16", True), (64, 96, "f16", True)])
+                                               (128, 128, "bf16", True), (64, 96, "f16", True),
+                                               (256, 256, "bf16", True), (192, 256, "f16", False)])
 def test_conv_submanifold_sweep(spv, sweep, cin, cout, dtype, bn):
     rc, _, _, _ = oracle.voxelize(sweep[::3] if cout >= 256 else sweep, 0.05)
     _, off, pairs = oracle.kernel_map(rc)
@@ -330,15 +343,16 @@ def test_conv_submanifold_sweep(spv, sweep, cin, cout, dtype, bn):
     check_close(got, ref, dtype)
 
 
-def test_conv_strided_and_transposed_sweep(spv, sweep):
+@pytest.mark.parametrize("c0,c1", [(64, 128), (256, 256)])
+def test_conv_strided_and_transposed_sweep(spv, sweep, c0, c1):
     rc, _, _, _ = oracle.voxelize(sweep, 0.05)
     oc, off, pairs = oracle.kernel_map(rc, 2, 2)
-    x = synth.normal((len(rc), 64), 1006, dtype="bf16")
-    W = synth.conv_weight(8, 64, 128, 1007, "bf16")
+    x = synth.normal((len(rc), c0), 1006, dtype="bf16")
+    W = synth.conv_weight(8, c0, c1, 1007, "bf16")
     got = run_conv(spv, x, off, pairs, W, len(oc), "bf16")
     ref = oracle.sparse_conv(x, off, pairs, W, len(oc), "bf16")
     check_close(got, ref, "bf16")
-    WT = synth.conv_weight(8, 128, 64, 1008, "bf16")
+    WT = synth.conv_weight(8, c1, c0, 1008, "bf16")
     gotT = run_conv(spv, ref, off, pairs, WT, len(rc), "bf16", transposed=True)
     refT = oracle.sparse_conv(ref, off, pairs, WT, len(rc), "bf16", transposed=True)
     check_close(gotT, refT, "bf16")
@@ -475,7 +489,8 @@ def test_devox_sweep(spv, sweep, mode, dtype, C):
     check_close(host(out, dtype)[:len(pts)], rout, dtype)
 
 
-@pytest.mark.parametrize("C,Cp,n", [(16, 0, 1000), (64, 24, 3001), (128, 128, 2047), (256, 96, 1500), (32, 8, 1)])
+@pytest.mark.parametrize("C,Cp,n", [(16, 0, 1000), (64, 24, 3001), (128, 128, 2047), (256, 96, 1500), (32, 8, 1),
+                                    (256, 0, 5000), (256, 32, 4097), (256, 128, 3000), (256, 200, 999)])
 def test_devox_shapes(spv, C, Cp, n):
     """Channel widths with and without a point branch, partial 32-channel slabs
     of the point MLP, widths past the matrix-core kernel and ragged point counts."""
@@ -495,13 +510,14 @@ def test_devox_shapes(spv, C, Cp, n):
     check_close(host(out, "bf16")[:n], ref, "bf16")
 
 
-def test_devox_coarse_grid(spv, sweep):
+@pytest.mark.parametrize("C", [32, 256])
+def test_devox_coarse_grid(spv, sweep, C):
     pts = sweep[::4]
     rc, _, _, _ = oracle.voxelize(pts, 0.05)
     c1, _, _ = oracle.kernel_map(rc, 2, 2)
     c2, _, _ = oracle.kernel_map(c1, 2, 2)
-    vf = synth.normal((len(c2), 32), 31, dtype="bf16")
-    ws = spv.Workspace.for_ops(len(pts), 32)
+    vf = synth.normal((len(c2), C), 31, dtype="bf16")
+    ws = spv.Workspace.for_ops(len(pts), C)
     out = spv.spv_devoxelize(ws, dev(c2), dev(vf, "bf16"), dev(pts), 0.05, stride_log2=2)
     rout = oracle.devoxelize(c2, vf, pts, 0.05, stride_log2=2, dtype="bf16")
     check_close(host(out, "bf16")[:len(pts)], rout, "bf16")
@@ -653,7 +669,8 @@ def test_block_graph_replay(spv, sweep):
 # pointwise linear layer and the split of a conv over concatenated inputs
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("cin,cout,dtype", [(32, 64, "bf16"), (96, 256, "bf16"), (256, 128, "f16"),
-                                            (128, 96, "bf16"), (8, 16, "bf16"), (96, 19, "bf16"), (40, 24, "f32")])
+                                            (128, 96, "bf16"), (8, 16, "bf16"), (96, 19, "bf16"), (32, 7, "f16"),
+                                            (96, 40, "bf16"), (12, 16, "bf16"), (40, 24, "f32")])
 @pytest.mark.parametrize("mode", ["plain", "res_before", "res_after"])
 def test_linear(spv, cin, cout, dtype, mode):
     """Rows past the live count (m_dev < m_cap) are left alone; 16-row blocks with a ragged tail."""
