@@ -53,11 +53,15 @@ def lib():
                                       vp, i32, vp, vp]
         L.spvo_block.argtypes = [vp, vp, vp, i64, vp, vp, vp]
         L.spvo_linear.argtypes = [vp, i64, i32, vp, vp, vp, vp, i32, i32, vp, i32, i32]
+        L.spvo_sparse_conv_wgrad.argtypes = [vp, i64, i32, vp, i64, i32, vp, vp, i32, i32, vp, i32]
+        L.spvo_voxelize_backward.argtypes = [vp, i64, i32, vp, vp, i64, vp, i32]
+        L.spvo_devoxelize_backward.argtypes = [vp, vp, vp, i64, i32, vp, i64, i32]
         L.spvo_decode.argtypes = [vp, i64, i32]
         L.spvo_decode.restype = ct.c_double
         L.spvo_round_store.argtypes = [ct.c_double, vp, i64, i32]
         for f in ("spvo_voxelize", "spvo_kernel_map", "spvo_sparse_conv", "spvo_sparse_conv_res", "spvo_devoxelize",
-                  "spvo_block", "spvo_linear"):
+                  "spvo_block", "spvo_linear", "spvo_sparse_conv_wgrad", "spvo_voxelize_backward",
+                  "spvo_devoxelize_backward"):
             getattr(L, f).restype = ct.c_int
         _lib = L
     return _lib
@@ -150,6 +154,53 @@ def sparse_conv_sliced(x, off, pairs, W_full, m_out, Cout, dtype="f32", scale=No
     return sparse_conv(x, off, pairs, W_full[:, :Cin, :Cout], m_out, dtype,
                        None if scale is None else np.asarray(scale)[:Cout],
                        None if shift is None else np.asarray(shift)[:Cout], relu, transposed)
+
+
+def conv_dgrad(dy, off, pairs, W, m_in, dtype="f32", transposed=False):
+    """Input gradient of a sparse conv: dx[i] = sum over the pairs (i, j, k) of dy[j] @ W[k]^T --
+    the same map with the roles of each pair swapped and every W[k] transposed."""
+    WT = np.ascontiguousarray(np.asarray(W).transpose(0, 2, 1))
+    return sparse_conv(dy, off, pairs, WT, m_in, dtype, transposed=not transposed)
+
+
+def conv_wgrad(x, dy, off, pairs, K3, dtype="f32", transposed=False):
+    """Weight gradient of a sparse conv: dW[k] = sum over the pairs (i, j) of offset k of
+    x[i]^T dy[j]; float32 [K3][Cin][Cout]."""
+    x = np.ascontiguousarray(x, dtype=_sdt(dtype))
+    dy = np.ascontiguousarray(dy, dtype=_sdt(dtype))
+    off = np.ascontiguousarray(off, dtype=np.int32)
+    pairs = np.ascontiguousarray(pairs, dtype=np.int32).reshape(-1, 2)
+    dW = np.zeros((K3, x.shape[1], dy.shape[1]), np.float32)
+    st = lib().spvo_sparse_conv_wgrad(_p(x), x.shape[0], x.shape[1], _p(dy), dy.shape[0], dy.shape[1], _p(off),
+                                      _p(pairs), K3, int(transposed), _p(dW), DT[dtype])
+    _chk(st, "conv_wgrad")
+    return dW
+
+
+def voxelize_backward(dv, counts, pt2vox, dtype="f32"):
+    """Backward of the scatter-mean (Eq. 2): dfeat[k] = dv[pt2vox[k]] / N_{pt2vox[k]}."""
+    dv = np.ascontiguousarray(dv, dtype=_sdt(dtype))
+    counts = np.ascontiguousarray(counts, dtype=np.int32)
+    pt2vox = np.ascontiguousarray(pt2vox, dtype=np.int32)
+    m, C = dv.shape
+    n = len(pt2vox)
+    out = np.zeros((max(n, 1), C), _sdt(dtype))
+    st = lib().spvo_voxelize_backward(_p(dv), m, C, _p(counts), _p(pt2vox), n, _p(out), DT[dtype])
+    _chk(st, "voxelize_backward")
+    return out[:n]
+
+
+def devoxelize_backward(corner_idx, corner_w, dout, m, dtype="f32"):
+    """Backward of the renormalized trilinear devoxelization w.r.t. the voxel features
+    (float32 [m][C]), from devoxelize's corner indices and raw weights."""
+    ci = np.ascontiguousarray(corner_idx, dtype=np.int32)
+    cw = np.ascontiguousarray(corner_w, dtype=np.float32)
+    dout = np.ascontiguousarray(dout, dtype=_sdt(dtype))
+    n, C = dout.shape
+    dv = np.zeros((max(m, 1), C), np.float32)
+    st = lib().spvo_devoxelize_backward(_p(ci), _p(cw), _p(dout), n, C, _p(dv), m, DT[dtype])
+    _chk(st, "devoxelize_backward")
+    return dv[:m]
 
 
 def linear(x, W, dtype="f32", scale=None, shift=None, relu=False, res=None, res_after_act=False):

@@ -404,6 +404,91 @@ int spvo_sparse_conv(const void* in, int64_t m_in, int32_t Cin,
 }
 
 /* ------------------------------------------------------------------------- */
+/* backward passes                                                            */
+/* ------------------------------------------------------------------------- */
+
+/* weight gradient of a sparse conv: dW[k] = sum over the pairs (i, j) of offset
+ * k of x[i]^T dy[j] (roles of the pair swapped with transposed = 1); fp64
+ * accumulation in pair order, one rounding to float32 */
+int spvo_sparse_conv_wgrad(const void* x, int64_t m_in, int32_t Cin, const void* dy, int64_t m_out, int32_t Cout,
+                           const int32_t* off, const int32_t* pairs, int32_t K3, int32_t transposed, float* dW,
+                           int32_t dtype) {
+    if (m_in < 0 || m_out < 0 || Cin <= 0 || Cout <= 0 || !off || !dW || !valid_dtype(dtype))
+        return SPVO_ERR_INVALID_ARG;
+    if (!(K3 == 27 || K3 == 8)) return SPVO_ERR_UNSUPPORTED;
+    for (int k = 0; k < K3; ++k)
+        if (off[k] > off[k + 1] || off[0] != 0) return SPVO_ERR_INVALID_ARG;
+    const int64_t total = off[K3];
+    if (total > 0 && (!pairs || !x || !dy)) return SPVO_ERR_INVALID_ARG;
+    double* acc = (double*)calloc((size_t)Cin * Cout, sizeof(double));
+    if (!acc) return SPVO_ERR_CAPACITY;
+    for (int k = 0; k < K3; ++k) {
+        for (int64_t t = 0; t < (int64_t)Cin * Cout; ++t) acc[t] = 0.0;
+        for (int64_t p = off[k]; p < off[k + 1]; ++p) {
+            const int64_t i = transposed ? pairs[2 * p + 1] : pairs[2 * p];
+            const int64_t j = transposed ? pairs[2 * p] : pairs[2 * p + 1];
+            if (i < 0 || i >= m_in || j < 0 || j >= m_out) {
+                free(acc);
+                return SPVO_ERR_INVALID_ARG;
+            }
+            for (int32_t ci = 0; ci < Cin; ++ci) {
+                const double xv = spvo_decode(x, i * Cin + ci, dtype);
+                for (int32_t co = 0; co < Cout; ++co) acc[(int64_t)ci * Cout + co] += xv * spvo_decode(dy, j * Cout + co, dtype);
+            }
+        }
+        for (int64_t t = 0; t < (int64_t)Cin * Cout; ++t) dW[(int64_t)k * Cin * Cout + t] = (float)acc[t];
+    }
+    free(acc);
+    return SPVO_OK;
+}
+
+/* backward of the scatter-mean (Eq. 2): every point receives its voxel's
+ * gradient divided by the voxel's point count N_m; one rounding */
+int spvo_voxelize_backward(const void* dv, int64_t m, int32_t C, const int32_t* counts, const int32_t* pt2vox,
+                           int64_t n, void* dfeat, int32_t dtype) {
+    if (m < 0 || n < 0 || C <= 0 || !valid_dtype(dtype)) return SPVO_ERR_INVALID_ARG;
+    if (n > 0 && (!pt2vox || !dfeat || !counts || !dv)) return SPVO_ERR_INVALID_ARG;
+    for (int64_t k = 0; k < n; ++k) {
+        const int64_t v = pt2vox[k];
+        if (v < 0 || v >= m || counts[v] <= 0) return SPVO_ERR_INVALID_ARG;
+        for (int32_t c = 0; c < C; ++c)
+            spvo_round_store(spvo_decode(dv, v * C + c, dtype) / (double)counts[v], dfeat, k * C + c, dtype);
+    }
+    return SPVO_OK;
+}
+
+/* backward of the trilinear devoxelization w.r.t. the voxel features: point k
+ * scatters dout[k] times the weight its corner c had -- the raw weight over the
+ * sum of the present corners' raw weights -- to voxel idx[k][c]; fp64 sums,
+ * one rounding to float32 */
+int spvo_devoxelize_backward(const int32_t* cidx, const float* cw, const void* dout, int64_t n, int32_t C, float* dv,
+                             int64_t m, int32_t dtype) {
+    if (n < 0 || m < 0 || C <= 0 || !valid_dtype(dtype) || (m > 0 && !dv)) return SPVO_ERR_INVALID_ARG;
+    if (n > 0 && (!cidx || !cw || !dout)) return SPVO_ERR_INVALID_ARG;
+    double* acc = (double*)calloc((size_t)(m > 0 ? m : 1) * C, sizeof(double));
+    if (!acc) return SPVO_ERR_CAPACITY;
+    for (int64_t k = 0; k < n; ++k) {
+        double den = 0.0;
+        for (int c = 0; c < 8; ++c)
+            if (cidx[8 * k + c] >= 0) den += (double)cw[8 * k + c];
+        if (den <= 0.0) continue;
+        for (int c = 0; c < 8; ++c) {
+            const int64_t v = cidx[8 * k + c];
+            if (v < 0) continue;
+            if (v >= m) {
+                free(acc);
+                return SPVO_ERR_INVALID_ARG;
+            }
+            const double w = (double)cw[8 * k + c] / den;
+            for (int32_t ch = 0; ch < C; ++ch) acc[v * C + ch] += w * spvo_decode(dout, k * C + ch, dtype);
+        }
+    }
+    for (int64_t t = 0; t < m * C; ++t) dv[t] = (float)acc[t];
+    free(acc);
+    return SPVO_OK;
+}
+
+/* ------------------------------------------------------------------------- */
 /* pointwise linear layer                                                     */
 /* ------------------------------------------------------------------------- */
 

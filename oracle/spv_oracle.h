@@ -79,6 +79,18 @@ int spvo_sparse_conv_res(const void* in, int64_t m_in, int32_t Cin,
                          const void* W, const float* scale, const float* shift, const void* res, int32_t relu,
                          void* out, int64_t m_out, int32_t Cout, int32_t dtype);
 
+/* Backward passes.  Weight gradient of a sparse conv (float32 dW [K3][Cin][Cout]),
+ * the scatter-mean's backward (dfeat[k] = dv[pt2vox[k]] / N), and the
+ * devoxelization's backward w.r.t. the voxel features (float32 dv [m][C]) from the
+ * corner indices / raw weights that spvo_devoxelize reports. */
+int spvo_sparse_conv_wgrad(const void* x, int64_t m_in, int32_t Cin, const void* dy, int64_t m_out, int32_t Cout,
+                           const int32_t* off, const int32_t* pairs, int32_t K3, int32_t transposed, float* dW,
+                           int32_t dtype);
+int spvo_voxelize_backward(const void* dv, int64_t m, int32_t C, const int32_t* counts, const int32_t* pt2vox,
+                           int64_t n, void* dfeat, int32_t dtype);
+int spvo_devoxelize_backward(const int32_t* cidx, const float* cw, const void* dout, int64_t n, int32_t C, float* dv,
+                             int64_t m, int32_t dtype);
+
 /* Pointwise linear layer: out[i] = act(scale * (in[i] @ W) + shift + res[i]) with
  * res_after_act = 0, act(scale * (in[i] @ W) + shift) + res[i] with 1.  W is
  * [Cin][Cout] (storage dtype); scale/shift f32 [Cout] or NULL; res [m][Cout] or NULL. */
