@@ -187,6 +187,77 @@ spv_status spv_sparse_conv_sliced(void* stream, void* ws, size_t ws_bytes,
                                   spv_dtype dt);
 
 /*
+ * Backward passes (training, Sec. 4.2 trains the super network end to end).
+ *
+ * spv_sparse_conv_dgrad -- input gradient of spv_sparse_conv (without its
+ * scale / shift / activation, whose backward is elementwise):
+ *   dx[i] = sum over the pairs (i, j, k) of dy[j] @ W[k]^T
+ * i.e. the conv over the same map with every pair's roles swapped and each W[k]
+ * read transposed in place, on the same kernels.
+ * In:  dy [dy_rows][Cout] (dt); off / pairs / pair_cap / K3 / transposed: the
+ *      map and flag of the forward call; W [K3][Cin][Cout] (dt), the forward
+ *      weights.
+ * Out: dx [m_in_cap][Cin] (dt); rows < *m_in_dev (NULL = m_in_cap) are written.
+ * Errors: as spv_sparse_conv.
+ */
+spv_status spv_sparse_conv_dgrad(void* stream, void* ws, size_t ws_bytes,
+                                 const void* dy, int64_t dy_rows, int32_t Cout,
+                                 const int32_t* off, const int32_t* pairs, int64_t pair_cap,
+                                 int32_t K3, int32_t transposed, const void* W,
+                                 void* dx, const int64_t* m_in_dev, int64_t m_in_cap, int32_t Cin,
+                                 spv_dtype dt);
+
+/*
+ * spv_sparse_conv_wgrad -- weight gradient of spv_sparse_conv:
+ *   dW[k] = sum over the pairs (i, j) of offset k of x[i]^T dy[j]
+ * (roles of each pair swapped with transposed = 1); fp32 accumulation.  The
+ * result is deterministic: fixed slices of every offset's pairs are summed
+ * separately and the slices added in order.
+ * In:  x [x_rows][Cin], dy [dy_rows][Cout] (dt, 16-byte aligned); the map of
+ *      the forward call; pairs past pair_cap or with rows outside x / dy are
+ *      ignored.
+ * Out: dW [K3][Cin][Cout] float32.
+ * bf16/f16 with Cin % 16 == 0 and Cout % 16 == 0 run on MFMA; other shapes and
+ * f32 on a vector-ALU kernel.  Cin * Cout <= 65536.  The workspace holds the
+ * slices' partial sums: spv_wgrad_workspace_bytes(K3, Cin, Cout) bytes
+ * (K3 * S * Cin * Cout * 4 with S = 32, 16 or 8 as Cin * Cout grows).
+ * Errors: SPV_ERR_INVALID_ARG, SPV_ERR_UNSUPPORTED (K3, Cin * Cout),
+ *      SPV_ERR_CAPACITY (ws too small).
+ */
+size_t spv_wgrad_workspace_bytes(int32_t K3, int32_t Cin, int32_t Cout);
+spv_status spv_sparse_conv_wgrad(void* stream, void* ws, size_t ws_bytes,
+                                 const void* x, int64_t x_rows, int32_t Cin,
+                                 const void* dy, int64_t dy_rows, int32_t Cout,
+                                 const int32_t* off, const int32_t* pairs, int64_t pair_cap,
+                                 int32_t K3, int32_t transposed, float* dW, spv_dtype dt);
+
+/*
+ * spv_voxelize_backward -- backward of the scatter-mean (Eq. 2):
+ *   dfeat[k] = dvfeat[v] / N_v,  v = pt2vox[k]   (0 where v < 0 or v >= m)
+ * fp64 quotient, one rounding to dt.  No workspace.
+ * In:  dvfeat [m][C] (dt); counts [m] and pt2vox [n] from spv_voxelize.
+ * Out: dfeat [n][C] (dt).
+ */
+spv_status spv_voxelize_backward(void* stream, const void* dvfeat, int64_t m, int32_t C,
+                                 const int32_t* counts, const int32_t* pt2vox, int64_t n,
+                                 void* dfeat, spv_dtype dt);
+
+/*
+ * spv_devoxelize_backward -- backward of the trilinear devoxelization w.r.t.
+ * the voxel features (Sec. 3.3 "Sparse Devoxelization"): point k adds
+ * dout[k] * w_c / sum of the present corners' w to voxel corner_idx[k][c] for
+ * each present corner c (w = the raw trilinear weights).  dvfeat is zeroed
+ * first.  fp32 atomic accumulation: the last bits depend on the order of the
+ * additions.  No workspace.
+ * In:  corner_idx [n][8], corner_w [n][8] as spv_devoxelize reports them;
+ *      dout [n][C] (dt).
+ * Out: dvfeat [m][C] float32.
+ */
+spv_status spv_devoxelize_backward(void* stream, const int32_t* corner_idx, const float* corner_w,
+                                   const void* dout, int64_t n, int32_t C, float* dvfeat, int64_t m,
+                                   spv_dtype dt);
+
+/*
  * spv_linear -- a pointwise linear layer on feature rows:
  *   res_after_act = 0:  out[i] = act(scale * (in[i] @ W) + shift + res[i])
  *   res_after_act = 1:  out[i] = act(scale * (in[i] @ W) + shift) + res[i]

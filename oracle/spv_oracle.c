@@ -421,25 +421,30 @@ int spvo_sparse_conv_wgrad(const void* x, int64_t m_in, int32_t Cin, const void*
     const int64_t total = off[K3];
     if (total > 0 && (!pairs || !x || !dy)) return SPVO_ERR_INVALID_ARG;
     double* acc = (double*)calloc((size_t)Cin * Cout, sizeof(double));
-    if (!acc) return SPVO_ERR_CAPACITY;
-    for (int k = 0; k < K3; ++k) {
+    double* xr = (double*)malloc((size_t)Cin * sizeof(double));
+    double* gr = (double*)malloc((size_t)Cout * sizeof(double));
+    int st = (acc && xr && gr) ? SPVO_OK : SPVO_ERR_CAPACITY;
+    for (int k = 0; k < K3 && st == SPVO_OK; ++k) {
         for (int64_t t = 0; t < (int64_t)Cin * Cout; ++t) acc[t] = 0.0;
         for (int64_t p = off[k]; p < off[k + 1]; ++p) {
             const int64_t i = transposed ? pairs[2 * p + 1] : pairs[2 * p];
             const int64_t j = transposed ? pairs[2 * p] : pairs[2 * p + 1];
             if (i < 0 || i >= m_in || j < 0 || j >= m_out) {
-                free(acc);
-                return SPVO_ERR_INVALID_ARG;
+                st = SPVO_ERR_INVALID_ARG;
+                break;
             }
-            for (int32_t ci = 0; ci < Cin; ++ci) {
-                const double xv = spvo_decode(x, i * Cin + ci, dtype);
-                for (int32_t co = 0; co < Cout; ++co) acc[(int64_t)ci * Cout + co] += xv * spvo_decode(dy, j * Cout + co, dtype);
-            }
+            /* the pair's two rows, decoded once */
+            for (int32_t ci = 0; ci < Cin; ++ci) xr[ci] = spvo_decode(x, i * Cin + ci, dtype);
+            for (int32_t co = 0; co < Cout; ++co) gr[co] = spvo_decode(dy, j * Cout + co, dtype);
+            for (int32_t ci = 0; ci < Cin; ++ci)
+                for (int32_t co = 0; co < Cout; ++co) acc[(int64_t)ci * Cout + co] += xr[ci] * gr[co];
         }
         for (int64_t t = 0; t < (int64_t)Cin * Cout; ++t) dW[(int64_t)k * Cin * Cout + t] = (float)acc[t];
     }
     free(acc);
-    return SPVO_OK;
+    free(xr);
+    free(gr);
+    return st;
 }
 
 /* backward of the scatter-mean (Eq. 2): every point receives its voxel's

@@ -181,8 +181,16 @@ size_t spv_workspace_bytes(int64_t max_points, int32_t max_C) {
     s = std::max(s, layout_conv(nullptr, 0, max_points, 27, max_C, max_C, SPV_BF16, c));
     void* wl = nullptr;
     s = std::max(s, layout_linear(nullptr, 0, max_C, max_C, &wl));
+
     s = std::max(s, layout_devox(nullptr, 0, max_points, max_points, max_C, max_C, d));
     return s;
+}
+
+size_t spv_wgrad_workspace_bytes(int32_t K3, int32_t Cin, int32_t Cout) {
+    if (K3 <= 0 || Cin <= 0 || Cout <= 0) return 0;
+    Arena a(nullptr, 0);
+    plan_wgrad_ws(a, K3, Cin, Cout);
+    return a.used;
 }
 
 size_t spv_block_workspace_bytes(int64_t max_points, int32_t C) {
@@ -277,15 +285,19 @@ spv_status spv_kernel_map(void* stream, void* ws, size_t ws_bytes, const int32_t
     return st;
 }
 
-// Cin_full / Cout_full: W's stored shape [K3][Cin_full][Cout_full], of which the
-// leading Cin x Cout block of every offset is used
+// W[k][c][col] (c < Cin, col < Cout) at W[k * ldk + c * ldc + col * ldcol]
+struct WStrides {
+    int ldc, ldcol;
+    int64_t ldk;
+};
+
 static spv_status sparse_conv_call(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows,
                                    int32_t Cin, const int32_t* off, const int32_t* pairs, int64_t pair_cap, int32_t K3,
-                                   int32_t transposed, const void* W, int32_t Cin_full, int32_t Cout_full,
-                                   const float* scale, const float* shift, const void* res, int32_t relu, void* out,
+                                   int32_t transposed, const void* W, WStrides wst, const float* scale,
+                                   const float* shift, const void* res, int32_t relu, void* out,
                                    const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
     if (!ws || in_rows < 0 || m_out_cap < 0 || m_out_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !off ||
-        !W || pair_cap < 0 || !valid_dt(dt) || Cin > Cin_full || Cout > Cout_full)
+        !W || pair_cap < 0 || !valid_dt(dt))
         return SPV_ERR_INVALID_ARG;
     if (!(K3 == 27 || K3 == 8)) return SPV_ERR_UNSUPPORTED;
     if ((in_rows > 0 && !in) || (m_out_cap > 0 && !out) || (pair_cap > 0 && !pairs)) return SPV_ERR_INVALID_ARG;
@@ -298,16 +310,18 @@ static spv_status sparse_conv_call(void* stream, void* ws, size_t ws_bytes, cons
     hipStream_t s = (hipStream_t)stream;
     L.p.m_out_dev = m_out_dev;
     L.p.res = res;
-    L.p.w_ldc = Cout_full;
-    L.p.w_ldk = (int64_t)Cin_full * Cout_full;
-    // A transposed map gives an output few of the 27 offsets (a transposed
-    // stride-2 map at most 8, 2-3 on a sweep), which the neighbour-table kernel
-    // would still step through for every block: the tile kernel, which only
-    // visits pairs, takes it.
-    if (transposed) L.p.use_union = 0;
+    L.p.w_ldc = wst.ldc;
+    L.p.w_ldcol = wst.ldcol;
+    L.p.w_ldk = wst.ldk;
+    // A transposed stride-2 map gives an output few of the 27 offsets (at most
+    // 8, 2-3 on a sweep), which the neighbour-table kernel would still step
+    // through for every block: the tile kernel, which only visits pairs, takes
+    // it.  A transposed map with as many inputs as outputs (a submanifold map
+    // read backwards, as in the input gradient) is as dense as the forward one.
+    if (transposed && in_rows != m_out_cap) L.p.use_union = 0;
     // the plan clears the status header first and packs W in one of its launches
     launch_conv_plan(s, L.p, off, pairs, K3, transposed, pair_cap, in_rows,
-                     conv_pack_job(K3, W, L.wpack, Cin, Cout, dt, L.p.w_ldc, L.p.w_ldk), true);
+                     conv_pack_job(K3, W, L.wpack, Cin, Cout, dt, wst.ldc, wst.ldk, wst.ldcol), true);
     launch_conv_run(s, L.p, in, Cin, in_rows, pairs, pair_cap, transposed, W, L.wpack, scale, shift, relu, out, Cout,
                     dt);
     return hip_check();
@@ -317,8 +331,9 @@ spv_status spv_sparse_conv(void* stream, void* ws, size_t ws_bytes, const void* 
                            const int32_t* off, const int32_t* pairs, int64_t pair_cap, int32_t K3, int32_t transposed,
                            const void* W, const float* scale, const float* shift, int32_t relu, void* out,
                            const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
-    return sparse_conv_call(stream, ws, ws_bytes, in, in_rows, Cin, off, pairs, pair_cap, K3, transposed, W, Cin, Cout,
-                            scale, shift, nullptr, relu, out, m_out_dev, m_out_cap, Cout, dt);
+    return sparse_conv_call(stream, ws, ws_bytes, in, in_rows, Cin, off, pairs, pair_cap, K3, transposed, W,
+                            WStrides{Cout, 1, (int64_t)Cin * Cout}, scale, shift, nullptr, relu, out, m_out_dev,
+                            m_out_cap, Cout, dt);
 }
 
 spv_status spv_sparse_conv_sliced(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows,
@@ -326,8 +341,55 @@ spv_status spv_sparse_conv_sliced(void* stream, void* ws, size_t ws_bytes, const
                                   int32_t transposed, const void* W, int32_t Cin_full, int32_t Cout_full,
                                   const float* scale, const float* shift, const void* res, int32_t relu, void* out,
                                   const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
-    return sparse_conv_call(stream, ws, ws_bytes, in, in_rows, Cin, off, pairs, pair_cap, K3, transposed, W, Cin_full,
-                            Cout_full, scale, shift, res, relu, out, m_out_dev, m_out_cap, Cout, dt);
+    if (Cin > Cin_full || Cout > Cout_full) return SPV_ERR_INVALID_ARG;
+    return sparse_conv_call(stream, ws, ws_bytes, in, in_rows, Cin, off, pairs, pair_cap, K3, transposed, W,
+                            WStrides{Cout_full, 1, (int64_t)Cin_full * Cout_full}, scale, shift, res, relu, out,
+                            m_out_dev, m_out_cap, Cout, dt);
+}
+
+spv_status spv_sparse_conv_dgrad(void* stream, void* ws, size_t ws_bytes, const void* dy, int64_t dy_rows,
+                                 int32_t Cout, const int32_t* off, const int32_t* pairs, int64_t pair_cap, int32_t K3,
+                                 int32_t transposed, const void* W, void* dx, const int64_t* m_in_dev, int64_t m_in_cap,
+                                 int32_t Cin, spv_dtype dt) {
+    // dx[i] = sum over the pairs (i, j, k) of dy[j] @ W[k]^T: the conv over the
+    // same map with each pair's roles swapped, reading W[k] transposed in place
+    return sparse_conv_call(stream, ws, ws_bytes, dy, dy_rows, Cout, off, pairs, pair_cap, K3, transposed ? 0 : 1, W,
+                            WStrides{1, Cout, (int64_t)Cin * Cout}, nullptr, nullptr, nullptr, 0, dx, m_in_dev,
+                            m_in_cap, Cin, dt);
+}
+
+spv_status spv_sparse_conv_wgrad(void* stream, void* ws, size_t ws_bytes, const void* x, int64_t x_rows, int32_t Cin,
+                                 const void* dy, int64_t dy_rows, int32_t Cout, const int32_t* off, const int32_t* pairs,
+                                 int64_t pair_cap, int32_t K3, int32_t transposed, float* dW, spv_dtype dt) {
+    if (!ws || x_rows < 0 || dy_rows < 0 || Cin <= 0 || Cout <= 0 || !off || !dW || pair_cap < 0 || !valid_dt(dt))
+        return SPV_ERR_INVALID_ARG;
+    if (!(K3 == 27 || K3 == 8) || !wgrad_supported(Cin, Cout)) return SPV_ERR_UNSUPPORTED;
+    if ((x_rows > 0 && !x) || (dy_rows > 0 && !dy) || (pair_cap > 0 && !pairs)) return SPV_ERR_INVALID_ARG;
+    if (!aligned16(x) || !aligned16(dy)) return SPV_ERR_INVALID_ARG;
+    Arena probe(nullptr, 0);
+    plan_wgrad_ws(probe, K3, Cin, Cout);
+    if (need(probe.used, ws_bytes)) return SPV_ERR_CAPACITY;
+    Arena a(ws, ws_bytes);
+    float* partial = (float*)plan_wgrad_ws(a, K3, Cin, Cout);
+    WgradArgs w{x, x_rows, Cin, dy, dy_rows, Cout, off, pairs, pair_cap, K3, transposed ? 1 : 0, (int)dt};
+    launch_wgrad((hipStream_t)stream, w, partial, dW);
+    return hip_check();
+}
+
+spv_status spv_voxelize_backward(void* stream, const void* dvfeat, int64_t m, int32_t C, const int32_t* counts,
+                                 const int32_t* pt2vox, int64_t n, void* dfeat, spv_dtype dt) {
+    if (m < 0 || n < 0 || C <= 0 || !valid_dt(dt)) return SPV_ERR_INVALID_ARG;
+    if (n > 0 && (!dvfeat || !counts || !pt2vox || !dfeat)) return SPV_ERR_INVALID_ARG;
+    launch_voxelize_backward((hipStream_t)stream, dvfeat, C, counts, pt2vox, n, m, dfeat, (int)dt);
+    return hip_check();
+}
+
+spv_status spv_devoxelize_backward(void* stream, const int32_t* corner_idx, const float* corner_w, const void* dout,
+                                   int64_t n, int32_t C, float* dvfeat, int64_t m, spv_dtype dt) {
+    if (m < 0 || n < 0 || C <= 0 || !valid_dt(dt) || (m > 0 && !dvfeat)) return SPV_ERR_INVALID_ARG;
+    if (n > 0 && (!corner_idx || !corner_w || !dout)) return SPV_ERR_INVALID_ARG;
+    launch_devoxelize_backward((hipStream_t)stream, corner_idx, corner_w, dout, n, C, dvfeat, m, (int)dt);
+    return hip_check();
 }
 
 spv_status spv_linear(void* stream, void* ws, size_t ws_bytes, const void* in, const int64_t* m_dev, int64_t m_cap,

@@ -64,10 +64,12 @@ __device__ inline int64_t tile_of(int64_t j, int64_t m, int64_t nt, int T) {
 }
 
 // fragment t of the packing (t = ((k * KCH + kc) * NB + nb) * 64 + lane)
-// W[k][c][col] sits at W[k * ldk + c * ldc + col] (ldc = Cout, ldk = Cin * Cout
-// for a dense [K3][Cin][Cout] tensor; larger for a channel slice of a wider one)
-__device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int Cout, int ldc, int64_t ldk, int KCH, int NB,
-                                     int64_t t) {
+// W[k][c][col] sits at W[k * ldk + c * ldc + col * ldcol] (ldc = Cout, ldcol = 1,
+// ldk = Cin * Cout for a dense [K3][Cin][Cout] tensor; larger ldc / ldk for a
+// channel slice of a wider one; ldc = 1, ldcol = the stored row length to read
+// every W[k] transposed)
+__device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int Cout, int ldc, int ldcol, int64_t ldk, int KCH,
+                                     int NB, int64_t t) {
     const int lane = (int)(t & 63);
     int64_t f = t >> 6;
     const int nb = (int)(f % NB);
@@ -81,8 +83,8 @@ __device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int Cout, int 
         uint32_t lo = 0, hi = 0;
         const int c0 = ci0 + 2 * e, c1 = ci0 + 2 * e + 1;
         // zeros past the last input channel and past the last output column
-        if (c0 < Cin && col < Cout) lo = W[(int64_t)k * ldk + (int64_t)c0 * ldc + col];
-        if (c1 < Cin && col < Cout) hi = W[(int64_t)k * ldk + (int64_t)c1 * ldc + col];
+        if (c0 < Cin && col < Cout) lo = W[(int64_t)k * ldk + (int64_t)c0 * ldc + (int64_t)col * ldcol];
+        if (c1 < Cin && col < Cout) hi = W[(int64_t)k * ldk + (int64_t)c1 * ldc + (int64_t)col * ldcol];
         w[e] = lo | (hi << 16);
     }
     return make_uint4(w[0], w[1], w[2], w[3]);
@@ -91,7 +93,7 @@ __device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int Cout, int 
 // a weight packing run alongside another kernel's work (grid-stride)
 __device__ inline void pack_job_run(const PackJob& q) {
     for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < q.total; t += (int64_t)gridDim.x * blockDim.x)
-        q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.ldc, q.ldk, q.KCH, q.NB, t);
+        q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.ldc, q.ldcol, q.ldk, q.KCH, q.NB, t);
 }
 
 // For every offset k and tile t in [0, nt]: bnd[k][t] = first pair of offset k
@@ -236,7 +238,7 @@ __global__ __launch_bounds__(256) void k_block_prologue(PrologueArgs a) {
     for (int j = 0; j < a.njobs; ++j) {
         const PackJob& q = a.job[j];
         for (int64_t t = t0; t < q.total; t += stride)
-            q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.ldc, q.ldk, q.KCH, q.NB, t);
+            q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.ldc, q.ldcol, q.ldk, q.KCH, q.NB, t);
     }
 }
 
@@ -549,6 +551,7 @@ __global__ __launch_bounds__(256) void k_conv_tile_valu(ConvPlan p, const void* 
     const int isel = transposed ? 1 : 0;
     const int64_t bs = p.ntile_cap + 1;
     const int64_t ldc = p.w_ldc > 0 ? p.w_ldc : Cout, ldk = p.w_ldk > 0 ? p.w_ldk : (int64_t)Cin * Cout;
+    const int64_t ldcol = p.w_ldcol > 0 ? p.w_ldcol : 1;
     for (int k = 0; k < K3; ++k) {
         int64_t lo = p.bnd[k * bs + t], hi = p.bnd[k * bs + t + 1];
         lo = lo < 0 ? 0 : (lo > pair_bound ? pair_bound : lo);
@@ -559,7 +562,7 @@ __global__ __launch_bounds__(256) void k_conv_tile_valu(ConvPlan p, const void* 
             if (!cok || o < 0 || o >= rows || i < 0 || i >= in_rows) continue;
             float s = 0.f;
             for (int ci = 0; ci < Cin; ++ci)
-                s += ld_feat<DT>(in, (int64_t)i * Cin + ci) * ld_feat<DT>(W, k * ldk + ci * ldc + col);
+                s += ld_feat<DT>(in, (int64_t)i * Cin + ci) * ld_feat<DT>(W, k * ldk + ci * ldc + col * ldcol);
             acc[o * 64 + cl] += s;
         }
         __syncthreads();
@@ -673,9 +676,10 @@ static void launch_tile(hipStream_t s, const ConvPlan& p, const void* in, int Ci
     }
 }
 
-PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int dt, int ldc, int64_t ldk) {
+PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int dt, int ldc, int64_t ldk,
+                      int ldcol) {
     PackJob q{(const uint16_t*)W, (uint4*)wpack, K3, Cin, Cout, 0, 0, 0, ldc > 0 ? ldc : Cout,
-              ldk > 0 ? ldk : (int64_t)Cin * Cout};
+              ldk > 0 ? ldk : (int64_t)Cin * Cout, ldcol > 0 ? ldcol : 1};
     if (!conv_mfma_supported(Cin, Cout, dt)) return q;
     q.KCH = conv_kch(Cin);
     q.NB = Cout / 16;

@@ -404,7 +404,7 @@ __global__ void k_pack_wp(const uint16_t* W, int Cin, int Cout, int KCH, int NB,
 // the point-MLP weight [Cp][C] packed like a single-offset conv weight, when
 // the MFMA kernel runs with point features
 PackJob devox_pack_job(const DevoxArgs& a, void* wpack) {
-    PackJob q{(const uint16_t*)a.Wp, (uint4*)wpack, 1, a.Cp, a.C, 0, 0, 0, a.C, (int64_t)a.Cp * a.C};
+    PackJob q{(const uint16_t*)a.Wp, (uint4*)wpack, 1, a.Cp, a.C, 0, 0, 0, a.C, (int64_t)a.Cp * a.C, 1};
     if (a.n <= 0 || !a.pfeat || !devox_mfma_supported(a.C, a.Cp, a.dt)) return q;
     q.KCH = (a.Cp + 31) / 32;
     q.NB = a.C / 16;

@@ -240,6 +240,13 @@ __device__ inline uint16_t to16(float v) {
     if constexpr (DT == SPV_BF16) return f32_to_bf16(v);
     else return f32_to_f16(v);
 }
+// fp64 -> fp32 rounding to odd: a following round-to-nearest-even to a format
+// with at most 22 fraction bits then rounds the fp64 value exactly once
+__device__ inline float f64_to_f32_odd(double d) {
+    float f = __double2float_rz(d);
+    if ((double)f != d) f = __uint_as_float(__float_as_uint(f) | 1u);
+    return f;
+}
 template <int DT>
 __device__ inline float from16(uint32_t h) {
     if constexpr (DT == SPV_BF16) return bf16_to_f32((uint16_t)h);

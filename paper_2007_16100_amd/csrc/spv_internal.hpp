@@ -212,6 +212,7 @@ struct ConvPlan {
     // (0: a dense [K3][Cin][Cout] tensor)
     int w_ldc = 0;
     int64_t w_ldk = 0;
+    int w_ldcol = 0;
 };
 void plan_conv_ws(Arena& a, ConvPlan& p, int64_t m_out_cap, int K3, int Cin, int Cout, int dt);
 struct PackJob;
@@ -232,10 +233,12 @@ struct PackJob {
     int64_t total;      // fragments * 64 lanes
     int ldc;            // elements between input channels (Cout when dense)
     int64_t ldk;        // elements between offsets (Cin * Cout when dense)
+    int ldcol = 1;      // elements between output channels (1 when dense)
 };
 // ldc / ldk <= 0: W is a dense [K3][Cin][Cout] tensor; otherwise the leading
 // Cin x Cout block of each offset of a wider tensor (a channel slice)
-PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int dt, int ldc = 0, int64_t ldk = 0);
+PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int dt, int ldc = 0, int64_t ldk = 0,
+                      int ldcol = 0);
 // the weight packing q as a launch of its own
 void launch_pack_job(hipStream_t s, const PackJob& q);
 
@@ -258,6 +261,28 @@ bool linear_mfma_supported(int Cin, int Cout, int dt);
 void* plan_linear_ws(Arena& a, int Cin, int Cout);
 // packs W into wpack (MFMA path) and runs the layer
 void launch_linear(hipStream_t s, const LinearArgs& a, void* wpack);
+
+// --- backward passes (backward.hip) --------------------------------------------
+struct WgradArgs {
+    const void* x;           // [x_rows][Cin] conv input
+    int64_t x_rows;
+    int Cin;
+    const void* dy;          // [dy_rows][Cout] gradient of the conv output
+    int64_t dy_rows;
+    int Cout;
+    const int32_t* off;      // [K3 + 1]
+    const int32_t* pairs;    // [pair_bound][2]
+    int64_t pair_bound;
+    int K3, transposed, dt;
+};
+bool wgrad_supported(int Cin, int Cout);
+void* plan_wgrad_ws(Arena& a, int K3, int Cin, int Cout);
+// dW [K3][Cin][Cout] fp32 via per-slice partials in `partial`
+void launch_wgrad(hipStream_t s, const WgradArgs& a, float* partial, float* dW);
+void launch_voxelize_backward(hipStream_t s, const void* dv, int C, const int32_t* counts, const int32_t* pt2vox,
+                              int64_t n, int64_t m, void* dfeat, int dt);
+void launch_devoxelize_backward(hipStream_t s, const int32_t* cidx, const float* cw, const void* dout, int64_t n, int C,
+                                float* dv, int64_t m, int dt);
 
 // The first kernel of a block call: clears the voxel table and the status
 // header, and packs up to kMaxPackJobs weights, in one grid-stride launch.

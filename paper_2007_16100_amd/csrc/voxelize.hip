@@ -127,13 +127,6 @@ __global__ void k_vox_fill(const int32_t* pt2vox, int64_t n, const int32_t* seg,
     plist[pos] = (int32_t)k;
 }
 
-// fp64 -> fp32 rounding to odd: a following round-to-nearest-even to a format
-// with at most 22 fraction bits then rounds the fp64 value exactly once
-__device__ inline float f64_to_f32_odd(double d) {
-    float f = __double2float_rz(d);
-    if ((double)f != d) f = __uint_as_float(__float_as_uint(f) | 1u);
-    return f;
-}
 
 // Eq. 2: one thread per (voxel, VEC consecutive channels).  The points are
 // summed in fp64 -- exact for 16-bit features of ordinary range, so the result

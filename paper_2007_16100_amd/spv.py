@@ -30,7 +30,9 @@ _DT = {torch.float32: SPV_F32, torch.bfloat16: SPV_BF16, torch.float16: SPV_F16}
 
 # every symbol include/spv.h declares
 EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced",
-           "spv_linear", "spv_devoxelize",
+           "spv_linear", "spv_sparse_conv_dgrad", "spv_wgrad_workspace_bytes", "spv_sparse_conv_wgrad",
+           "spv_voxelize_backward",
+           "spv_devoxelize_backward", "spv_devoxelize",
            "spv_block_workspace_bytes", "spv_block", "spv_lookup", "spv_status_check", "spv_status_string",
            "spv_last_hip_error")
 
@@ -73,6 +75,12 @@ def lib():
         L.spv_sparse_conv_sliced.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i64, i32, i32, vp, i32, i32, vp, vp,
                                              vp, i32, vp, vp, i64, i32, i32]
         L.spv_linear.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, i32, i32, vp, vp, i32, vp, i32, vp, i32, i32]
+        L.spv_sparse_conv_dgrad.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i64, i32, i32, vp, vp, vp, i64, i32, i32]
+        L.spv_sparse_conv_wgrad.argtypes = [vp, vp, sz, vp, i64, i32, vp, i64, i32, vp, vp, i64, i32, i32, vp, i32]
+        L.spv_wgrad_workspace_bytes.argtypes = [i32, i32, i32]
+        L.spv_wgrad_workspace_bytes.restype = sz
+        L.spv_voxelize_backward.argtypes = [vp, vp, i64, i32, vp, vp, i64, vp, i32]
+        L.spv_devoxelize_backward.argtypes = [vp, vp, vp, vp, i64, i32, vp, i64, i32]
         L.spv_devoxelize.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, vp, i64, f32, i32, vp, i32, vp, i32, vp, vp,
                                      vp, i32, vp, i32, vp, vp]
         L.spv_block.argtypes = [vp, vp, sz, ct.POINTER(BlockParams), vp, vp, i64, vp, vp, vp]
@@ -82,7 +90,8 @@ def lib():
         L.spv_status_string.restype = ct.c_char_p
         L.spv_last_hip_error.argtypes = []
         for f in ("spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced", "spv_linear",
-                  "spv_devoxelize", "spv_block", "spv_lookup", "spv_status_check"):
+                  "spv_sparse_conv_dgrad", "spv_sparse_conv_wgrad", "spv_voxelize_backward",
+                  "spv_devoxelize_backward", "spv_devoxelize", "spv_block", "spv_lookup", "spv_status_check"):
             getattr(L, f).restype = ct.c_int
         _lib = L
     return _lib
@@ -119,6 +128,10 @@ class Workspace:
     @classmethod
     def for_ops(cls, max_points: int, max_C: int, device="cuda"):
         return cls(lib().spv_workspace_bytes(max_points, max_C), device)
+
+    @classmethod
+    def for_wgrad(cls, K3: int, Cin: int, Cout: int, device="cuda"):
+        return cls(lib().spv_wgrad_workspace_bytes(K3, Cin, Cout), device)
 
     @classmethod
     def for_block(cls, max_points: int, C: int, device="cuda"):
@@ -260,6 +273,55 @@ def spv_linear(ws: Workspace, x: torch.Tensor, W: torch.Tensor, Cout: Optional[i
                           Cout_full, _ptr(scale), _ptr(shift), int(relu), _ptr(res), int(res_after_act), _ptr(out),
                           Cout, _DT[x.dtype])
     _chk(st, "spv_linear")
+    return out
+
+
+def spv_sparse_conv_dgrad(ws: Workspace, dy: torch.Tensor, off: torch.Tensor, pairs: torch.Tensor, W: torch.Tensor,
+                          m_in_cap: int, m_in_dev: Optional[torch.Tensor] = None, transposed: bool = False,
+                          out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """dx[i] = sum over the pairs (i, j, k) of dy[j] @ W[k]^T (W: the forward weights [K3][Cin][Cout])."""
+    K3, Cin, Cout = W.shape
+    if out is None:
+        out = torch.empty((max(m_in_cap, 1), Cin), dtype=dy.dtype, device=dy.device)
+    st = lib().spv_sparse_conv_dgrad(_stream(), ws.ptr, ws.nbytes, _ptr(dy), dy.shape[0], Cout, _ptr(off), _ptr(pairs),
+                                     pairs.shape[0], K3, int(transposed), _ptr(W), _ptr(out), _ptr(m_in_dev), m_in_cap,
+                                     Cin, _DT[dy.dtype])
+    _chk(st, "spv_sparse_conv_dgrad")
+    return out
+
+
+def spv_sparse_conv_wgrad(ws: Workspace, x: torch.Tensor, dy: torch.Tensor, off: torch.Tensor, pairs: torch.Tensor,
+                          K3: int, transposed: bool = False, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """dW[k] = sum over the pairs (i, j) of offset k of x[i]^T dy[j], float32 [K3][Cin][Cout]."""
+    Cin, Cout = x.shape[1], dy.shape[1]
+    if out is None:
+        out = torch.empty((K3, Cin, Cout), dtype=torch.float32, device=x.device)
+    st = lib().spv_sparse_conv_wgrad(_stream(), ws.ptr, ws.nbytes, _ptr(x), x.shape[0], Cin, _ptr(dy), dy.shape[0],
+                                     Cout, _ptr(off), _ptr(pairs), pairs.shape[0], K3, int(transposed), _ptr(out),
+                                     _DT[x.dtype])
+    _chk(st, "spv_sparse_conv_wgrad")
+    return out
+
+
+def spv_voxelize_backward(dvfeat: torch.Tensor, counts: torch.Tensor, pt2vox: torch.Tensor, m: int,
+                          out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    n, C = pt2vox.shape[0], dvfeat.shape[1]
+    if out is None:
+        out = torch.empty((max(n, 1), C), dtype=dvfeat.dtype, device=dvfeat.device)
+    st = lib().spv_voxelize_backward(_stream(), _ptr(dvfeat), m, C, _ptr(counts), _ptr(pt2vox), n, _ptr(out),
+                                     _DT[dvfeat.dtype])
+    _chk(st, "spv_voxelize_backward")
+    return out
+
+
+def spv_devoxelize_backward(corner_idx: torch.Tensor, corner_w: torch.Tensor, dout: torch.Tensor, m: int,
+                            out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    n, C = dout.shape
+    if out is None:
+        out = torch.empty((max(m, 1), C), dtype=torch.float32, device=dout.device)
+    st = lib().spv_devoxelize_backward(_stream(), _ptr(corner_idx), _ptr(corner_w), _ptr(dout), n, C, _ptr(out), m,
+                                       _DT[dout.dtype])
+    _chk(st, "spv_devoxelize_backward")
     return out
 
 

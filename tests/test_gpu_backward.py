@@ -1,0 +1,130 @@
+"""GPU parity of the backward passes (through the C ABI) against the oracle's.
+
+* conv input gradient: the conv kernels over the swapped map with W read
+  transposed -- normwise bound of the forward conv;
+* conv weight gradient: fp32 result, sums over up to ~10^5 pairs per offset in
+  fp32 -- normwise 1e-3 -- and bit-identical across runs (fixed slices, added in
+  order);
+* scatter-mean backward: bit-exact (fp64 quotient, one rounding on both sides);
+* devoxelization backward: fp32 atomics -- normwise 1e-5.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2007_16100_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 2e-2, "f16": 2e-2}
+TD = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
+
+
+@pytest.fixture(scope="module")
+def spv():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2007_16100_amd import spv as s
+    s.lib()
+    return s
+
+
+@pytest.fixture(scope="module")
+def sweep():
+    return synth.lidar_sweep(1002)
+
+
+def dev(a, dtype=None):
+    if dtype in ("bf16", "f16"):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(TD[dtype]).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t, dtype=None):
+    t = t.detach().cpu()
+    if dtype in ("bf16", "f16"):
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()
+
+
+def normwise(g, r):
+    g = np.asarray(g, np.float64)
+    r = np.asarray(r, np.float64)
+    return float(np.max(np.abs(g - r)) / max(np.max(np.abs(r)), 1e-30))
+
+
+def _map(rc, kind):
+    if kind == "subm":
+        oc, off, pairs = oracle.kernel_map(rc)
+        return len(rc), len(rc), 27, False, off, pairs
+    if kind == "k2s2":
+        oc, off, pairs = oracle.kernel_map(rc, 2, 2)
+        return len(rc), len(oc), 8, False, off, pairs
+    if kind == "k3s2":
+        oc, off, pairs = oracle.kernel_map(rc, 3, 2)
+        return len(rc), len(oc), 27, False, off, pairs
+    oc, off, pairs = oracle.kernel_map(rc, 2, 2)  # transposed k2s2: coarse -> fine
+    return len(oc), len(rc), 8, True, off, pairs
+
+
+@pytest.mark.parametrize("kind,cin,cout,dtype,step", [
+    ("subm", 32, 32, "bf16", 2), ("subm", 96, 96, "bf16", 2), ("subm", 64, 128, "f16", 2), ("subm", 16, 16, "f32", 6),
+    ("subm", 256, 256, "bf16", 8), ("k2s2", 64, 128, "bf16", 2), ("k3s2", 32, 64, "bf16", 2),
+    ("transposed", 128, 64, "bf16", 2)])
+def test_conv_dgrad(spv, sweep, kind, cin, cout, dtype, step):
+    rc, _, _, _ = oracle.voxelize(sweep[::step], 0.05)
+    m_in, m_out, K3, tr, off, pairs = _map(rc, kind)
+    W = synth.conv_weight(K3, cin, cout, 1101, dtype)
+    dy = synth.normal((m_out, cout), 1102, dtype=dtype)
+    ws = spv.Workspace.for_ops(max(m_in, m_out), max(cin, cout))
+    got = spv.spv_sparse_conv_dgrad(ws, dev(dy, dtype), dev(off), dev(pairs), dev(W, dtype), m_in, transposed=tr)
+    ref = oracle.conv_dgrad(dy, off, pairs, W, m_in, dtype, transposed=tr)
+    g = synth.from_storage(host(got, dtype)[:m_in], dtype)
+    e = normwise(g, synth.from_storage(ref, dtype))
+    assert e <= TOL[dtype], e
+
+
+@pytest.mark.parametrize("kind,cin,cout,dtype,step", [
+    ("subm", 32, 32, "bf16", 2), ("subm", 96, 96, "bf16", 4), ("subm", 64, 128, "f16", 4), ("subm", 16, 16, "f32", 8),
+    ("subm", 256, 256, "bf16", 16), ("subm", 24, 40, "bf16", 8), ("k2s2", 64, 128, "bf16", 2),
+    ("k3s2", 32, 64, "bf16", 4), ("transposed", 128, 64, "bf16", 2)])
+def test_conv_wgrad(spv, sweep, kind, cin, cout, dtype, step):
+    rc, _, _, _ = oracle.voxelize(sweep[::step], 0.05)
+    m_in, m_out, K3, tr, off, pairs = _map(rc, kind)
+    x = synth.normal((m_in, cin), 1103, dtype=dtype)
+    dy = synth.normal((m_out, cout), 1104, dtype=dtype)
+    print(f"wgrad {kind} {cin}->{cout} {dtype} pairs={len(pairs)}", flush=True)
+    ws = spv.Workspace.for_wgrad(K3, cin, cout)
+    args = (ws, dev(x, dtype), dev(dy, dtype), dev(off), dev(pairs), K3)
+    got = host(spv.spv_sparse_conv_wgrad(*args, transposed=tr))
+    again = host(spv.spv_sparse_conv_wgrad(*args, transposed=tr))
+    np.testing.assert_array_equal(got, again)  # deterministic
+    ref = oracle.conv_wgrad(x, dy, off, pairs, K3, dtype, transposed=tr)
+    e = normwise(got, ref)
+    assert e <= 1e-3, e
+
+
+@pytest.mark.parametrize("dtype,C", [("bf16", 96), ("f32", 8), ("f16", 5)])
+def test_voxelize_backward(spv, sweep, dtype, C):
+    coords, vf, counts, p2v = oracle.voxelize(sweep, 0.2)
+    dv = synth.normal((len(coords), C), 1105, dtype=dtype)
+    got = spv.spv_voxelize_backward(dev(dv, dtype), dev(counts), dev(p2v), len(coords))
+    ref = oracle.voxelize_backward(dv, counts, p2v, dtype)
+    np.testing.assert_array_equal(host(got, dtype)[: len(sweep)], ref)
+
+
+@pytest.mark.parametrize("mode,stride_log2,C,dtype", [("center", 0, 96, "bf16"), ("corner", 0, 32, "f32"),
+                                                      ("center", 2, 64, "bf16")])
+def test_devoxelize_backward(spv, sweep, mode, stride_log2, C, dtype):
+    pts = sweep[::2]
+    rc, _, _, _ = oracle.voxelize(pts, 0.05)
+    for _ in range(stride_log2):
+        rc, _, _ = oracle.kernel_map(rc, 2, 2)
+    vf = synth.normal((len(rc), C), 1106, dtype=dtype)
+    _, ci, cw = oracle.devoxelize(rc, vf, pts, 0.05, stride_log2, mode, dtype=dtype, want_corners=True)
+    dout = synth.normal((len(pts), C), 1107, dtype=dtype)
+    got = host(spv.spv_devoxelize_backward(dev(ci), dev(cw), dev(dout, dtype), len(rc)))[: len(rc)]
+    ref = oracle.devoxelize_backward(ci, cw, dout, len(rc), dtype)
+    e = normwise(got, ref)
+    assert e <= 1e-5, e
