@@ -378,6 +378,69 @@ def spvcnn_mode(args):
                       "eff_flops": F, "TFLOPs": F / (ms * 1e-3) / 1e12, "steps": args.steps}), flush=True)
 
 
+def backward_mode(args):
+    """The backward passes at the block's shape (sweep 1004, C = 96, bf16): conv input and
+    weight gradients on the submanifold map, scatter-mean and devoxelization backward.  One
+    JSON line per op: median HIP-event time, effective TFLOP/s or algorithmic GB/s."""
+    import torch
+    from paper_2007_16100_amd import spv, synth
+    dev = torch.device("cuda:0")
+    C = 96
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(args.steps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            ts.append((a, b))
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) for a, b in ts]))
+
+    xyz = synth.lidar_sweep(1004)
+    n = len(xyz)
+    d_xyz = torch.from_numpy(xyz).to(dev)
+    ws = spv.Workspace.for_ops(n, C)
+    vox = spv.spv_voxelize(ws, d_xyz, 0.05, bf(synth.normal((n, C), 1, dtype="bf16")))
+    m = vox.m
+    coords = vox.coords[:m].contiguous()
+    km = spv.spv_kernel_map(ws, coords)
+    P = km.total
+    x = bf(synth.normal((m, C), 2, dtype="bf16"))
+    dy = bf(synth.normal((m, C), 3, dtype="bf16"))
+    W = bf(synth.conv_weight(27, C, C, 4, "bf16"))
+    dx = torch.empty((m, C), dtype=torch.bfloat16, device=dev)
+    F = 2.0 * C * C * P
+
+    def line(op, ms, flops=0.0, nbytes=0.0):
+        print(json.dumps({"op": op, "ms_median": ms, "eff_flops": flops, "TFLOPs": flops / (ms * 1e-3) / 1e12,
+                          "alg_bytes": nbytes, "GBps": nbytes / (ms * 1e-3) / 1e9, "voxels": m, "pairs": P,
+                          "points": n}), flush=True)
+
+    ms = timed(lambda: spv.spv_sparse_conv_dgrad(ws, dy, km.off, km.pairs, W, m, out=dx))
+    line("conv dgrad 96->96 (plan included)", ms, F, 2 * 2 * C * m + 8 * P + 27 * C * C * 2)
+    wsw = spv.Workspace.for_wgrad(27, C, C)
+    dW = torch.empty((27, C, C), dtype=torch.float32, device=dev)
+    ms = timed(lambda: spv.spv_sparse_conv_wgrad(wsw, x, dy, km.off, km.pairs, 27, out=dW))
+    line("conv wgrad 96->96", ms, F, 2 * 2 * C * m + 8 * P + 27 * C * C * 4)
+    dvf = bf(synth.normal((m, C), 5, dtype="bf16"))
+    dfeat = torch.empty((n, C), dtype=torch.bfloat16, device=dev)
+    ms = timed(lambda: spv.spv_voxelize_backward(dvf, vox.counts, vox.pt2vox, m, out=dfeat))
+    line("voxelize backward C=96", ms, 0.0, 2 * C * m + 4 * m + 4 * n + 2 * C * n)
+    _, ci, cw = spv.spv_devoxelize(ws, coords, x, d_xyz, 0.05, want_corners=True)
+    dout = bf(synth.normal((n, C), 6, dtype="bf16"))
+    dv = torch.empty((m, C), dtype=torch.float32, device=dev)
+    ms = timed(lambda: spv.spv_devoxelize_backward(ci, cw, dout, m, out=dv))
+    line("devoxelize backward C=96", ms, 0.0, 64 * n + 2 * C * n + 4 * C * m)
+
+
 def cpu_baseline(xyz, convs, C, v=0.05):
     """The oracle, as it stands, on one full 96->96 conv layer of the workload (one thread)."""
     import oracle
@@ -412,7 +475,12 @@ def main():
                     help="map build and conv alone at the 32->32 and 64<->128 (k2s2, transposed) shapes")
     ap.add_argument("--spvcnn", action="store_true",
                     help="the SPVCNN-style encoder-decoder forward on a batch of 4 sweeps")
+    ap.add_argument("--backward", action="store_true",
+                    help="the backward passes (conv input / weight gradients, scatter-mean and devox backward)")
     args = ap.parse_args()
+    if args.backward:
+        backward_mode(args)
+        return
     if args.spvcnn:
         spvcnn_mode(args)
         return

@@ -25,9 +25,14 @@ constexpr int kWgWaves = 8;
 constexpr int kWgChunk = 64;  // pairs per LDS fill: two MFMA K-steps of 32
 constexpr int kWgLd = kWgChunk + 8;  // LDS row length in 16-bit elements (padded)
 
+// slices per offset: as many as a 64 MB partial-sum buffer holds (the centre
+// offset of a submanifold map has ~15% of the pairs: more slices spread it
+// over more compute units), a power of two in [8, 64]
 static int wgrad_slices(int Cin, int Cout) {
-    const int64_t cc = (int64_t)Cin * Cout;
-    return cc <= 128 * 128 ? 32 : (cc <= 128 * 256 ? 16 : 8);
+    const int64_t per = (int64_t)27 * Cin * Cout * 4;
+    int S = 64;
+    while (S > 8 && per * S > ((int64_t)64 << 20)) S >>= 1;
+    return S;
 }
 
 bool wgrad_supported(int Cin, int Cout) { return (int64_t)Cin * Cout <= 256 * 256; }
@@ -43,7 +48,8 @@ __device__ inline void pair_range(const int32_t* off, int k, int64_t pair_bound,
     hi = hi < lo ? lo : (hi > pair_bound ? pair_bound : hi);
 }
 
-template <int DT, int TPW>
+// PPT: 16-byte pieces each thread gathers per chunk (>= chunk pieces / threads)
+template <int DT, int TPW, int PPT>
 __global__ __launch_bounds__(64 * kWgWaves) void k_conv_wgrad_mfma(
     const uint16_t* __restrict__ x, int64_t x_rows, int Cin, const uint16_t* __restrict__ dy, int64_t dy_rows,
     int Cout, const int32_t* __restrict__ off, const int32_t* __restrict__ pairs, int64_t pair_bound, int transposed,
@@ -64,13 +70,21 @@ __global__ __launch_bounds__(64 * kWgWaves) void k_conv_wgrad_mfma(
 #pragma unroll
     for (int u = 0; u < TPW; ++u) acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int64_t c0 = lo + (int64_t)sl * kWgChunk; c0 < hi; c0 += (int64_t)S * kWgChunk) {
+    // the thread's pieces of chunk c0 into registers: item e = threadIdx.x + r * threads
+    // is piece e / 64 of pair e % 64 -- a wave's lanes take the same piece of 64
+    // pairs, so their transposed LDS writes below fill consecutive columns of one
+    // row (pieces of one pair in consecutive lanes would all hit one bank);
+    // zeros past the chunk's pairs and the rows
+    static_assert(kWgChunk == 64, "one pair per lane");
+    uint4 pv[PPT];
+    auto gather = [&](int64_t c0) {
         const int np = (hi - c0) < kWgChunk ? (int)(hi - c0) : kWgChunk;
-        // gather: piece q of pair p, written channel-major (zeros past the chunk's pairs)
-        for (int e = threadIdx.x; e < kWgChunk * qq; e += blockDim.x) {
-            const int p = e / qq, q = e - p * qq;
+#pragma unroll
+        for (int r = 0; r < PPT; ++r) {
+            const int e = threadIdx.x + r * 64 * kWgWaves;
+            const int p = e & (kWgChunk - 1), q = e / kWgChunk;
             uint4 v = make_uint4(0u, 0u, 0u, 0u);
-            if (p < np) {
+            if (q < qq && p < np && c0 < hi) {
                 const int64_t pp = c0 + p;
                 if (q < qx) {
                     const int64_t i = pairs[2 * pp + isel];
@@ -80,15 +94,31 @@ __global__ __launch_bounds__(64 * kWgWaves) void k_conv_wgrad_mfma(
                     if (j >= 0 && j < dy_rows) v = *(const uint4*)(dy + j * Cout + (q - qx) * 8);
                 }
             }
-            uint16_t* dst = (q < qx ? xt + (size_t)(q * 8) * kWgLd : gt + (size_t)((q - qx) * 8) * kWgLd) + p;
-            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+            pv[r] = v;
+        }
+    };
+    const int64_t step = (int64_t)S * kWgChunk;
+    int64_t c0 = lo + (int64_t)sl * kWgChunk;
+    if (c0 < hi) gather(c0);
+    for (; c0 < hi; c0 += step) {
+        // the pieces in registers -> LDS, channel-major
 #pragma unroll
-            for (int h = 0; h < 4; ++h) {
-                dst[(2 * h) * kWgLd] = (uint16_t)(w[h] & 0xFFFF);
-                dst[(2 * h + 1) * kWgLd] = (uint16_t)(w[h] >> 16);
+        for (int r = 0; r < PPT; ++r) {
+            const int e = threadIdx.x + r * 64 * kWgWaves;
+            const int p = e & (kWgChunk - 1), q = e / kWgChunk;
+            if (q < qq) {
+                uint16_t* dst = (q < qx ? xt + (size_t)(q * 8) * kWgLd : gt + (size_t)((q - qx) * 8) * kWgLd) + p;
+                const uint32_t w[4] = {pv[r].x, pv[r].y, pv[r].z, pv[r].w};
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    dst[(2 * h) * kWgLd] = (uint16_t)(w[h] & 0xFFFF);
+                    dst[(2 * h + 1) * kWgLd] = (uint16_t)(w[h] >> 16);
+                }
             }
         }
         __syncthreads();
+        // the next chunk's gathers are in flight while this one is multiplied
+        gather(c0 + step);
 #pragma unroll
         for (int ks = 0; ks < kWgChunk / 32; ++ks) {
 #pragma unroll
@@ -151,16 +181,26 @@ __global__ void k_wgrad_reduce(const float* __restrict__ partial, int S, int64_t
     dW[t] = s;
 }
 
-template <int DT, int TPW>
-static void launch_wgrad_mfma(hipStream_t s, dim3 grid, const WgradArgs& a, float* partial) {
+template <int DT, int TPW, int PPT>
+static void launch_wgrad_mfma3(hipStream_t s, dim3 grid, const WgradArgs& a, float* partial) {
     const size_t lds = (size_t)(a.Cin + a.Cout) * kWgLd * 2;
-    static const bool lds_ok = hipFuncSetAttribute((const void*)k_conv_wgrad_mfma<DT, TPW>,
+    static const bool lds_ok = hipFuncSetAttribute((const void*)k_conv_wgrad_mfma<DT, TPW, PPT>,
                                                    hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) ==
                                hipSuccess;
     (void)lds_ok;
-    k_conv_wgrad_mfma<DT, TPW><<<grid, 64 * kWgWaves, lds, s>>>((const uint16_t*)a.x, a.x_rows, a.Cin,
-                                                                (const uint16_t*)a.dy, a.dy_rows, a.Cout, a.off,
-                                                                a.pairs, a.pair_bound, a.transposed, partial);
+    k_conv_wgrad_mfma<DT, TPW, PPT><<<grid, 64 * kWgWaves, lds, s>>>((const uint16_t*)a.x, a.x_rows, a.Cin,
+                                                                     (const uint16_t*)a.dy, a.dy_rows, a.Cout, a.off,
+                                                                     a.pairs, a.pair_bound, a.transposed, partial);
+}
+
+template <int DT, int TPW>
+static void launch_wgrad_mfma(hipStream_t s, dim3 grid, const WgradArgs& a, float* partial) {
+    // pieces per thread: 64 pairs x (Cin + Cout) / 8 pieces over 512 threads
+    const int ppt = (kWgChunk * ((a.Cin + a.Cout) / 8) + 64 * kWgWaves - 1) / (64 * kWgWaves);
+    if (ppt <= 1) launch_wgrad_mfma3<DT, TPW, 1>(s, grid, a, partial);
+    else if (ppt <= 2) launch_wgrad_mfma3<DT, TPW, 2>(s, grid, a, partial);
+    else if (ppt <= 4) launch_wgrad_mfma3<DT, TPW, 4>(s, grid, a, partial);
+    else launch_wgrad_mfma3<DT, TPW, 8>(s, grid, a, partial);
 }
 
 template <int DT>
