@@ -220,7 +220,7 @@ __global__ __launch_bounds__(64 * NW) void k_conv_union(
 bool union_supported(int K3, int Cin, int Cout, int dt) {
     if (K3 != 27 || dt == SPV_F32) return false;
     const auto width_ok = [](int c) { return c == 32 || c == 64 || c == 96 || c == 128; };
-    return width_ok(Cin) && width_ok(Cout);
+    return (width_ok(Cin) && width_ok(Cout)) || (Cin == 256 && Cout == 256);
 }
 
 // Launch shape per width: 11 waves of 2 blocks (352 rows per workgroup: a
@@ -232,7 +232,8 @@ template <int DT, int KCH, int NB>
 static void launch_union_c(hipStream_t s, const ConvPlan& p, const void* in, int64_t in_rows, const void* wpack,
                            const float* scale, const float* shift, int relu, void* out) {
     constexpr int FR = KCH * NB;
-    constexpr int RB = FR >= 32 ? 1 : 2, NW = 11;
+    // 256 -> 256: 8 waves (256 registers each), one offset's 128 KB of weights per phase
+    constexpr int RB = FR >= 32 ? 1 : 2, NW = FR >= 128 ? 8 : 11;
     constexpr int PH = (128 / FR) < kUK3 ? (128 / FR) : kUK3;  // 27, 14, 7, 4 for C -> C = 32, 64, 96, 128
     constexpr int64_t rows_wg = (int64_t)NW * RB * 16;
     // a multiple of 8 workgroups: the kernel spreads the live tiles over the 8 XCDs
@@ -256,6 +257,10 @@ static void launch_union_cin(hipStream_t s, const ConvPlan& p, const void* in, i
 template <int DT>
 static void launch_union(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int Cout, int64_t in_rows,
                          const void* wpack, const float* scale, const float* shift, int relu, void* out) {
+    if (Cin == 256) {
+        launch_union_c<DT, 8, 16>(s, p, in, in_rows, wpack, scale, shift, relu, out);
+        return;
+    }
     switch (Cin) {
         case 32: launch_union_cin<DT, 1>(s, p, in, Cout, in_rows, wpack, scale, shift, relu, out); break;
         case 64: launch_union_cin<DT, 2>(s, p, in, Cout, in_rows, wpack, scale, shift, relu, out); break;
