@@ -325,18 +325,19 @@ def spvcnn_flops(P, plan, n):
     2 * C_in * C_out times its kernel-map pairs (convs) or rows (1x1 shortcuts, point MLPs,
     head)."""
     pairs = lambda km: int(km.off[-1].item())
+    subm = [int((plan.nbr[s][: plan.m[s]] > 0).sum().item()) for s in range(5)]  # nonzero table entries
     units = {}
     for name in P:
         parts = name.split(".")
         if parts[0] == "stem":
-            units[name] = pairs(plan.subm[0])
+            units[name] = subm[0]
         elif parts[0] == "down":
             units[name] = pairs(plan.down[int(parts[1])])
         elif parts[0] == "up":
             units[name] = pairs(plan.down[5 - int(parts[1])])
         elif parts[0] in ("enc", "dec"):
             s = int(parts[1]) if parts[0] == "enc" else 4 - int(parts[1])
-            units[name] = plan.m[s] if parts[3] == "sc" else pairs(plan.subm[s])
+            units[name] = plan.m[s] if parts[3] == "sc" else subm[s]
         else:  # point MLPs and the head run on every point
             units[name] = n
     return sum(2.0 * P[k][0].shape[-2] * P[k][0].shape[-1] * u for k, u in units.items())

@@ -187,6 +187,34 @@ spv_status spv_sparse_conv_sliced(void* stream, void* ws, size_t ws_bytes,
                                   spv_dtype dt);
 
 /*
+ * A submanifold 3x3x3 map as a dense neighbour table, for a network that runs
+ * several convolutions on one voxel set (Sec. 3.3's blocks, a U-Net stage):
+ *
+ * spv_kernel_map_nbr -- nbr[j][k] = i + 1 when voxel i sits at c_j + delta_k
+ * (k = 9(dx+1) + 3(dy+1) + (dz+1)), 0 when no voxel does: the pairs of the
+ * K=3 stride-1 spv_kernel_map, stored by output row.
+ * In:  in_coords [m_cap][4] (distinct); m_in_dev: device count (NULL = m_cap).
+ * Out: nbr [m_cap][27] int32 (rows < count written).  Device-detected errors
+ *      (duplicate or out-of-range coordinates) go to the workspace status.
+ *
+ * spv_sparse_conv_nbr -- spv_sparse_conv_sliced on such a table: the
+ * neighbour-table conv kernel without the per-call plan (no table build, only
+ * the weight packing).  Only the shapes that kernel takes: bf16/f16 with Cin,
+ * Cout in {32, 64, 96, 128} or Cin = Cout = 256 (else SPV_ERR_UNSUPPORTED).
+ * In:  nbr [m_out_cap][27] from spv_kernel_map_nbr on the output voxels (the
+ *      inputs are the same voxels: in_rows = their count); every other
+ *      argument as in spv_sparse_conv_sliced.
+ */
+spv_status spv_kernel_map_nbr(void* stream, void* ws, size_t ws_bytes,
+                              const int32_t* in_coords, const int64_t* m_in_dev, int64_t m_cap, int32_t* nbr);
+spv_status spv_sparse_conv_nbr(void* stream, void* ws, size_t ws_bytes,
+                               const void* in, int64_t in_rows, int32_t Cin, const int32_t* nbr,
+                               const void* W, int32_t Cin_full, int32_t Cout_full,
+                               const float* scale, const float* shift, const void* res, int32_t relu,
+                               void* out, const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout,
+                               spv_dtype dt);
+
+/*
  * Backward passes (training, Sec. 4.2 trains the super network end to end).
  *
  * spv_sparse_conv_dgrad -- input gradient of spv_sparse_conv (without its

@@ -5,7 +5,7 @@
 #include <math.h>
 #include <string.h>
 
-#include "spv_internal.hpp"
+#include "conv_common.hpp"
 
 using namespace spv;
 
@@ -345,6 +345,49 @@ spv_status spv_sparse_conv_sliced(void* stream, void* ws, size_t ws_bytes, const
     return sparse_conv_call(stream, ws, ws_bytes, in, in_rows, Cin, off, pairs, pair_cap, K3, transposed, W,
                             WStrides{Cout_full, 1, (int64_t)Cin_full * Cout_full}, scale, shift, res, relu, out,
                             m_out_dev, m_out_cap, Cout, dt);
+}
+
+spv_status spv_kernel_map_nbr(void* stream, void* ws, size_t ws_bytes, const int32_t* in_coords,
+                              const int64_t* m_in_dev, int64_t m_cap, int32_t* nbr) {
+    if (!ws || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || (m_cap > 0 && (!in_coords || !nbr)))
+        return SPV_ERR_INVALID_ARG;
+    if (m_cap * 27 * 4 > (int64_t)0xFFFFE000) return SPV_ERR_UNSUPPORTED;
+    MapLayout L;
+    if (need(layout_kmap(nullptr, 0, m_cap, 3, 1, L), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_kmap(ws, ws_bytes, m_cap, 3, 1, L);
+    if (m_cap == 0) return SPV_OK;
+    hipStream_t s = (hipStream_t)stream;
+    launch_clear(s, L.h, L.w.fine, true);
+    launch_table_build(s, L.h, L.w.fine, in_coords, m_in_dev, m_cap);
+    launch_kernel_map_nbr(s, L.w, in_coords, m_in_dev, m_cap, nbr);
+    return hip_check();
+}
+
+spv_status spv_sparse_conv_nbr(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows, int32_t Cin,
+                               const int32_t* nbr, const void* W, int32_t Cin_full, int32_t Cout_full,
+                               const float* scale, const float* shift, const void* res, int32_t relu, void* out,
+                               const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
+    if (!ws || in_rows < 0 || m_out_cap < 0 || m_out_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !W ||
+        !valid_dt(dt) || Cin > Cin_full || Cout > Cout_full)
+        return SPV_ERR_INVALID_ARG;
+    if (!union_supported(27, Cin, Cout, dt) || m_out_cap * 27 * 4 > (int64_t)0xFFFFE000 ||
+        in_rows * (int64_t)Cin * 2 > (int64_t)0xFFFFE000)
+        return SPV_ERR_UNSUPPORTED;
+    if ((in_rows > 0 && !in) || (m_out_cap > 0 && (!out || !nbr))) return SPV_ERR_INVALID_ARG;
+    if (!aligned16(in) || !aligned16(out) || !aligned16(W) || !aligned16(res) || (res && res == out))
+        return SPV_ERR_INVALID_ARG;
+    ConvLayout L;
+    if (need(layout_conv(nullptr, 0, m_out_cap, 27, Cin, Cout, dt, L), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_conv(ws, ws_bytes, m_out_cap, 27, Cin, Cout, dt, L);
+    if (m_out_cap == 0) return SPV_OK;
+    hipStream_t s = (hipStream_t)stream;
+    ConvPlan p = L.p;
+    p.nbr = const_cast<int32_t*>(nbr);  // read only
+    p.m_out_dev = m_out_dev;
+    p.res = res;
+    launch_pack_job(s, conv_pack_job(27, W, L.wpack, Cin, Cout, dt, Cout_full, (int64_t)Cin_full * Cout_full));
+    launch_conv_union(s, p, in, Cin, in_rows, Cout, L.wpack, scale, shift, relu, out, dt);
+    return hip_check();
 }
 
 spv_status spv_sparse_conv_dgrad(void* stream, void* ws, size_t ws_bytes, const void* dy, int64_t dy_rows,

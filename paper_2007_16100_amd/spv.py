@@ -30,7 +30,7 @@ _DT = {torch.float32: SPV_F32, torch.bfloat16: SPV_BF16, torch.float16: SPV_F16}
 
 # every symbol include/spv.h declares
 EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced",
-           "spv_linear", "spv_sparse_conv_dgrad", "spv_wgrad_workspace_bytes", "spv_sparse_conv_wgrad",
+           "spv_linear", "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_sparse_conv_dgrad", "spv_wgrad_workspace_bytes", "spv_sparse_conv_wgrad",
            "spv_voxelize_backward",
            "spv_devoxelize_backward", "spv_devoxelize",
            "spv_block_workspace_bytes", "spv_block", "spv_lookup", "spv_status_check", "spv_status_string",
@@ -75,6 +75,9 @@ def lib():
         L.spv_sparse_conv_sliced.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i64, i32, i32, vp, i32, i32, vp, vp,
                                              vp, i32, vp, vp, i64, i32, i32]
         L.spv_linear.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, i32, i32, vp, vp, i32, vp, i32, vp, i32, i32]
+        L.spv_kernel_map_nbr.argtypes = [vp, vp, sz, vp, vp, i64, vp]
+        L.spv_sparse_conv_nbr.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i32, i32, vp, vp, vp, i32, vp, vp, i64, i32,
+                                          i32]
         L.spv_sparse_conv_dgrad.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i64, i32, i32, vp, vp, vp, i64, i32, i32]
         L.spv_sparse_conv_wgrad.argtypes = [vp, vp, sz, vp, i64, i32, vp, i64, i32, vp, vp, i64, i32, i32, vp, i32]
         L.spv_wgrad_workspace_bytes.argtypes = [i32, i32, i32]
@@ -90,7 +93,8 @@ def lib():
         L.spv_status_string.restype = ct.c_char_p
         L.spv_last_hip_error.argtypes = []
         for f in ("spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced", "spv_linear",
-                  "spv_sparse_conv_dgrad", "spv_sparse_conv_wgrad", "spv_voxelize_backward",
+                  "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_sparse_conv_dgrad", "spv_sparse_conv_wgrad",
+                  "spv_voxelize_backward",
                   "spv_devoxelize_backward", "spv_devoxelize", "spv_block", "spv_lookup", "spv_status_check"):
             getattr(L, f).restype = ct.c_int
         _lib = L
@@ -273,6 +277,38 @@ def spv_linear(ws: Workspace, x: torch.Tensor, W: torch.Tensor, Cout: Optional[i
                           Cout_full, _ptr(scale), _ptr(shift), int(relu), _ptr(res), int(res_after_act), _ptr(out),
                           Cout, _DT[x.dtype])
     _chk(st, "spv_linear")
+    return out
+
+
+def spv_kernel_map_nbr(ws: Workspace, coords: torch.Tensor, m_dev: Optional[torch.Tensor] = None,
+                       out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """nbr [m][27] int32: entry k of row j is i + 1 for the voxel i at c_j + delta_k, else 0."""
+    m_cap = coords.shape[0]
+    if out is None:
+        out = torch.empty((max(m_cap, 1), 27), dtype=torch.int32, device=coords.device)
+    st = lib().spv_kernel_map_nbr(_stream(), ws.ptr, ws.nbytes, _ptr(coords), _ptr(m_dev), m_cap, _ptr(out))
+    _chk(st, "spv_kernel_map_nbr")
+    return out
+
+
+def spv_sparse_conv_nbr(ws: Workspace, x: torch.Tensor, nbr: torch.Tensor, W_full: torch.Tensor, Cout: int,
+                        m_out_cap: int, m_out_dev: Optional[torch.Tensor] = None, scale: Optional[torch.Tensor] = None,
+                        shift: Optional[torch.Tensor] = None, relu: bool = False,
+                        res: Optional[torch.Tensor] = None, cin_offset: int = 0,
+                        out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The sliced conv (input channels cin_offset .. + x's width, first Cout outputs) on a
+    neighbour table from spv_kernel_map_nbr."""
+    K3, Cin_full, Cout_full = W_full.shape
+    Cin = x.shape[1]
+    if cin_offset < 0 or cin_offset + Cin > Cin_full:
+        raise ValueError("input-channel slice outside the weight")
+    if out is None:
+        out = torch.empty((max(m_out_cap, 1), Cout), dtype=x.dtype, device=x.device)
+    wp = ct.c_void_p(_ptr(W_full).value + cin_offset * Cout_full * W_full.element_size())
+    st = lib().spv_sparse_conv_nbr(_stream(), ws.ptr, ws.nbytes, _ptr(x), x.shape[0], Cin, _ptr(nbr), wp, Cin_full,
+                                   Cout_full, _ptr(scale), _ptr(shift), _ptr(res), int(relu), _ptr(out),
+                                   _ptr(m_out_dev), m_out_cap, Cout, _DT[x.dtype])
+    _chk(st, "spv_sparse_conv_nbr")
     return out
 
 

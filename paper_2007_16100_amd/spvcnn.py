@@ -12,8 +12,10 @@ Every step runs in libspv's kernels; this module only sequences the calls and
 holds the device buffers:
 
 * plan: voxelization at stride 1, the four stride-2 maps (which give the
-  coordinate sets of strides 2..16) and the five submanifold maps, one
-  synchronization per stride to size what follows exactly;
+  coordinate sets of strides 2..16) and a submanifold neighbour table per stride,
+  one synchronization per stride to size what follows exactly; every 3x3x3 conv
+  the neighbour-table kernel takes runs on that table (no per-call plan), the
+  others on the stride's pairs, built on first use;
 * a conv over a skip concatenation [t; x] runs as two sliced convs,
   W_t t (scaled, unshifted) handed as the residual input of W_x x + shift;
   the 1x1 shortcut over it likewise as two linear layers;
@@ -46,7 +48,8 @@ class Plan:
     coords: List[torch.Tensor]      # [m_s][4] per stride 2^s, s = 0..4
     m: List[int]
     down: List[Optional[spv.KernelMap]]   # down[s]: stride 2^(s-1) -> 2^s (s = 1..4)
-    subm: List[spv.KernelMap]
+    nbr: List[torch.Tensor]         # submanifold neighbour table [m_s][27] per stride
+    subm: List[Optional[spv.KernelMap]]   # submanifold pairs, built on first use
 
 
 class SPVCNN:
@@ -97,8 +100,8 @@ class SPVCNN:
             down.append(km)
             m.append(ms)
             coords.append(km.out_coords[:ms])
-        subm = [spv.spv_kernel_map(ws, c, sync=False) for c in coords]
-        return Plan(coords, m, down, subm), vox
+        nbr = [spv.spv_kernel_map_nbr(ws, c) for c in coords]
+        return Plan(coords, m, down, nbr, [None] * 5), vox
 
     # -- layers --------------------------------------------------------------
     def _conv(self, x, name, km, m_out, relu=True, transposed=False, res=None, cin_offset=0, cout=None,
@@ -109,31 +112,44 @@ class SPVCNN:
                                           shift=sh if shift else None, relu=relu, transposed=transposed, res=res,
                                           cin_offset=cin_offset)
 
+    def _subm(self, plan, x, name, s, relu=True, res=None, cin_offset=0, shift=True):
+        """A submanifold 3x3x3 conv at stride 2^s: on the stride's neighbour table where the
+        neighbour-table kernel takes the shape, else on the pairs (built once per stride)."""
+        W, sc, sh = self.P[name]
+        Cin, Cout = x.shape[1], W.shape[2]
+        widths = (32, 64, 96, 128)
+        if self.dt != torch.float32 and ((Cin in widths and Cout in widths) or (Cin == 256 and Cout == 256)):
+            return spv.spv_sparse_conv_nbr(self.ws, x, plan.nbr[s], W, Cout, plan.m[s], scale=sc,
+                                           shift=sh if shift else None, relu=relu, res=res, cin_offset=cin_offset)
+        if plan.subm[s] is None:
+            plan.subm[s] = spv.spv_kernel_map(self.ws, plan.coords[s], sync=False)
+        return self._conv(x, name, plan.subm[s], plan.m[s], relu=relu, res=res, cin_offset=cin_offset, shift=shift)
+
     def _lin(self, x, name, relu=False, res=None, res_after=False, cin_offset=0, shift=True):
         W, sc, sh = self.P[name]
         return spv.spv_linear(self.ws, x, W, scale=sc, shift=sh if shift else None, relu=relu, res=res,
                               res_after_act=res_after, cin_offset=cin_offset)
 
-    def _resblock(self, parts, name, km):
-        """Residual block over the concatenation of `parts` (one tensor: no concatenation)."""
-        m = parts[0].shape[0]
+    def _resblock(self, plan, parts, name, s):
+        """Residual block at stride 2^s over the concatenation of `parts` (one tensor: no
+        concatenation).  Each layer over the concatenation runs part by part: every part but
+        the last gives a scaled, unshifted, unactivated partial sum, the residual input of the
+        next part's layer."""
         offs = np.cumsum([0] + [p.shape[1] for p in parts[:-1]])
 
-        def over_parts(layer, last_kw):
+        def over_parts(layer):
             r = None
             for i, (p, o) in enumerate(zip(parts, offs)):
-                final = i == len(parts) - 1
-                r = layer(p, int(o), r, final, last_kw if final else {})
+                r = layer(p, int(o), r, i == len(parts) - 1)
             return r
 
-        h = over_parts(lambda p, o, r, final, kw: self._conv(p, name + ".a", km, m, relu=final, res=r,
-                                                             cin_offset=o, shift=final), {})
+        h = over_parts(lambda p, o, r, final: self._subm(plan, p, name + ".a", s, relu=final, res=r, cin_offset=o,
+                                                          shift=final))
         if name + ".sc" in self.P:
-            s = over_parts(lambda p, o, r, final, kw: self._lin(p, name + ".sc", res=r, cin_offset=o, shift=final),
-                           {})
+            sc = over_parts(lambda p, o, r, final: self._lin(p, name + ".sc", res=r, cin_offset=o, shift=final))
         else:
-            s = parts[0]
-        return self._conv(h, name + ".b", km, m, res=s)
+            sc = parts[0]
+        return self._subm(plan, h, name + ".b", s, res=sc)
 
     def _fuse(self, plan, vfeat, s, z, name, xyz, batch):
         W, sc, sh = self.P[name]
@@ -160,23 +176,23 @@ class SPVCNN:
         plan, vox = self.plan(xyz, batch, feat)
         m = plan.m
         x = vox.vfeat[: m[0]]
-        x = self._conv(x, "stem.0", plan.subm[0], m[0])
-        x = self._conv(x, "stem.1", plan.subm[0], m[0])
+        x = self._subm(plan, x, "stem.0", 0)
+        x = self._subm(plan, x, "stem.1", 0)
         skips = [x]
         z = self._fuse(plan, x, 0, feat, "point.0", xyz, batch)
 
         x, _ = self._revoxelize(xyz, z, 0, batch, m[0])
         for s in range(1, 5):
             x = self._conv(x, f"down.{s}", plan.down[s], m[s])
-            x = self._resblock([x], f"enc.{s}.0", plan.subm[s])
-            x = self._resblock([x], f"enc.{s}.1", plan.subm[s])
+            x = self._resblock(plan, [x], f"enc.{s}.0", s)
+            x = self._resblock(plan, [x], f"enc.{s}.1", s)
             skips.append(x)
         z = self._fuse(plan, x, 4, z, "point.1", xyz, batch)
 
         def up(y, u):
             t = self._conv(y, f"up.{u}", plan.down[5 - u], m[4 - u], transposed=True)
-            y = self._resblock([t, skips[4 - u]], f"dec.{u}.0", plan.subm[4 - u])
-            return self._resblock([y], f"dec.{u}.1", plan.subm[4 - u])
+            y = self._resblock(plan, [t, skips[4 - u]], f"dec.{u}.0", 4 - u)
+            return self._resblock(plan, [y], f"dec.{u}.1", 4 - u)
 
         y, vox4 = self._revoxelize(xyz, z, 4, batch, m[4])
         y = up(up(y, 1), 2)

@@ -727,3 +727,50 @@ def test_conv_concat_split(spv, sweep, ca, cb, cout, transposed):
     got = spv.spv_sparse_conv_sliced(ws, dev(b, "bf16"), d_off, d_pairs, d_W, cb, cout, m_out, scale=dev(sc),
                                      shift=dev(sh), relu=True, transposed=transposed, res=part, cin_offset=ca)
     check_close(host(got, "bf16")[:m_out], ref, "bf16")
+
+
+# ---------------------------------------------------------------------------
+# neighbour tables shared by several convs
+# ---------------------------------------------------------------------------
+def test_kernel_map_nbr_matches_pairs(spv, sweep):
+    """nbr[j][k] = i + 1 exactly for the pairs (i, j, k) of the oracle's submanifold map."""
+    rc, _, _, _ = oracle.voxelize(sweep, 0.05)
+    _, off, pairs = oracle.kernel_map(rc)
+    ws = spv.Workspace.for_ops(len(rc), 16)
+    got = host(spv.spv_kernel_map_nbr(ws, dev(rc)))[: len(rc)]
+    want = np.zeros((len(rc), 27), np.int32)
+    for k in range(27):
+        p = pairs[off[k]:off[k + 1]]
+        want[p[:, 1], k] = p[:, 0] + 1
+    np.testing.assert_array_equal(got, want)
+
+
+@pytest.mark.parametrize("cin,cout,dtype,res", [(32, 32, "bf16", False), (96, 96, "bf16", True),
+                                                (64, 128, "f16", True), (256, 256, "bf16", False)])
+def test_conv_on_neighbour_table(spv, sweep, cin, cout, dtype, res):
+    """The conv on a prebuilt table gives the bits of the conv planned from the pairs."""
+    rc, _, _, _ = oracle.voxelize(sweep[::2] if cin == 256 else sweep, 0.05)
+    _, off, pairs = oracle.kernel_map(rc)
+    x = synth.normal((len(rc), cin), 1201, dtype=dtype)
+    W = synth.conv_weight(27, cin, cout, 1202, dtype)
+    sc, sh = synth.folded_bn(cout, 1203)
+    r = synth.normal((len(rc), cout), 1204, dtype=dtype) if res else None
+    ws = spv.Workspace.for_ops(len(rc), max(cin, cout))
+    nbr = spv.spv_kernel_map_nbr(ws, dev(rc))
+    got = spv.spv_sparse_conv_nbr(ws, dev(x, dtype), nbr, dev(W, dtype), cout, len(rc), scale=dev(sc),
+                                  shift=dev(sh), relu=True, res=None if r is None else dev(r, dtype))
+    want = spv.spv_sparse_conv_sliced(ws, dev(x, dtype), dev(off), dev(pairs), dev(W, dtype), cin, cout, len(rc),
+                                      scale=dev(sc), shift=dev(sh), relu=True, res=None if r is None else dev(r, dtype))
+    np.testing.assert_array_equal(host(got, dtype)[: len(rc)], host(want, dtype)[: len(rc)])
+    ref = oracle.sparse_conv(x, off, pairs, W, len(rc), dtype, sc, sh, True, res=r)
+    check_close(host(got, dtype)[: len(rc)], ref, dtype)
+
+
+def test_conv_on_neighbour_table_rejects_other_shapes(spv):
+    ws = spv.Workspace.for_ops(16, 48)
+    x = torch.zeros((4, 48), dtype=torch.bfloat16, device="cuda")
+    nbr = torch.zeros((4, 27), dtype=torch.int32, device="cuda")
+    W = torch.zeros((27, 48, 48), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(spv.SpvError) as e:
+        spv.spv_sparse_conv_nbr(ws, x, nbr, W, 48, 4)
+    assert e.value.status == spv.SPV_ERR_UNSUPPORTED
