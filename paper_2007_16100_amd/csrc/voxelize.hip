@@ -109,22 +109,42 @@ __global__ void k_vox_rank(const Header* h, SortBufs sb, Table t, int32_t* coord
 }
 
 // every point's voxel index, read at the table slot its insert found
+// Runs of equal voxel ids in consecutive lanes (points of a sweep arrive in scan
+// order, so a coarse voxel's points are mostly consecutive): one atomic per run,
+// by its first lane, instead of one per point -- a stride-16 voxel can hold 10^3
+// points.  run_of gives a lane its run's first lane and the run's length.
+__device__ inline void run_of(int32_t v, int& first, int& len) {
+    const int lane = threadIdx.x & 63;
+    const int32_t prev = __shfl_up(v, 1, 64);
+    const uint64_t heads = __ballot(lane == 0 || prev != v);
+    first = 63 - __clzll(heads & (~0ull >> (63 - lane)));
+    const uint64_t later = heads & ~((2ull << first) - 1ull);  // heads after the run's first lane
+    len = (later ? __builtin_ctzll(later) : 64) - first;
+}
+
 __global__ void k_vox_lookup(Table t, const uint32_t* pslot, int64_t n, int32_t* pt2vox, int32_t* counts) {
-    int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    if (k >= n) return;
-    const uint32_t ps = pslot[k];
-    int32_t v = (ps == kNoSlot) ? -1 : t.vals[ps];
-    pt2vox[k] = v;
-    if (v >= 0) atomicAdd(&counts[v], 1);
+    const int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    int32_t v = -1;
+    if (k < n) {
+        const uint32_t ps = pslot[k];
+        v = (ps == kNoSlot) ? -1 : t.vals[ps];
+        pt2vox[k] = v;
+    }
+    int first, len;
+    run_of(v, first, len);
+    if (v >= 0 && (int)(threadIdx.x & 63) == first) atomicAdd(&counts[v], len);
 }
 
 __global__ void k_vox_fill(const int32_t* pt2vox, int64_t n, const int32_t* seg, int32_t* fill, int32_t* plist) {
-    int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    if (k >= n) return;
-    int32_t v = pt2vox[k];
-    if (v < 0) return;
-    int32_t pos = seg[v] + atomicAdd(&fill[v], 1);
-    plist[pos] = (int32_t)k;
+    const int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    const int32_t v = k < n ? pt2vox[k] : -1;
+    int first, len;
+    run_of(v, first, len);
+    const int lane = threadIdx.x & 63;
+    int base = 0;
+    if (v >= 0 && lane == first) base = atomicAdd(&fill[v], len);
+    base = __shfl(base, first, 64);
+    if (v >= 0) plist[seg[v] + base + (lane - first)] = (int32_t)k;
 }
 
 
