@@ -200,7 +200,7 @@ spv_status spv_sparse_conv_sliced(void* stream, void* ws, size_t ws_bytes,
  * spv_sparse_conv_nbr -- spv_sparse_conv_sliced on such a table: the
  * neighbour-table conv kernel without the per-call plan (no table build, only
  * the weight packing).  Only the shapes that kernel takes: bf16/f16 with Cin,
- * Cout in {32, 64, 96, 128} or Cin = Cout = 256 (else SPV_ERR_UNSUPPORTED).
+ * Cout in {32, 64, 96, 128, 256} (else SPV_ERR_UNSUPPORTED).
  * In:  nbr [m_out_cap][27] from spv_kernel_map_nbr on the output voxels (the
  *      inputs are the same voxels: in_rows = their count); every other
  *      argument as in spv_sparse_conv_sliced.

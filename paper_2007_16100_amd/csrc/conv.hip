@@ -13,7 +13,7 @@
 //   wave's gathers for the next offset are in flight while the current one is
 //   multiplied.  The cost is MFMA work on absent neighbours: on a LiDAR sweep
 //   the 16-row unions of present offsets are ~3x the pairs.  Widths C_in,
-//   C_out in {32, 64, 96, 128}; submanifold and strided 3x3x3 maps.
+//   C_out in {32, 64, 96, 128, 256}; submanifold and strided 3x3x3 maps.
 //
 // * k_conv_tile (K = 2 maps, transposed maps -- where a 16-row union would be
 //   mostly empty -- and the other widths): output rows in tiles of T with an

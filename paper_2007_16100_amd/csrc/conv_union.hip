@@ -214,13 +214,13 @@ __global__ __launch_bounds__(64 * NW) void k_conv_union(
     }
 }
 
-// instantiated for C_in, C_out in {32, 64, 96, 128} (the widths of the blocks
-// and networks built here, square layers and the channel changes between
-// stages); other shapes use the tile kernel
+// instantiated for C_in, C_out in {32, 64, 96, 128, 256} (the widths of the
+// blocks and networks built here, square layers and the channel changes
+// between stages); other shapes use the tile kernel
 bool union_supported(int K3, int Cin, int Cout, int dt) {
     if (K3 != 27 || dt == SPV_F32) return false;
-    const auto width_ok = [](int c) { return c == 32 || c == 64 || c == 96 || c == 128; };
-    return (width_ok(Cin) && width_ok(Cout)) || (Cin == 256 && Cout == 256);
+    const auto width_ok = [](int c) { return c == 32 || c == 64 || c == 96 || c == 128 || c == 256; };
+    return width_ok(Cin) && width_ok(Cout);
 }
 
 // Launch shape per width: 11 waves of 2 blocks (352 rows per workgroup: a
@@ -232,8 +232,9 @@ template <int DT, int KCH, int NB>
 static void launch_union_c(hipStream_t s, const ConvPlan& p, const void* in, int64_t in_rows, const void* wpack,
                            const float* scale, const float* shift, int relu, void* out) {
     constexpr int FR = KCH * NB;
-    // 256 -> 256: 8 waves (256 registers each), one offset's 128 KB of weights per phase
-    constexpr int RB = FR >= 32 ? 1 : 2, NW = FR >= 128 ? 8 : 11;
+    // 256 channels in or out: 8 waves (256 registers each); 256 -> 256 holds one
+    // offset's 128 KB of weights per phase
+    constexpr int RB = FR >= 32 ? 1 : 2, NW = (NB >= 16 || KCH >= 8) ? 8 : 11;
     constexpr int PH = (128 / FR) < kUK3 ? (128 / FR) : kUK3;  // 27, 14, 7, 4 for C -> C = 32, 64, 96, 128
     constexpr int64_t rows_wg = (int64_t)NW * RB * 16;
     // a multiple of 8 workgroups: the kernel spreads the live tiles over the 8 XCDs
@@ -251,21 +252,19 @@ static void launch_union_cin(hipStream_t s, const ConvPlan& p, const void* in, i
         case 64: launch_union_c<DT, KCH, 4>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
         case 96: launch_union_c<DT, KCH, 6>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
         case 128: launch_union_c<DT, KCH, 8>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
+        case 256: launch_union_c<DT, KCH, 16>(s, p, in, in_rows, wpack, scale, shift, relu, out); break;
     }
 }
 
 template <int DT>
 static void launch_union(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int Cout, int64_t in_rows,
                          const void* wpack, const float* scale, const float* shift, int relu, void* out) {
-    if (Cin == 256) {
-        launch_union_c<DT, 8, 16>(s, p, in, in_rows, wpack, scale, shift, relu, out);
-        return;
-    }
     switch (Cin) {
         case 32: launch_union_cin<DT, 1>(s, p, in, Cout, in_rows, wpack, scale, shift, relu, out); break;
         case 64: launch_union_cin<DT, 2>(s, p, in, Cout, in_rows, wpack, scale, shift, relu, out); break;
         case 96: launch_union_cin<DT, 3>(s, p, in, Cout, in_rows, wpack, scale, shift, relu, out); break;
         case 128: launch_union_cin<DT, 4>(s, p, in, Cout, in_rows, wpack, scale, shift, relu, out); break;
+        case 256: launch_union_cin<DT, 8>(s, p, in, Cout, in_rows, wpack, scale, shift, relu, out); break;
     }
 }
 

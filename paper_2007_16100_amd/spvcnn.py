@@ -59,11 +59,12 @@ class SPVCNN:
         self.v = voxel_size
         self.mode = mode
         self.device = device
-        # the input channels are padded with zeros to a multiple of 8 (the matrix cores' K
-        # granularity is 8 16-bit values per lane): the stem conv and the first point MLP get
-        # zero weight rows for them, which adds exact zeros
+        # the input channels are padded with zeros to 32, the narrowest width of the
+        # neighbour-table conv kernel (whose matrix-core K step is 32 channels), so that the stem
+        # runs on the stride's neighbour table like every other 3x3x3 conv: the stem conv and the
+        # first point MLP get zero weight rows for them, which adds exact zeros
         self.c_in = params["stem.0"][0].shape[1]
-        self.c_pad = self.c_in if self.dt == torch.float32 else (self.c_in + 7) // 8 * 8
+        self.c_pad = self.c_in if self.dt == torch.float32 else (self.c_in + 31) // 32 * 32
         self.P = {}
         for name, (W, sc, sh) in params.items():
             if name in ("stem.0", "point.0") and self.c_pad != self.c_in:
@@ -117,8 +118,8 @@ class SPVCNN:
         neighbour-table kernel takes the shape, else on the pairs (built once per stride)."""
         W, sc, sh = self.P[name]
         Cin, Cout = x.shape[1], W.shape[2]
-        widths = (32, 64, 96, 128)
-        if self.dt != torch.float32 and ((Cin in widths and Cout in widths) or (Cin == 256 and Cout == 256)):
+        widths = (32, 64, 96, 128, 256)
+        if self.dt != torch.float32 and Cin in widths and Cout in widths:
             return spv.spv_sparse_conv_nbr(self.ws, x, plan.nbr[s], W, Cout, plan.m[s], scale=sc,
                                            shift=sh if shift else None, relu=relu, res=res, cin_offset=cin_offset)
         if plan.subm[s] is None:

@@ -331,7 +331,9 @@ def run_conv(spv, x, off, pairs, W, m_out, dtype, scale=None, shift=None, relu=F
                                                (32, 64, "bf16", True), (64, 128, "f16", False),
                                                (128, 64, "bf16", True), (96, 32, "bf16", False),
                                                (128, 128, "bf16", True), (64, 96, "f16", True),
-                                               (256, 256, "bf16", True), (192, 256, "f16", False)])
+                                               (256, 256, "bf16", True), (192, 256, "f16", False),
+                                               (128, 256, "f16", True), (256, 64, "bf16", False),
+                                               (32, 256, "bf16", True)])
 def test_conv_submanifold_sweep(spv, sweep, cin, cout, dtype, bn):
     rc, _, _, _ = oracle.voxelize(sweep[::3] if cout >= 256 else sweep, 0.05)
     _, off, pairs = oracle.kernel_map(rc)
