@@ -105,11 +105,9 @@ class SPVCNN:
         return Plan(coords, m, down, nbr, [None] * 5), vox
 
     # -- layers --------------------------------------------------------------
-    def _conv(self, x, name, km, m_out, relu=True, transposed=False, res=None, cin_offset=0, cout=None,
-              shift=True):
+    def _conv(self, x, name, km, m_out, relu=True, transposed=False, res=None, cin_offset=0, shift=True):
         W, sc, sh = self.P[name]
-        Cout = W.shape[2] if cout is None else cout
-        return spv.spv_sparse_conv_sliced(self.ws, x, km.off, km.pairs, W, x.shape[1], Cout, m_out, scale=sc,
+        return spv.spv_sparse_conv_sliced(self.ws, x, km.off, km.pairs, W, x.shape[1], W.shape[2], m_out, scale=sc,
                                           shift=sh if shift else None, relu=relu, transposed=transposed, res=res,
                                           cin_offset=cin_offset)
 
