@@ -215,6 +215,43 @@ spv_status spv_sparse_conv_nbr(void* stream, void* ws, size_t ws_bytes,
                                spv_dtype dt);
 
 /*
+ * The transposed k=2 s=2 conv (a decoder's upsampling) on the stride-2 map's
+ * child table:
+ *
+ * spv_map_children -- children[j][k] = i + 1 for every pair (fine i, coarse j)
+ * of offset k of a K=2 stride-2 map from spv_kernel_map, 0 where coarse voxel j
+ * has no child at offset k.  Pairs past pair_cap or with rows outside
+ * [0, fine_rows) / [0, coarse count) are ignored; a map with unsorted or
+ * repeated pairs sets SPV_ERR_INVALID_ARG in the workspace status.
+ * In:  off [9], pairs [pair_cap][2] (device); m_coarse_dev: device count of the
+ *      coarse voxels (NULL = m_coarse_cap).
+ * Out: children [m_coarse_cap][8] int32 (16-byte aligned).
+ *
+ * spv_sparse_conv_up -- for every coarse row j < count and offset k with
+ * children[j][k] = i + 1 (i < out_rows):
+ *   out[i] = act(scale * (in[j] @ W[k][:Cin][:Cout]) + shift + res[i])
+ * which is spv_sparse_conv_sliced(transposed = 1) on that map whenever every
+ * output row is some coarse voxel's child -- always the case for the fine
+ * voxels a stride-2 spv_kernel_map was built on.  Output rows that are no
+ * child are not written.  Each product row is stored once, straight from the
+ * matrix-core accumulators (no gathers, no accumulation across pairs).
+ * In:  in [m_in_cap][Cin] coarse rows (dt); children from spv_map_children;
+ *      W [8][Cin_full][Cout_full] (dt) with the slicing of
+ *      spv_sparse_conv_sliced; scale/shift f32 or NULL; res [out_rows][Cout]
+ *      (dt) or NULL.  bf16/f16 with Cin, Cout in {32, 64, 96, 128, 256}, else
+ *      SPV_ERR_UNSUPPORTED.
+ * Out: out [out_rows][Cout] (dt).
+ */
+spv_status spv_map_children(void* stream, void* ws, size_t ws_bytes,
+                            const int32_t* off, const int32_t* pairs, int64_t pair_cap, int64_t fine_rows,
+                            const int64_t* m_coarse_dev, int64_t m_coarse_cap, int32_t* children);
+spv_status spv_sparse_conv_up(void* stream, void* ws, size_t ws_bytes,
+                              const void* in, const int64_t* m_in_dev, int64_t m_in_cap, int32_t Cin,
+                              const int32_t* children, const void* W, int32_t Cin_full, int32_t Cout_full,
+                              const float* scale, const float* shift, const void* res, int32_t relu,
+                              void* out, int64_t out_rows, int32_t Cout, spv_dtype dt);
+
+/*
  * Backward passes (training, Sec. 4.2 trains the super network end to end).
  *
  * spv_sparse_conv_dgrad -- input gradient of spv_sparse_conv (without its

@@ -43,6 +43,7 @@ spv_status sync_status(hipStream_t s, const Header* h, Header* out) {
 bool valid_dt(int dt) { return dt == SPV_F32 || dt == SPV_BF16 || dt == SPV_F16; }
 size_t esize(int dt) { return dt == SPV_F32 ? 4 : 2; }
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+constexpr int kUpChildren = 8;  // offsets of a k=2 s=2 map
 bool valid_v(float v) { return isfinite(v) && v > 0.0f; }
 
 // --- workspace layouts (a null base gives the size) -----------------------------
@@ -387,6 +388,43 @@ spv_status spv_sparse_conv_nbr(void* stream, void* ws, size_t ws_bytes, const vo
     p.res = res;
     launch_pack_job(s, conv_pack_job(27, W, L.wpack, Cin, Cout, dt, Cout_full, (int64_t)Cin_full * Cout_full));
     launch_conv_union(s, p, in, Cin, in_rows, Cout, L.wpack, scale, shift, relu, out, dt);
+    return hip_check();
+}
+
+spv_status spv_map_children(void* stream, void* ws, size_t ws_bytes, const int32_t* off, const int32_t* pairs,
+                            int64_t pair_cap, int64_t fine_rows, const int64_t* m_coarse_dev, int64_t m_coarse_cap,
+                            int32_t* children) {
+    if (!ws || !off || pair_cap < 0 || fine_rows < 0 || m_coarse_cap < 0 || m_coarse_cap >= ((int64_t)1 << 31))
+        return SPV_ERR_INVALID_ARG;
+    if ((pair_cap > 0 && !pairs) || (m_coarse_cap > 0 && !children) || !aligned16(children)) return SPV_ERR_INVALID_ARG;
+    if (need(sizeof(Header), ws_bytes)) return SPV_ERR_CAPACITY;
+    if (m_coarse_cap == 0) return SPV_OK;
+    launch_nbr_table((hipStream_t)stream, off, pairs, kUpChildren, pair_cap, m_coarse_dev, m_coarse_cap, fine_rows,
+                     children, (Header*)ws);
+    return hip_check();
+}
+
+spv_status spv_sparse_conv_up(void* stream, void* ws, size_t ws_bytes, const void* in, const int64_t* m_in_dev,
+                              int64_t m_in_cap, int32_t Cin, const int32_t* children, const void* W, int32_t Cin_full,
+                              int32_t Cout_full, const float* scale, const float* shift, const void* res, int32_t relu,
+                              void* out, int64_t out_rows, int32_t Cout, spv_dtype dt) {
+    if (!ws || m_in_cap < 0 || m_in_cap >= ((int64_t)1 << 31) || out_rows < 0 || Cin <= 0 || Cout <= 0 || !W ||
+        !valid_dt(dt) || Cin > Cin_full || Cout > Cout_full)
+        return SPV_ERR_INVALID_ARG;
+    if (!up_supported(Cin, Cout, dt)) return SPV_ERR_UNSUPPORTED;
+    if ((m_in_cap > 0 && (!in || !children)) || (out_rows > 0 && !out)) return SPV_ERR_INVALID_ARG;
+    if (!aligned16(in) || !aligned16(out) || !aligned16(W) || !aligned16(res) || (res && res == out) || in == out)
+        return SPV_ERR_INVALID_ARG;
+    Arena probe(nullptr, 0);
+    plan_wpack_ws(probe, kUpChildren, Cin, Cout);
+    if (need(probe.used, ws_bytes)) return SPV_ERR_CAPACITY;
+    Arena a(ws, ws_bytes);
+    void* wpack = plan_wpack_ws(a, kUpChildren, Cin, Cout);
+    if (m_in_cap == 0) return SPV_OK;
+    hipStream_t s = (hipStream_t)stream;
+    launch_pack_job(s, conv_pack_job(kUpChildren, W, wpack, Cin, Cout, dt, Cout_full, (int64_t)Cin_full * Cout_full));
+    UpArgs u{children, m_in_dev, m_in_cap, in, Cin, Cout, (int)dt, scale, shift, relu, res, out, out_rows};
+    launch_conv_up(s, u, wpack);
     return hip_check();
 }
 

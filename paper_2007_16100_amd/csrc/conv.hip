@@ -184,6 +184,16 @@ __global__ void k_nbr_scatter(const int32_t* off, const int32_t* pairs, int K3, 
     }
 }
 
+void launch_nbr_table(hipStream_t s, const int32_t* off, const int32_t* pairs, int K3, int64_t pair_bound,
+                      const int64_t* m_out_dev, int64_t m_cap, int64_t in_rows, int32_t* nbr, Header* h) {
+    unsigned gc = blocks_for(m_cap * K3, 1024);
+    if (gc > 2048) gc = 2048;
+    k_nbr_clear<<<gc, 256, 0, s>>>(nbr, m_out_dev, m_cap, K3, h, PackJob{});
+    unsigned g = blocks_for(pair_bound + K3, 256);
+    if (g > 2048) g = 2048;
+    k_nbr_scatter<<<g, 256, 0, s>>>(off, pairs, K3, 0, pair_bound, m_out_dev, m_cap, in_rows, nbr, h);
+}
+
 void launch_conv_plan(hipStream_t s, const ConvPlan& p, const int32_t* off, const int32_t* pairs, int K3,
                       int transposed, int64_t pair_bound, int64_t in_rows, const PackJob& pk, bool clear_header) {
     unsigned g = blocks_for(pair_bound + K3, 256);

@@ -262,6 +262,27 @@ void* plan_linear_ws(Arena& a, int Cin, int Cout);
 // packs W into wpack (MFMA path) and runs the layer
 void launch_linear(hipStream_t s, const LinearArgs& a, void* wpack);
 
+// --- transposed k=2 s=2 conv on a child table (conv_up.hip) -----------------------
+struct UpArgs {
+    const int32_t* children;  // [m_cap][8]: fine row + 1 of the child at offset k, 0 = none
+    const int64_t* m_dev;     // coarse row count (nullptr = m_cap)
+    int64_t m_cap;
+    const void* in;           // [m_cap][Cin] coarse rows
+    int Cin, Cout, dt;
+    const float* scale;
+    const float* shift;
+    int relu;
+    const void* res;          // [out_rows][Cout] or nullptr
+    void* out;                // [out_rows][Cout] fine rows
+    int64_t out_rows;
+};
+bool up_supported(int Cin, int Cout, int dt);
+void launch_conv_up(hipStream_t s, const UpArgs& a, const void* wpack);
+// the neighbour table nbr[j][k] = i + 1 of a map's pairs (i, j) (rows by output),
+// cleared first; unsorted or repeated pairs raise the header's flags
+void launch_nbr_table(hipStream_t s, const int32_t* off, const int32_t* pairs, int K3, int64_t pair_bound,
+                      const int64_t* m_out_dev, int64_t m_cap, int64_t in_rows, int32_t* nbr, Header* h);
+
 // --- backward passes (backward.hip) --------------------------------------------
 struct WgradArgs {
     const void* x;           // [x_rows][Cin] conv input

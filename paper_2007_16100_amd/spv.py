@@ -30,7 +30,8 @@ _DT = {torch.float32: SPV_F32, torch.bfloat16: SPV_BF16, torch.float16: SPV_F16}
 
 # every symbol include/spv.h declares
 EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced",
-           "spv_linear", "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_sparse_conv_dgrad", "spv_wgrad_workspace_bytes", "spv_sparse_conv_wgrad",
+           "spv_linear", "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_map_children", "spv_sparse_conv_up",
+           "spv_sparse_conv_dgrad", "spv_wgrad_workspace_bytes", "spv_sparse_conv_wgrad",
            "spv_voxelize_backward",
            "spv_devoxelize_backward", "spv_devoxelize",
            "spv_block_workspace_bytes", "spv_block", "spv_lookup", "spv_status_check", "spv_status_string",
@@ -78,6 +79,9 @@ def lib():
         L.spv_kernel_map_nbr.argtypes = [vp, vp, sz, vp, vp, i64, vp]
         L.spv_sparse_conv_nbr.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i32, i32, vp, vp, vp, i32, vp, vp, i64, i32,
                                           i32]
+        L.spv_map_children.argtypes = [vp, vp, sz, vp, vp, i64, i64, vp, i64, vp]
+        L.spv_sparse_conv_up.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, vp, i32, i32, vp, vp, vp, i32, vp, i64, i32,
+                                         i32]
         L.spv_sparse_conv_dgrad.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i64, i32, i32, vp, vp, vp, i64, i32, i32]
         L.spv_sparse_conv_wgrad.argtypes = [vp, vp, sz, vp, i64, i32, vp, i64, i32, vp, vp, i64, i32, i32, vp, i32]
         L.spv_wgrad_workspace_bytes.argtypes = [i32, i32, i32]
@@ -93,7 +97,8 @@ def lib():
         L.spv_status_string.restype = ct.c_char_p
         L.spv_last_hip_error.argtypes = []
         for f in ("spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced", "spv_linear",
-                  "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_sparse_conv_dgrad", "spv_sparse_conv_wgrad",
+                  "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_map_children", "spv_sparse_conv_up",
+                  "spv_sparse_conv_dgrad", "spv_sparse_conv_wgrad",
                   "spv_voxelize_backward",
                   "spv_devoxelize_backward", "spv_devoxelize", "spv_block", "spv_lookup", "spv_status_check"):
             getattr(L, f).restype = ct.c_int
@@ -309,6 +314,36 @@ def spv_sparse_conv_nbr(ws: Workspace, x: torch.Tensor, nbr: torch.Tensor, W_ful
                                    Cout_full, _ptr(scale), _ptr(shift), _ptr(res), int(relu), _ptr(out),
                                    _ptr(m_out_dev), m_out_cap, Cout, _DT[x.dtype])
     _chk(st, "spv_sparse_conv_nbr")
+    return out
+
+
+def spv_map_children(ws: Workspace, off: torch.Tensor, pairs: torch.Tensor, fine_rows: int, m_coarse: int,
+                     m_coarse_dev: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """children [m_coarse][8] int32 of a K=2 stride-2 map: fine row + 1 per offset, 0 = none."""
+    if out is None:
+        out = torch.empty((max(m_coarse, 1), 8), dtype=torch.int32, device=off.device)
+    st = lib().spv_map_children(_stream(), ws.ptr, ws.nbytes, _ptr(off), _ptr(pairs), pairs.shape[0], fine_rows,
+                                _ptr(m_coarse_dev), m_coarse, _ptr(out))
+    _chk(st, "spv_map_children")
+    return out
+
+
+def spv_sparse_conv_up(ws: Workspace, x: torch.Tensor, children: torch.Tensor, W_full: torch.Tensor, Cout: int,
+                       out_rows: int, m_in_dev: Optional[torch.Tensor] = None, scale: Optional[torch.Tensor] = None,
+                       shift: Optional[torch.Tensor] = None, relu: bool = False, res: Optional[torch.Tensor] = None,
+                       cin_offset: int = 0, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The transposed k=2 s=2 conv of the coarse rows x onto the fine rows, from the child table."""
+    K3, Cin_full, Cout_full = W_full.shape
+    Cin = x.shape[1]
+    if K3 != 8 or cin_offset < 0 or cin_offset + Cin > Cin_full:
+        raise ValueError("W_full must be [8][Cin_full][Cout_full] holding the input-channel slice")
+    if out is None:
+        out = torch.empty((max(out_rows, 1), Cout), dtype=x.dtype, device=x.device)
+    wp = ct.c_void_p(_ptr(W_full).value + cin_offset * Cout_full * W_full.element_size())
+    st = lib().spv_sparse_conv_up(_stream(), ws.ptr, ws.nbytes, _ptr(x), _ptr(m_in_dev), x.shape[0], Cin,
+                                  _ptr(children), wp, Cin_full, Cout_full, _ptr(scale), _ptr(shift), _ptr(res),
+                                  int(relu), _ptr(out), out_rows, Cout, _DT[x.dtype])
+    _chk(st, "spv_sparse_conv_up")
     return out
 
 

@@ -16,6 +16,8 @@ holds the device buffers:
   one synchronization per stride to size what follows exactly; every 3x3x3 conv
   the neighbour-table kernel takes runs on that table (no per-call plan), the
   others on the stride's pairs, built on first use;
+* the transposed stride-2 convs run on the stride-2 maps' child tables: every
+  fine voxel has its parent, so each output row is one product row, stored once;
 * a conv over a skip concatenation [t; x] runs as two sliced convs,
   W_t t (scaled, unshifted) handed as the residual input of W_x x + shift;
   the 1x1 shortcut over it likewise as two linear layers;
@@ -50,6 +52,7 @@ class Plan:
     down: List[Optional[spv.KernelMap]]   # down[s]: stride 2^(s-1) -> 2^s (s = 1..4)
     nbr: List[torch.Tensor]         # submanifold neighbour table [m_s][27] per stride
     subm: List[Optional[spv.KernelMap]]   # submanifold pairs, built on first use
+    children: List[Optional[torch.Tensor]]  # children[s]: child table [m_s][8] of down[s]
 
 
 class SPVCNN:
@@ -102,7 +105,8 @@ class SPVCNN:
             m.append(ms)
             coords.append(km.out_coords[:ms])
         nbr = [spv.spv_kernel_map_nbr(ws, c) for c in coords]
-        return Plan(coords, m, down, nbr, [None] * 5), vox
+        children = [None] + [spv.spv_map_children(ws, down[s].off, down[s].pairs, m[s - 1], m[s]) for s in range(1, 5)]
+        return Plan(coords, m, down, nbr, [None] * 5, children), vox
 
     # -- layers --------------------------------------------------------------
     def _conv(self, x, name, km, m_out, relu=True, transposed=False, res=None, cin_offset=0, shift=True):
@@ -189,7 +193,14 @@ class SPVCNN:
         z = self._fuse(plan, x, 4, z, "point.1", xyz, batch)
 
         def up(y, u):
-            t = self._conv(y, f"up.{u}", plan.down[5 - u], m[4 - u], transposed=True)
+            W, sc, sh = self.P[f"up.{u}"]
+            widths = (32, 64, 96, 128, 256)
+            if self.dt != torch.float32 and y.shape[1] in widths and W.shape[2] in widths:
+                # every fine voxel has its parent: the child-table kernel writes each output row once
+                t = spv.spv_sparse_conv_up(self.ws, y, plan.children[5 - u], W, W.shape[2], m[4 - u], scale=sc,
+                                           shift=sh, relu=True)
+            else:
+                t = self._conv(y, f"up.{u}", plan.down[5 - u], m[4 - u], transposed=True)
             y = self._resblock(plan, [t, skips[4 - u]], f"dec.{u}.0", 4 - u)
             return self._resblock(plan, [y], f"dec.{u}.1", 4 - u)
 

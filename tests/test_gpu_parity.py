@@ -776,3 +776,51 @@ def test_conv_on_neighbour_table_rejects_other_shapes(spv):
     with pytest.raises(spv.SpvError) as e:
         spv.spv_sparse_conv_nbr(ws, x, nbr, W, 48, 4)
     assert e.value.status == spv.SPV_ERR_UNSUPPORTED
+
+
+# ---------------------------------------------------------------------------
+# the transposed k=2 s=2 conv on the child table
+# ---------------------------------------------------------------------------
+def test_map_children_matches_pairs(spv, sweep):
+    rc, _, _, _ = oracle.voxelize(sweep, 0.05)
+    oc, off, pairs = oracle.kernel_map(rc, 2, 2)
+    ws = spv.Workspace.for_ops(len(rc), 16)
+    got = host(spv.spv_map_children(ws, dev(off), dev(pairs), len(rc), len(oc)))[: len(oc)]
+    want = np.zeros((len(oc), 8), np.int32)
+    for k in range(8):
+        p = pairs[off[k]:off[k + 1]]
+        want[p[:, 1], k] = p[:, 0] + 1
+    np.testing.assert_array_equal(got, want)
+    assert spv.spv_status_check(ws) == spv.SPV_OK
+
+
+@pytest.mark.parametrize("cin,cout,dtype,res", [(128, 64, "bf16", False), (96, 96, "bf16", True),
+                                                (256, 128, "f16", False), (256, 256, "bf16", True),
+                                                (32, 96, "bf16", False)])
+def test_conv_up(spv, sweep, cin, cout, dtype, res):
+    """The child-table upsampling conv equals the transposed conv on the pairs (every fine
+    voxel has its parent), against the oracle."""
+    rc, _, _, _ = oracle.voxelize(sweep, 0.05)
+    oc, off, pairs = oracle.kernel_map(rc, 2, 2)
+    x = synth.normal((len(oc), cin), 1301, dtype=dtype)
+    W = synth.conv_weight(8, cin, cout, 1302, dtype)
+    sc, sh = synth.folded_bn(cout, 1303)
+    r = synth.normal((len(rc), cout), 1304, dtype=dtype) if res else None
+    ws = spv.Workspace.for_ops(len(rc), max(cin, cout))
+    ch = spv.spv_map_children(ws, dev(off), dev(pairs), len(rc), len(oc))
+    out = torch.full((len(rc), cout), 7.0, dtype=TD[dtype], device="cuda")
+    spv.spv_sparse_conv_up(ws, dev(x, dtype), ch, dev(W, dtype), cout, len(rc), scale=dev(sc), shift=dev(sh),
+                           relu=True, res=None if r is None else dev(r, dtype), out=out)
+    got = host(out, dtype)
+    ref = oracle.sparse_conv(x, off, pairs, W, len(rc), dtype, sc, sh, True, transposed=True, res=r)
+    check_close(got, ref, dtype)
+
+
+def test_conv_up_rejects_other_shapes(spv):
+    ws = spv.Workspace.for_ops(16, 48)
+    x = torch.zeros((4, 48), dtype=torch.bfloat16, device="cuda")
+    ch = torch.zeros((4, 8), dtype=torch.int32, device="cuda")
+    W = torch.zeros((8, 48, 48), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(spv.SpvError) as e:
+        spv.spv_sparse_conv_up(ws, x, ch, W, 48, 4)
+    assert e.value.status == spv.SPV_ERR_UNSUPPORTED
