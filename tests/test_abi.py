@@ -81,6 +81,31 @@ def test_host_side_validation_without_gpu():
     st = L.spv_linear(None, ws, 16, ct.c_void_p(16), None, 4, 32, ct.c_void_p(16), 32, 32, None, None, 0, None,
                       0, ct.c_void_p(48), 32, 1)
     assert st == spv.SPV_ERR_CAPACITY
+    # neighbour-table conv: a width the kernel does not take; a missing table
+    st = L.spv_sparse_conv_nbr(None, ws, 1 << 30, ct.c_void_p(16), 4, 48, ct.c_void_p(16), ct.c_void_p(16), 48, 48,
+                               None, None, None, 0, ct.c_void_p(32), None, 4, 48, 1)
+    assert st == spv.SPV_ERR_UNSUPPORTED
+    st = L.spv_sparse_conv_nbr(None, ws, 1 << 30, ct.c_void_p(16), 4, 32, None, ct.c_void_p(16), 32, 32,
+                               None, None, None, 0, ct.c_void_p(32), None, 4, 32, 1)
+    assert st == spv.SPV_ERR_INVALID_ARG
+    # child-table upsampling: f32 is not taken; children misaligned
+    st = L.spv_sparse_conv_up(None, ws, 1 << 30, ct.c_void_p(16), None, 4, 32, ct.c_void_p(16), ct.c_void_p(16), 32,
+                              32, None, None, None, 0, ct.c_void_p(32), 8, 32, 0)
+    assert st == spv.SPV_ERR_UNSUPPORTED
+    st = L.spv_map_children(None, ws, 1 << 30, ct.c_void_p(16), ct.c_void_p(16), 4, 8, None, 4, ct.c_void_p(20))
+    assert st == spv.SPV_ERR_INVALID_ARG
+    # weight gradient: Cin * Cout too large; workspace too small
+    st = L.spv_sparse_conv_wgrad(None, ws, 1 << 30, ct.c_void_p(16), 4, 512, ct.c_void_p(16), 4, 256,
+                                 ct.c_void_p(16), ct.c_void_p(16), 4, 27, 0, ct.c_void_p(16), 1)
+    assert st == spv.SPV_ERR_UNSUPPORTED
+    st = L.spv_sparse_conv_wgrad(None, ws, 1024, ct.c_void_p(16), 4, 32, ct.c_void_p(16), 4, 32,
+                                 ct.c_void_p(16), ct.c_void_p(16), 4, 27, 0, ct.c_void_p(16), 1)
+    assert st == spv.SPV_ERR_CAPACITY
+    assert L.spv_wgrad_workspace_bytes(27, 32, 32) >= 27 * 32 * 32 * 4
+    assert L.spv_wgrad_workspace_bytes(27, 0, 32) == 0
+    # backward of the scatter-mean / devox: negative sizes
+    assert L.spv_voxelize_backward(None, None, -1, 4, None, None, 0, None, 1) == spv.SPV_ERR_INVALID_ARG
+    assert L.spv_devoxelize_backward(None, None, None, None, 4, 8, None, 4, 1) == spv.SPV_ERR_INVALID_ARG
     # misaligned feature pointer
     st = L.spv_sparse_conv(None, ws, 1 << 30, ct.c_void_p(18), 4, 8, ct.c_void_p(16), ct.c_void_p(16), 4, 27, 0,
                            ct.c_void_p(16), None, None, 0, ct.c_void_p(16), None, 4, 16, 1)
