@@ -351,7 +351,7 @@ __global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __
     }
 }
 
-// 16-bit features, C in {16, 32, 64, 96, 128} and Cp <= 128 (LDS: the Wp
+// 16-bit features, C in {16, 32, 64, 96, 128, 256} and Cp <= 128 (LDS: the Wp
 // fragments plus each wave's row tile); everything else takes the generic path
 bool devox_mfma_supported(int C, int Cp, int dt) {
     if (dt == SPV_F32 || C % 16 != 0) return false;
