@@ -824,3 +824,40 @@ def test_conv_up_rejects_other_shapes(spv):
     with pytest.raises(spv.SpvError) as e:
         spv.spv_sparse_conv_up(ws, x, ch, W, 48, 4)
     assert e.value.status == spv.SPV_ERR_UNSUPPORTED
+
+
+# ---------------------------------------------------------------------------
+# empty inputs of the later entry points
+# ---------------------------------------------------------------------------
+def test_empty_inputs_of_network_entry_points(spv):
+    """Zero rows: every entry point returns SPV_OK and writes nothing it should not; the
+    weight gradient of an empty map is zero, the devox gradient of no points is zero."""
+    d = "cuda"
+    ws = spv.Workspace.for_ops(16, 64)
+    e32 = torch.zeros((0, 32), dtype=torch.bfloat16, device=d)
+    W = torch.ones((32, 32), dtype=torch.bfloat16, device=d)
+    out = spv.spv_linear(ws, e32, W)
+    assert out.shape[0] == 1  # capacity floor of the binding; nothing to compute
+    nbr = spv.spv_kernel_map_nbr(ws, torch.zeros((0, 4), dtype=torch.int32, device=d))
+    assert nbr.shape == (1, 27)
+    W27 = torch.ones((27, 32, 32), dtype=torch.bfloat16, device=d)
+    spv.spv_sparse_conv_nbr(ws, e32, nbr, W27, 32, 0)
+    W8 = torch.ones((8, 32, 32), dtype=torch.bfloat16, device=d)
+    ch = torch.zeros((1, 8), dtype=torch.int32, device=d)
+    spv.spv_sparse_conv_up(ws, e32, ch, W8, 32, 0)
+    off = torch.zeros(28, dtype=torch.int32, device=d)
+    pairs = torch.zeros((1, 2), dtype=torch.int32, device=d)
+    wsw = spv.Workspace.for_wgrad(27, 32, 32)
+    dW = spv.spv_sparse_conv_wgrad(wsw, torch.zeros((4, 32), dtype=torch.bfloat16, device=d),
+                                   torch.zeros((4, 32), dtype=torch.bfloat16, device=d), off, pairs, 27)
+    assert torch.count_nonzero(dW).item() == 0
+    dv = spv.spv_devoxelize_backward(torch.zeros((0, 8), dtype=torch.int32, device=d),
+                                     torch.zeros((0, 8), dtype=torch.float32, device=d),
+                                     torch.zeros((0, 16), dtype=torch.bfloat16, device=d), 5,
+                                     out=torch.full((5, 16), 3.0, dtype=torch.float32, device=d))
+    assert torch.count_nonzero(dv).item() == 0
+    spv.spv_voxelize_backward(torch.zeros((3, 16), dtype=torch.bfloat16, device=d),
+                              torch.ones(3, dtype=torch.int32, device=d), torch.zeros(0, dtype=torch.int32, device=d),
+                              3)
+    torch.cuda.synchronize()
+    assert spv.spv_status_check(ws) == spv.SPV_OK
