@@ -98,6 +98,32 @@ spv_status spv_voxelize(void* stream, void* ws, size_t ws_bytes,
                         int64_t* m_dev, int64_t* m_host);
 
 /*
+ * spv_voxelize_onto -- the scatter-mean of Eq. 2 onto a given voxel set (the
+ * re-voxelization of Sec. 3.3's later SPVConv modules, whose voxels at each
+ * stride are already known): point k belongs to the voxel of coords whose
+ * coordinates equal its Eq. 1 key at voxel_size;
+ *   f_j = (1/N_j) sum of the features of the points of voxel j,
+ * summed exactly for 16-bit features (fp64) and rounded once to dt; a voxel
+ * of the set that no point falls into gets N_j = 0 and f_j = 0, and a point
+ * whose voxel is not in the set gets pt2vox = -1 and adds to nothing.  No sort:
+ * a hash table of the given set, one probe per point, a counting sort of the
+ * points by voxel.  With coords = the output of spv_voxelize on the same
+ * points and voxel size, the results equal spv_voxelize's.
+ * In:  coords [m_cap][4] i32 (distinct; any order: output row j is coords
+ *      row j); m_dev: device count (NULL = m_cap); xyz, batch, feat, C, dt as
+ *      in spv_voxelize (feat may be NULL: counts and pt2vox only).
+ * Out: vfeat [m_cap][C] (dt; rows < count written), counts [m_cap] i32 = N_j,
+ *      pt2vox [n] i32.  Workspace: spv_workspace_bytes(max(n, m_cap), C).
+ * Errors: as spv_voxelize; duplicate coordinates in the set are a
+ *      device-detected SPV_ERR_INVALID_ARG.
+ */
+spv_status spv_voxelize_onto(void* stream, void* ws, size_t ws_bytes,
+                             const int32_t* coords, const int64_t* m_dev, int64_t m_cap,
+                             const float* xyz, const int32_t* batch, int64_t n, float voxel_size,
+                             const void* feat, int32_t C, spv_dtype dt,
+                             void* vfeat, int32_t* counts, int32_t* pt2vox);
+
+/*
  * spv_kernel_map -- the kernel map of a sparse convolution (Sec. 3.2: all
  * active synapses between input and output voxels; Sec. 3.3 "Feature
  * Aggregation": built with the same GPU hash table as the voxelization).

@@ -46,6 +46,7 @@ def lib():
         L = ct.CDLL(_LIB)
         vp, i64, i32, f32 = ct.c_void_p, ct.c_int64, ct.c_int32, ct.c_float
         L.spvo_voxelize.argtypes = [vp, vp, i64, f32, vp, i32, i32, vp, vp, vp, vp, vp]
+        L.spvo_voxelize_onto.argtypes = [vp, i64, vp, vp, i64, f32, vp, i32, i32, vp, vp, vp]
         L.spvo_kernel_map.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, i64, vp]
         L.spvo_sparse_conv.argtypes = [vp, i64, i32, vp, vp, i32, i32, vp, vp, vp, i32, vp, i64, i32, i32]
         L.spvo_sparse_conv_res.argtypes = [vp, i64, i32, vp, vp, i32, i32, vp, vp, vp, vp, i32, vp, i64, i32, i32]
@@ -104,6 +105,23 @@ def voxelize(xyz, voxel_size, feat=None, dtype="f32", batch=None):
     _chk(st, "voxelize")
     m = m.value
     return coords[:m], (None if vfeat is None else vfeat[:m]), counts[:m], pt2vox[:n]
+
+
+def voxelize_onto(coords, xyz, voxel_size, feat=None, dtype="f32", batch=None):
+    """Eq. 2 onto a given voxel set.  Returns (vfeat [m,C] or None, counts [m], pt2vox [n])."""
+    coords = np.ascontiguousarray(coords, dtype=np.int32).reshape(-1, 4)
+    xyz = np.ascontiguousarray(xyz, dtype=np.float32)
+    m, n = coords.shape[0], xyz.shape[0]
+    batch = None if batch is None else np.ascontiguousarray(batch, dtype=np.int32)
+    C = 0 if feat is None else feat.shape[1]
+    feat = None if feat is None else np.ascontiguousarray(feat, dtype=_sdt(dtype))
+    counts = np.zeros(max(m, 1), np.int32)
+    pt2vox = np.zeros(max(n, 1), np.int32)
+    vfeat = None if feat is None else np.zeros((max(m, 1), C), _sdt(dtype))
+    st = lib().spvo_voxelize_onto(_p(coords), m, _p(xyz), _p(batch), n, ct.c_float(voxel_size), _p(feat), C,
+                                  DT[dtype], _p(vfeat), _p(counts), _p(pt2vox))
+    _chk(st, "voxelize_onto")
+    return (None if vfeat is None else vfeat[:m]), counts[:m], pt2vox[:n]
 
 
 def kernel_map(in_coords, K=3, stride=1, pair_cap=None):

@@ -258,6 +258,51 @@ int spvo_voxelize(const float* xyz, const int32_t* batch, int64_t n, float voxel
     return SPVO_OK;
 }
 
+/* Eq. 2 onto a given voxel set: N_j and f_j over the points whose Eq. 1
+ * coordinates equal coords[j]; points outside the set have pt2vox = -1, and a
+ * voxel without points gets f_j = 0.  Features summed in point order. */
+int spvo_voxelize_onto(const int32_t* coords, int64_t m, const float* xyz, const int32_t* batch, int64_t n,
+                       float voxel_size, const void* feat, int32_t C, int32_t dtype,
+                       void* vfeat, int32_t* counts, int32_t* pt2vox) {
+    if (n < 0 || n >= ((int64_t)1 << 31) || m < 0 || m >= ((int64_t)1 << 31)) return SPVO_ERR_INVALID_ARG;
+    if (!valid_voxel_size(voxel_size)) return SPVO_ERR_INVALID_ARG;
+    if ((n > 0 && (!xyz || !pt2vox)) || (m > 0 && (!coords || !counts))) return SPVO_ERR_INVALID_ARG;
+    if (feat && (C <= 0 || (m > 0 && !vfeat) || !valid_dtype(dtype))) return SPVO_ERR_INVALID_ARG;
+    int st = check_points(xyz, batch, n, voxel_size);
+    if (st) return st;
+    if (!coords_in_range(coords, m)) return SPVO_ERR_RANGE;
+    coordset set;
+    st = coordset_build(&set, coords, m);
+    if (st) {
+        coordset_free(&set);
+        return st;
+    }
+    for (int64_t j = 0; j < m; ++j) counts[j] = 0;
+    for (int64_t k = 0; k < n; ++k) {
+        int32_t c[4];
+        c[0] = batch ? batch[k] : 0;
+        for (int d = 0; d < 3; ++d) quantize_axis(xyz[3 * k + d], voxel_size, NULL, &c[1 + d]);
+        const int64_t j = coordset_find(&set, c);
+        pt2vox[k] = (int32_t)j;
+        if (j >= 0) counts[j] += 1;
+    }
+    coordset_free(&set);
+    if (feat && m > 0) {
+        double* acc = (double*)calloc((size_t)m * (size_t)C, sizeof(double));
+        if (!acc) return SPVO_ERR_CAPACITY;
+        for (int64_t k = 0; k < n; ++k) {
+            if (pt2vox[k] < 0) continue;
+            double* a = acc + (int64_t)pt2vox[k] * C;
+            for (int32_t c = 0; c < C; ++c) a[c] += spvo_decode(feat, k * C + c, dtype);
+        }
+        for (int64_t j = 0; j < m; ++j)
+            for (int32_t c = 0; c < C; ++c)
+                spvo_round_store(counts[j] ? acc[j * C + c] / (double)counts[j] : 0.0, vfeat, j * C + c, dtype);
+        free(acc);
+    }
+    return SPVO_OK;
+}
+
 /* ------------------------------------------------------------------------- */
 /* kernel map                                                                 */
 /* ------------------------------------------------------------------------- */

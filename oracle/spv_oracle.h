@@ -56,6 +56,14 @@ int spvo_voxelize(const float* xyz, const int32_t* batch, int64_t n, float voxel
                   int32_t* coords, void* vfeat, int32_t* counts, int32_t* pt2vox,
                   int64_t* m_out);
 
+/* Eq. 2 onto a given set of m distinct voxels coords[m][4] (output row j =
+ * coords row j): counts[j] = N_j, vfeat[j] = mean of the features of those
+ * points (0 when N_j = 0), pt2vox[k] = j or -1 when the point's voxel is not
+ * in the set.  Duplicate coordinates: SPVO_ERR_INVALID_ARG. */
+int spvo_voxelize_onto(const int32_t* coords, int64_t m, const float* xyz, const int32_t* batch, int64_t n,
+                       float voxel_size, const void* feat, int32_t C, int32_t dtype,
+                       void* vfeat, int32_t* counts, int32_t* pt2vox);
+
 /* Kernel map.  K=3 stride=1: submanifold (outputs = inputs).  Stride 2 (K=2 or
  * K=3): outputs = unique floor(c/2), written to out_coords in ascending order;
  * (in, out) is a pair of offset k iff in = 2 out + delta_k (delta in {0,1}^3 for

@@ -240,6 +240,27 @@ spv_status spv_voxelize(void* stream, void* ws, size_t ws_bytes, const float* xy
     return st;
 }
 
+spv_status spv_voxelize_onto(void* stream, void* ws, size_t ws_bytes, const int32_t* coords, const int64_t* m_dev,
+                             int64_t m_cap, const float* xyz, const int32_t* batch, int64_t n, float voxel_size,
+                             const void* feat, int32_t C, spv_dtype dt, void* vfeat, int32_t* counts,
+                             int32_t* pt2vox) {
+    if (!ws || n < 0 || n >= ((int64_t)1 << 31) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || !valid_v(voxel_size))
+        return SPV_ERR_INVALID_ARG;
+    if (n > 0 && (!xyz || !pt2vox)) return SPV_ERR_INVALID_ARG;
+    if (m_cap > 0 && (!coords || !counts)) return SPV_ERR_INVALID_ARG;
+    if (feat && (C <= 0 || !valid_dt(dt))) return SPV_ERR_INVALID_ARG;
+    if (feat && m_cap > 0 && !vfeat) return SPV_ERR_INVALID_ARG;
+    if (((uintptr_t)ws & 255u) != 0) return SPV_ERR_INVALID_ARG;
+    VoxLayout L;
+    const int64_t cap = n > m_cap ? n : m_cap;
+    if (need(layout_voxelize(nullptr, 0, cap, L), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_voxelize(ws, ws_bytes, cap, L);
+    if (feat && (!aligned16(feat) || (m_cap > 0 && !aligned16(vfeat)))) return SPV_ERR_INVALID_ARG;
+    launch_voxelize_onto((hipStream_t)stream, L.w, coords, m_dev, m_cap, xyz, batch, n, voxel_size, feat, C, dt, vfeat,
+                         counts, pt2vox);
+    return hip_check();
+}
+
 spv_status spv_lookup(void* stream, void* ws, size_t ws_bytes, const int32_t* table_coords, const int64_t* m_dev,
                       int64_t m_cap, const int32_t* qcoords, int64_t q, int32_t* idx) {
     if (!ws || m_cap < 0 || q < 0 || (m_cap > 0 && !table_coords) || (q > 0 && (!qcoords || !idx)))

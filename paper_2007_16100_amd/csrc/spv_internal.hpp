@@ -159,6 +159,11 @@ void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const
                      float voxel_size, const void* feat, int32_t C, int dt, int32_t* coords, void* vfeat,
                      int32_t* counts, int32_t* pt2vox, int64_t* m_dev,
                      bool table_cleared = false);
+// scatter-mean onto the given voxel set coords[min(*m_dev, m_cap)] (value = row);
+// points whose voxel is not in the set get pt2vox -1; ws planned for max(n, m_cap)
+void launch_voxelize_onto(hipStream_t s, const VoxelizeWs& w, const int32_t* coords, const int64_t* m_dev,
+                          int64_t m_cap, const float* xyz, const int32_t* batch, int64_t n, float voxel_size,
+                          const void* feat, int32_t C, int dt, void* vfeat, int32_t* counts, int32_t* pt2vox);
 
 // --- kernel map (kmap.hip) -----------------------------------------------------
 struct KmapWs {

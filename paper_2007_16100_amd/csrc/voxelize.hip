@@ -27,6 +27,32 @@ void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n) {
     w.scan_tmp = a.take<int32_t>(scan_tmp_entries(nn));
 }
 
+// Eq. 1 for point k: its packed key with the quantized (b, q), or kEmpty with
+// the status flag raised for a non-finite or out-of-range point
+__device__ inline uint64_t point_key(Header* h, const float* xyz, const int32_t* batch, int64_t k, float v,
+                                     int (&q)[3], int& b) {
+    const float p[3] = {xyz[3 * k], xyz[3 * k + 1], xyz[3 * k + 2]};
+    b = batch ? batch[k] : 0;
+    const bool finite = isfinite(p[0]) && isfinite(p[1]) && isfinite(p[2]);
+    bool inrange = b >= 0 && b <= kBatchMax;
+#pragma unroll
+    for (int d = 0; d < 3; ++d) {
+        const float a = p[d] / v;  // IEEE single-precision, correctly rounded
+        const float f = floorf(a);
+        inrange = inrange && isfinite(a) && f >= (float)kCoordMin && f <= (float)kCoordMax;
+        q[d] = inrange ? (int)f : 0;
+    }
+    if (!finite) {
+        raise_flag(h, kFlagNonfinite);
+        return kEmpty;
+    }
+    if (!inrange) {
+        raise_flag(h, kFlagRange);
+        return kEmpty;
+    }
+    return pack_key(b, q[0], q[1], q[2]);
+}
+
 // Eq. 1 per point, then hash insert.  Invalid points get kEmpty and a status
 // flag.  Consecutive returns of a sweep often share a voxel: a lane whose key
 // equals the previous lane's leaves the insert to the head of its run.  The
@@ -40,26 +66,7 @@ __global__ __launch_bounds__(kAppendThreads) void k_vox_insert(Header* h, Table 
     uint64_t key = kEmpty;
     int q[3] = {0, 0, 0};
     int b = 0;
-    if (k < n) {
-        const float p[3] = {xyz[3 * k], xyz[3 * k + 1], xyz[3 * k + 2]};
-        b = batch ? batch[k] : 0;
-        const bool finite = isfinite(p[0]) && isfinite(p[1]) && isfinite(p[2]);
-        bool inrange = b >= 0 && b <= kBatchMax;
-#pragma unroll
-        for (int d = 0; d < 3; ++d) {
-            const float a = p[d] / v;  // IEEE single-precision, correctly rounded
-            const float f = floorf(a);
-            inrange = inrange && isfinite(a) && f >= (float)kCoordMin && f <= (float)kCoordMax;
-            q[d] = inrange ? (int)f : 0;
-        }
-        if (!finite) {
-            raise_flag(h, kFlagNonfinite);
-        } else if (!inrange) {
-            raise_flag(h, kFlagRange);
-        } else {
-            key = pack_key(b, q[0], q[1], q[2]);
-        }
-    }
+    if (k < n) key = point_key(h, xyz, batch, k, v, q, b);
     // runs of equal keys inside the wave: the head inserts, the others take its
     // slot (every lane between a head and a later lane of its run has its key)
     const int lane = threadIdx.x & 63;
@@ -147,6 +154,38 @@ __global__ void k_vox_fill(const int32_t* pt2vox, int64_t n, const int32_t* seg,
     if (v >= 0) plist[seg[v] + base + (lane - first)] = (int32_t)k;
 }
 
+// Scatter-mean onto a given voxel set: each point's voxel index is found in
+// the table of that set (-1 when its voxel is not in it), one probe per run of
+// equal keys in the wave, and N_m is counted as in k_vox_lookup.
+__global__ void k_vox_locate(Header* h, Table t, const float* xyz, const int32_t* batch, int64_t n, float v,
+                             int32_t* pt2vox, int32_t* counts) {
+    const int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    uint64_t key = kEmpty;
+    int q[3];
+    int b;
+    if (k < n) key = point_key(h, xyz, batch, k, v, q, b);
+    const int lane = threadIdx.x & 63;
+    const uint64_t prev_key = __shfl_up(key, 1, 64);
+    const bool head = key != kEmpty && (lane == 0 || prev_key != key);
+    const int32_t found = head ? table_find(t, key) : -1;
+    const uint64_t heads = __ballot(head) & (~0ull >> (63 - lane));
+    const int src = heads ? 63 - __clzll(heads) : lane;
+    const int32_t run_found = __shfl(found, src, 64);
+    const int32_t vox = key == kEmpty ? -1 : run_found;
+    if (k < n) pt2vox[k] = vox;
+    int first, len;
+    run_of(vox, first, len);
+    if (vox >= 0 && lane == first) atomicAdd(&counts[vox], len);
+}
+
+__global__ void k_vox_zero(int32_t* a, int32_t* b, int64_t m) {
+    const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (i < m) {
+        a[i] = 0;
+        b[i] = 0;
+    }
+}
+
 
 // Eq. 2: one thread per (voxel, VEC consecutive channels).  The points are
 // summed in fp64 -- exact for 16-bit features of ordinary range, so the result
@@ -178,6 +217,7 @@ __device__ inline void mean_add(double (&acc)[VEC], const void* feat, int64_t ro
 
 template <int DT, int VEC>
 __device__ inline void mean_store(const double (&acc)[VEC], double N, void* vfeat, int64_t orow) {
+    if (N < 1.0) N = 1.0;  // a given voxel no point falls into (scatter-mean onto a set): mean 0
     if constexpr (VEC == 8) {
         uint32_t w[4];
 #pragma unroll
@@ -266,6 +306,21 @@ static void launch_mean(hipStream_t s, const VoxelizeWs& w, int64_t n, const voi
     }
 }
 
+static void launch_mean_dt(hipStream_t s, const VoxelizeWs& w, int64_t cap, const void* feat, int C, int dt,
+                           void* vfeat) {
+    const bool v16 = (dt != SPV_F32) && (C % 8 == 0), v32 = (dt == SPV_F32) && (C % 4 == 0);
+    if (dt == SPV_F32) {
+        if (v32) launch_mean<SPV_F32, 4>(s, w, cap, feat, C, vfeat);
+        else launch_mean<SPV_F32, 1>(s, w, cap, feat, C, vfeat);
+    } else if (dt == SPV_BF16) {
+        if (v16) launch_mean<SPV_BF16, 8>(s, w, cap, feat, C, vfeat);
+        else launch_mean<SPV_BF16, 1>(s, w, cap, feat, C, vfeat);
+    } else {
+        if (v16) launch_mean<SPV_F16, 8>(s, w, cap, feat, C, vfeat);
+        else launch_mean<SPV_F16, 1>(s, w, cap, feat, C, vfeat);
+    }
+}
+
 void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const int32_t* batch, int64_t n,
                      float voxel_size, const void* feat, int32_t C, int dt, int32_t* coords, void* vfeat,
                      int32_t* counts, int32_t* pt2vox, int64_t* m_dev, bool table_cleared) {
@@ -279,17 +334,22 @@ void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const
     if (!feat) return;
     launch_exclusive_scan(s, counts, w.seg, &w.h->m, n, w.scan_tmp);
     k_vox_fill<<<blocks_for(n, 256), 256, 0, s>>>(pt2vox, n, w.seg, w.fill, w.plist);
-    const bool v16 = (dt != SPV_F32) && (C % 8 == 0), v32 = (dt == SPV_F32) && (C % 4 == 0);
-    if (dt == SPV_F32) {
-        if (v32) launch_mean<SPV_F32, 4>(s, w, n, feat, C, vfeat);
-        else launch_mean<SPV_F32, 1>(s, w, n, feat, C, vfeat);
-    } else if (dt == SPV_BF16) {
-        if (v16) launch_mean<SPV_BF16, 8>(s, w, n, feat, C, vfeat);
-        else launch_mean<SPV_BF16, 1>(s, w, n, feat, C, vfeat);
-    } else {
-        if (v16) launch_mean<SPV_F16, 8>(s, w, n, feat, C, vfeat);
-        else launch_mean<SPV_F16, 1>(s, w, n, feat, C, vfeat);
-    }
+    launch_mean_dt(s, w, n, feat, C, dt, vfeat);
+}
+
+void launch_voxelize_onto(hipStream_t s, const VoxelizeWs& w, const int32_t* coords, const int64_t* m_dev,
+                          int64_t m_cap, const float* xyz, const int32_t* batch, int64_t n, float voxel_size,
+                          const void* feat, int32_t C, int dt, void* vfeat, int32_t* counts, int32_t* pt2vox) {
+    launch_clear(s, w.h, w.table, true);
+    // the set's table (value = row) and its count into h->m, which the scan and the means read
+    if (m_cap > 0) launch_table_build(s, w.h, w.table, coords, m_dev, m_cap, &w.h->m);
+    if (m_cap > 0) k_vox_zero<<<blocks_for(m_cap, 256), 256, 0, s>>>(counts, w.fill, m_cap);
+    if (n > 0)
+        k_vox_locate<<<blocks_for(n, 256), 256, 0, s>>>(w.h, w.table, xyz, batch, n, voxel_size, pt2vox, counts);
+    if (!feat || m_cap == 0) return;
+    launch_exclusive_scan(s, counts, w.seg, &w.h->m, m_cap, w.scan_tmp);
+    if (n > 0) k_vox_fill<<<blocks_for(n, 256), 256, 0, s>>>(pt2vox, n, w.seg, w.fill, w.plist);
+    launch_mean_dt(s, w, m_cap, feat, C, dt, vfeat);
 }
 
 }  // namespace spv

@@ -29,7 +29,7 @@ SPV_DEVOX_CENTER, SPV_DEVOX_CORNER, SPV_DEVOX_NEAREST = 0, 1, 2
 _DT = {torch.float32: SPV_F32, torch.bfloat16: SPV_BF16, torch.float16: SPV_F16}
 
 # every symbol include/spv.h declares
-EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced",
+EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_voxelize_onto", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced",
            "spv_linear", "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_map_children", "spv_sparse_conv_up",
            "spv_sparse_conv_dgrad", "spv_wgrad_workspace_bytes", "spv_sparse_conv_wgrad",
            "spv_voxelize_backward",
@@ -70,6 +70,7 @@ def lib():
         L.spv_block_workspace_bytes.argtypes = [i64, i32]
         L.spv_block_workspace_bytes.restype = sz
         L.spv_voxelize.argtypes = [vp, vp, sz, vp, vp, i64, f32, vp, i32, i32, vp, vp, vp, vp, vp, vp]
+        L.spv_voxelize_onto.argtypes = [vp, vp, sz, vp, vp, i64, vp, vp, i64, f32, vp, i32, i32, vp, vp, vp]
         L.spv_kernel_map.argtypes = [vp, vp, sz, vp, vp, i64, i32, i32, vp, vp, vp, vp, i64, vp]
         L.spv_sparse_conv.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i64, i32, i32, vp, vp, vp, i32, vp, vp, i64,
                                       i32, i32]
@@ -96,7 +97,7 @@ def lib():
         L.spv_status_string.argtypes = [i32]
         L.spv_status_string.restype = ct.c_char_p
         L.spv_last_hip_error.argtypes = []
-        for f in ("spv_voxelize", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced", "spv_linear",
+        for f in ("spv_voxelize", "spv_voxelize_onto", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced", "spv_linear",
                   "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_map_children", "spv_sparse_conv_up",
                   "spv_sparse_conv_dgrad", "spv_sparse_conv_wgrad",
                   "spv_voxelize_backward",
@@ -189,6 +190,30 @@ def spv_voxelize(ws: Workspace, xyz: torch.Tensor, voxel_size: float, feat: Opti
                             _ptr(out.m_dev), ct.byref(m_host) if sync else None)
     _chk(st, "spv_voxelize")
     out.m = m_host.value if sync else None
+    return out
+
+
+def spv_voxelize_onto(ws: Workspace, coords: torch.Tensor, xyz: torch.Tensor, voxel_size: float,
+                      feat: Optional[torch.Tensor] = None, batch: Optional[torch.Tensor] = None,
+                      m_dev: Optional[torch.Tensor] = None, out: Optional[Voxelized] = None) -> Voxelized:
+    """Scatter-mean of the points onto the given voxel set (row j of the outputs is coords row j);
+    points whose voxel is not in the set get pt2vox -1.  Returns a Voxelized whose coords are
+    the given ones."""
+    n = xyz.shape[0]
+    m_cap = coords.shape[0]
+    dev = xyz.device
+    C = feat.shape[1] if feat is not None else 0
+    dt = _DT[feat.dtype] if feat is not None else SPV_F32
+    if out is None:
+        out = Voxelized(coords, torch.empty((max(m_cap, 1), C), dtype=feat.dtype, device=dev)
+                        if feat is not None else None,
+                        torch.empty(max(m_cap, 1), dtype=torch.int32, device=dev),
+                        torch.empty(max(n, 1), dtype=torch.int32, device=dev), m_dev,
+                        m_cap if m_dev is None else None)
+    st = lib().spv_voxelize_onto(_stream(), ws.ptr, ws.nbytes, _ptr(coords), _ptr(m_dev), m_cap, _ptr(xyz),
+                                 _ptr(batch), n, ct.c_float(voxel_size), _ptr(feat), C, dt, _ptr(out.vfeat),
+                                 _ptr(out.counts), _ptr(out.pt2vox))
+    _chk(st, "spv_voxelize_onto")
     return out
 
 

@@ -16,6 +16,8 @@ holds the device buffers:
   one synchronization per stride to size what follows exactly; every 3x3x3 conv
   the neighbour-table kernel takes runs on that table (no per-call plan), the
   others on the stride's pairs, built on first use;
+* the later modules' voxelizations scatter the point features onto the voxel set the
+  plan holds for their stride (no sort);
 * the transposed stride-2 convs run on the stride-2 maps' child tables: every
   fine voxel has its parent, so each output row is one product row, stored once;
 * a conv over a skip concatenation [t; x] runs as two sliced convs,
@@ -165,9 +167,12 @@ class SPVCNN:
         d = spv.spv_devoxelize(self.ws, plan.coords[s], vfeat, xyz, self.v, s, self.mode, batch)
         return spv.spv_linear(self.ws, z, W, scale=sc, shift=sh, relu=True, res=d, res_after_act=True)
 
-    def _revoxelize(self, xyz, z, s, batch, m):
-        vox = spv.spv_voxelize(self.ws, xyz, voxel_size_at(self.v, s), z, batch, sync=False)
-        return vox.vfeat[:m], vox
+    def _revoxelize(self, plan, xyz, z, s, batch):
+        """Scatter-mean of the point features at stride 2^s onto that stride's voxels, which the
+        plan already holds (the points quantized at voxel_size_at(v, s) land exactly on them):
+        no insert and no sort, one table probe per point."""
+        vox = spv.spv_voxelize_onto(self.ws, plan.coords[s], xyz, voxel_size_at(self.v, s), z, batch)
+        return vox.vfeat[: plan.m[s]], vox
 
     # -- forward -------------------------------------------------------------
     def forward(self, xyz: torch.Tensor, feat: torch.Tensor, batch: Optional[torch.Tensor] = None,
@@ -184,7 +189,7 @@ class SPVCNN:
         skips = [x]
         z = self._fuse(plan, x, 0, feat, "point.0", xyz, batch)
 
-        x, _ = self._revoxelize(xyz, z, 0, batch, m[0])
+        x, _ = self._revoxelize(plan, xyz, z, 0, batch)
         for s in range(1, 5):
             x = self._conv(x, f"down.{s}", plan.down[s], m[s])
             x = self._resblock(plan, [x], f"enc.{s}.0", s)
@@ -204,10 +209,10 @@ class SPVCNN:
             y = self._resblock(plan, [t, skips[4 - u]], f"dec.{u}.0", 4 - u)
             return self._resblock(plan, [y], f"dec.{u}.1", 4 - u)
 
-        y, vox4 = self._revoxelize(xyz, z, 4, batch, m[4])
+        y, vox4 = self._revoxelize(plan, xyz, z, 4, batch)
         y = up(up(y, 1), 2)
         z = self._fuse(plan, y, 2, z, "point.2", xyz, batch)
-        y, vox2 = self._revoxelize(xyz, z, 2, batch, m[2])
+        y, vox2 = self._revoxelize(plan, xyz, z, 2, batch)
         y = up(up(y, 3), 4)
         z = self._fuse(plan, y, 0, z, "point.3", xyz, batch)
         W, _, bias = self.P["head"]

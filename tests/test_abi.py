@@ -46,6 +46,20 @@ def test_host_side_validation_without_gpu():
     st = L.spv_voxelize(None, ws, 16, ct.c_void_p(16), None, 4, ct.c_float(0.1), None, 0, 0, ct.c_void_p(16), None,
                         ct.c_void_p(16), ct.c_void_p(16), None, None)
     assert st == spv.SPV_ERR_CAPACITY
+    # scatter-mean onto a given set: bad voxel size, a missing coordinate list, negative
+    # capacity, features without an output, a workspace too small
+    P = ct.c_void_p(16)
+    for v in (0.0, float("inf")):
+        assert L.spv_voxelize_onto(None, ws, 1 << 30, P, None, 4, P, None, 4, ct.c_float(v), None, 0, 0, None, P,
+                                   P) == spv.SPV_ERR_INVALID_ARG
+    assert L.spv_voxelize_onto(None, ws, 1 << 30, None, None, 4, P, None, 4, ct.c_float(0.1), None, 0, 0, None, P,
+                               P) == spv.SPV_ERR_INVALID_ARG
+    assert L.spv_voxelize_onto(None, ws, 1 << 30, P, None, -1, P, None, 4, ct.c_float(0.1), None, 0, 0, None, P,
+                               P) == spv.SPV_ERR_INVALID_ARG
+    assert L.spv_voxelize_onto(None, ws, 1 << 30, P, None, 4, P, None, 4, ct.c_float(0.1), P, 8, 1, None, P,
+                               P) == spv.SPV_ERR_INVALID_ARG
+    assert L.spv_voxelize_onto(None, ws, 16, P, None, 4, P, None, 4, ct.c_float(0.1), None, 0, 0, None, P,
+                               P) == spv.SPV_ERR_CAPACITY
     # unsupported kernel-map geometry
     st = L.spv_kernel_map(None, ws, 1 << 30, ct.c_void_p(16), None, 4, 2, 1, ct.c_void_p(16), None, ct.c_void_p(16),
                           ct.c_void_p(16), 100, None)

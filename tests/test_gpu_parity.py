@@ -166,6 +166,71 @@ def test_voxelize_coarse_long_runs(spv, sweep, dtype, C):
     np.testing.assert_array_equal(vf, rvf)
 
 
+# ---------------------------------------------------------------------------
+# scatter-mean onto a given voxel set
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype,C,v", [("bf16", 96, 0.05), ("bf16", 256, 0.8), ("f32", 12, 0.8), ("f16", 5, 0.1)])
+def test_voxelize_onto_own_set(spv, sweep, dtype, C, v):
+    """Onto the set spv_voxelize finds (its device count), the outputs are spv_voxelize's and
+    the oracle's bit for bit -- voxels of over 32 points included at 0.8 m."""
+    feat = synth.normal((len(sweep), C), 1013, dtype=dtype)
+    c, vf, cnt, p2v, out = run_voxelize(spv, sweep, v, feat, dtype)
+    ws = spv.Workspace.for_ops(len(sweep), C)
+    o = spv.spv_voxelize_onto(ws, out.coords, dev(sweep), v, dev(feat, dtype), m_dev=out.m_dev)
+    assert spv.spv_status_check(ws) == 0
+    m = len(c)
+    np.testing.assert_array_equal(host(o.counts)[:m], cnt)
+    np.testing.assert_array_equal(host(o.pt2vox)[:len(sweep)], p2v)
+    np.testing.assert_array_equal(host(o.vfeat, dtype)[:m], vf)
+    rvf, rcnt, rp2v = oracle.voxelize_onto(c, sweep, v, feat, dtype)
+    np.testing.assert_array_equal(host(o.vfeat, dtype)[:m], rvf)
+    np.testing.assert_array_equal(rcnt, cnt)
+
+
+@pytest.mark.parametrize("dtype,C", [("bf16", 32), ("f32", 8)])
+def test_voxelize_onto_subset(spv, sweep, dtype, C):
+    """A shuffled two-thirds of the occupied voxels plus voxels no point falls into: the
+    points of the dropped voxels get -1, the empty voxels count 0 with zero features."""
+    rng = np.random.default_rng(1014)
+    v = 0.1
+    batch = (np.arange(len(sweep)) * 3 // len(sweep)).astype(np.int32)
+    feat = synth.normal((len(sweep), C), 1015, dtype=dtype)
+    rc, _, _, _ = oracle.voxelize(sweep, v, batch=batch)
+    keep = rng.permutation(len(rc))[: 2 * len(rc) // 3]
+    empty = np.array([[0, 30000, 0, 0], [2, -5, 7, 9], [5, 0, 0, 0]], np.int32)
+    gset = np.concatenate([rc[keep], empty])
+    gset = np.ascontiguousarray(gset[rng.permutation(len(gset))])
+    ws = spv.Workspace.for_ops(len(sweep), C)
+    o = spv.spv_voxelize_onto(ws, dev(gset), dev(sweep), v, dev(feat, dtype), dev(batch))
+    assert spv.spv_status_check(ws) == 0
+    rvf, rcnt, rp2v = oracle.voxelize_onto(gset, sweep, v, feat, dtype, batch)
+    assert (rp2v < 0).sum() > 1000 and (rcnt == 0).sum() == len(empty)
+    np.testing.assert_array_equal(host(o.counts), rcnt)
+    np.testing.assert_array_equal(host(o.pt2vox), rp2v)
+    np.testing.assert_array_equal(host(o.vfeat, dtype), rvf)
+
+
+def test_voxelize_onto_edge_cases(spv):
+    xyz = np.array([[0.05, 0.05, 0.05], [0.15, 0.05, 0.05], [0.16, 0.07, 0.01]], np.float32)
+    feat = synth.normal((3, 8), 3, dtype="bf16")
+    ws = spv.Workspace.for_ops(16, 8)
+    # empty set: every point outside it
+    o = spv.spv_voxelize_onto(ws, torch.zeros((0, 4), dtype=torch.int32, device="cuda"), dev(xyz), 0.1,
+                              dev(feat, "bf16"))
+    np.testing.assert_array_equal(host(o.pt2vox), [-1, -1, -1])
+    # no features: counts and pt2vox only
+    gset = np.array([[0, 1, 0, 0], [0, 0, 0, 0], [0, 9, 9, 9]], np.int32)
+    o = spv.spv_voxelize_onto(ws, dev(gset), dev(xyz), 0.1)
+    np.testing.assert_array_equal(host(o.counts), [2, 1, 0])
+    np.testing.assert_array_equal(host(o.pt2vox), [1, 0, 0])
+    # no points: every voxel of the set counts 0
+    o = spv.spv_voxelize_onto(ws, dev(gset), dev(np.zeros((0, 3), np.float32)), 0.1)
+    np.testing.assert_array_equal(host(o.counts), [0, 0, 0])
+    # a repeated set coordinate is a device-detected invalid argument
+    spv.spv_voxelize_onto(ws, dev(np.array([[0, 1, 0, 0], [0, 1, 0, 0]], np.int32)), dev(xyz), 0.1)
+    assert spv.spv_status_check(ws) == spv.SPV_ERR_INVALID_ARG
+
+
 def test_voxelize_wide_keys(spv):
     """Coordinates spanning nearly the whole key range (48 significant bits once
     compacted): the sort's passes past 32 bits run."""

@@ -54,7 +54,7 @@ def _case(n_sweeps, stride, seed):
 
 @pytest.mark.parametrize("dtype,n_sweeps,stride", [("bf16", 1, 6), ("f32", 1, 12), ("bf16", 2, 10)])
 def test_spvcnn_forward(spv, dtype, n_sweeps, stride):
-    from paper_2007_16100_amd.spvcnn import SPVCNN
+    from paper_2007_16100_amd.spvcnn import SPVCNN, voxel_size_at
     xyz, batch = _case(n_sweeps, stride, 1005)
     feat = synth.point_features(xyz, 77, dtype)
     P = synth.spvcnn_params(78, dtype)
@@ -74,8 +74,12 @@ def test_spvcnn_forward(spv, dtype, n_sweeps, stride):
         np.testing.assert_array_equal(plan.coords[s].cpu().numpy(), c)
         if s < 4:
             c, _, _ = oracle.kernel_map(c, 2, 2)
+    # the re-voxelizations onto the plan's voxel sets: every point lands in a voxel of the set,
+    # with the counts of a fresh voxelization at that stride's voxel size
     for vox, s in zip(gtr["revox"], (4, 2)):
-        np.testing.assert_array_equal(vox.coords[: plan.m[s]].cpu().numpy(), plan.coords[s].cpu().numpy())
+        assert bool((vox.pt2vox[: len(xyz)] >= 0).all())
+        _, _, cnt, _ = oracle.voxelize(xyz, voxel_size_at(0.05, s), batch=batch)
+        np.testing.assert_array_equal(vox.counts[: plan.m[s]].cpu().numpy(), cnt)
     r = ref.astype(np.float64) if dtype == "f32" else synth.from_storage(ref, dtype).astype(np.float64)
     g = _to_host(out, dtype)[: len(xyz)]
     err = float(np.max(np.abs(g - r)) / np.max(np.abs(r)))

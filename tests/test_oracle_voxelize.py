@@ -159,3 +159,73 @@ def test_storage_rounding(oracle_lib, dtype):
     np.testing.assert_array_equal(buf, expect)
     back = np.array([o.lib().spvo_decode(buf.ctypes.data_as(ct.c_void_p), i, o.DT[dtype]) for i in range(len(x))])
     np.testing.assert_array_equal(back, synth.from_storage(expect, dtype).astype(np.float64))
+
+
+# -- Eq. 2 onto a given voxel set --------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_onto_own_set_equals_voxelize(oracle_lib, dtype):
+    # onto the very set the voxelization finds, the outputs are the voxelization's
+    rng = np.random.default_rng(5)
+    n = 400
+    xyz = rng.uniform(-0.5, 0.5, size=(n, 3)).astype(np.float32)
+    batch = rng.integers(0, 3, size=n).astype(np.int32)
+    feat = synth.normal((n, 6), 7, dtype=dtype)
+    coords, vf, counts, p2v = oracle_lib.voxelize(xyz, 0.1, feat, dtype=dtype, batch=batch)
+    vf2, counts2, p2v2 = oracle_lib.voxelize_onto(coords, xyz, 0.1, feat, dtype=dtype, batch=batch)
+    np.testing.assert_array_equal(counts2, counts)
+    np.testing.assert_array_equal(p2v2, p2v)
+    np.testing.assert_array_equal(vf2.view(np.uint8), vf.view(np.uint8))
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_onto_subset_literal(oracle_lib, seed, dtype):
+    # a shuffled subset of the occupied voxels plus voxels no point falls into, against the
+    # indicator form of Eq. 2 over all occupied voxels
+    rng = np.random.default_rng(seed)
+    n = 300
+    v = 0.1
+    xyz = rng.uniform(-0.4, 0.4, size=(n, 3)).astype(np.float32)
+    batch = rng.integers(0, 2, size=n).astype(np.int32)
+    feat = synth.normal((n, 5), seed + 40, dtype=dtype)
+    rc, rmean, rN = dense_ref.eq2_literal(xyz, synth.from_storage(feat, dtype).astype(np.float64), v, batch)
+    keep = rng.permutation(len(rc))[: len(rc) // 2]
+    empty = np.array([[0, 100, 0, 0], [1, -7, 9, 30], [1, 0, 0, 5]], np.int32)
+    gset = np.concatenate([rc[keep], empty])
+    order = rng.permutation(len(gset))
+    gset = gset[order]
+    src = np.concatenate([keep, -np.ones(len(empty), np.int64)])[order]  # literal row, -1 = empty voxel
+    vf, counts, p2v = oracle_lib.voxelize_onto(gset, xyz, v, feat, dtype=dtype, batch=batch)
+    np.testing.assert_array_equal(counts, np.where(src >= 0, rN[np.maximum(src, 0)], 0))
+    got = synth.from_storage(vf, dtype).astype(np.float64)
+    want = np.where((src >= 0)[:, None], rmean[np.maximum(src, 0)], 0.0)
+    ulp = 2.0 ** -24 if dtype == "f32" else 2.0 ** -8
+    assert np.all(np.abs(got - want) <= ulp * np.abs(want) + 1e-300)
+    assert np.all(got[src < 0] == 0.0)
+    # pt2vox: the row of the point's own key in the set, or -1
+    row_of = {tuple(c): j for j, c in enumerate(gset.tolist())}
+    pk = np.concatenate([batch[:, None], dense_ref.quantize(xyz, v)], 1)
+    np.testing.assert_array_equal(p2v, [row_of.get(tuple(c), -1) for c in pk.tolist()])
+
+
+def test_onto_edge_cases(oracle_lib):
+    o = oracle_lib
+    xyz = np.array([[0.05, 0.05, 0.05], [0.15, 0.05, 0.05]], np.float32)
+    feat = np.array([[1.0, 2.0], [3.0, 4.0]], np.float32)
+    # empty set: every point outside it
+    vf, counts, p2v = o.voxelize_onto(np.zeros((0, 4), np.int32), xyz, 0.1, feat)
+    assert vf.shape == (0, 2) and counts.shape == (0,)
+    np.testing.assert_array_equal(p2v, [-1, -1])
+    # no points: every voxel empty, mean 0
+    vf, counts, p2v = o.voxelize_onto(np.array([[0, 0, 0, 0]], np.int32), np.zeros((0, 3), np.float32), 0.1,
+                                      np.zeros((0, 2), np.float32))
+    np.testing.assert_array_equal(counts, [0])
+    np.testing.assert_array_equal(vf, [[0.0, 0.0]])
+    # duplicate and out-of-range set coordinates
+    with pytest.raises(o.OracleError) as e:
+        o.voxelize_onto(np.array([[0, 0, 0, 0], [0, 0, 0, 0]], np.int32), xyz, 0.1, feat)
+    assert e.value.status == o.ERR_INVALID_ARG
+    with pytest.raises(o.OracleError) as e:
+        o.voxelize_onto(np.array([[0, 40000, 0, 0]], np.int32), xyz, 0.1, feat)
+    assert e.value.status == o.ERR_RANGE
