@@ -126,14 +126,20 @@ constexpr int kDevoxPB = 4;  // 16-point blocks per wave
 
 // NBR: corners read from the grid's neighbour table (a.nbr), else probed
 template <int DT, int KCH, int NB, bool NBR>
-__global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __restrict__ wpack) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_devox_mfma(DevoxArgs a,
+                                                                                            const uint4* __restrict__ wpack) {
     constexpr int PB = kDevoxPB;
     constexpr int C = NB * 16;
-    constexpr int NCH = C / 8;  // 16-byte chunks per output row
+    // above 128 channels the row tile holds half the channels at a time (LDS for
+    // two workgroups per CU) and each lane keeps the corner rows of 2 of its
+    // tasks in flight at once instead of all of them
+    constexpr int HV = NB > 8 ? 2 : 1;
+    constexpr int CH = C / HV;   // channels per half
+    constexpr int NCH = CH / 8;  // 16-byte chunks per half row
     __shared__ __align__(16) uint4 wl[KCH * NB * 64];
     __shared__ __align__(16) int32_t sidx[4][PB * 16][8];
     __shared__ __align__(16) float sw[4][PB * 16][8];
-    __shared__ __align__(16) float ys[4][16][C + 4];
+    __shared__ __align__(16) float ys[4][16][CH + 4];
     __shared__ float ssc[C], ssh[C];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -269,85 +275,93 @@ __global__ __launch_bounds__(256) void k_devox_mfma(DevoxArgs a, const uint4* __
                                                acc[nb]);
             }
         }
-        // 2. activated MLP rows of block b into the wave's row tile
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (mlp) {
-                const int col = nb * 16 + 4 * g;
-                float sc[4], sh[4];
+        for (int hv = 0; hv < HV; ++hv) {
+            // 2. activated MLP rows of block b (this half's channels) into the wave's row tile
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    sc[e] = ssc[col + e];
-                    sh[e] = ssh[col + e];
+            for (int nb = hv * (NB / HV); nb < (hv + 1) * (NB / HV); ++nb) {
+                float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (mlp) {
+                    const int col = nb * 16 + 4 * g;
+                    float sc[4], sh[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        sc[e] = ssc[col + e];
+                        sh[e] = ssh[col + e];
+                    }
+                    y.x = acc[nb][0] * sc[0] + sh[0];
+                    y.y = acc[nb][1] * sc[1] + sh[1];
+                    y.z = acc[nb][2] * sc[2] + sh[2];
+                    y.w = acc[nb][3] * sc[3] + sh[3];
+                    if (a.relu_p) {
+                        y.x = fmaxf(y.x, 0.f);
+                        y.y = fmaxf(y.y, 0.f);
+                        y.z = fmaxf(y.z, 0.f);
+                        y.w = fmaxf(y.w, 0.f);
+                    }
                 }
-                y.x = acc[nb][0] * sc[0] + sh[0];
-                y.y = acc[nb][1] * sc[1] + sh[1];
-                y.z = acc[nb][2] * sc[2] + sh[2];
-                y.w = acc[nb][3] * sc[3] + sh[3];
-                if (a.relu_p) {
-                    y.x = fmaxf(y.x, 0.f);
-                    y.y = fmaxf(y.y, 0.f);
-                    y.z = fmaxf(y.z, 0.f);
-                    y.w = fmaxf(y.w, 0.f);
+                *(float4*)&ys[wave][r16][nb * 16 - hv * CH + 4 * g] = y;
+            }
+            __builtin_amdgcn_wave_barrier();
+            // 3. blend: tasks (point, chunk) of block b; the corner rows of a group of
+            // a lane's tasks are requested before any of them is used
+            constexpr int NT = (16 * NCH + 63) / 64;
+            constexpr int G = HV > 1 ? 2 : NT;
+#pragma unroll
+            for (int j0 = 0; j0 < NT; j0 += G) {
+                int32_t ci[G][8];
+                float cw[G][8];
+                uint4 v[G][8];
+#pragma unroll
+                for (int j = 0; j < G; ++j) {
+                    const int t = lane + 64 * (j0 + j);
+                    const int pt = (t < 16 * NCH ? t : 0) / NCH, ch = (t < 16 * NCH ? t : 0) % NCH;
+                    const i32x4v ia = *(const i32x4v*)&sidx[wave][b * 16 + pt][0];
+                    const i32x4v ib = *(const i32x4v*)&sidx[wave][b * 16 + pt][4];
+                    const float4 wa = *(const float4*)&sw[wave][b * 16 + pt][0];
+                    const float4 wb = *(const float4*)&sw[wave][b * 16 + pt][4];
+                    const int32_t ii[8] = {ia.x, ia.y, ia.z, ia.w, ib.x, ib.y, ib.z, ib.w};
+                    const float ww[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
+#pragma unroll
+                    for (int cc = 0; cc < 8; ++cc) {
+                        ci[j][cc] = t < 16 * NCH ? ii[cc] : -1;
+                        cw[j][cc] = ww[cc];
+                        v[j][cc] = make_uint4(0, 0, 0, 0);
+                        if (ci[j][cc] >= 0) v[j][cc] = *(const uint4*)(V + (int64_t)ci[j][cc] * C + hv * CH + ch * 8);
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < G; ++j) {
+                    const int t = lane + 64 * (j0 + j);
+                    if (t >= 16 * NCH) break;
+                    const int pt = t / NCH, ch = t - pt * NCH;
+                    const int64_t k = p0 + b * 16 + pt;
+                    float dv[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) dv[e] = 0.f;
+#pragma unroll
+                    for (int cc = 0; cc < 8; ++cc) {
+                        if (ci[j][cc] < 0) continue;
+                        const uint32_t u[4] = {v[j][cc].x, v[j][cc].y, v[j][cc].z, v[j][cc].w};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            dv[2 * e] += cw[j][cc] * from16<DT>(u[e] & 0xFFFF);
+                            dv[2 * e + 1] += cw[j][cc] * from16<DT>(u[e] >> 16);
+                        }
+                    }
+                    const float4 y0 = *(const float4*)&ys[wave][pt][ch * 8];
+                    const float4 y1 = *(const float4*)&ys[wave][pt][ch * 8 + 4];
+                    const float yy[8] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w};
+                    uint32_t o[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        o[e] = (uint32_t)to16<DT>(yy[2 * e] + dv[2 * e]) |
+                               ((uint32_t)to16<DT>(yy[2 * e + 1] + dv[2 * e + 1]) << 16);
+                    if (k < a.n) *(uint4*)(out + k * C + hv * CH + ch * 8) = make_uint4(o[0], o[1], o[2], o[3]);
                 }
             }
-            *(float4*)&ys[wave][r16][nb * 16 + 4 * g] = y;
+            __builtin_amdgcn_wave_barrier();
         }
-        __builtin_amdgcn_wave_barrier();
-        // 3. blend: tasks (point, chunk) of block b; the corner rows of all of
-        // a lane's tasks are requested before any of them is used
-        constexpr int NT = (16 * NCH + 63) / 64;
-        int32_t ci[NT][8];
-        float cw[NT][8];
-        uint4 v[NT][8];
-#pragma unroll
-        for (int j = 0; j < NT; ++j) {
-            const int t = lane + 64 * j;
-            const int pt = (t < 16 * NCH ? t : 0) / NCH, ch = (t < 16 * NCH ? t : 0) % NCH;
-            const i32x4v ia = *(const i32x4v*)&sidx[wave][b * 16 + pt][0];
-            const i32x4v ib = *(const i32x4v*)&sidx[wave][b * 16 + pt][4];
-            const float4 wa = *(const float4*)&sw[wave][b * 16 + pt][0];
-            const float4 wb = *(const float4*)&sw[wave][b * 16 + pt][4];
-            const int32_t ii[8] = {ia.x, ia.y, ia.z, ia.w, ib.x, ib.y, ib.z, ib.w};
-            const float ww[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
-#pragma unroll
-            for (int cc = 0; cc < 8; ++cc) {
-                ci[j][cc] = t < 16 * NCH ? ii[cc] : -1;
-                cw[j][cc] = ww[cc];
-                v[j][cc] = make_uint4(0, 0, 0, 0);
-                if (ci[j][cc] >= 0) v[j][cc] = *(const uint4*)(V + (int64_t)ci[j][cc] * C + ch * 8);
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < NT; ++j) {
-            const int t = lane + 64 * j;
-            if (t >= 16 * NCH) break;
-            const int pt = t / NCH, ch = t - pt * NCH;
-            const int64_t k = p0 + b * 16 + pt;
-            float dv[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) dv[e] = 0.f;
-#pragma unroll
-            for (int cc = 0; cc < 8; ++cc) {
-                if (ci[j][cc] < 0) continue;
-                const uint32_t u[4] = {v[j][cc].x, v[j][cc].y, v[j][cc].z, v[j][cc].w};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    dv[2 * e] += cw[j][cc] * from16<DT>(u[e] & 0xFFFF);
-                    dv[2 * e + 1] += cw[j][cc] * from16<DT>(u[e] >> 16);
-                }
-            }
-            const float4 y0 = *(const float4*)&ys[wave][pt][ch * 8];
-            const float4 y1 = *(const float4*)&ys[wave][pt][ch * 8 + 4];
-            const float yy[8] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w};
-            uint32_t o[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                o[e] = (uint32_t)to16<DT>(yy[2 * e] + dv[2 * e]) | ((uint32_t)to16<DT>(yy[2 * e + 1] + dv[2 * e + 1]) << 16);
-            if (k < a.n) *(uint4*)(out + k * C + ch * 8) = make_uint4(o[0], o[1], o[2], o[3]);
-        }
-        __builtin_amdgcn_wave_barrier();
     }
 }
 
