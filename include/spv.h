@@ -26,7 +26,10 @@
  *    Device-detected errors (non-finite or out-of-range coordinates, exhausted
  *    capacity) are recorded in the workspace status word: spv_status_check
  *    (which synchronizes) or any call given a host read-back pointer returns them.
- *    Each public call clears the status word when it starts.  After a device
+ *    Every call that can record such an error clears the status word when it
+ *    starts, also when it has nothing to compute; spv_sparse_conv_nbr,
+ *    spv_sparse_conv_up, spv_linear and spv_sparse_conv_wgrad record none and
+ *    leave it as it is.  After a device
  *    error the contents of the outputs are unspecified (but every access stays
  *    inside the caller's buffers).
  *  - Feature storage dtype: SPV_F32, SPV_BF16 or SPV_F16; weights use the

@@ -47,6 +47,13 @@ constexpr int kUpChildren = 8;  // offsets of a k=2 s=2 map
 bool valid_v(float v) { return isfinite(v) && v > 0.0f; }
 
 // --- workspace layouts (a null base gives the size) -----------------------------
+// A call that records device-detected errors and has nothing to compute still
+// clears the status word (at workspace offset 0), as its launches would.
+static spv_status clear_status_only(hipStream_t s, void* ws) {
+    launch_clear_header(s, (Header*)ws);
+    return hip_check();
+}
+
 struct VoxLayout {
     Header* h;
     VoxelizeWs w;
@@ -328,8 +335,8 @@ static spv_status sparse_conv_call(void* stream, void* ws, size_t ws_bytes, cons
     ConvLayout L;
     if (need(layout_conv(nullptr, 0, m_out_cap, K3, Cin, Cout, dt, L), ws_bytes)) return SPV_ERR_CAPACITY;
     layout_conv(ws, ws_bytes, m_out_cap, K3, Cin, Cout, dt, L);
-    if (m_out_cap == 0) return SPV_OK;
     hipStream_t s = (hipStream_t)stream;
+    if (m_out_cap == 0) return clear_status_only(s, ws);
     L.p.m_out_dev = m_out_dev;
     L.p.res = res;
     L.p.w_ldc = wst.ldc;
@@ -377,8 +384,8 @@ spv_status spv_kernel_map_nbr(void* stream, void* ws, size_t ws_bytes, const int
     MapLayout L;
     if (need(layout_kmap(nullptr, 0, m_cap, 3, 1, L), ws_bytes)) return SPV_ERR_CAPACITY;
     layout_kmap(ws, ws_bytes, m_cap, 3, 1, L);
-    if (m_cap == 0) return SPV_OK;
     hipStream_t s = (hipStream_t)stream;
+    if (m_cap == 0) return clear_status_only(s, ws);
     launch_clear(s, L.h, L.w.fine, true);
     launch_table_build(s, L.h, L.w.fine, in_coords, m_in_dev, m_cap);
     launch_kernel_map_nbr(s, L.w, in_coords, m_in_dev, m_cap, nbr);
@@ -419,7 +426,7 @@ spv_status spv_map_children(void* stream, void* ws, size_t ws_bytes, const int32
         return SPV_ERR_INVALID_ARG;
     if ((pair_cap > 0 && !pairs) || (m_coarse_cap > 0 && !children) || !aligned16(children)) return SPV_ERR_INVALID_ARG;
     if (need(sizeof(Header), ws_bytes)) return SPV_ERR_CAPACITY;
-    if (m_coarse_cap == 0) return SPV_OK;
+    if (m_coarse_cap == 0) return clear_status_only((hipStream_t)stream, ws);
     launch_nbr_table((hipStream_t)stream, off, pairs, kUpChildren, pair_cap, m_coarse_dev, m_coarse_cap, fine_rows,
                      children, (Header*)ws);
     return hip_check();

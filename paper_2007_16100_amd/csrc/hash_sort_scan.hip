@@ -82,7 +82,7 @@ void launch_table_lookup(hipStream_t s, Table t, const int32_t* q, int64_t nq, i
 // radix sort of packed voxel keys with a device-side count
 // ---------------------------------------------------------------------------
 constexpr int kSortThreads = 256;
-constexpr int kSortItems = 8;
+constexpr int kSortItems = 4;
 constexpr int kSortTile = kSortThreads * kSortItems;
 constexpr int kSortParts = 256;            // partial records of the stand-alone min / max kernel
 constexpr uint32_t kFusedSortBlocks = 256;  // up to this many tiles a scatter block scans the histograms itself

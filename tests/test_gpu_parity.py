@@ -899,6 +899,7 @@ def test_empty_inputs_of_network_entry_points(spv):
     weight gradient of an empty map is zero, the devox gradient of no points is zero."""
     d = "cuda"
     ws = spv.Workspace.for_ops(16, 64)
+    ws.buf.fill_(3)  # a stale status word: the calls that record device errors clear it
     e32 = torch.zeros((0, 32), dtype=torch.bfloat16, device=d)
     W = torch.ones((32, 32), dtype=torch.bfloat16, device=d)
     out = spv.spv_linear(ws, e32, W)
@@ -926,3 +927,12 @@ def test_empty_inputs_of_network_entry_points(spv):
                               3)
     torch.cuda.synchronize()
     assert spv.spv_status_check(ws) == spv.SPV_OK
+    # the other empty calls that record device errors clear a stale status word too
+    off9 = torch.zeros(9, dtype=torch.int32, device=d)
+    for call in (lambda: spv.spv_map_children(ws, off9, pairs, 0, 0),
+                 lambda: spv.spv_sparse_conv(ws, e32, off, pairs, W27, 0),
+                 lambda: spv.spv_voxelize_onto(ws, torch.zeros((0, 4), dtype=torch.int32, device=d),
+                                               torch.zeros((0, 3), dtype=torch.float32, device=d), 0.1)):
+        ws.buf.fill_(3)
+        call()
+        assert spv.spv_status_check(ws) == spv.SPV_OK
