@@ -281,6 +281,51 @@ spv_status spv_sparse_conv_up(void* stream, void* ws, size_t ws_bytes,
                               void* out, int64_t out_rows, int32_t Cout, spv_dtype dt);
 
 /*
+ * Pre-packed weights.  The neighbour-table conv, the upsampling conv and the
+ * linear layer copy their weights into matrix-core fragments in every call; a
+ * network whose weights stay fixed across forwards packs each once:
+ *
+ * spv_packed_weights_bytes -- bytes of the packed form of W[K3][Cin][Cout]
+ * (K3 in 1..27), or 0 when no kernel reads that shape (ceil(Cin/32) must be 1,
+ * 2, 3, 4, 6 or 8; ceil(Cout/16) at most 16).
+ *
+ * spv_pack_weights -- packs the slice W[:K3][:Cin][:Cout] of a 16-bit weight
+ * tensor W[K3][Cin_full][Cout_full] (device) into `packed` (device, 16-byte
+ * aligned, packed_bytes from spv_packed_weights_bytes).  A channel slice at an
+ * input-channel offset is packed by passing W advanced by offset * Cout_full
+ * elements.  Enqueued on `stream`, like the kernels that read it.
+ * Errors: SPV_ERR_INVALID_ARG (null or misaligned pointers, a slice wider than
+ * W), SPV_ERR_UNSUPPORTED (float32, or a shape of size 0 above),
+ * SPV_ERR_CAPACITY (packed_bytes too small).
+ *
+ * spv_sparse_conv_nbr_packed, spv_sparse_conv_up_packed, spv_linear_packed --
+ * spv_sparse_conv_nbr, spv_sparse_conv_up and spv_linear with weights packed by
+ * spv_pack_weights for exactly (K3 = 27, 8 and 1 respectively, Cin, Cout) in
+ * place of W, Cin_full and Cout_full; results are identical to the unpacked
+ * calls'.  spv_linear_packed takes only the shapes of its matrix-core kernel
+ * (bf16/f16, Cin a multiple of 8 with ceil(Cin/32) in {1, 2, 3, 4, 8}, Cout/16
+ * rounded up in {1, 2, 4, 6, 8, 16}, Cout a multiple of 16 unless at most 32),
+ * else SPV_ERR_UNSUPPORTED.  No weight packing is launched.
+ */
+size_t spv_packed_weights_bytes(int32_t K3, int32_t Cin, int32_t Cout);
+spv_status spv_pack_weights(void* stream, const void* W, int32_t K3, int32_t Cin_full, int32_t Cout_full,
+                            int32_t Cin, int32_t Cout, spv_dtype dt, void* packed, size_t packed_bytes);
+spv_status spv_sparse_conv_nbr_packed(void* stream, void* ws, size_t ws_bytes,
+                                      const void* in, int64_t in_rows, int32_t Cin, const int32_t* nbr,
+                                      const void* Wpacked, const float* scale, const float* shift,
+                                      const void* res, int32_t relu, void* out, const int64_t* m_out_dev,
+                                      int64_t m_out_cap, int32_t Cout, spv_dtype dt);
+spv_status spv_sparse_conv_up_packed(void* stream, void* ws, size_t ws_bytes,
+                                     const void* in, const int64_t* m_in_dev, int64_t m_in_cap, int32_t Cin,
+                                     const int32_t* children, const void* Wpacked,
+                                     const float* scale, const float* shift, const void* res, int32_t relu,
+                                     void* out, int64_t out_rows, int32_t Cout, spv_dtype dt);
+spv_status spv_linear_packed(void* stream, void* ws, size_t ws_bytes,
+                             const void* in, const int64_t* m_dev, int64_t m_cap, int32_t Cin,
+                             const void* Wpacked, const float* scale, const float* shift, int32_t relu,
+                             const void* res, int32_t res_after_act, void* out, int32_t Cout, spv_dtype dt);
+
+/*
  * Backward passes (training, Sec. 4.2 trains the super network end to end).
  *
  * spv_sparse_conv_dgrad -- input gradient of spv_sparse_conv (without its

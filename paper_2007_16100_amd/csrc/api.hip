@@ -92,8 +92,11 @@ size_t layout_conv(void* ws, size_t bytes, int64_t m_out_cap, int K3, int Cin, i
     return a.used;
 }
 
+// every layout starts with the status header, which calls that record no device
+// errors leave untouched
 size_t layout_linear(void* ws, size_t bytes, int Cin, int Cout, void** wpack) {
     Arena a(ws, bytes);
+    a.take<Header>(1);
     *wpack = plan_linear_ws(a, Cin, Cout);
     return a.used;
 }
@@ -197,6 +200,7 @@ size_t spv_workspace_bytes(int64_t max_points, int32_t max_C) {
 size_t spv_wgrad_workspace_bytes(int32_t K3, int32_t Cin, int32_t Cout) {
     if (K3 <= 0 || Cin <= 0 || Cout <= 0) return 0;
     Arena a(nullptr, 0);
+    a.take<Header>(1);
     plan_wgrad_ws(a, K3, Cin, Cout);
     return a.used;
 }
@@ -392,10 +396,12 @@ spv_status spv_kernel_map_nbr(void* stream, void* ws, size_t ws_bytes, const int
     return hip_check();
 }
 
-spv_status spv_sparse_conv_nbr(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows, int32_t Cin,
-                               const int32_t* nbr, const void* W, int32_t Cin_full, int32_t Cout_full,
-                               const float* scale, const float* shift, const void* res, int32_t relu, void* out,
-                               const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
+// W: the weights to pack into the workspace, or (packed != NULL) unused
+static spv_status conv_nbr_call(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows, int32_t Cin,
+                                const int32_t* nbr, const void* W, int32_t Cin_full, int32_t Cout_full,
+                                const void* packed, const float* scale, const float* shift, const void* res,
+                                int32_t relu, void* out, const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout,
+                                spv_dtype dt) {
     if (!ws || in_rows < 0 || m_out_cap < 0 || m_out_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !W ||
         !valid_dt(dt) || Cin > Cin_full || Cout > Cout_full)
         return SPV_ERR_INVALID_ARG;
@@ -414,9 +420,28 @@ spv_status spv_sparse_conv_nbr(void* stream, void* ws, size_t ws_bytes, const vo
     p.nbr = const_cast<int32_t*>(nbr);  // read only
     p.m_out_dev = m_out_dev;
     p.res = res;
-    launch_pack_job(s, conv_pack_job(27, W, L.wpack, Cin, Cout, dt, Cout_full, (int64_t)Cin_full * Cout_full));
-    launch_conv_union(s, p, in, Cin, in_rows, Cout, L.wpack, scale, shift, relu, out, dt);
+    void* wpack = packed ? const_cast<void*>(packed) : L.wpack;
+    if (!packed)
+        launch_pack_job(s, conv_pack_job(27, W, L.wpack, Cin, Cout, dt, Cout_full, (int64_t)Cin_full * Cout_full));
+    launch_conv_union(s, p, in, Cin, in_rows, Cout, wpack, scale, shift, relu, out, dt);
     return hip_check();
+}
+
+spv_status spv_sparse_conv_nbr(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows, int32_t Cin,
+                               const int32_t* nbr, const void* W, int32_t Cin_full, int32_t Cout_full,
+                               const float* scale, const float* shift, const void* res, int32_t relu, void* out,
+                               const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
+    return conv_nbr_call(stream, ws, ws_bytes, in, in_rows, Cin, nbr, W, Cin_full, Cout_full, nullptr, scale, shift,
+                         res, relu, out, m_out_dev, m_out_cap, Cout, dt);
+}
+
+spv_status spv_sparse_conv_nbr_packed(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t in_rows,
+                                      int32_t Cin, const int32_t* nbr, const void* Wpacked, const float* scale,
+                                      const float* shift, const void* res, int32_t relu, void* out,
+                                      const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
+    if (!Wpacked) return SPV_ERR_INVALID_ARG;
+    return conv_nbr_call(stream, ws, ws_bytes, in, in_rows, Cin, nbr, Wpacked, Cin, Cout, Wpacked, scale, shift, res,
+                         relu, out, m_out_dev, m_out_cap, Cout, dt);
 }
 
 spv_status spv_map_children(void* stream, void* ws, size_t ws_bytes, const int32_t* off, const int32_t* pairs,
@@ -432,10 +457,11 @@ spv_status spv_map_children(void* stream, void* ws, size_t ws_bytes, const int32
     return hip_check();
 }
 
-spv_status spv_sparse_conv_up(void* stream, void* ws, size_t ws_bytes, const void* in, const int64_t* m_in_dev,
-                              int64_t m_in_cap, int32_t Cin, const int32_t* children, const void* W, int32_t Cin_full,
-                              int32_t Cout_full, const float* scale, const float* shift, const void* res, int32_t relu,
-                              void* out, int64_t out_rows, int32_t Cout, spv_dtype dt) {
+static spv_status conv_up_call(void* stream, void* ws, size_t ws_bytes, const void* in, const int64_t* m_in_dev,
+                               int64_t m_in_cap, int32_t Cin, const int32_t* children, const void* W, int32_t Cin_full,
+                               int32_t Cout_full, const void* packed, const float* scale, const float* shift,
+                               const void* res, int32_t relu, void* out, int64_t out_rows, int32_t Cout,
+                               spv_dtype dt) {
     if (!ws || m_in_cap < 0 || m_in_cap >= ((int64_t)1 << 31) || out_rows < 0 || Cin <= 0 || Cout <= 0 || !W ||
         !valid_dt(dt) || Cin > Cin_full || Cout > Cout_full)
         return SPV_ERR_INVALID_ARG;
@@ -444,16 +470,39 @@ spv_status spv_sparse_conv_up(void* stream, void* ws, size_t ws_bytes, const voi
     if (!aligned16(in) || !aligned16(out) || !aligned16(W) || !aligned16(res) || (res && res == out) || in == out)
         return SPV_ERR_INVALID_ARG;
     Arena probe(nullptr, 0);
+    probe.take<Header>(1);
     plan_wpack_ws(probe, kUpChildren, Cin, Cout);
     if (need(probe.used, ws_bytes)) return SPV_ERR_CAPACITY;
     Arena a(ws, ws_bytes);
+    a.take<Header>(1);
     void* wpack = plan_wpack_ws(a, kUpChildren, Cin, Cout);
     if (m_in_cap == 0) return SPV_OK;
     hipStream_t s = (hipStream_t)stream;
-    launch_pack_job(s, conv_pack_job(kUpChildren, W, wpack, Cin, Cout, dt, Cout_full, (int64_t)Cin_full * Cout_full));
+    if (packed)
+        wpack = const_cast<void*>(packed);
+    else
+        launch_pack_job(s, conv_pack_job(kUpChildren, W, wpack, Cin, Cout, dt, Cout_full,
+                                         (int64_t)Cin_full * Cout_full));
     UpArgs u{children, m_in_dev, m_in_cap, in, Cin, Cout, (int)dt, scale, shift, relu, res, out, out_rows};
     launch_conv_up(s, u, wpack);
     return hip_check();
+}
+
+spv_status spv_sparse_conv_up(void* stream, void* ws, size_t ws_bytes, const void* in, const int64_t* m_in_dev,
+                              int64_t m_in_cap, int32_t Cin, const int32_t* children, const void* W, int32_t Cin_full,
+                              int32_t Cout_full, const float* scale, const float* shift, const void* res, int32_t relu,
+                              void* out, int64_t out_rows, int32_t Cout, spv_dtype dt) {
+    return conv_up_call(stream, ws, ws_bytes, in, m_in_dev, m_in_cap, Cin, children, W, Cin_full, Cout_full, nullptr,
+                        scale, shift, res, relu, out, out_rows, Cout, dt);
+}
+
+spv_status spv_sparse_conv_up_packed(void* stream, void* ws, size_t ws_bytes, const void* in, const int64_t* m_in_dev,
+                                     int64_t m_in_cap, int32_t Cin, const int32_t* children, const void* Wpacked,
+                                     const float* scale, const float* shift, const void* res, int32_t relu, void* out,
+                                     int64_t out_rows, int32_t Cout, spv_dtype dt) {
+    if (!Wpacked) return SPV_ERR_INVALID_ARG;
+    return conv_up_call(stream, ws, ws_bytes, in, m_in_dev, m_in_cap, Cin, children, Wpacked, Cin, Cout, Wpacked,
+                        scale, shift, res, relu, out, out_rows, Cout, dt);
 }
 
 spv_status spv_sparse_conv_dgrad(void* stream, void* ws, size_t ws_bytes, const void* dy, int64_t dy_rows,
@@ -476,9 +525,11 @@ spv_status spv_sparse_conv_wgrad(void* stream, void* ws, size_t ws_bytes, const 
     if ((x_rows > 0 && !x) || (dy_rows > 0 && !dy) || (pair_cap > 0 && !pairs)) return SPV_ERR_INVALID_ARG;
     if (!aligned16(x) || !aligned16(dy)) return SPV_ERR_INVALID_ARG;
     Arena probe(nullptr, 0);
+    probe.take<Header>(1);
     plan_wgrad_ws(probe, K3, Cin, Cout);
     if (need(probe.used, ws_bytes)) return SPV_ERR_CAPACITY;
     Arena a(ws, ws_bytes);
+    a.take<Header>(1);
     float* partial = (float*)plan_wgrad_ws(a, K3, Cin, Cout);
     WgradArgs w{x, x_rows, Cin, dy, dy_rows, Cout, off, pairs, pair_cap, K3, transposed ? 1 : 0, (int)dt};
     launch_wgrad((hipStream_t)stream, w, partial, dW);
@@ -501,10 +552,10 @@ spv_status spv_devoxelize_backward(void* stream, const int32_t* corner_idx, cons
     return hip_check();
 }
 
-spv_status spv_linear(void* stream, void* ws, size_t ws_bytes, const void* in, const int64_t* m_dev, int64_t m_cap,
-                      int32_t Cin, const void* W, int32_t Cin_full, int32_t Cout_full, const float* scale,
-                      const float* shift, int32_t relu, const void* res, int32_t res_after_act, void* out,
-                      int32_t Cout, spv_dtype dt) {
+static spv_status linear_call(void* stream, void* ws, size_t ws_bytes, const void* in, const int64_t* m_dev,
+                              int64_t m_cap, int32_t Cin, const void* W, int32_t Cin_full, int32_t Cout_full,
+                              const void* packed, const float* scale, const float* shift, int32_t relu,
+                              const void* res, int32_t res_after_act, void* out, int32_t Cout, spv_dtype dt) {
     if (!ws || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !W || !valid_dt(dt) ||
         Cin > Cin_full || Cout > Cout_full)
         return SPV_ERR_INVALID_ARG;
@@ -517,7 +568,55 @@ spv_status spv_linear(void* stream, void* ws, size_t ws_bytes, const void* in, c
     if (m_cap == 0) return SPV_OK;
     LinearArgs a{in, m_dev, m_cap, Cin, Cout, (int)dt, W, Cout_full, scale, shift, relu, res, res_after_act ? 1 : 0,
                  out};
-    launch_linear((hipStream_t)stream, a, wpack);
+    launch_linear((hipStream_t)stream, a, packed ? const_cast<void*>(packed) : wpack, packed != nullptr);
+    return hip_check();
+}
+
+spv_status spv_linear(void* stream, void* ws, size_t ws_bytes, const void* in, const int64_t* m_dev, int64_t m_cap,
+                      int32_t Cin, const void* W, int32_t Cin_full, int32_t Cout_full, const float* scale,
+                      const float* shift, int32_t relu, const void* res, int32_t res_after_act, void* out,
+                      int32_t Cout, spv_dtype dt) {
+    return linear_call(stream, ws, ws_bytes, in, m_dev, m_cap, Cin, W, Cin_full, Cout_full, nullptr, scale, shift,
+                       relu, res, res_after_act, out, Cout, dt);
+}
+
+spv_status spv_linear_packed(void* stream, void* ws, size_t ws_bytes, const void* in, const int64_t* m_dev,
+                             int64_t m_cap, int32_t Cin, const void* Wpacked, const float* scale, const float* shift,
+                             int32_t relu, const void* res, int32_t res_after_act, void* out, int32_t Cout,
+                             spv_dtype dt) {
+    if (!Wpacked) return SPV_ERR_INVALID_ARG;
+    // the vector-ALU path reads W itself: packed weights serve the matrix-core kernel only
+    if (!linear_mfma_supported(Cin, Cout, dt)) return SPV_ERR_UNSUPPORTED;
+    return linear_call(stream, ws, ws_bytes, in, m_dev, m_cap, Cin, Wpacked, Cin, Cout, Wpacked, scale, shift, relu,
+                       res, res_after_act, out, Cout, dt);
+}
+
+// the fragment layout the neighbour-table, upsampling and linear kernels read
+static bool packed_shape(int32_t K3, int32_t Cin, int32_t Cout, int* kch, int* nb) {
+    const int k = (Cin + 31) / 32, n = (Cout + 15) / 16;
+    if (K3 <= 0 || K3 > 27 || Cin <= 0 || Cout <= 0) return false;
+    if (!(k == 1 || k == 2 || k == 3 || k == 4 || k == 6 || k == 8) || n > 16) return false;
+    *kch = k;
+    *nb = n;
+    return true;
+}
+
+size_t spv_packed_weights_bytes(int32_t K3, int32_t Cin, int32_t Cout) {
+    int kch, nb;
+    if (!packed_shape(K3, Cin, Cout, &kch, &nb)) return 0;
+    return (size_t)K3 * kch * nb * 64 * sizeof(uint4);
+}
+
+spv_status spv_pack_weights(void* stream, const void* W, int32_t K3, int32_t Cin_full, int32_t Cout_full, int32_t Cin,
+                            int32_t Cout, spv_dtype dt, void* packed, size_t packed_bytes) {
+    if (!W || !packed || Cin > Cin_full || Cout > Cout_full || !valid_dt(dt)) return SPV_ERR_INVALID_ARG;
+    if (!aligned16(packed)) return SPV_ERR_INVALID_ARG;
+    int kch, nb;
+    if (dt == SPV_F32 || !packed_shape(K3, Cin, Cout, &kch, &nb)) return SPV_ERR_UNSUPPORTED;
+    if (packed_bytes < spv_packed_weights_bytes(K3, Cin, Cout)) return SPV_ERR_CAPACITY;
+    PackJob q{(const uint16_t*)W, (uint4*)packed, K3, Cin, Cout, kch, nb, (int64_t)K3 * kch * nb * 64, Cout_full,
+              (int64_t)Cin_full * Cout_full, 1};
+    launch_pack_job((hipStream_t)stream, q);
     return hip_check();
 }
 

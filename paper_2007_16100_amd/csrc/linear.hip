@@ -180,13 +180,13 @@ static void launch_lin_dt(hipStream_t s, const LinearArgs& a, const void* wpack)
     }
 }
 
-void launch_linear(hipStream_t s, const LinearArgs& a, void* wpack) {
+void launch_linear(hipStream_t s, const LinearArgs& a, void* wpack, bool prepacked) {
     if (a.m_cap <= 0) return;
     if (linear_mfma_supported(a.Cin, a.Cout, a.dt)) {
         const int KCH = linear_kch(a.Cin), NB = (a.Cout + 15) / 16;
         PackJob q{(const uint16_t*)a.W, (uint4*)wpack, 1, a.Cin, a.Cout, KCH, NB, (int64_t)KCH * NB * 64, a.ldw,
                   (int64_t)a.Cin * a.ldw, 1};
-        launch_pack_job(s, q);
+        if (!prepacked) launch_pack_job(s, q);
         if (a.dt == SPV_BF16) launch_lin_dt<SPV_BF16>(s, a, wpack);
         else launch_lin_dt<SPV_F16>(s, a, wpack);
         return;

@@ -265,7 +265,8 @@ struct LinearArgs {
 bool linear_mfma_supported(int Cin, int Cout, int dt);
 void* plan_linear_ws(Arena& a, int Cin, int Cout);
 // packs W into wpack (MFMA path) and runs the layer
-void launch_linear(hipStream_t s, const LinearArgs& a, void* wpack);
+// prepacked: wpack already holds W's fragments (spv_pack_weights), no packing launch
+void launch_linear(hipStream_t s, const LinearArgs& a, void* wpack, bool prepacked = false);
 
 // --- transposed k=2 s=2 conv on a child table (conv_up.hip) -----------------------
 struct UpArgs {

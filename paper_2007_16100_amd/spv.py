@@ -29,7 +29,9 @@ SPV_DEVOX_CENTER, SPV_DEVOX_CORNER, SPV_DEVOX_NEAREST = 0, 1, 2
 _DT = {torch.float32: SPV_F32, torch.bfloat16: SPV_BF16, torch.float16: SPV_F16}
 
 # every symbol include/spv.h declares
-EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_voxelize_onto", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced",
+EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_voxelize_onto", "spv_packed_weights_bytes",
+           "spv_pack_weights", "spv_sparse_conv_nbr_packed", "spv_sparse_conv_up_packed", "spv_linear_packed",
+           "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced",
            "spv_linear", "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_map_children", "spv_sparse_conv_up",
            "spv_sparse_conv_dgrad", "spv_wgrad_workspace_bytes", "spv_sparse_conv_wgrad",
            "spv_voxelize_backward",
@@ -70,6 +72,14 @@ def lib():
         L.spv_block_workspace_bytes.argtypes = [i64, i32]
         L.spv_block_workspace_bytes.restype = sz
         L.spv_voxelize.argtypes = [vp, vp, sz, vp, vp, i64, f32, vp, i32, i32, vp, vp, vp, vp, vp, vp]
+        L.spv_packed_weights_bytes.argtypes = [i32, i32, i32]
+        L.spv_packed_weights_bytes.restype = sz
+        L.spv_pack_weights.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, vp, sz]
+        L.spv_sparse_conv_nbr_packed.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, vp, vp, vp, i32, vp, vp, i64, i32,
+                                                 i32]
+        L.spv_sparse_conv_up_packed.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, vp, vp, vp, vp, i32, vp, i64, i32,
+                                                i32]
+        L.spv_linear_packed.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, vp, vp, i32, vp, i32, vp, i32, i32]
         L.spv_voxelize_onto.argtypes = [vp, vp, sz, vp, vp, i64, vp, vp, i64, f32, vp, i32, i32, vp, vp, vp]
         L.spv_kernel_map.argtypes = [vp, vp, sz, vp, vp, i64, i32, i32, vp, vp, vp, vp, i64, vp]
         L.spv_sparse_conv.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i64, i32, i32, vp, vp, vp, i32, vp, vp, i64,
@@ -97,7 +107,8 @@ def lib():
         L.spv_status_string.argtypes = [i32]
         L.spv_status_string.restype = ct.c_char_p
         L.spv_last_hip_error.argtypes = []
-        for f in ("spv_voxelize", "spv_voxelize_onto", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced", "spv_linear",
+        for f in ("spv_voxelize", "spv_voxelize_onto", "spv_pack_weights", "spv_sparse_conv_nbr_packed",
+                  "spv_sparse_conv_up_packed", "spv_linear_packed", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced", "spv_linear",
                   "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_map_children", "spv_sparse_conv_up",
                   "spv_sparse_conv_dgrad", "spv_sparse_conv_wgrad",
                   "spv_voxelize_backward",
@@ -307,6 +318,73 @@ def spv_linear(ws: Workspace, x: torch.Tensor, W: torch.Tensor, Cout: Optional[i
                           Cout_full, _ptr(scale), _ptr(shift), int(relu), _ptr(res), int(res_after_act), _ptr(out),
                           Cout, _DT[x.dtype])
     _chk(st, "spv_linear")
+    return out
+
+
+def spv_pack_weights(W: torch.Tensor, Cin: Optional[int] = None, Cout: Optional[int] = None,
+                     cin_offset: int = 0) -> Optional[torch.Tensor]:
+    """The matrix-core fragments of W[:, cin_offset : cin_offset + Cin, :Cout] (W [K3][Cin_full][Cout_full],
+    or [Cin_full][Cout_full] for a linear layer) as a uint8 device tensor, or None where no kernel
+    reads that shape (and for float32)."""
+    W3 = W if W.dim() == 3 else W.unsqueeze(0)
+    K3, Cin_full, Cout_full = W3.shape
+    Cin = Cin_full - cin_offset if Cin is None else Cin
+    Cout = Cout_full if Cout is None else Cout
+    if cin_offset < 0 or cin_offset + Cin > Cin_full:
+        raise ValueError("input-channel slice outside the weight")
+    nbytes = lib().spv_packed_weights_bytes(K3, Cin, Cout)
+    if nbytes == 0 or W.dtype == torch.float32:
+        return None
+    out = torch.empty(nbytes, dtype=torch.uint8, device=W.device)
+    wp = ct.c_void_p(_ptr(W3).value + cin_offset * Cout_full * W3.element_size())
+    st = lib().spv_pack_weights(_stream(), wp, K3, Cin_full, Cout_full, Cin, Cout, _DT[W.dtype], _ptr(out), nbytes)
+    _chk(st, "spv_pack_weights")
+    return out
+
+
+def spv_sparse_conv_nbr_packed(ws: Workspace, x: torch.Tensor, nbr: torch.Tensor, Wp: torch.Tensor, Cout: int,
+                               m_out_cap: int, m_out_dev: Optional[torch.Tensor] = None,
+                               scale: Optional[torch.Tensor] = None, shift: Optional[torch.Tensor] = None,
+                               relu: bool = False, res: Optional[torch.Tensor] = None,
+                               out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """spv_sparse_conv_nbr with weights from spv_pack_weights (K3 = 27, x's width, Cout)."""
+    if out is None:
+        out = torch.empty((max(m_out_cap, 1), Cout), dtype=x.dtype, device=x.device)
+    st = lib().spv_sparse_conv_nbr_packed(_stream(), ws.ptr, ws.nbytes, _ptr(x), x.shape[0], x.shape[1], _ptr(nbr),
+                                          _ptr(Wp), _ptr(scale), _ptr(shift), _ptr(res), int(relu), _ptr(out),
+                                          _ptr(m_out_dev), m_out_cap, Cout, _DT[x.dtype])
+    _chk(st, "spv_sparse_conv_nbr_packed")
+    return out
+
+
+def spv_sparse_conv_up_packed(ws: Workspace, x: torch.Tensor, children: torch.Tensor, Wp: torch.Tensor, Cout: int,
+                              out_rows: int, m_in_dev: Optional[torch.Tensor] = None,
+                              scale: Optional[torch.Tensor] = None, shift: Optional[torch.Tensor] = None,
+                              relu: bool = False, res: Optional[torch.Tensor] = None,
+                              out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """spv_sparse_conv_up with weights from spv_pack_weights (K3 = 8, x's width, Cout)."""
+    if out is None:
+        out = torch.empty((max(out_rows, 1), Cout), dtype=x.dtype, device=x.device)
+    st = lib().spv_sparse_conv_up_packed(_stream(), ws.ptr, ws.nbytes, _ptr(x), _ptr(m_in_dev), x.shape[0],
+                                         x.shape[1], _ptr(children), _ptr(Wp), _ptr(scale), _ptr(shift), _ptr(res),
+                                         int(relu), _ptr(out), out_rows, Cout, _DT[x.dtype])
+    _chk(st, "spv_sparse_conv_up_packed")
+    return out
+
+
+def spv_linear_packed(ws: Workspace, x: torch.Tensor, Wp: torch.Tensor, Cout: int,
+                      m_dev: Optional[torch.Tensor] = None, m_cap: Optional[int] = None,
+                      scale: Optional[torch.Tensor] = None, shift: Optional[torch.Tensor] = None, relu: bool = False,
+                      res: Optional[torch.Tensor] = None, res_after_act: bool = False,
+                      out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """spv_linear with weights from spv_pack_weights (K3 = 1, x's width, Cout)."""
+    m_cap = x.shape[0] if m_cap is None else m_cap
+    if out is None:
+        out = torch.empty((max(m_cap, 1), Cout), dtype=x.dtype, device=x.device)
+    st = lib().spv_linear_packed(_stream(), ws.ptr, ws.nbytes, _ptr(x), _ptr(m_dev), m_cap, x.shape[1], _ptr(Wp),
+                                 _ptr(scale), _ptr(shift), int(relu), _ptr(res), int(res_after_act), _ptr(out), Cout,
+                                 _DT[x.dtype])
+    _chk(st, "spv_linear_packed")
     return out
 
 

@@ -23,6 +23,8 @@ holds the device buffers:
 * a conv over a skip concatenation [t; x] runs as two sliced convs,
   W_t t (scaled, unshifted) handed as the residual input of W_x x + shift;
   the 1x1 shortcut over it likewise as two linear layers;
+* the weights of the neighbour-table, upsampling and linear layers are packed into
+  matrix-core fragments once, on first use, and read packed by every later forward;
 * a devoxelization whose point MLP the fused kernel does not take on matrix
   cores (C_p above 128) runs as a devoxelization plus a linear layer that adds
   it after the activation.
@@ -80,6 +82,9 @@ class SPVCNN:
             self.P[name] = (self._dev(W), None if sc is None else torch.from_numpy(np.asarray(sc)).to(device),
                             None if sh is None else torch.from_numpy(np.asarray(sh)).to(device))
         self.ws = None
+        # matrix-core fragments of every (layer, input-channel slice) that a kernel reading packed
+        # weights runs, packed on first use: the weights stay fixed across forwards
+        self._pk: Dict[tuple, Optional[torch.Tensor]] = {}
 
     def _dev(self, a):
         a = np.ascontiguousarray(a)
@@ -111,6 +116,12 @@ class SPVCNN:
         return Plan(coords, m, down, nbr, [None] * 5, children), vox
 
     # -- layers --------------------------------------------------------------
+    def _packed(self, name, cin_offset, Cin, Cout):
+        key = (name, cin_offset, Cin, Cout)
+        if key not in self._pk:
+            self._pk[key] = spv.spv_pack_weights(self.P[name][0], Cin, Cout, cin_offset)
+        return self._pk[key]
+
     def _conv(self, x, name, km, m_out, relu=True, transposed=False, res=None, cin_offset=0, shift=True):
         W, sc, sh = self.P[name]
         return spv.spv_sparse_conv_sliced(self.ws, x, km.off, km.pairs, W, x.shape[1], W.shape[2], m_out, scale=sc,
@@ -124,16 +135,28 @@ class SPVCNN:
         Cin, Cout = x.shape[1], W.shape[2]
         widths = (32, 64, 96, 128, 256)
         if self.dt != torch.float32 and Cin in widths and Cout in widths:
-            return spv.spv_sparse_conv_nbr(self.ws, x, plan.nbr[s], W, Cout, plan.m[s], scale=sc,
-                                           shift=sh if shift else None, relu=relu, res=res, cin_offset=cin_offset)
+            return spv.spv_sparse_conv_nbr_packed(self.ws, x, plan.nbr[s], self._packed(name, cin_offset, Cin, Cout),
+                                                  Cout, plan.m[s], scale=sc, shift=sh if shift else None, relu=relu,
+                                                  res=res)
         if plan.subm[s] is None:
             plan.subm[s] = spv.spv_kernel_map(self.ws, plan.coords[s], sync=False)
         return self._conv(x, name, plan.subm[s], plan.m[s], relu=relu, res=res, cin_offset=cin_offset, shift=shift)
 
     def _lin(self, x, name, relu=False, res=None, res_after=False, cin_offset=0, shift=True):
         W, sc, sh = self.P[name]
+        Cin, Cout = x.shape[1], W.shape[1]
+        wp = self._packed(name, cin_offset, Cin, Cout) if self._linear_packable(Cin, Cout) else None
+        if wp is not None:
+            return spv.spv_linear_packed(self.ws, x, wp, Cout, scale=sc, shift=sh if shift else None, relu=relu,
+                                         res=res, res_after_act=res_after)
         return spv.spv_linear(self.ws, x, W, scale=sc, shift=sh if shift else None, relu=relu, res=res,
                               res_after_act=res_after, cin_offset=cin_offset)
+
+    def _linear_packable(self, Cin, Cout):
+        """The shapes of the matrix-core linear kernel, the one that reads packed weights."""
+        kch, nb = (Cin + 31) // 32, (Cout + 15) // 16
+        return (self.dt != torch.float32 and Cin % 8 == 0 and kch in (1, 2, 3, 4, 8) and nb in (1, 2, 4, 6, 8, 16)
+                and (Cout % 16 == 0 or nb <= 2))
 
     def _resblock(self, plan, parts, name, s):
         """Residual block at stride 2^s over the concatenation of `parts` (one tensor: no
@@ -165,7 +188,7 @@ class SPVCNN:
             return spv.spv_devoxelize(self.ws, plan.coords[s], vfeat, xyz, self.v, s, self.mode, batch, pfeat=z, Wp=W,
                                       scale_p=sc, shift_p=sh, relu_p=True)
         d = spv.spv_devoxelize(self.ws, plan.coords[s], vfeat, xyz, self.v, s, self.mode, batch)
-        return spv.spv_linear(self.ws, z, W, scale=sc, shift=sh, relu=True, res=d, res_after_act=True)
+        return self._lin(z, name, relu=True, res=d, res_after=True)
 
     def _revoxelize(self, plan, xyz, z, s, batch):
         """Scatter-mean of the point features at stride 2^s onto that stride's voxels, which the
@@ -202,8 +225,9 @@ class SPVCNN:
             widths = (32, 64, 96, 128, 256)
             if self.dt != torch.float32 and y.shape[1] in widths and W.shape[2] in widths:
                 # every fine voxel has its parent: the child-table kernel writes each output row once
-                t = spv.spv_sparse_conv_up(self.ws, y, plan.children[5 - u], W, W.shape[2], m[4 - u], scale=sc,
-                                           shift=sh, relu=True)
+                t = spv.spv_sparse_conv_up_packed(self.ws, y, plan.children[5 - u],
+                                                  self._packed(f"up.{u}", 0, y.shape[1], W.shape[2]), W.shape[2],
+                                                  m[4 - u], scale=sc, shift=sh, relu=True)
             else:
                 t = self._conv(y, f"up.{u}", plan.down[5 - u], m[4 - u], transposed=True)
             y = self._resblock(plan, [t, skips[4 - u]], f"dec.{u}.0", 4 - u)
@@ -215,8 +239,7 @@ class SPVCNN:
         y, vox2 = self._revoxelize(plan, xyz, z, 2, batch)
         y = up(up(y, 3), 4)
         z = self._fuse(plan, y, 0, z, "point.3", xyz, batch)
-        W, _, bias = self.P["head"]
-        out = spv.spv_linear(self.ws, z, W, shift=bias)
+        out = self._lin(z, "head")
         if trace is not None:
             trace.update(plan=plan, revox=[vox4, vox2], z3=z, y4=y, skips=skips)
         return out

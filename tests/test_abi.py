@@ -60,6 +60,22 @@ def test_host_side_validation_without_gpu():
                                P) == spv.SPV_ERR_INVALID_ARG
     assert L.spv_voxelize_onto(None, ws, 16, P, None, 4, P, None, 4, ct.c_float(0.1), None, 0, 0, None, P,
                                P) == spv.SPV_ERR_CAPACITY
+    # pre-packed weights: sizes, and the host-side rejections
+    frag = 64 * 16
+    assert L.spv_packed_weights_bytes(27, 96, 96) == 27 * 3 * 6 * frag
+    assert L.spv_packed_weights_bytes(1, 96, 19) == 3 * 2 * frag
+    assert L.spv_packed_weights_bytes(8, 256, 256) == 8 * 8 * 16 * frag
+    assert L.spv_packed_weights_bytes(27, 160, 96) == 0 and L.spv_packed_weights_bytes(27, 96, 272) == 0
+    big = ct.c_size_t(1 << 30)
+    assert L.spv_pack_weights(None, None, 27, 96, 96, 96, 96, 1, P, big) == spv.SPV_ERR_INVALID_ARG
+    assert L.spv_pack_weights(None, P, 27, 64, 96, 96, 96, 1, P, big) == spv.SPV_ERR_INVALID_ARG  # slice too wide
+    assert L.spv_pack_weights(None, P, 27, 96, 96, 96, 96, 0, P, big) == spv.SPV_ERR_UNSUPPORTED  # float32
+    assert L.spv_pack_weights(None, P, 27, 160, 96, 160, 96, 1, P, big) == spv.SPV_ERR_UNSUPPORTED
+    assert L.spv_pack_weights(None, P, 27, 96, 96, 96, 96, 1, P, 1000) == spv.SPV_ERR_CAPACITY
+    assert L.spv_linear_packed(None, ws, 1 << 30, P, None, 4, 96, P, None, None, 0, None, 0, P, 96,
+                               0) == spv.SPV_ERR_UNSUPPORTED  # float32: no matrix-core linear
+    assert L.spv_sparse_conv_nbr_packed(None, ws, 1 << 30, P, 4, 96, P, None, None, None, None, 0, P, None, 4, 96,
+                                        1) == spv.SPV_ERR_INVALID_ARG  # no packed weights
     # unsupported kernel-map geometry
     st = L.spv_kernel_map(None, ws, 1 << 30, ct.c_void_p(16), None, 4, 2, 1, ct.c_void_p(16), None, ct.c_void_p(16),
                           ct.c_void_p(16), 100, None)

@@ -892,6 +892,74 @@ def test_conv_up_rejects_other_shapes(spv):
 
 
 # ---------------------------------------------------------------------------
+# pre-packed weights
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("cin,cout,coff", [(96, 96, 0), (256, 256, 0), (32, 64, 32), (128, 96, 64), (64, 256, 0)])
+def test_packed_weights_match_unpacked(spv, sweep, cin, cout, coff):
+    """Weights packed once give the unpacked calls' outputs bit for bit: the neighbour-table
+    conv and the upsampling conv (on an input-channel slice at offset coff), and the linear layer."""
+    dt = "bf16"
+    rc, _, _, _ = oracle.voxelize(sweep, 0.05)
+    oc, off, pairs = oracle.kernel_map(rc, 2, 2)
+    ws = spv.Workspace.for_ops(len(rc), 256)
+    sc, sh = (dev(a) for a in synth.folded_bn(cout, 1403))
+    r = dev(synth.normal((len(rc), cout), 1404, dtype=dt), dt)
+    # neighbour-table conv
+    nbr = spv.spv_kernel_map_nbr(ws, dev(rc))
+    x = dev(synth.normal((len(rc), cin), 1401, dtype=dt), dt)
+    W = dev(synth.conv_weight(27, cin + coff, cout, 1402, dt), dt)
+    a = spv.spv_sparse_conv_nbr(ws, x, nbr, W, cout, len(rc), scale=sc, shift=sh, relu=True, res=r, cin_offset=coff)
+    wp = spv.spv_pack_weights(W, cin, cout, coff)
+    assert wp.numel() == spv.lib().spv_packed_weights_bytes(27, cin, cout)
+    b = spv.spv_sparse_conv_nbr_packed(ws, x, nbr, wp, cout, len(rc), scale=sc, shift=sh, relu=True, res=r)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    # upsampling conv on the stride-2 map's child table
+    ch = spv.spv_map_children(ws, dev(off), dev(pairs), len(rc), len(oc))
+    x2 = dev(synth.normal((len(oc), cin), 1405, dtype=dt), dt)
+    W8 = dev(synth.conv_weight(8, cin + coff, cout, 1406, dt), dt)
+    a = spv.spv_sparse_conv_up(ws, x2, ch, W8, cout, len(rc), scale=sc, shift=sh, relu=True, res=r, cin_offset=coff)
+    b = spv.spv_sparse_conv_up_packed(ws, x2, ch, spv.spv_pack_weights(W8, cin, cout, coff), cout, len(rc), scale=sc,
+                                      shift=sh, relu=True, res=r)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    # linear layer, and the ragged classifier width
+    for co in (cout, 19):
+        W1 = dev(synth.linear_weight(cin + coff, co, 1407, dt), dt)
+        sc1, sh1 = (dev(v) for v in synth.folded_bn(co, 1408))
+        a = spv.spv_linear(ws, x, W1, scale=sc1, shift=sh1, relu=True, cin_offset=coff)
+        b = spv.spv_linear_packed(ws, x, spv.spv_pack_weights(W1, cin, co, coff), co, scale=sc1, shift=sh1, relu=True)
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    torch.cuda.synchronize()
+    assert spv.spv_status_check(ws) == spv.SPV_OK
+
+
+def test_calls_without_device_errors_keep_the_status_word(spv):
+    """The linear layer, the upsampling conv (plain and packed) and the weight gradient record
+    no device errors and keep their weights and partial sums clear of the status word: a
+    pending error of an earlier call on the same workspace survives them."""
+    d, bf = "cuda", torch.bfloat16
+    ws = spv.Workspace.for_ops(64, 64)
+    spv.spv_voxelize(ws, torch.tensor([[1e6, 0.0, 0.0]], dtype=torch.float32, device=d), 0.05, sync=False)
+    x = torch.ones((16, 32), dtype=bf, device=d)
+    W = torch.ones((32, 32), dtype=bf, device=d)
+    W8 = torch.ones((8, 32, 32), dtype=bf, device=d)
+    ch = torch.zeros((16, 8), dtype=torch.int32, device=d)
+    spv.spv_linear(ws, x, W)
+    spv.spv_linear_packed(ws, x, spv.spv_pack_weights(W), 32)
+    spv.spv_sparse_conv_up(ws, x, ch, W8, 32, 16)
+    spv.spv_sparse_conv_up_packed(ws, x, ch, spv.spv_pack_weights(W8), 32, 16)
+    torch.cuda.synchronize()
+    assert spv.spv_status_check(ws) == spv.SPV_ERR_RANGE
+    wsw = spv.Workspace.for_wgrad(27, 32, 32)
+    wsw.buf.zero_()
+    off = torch.ones(28, dtype=torch.int32, device=d)
+    off[0] = 0
+    pairs = torch.zeros((1, 2), dtype=torch.int32, device=d)
+    dW = spv.spv_sparse_conv_wgrad(wsw, x, x, off, pairs, 27)
+    assert float(dW[0, 0, 0]) == 1.0
+    assert spv.spv_status_check(wsw) == spv.SPV_OK
+
+
+# ---------------------------------------------------------------------------
 # empty inputs of the later entry points
 # ---------------------------------------------------------------------------
 def test_empty_inputs_of_network_entry_points(spv):
