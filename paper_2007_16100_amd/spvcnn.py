@@ -116,6 +116,11 @@ class SPVCNN:
         return Plan(coords, m, down, nbr, [None] * 5, children), vox
 
     # -- layers --------------------------------------------------------------
+    def clear_packed(self):
+        """Drop the packed weights: call after changing any weight in ``self.P`` in place, so that
+        the next forward packs the new values."""
+        self._pk.clear()
+
     def _packed(self, name, cin_offset, Cin, Cout):
         key = (name, cin_offset, Cin, Cout)
         if key not in self._pk:
