@@ -150,18 +150,19 @@ class SPVCNN:
     def _lin(self, x, name, relu=False, res=None, res_after=False, cin_offset=0, shift=True):
         W, sc, sh = self.P[name]
         Cin, Cout = x.shape[1], W.shape[1]
-        wp = self._packed(name, cin_offset, Cin, Cout) if self._linear_packable(Cin, Cout) else None
+        key = (name, cin_offset, Cin, Cout)
+        wp = self._packed(name, cin_offset, Cin, Cout)
         if wp is not None:
-            return spv.spv_linear_packed(self.ws, x, wp, Cout, scale=sc, shift=sh if shift else None, relu=relu,
-                                         res=res, res_after_act=res_after)
+            try:
+                return spv.spv_linear_packed(self.ws, x, wp, Cout, scale=sc, shift=sh if shift else None,
+                                             relu=relu, res=res, res_after_act=res_after)
+            except spv.SpvError as e:
+                # a shape only the vector-ALU kernel takes: that kernel reads W itself
+                if e.status != spv.SPV_ERR_UNSUPPORTED:
+                    raise
+                self._pk[key] = None
         return spv.spv_linear(self.ws, x, W, scale=sc, shift=sh if shift else None, relu=relu, res=res,
                               res_after_act=res_after, cin_offset=cin_offset)
-
-    def _linear_packable(self, Cin, Cout):
-        """The shapes of the matrix-core linear kernel, the one that reads packed weights."""
-        kch, nb = (Cin + 31) // 32, (Cout + 15) // 16
-        return (self.dt != torch.float32 and Cin % 8 == 0 and kch in (1, 2, 3, 4, 8) and nb in (1, 2, 4, 6, 8, 16)
-                and (Cout % 16 == 0 or nb <= 2))
 
     def _resblock(self, plan, parts, name, s):
         """Residual block at stride 2^s over the concatenation of `parts` (one tensor: no
