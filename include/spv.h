@@ -281,6 +281,30 @@ spv_status spv_sparse_conv_up(void* stream, void* ws, size_t ws_bytes,
                               void* out, int64_t out_rows, int32_t Cout, spv_dtype dt);
 
 /*
+ * spv_devoxelize_nbr -- spv_devoxelize (Sec. 3.3 "Sparse Devoxelization", with
+ * the point MLP and the fusion add) on a grid that is the points' own
+ * voxelization at voxel_size * 2^stride_log2: point k's voxel is pt2vox[k]
+ * (from spv_voxelize or spv_voxelize_onto at that voxel size) and nbr is the
+ * grid's neighbour table from spv_kernel_map_nbr.  Every corner of a point lies
+ * within one voxel of its own, so the 8 corner indices are read from the
+ * point's row of nbr: no hash table is built.  Results equal spv_devoxelize's
+ * on the same grid.  A point with pt2vox outside [0, m_cap) has no corners
+ * (its output is the MLP term alone).  Only the matrix-core kernel's shapes
+ * (bf16/f16, C/16 in {1, 2, 4, 6, 8, 16}, Cp a multiple of 8 up to 128 or no
+ * MLP), else SPV_ERR_UNSUPPORTED.  No corner outputs.
+ * In:  grid_coords [m_cap][4], vfeat [m_cap][C], nbr [m_cap][27], pt2vox [n];
+ *      the rest as in spv_devoxelize.
+ */
+spv_status spv_devoxelize_nbr(void* stream, void* ws, size_t ws_bytes,
+                              const int32_t* grid_coords, const int64_t* m_dev, int64_t m_cap,
+                              const int32_t* nbr, const int32_t* pt2vox, int32_t stride_log2,
+                              const float* xyz, const int32_t* batch, int64_t n, float voxel_size,
+                              spv_devox_mode mode, const void* vfeat, int32_t C,
+                              const void* pfeat, int32_t Cp, const void* Wp,
+                              const float* scale_p, const float* shift_p, int32_t relu_p,
+                              void* out, spv_dtype dt);
+
+/*
  * Pre-packed weights.  The neighbour-table conv, the upsampling conv and the
  * linear layer copy their weights into matrix-core fragments in every call; a
  * network whose weights stay fixed across forwards packs each once:

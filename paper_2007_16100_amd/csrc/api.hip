@@ -665,6 +665,66 @@ spv_status spv_devoxelize(void* stream, void* ws, size_t ws_bytes, const int32_t
     return hip_check();
 }
 
+spv_status spv_devoxelize_nbr(void* stream, void* ws, size_t ws_bytes, const int32_t* grid_coords, const int64_t* m_dev,
+                              int64_t m_cap, const int32_t* nbr, const int32_t* pt2vox, int32_t stride_log2,
+                              const float* xyz, const int32_t* batch, int64_t n, float voxel_size, spv_devox_mode mode,
+                              const void* vfeat, int32_t C, const void* pfeat, int32_t Cp, const void* Wp,
+                              const float* scale_p, const float* shift_p, int32_t relu_p, void* out, spv_dtype dt) {
+    if (!ws || n < 0 || n >= ((int64_t)1 << 31) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || C <= 0 ||
+        !valid_dt(dt) || !valid_v(voxel_size) || stride_log2 < 0 || stride_log2 > 15)
+        return SPV_ERR_INVALID_ARG;
+    if (mode != SPV_DEVOX_CENTER && mode != SPV_DEVOX_CORNER && mode != SPV_DEVOX_NEAREST) return SPV_ERR_INVALID_ARG;
+    if ((n > 0 && (!xyz || !out || !pt2vox)) || (m_cap > 0 && (!grid_coords || !vfeat || !nbr)))
+        return SPV_ERR_INVALID_ARG;
+    if (pfeat && (Cp <= 0 || !Wp)) return SPV_ERR_INVALID_ARG;
+    if (!aligned16(vfeat) || !aligned16(out) || !aligned16(pfeat) || !aligned16(Wp)) return SPV_ERR_INVALID_ARG;
+    const int cp = pfeat ? Cp : 0;
+    // only the matrix-core kernel reads corners from the neighbour table
+    if (!devox_mfma_supported(C, cp, dt)) return SPV_ERR_UNSUPPORTED;
+    Arena probe(nullptr, 0);
+    probe.take<Header>(1);
+    probe.take<uint64_t>(4);
+    probe.take<int32_t>(4);
+    void* wp_probe = plan_devox_ws(probe, C, cp);
+    (void)wp_probe;
+    if (need(probe.used, ws_bytes)) return SPV_ERR_CAPACITY;
+    Arena ar(ws, ws_bytes);
+    Header* h = ar.take<Header>(1);
+    // an empty 4-slot table: the kernel's probe for a corner outside the point's
+    // 3x3x3 neighbourhood (not reached when pt2vox is the grid's own) finds nothing
+    Table t{ar.take<uint64_t>(4), ar.take<int32_t>(4), 3};
+    void* wpack = plan_devox_ws(ar, C, cp);
+    hipStream_t s = (hipStream_t)stream;
+    launch_clear(s, h, t, true);
+    DevoxArgs a;
+    a.table = t;
+    a.stride_log2 = stride_log2;
+    a.xyz = xyz;
+    a.batch = batch;
+    a.n = n;
+    a.voxel_size = voxel_size;
+    a.mode = mode;
+    a.vfeat = vfeat;
+    a.C = C;
+    a.pfeat = pfeat;
+    a.Cp = cp;
+    a.Wp = Wp;
+    a.scale_p = scale_p;
+    a.shift_p = shift_p;
+    a.relu_p = relu_p;
+    a.out = out;
+    a.dt = dt;
+    a.corner_idx = nullptr;
+    a.corner_w = nullptr;
+    a.h = h;
+    a.pt2vox = pt2vox;
+    a.grid_coords = grid_coords;
+    a.nbr = nbr;
+    a.nbr_rows = m_cap;
+    launch_devox(s, a, wpack, nullptr, nullptr);
+    return hip_check();
+}
+
 spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_params* p, const float* xyz,
                      const int32_t* batch, int64_t n, const void* feat, void* out, int64_t* m_host) {
     if (!ws || !p || n < 0 || n >= ((int64_t)1 << 31) || p->C <= 0 || !valid_dt(p->dtype) ||
@@ -713,6 +773,7 @@ spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_pa
         a.pt2vox = L.pt2vox;
         a.grid_coords = L.coords;
         a.nbr = L.plan.nbr;
+        a.nbr_rows = L.plan.m_cap;
     }
     mark(0);
     // one launch clears the voxel table and packs every weight of the block

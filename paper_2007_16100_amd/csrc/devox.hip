@@ -199,6 +199,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         for (int b = 0; b < PB; ++b) {
             const int64_t k = p0 + b * 16 + r16;
             j[b] = (cn[b].ok && k < a.n) ? a.pt2vox[k] : -1;
+            if (j[b] >= a.nbr_rows) j[b] = -1;
         }
         int own[PB][3];
 #pragma unroll

@@ -349,6 +349,7 @@ struct DevoxArgs {
     const int32_t* pt2vox = nullptr;
     const int32_t* grid_coords = nullptr;
     const int32_t* nbr = nullptr;
+    int64_t nbr_rows = 0;  // rows of nbr / grid_coords: a pt2vox entry outside [0, nbr_rows) has no corners
 };
 bool devox_mfma_supported(int C, int Cp, int dt);
 void* plan_devox_ws(Arena& a, int C, int Cp);

@@ -30,7 +30,7 @@ _DT = {torch.float32: SPV_F32, torch.bfloat16: SPV_BF16, torch.float16: SPV_F16}
 
 # every symbol include/spv.h declares
 EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_voxelize_onto", "spv_packed_weights_bytes",
-           "spv_pack_weights", "spv_sparse_conv_nbr_packed", "spv_sparse_conv_up_packed", "spv_linear_packed",
+           "spv_pack_weights", "spv_devoxelize_nbr", "spv_sparse_conv_nbr_packed", "spv_sparse_conv_up_packed", "spv_linear_packed",
            "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced",
            "spv_linear", "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_map_children", "spv_sparse_conv_up",
            "spv_sparse_conv_dgrad", "spv_wgrad_workspace_bytes", "spv_sparse_conv_wgrad",
@@ -101,13 +101,15 @@ def lib():
         L.spv_devoxelize_backward.argtypes = [vp, vp, vp, vp, i64, i32, vp, i64, i32]
         L.spv_devoxelize.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, vp, i64, f32, i32, vp, i32, vp, i32, vp, vp,
                                      vp, i32, vp, i32, vp, vp]
+        L.spv_devoxelize_nbr.argtypes = [vp, vp, sz, vp, vp, i64, vp, vp, i32, vp, vp, i64, f32, i32, vp, i32, vp,
+                                         i32, vp, vp, vp, i32, vp, i32]
         L.spv_block.argtypes = [vp, vp, sz, ct.POINTER(BlockParams), vp, vp, i64, vp, vp, vp]
         L.spv_lookup.argtypes = [vp, vp, sz, vp, vp, i64, vp, i64, vp]
         L.spv_status_check.argtypes = [vp, vp]
         L.spv_status_string.argtypes = [i32]
         L.spv_status_string.restype = ct.c_char_p
         L.spv_last_hip_error.argtypes = []
-        for f in ("spv_voxelize", "spv_voxelize_onto", "spv_pack_weights", "spv_sparse_conv_nbr_packed",
+        for f in ("spv_voxelize", "spv_voxelize_onto", "spv_pack_weights", "spv_devoxelize_nbr", "spv_sparse_conv_nbr_packed",
                   "spv_sparse_conv_up_packed", "spv_linear_packed", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced", "spv_linear",
                   "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_map_children", "spv_sparse_conv_up",
                   "spv_sparse_conv_dgrad", "spv_sparse_conv_wgrad",
@@ -519,6 +521,28 @@ def spv_devoxelize(ws: Workspace, grid_coords: torch.Tensor, vfeat: torch.Tensor
                               _ptr(ci), _ptr(cw))
     _chk(st, "spv_devoxelize")
     return (out, ci, cw) if want_corners else out
+
+
+def spv_devoxelize_nbr(ws: Workspace, grid_coords: torch.Tensor, vfeat: torch.Tensor, nbr: torch.Tensor,
+                       pt2vox: torch.Tensor, xyz: torch.Tensor, voxel_size: float, stride_log2: int = 0,
+                       mode: int = SPV_DEVOX_CENTER, batch: Optional[torch.Tensor] = None,
+                       m_dev: Optional[torch.Tensor] = None, m_cap: Optional[int] = None,
+                       pfeat: Optional[torch.Tensor] = None, Wp: Optional[torch.Tensor] = None,
+                       scale_p: Optional[torch.Tensor] = None, shift_p: Optional[torch.Tensor] = None,
+                       relu_p: bool = False, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """spv_devoxelize on the points' own voxelization at that stride: corners from the neighbour table."""
+    n = xyz.shape[0]
+    C = vfeat.shape[1]
+    m_cap = grid_coords.shape[0] if m_cap is None else m_cap
+    Cp = pfeat.shape[1] if pfeat is not None else 0
+    if out is None:
+        out = torch.empty((max(n, 1), C), dtype=vfeat.dtype, device=xyz.device)
+    st = lib().spv_devoxelize_nbr(_stream(), ws.ptr, ws.nbytes, _ptr(grid_coords), _ptr(m_dev), m_cap, _ptr(nbr),
+                                  _ptr(pt2vox), stride_log2, _ptr(xyz), _ptr(batch), n, ct.c_float(voxel_size), mode,
+                                  _ptr(vfeat), C, _ptr(pfeat), Cp, _ptr(Wp), _ptr(scale_p), _ptr(shift_p), int(relu_p),
+                                  _ptr(out), _DT[vfeat.dtype])
+    _chk(st, "spv_devoxelize_nbr")
+    return out
 
 
 def make_block_params(C: int, dtype: torch.dtype, voxel_size: float, convs: Sequence, Wp: torch.Tensor,

@@ -23,6 +23,8 @@ holds the device buffers:
 * a conv over a skip concatenation [t; x] runs as two sliced convs,
   W_t t (scaled, unshifted) handed as the residual input of W_x x + shift;
   the 1x1 shortcut over it likewise as two linear layers;
+* the stride-1 fusions read each point's corners from the stride-1 neighbour table (the grid
+  is the points' own voxelization), without a hash table;
 * the weights of the neighbour-table, upsampling and linear layers are packed into
   matrix-core fragments once, on first use, and read packed by every later forward;
 * a devoxelization whose point MLP the fused kernel does not take on matrix
@@ -57,6 +59,7 @@ class Plan:
     nbr: List[torch.Tensor]         # submanifold neighbour table [m_s][27] per stride
     subm: List[Optional[spv.KernelMap]]   # submanifold pairs, built on first use
     children: List[Optional[torch.Tensor]]  # children[s]: child table [m_s][8] of down[s]
+    pt2vox0: torch.Tensor           # every point's stride-1 voxel
 
 
 class SPVCNN:
@@ -113,7 +116,7 @@ class SPVCNN:
             coords.append(km.out_coords[:ms])
         nbr = [spv.spv_kernel_map_nbr(ws, c) for c in coords]
         children = [None] + [spv.spv_map_children(ws, down[s].off, down[s].pairs, m[s - 1], m[s]) for s in range(1, 5)]
-        return Plan(coords, m, down, nbr, [None] * 5, children), vox
+        return Plan(coords, m, down, nbr, [None] * 5, children, vox.pt2vox), vox
 
     # -- layers --------------------------------------------------------------
     def clear_packed(self):
@@ -190,6 +193,10 @@ class SPVCNN:
         C, Cp = vfeat.shape[1], z.shape[1]
         fused = self.dt != torch.float32 and C % 16 == 0 and C // 16 in (1, 2, 4, 6, 8, 16) and Cp % 8 == 0 and \
             Cp <= 128
+        if fused and s == 0:
+            # the grid is the points' own voxelization: corners from the stride's neighbour table
+            return spv.spv_devoxelize_nbr(self.ws, plan.coords[0], vfeat, plan.nbr[0], plan.pt2vox0, xyz, self.v, 0,
+                                          self.mode, batch, pfeat=z, Wp=W, scale_p=sc, shift_p=sh, relu_p=True)
         if fused:
             return spv.spv_devoxelize(self.ws, plan.coords[s], vfeat, xyz, self.v, s, self.mode, batch, pfeat=z, Wp=W,
                                       scale_p=sc, shift_p=sh, relu_p=True)

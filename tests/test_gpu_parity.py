@@ -892,6 +892,55 @@ def test_conv_up_rejects_other_shapes(spv):
 
 
 # ---------------------------------------------------------------------------
+# devoxelization with corners from the neighbour table
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("C,Cp,s,mode", [(96, 96, 0, "center"), (96, 0, 0, "corner"), (256, 32, 0, "center"),
+                                         (64, 64, 2, "center"), (32, 32, 2, "nearest")])
+def test_devoxelize_nbr_matches_hash(spv, sweep, C, Cp, s, mode):
+    """On the points' own voxelization at stride 2^s, corners read from the neighbour table give
+    the hash-table devoxelization's outputs bit for bit; against the oracle as well."""
+    from paper_2007_16100_amd.spvcnn import voxel_size_at
+    dt, v = "bf16", 0.05
+    md = {"center": spv.SPV_DEVOX_CENTER, "corner": spv.SPV_DEVOX_CORNER, "nearest": spv.SPV_DEVOX_NEAREST}[mode]
+    ws = spv.Workspace.for_ops(len(sweep), 256)
+    xyz = dev(sweep)
+    vox = spv.spv_voxelize(ws, xyz, voxel_size_at(v, s))
+    m = vox.m
+    coords = vox.coords[:m]
+    nbr = spv.spv_kernel_map_nbr(ws, coords)
+    vf = synth.normal((m, C), 1501, dtype=dt)
+    kw = {}
+    if Cp:
+        kw = dict(pfeat=dev(synth.normal((len(sweep), Cp), 1502, dtype=dt), dt),
+                  Wp=dev(synth.linear_weight(Cp, C, 1503, dt), dt), relu_p=True)
+        kw["scale_p"], kw["shift_p"] = (dev(a) for a in synth.folded_bn(C, 1504))
+    a = spv.spv_devoxelize(ws, coords, dev(vf, dt), xyz, v, s, md, **kw)
+    b = spv.spv_devoxelize_nbr(ws, coords, dev(vf, dt), nbr, vox.pt2vox, xyz, v, s, md, **kw)
+    torch.cuda.synchronize()
+    assert spv.spv_status_check(ws) == spv.SPV_OK
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    if not Cp:
+        ref = oracle.devoxelize(host(coords), vf, sweep, v, s, mode, dtype=dt)
+        check_close(host(b, dt)[: len(sweep)], ref, dt)
+
+
+def test_devoxelize_nbr_bad_voxel_index(spv):
+    """A pt2vox entry outside the grid gives the point no corners (no read outside the table)."""
+    d = "cuda"
+    xyz = torch.tensor([[0.01, 0.01, 0.01], [0.06, 0.01, 0.01]], dtype=torch.float32, device=d)
+    ws = spv.Workspace.for_ops(16, 32)
+    vox = spv.spv_voxelize(ws, xyz, 0.05)
+    coords = vox.coords[: vox.m]
+    nbr = spv.spv_kernel_map_nbr(ws, coords)
+    vf = torch.ones((vox.m, 32), dtype=torch.bfloat16, device=d)
+    p2v = vox.pt2vox.clone()
+    p2v[0] = 1000
+    out = spv.spv_devoxelize_nbr(ws, coords, vf, nbr, p2v, xyz, 0.05)
+    torch.cuda.synchronize()
+    assert float(out[0].float().abs().max()) == 0.0 and float(out[1, 0]) == 1.0
+
+
+# ---------------------------------------------------------------------------
 # pre-packed weights
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("cin,cout,coff", [(96, 96, 0), (256, 256, 0), (32, 64, 32), (128, 96, 64), (64, 256, 0)])
