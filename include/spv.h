@@ -380,10 +380,12 @@ spv_status spv_sparse_conv_dgrad(void* stream, void* ws, size_t ws_bytes,
  *      the forward call; pairs past pair_cap or with rows outside x / dy are
  *      ignored.
  * Out: dW [K3][Cin][Cout] float32.
- * bf16/f16 with Cin % 16 == 0 and Cout % 16 == 0 run on MFMA; other shapes and
- * f32 on a vector-ALU kernel.  Cin * Cout <= 65536.  The workspace holds the
- * slices' partial sums: spv_wgrad_workspace_bytes(K3, Cin, Cout) bytes
- * (K3 * S * Cin * Cout * 4 with S = 32, 16 or 8 as Cin * Cout grows).
+ * bf16/f16 with Cin % 16 == 0, Cout % 16 == 0 and Cin + Cout <= 512 run on
+ * MFMA; other shapes and f32 on a vector-ALU kernel.  Cin * Cout <= 65536.
+ * The workspace holds the slices' partial sums:
+ * spv_wgrad_workspace_bytes(K3, Cin, Cout) bytes (K3 * S * Cin * Cout * 4,
+ * with S slices per offset: the largest power of two in [8, 64] for which
+ * 27 * S * Cin * Cout * 4 <= 64 MiB, or 8).
  * Errors: SPV_ERR_INVALID_ARG, SPV_ERR_UNSUPPORTED (K3, Cin * Cout),
  *      SPV_ERR_CAPACITY (ws too small).
  */
@@ -521,6 +523,34 @@ spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_pa
 spv_status spv_lookup(void* stream, void* ws, size_t ws_bytes,
                       const int32_t* table_coords, const int64_t* m_dev, int64_t m_cap,
                       const int32_t* qcoords, int64_t q, int32_t* idx);
+
+/*
+ * spv_voxel_lookup -- queries the hash table the last spv_voxelize call on ws
+ * built (Sec. 3.3: one O(1) lookup per coordinate), without rebuilding it.
+ * In:  ws / ws_bytes / n: the workspace and point count of that spv_voxelize
+ *      call (the table's place in the workspace follows from n); qcoords
+ *      [q][4] int32 (b, x, y, z), any values.
+ * Out: idx [q] int32: the voxel's canonical index (its row in spv_voxelize's
+ *      coords), -1 if the voxel is not in the table.
+ * Errors: SPV_ERR_INVALID_ARG (null or misaligned ws, negative sizes),
+ *      SPV_ERR_CAPACITY (ws_bytes below what n needs).  Reads ws only.
+ */
+spv_status spv_voxel_lookup(void* stream, const void* ws, size_t ws_bytes, int64_t n,
+                            const int32_t* qcoords, int64_t q, int32_t* idx);
+
+/*
+ * spv_conv_kernel -- the kernel spv_sparse_conv (and its sliced / dgrad forms)
+ * runs on for a shape and its sizes, as the call decides it on the host:
+ * 0 = the neighbour-table MFMA kernel (3x3x3 maps), 1 = the tile MFMA kernel,
+ * 2 = the vector-ALU kernel; -1 for arguments the calls reject.  The
+ * neighbour-table kernel addresses the input rows and its table with 32-bit
+ * offsets: in_rows * Cin * 2 and m_out_cap * 27 * 4 must stay below
+ * 0xFFFFE000, else a larger shape falls back to the next kernel.  Host only.
+ * spv_block_conv_kernel gives the same for the convs of spv_block(n, C, dt).
+ */
+int32_t spv_conv_kernel(int32_t K3, int32_t Cin, int32_t Cout, spv_dtype dt, int64_t in_rows, int64_t m_out_cap,
+                        int64_t pair_cap, int32_t transposed);
+int32_t spv_block_conv_kernel(int64_t n, int32_t C, spv_dtype dt);
 
 /* Synchronizes the stream and returns the first device-detected error recorded
  * in the workspace status word (NONFINITE before RANGE before CAPACITY). */

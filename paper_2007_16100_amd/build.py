@@ -18,7 +18,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libspv.so")
 BUILD_DIR = os.path.join(HERE, "_build")
-SOURCES = ["hash_sort_scan.hip", "voxelize.hip", "kmap.hip", "conv.hip", "conv_union.hip", "conv_up.hip", "devox.hip",
+SOURCES = ["hash_sort_scan.hip", "radix.hip", "voxelize.hip", "kmap.hip", "conv.hip", "conv_union.hip", "conv_up.hip", "devox.hip",
            "linear.hip", "backward.hip", "api.hip"]
 ARCH = os.environ.get("SPV_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

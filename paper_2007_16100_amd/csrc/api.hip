@@ -27,6 +27,7 @@ spv_status flags_to_status(uint32_t f) {
     if (f & kFlagRange) return SPV_ERR_RANGE;
     if (f & (kFlagCapacity | kFlagTableFull)) return SPV_ERR_CAPACITY;
     if (f & (kFlagDuplicate | kFlagUnsorted)) return SPV_ERR_INVALID_ARG;
+    if (f & kFlagInternal) return SPV_ERR_HIP;
     return SPV_OK;
 }
 
@@ -41,6 +42,8 @@ spv_status sync_status(hipStream_t s, const Header* h, Header* out) {
 }
 
 bool valid_dt(int dt) { return dt == SPV_F32 || dt == SPV_BF16 || dt == SPV_F16; }
+// a workspace pointer every layout can carve from (its offsets are 256-byte multiples)
+bool ws_ok(const void* ws) { return ws && ((uintptr_t)ws & 255u) == 0; }
 size_t esize(int dt) { return dt == SPV_F32 ? 4 : 2; }
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 constexpr int kUpChildren = 8;  // offsets of a k=2 s=2 map
@@ -83,10 +86,11 @@ struct ConvLayout {
     ConvPlan p;
     void* wpack;
 };
-size_t layout_conv(void* ws, size_t bytes, int64_t m_out_cap, int K3, int Cin, int Cout, int dt, ConvLayout& L) {
+size_t layout_conv(void* ws, size_t bytes, int64_t m_out_cap, int K3, int Cin, int Cout, int dt, ConvLayout& L,
+                   int64_t in_rows, bool sparse_transposed = false) {
     Arena a(ws, bytes);
     L.h = a.take<Header>(1);
-    plan_conv_ws(a, L.p, m_out_cap, K3, Cin, Cout, dt);
+    plan_conv_ws(a, L.p, m_out_cap, K3, Cin, Cout, dt, in_rows, sparse_transposed);
     L.p.h = L.h;
     L.wpack = plan_wpack_ws(a, K3, Cin, Cout > 16 ? Cout : 16);
     return a.used;
@@ -151,7 +155,7 @@ size_t layout_block(void* ws, size_t bytes, int64_t n, int C, int dt, BlockLayou
     L.map.h = L.h;
     L.map.fine = L.vox.table;  // the voxelization's table serves the kernel map and the devoxelization
     plan_kmap_ws(a, L.map, nn, 3, 1, false, false);
-    plan_conv_ws(a, L.plan, nn, 27, C, C, dt);
+    plan_conv_ws(a, L.plan, nn, 27, C, C, dt, nn);
     L.plan.h = L.h;
     L.map.nbr = L.plan.nbr;  // the map's neighbour table is the 3x3x3 conv's plan
     L.coords = a.take<int32_t>(4 * nn);
@@ -189,7 +193,7 @@ size_t spv_workspace_bytes(int64_t max_points, int32_t max_C) {
     s = std::max(s, layout_kmap(nullptr, 0, max_points, 3, 1, m));
     s = std::max(s, layout_kmap(nullptr, 0, max_points, 2, 2, m));
     s = std::max(s, layout_kmap(nullptr, 0, max_points, 3, 2, m));
-    s = std::max(s, layout_conv(nullptr, 0, max_points, 27, max_C, max_C, SPV_BF16, c));
+    s = std::max(s, layout_conv(nullptr, 0, max_points, 27, max_C, max_C, SPV_BF16, c, max_points));
     void* wl = nullptr;
     s = std::max(s, layout_linear(nullptr, 0, max_C, max_C, &wl));
 
@@ -226,17 +230,32 @@ const char* spv_status_string(spv_status s) {
 int spv_last_hip_error(void) { return g_last_hip_error; }
 
 spv_status spv_status_check(const void* ws, void* stream) {
-    if (!ws) return SPV_ERR_INVALID_ARG;
+    if (!ws_ok(ws)) return SPV_ERR_INVALID_ARG;
     return sync_status((hipStream_t)stream, (const Header*)ws, nullptr);
+}
+
+int32_t spv_conv_kernel(int32_t K3, int32_t Cin, int32_t Cout, spv_dtype dt, int64_t in_rows, int64_t m_out_cap,
+                        int64_t pair_cap, int32_t transposed) {
+    if (!(K3 == 27 || K3 == 8) || Cin <= 0 || Cout <= 0 || !valid_dt(dt) || in_rows < 0 || m_out_cap < 0 ||
+        pair_cap < 0)
+        return -1;
+    return conv_kernel_choice(K3, Cin, Cout, dt, m_out_cap > 0 ? m_out_cap : 1, in_rows, pair_cap,
+                              transposed && in_rows != m_out_cap);
+}
+
+int32_t spv_block_conv_kernel(int64_t n, int32_t C, spv_dtype dt) {
+    if (n < 0 || C <= 0 || !valid_dt(dt)) return -1;
+    // the block's plan makes this choice (its pair list holds 27 n pairs)
+    const int64_t nn = n > 0 ? n : 1;
+    return conv_kernel_choice(27, C, C, dt, nn, nn, 27 * nn, false);
 }
 
 spv_status spv_voxelize(void* stream, void* ws, size_t ws_bytes, const float* xyz, const int32_t* batch, int64_t n,
                         float voxel_size, const void* feat, int32_t C, spv_dtype dt, int32_t* coords, void* vfeat,
                         int32_t* counts, int32_t* pt2vox, int64_t* m_dev, int64_t* m_host) {
-    if (!ws || n < 0 || n >= ((int64_t)1 << 31) || !valid_v(voxel_size)) return SPV_ERR_INVALID_ARG;
+    if (!ws_ok(ws) || n < 0 || n >= ((int64_t)1 << 31) || !valid_v(voxel_size)) return SPV_ERR_INVALID_ARG;
     if (n > 0 && (!xyz || !coords || !counts || !pt2vox)) return SPV_ERR_INVALID_ARG;
     if (feat && (C <= 0 || !vfeat || !valid_dt(dt))) return SPV_ERR_INVALID_ARG;
-    if (((uintptr_t)ws & 255u) != 0) return SPV_ERR_INVALID_ARG;
     VoxLayout L;
     if (need(layout_voxelize(nullptr, 0, n, L), ws_bytes)) return SPV_ERR_CAPACITY;
     layout_voxelize(ws, ws_bytes, n, L);
@@ -255,13 +274,12 @@ spv_status spv_voxelize_onto(void* stream, void* ws, size_t ws_bytes, const int3
                              int64_t m_cap, const float* xyz, const int32_t* batch, int64_t n, float voxel_size,
                              const void* feat, int32_t C, spv_dtype dt, void* vfeat, int32_t* counts,
                              int32_t* pt2vox) {
-    if (!ws || n < 0 || n >= ((int64_t)1 << 31) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || !valid_v(voxel_size))
+    if (!ws_ok(ws) || n < 0 || n >= ((int64_t)1 << 31) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || !valid_v(voxel_size))
         return SPV_ERR_INVALID_ARG;
     if (n > 0 && (!xyz || !pt2vox)) return SPV_ERR_INVALID_ARG;
     if (m_cap > 0 && (!coords || !counts)) return SPV_ERR_INVALID_ARG;
     if (feat && (C <= 0 || !valid_dt(dt))) return SPV_ERR_INVALID_ARG;
     if (feat && m_cap > 0 && !vfeat) return SPV_ERR_INVALID_ARG;
-    if (((uintptr_t)ws & 255u) != 0) return SPV_ERR_INVALID_ARG;
     VoxLayout L;
     const int64_t cap = n > m_cap ? n : m_cap;
     if (need(layout_voxelize(nullptr, 0, cap, L), ws_bytes)) return SPV_ERR_CAPACITY;
@@ -274,7 +292,7 @@ spv_status spv_voxelize_onto(void* stream, void* ws, size_t ws_bytes, const int3
 
 spv_status spv_lookup(void* stream, void* ws, size_t ws_bytes, const int32_t* table_coords, const int64_t* m_dev,
                       int64_t m_cap, const int32_t* qcoords, int64_t q, int32_t* idx) {
-    if (!ws || m_cap < 0 || q < 0 || (m_cap > 0 && !table_coords) || (q > 0 && (!qcoords || !idx)))
+    if (!ws_ok(ws) || m_cap < 0 || q < 0 || (m_cap > 0 && !table_coords) || (q > 0 && (!qcoords || !idx)))
         return SPV_ERR_INVALID_ARG;
     Arena probe(nullptr, 0);
     probe.take<Header>(1);
@@ -292,10 +310,21 @@ spv_status spv_lookup(void* stream, void* ws, size_t ws_bytes, const int32_t* ta
     return hip_check();
 }
 
+spv_status spv_voxel_lookup(void* stream, const void* ws, size_t ws_bytes, int64_t n, const int32_t* qcoords,
+                            int64_t q, int32_t* idx) {
+    if (!ws_ok(ws) || n < 0 || n >= ((int64_t)1 << 31) || q < 0 || (q > 0 && (!qcoords || !idx)))
+        return SPV_ERR_INVALID_ARG;
+    VoxLayout L;
+    if (need(layout_voxelize(nullptr, 0, n, L), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_voxelize(const_cast<void*>(ws), ws_bytes, n, L);
+    launch_table_lookup((hipStream_t)stream, L.w.table, qcoords, q, idx);
+    return hip_check();
+}
+
 spv_status spv_kernel_map(void* stream, void* ws, size_t ws_bytes, const int32_t* in_coords, const int64_t* m_in_dev,
                           int64_t m_cap, int32_t K, int32_t stride, int32_t* out_coords, int64_t* m_out_dev,
                           int32_t* off, int32_t* pairs, int64_t pair_cap, int64_t* total_host) {
-    if (!ws || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || !off || pair_cap < 0) return SPV_ERR_INVALID_ARG;
+    if (!ws_ok(ws) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || !off || pair_cap < 0) return SPV_ERR_INVALID_ARG;
     if (m_cap > 0 && !in_coords) return SPV_ERR_INVALID_ARG;
     if (!((K == 3 && (stride == 1 || stride == 2)) || (K == 2 && stride == 2))) return SPV_ERR_UNSUPPORTED;
     if (stride == 2 && !out_coords) return SPV_ERR_INVALID_ARG;
@@ -329,16 +358,23 @@ static spv_status sparse_conv_call(void* stream, void* ws, size_t ws_bytes, cons
                                    int32_t transposed, const void* W, WStrides wst, const float* scale,
                                    const float* shift, const void* res, int32_t relu, void* out,
                                    const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
-    if (!ws || in_rows < 0 || m_out_cap < 0 || m_out_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !off ||
+    if (!ws_ok(ws) || in_rows < 0 || m_out_cap < 0 || m_out_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !off ||
         !W || pair_cap < 0 || !valid_dt(dt))
         return SPV_ERR_INVALID_ARG;
     if (!(K3 == 27 || K3 == 8)) return SPV_ERR_UNSUPPORTED;
     if ((in_rows > 0 && !in) || (m_out_cap > 0 && !out) || (pair_cap > 0 && !pairs)) return SPV_ERR_INVALID_ARG;
     if (!aligned16(in) || !aligned16(out) || !aligned16(W) || !aligned16(res) || (res && res == out))
         return SPV_ERR_INVALID_ARG;
+    // A transposed stride-2 map gives an output few of the 27 offsets (at most
+    // 8, 2-3 on a sweep), which the neighbour-table kernel would still step
+    // through for every block: the tile kernel, which only visits pairs, takes
+    // it.  A transposed map with as many inputs as outputs (a submanifold map
+    // read backwards, as in the input gradient) is as dense as the forward one.
+    const bool sparse_tr = transposed && in_rows != m_out_cap;
     ConvLayout L;
-    if (need(layout_conv(nullptr, 0, m_out_cap, K3, Cin, Cout, dt, L), ws_bytes)) return SPV_ERR_CAPACITY;
-    layout_conv(ws, ws_bytes, m_out_cap, K3, Cin, Cout, dt, L);
+    if (need(layout_conv(nullptr, 0, m_out_cap, K3, Cin, Cout, dt, L, in_rows, sparse_tr), ws_bytes))
+        return SPV_ERR_CAPACITY;
+    layout_conv(ws, ws_bytes, m_out_cap, K3, Cin, Cout, dt, L, in_rows, sparse_tr);
     hipStream_t s = (hipStream_t)stream;
     if (m_out_cap == 0) return clear_status_only(s, ws);
     L.p.m_out_dev = m_out_dev;
@@ -346,12 +382,6 @@ static spv_status sparse_conv_call(void* stream, void* ws, size_t ws_bytes, cons
     L.p.w_ldc = wst.ldc;
     L.p.w_ldcol = wst.ldcol;
     L.p.w_ldk = wst.ldk;
-    // A transposed stride-2 map gives an output few of the 27 offsets (at most
-    // 8, 2-3 on a sweep), which the neighbour-table kernel would still step
-    // through for every block: the tile kernel, which only visits pairs, takes
-    // it.  A transposed map with as many inputs as outputs (a submanifold map
-    // read backwards, as in the input gradient) is as dense as the forward one.
-    if (transposed && in_rows != m_out_cap) L.p.use_union = 0;
     // the plan clears the status header first and packs W in one of its launches
     launch_conv_plan(s, L.p, off, pairs, K3, transposed, pair_cap, in_rows,
                      conv_pack_job(K3, W, L.wpack, Cin, Cout, dt, wst.ldc, wst.ldk, wst.ldcol), true);
@@ -382,7 +412,7 @@ spv_status spv_sparse_conv_sliced(void* stream, void* ws, size_t ws_bytes, const
 
 spv_status spv_kernel_map_nbr(void* stream, void* ws, size_t ws_bytes, const int32_t* in_coords,
                               const int64_t* m_in_dev, int64_t m_cap, int32_t* nbr) {
-    if (!ws || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || (m_cap > 0 && (!in_coords || !nbr)))
+    if (!ws_ok(ws) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || (m_cap > 0 && (!in_coords || !nbr)))
         return SPV_ERR_INVALID_ARG;
     if (m_cap * 27 * 4 > (int64_t)0xFFFFE000) return SPV_ERR_UNSUPPORTED;
     MapLayout L;
@@ -402,7 +432,7 @@ static spv_status conv_nbr_call(void* stream, void* ws, size_t ws_bytes, const v
                                 const void* packed, const float* scale, const float* shift, const void* res,
                                 int32_t relu, void* out, const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout,
                                 spv_dtype dt) {
-    if (!ws || in_rows < 0 || m_out_cap < 0 || m_out_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !W ||
+    if (!ws_ok(ws) || in_rows < 0 || m_out_cap < 0 || m_out_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !W ||
         !valid_dt(dt) || Cin > Cin_full || Cout > Cout_full)
         return SPV_ERR_INVALID_ARG;
     if (!union_supported(27, Cin, Cout, dt) || m_out_cap * 27 * 4 > (int64_t)0xFFFFE000 ||
@@ -412,8 +442,8 @@ static spv_status conv_nbr_call(void* stream, void* ws, size_t ws_bytes, const v
     if (!aligned16(in) || !aligned16(out) || !aligned16(W) || !aligned16(res) || (res && res == out))
         return SPV_ERR_INVALID_ARG;
     ConvLayout L;
-    if (need(layout_conv(nullptr, 0, m_out_cap, 27, Cin, Cout, dt, L), ws_bytes)) return SPV_ERR_CAPACITY;
-    layout_conv(ws, ws_bytes, m_out_cap, 27, Cin, Cout, dt, L);
+    if (need(layout_conv(nullptr, 0, m_out_cap, 27, Cin, Cout, dt, L, in_rows), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_conv(ws, ws_bytes, m_out_cap, 27, Cin, Cout, dt, L, in_rows);
     if (m_out_cap == 0) return SPV_OK;
     hipStream_t s = (hipStream_t)stream;
     ConvPlan p = L.p;
@@ -447,7 +477,7 @@ spv_status spv_sparse_conv_nbr_packed(void* stream, void* ws, size_t ws_bytes, c
 spv_status spv_map_children(void* stream, void* ws, size_t ws_bytes, const int32_t* off, const int32_t* pairs,
                             int64_t pair_cap, int64_t fine_rows, const int64_t* m_coarse_dev, int64_t m_coarse_cap,
                             int32_t* children) {
-    if (!ws || !off || pair_cap < 0 || fine_rows < 0 || m_coarse_cap < 0 || m_coarse_cap >= ((int64_t)1 << 31))
+    if (!ws_ok(ws) || !off || pair_cap < 0 || fine_rows < 0 || m_coarse_cap < 0 || m_coarse_cap >= ((int64_t)1 << 31))
         return SPV_ERR_INVALID_ARG;
     if ((pair_cap > 0 && !pairs) || (m_coarse_cap > 0 && !children) || !aligned16(children)) return SPV_ERR_INVALID_ARG;
     if (need(sizeof(Header), ws_bytes)) return SPV_ERR_CAPACITY;
@@ -462,7 +492,7 @@ static spv_status conv_up_call(void* stream, void* ws, size_t ws_bytes, const vo
                                int32_t Cout_full, const void* packed, const float* scale, const float* shift,
                                const void* res, int32_t relu, void* out, int64_t out_rows, int32_t Cout,
                                spv_dtype dt) {
-    if (!ws || m_in_cap < 0 || m_in_cap >= ((int64_t)1 << 31) || out_rows < 0 || Cin <= 0 || Cout <= 0 || !W ||
+    if (!ws_ok(ws) || m_in_cap < 0 || m_in_cap >= ((int64_t)1 << 31) || out_rows < 0 || Cin <= 0 || Cout <= 0 || !W ||
         !valid_dt(dt) || Cin > Cin_full || Cout > Cout_full)
         return SPV_ERR_INVALID_ARG;
     if (!up_supported(Cin, Cout, dt)) return SPV_ERR_UNSUPPORTED;
@@ -519,7 +549,7 @@ spv_status spv_sparse_conv_dgrad(void* stream, void* ws, size_t ws_bytes, const 
 spv_status spv_sparse_conv_wgrad(void* stream, void* ws, size_t ws_bytes, const void* x, int64_t x_rows, int32_t Cin,
                                  const void* dy, int64_t dy_rows, int32_t Cout, const int32_t* off, const int32_t* pairs,
                                  int64_t pair_cap, int32_t K3, int32_t transposed, float* dW, spv_dtype dt) {
-    if (!ws || x_rows < 0 || dy_rows < 0 || Cin <= 0 || Cout <= 0 || !off || !dW || pair_cap < 0 || !valid_dt(dt))
+    if (!ws_ok(ws) || x_rows < 0 || dy_rows < 0 || Cin <= 0 || Cout <= 0 || !off || !dW || pair_cap < 0 || !valid_dt(dt))
         return SPV_ERR_INVALID_ARG;
     if (!(K3 == 27 || K3 == 8) || !wgrad_supported(Cin, Cout)) return SPV_ERR_UNSUPPORTED;
     if ((x_rows > 0 && !x) || (dy_rows > 0 && !dy) || (pair_cap > 0 && !pairs)) return SPV_ERR_INVALID_ARG;
@@ -556,7 +586,7 @@ static spv_status linear_call(void* stream, void* ws, size_t ws_bytes, const voi
                               int64_t m_cap, int32_t Cin, const void* W, int32_t Cin_full, int32_t Cout_full,
                               const void* packed, const float* scale, const float* shift, int32_t relu,
                               const void* res, int32_t res_after_act, void* out, int32_t Cout, spv_dtype dt) {
-    if (!ws || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !W || !valid_dt(dt) ||
+    if (!ws_ok(ws) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !W || !valid_dt(dt) ||
         Cin > Cin_full || Cout > Cout_full)
         return SPV_ERR_INVALID_ARG;
     if (m_cap > 0 && (!in || !out)) return SPV_ERR_INVALID_ARG;
@@ -625,7 +655,7 @@ spv_status spv_devoxelize(void* stream, void* ws, size_t ws_bytes, const int32_t
                           float voxel_size, spv_devox_mode mode, const void* vfeat, int32_t C, const void* pfeat,
                           int32_t Cp, const void* Wp, const float* scale_p, const float* shift_p, int32_t relu_p,
                           void* out, spv_dtype dt, int32_t* corner_idx, float* corner_w) {
-    if (!ws || n < 0 || n >= ((int64_t)1 << 31) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || C <= 0 ||
+    if (!ws_ok(ws) || n < 0 || n >= ((int64_t)1 << 31) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || C <= 0 ||
         !valid_dt(dt) || !valid_v(voxel_size) || stride_log2 < 0 || stride_log2 > 15)
         return SPV_ERR_INVALID_ARG;
     if (mode != SPV_DEVOX_CENTER && mode != SPV_DEVOX_CORNER && mode != SPV_DEVOX_NEAREST) return SPV_ERR_INVALID_ARG;
@@ -670,7 +700,7 @@ spv_status spv_devoxelize_nbr(void* stream, void* ws, size_t ws_bytes, const int
                               const float* xyz, const int32_t* batch, int64_t n, float voxel_size, spv_devox_mode mode,
                               const void* vfeat, int32_t C, const void* pfeat, int32_t Cp, const void* Wp,
                               const float* scale_p, const float* shift_p, int32_t relu_p, void* out, spv_dtype dt) {
-    if (!ws || n < 0 || n >= ((int64_t)1 << 31) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || C <= 0 ||
+    if (!ws_ok(ws) || n < 0 || n >= ((int64_t)1 << 31) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || C <= 0 ||
         !valid_dt(dt) || !valid_v(voxel_size) || stride_log2 < 0 || stride_log2 > 15)
         return SPV_ERR_INVALID_ARG;
     if (mode != SPV_DEVOX_CENTER && mode != SPV_DEVOX_CORNER && mode != SPV_DEVOX_NEAREST) return SPV_ERR_INVALID_ARG;
@@ -721,13 +751,14 @@ spv_status spv_devoxelize_nbr(void* stream, void* ws, size_t ws_bytes, const int
     a.grid_coords = grid_coords;
     a.nbr = nbr;
     a.nbr_rows = m_cap;
+    a.nbr_m_dev = m_dev;
     launch_devox(s, a, wpack, nullptr, nullptr);
     return hip_check();
 }
 
 spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_params* p, const float* xyz,
                      const int32_t* batch, int64_t n, const void* feat, void* out, int64_t* m_host) {
-    if (!ws || !p || n < 0 || n >= ((int64_t)1 << 31) || p->C <= 0 || !valid_dt(p->dtype) ||
+    if (!ws_ok(ws) || !p || n < 0 || n >= ((int64_t)1 << 31) || p->C <= 0 || !valid_dt(p->dtype) ||
         !valid_v(p->voxel_size))
         return SPV_ERR_INVALID_ARG;
     if (p->n_convs < 1 || p->n_convs > 2 || !p->Wp) return SPV_ERR_INVALID_ARG;
@@ -774,17 +805,17 @@ spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_pa
         a.grid_coords = L.coords;
         a.nbr = L.plan.nbr;
         a.nbr_rows = L.plan.m_cap;
+        a.nbr_m_dev = L.m_dev;
     }
     mark(0);
-    // one launch clears the voxel table and packs every weight of the block
+    // voxel branch: Eq. 1-2 into the hashed grid; its first launch also clears
+    // the voxel table and packs every weight of the block
     PackJob jobs[kMaxPackJobs];
     int njobs = 0;
     for (int l = 0; l < p->n_convs; ++l) jobs[njobs++] = conv_pack_job(27, p->W[l], L.wpack_conv[l], C, C, dt);
     jobs[njobs++] = devox_pack_job(a, L.wpack_mlp);
-    launch_block_prologue(s, L.h, L.vox.table, jobs, njobs);
-    // voxel branch: Eq. 1-2 into the hashed grid
     launch_voxelize(s, L.vox, xyz, batch, n, p->voxel_size, feat, C, dt, L.coords, L.va, L.counts, L.pt2vox, L.m_dev,
-                    true);
+                    jobs, njobs);
     mark(1);
     // one kernel map for both convs, probing the voxelization's table; the
     // neighbour-table conv needs only the table, the other kernels the pairs

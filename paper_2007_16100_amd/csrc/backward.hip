@@ -24,6 +24,7 @@ namespace spv {
 constexpr int kWgWaves = 8;
 constexpr int kWgChunk = 64;  // pairs per LDS fill: two MFMA K-steps of 32
 constexpr int kWgLd = kWgChunk + 8;  // LDS row length in 16-bit elements (padded)
+constexpr int kWgMaxRowPair = 512;    // Cin + Cout the MFMA kernel takes (8 pieces per thread)
 
 // slices per offset: as many as a 64 MB partial-sum buffer holds (the centre
 // offset of a submanifold map has ~15% of the pairs: more slices spread it
@@ -200,7 +201,7 @@ static void launch_wgrad_mfma(hipStream_t s, dim3 grid, const WgradArgs& a, floa
     if (ppt <= 1) launch_wgrad_mfma3<DT, TPW, 1>(s, grid, a, partial);
     else if (ppt <= 2) launch_wgrad_mfma3<DT, TPW, 2>(s, grid, a, partial);
     else if (ppt <= 4) launch_wgrad_mfma3<DT, TPW, 4>(s, grid, a, partial);
-    else launch_wgrad_mfma3<DT, TPW, 8>(s, grid, a, partial);
+    else launch_wgrad_mfma3<DT, TPW, 8>(s, grid, a, partial);  // Cin + Cout <= kWgMaxRowPair
 }
 
 template <int DT>
@@ -218,7 +219,10 @@ static void launch_wgrad_tpw(hipStream_t s, dim3 grid, const WgradArgs& a, float
 void launch_wgrad(hipStream_t s, const WgradArgs& a, float* partial, float* dW) {
     const int S = wgrad_slices(a.Cin, a.Cout);
     const dim3 grid((unsigned)S, (unsigned)a.K3);
-    const bool mfma = a.dt != SPV_F32 && a.Cin % 16 == 0 && a.Cout % 16 == 0;
+    // the MFMA kernel gathers at most 8 pieces of 16 bytes per thread, i.e. 64
+    // pieces (512 channels) of a pair's two rows, and holds both rows of 64
+    // pairs in LDS: wider pairs run on the vector-ALU kernel
+    const bool mfma = a.dt != SPV_F32 && a.Cin % 16 == 0 && a.Cout % 16 == 0 && a.Cin + a.Cout <= kWgMaxRowPair;
     if (mfma) {
         if (a.dt == SPV_BF16) launch_wgrad_tpw<SPV_BF16>(s, grid, a, partial);
         else launch_wgrad_tpw<SPV_F16>(s, grid, a, partial);

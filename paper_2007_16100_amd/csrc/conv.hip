@@ -35,10 +35,13 @@ static int conv_tile_rows(int Cin, int Cout, int dt);
 // The boundary array is sized for the smallest tile (16 rows) and the neighbour
 // table is reserved for every 3x3x3 plan, so the workspace size does not depend
 // on the channel counts or the dtype.
-void plan_conv_ws(Arena& a, ConvPlan& p, int64_t m_out_cap, int K3, int Cin, int Cout, int dt) {
+void plan_conv_ws(Arena& a, ConvPlan& p, int64_t m_out_cap, int K3, int Cin, int Cout, int dt, int64_t in_rows,
+                  bool sparse_transposed) {
     p.m_cap = m_out_cap > 0 ? m_out_cap : 1;
     p.K3 = K3;
-    p.use_union = union_supported(K3, Cin, Cout, dt) && p.m_cap * K3 * 4 <= (int64_t)0xFFFFE000 ? 1 : 0;
+    // decided once here: launch_conv_plan builds what this kernel reads
+    // (neighbour table or tile bounds) and launch_conv_run runs it
+    p.use_union = conv_kernel_choice(K3, Cin, Cout, dt, p.m_cap, in_rows, 0, sparse_transposed) == kConvUnion ? 1 : 0;
     p.tile_rows = conv_tile_rows(Cin, Cout, dt);
     p.ntile_cap = (p.m_cap + p.tile_rows - 1) / p.tile_rows;
     p.bnd = a.take<int32_t>((size_t)K3 * ((p.m_cap + kChunk - 1) / kChunk + 1));
@@ -61,39 +64,6 @@ __device__ inline int64_t tile_of(int64_t j, int64_t m, int64_t nt, int T) {
     if (j < 0) return 0;
     if (j >= m) return nt;
     return j / T;
-}
-
-// fragment t of the packing (t = ((k * KCH + kc) * NB + nb) * 64 + lane)
-// W[k][c][col] sits at W[k * ldk + c * ldc + col * ldcol] (ldc = Cout, ldcol = 1,
-// ldk = Cin * Cout for a dense [K3][Cin][Cout] tensor; larger ldc / ldk for a
-// channel slice of a wider one; ldc = 1, ldcol = the stored row length to read
-// every W[k] transposed)
-__device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int Cout, int ldc, int ldcol, int64_t ldk, int KCH,
-                                     int NB, int64_t t) {
-    const int lane = (int)(t & 63);
-    int64_t f = t >> 6;
-    const int nb = (int)(f % NB);
-    f /= NB;
-    const int kc = (int)(f % KCH);
-    const int k = (int)(f / KCH);
-    const int col = nb * 16 + (lane & 15);
-    const int ci0 = kc * 32 + 8 * (lane >> 4);
-    uint32_t w[4];
-    for (int e = 0; e < 4; ++e) {
-        uint32_t lo = 0, hi = 0;
-        const int c0 = ci0 + 2 * e, c1 = ci0 + 2 * e + 1;
-        // zeros past the last input channel and past the last output column
-        if (c0 < Cin && col < Cout) lo = W[(int64_t)k * ldk + (int64_t)c0 * ldc + (int64_t)col * ldcol];
-        if (c1 < Cin && col < Cout) hi = W[(int64_t)k * ldk + (int64_t)c1 * ldc + (int64_t)col * ldcol];
-        w[e] = lo | (hi << 16);
-    }
-    return make_uint4(w[0], w[1], w[2], w[3]);
-}
-
-// a weight packing run alongside another kernel's work (grid-stride)
-__device__ inline void pack_job_run(const PackJob& q) {
-    for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < q.total; t += (int64_t)gridDim.x * blockDim.x)
-        q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.ldc, q.ldcol, q.ldk, q.KCH, q.NB, t);
 }
 
 // For every offset k and tile t in [0, nt]: bnd[k][t] = first pair of offset k
@@ -226,32 +196,6 @@ void launch_pack_job(hipStream_t s, const PackJob& q) {
     if (g > 1024) g = 1024;
     k_pack_job<<<(unsigned)g, 256, 0, s>>>(q);
 }
-
-struct PrologueArgs {
-    Header* h;
-    uint64_t* keys;
-    uint32_t nslots;
-    int njobs;
-    PackJob job[kMaxPackJobs];
-};
-
-// table + header clear and weight packing of a block call, grid-stride
-__global__ __launch_bounds__(256) void k_block_prologue(PrologueArgs a) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        a.h->status = 0;
-        a.h->m = 0;
-        for (int i = 0; i < 4; ++i) a.h->aux[i] = 0;
-    }
-    const int64_t t0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = t0; i < (int64_t)a.nslots; i += stride) a.keys[i] = kEmpty;
-    for (int j = 0; j < a.njobs; ++j) {
-        const PackJob& q = a.job[j];
-        for (int64_t t = t0; t < q.total; t += stride)
-            q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.ldc, q.ldcol, q.ldk, q.KCH, q.NB, t);
-    }
-}
-
 
 static int conv_kch(int Cin);
 
@@ -697,34 +641,29 @@ PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int
     return q;
 }
 
-void launch_block_prologue(hipStream_t s, Header* h, Table t, const PackJob* jobs, int njobs) {
-    PrologueArgs a;
-    a.h = h;
-    a.keys = t.keys;
-    a.nslots = t.mask + 1;
-    a.njobs = 0;
-    int64_t work = a.nslots;
-    for (int j = 0; j < njobs && a.njobs < kMaxPackJobs; ++j)
-        if (jobs[j].total > 0) {
-            a.job[a.njobs++] = jobs[j];
-            work += jobs[j].total;
-        }
-    k_block_prologue<<<blocks_for(work, 256 * 2), 256, 0, s>>>(a);
-}
-
-// the MFMA kernel addresses the input rows and the pair list with 32-bit buffer offsets
+// the MFMA kernels address the input rows, the neighbour table and the pair
+// list with 32-bit buffer offsets
 static bool conv_fits_buffers(int64_t in_rows, int Cin, int64_t pair_bound) {
     return in_rows * (int64_t)Cin * 2 <= (int64_t)0xFFFFE000 && pair_bound * 8 <= (int64_t)0xFFFFE000;
+}
+
+int conv_kernel_choice(int K3, int Cin, int Cout, int dt, int64_t m_out_cap, int64_t in_rows, int64_t pair_bound,
+                       bool sparse_transposed) {
+    if (!sparse_transposed && union_supported(K3, Cin, Cout, dt) && m_out_cap * K3 * 4 <= (int64_t)0xFFFFE000 &&
+        conv_fits_buffers(in_rows, Cin, 0))
+        return kConvUnion;
+    if (conv_mfma_supported(Cin, Cout, dt) && conv_fits_buffers(in_rows, Cin, pair_bound)) return kConvTile;
+    return kConvValu;
 }
 
 void launch_conv_run(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows, const int32_t* pairs,
                      int64_t pair_bound, int transposed, const void* W, const void* wpack, const float* scale,
                      const float* shift, int relu, void* out, int Cout, int dt) {
-    if (p.use_union && conv_fits_buffers(in_rows, Cin, 0)) {
+    if (p.use_union) {  // the plan checked every bound this kernel needs
         launch_conv_union(s, p, in, Cin, in_rows, Cout, wpack, scale, shift, relu, out, dt);
         return;
     }
-    if (!p.use_union && conv_mfma_supported(Cin, Cout, dt) && conv_fits_buffers(in_rows, Cin, pair_bound)) {
+    if (conv_mfma_supported(Cin, Cout, dt) && conv_fits_buffers(in_rows, Cin, pair_bound)) {
         if (dt == SPV_BF16)
             launch_tile<SPV_BF16>(s, p, in, Cin, in_rows, pairs, pair_bound, transposed, wpack, scale, shift, relu,
                                   out, Cout);

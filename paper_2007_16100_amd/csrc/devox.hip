@@ -194,12 +194,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         // table: every corner lies in the neighbourhood of the point's voxel j,
         // so corner c is entry 9(dx+1) + 3(dy+1) + (dz+1) of row j, with
         // d = base + c - (voxel j's coordinates) in {-1, 0, 1} per axis
+        // rows of the grid that exist: the live count when given, else the capacity
+        int64_t rows = a.nbr_rows;
+        if (a.nbr_m_dev) {
+            const int64_t md = *a.nbr_m_dev;
+            rows = md < 0 ? 0 : (md < rows ? md : rows);
+        }
         int32_t j[PB];
 #pragma unroll
         for (int b = 0; b < PB; ++b) {
             const int64_t k = p0 + b * 16 + r16;
             j[b] = (cn[b].ok && k < a.n) ? a.pt2vox[k] : -1;
-            if (j[b] >= a.nbr_rows) j[b] = -1;
+            if (j[b] >= rows) j[b] = -1;
         }
         int own[PB][3];
 #pragma unroll

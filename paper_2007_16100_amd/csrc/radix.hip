@@ -1,0 +1,338 @@
+// radix.hip -- stable LSD radix sort of (64-bit key, 32-bit payload) pairs with
+// one kernel per 8-bit digit: the canonical (b, x, y, z) order of the voxels of
+// Sec. 3.3 (the paper leaves the order of the m voxels open; this build makes it
+// ascending key order).
+//
+// The producer of the keys (the voxelization's quantize kernel, for instance)
+// writes raw packed keys -- kEmpty for an invalid item -- and one record per
+// block of per-field minima / maxima and invalid counts.  Then:
+//   k_rs_hist   reduces the records into the compaction (per-field minimum
+//               subtracted, fields packed into their bit widths) and counts the
+//               digits of every pass over all keys at once (global histograms);
+//   k_rs_pass   one launch per digit: a tile of keys ranks its items by digit
+//               in index order (stable), publishes its digit counts, reads the
+//               counts of the tiles before it (decoupled look-back: a tile that
+//               has finished publishes its inclusive prefix, so a reader stops
+//               there) and scatters its items to bucket base + prefix + rank.
+// Tiles take their place in the order they start (a counter), so every tile a
+// reader waits for is already running: the look-back always ends.  Passes past
+// the significant bits of the compacted key exit at once.  Invalid items get
+// the all-ones key, which no valid compacted key reaches; their presence makes
+// the sort cover all 64 bits so that they end up last.
+#include "spv_internal.hpp"
+
+namespace spv {
+
+constexpr uint64_t kRsFlagAgg = 1ull << 62;  // status word: the tile's own count
+constexpr uint64_t kRsFlagInc = 2ull << 62;  // ... the inclusive prefix (counts of this tile and all before)
+constexpr uint32_t kRsSpinLimit = 1u << 22;  // polls of one status word before the sort gives up (flags an error)
+
+size_t radix_tiles(int64_t cap) { return blocks_for(cap > 0 ? cap : 1, kRsTile); }
+
+void plan_radix_ws(Arena& a, RadixWs& w, int64_t cap) {
+    const int64_t c = cap > 0 ? cap : 1;
+    w.ka = a.take<uint64_t>(c);
+    w.kb = a.take<uint64_t>(c);
+    w.va = a.take<uint32_t>(c);
+    w.vb = a.take<uint32_t>(c);
+    w.rec = a.take<int32_t>((size_t)kRsRecWords * blocks_for(c, kRsProducerBlock));
+    w.st = a.take<SortStats>(1);
+    w.ntiles = (int64_t)radix_tiles(c);
+    // zeroed by the producer: digit histograms and tile counters
+    w.zero = a.take<uint32_t>(radix_zero_words(c));
+    w.ghist = w.zero;
+    w.ctr = w.zero + kRsPasses * 256;
+    // look-back words, cleared by the sort's own kernels before each use
+    w.status = a.take<uint64_t>((size_t)kRsPasses * 256 * w.ntiles + w.ntiles);
+}
+
+size_t radix_zero_words(int64_t) { return (size_t)kRsPasses * 256 + 64; }
+
+// the compacted form of a raw key (all ones for an invalid item)
+__device__ inline uint64_t rs_compact(uint64_t k, const SortStats& st) {
+    if (k == kEmpty) return kEmpty;
+    uint64_t ck = (uint64_t)(uint32_t)(key_b(k) - st.fmin[0]);
+    ck = (ck << st.fbits[1]) | (uint64_t)(uint32_t)(key_x(k) - st.fmin[1]);
+    ck = (ck << st.fbits[2]) | (uint64_t)(uint32_t)(key_y(k) - st.fmin[2]);
+    ck = (ck << st.fbits[3]) | (uint64_t)(uint32_t)(key_z(k) - st.fmin[3]);
+    return ck;
+}
+
+// The sort's statistics from the producer's records, by one block (every
+// thread receives them).  sort_bits covers all 64 bits when any item is
+// invalid, so that the all-ones keys sort last.
+__device__ inline void rs_reduce_stats(const int32_t* rec, uint32_t nrec, int64_t count, SortStats* out) {
+    int mn[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
+    int mx[4] = {(int)0x80000000, (int)0x80000000, (int)0x80000000, (int)0x80000000};
+    uint32_t inv = 0, iflags = 0;
+    for (uint32_t r = threadIdx.x; r < nrec; r += blockDim.x) {
+        const int32_t* q = rec + (size_t)kRsRecWords * r;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            mn[d] = min(mn[d], q[d]);
+            mx[d] = max(mx[d], q[4 + d]);
+        }
+        inv += (uint32_t)q[8] + (uint32_t)q[9];
+        iflags |= (q[8] ? 1u : 0u) | (q[9] ? 2u : 0u);
+    }
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            mn[d] = min(mn[d], __shfl_xor(mn[d], o, 64));
+            mx[d] = max(mx[d], __shfl_xor(mx[d], o, 64));
+        }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        inv += __shfl_xor(inv, o, 64);
+        iflags |= __shfl_xor(iflags, o, 64);
+    }
+    __shared__ int32_t red[8];
+    __shared__ uint32_t sinv, sflags;
+    __shared__ SortStats res;
+    if (threadIdx.x < 8) red[threadIdx.x] = threadIdx.x < 4 ? 0x7fffffff : (int)0x80000000;
+    if (threadIdx.x == 0) sinv = sflags = 0;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            atomicMin(&red[d], mn[d]);  // LDS
+            atomicMax(&red[4 + d], mx[d]);
+        }
+        atomicAdd(&sinv, inv);
+        atomicOr(&sflags, iflags);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const bool any = (int64_t)sinv < count;  // at least one valid key
+        uint32_t bits = 0;
+        for (int d = 0; d < 4; ++d) {
+            const uint32_t range = any ? (uint32_t)(red[4 + d] - red[d]) : 0u;
+            const uint32_t w = range ? 32u - __clz(range) : 0u;
+            res.fmin[d] = any ? red[d] : 0;
+            res.fmax[d] = any ? red[4 + d] : 0;
+            res.fbits[d] = w;
+            bits += w;
+        }
+        res.n_invalid = sinv;
+        res.invalid_kinds = sflags;
+        res.sort_bits = sinv ? 64u : bits;
+    }
+    __syncthreads();
+    *out = res;
+}
+
+__device__ inline int64_t rs_count(const int64_t* count_dev, int64_t cap) {
+    if (!count_dev) return cap;
+    const int64_t c = *count_dev;
+    return c < 0 ? 0 : (c > cap ? cap : c);
+}
+
+// Statistics (block 0 stores them) and the digit histograms of every pass
+// that the significant bits need, over this block's keys.
+__global__ __launch_bounds__(kRsThreads) void k_rs_hist(RadixWs w, const int64_t* count_dev, int64_t cap,
+                                                        uint32_t nrec) {
+    const int64_t count = rs_count(count_dev, cap);
+    const int64_t base = (int64_t)blockIdx.x * kRsTile;
+    uint64_t raw[kRsItems];  // loaded before the statistics are reduced (no dependence between the two)
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r) {
+        const int64_t i = base + r * kRsThreads + threadIdx.x;
+        raw[r] = i < count ? w.ka[i] : 0ull;
+    }
+    // this tile's look-back words of pass 0 and of the consumer's scan start empty
+    w.status[(size_t)blockIdx.x * 256 + threadIdx.x] = 0ull;
+    if (threadIdx.x == 0) w.status[(size_t)kRsPasses * 256 * w.ntiles + blockIdx.x] = 0ull;
+    SortStats st;
+    rs_reduce_stats(w.rec, nrec, count, &st);
+    if (blockIdx.x == 0 && threadIdx.x == 0) *w.st = st;
+    __shared__ uint32_t hist[kRsPasses][256];
+#pragma unroll
+    for (int p = 0; p < kRsPasses; ++p) hist[p][threadIdx.x] = 0;
+    __syncthreads();
+    const int passes = rs_passes(st);
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r) {
+        const int64_t i = base + r * kRsThreads + threadIdx.x;
+        if (i < count) {
+            const uint64_t ck = rs_compact(raw[r], st);
+            for (int p = 0; p < passes; ++p) atomicAdd(&hist[p][(uint32_t)(ck >> (8 * p)) & 0xFF], 1u);  // LDS
+        }
+    }
+    __syncthreads();
+    for (int p = 0; p < passes; ++p) {
+        const uint32_t c = hist[p][threadIdx.x];
+        if (c) atomicAdd(&w.ghist[p * 256 + threadIdx.x], c);
+    }
+}
+
+// lanes of this wave whose valid digit d equals this lane's (8 ballots)
+__device__ inline uint64_t rs_peers(uint32_t d, bool valid) {
+    uint64_t peers = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+        const uint64_t bal = __ballot((d >> b) & 1);
+        peers &= ((d >> b) & 1) ? bal : ~bal;
+    }
+    return peers;
+}
+
+__device__ inline uint64_t rs_load_status(const uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void rs_store_status(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Exclusive prefix of this tile's count for one digit: the counts of the tiles
+// before it, read kRsWindow at a time from the nearest down, until a tile that
+// holds its inclusive prefix.  A status word not yet written is polled again
+// (the tile that writes it is running); after kRsSpinLimit polls the sort
+// records an error and goes on without it, so the kernel always ends.
+constexpr int kRsWindow = 16;
+__device__ inline uint32_t rs_lookback(const uint64_t* col, int64_t stride, int64_t tile, bool& stalled) {
+    uint32_t excl = 0;
+    int64_t j = tile - 1;
+    uint32_t spins = 0;
+    while (j >= 0) {
+        uint64_t s[kRsWindow];
+#pragma unroll
+        for (int q = 0; q < kRsWindow; ++q) s[q] = (j - q >= 0) ? rs_load_status(col + (j - q) * stride) : kRsFlagInc;
+        int q = 0;
+        bool done = false;
+        for (; q < kRsWindow; ++q) {
+            const uint64_t f = s[q] & (3ull << 62);
+            if (f == 0) break;  // not written yet: read it again
+            excl += (uint32_t)s[q];
+            if (f == kRsFlagInc) {
+                done = true;
+                break;
+            }
+        }
+        if (done) break;
+        j -= q;
+        if (q == 0) {
+            if (++spins > kRsSpinLimit) {
+                stalled = true;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+    }
+    return excl;
+}
+
+template <bool FIRST>
+__global__ __launch_bounds__(kRsThreads) void k_rs_pass(RadixWs w, Header* h, const int64_t* count_dev, int64_t cap,
+                                                        int pass) {
+    constexpr int NWV = kRsThreads / 64;
+    const SortStats* gst = w.st;
+    // the first pass always runs: it writes the compacted keys and the payload
+    if (pass > 0 && (uint32_t)(8 * pass) >= gst->sort_bits) return;
+    // per (round, wave, digit) counts, then offsets relative to the tile's first
+    // item of that digit (both at most kRsTile, 16 bits); dbase: the digit's
+    // first output position for this tile
+    __shared__ uint16_t cnt[kRsItems][NWV][256];
+    __shared__ uint32_t dbase[256];
+    __shared__ int lds[NWV + 1];
+    __shared__ uint32_t s_tile;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    if (t == 0) s_tile = atomicAdd(&w.ctr[pass], 1u);
+    // bucket base of digit t: all keys of smaller digits
+    int all;
+    const uint32_t gbase = (uint32_t)block_exclusive_scan((int)w.ghist[pass * 256 + t], lds, &all);
+    const int64_t tile = s_tile;
+    const int64_t count = rs_count(count_dev, cap);
+    const int64_t base = tile * kRsTile;
+    // the next pass's look-back words of this tile start empty (that pass starts after this one ends)
+    if (pass + 1 < kRsPasses) w.status[((size_t)(pass + 1) * w.ntiles + tile) * 256 + t] = 0ull;
+    const uint64_t* ksrc = (pass & 1) ? w.kb : w.ka;
+    uint64_t* kdst = (pass & 1) ? w.ka : w.kb;
+    const uint32_t* vsrc = (pass & 1) ? w.vb : w.va;
+    uint32_t* vdst = (pass & 1) ? w.va : w.vb;
+    SortStats st;
+    if constexpr (FIRST) st = *gst;
+    uint64_t keys[kRsItems];
+    uint32_t vals[kRsItems];
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r) {
+        const int64_t i = base + r * kRsThreads + t;
+        if constexpr (FIRST) {
+            keys[r] = i < count ? rs_compact(ksrc[i], st) : 0ull;
+            vals[r] = (uint32_t)i;  // the first pass sorts the item indices
+        } else {
+            keys[r] = i < count ? ksrc[i] : 0ull;
+            vals[r] = i < count ? vsrc[i] : 0u;
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r)
+#pragma unroll
+        for (int q = 0; q < NWV; ++q) cnt[r][q][t] = 0;
+    __syncthreads();
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    uint32_t rank[kRsItems];
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r) {
+        const int64_t i = base + r * kRsThreads + t;
+        const bool valid = i < count;
+        const uint32_t d = (uint32_t)(keys[r] >> (8 * pass)) & 0xFF;
+        const uint64_t peers = rs_peers(d, valid);
+        rank[r] = (uint32_t)__popcll(peers & lt);
+        if (valid && rank[r] == 0) cnt[r][wave][d] = (uint16_t)__popcll(peers);
+    }
+    __syncthreads();
+    // thread t owns digit t: the tile's count, published before the look-back
+    uint32_t tot = 0;
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r)
+#pragma unroll
+        for (int q = 0; q < NWV; ++q) tot += (uint32_t)cnt[r][q][t];
+    uint64_t* col = w.status + (size_t)pass * 256 * w.ntiles + t;  // status[pass][tile][digit] at col + tile * 256
+    bool stalled = false;
+    uint32_t excl = 0;
+    if (tile == 0) {
+        rs_store_status(col, kRsFlagInc | tot);
+    } else {
+        rs_store_status(col + tile * 256, kRsFlagAgg | tot);
+        excl = rs_lookback(col, 256, tile, stalled);
+        rs_store_status(col + tile * 256, kRsFlagInc | (uint64_t)(excl + tot));
+    }
+    if (stalled) raise_flag(h, kFlagInternal);
+    // running write offsets over (round, wave) in index order
+    dbase[t] = gbase + excl;
+    uint32_t run = 0;
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r)
+#pragma unroll
+        for (int q = 0; q < NWV; ++q) {
+            const uint32_t c = cnt[r][q][t];
+            cnt[r][q][t] = (uint16_t)run;
+            run += c;
+        }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r) {
+        const int64_t i = base + r * kRsThreads + t;
+        if (i < count) {
+            const uint32_t d = (uint32_t)(keys[r] >> (8 * pass)) & 0xFF;
+            const uint32_t pos = dbase[d] + cnt[r][wave][d] + rank[r];
+            kdst[pos] = keys[r];
+            vdst[pos] = vals[r];
+        }
+    }
+}
+
+void launch_radix_sort(hipStream_t s, const RadixWs& w, Header* h, const int64_t* count_dev, int64_t cap,
+                       uint32_t nrec) {
+    if (cap < 0) cap = 0;
+    const unsigned nt = (unsigned)radix_tiles(cap);  // at least one tile: the first pass always writes its outputs
+    k_rs_hist<<<nt, kRsThreads, 0, s>>>(w, count_dev, cap, nrec);
+    // the significant bits are known on the device only: every pass a 64-bit
+    // key may need is launched, and passes beyond them exit at once
+    k_rs_pass<true><<<nt, kRsThreads, 0, s>>>(w, h, count_dev, cap, 0);
+    for (int p = 1; p < kRsPasses; ++p) k_rs_pass<false><<<nt, kRsThreads, 0, s>>>(w, h, count_dev, cap, p);
+}
+
+}  // namespace spv

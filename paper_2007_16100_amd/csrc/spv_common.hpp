@@ -41,6 +41,7 @@ enum : uint32_t {
     kFlagDuplicate = 1u << 3,  // repeated coordinate where distinct ones are required
     kFlagTableFull = 1u << 4,
     kFlagUnsorted = 1u << 5,   // a kernel-map offset group not sorted by output row
+    kFlagInternal = 1u << 6,   // a kernel gave up waiting on another (a runtime fault, not an input error)
 };
 
 // Workspace header: first 256 bytes of every workspace.

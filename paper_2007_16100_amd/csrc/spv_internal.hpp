@@ -101,7 +101,9 @@ struct SortStats {
     int32_t fmin[4];    // per-field minimum of the keys being sorted (b, x, y, z)
     int32_t fmax[4];
     uint32_t fbits[4];  // bit width of each compacted field
-    uint32_t sort_bits; // significant bits of the compacted key
+    uint32_t sort_bits; // significant bits of the compacted key (64 when any item is invalid)
+    uint32_t n_invalid; // items with an invalid key (radix sort of pairs only)
+    uint32_t invalid_kinds;  // bit 0: a non-finite item, bit 1: an item out of the key range
 };
 struct SortBufs {
     uint64_t* a;       // [cap] input keys / ping
@@ -132,6 +134,62 @@ __device__ inline uint64_t sorted_key(const SortBufs& sb, int64_t r) {
     return pack_key(b, x, y, z);
 }
 
+// --- radix sort of (key, payload) pairs, one launch per digit (radix.hip) -------
+// The producer writes raw packed keys (kEmpty: invalid item) to ka[0..count) and,
+// per block of kRsProducerBlock items, a record of kRsRecWords ints: per-field
+// minima (4) and maxima (4) of its valid keys, then its non-finite and
+// out-of-range item counts.  It also zeroes zero[0..radix_zero_words).  After
+// launch_radix_sort the compacted keys, ascending, and the items' original
+// indices sit in rs_keys / rs_vals (which of the two buffers depends on the
+// number of passes, known on the device).
+constexpr int kRsThreads = 256;
+constexpr int kRsItems = 16;
+constexpr int kRsTile = kRsThreads * kRsItems;  // keys per tile
+constexpr int kRsPasses = 8;                    // 8-bit digits of a 64-bit key
+constexpr int kRsRecWords = 12;
+constexpr int kRsProducerBlock = 1024;
+struct RadixWs {
+    uint64_t* ka;
+    uint64_t* kb;
+    uint32_t* va;
+    uint32_t* vb;
+    int32_t* rec;       // producer records
+    SortStats* st;
+    int64_t ntiles;     // tiles of the capacity (a pass grid)
+    uint32_t* zero;     // the region the producer zeroes (radix_zero_words):
+    uint32_t* ghist;    //   [kRsPasses][256] digit counts over all keys
+    uint32_t* ctr;      //   [64] tile counters (0..7 the passes, 8.. for the consumers)
+    uint64_t* status;   // [kRsPasses][ntiles][256] look-back words, then [ntiles] for a consumer's scan:
+                        // the histogram kernel clears pass 0's and the consumer's, pass p clears pass p+1's
+};
+size_t radix_tiles(int64_t cap);
+size_t radix_zero_words(int64_t cap);
+void plan_radix_ws(Arena& a, RadixWs& w, int64_t cap);
+// count_dev: device item count (nullptr: cap); nrec: producer records
+void launch_radix_sort(hipStream_t s, const RadixWs& w, Header* h, const int64_t* count_dev, int64_t cap,
+                       uint32_t nrec);
+__host__ __device__ inline int rs_passes(const SortStats& st) {
+    const int p = (int)((st.sort_bits + 7) / 8);
+    return p > 0 ? p : 1;
+}
+__device__ inline const uint64_t* rs_keys(const RadixWs& w, const SortStats& st) {
+    return (rs_passes(st) & 1) ? w.kb : w.ka;
+}
+__device__ inline const uint32_t* rs_vals(const RadixWs& w, const SortStats& st) {
+    return (rs_passes(st) & 1) ? w.vb : w.va;
+}
+// the packed key of a compacted key
+__device__ inline uint64_t rs_expand(uint64_t ck, const SortStats& st) {
+    const uint32_t bz = st.fbits[3], by = st.fbits[2], bx = st.fbits[1];
+    const int z = (int)(ck & ((1ull << bz) - 1)) + st.fmin[3];
+    ck >>= bz;
+    const int y = (int)(ck & ((1ull << by) - 1)) + st.fmin[2];
+    ck >>= by;
+    const int x = (int)(ck & ((1ull << bx) - 1)) + st.fmin[1];
+    ck >>= bx;
+    return pack_key((int)ck + st.fmin[0], x, y, z);
+}
+
 // --- prefix sums with a device-side count (hash_sort_scan.hip) ----------------
 // out[i] = sum_{j<i} in[j] for i in [0, count]; out must hold cap + 1 ints;
 // tmp must hold scan_tmp_entries(cap) ints.
@@ -142,11 +200,11 @@ void launch_exclusive_scan(hipStream_t s, const int32_t* in, int32_t* out, const
 void launch_exclusive_scan_small(hipStream_t s, const uint32_t* in, uint32_t* out, int64_t n);
 
 // --- voxelize (voxelize.hip) ---------------------------------------------------
+struct PackJob;
 struct VoxelizeWs {
     Header* h;          // assigned by the caller (workspace offset 0)
     Table table;
-    SortBufs sort;
-    uint32_t* pslot;    // [n] table slot of each point's key (kNoSlot if invalid)
+    RadixWs rs;         // the points sorted by key
     int32_t* seg;       // [n + 1] CSR offsets of the points of each voxel
     int32_t* fill;      // [n]
     int32_t* plist;     // [n] point ids grouped by voxel
@@ -154,11 +212,13 @@ struct VoxelizeWs {
     int32_t* scan_tmp;  // [scan_tmp_entries(n)]
 };
 void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n);
-// coords/counts/pt2vox and (if feat) vfeat; m into h->m and *m_dev
+// coords/counts/pt2vox and (if feat) vfeat; m into h->m and *m_dev.  The first
+// launch clears the status header and the table and also runs the weight
+// packings `jobs` (a block call packs its layers' weights there).
 void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const int32_t* batch, int64_t n,
                      float voxel_size, const void* feat, int32_t C, int dt, int32_t* coords, void* vfeat,
-                     int32_t* counts, int32_t* pt2vox, int64_t* m_dev,
-                     bool table_cleared = false);
+                     int32_t* counts, int32_t* pt2vox, int64_t* m_dev, const PackJob* jobs = nullptr,
+                     int njobs = 0);
 // scatter-mean onto the given voxel set coords[min(*m_dev, m_cap)] (value = row);
 // points whose voxel is not in the set get pt2vox -1; ws planned for max(n, m_cap)
 void launch_voxelize_onto(hipStream_t s, const VoxelizeWs& w, const int32_t* coords, const int64_t* m_dev,
@@ -219,7 +279,16 @@ struct ConvPlan {
     int64_t w_ldk = 0;
     int w_ldcol = 0;
 };
-void plan_conv_ws(Arena& a, ConvPlan& p, int64_t m_out_cap, int K3, int Cin, int Cout, int dt);
+// The kernel a conv runs on, decided on the host from the shape and the sizes
+// (kConvUnion needs every neighbour-table and input offset within 32 bits; a
+// transposed map with fewer inputs than outputs -- sparse_transposed -- goes to
+// the tile kernel, which visits pairs only).
+enum ConvKernel { kConvUnion = 0, kConvTile = 1, kConvValu = 2 };
+int conv_kernel_choice(int K3, int Cin, int Cout, int dt, int64_t m_out_cap, int64_t in_rows, int64_t pair_bound,
+                       bool sparse_transposed);
+// in_rows: rows of the conv's input (the plan's kernel choice depends on it)
+void plan_conv_ws(Arena& a, ConvPlan& p, int64_t m_out_cap, int K3, int Cin, int Cout, int dt, int64_t in_rows,
+                  bool sparse_transposed = false);
 struct PackJob;
 // plans the conv on a kernel map (neighbour table or tile bounds), runs the
 // weight packing pk (total = 0: none) in one of its launches and, with
@@ -240,6 +309,39 @@ struct PackJob {
     int64_t ldk;        // elements between offsets (Cin * Cout when dense)
     int ldcol = 1;      // elements between output channels (1 when dense)
 };
+// fragment t of the packing (t = ((k * KCH + kc) * NB + nb) * 64 + lane)
+// W[k][c][col] sits at W[k * ldk + c * ldc + col * ldcol] (ldc = Cout, ldcol = 1,
+// ldk = Cin * Cout for a dense [K3][Cin][Cout] tensor; larger ldc / ldk for a
+// channel slice of a wider one; ldc = 1, ldcol = the stored row length to read
+// every W[k] transposed)
+__device__ inline uint4 pack_fragment(const uint16_t* W, int Cin, int Cout, int ldc, int ldcol, int64_t ldk, int KCH,
+                                     int NB, int64_t t) {
+    const int lane = (int)(t & 63);
+    int64_t f = t >> 6;
+    const int nb = (int)(f % NB);
+    f /= NB;
+    const int kc = (int)(f % KCH);
+    const int k = (int)(f / KCH);
+    const int col = nb * 16 + (lane & 15);
+    const int ci0 = kc * 32 + 8 * (lane >> 4);
+    uint32_t w[4];
+    for (int e = 0; e < 4; ++e) {
+        uint32_t lo = 0, hi = 0;
+        const int c0 = ci0 + 2 * e, c1 = ci0 + 2 * e + 1;
+        // zeros past the last input channel and past the last output column
+        if (c0 < Cin && col < Cout) lo = W[(int64_t)k * ldk + (int64_t)c0 * ldc + (int64_t)col * ldcol];
+        if (c1 < Cin && col < Cout) hi = W[(int64_t)k * ldk + (int64_t)c1 * ldc + (int64_t)col * ldcol];
+        w[e] = lo | (hi << 16);
+    }
+    return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// a weight packing run alongside another kernel's work (grid-stride)
+__device__ inline void pack_job_run(const PackJob& q) {
+    for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < q.total; t += (int64_t)gridDim.x * blockDim.x)
+        q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.ldc, q.ldcol, q.ldk, q.KCH, q.NB, t);
+}
+
 // ldc / ldk <= 0: W is a dense [K3][Cin][Cout] tensor; otherwise the leading
 // Cin x Cout block of each offset of a wider tensor (a channel slice)
 PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int dt, int ldc = 0, int64_t ldk = 0,
@@ -311,10 +413,8 @@ void launch_voxelize_backward(hipStream_t s, const void* dv, int C, const int32_
 void launch_devoxelize_backward(hipStream_t s, const int32_t* cidx, const float* cw, const void* dout, int64_t n, int C,
                                 float* dv, int64_t m, int dt);
 
-// The first kernel of a block call: clears the voxel table and the status
-// header, and packs up to kMaxPackJobs weights, in one grid-stride launch.
+// weight packings a block call runs inside its voxelization's first launch
 constexpr int kMaxPackJobs = 3;
-void launch_block_prologue(hipStream_t s, Header* h, Table t, const PackJob* jobs, int njobs);
 // the convolution itself (one kernel); wpack must have been packed from W
 void launch_conv_run(hipStream_t s, const ConvPlan& p, const void* in, int Cin, int64_t in_rows, const int32_t* pairs,
                      int64_t pair_bound, int transposed, const void* W, const void* wpack, const float* scale,
@@ -350,6 +450,7 @@ struct DevoxArgs {
     const int32_t* grid_coords = nullptr;
     const int32_t* nbr = nullptr;
     int64_t nbr_rows = 0;  // rows of nbr / grid_coords: a pt2vox entry outside [0, nbr_rows) has no corners
+    const int64_t* nbr_m_dev = nullptr;  // live row count of the grid (bounds pt2vox entries further when given)
 };
 bool devox_mfma_supported(int C, int Cp, int dt);
 void* plan_devox_ws(Arena& a, int C, int Cp);

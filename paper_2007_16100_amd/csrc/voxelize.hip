@@ -1,13 +1,20 @@
 // voxelize.hip -- sparse voxelization (Sec. 3.3, Eq. 1 and Eq. 2).
 //
-// 1. every point's key floor(p / v) is inserted into the open-addressing hash;
-//    the thread that creates an entry appends the key to the unique-key list;
-// 2. the m unique keys are radix-sorted into canonical (b, x, y, z) order and the
-//    table values are set to the rank, which also writes the voxel coordinates;
-// 3. every point reads its voxel index (pt2vox) at the table slot its insert
-//    found, and counts N_m;
-// 4. a counting sort of the points by voxel (prefix sum + fill) lets each voxel
-//    gather and average its own points -- no float atomics, one write per voxel.
+// 1. k_vq_quantize: every point's key floor(p / v) (Eq. 1), packed; per block the
+//    per-field minima / maxima of the keys for the sort's compaction.  The same
+//    launch clears the status header and the hash table and, in a block call,
+//    packs the layers' weights;
+// 2. the points are radix-sorted by key (radix.hip): the canonical (b, x, y, z)
+//    order of the voxels and the grouping of the points by voxel in one step;
+// 3. k_vq_segments: a voxel starts wherever the sorted key changes.  A scan of
+//    those starts numbers the voxels; each voxel's coordinates, its first point
+//    and its hash-table entry (value = its index: one insert per voxel, no
+//    contention) are written at its start, and every point gets its voxel index;
+// 4. k_vox_mean: each voxel sums its own points (fp64) and writes its mean and
+//    count once -- no float atomics.
+// The scatter-mean onto a given voxel set (launch_voxelize_onto) finds each
+// point's voxel in the set's table instead and groups the points by a counting
+// sort.
 #include "spv_internal.hpp"
 
 namespace spv {
@@ -18,8 +25,7 @@ void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n) {
     w.table.keys = a.take<uint64_t>(S);
     w.table.vals = a.take<int32_t>(S);
     w.table.mask = S - 1;
-    plan_sort_ws(a, w.sort, nn);
-    w.pslot = a.take<uint32_t>(nn);
+    plan_radix_ws(a, w.rs, nn);
     w.seg = a.take<int32_t>(nn + 1);
     w.fill = a.take<int32_t>(nn);
     w.plist = a.take<int32_t>(nn);
@@ -53,66 +59,257 @@ __device__ inline uint64_t point_key(Header* h, const float* xyz, const int32_t*
     return pack_key(b, q[0], q[1], q[2]);
 }
 
-// Eq. 1 per point, then hash insert.  Invalid points get kEmpty and a status
-// flag.  Consecutive returns of a sweep often share a voxel: a lane whose key
-// equals the previous lane's leaves the insert to the head of its run.  The
-// block appends the keys it created to the unique-key list (one counter atomic
-// per block) and records their per-field min / max for the sort.
-__global__ __launch_bounds__(kAppendThreads) void k_vox_insert(Header* h, Table t, SortBufs sb, uint32_t* pslot,
-                                                               const float* xyz, const int32_t* batch, int64_t n,
-                                                               float v) {
-    const int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    bool created = false;
-    uint64_t key = kEmpty;
-    int q[3] = {0, 0, 0};
-    int b = 0;
-    if (k < n) key = point_key(h, xyz, batch, k, v, q, b);
-    // runs of equal keys inside the wave: the head inserts, the others take its
-    // slot (every lane between a head and a later lane of its run has its key)
-    const int lane = threadIdx.x & 63;
-    const uint64_t prev_key = __shfl_up(key, 1, 64);
-    const bool head = key != kEmpty && (lane == 0 || prev_key != key);
-    uint32_t slot = kNoSlot;
-    if (head) {
-        const int r = table_insert(t, key, &slot);
-        created = r > 0;
-        if (r < 0) {
-            raise_flag(h, kFlagTableFull);
-            slot = kNoSlot;
-        }
-    }
-    const uint64_t heads = __ballot(head) & (~0ull >> (63 - lane));  // heads at lanes <= this one
-    const int src = heads ? 63 - __clzll(heads) : lane;
-    const uint32_t run_slot = __shfl(slot, src, 64);
-    if (k < n) pslot[k] = key == kEmpty ? kNoSlot : run_slot;
-    int mn[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
-    int mx[4] = {(int)0x80000000, (int)0x80000000, (int)0x80000000, (int)0x80000000};
-    if (created) {
-        const int f[4] = {b, q[0], q[1], q[2]};
+// Eq. 1 for point k without side effects: the packed key, or kEmpty with
+// *why = 1 (a non-finite coordinate) or 2 (a voxel outside the key range)
+__device__ inline uint64_t point_key_of(const float* xyz, const int32_t* batch, int64_t k, float v, int& why) {
+    const float p[3] = {xyz[3 * k], xyz[3 * k + 1], xyz[3 * k + 2]};
+    const int b = batch ? batch[k] : 0;
+    const bool finite = isfinite(p[0]) && isfinite(p[1]) && isfinite(p[2]);
+    bool inrange = b >= 0 && b <= kBatchMax;
+    int q[3];
 #pragma unroll
-        for (int d = 0; d < 4; ++d) mn[d] = mx[d] = f[d];
+    for (int d = 0; d < 3; ++d) {
+        const float a = p[d] / v;  // IEEE single-precision, correctly rounded
+        const float f = floorf(a);
+        inrange = inrange && isfinite(a) && f >= (float)kCoordMin && f <= (float)kCoordMax;
+        q[d] = inrange ? (int)f : 0;
     }
-    block_append(created, key, sb.a, &h->m);
-    block_minmax_record(mn, mx, sb.part + 8 * blockIdx.x);
+    why = !finite ? 1 : (!inrange ? 2 : 0);
+    return why ? kEmpty : pack_key(b, q[0], q[1], q[2]);
 }
 
-// rank -> table value, voxel coordinates, zeroed counters
-__global__ void k_vox_rank(const Header* h, SortBufs sb, Table t, int32_t* coords, int32_t* counts, int32_t* fill,
-                           int64_t cap, int64_t* m_dev) {
+// What the first launch of a voxelization clears and packs besides Eq. 1.
+struct VoxFirst {
+    Header* h;
+    uint64_t* tkeys;  // the hash table's key slots -> empty
+    uint32_t nslots;
+    uint32_t* zero;   // the sort's counters and look-back words -> 0
+    int64_t nzero;
+    int njobs;
+    PackJob job[kMaxPackJobs];
+};
+
+// Eq. 1 per point into the sort's key buffer, with the block's record (per-field
+// minima / maxima of its valid keys, its non-finite and out-of-range counts).
+// Grid-stride alongside: the header, the table, the sort's scratch, the packings.
+__global__ __launch_bounds__(kRsProducerBlock) void k_vq_quantize(VoxFirst f, const float* xyz,
+                                                                  const int32_t* batch, int64_t n, float v,
+                                                                  uint64_t* keys, int32_t* rec) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        f.h->status = 0;
+        f.h->m = 0;
+        for (int i = 0; i < 4; ++i) f.h->aux[i] = 0;
+    }
+    const int64_t t0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = t0; i < (int64_t)f.nslots; i += stride) f.tkeys[i] = kEmpty;
+    for (int64_t i = t0; i < f.nzero; i += stride) f.zero[i] = 0u;
+    for (int j = 0; j < f.njobs; ++j) pack_job_run(f.job[j]);
+
+    int mn[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
+    int mx[4] = {(int)0x80000000, (int)0x80000000, (int)0x80000000, (int)0x80000000};
+    int why = 0;
+    if (t0 < n) {
+        const uint64_t key = point_key_of(xyz, batch, t0, v, why);
+        keys[t0] = key;
+        if (!why) {
+            const int fl[4] = {key_b(key), key_x(key), key_y(key), key_z(key)};
+#pragma unroll
+            for (int d = 0; d < 4; ++d) mn[d] = mx[d] = fl[d];
+        }
+    }
+    uint32_t nonfin = __popcll(__ballot(why == 1)), range = __popcll(__ballot(why == 2));
+    __shared__ uint32_t bad[2];
+    if (threadIdx.x < 2) bad[threadIdx.x] = 0;
+    block_minmax_record(mn, mx, rec + (size_t)kRsRecWords * blockIdx.x);  // synchronizes the block
+    if ((threadIdx.x & 63) == 0 && (nonfin | range)) {
+        atomicAdd(&bad[0], nonfin);  // LDS
+        atomicAdd(&bad[1], range);
+    }
+    __syncthreads();
+    if (threadIdx.x < 2) rec[(size_t)kRsRecWords * blockIdx.x + 8 + threadIdx.x] = (int32_t)bad[threadIdx.x];
+}
+
+// Exclusive prefix of a tile's count over the tiles before it, by one whole
+// wave: 64 predecessors' status words per round, nearest first, up to the
+// nearest one holding an inclusive prefix (same protocol as the sort's passes).
+__device__ inline uint32_t vq_lookback(const uint64_t* stat, int64_t tile, bool& stalled) {
+    const int lane = threadIdx.x & 63;
+    uint32_t excl = 0, spins = 0;
+    int64_t j = tile - 1;
+    while (j >= 0) {
+        const uint64_t s = (j - lane >= 0)
+                               ? __hip_atomic_load(stat + (j - lane), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                               : (2ull << 62);
+        const uint32_t f = (uint32_t)(s >> 62);
+        const uint64_t notready = __ballot(f == 0), inc = __ballot(f == 2);
+        const int fi = inc ? __builtin_ctzll(inc) : 64;                // nearest inclusive prefix
+        const uint64_t upto = fi < 63 ? ((2ull << fi) - 1ull) : ~0ull;  // lanes 0 .. fi
+        int take;
+        bool done;
+        if (notready & upto) {  // consume the ready lanes before the first one not written yet
+            take = __builtin_ctzll(notready & upto);
+            done = false;
+        } else {
+            take = fi < 64 ? fi + 1 : 64;
+            done = fi < 64;
+        }
+        uint32_t val = lane < take ? (uint32_t)s : 0u;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) val += __shfl_xor(val, o, 64);
+        excl += val;
+        if (done) break;
+        j -= take;
+        if (take == 0) {
+            if (++spins > (1u << 22)) {
+                stalled = true;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+    }
+    return excl;
+}
+
+// Voxels from the sorted keys: position i starts a voxel when its key differs
+// from position i-1's.  Tile-local ranks of the starts (position order: round,
+// wave, lane) plus the look-back give every start its voxel index; there the
+// voxel's coordinates, its first sorted position (seg) and its table entry are
+// written, and every point receives its voxel's index (invalid points, sorted
+// last, get -1).  The hash inserts of a thread's starts are issued together
+// (each key is new: a first compare-and-swap almost always claims its slot).
+// The last tile writes m.
+__global__ __launch_bounds__(kRsThreads) void k_vq_segments(RadixWs rs, Header* h, Table t, int64_t n,
+                                                            int64_t ntiles, int32_t* coords, int32_t* pt2vox,
+                                                            int32_t* seg, int32_t* plist, int64_t* m_dev) {
+    constexpr int I = kRsItems, NWV = kRsThreads / 64;
+    __shared__ uint32_t s_tile, s_excl;
+    __shared__ uint32_t wcnt[I][NWV];  // starts per (round, wave), then their exclusive prefix in the tile
+    __shared__ uint32_t s_tot;
+    const SortStats st = *rs.st;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (tid == 0) s_tile = atomicAdd(&rs.ctr[8], 1u);
+    const uint64_t* K = rs_keys(rs, st);
+    const uint32_t* V = rs_vals(rs, st);
+    const int64_t nvalid = n - (int64_t)st.n_invalid;
+    __syncthreads();
+    const int64_t tile = s_tile;
+    const int64_t base = tile * kRsTile;
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    uint64_t key[I];
+    uint32_t hb = 0;       // bit r: position of round r starts a voxel
+    uint32_t rk[I];        // rank of the start among its wave's starts of that round
+#pragma unroll
+    for (int r = 0; r < I; ++r) {
+        const int64_t i = base + r * kRsThreads + tid;
+        key[r] = i < nvalid ? K[i] : kEmpty;
+        const uint64_t pk = (i > 0 && i - 1 < nvalid) ? K[i - 1] : kEmpty;
+        const bool hd = i < nvalid && (i == 0 || key[r] != pk);
+        const uint64_t bal = __ballot(hd);
+        hb |= (hd ? 1u : 0u) << r;
+        rk[r] = (uint32_t)__popcll(bal & lt);
+        if (lane == 0) wcnt[r][wave] = (uint32_t)__popcll(bal);
+    }
+    __syncthreads();
+    if (tid == 0) {
+        uint32_t run = 0;
+        for (int r = 0; r < I; ++r)
+            for (int q = 0; q < NWV; ++q) {
+                const uint32_t c = wcnt[r][q];
+                wcnt[r][q] = run;
+                run += c;
+            }
+        s_tot = run;
+    }
+    __syncthreads();
+    const uint32_t tot = s_tot;
+    uint64_t* stat = rs.status + (size_t)kRsPasses * 256 * rs.ntiles;
+    if (tid < 64) {
+        bool stalled = false;
+        uint32_t excl = 0;
+        if (tile == 0) {
+            if (tid == 0)
+                __hip_atomic_store(stat, (2ull << 62) | tot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            if (tid == 0)
+                __hip_atomic_store(stat + tile, (1ull << 62) | tot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            excl = vq_lookback(stat, tile, stalled);
+            if (tid == 0)
+                __hip_atomic_store(stat + tile, (2ull << 62) | (uint64_t)(excl + tot), __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        }
+        if (tid == 0) {
+            s_excl = excl;
+            if (stalled) raise_flag(h, kFlagInternal);
+            if (tile == 0) {  // invalid points (their keys were counted by the sort) make the call report
+                if (st.invalid_kinds & 1u) raise_flag(h, kFlagNonfinite);
+                if (st.invalid_kinds & 2u) raise_flag(h, kFlagRange);
+            }
+        }
+    }
+    __syncthreads();
+    const int64_t excl = s_excl;
+    // voxel index of each position: the starts before it (in the tile and before
+    // the tile); a start takes the next index, any other position its last start's
+    int32_t vid[I];
+    uint64_t pk[I];
+    uint32_t slot[I];
+    uint64_t prev[I];
+#pragma unroll
+    for (int r = 0; r < I; ++r) {
+        const bool hd = (hb >> r) & 1u;
+        vid[r] = (int32_t)(excl + wcnt[r][wave] + rk[r]) - (hd ? 0 : 1);
+        pk[r] = hd ? rs_expand(key[r], st) : kEmpty;
+        slot[r] = hd ? hash_slot(pk[r], t.mask) : 0u;
+        prev[r] = hd ? atomicCAS((unsigned long long*)&t.keys[slot[r]], (unsigned long long)kEmpty,
+                                 (unsigned long long)pk[r])
+                     : 0ull;
+    }
+#pragma unroll
+    for (int r = 0; r < I; ++r) {
+        const int64_t i = base + r * kRsThreads + tid;
+        if (i >= n) continue;
+        const uint32_t k = V[i];
+        plist[i] = (int32_t)k;
+        if (i >= nvalid) {
+            pt2vox[k] = -1;
+            continue;
+        }
+        if ((hb >> r) & 1u) {
+            int32_t* cv = coords + 4 * (int64_t)vid[r];
+            cv[0] = key_b(pk[r]);
+            cv[1] = key_x(pk[r]);
+            cv[2] = key_y(pk[r]);
+            cv[3] = key_z(pk[r]);
+            seg[vid[r]] = (int32_t)i;
+            uint32_t sl = slot[r];
+            uint64_t pv = prev[r];
+            int ins = pv == kEmpty ? 1 : (pv == pk[r] ? 0 : 2);
+            for (uint32_t probe = 1; ins == 2 && probe <= t.mask; ++probe) {  // the slot was taken: probe on
+                sl = (sl + 1) & t.mask;
+                pv = atomicCAS((unsigned long long*)&t.keys[sl], (unsigned long long)kEmpty,
+                               (unsigned long long)pk[r]);
+                ins = pv == kEmpty ? 1 : (pv == pk[r] ? 0 : 2);
+            }
+            if (ins == 1) t.vals[sl] = (int32_t)vid[r];
+            else raise_flag(h, ins == 0 ? kFlagDuplicate : kFlagTableFull);
+        }
+        pt2vox[k] = (int32_t)vid[r];
+    }
+    if (tile == ntiles - 1 && tid == 0) {  // the voxel count, after the last tile's look-back
+        const int64_t m = excl + tot;
+        seg[m] = (int32_t)nvalid;
+        h->m = m;
+        if (m_dev) *m_dev = m;
+    }
+}
+
+// N_m = seg[v + 1] - seg[v] when there are no features to average
+__global__ void k_vq_counts(const Header* h, int64_t cap, const int32_t* seg, int32_t* counts) {
     int64_t m = h->m;
     if (m > cap) m = cap;
-    int64_t r = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    if (r == 0 && m_dev) *m_dev = m;
-    if (r >= m) return;
-    uint64_t key = sorted_key(sb, r);
-    int64_t slot = table_slot(t, key);
-    if (slot >= 0) t.vals[slot] = (int32_t)r;
-    coords[4 * r + 0] = key_b(key);
-    coords[4 * r + 1] = key_x(key);
-    coords[4 * r + 2] = key_y(key);
-    coords[4 * r + 3] = key_z(key);
-    counts[r] = 0;
-    fill[r] = 0;
+    const int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (v < m) counts[v] = seg[v + 1] - seg[v];
 }
 
 // every point's voxel index, read at the table slot its insert found
@@ -127,19 +324,6 @@ __device__ inline void run_of(int32_t v, int& first, int& len) {
     first = 63 - __clzll(heads & (~0ull >> (63 - lane)));
     const uint64_t later = heads & ~((2ull << first) - 1ull);  // heads after the run's first lane
     len = (later ? __builtin_ctzll(later) : 64) - first;
-}
-
-__global__ void k_vox_lookup(Table t, const uint32_t* pslot, int64_t n, int32_t* pt2vox, int32_t* counts) {
-    const int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    int32_t v = -1;
-    if (k < n) {
-        const uint32_t ps = pslot[k];
-        v = (ps == kNoSlot) ? -1 : t.vals[ps];
-        pt2vox[k] = v;
-    }
-    int first, len;
-    run_of(v, first, len);
-    if (v >= 0 && (int)(threadIdx.x & 63) == first) atomicAdd(&counts[v], len);
 }
 
 __global__ void k_vox_fill(const int32_t* pt2vox, int64_t n, const int32_t* seg, int32_t* fill, int32_t* plist) {
@@ -236,7 +420,7 @@ __device__ inline void mean_store(const double (&acc)[VEC], double N, void* vfea
 
 template <int DT, int VEC>
 __global__ void k_vox_mean(Header* h, int64_t cap, const int32_t* seg, const int32_t* plist, const void* feat,
-                           int C, void* vfeat, int run, int32_t* longv) {
+                           int C, void* vfeat, int run, int32_t* longv, int32_t* counts) {
     int64_t m = h->m;
     if (m > cap) m = cap;
     const int nch = C / VEC;
@@ -245,6 +429,7 @@ __global__ void k_vox_mean(Header* h, int64_t cap, const int32_t* seg, const int
     int ch = (int)(t - vox * nch) * VEC;
     if (vox >= m) return;
     int32_t lo = seg[vox], hi = seg[vox + 1];
+    if (counts && ch == 0) counts[vox] = hi - lo;  // N_m (when the caller has not counted it)
     if (hi - lo > run) {
         if (ch == 0) longv[atomicAdd((unsigned long long*)&h->aux[0], 1ull)] = (int32_t)vox;
         return;
@@ -294,11 +479,12 @@ __global__ __launch_bounds__(kMeanLongThreads) void k_vox_mean_long(const Header
 constexpr int kMeanRun = 32;  // points a single thread sums
 
 template <int DT, int VEC>
-static void launch_mean(hipStream_t s, const VoxelizeWs& w, int64_t n, const void* feat, int C, void* vfeat) {
+static void launch_mean(hipStream_t s, const VoxelizeWs& w, int64_t n, const void* feat, int C, void* vfeat,
+                        int32_t* counts) {
     const int64_t threads = n * (C / VEC);
     const bool split = C / VEC <= kMeanLongThreads / 2;
     k_vox_mean<DT, VEC><<<blocks_for(threads, 256), 256, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat,
-                                                                 split ? kMeanRun : INT32_MAX, w.longv);
+                                                                 split ? kMeanRun : INT32_MAX, w.longv, counts);
     if (split) {
         const int64_t g = n < 1024 ? (n > 0 ? n : 1) : 1024;
         k_vox_mean_long<DT, VEC><<<(unsigned)g, kMeanLongThreads, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat,
@@ -306,35 +492,42 @@ static void launch_mean(hipStream_t s, const VoxelizeWs& w, int64_t n, const voi
     }
 }
 
+// counts: written from seg when given (nullptr: the caller counted N_m already)
 static void launch_mean_dt(hipStream_t s, const VoxelizeWs& w, int64_t cap, const void* feat, int C, int dt,
-                           void* vfeat) {
+                           void* vfeat, int32_t* counts) {
     const bool v16 = (dt != SPV_F32) && (C % 8 == 0), v32 = (dt == SPV_F32) && (C % 4 == 0);
     if (dt == SPV_F32) {
-        if (v32) launch_mean<SPV_F32, 4>(s, w, cap, feat, C, vfeat);
-        else launch_mean<SPV_F32, 1>(s, w, cap, feat, C, vfeat);
+        if (v32) launch_mean<SPV_F32, 4>(s, w, cap, feat, C, vfeat, counts);
+        else launch_mean<SPV_F32, 1>(s, w, cap, feat, C, vfeat, counts);
     } else if (dt == SPV_BF16) {
-        if (v16) launch_mean<SPV_BF16, 8>(s, w, cap, feat, C, vfeat);
-        else launch_mean<SPV_BF16, 1>(s, w, cap, feat, C, vfeat);
+        if (v16) launch_mean<SPV_BF16, 8>(s, w, cap, feat, C, vfeat, counts);
+        else launch_mean<SPV_BF16, 1>(s, w, cap, feat, C, vfeat, counts);
     } else {
-        if (v16) launch_mean<SPV_F16, 8>(s, w, cap, feat, C, vfeat);
-        else launch_mean<SPV_F16, 1>(s, w, cap, feat, C, vfeat);
+        if (v16) launch_mean<SPV_F16, 8>(s, w, cap, feat, C, vfeat, counts);
+        else launch_mean<SPV_F16, 1>(s, w, cap, feat, C, vfeat, counts);
     }
 }
 
 void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const int32_t* batch, int64_t n,
                      float voxel_size, const void* feat, int32_t C, int dt, int32_t* coords, void* vfeat,
-                     int32_t* counts, int32_t* pt2vox, int64_t* m_dev, bool table_cleared) {
-    if (!table_cleared) launch_clear(s, w.h, w.table, true);
-    const unsigned nins = n > 0 ? blocks_for(n, kAppendThreads) : 0u;
-    if (n > 0) k_vox_insert<<<nins, kAppendThreads, 0, s>>>(w.h, w.table, w.sort, w.pslot, xyz, batch, n, voxel_size);
-    launch_sort_keys(s, w.sort, &w.h->m, n, nins);
-    k_vox_rank<<<blocks_for(n, 256), 256, 0, s>>>(w.h, w.sort, w.table, coords, counts, w.fill, n, m_dev);
-    if (n == 0) return;
-    k_vox_lookup<<<blocks_for(n, 256), 256, 0, s>>>(w.table, w.pslot, n, pt2vox, counts);
-    if (!feat) return;
-    launch_exclusive_scan(s, counts, w.seg, &w.h->m, n, w.scan_tmp);
-    k_vox_fill<<<blocks_for(n, 256), 256, 0, s>>>(pt2vox, n, w.seg, w.fill, w.plist);
-    launch_mean_dt(s, w, n, feat, C, dt, vfeat);
+                     int32_t* counts, int32_t* pt2vox, int64_t* m_dev, const PackJob* jobs, int njobs) {
+    VoxFirst f;
+    f.h = w.h;
+    f.tkeys = w.table.keys;
+    f.nslots = w.table.mask + 1;
+    f.zero = w.rs.zero;  // the sort's histograms and tile counters
+    f.nzero = (int64_t)radix_zero_words(n);
+    f.njobs = 0;
+    for (int j = 0; j < njobs && f.njobs < kMaxPackJobs; ++j)
+        if (jobs[j].total > 0) f.job[f.njobs++] = jobs[j];
+    const unsigned nq = blocks_for(n, kRsProducerBlock);
+    k_vq_quantize<<<nq, kRsProducerBlock, 0, s>>>(f, xyz, batch, n, voxel_size, w.rs.ka, w.rs.rec);
+    launch_radix_sort(s, w.rs, w.h, nullptr, n, nq);
+    const int64_t nt = (int64_t)radix_tiles(n);
+    k_vq_segments<<<(unsigned)nt, kRsThreads, 0, s>>>(w.rs, w.h, w.table, n, nt, coords, pt2vox, w.seg, w.plist,
+                                                      m_dev);
+    if (feat) launch_mean_dt(s, w, n, feat, C, dt, vfeat, counts);
+    else k_vq_counts<<<blocks_for(n, 256), 256, 0, s>>>(w.h, n, w.seg, counts);
 }
 
 void launch_voxelize_onto(hipStream_t s, const VoxelizeWs& w, const int32_t* coords, const int64_t* m_dev,
@@ -349,7 +542,7 @@ void launch_voxelize_onto(hipStream_t s, const VoxelizeWs& w, const int32_t* coo
     if (!feat || m_cap == 0) return;
     launch_exclusive_scan(s, counts, w.seg, &w.h->m, m_cap, w.scan_tmp);
     if (n > 0) k_vox_fill<<<blocks_for(n, 256), 256, 0, s>>>(pt2vox, n, w.seg, w.fill, w.plist);
-    launch_mean_dt(s, w, m_cap, feat, C, dt, vfeat);
+    launch_mean_dt(s, w, m_cap, feat, C, dt, vfeat, nullptr);
 }
 
 }  // namespace spv

@@ -36,8 +36,8 @@ EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_voxelize_onto", "spv_pack
            "spv_sparse_conv_dgrad", "spv_wgrad_workspace_bytes", "spv_sparse_conv_wgrad",
            "spv_voxelize_backward",
            "spv_devoxelize_backward", "spv_devoxelize",
-           "spv_block_workspace_bytes", "spv_block", "spv_lookup", "spv_status_check", "spv_status_string",
-           "spv_last_hip_error")
+           "spv_block_workspace_bytes", "spv_block", "spv_lookup", "spv_voxel_lookup", "spv_conv_kernel",
+           "spv_block_conv_kernel", "spv_status_check", "spv_status_string", "spv_last_hip_error")
 
 
 class SpvError(RuntimeError):
@@ -105,6 +105,11 @@ def lib():
                                          i32, vp, vp, vp, i32, vp, i32]
         L.spv_block.argtypes = [vp, vp, sz, ct.POINTER(BlockParams), vp, vp, i64, vp, vp, vp]
         L.spv_lookup.argtypes = [vp, vp, sz, vp, vp, i64, vp, i64, vp]
+        L.spv_voxel_lookup.argtypes = [vp, vp, sz, i64, vp, i64, vp]
+        L.spv_conv_kernel.argtypes = [i32, i32, i32, i32, i64, i64, i64, i32]
+        L.spv_conv_kernel.restype = i32
+        L.spv_block_conv_kernel.argtypes = [i64, i32, i32]
+        L.spv_block_conv_kernel.restype = i32
         L.spv_status_check.argtypes = [vp, vp]
         L.spv_status_string.argtypes = [i32]
         L.spv_status_string.restype = ct.c_char_p
@@ -114,7 +119,8 @@ def lib():
                   "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_map_children", "spv_sparse_conv_up",
                   "spv_sparse_conv_dgrad", "spv_sparse_conv_wgrad",
                   "spv_voxelize_backward",
-                  "spv_devoxelize_backward", "spv_devoxelize", "spv_block", "spv_lookup", "spv_status_check"):
+                  "spv_devoxelize_backward", "spv_devoxelize", "spv_block", "spv_lookup", "spv_voxel_lookup",
+                  "spv_status_check"):
             getattr(L, f).restype = ct.c_int
         _lib = L
     return _lib
@@ -593,3 +599,22 @@ def spv_lookup(ws: Workspace, table_coords: torch.Tensor, qcoords: torch.Tensor,
                           _ptr(qcoords), q, _ptr(idx))
     _chk(st, "spv_lookup")
     return idx[:q]
+
+
+def spv_voxel_lookup(ws: Workspace, n: int, qcoords: torch.Tensor) -> torch.Tensor:
+    """Lookups in the table the last spv_voxelize(ws, ..., n points) built."""
+    q = qcoords.shape[0]
+    idx = torch.empty(max(q, 1), dtype=torch.int32, device=qcoords.device)
+    st = lib().spv_voxel_lookup(_stream(), ws.ptr, ws.nbytes, n, _ptr(qcoords), q, _ptr(idx))
+    _chk(st, "spv_voxel_lookup")
+    return idx[:q]
+
+
+def spv_conv_kernel(K3: int, Cin: int, Cout: int, dtype: torch.dtype, in_rows: int, m_out_cap: int,
+                    pair_cap: int, transposed: bool = False) -> int:
+    """Host query: 0 neighbour-table MFMA, 1 tile MFMA, 2 vector ALU, -1 rejected."""
+    return lib().spv_conv_kernel(K3, Cin, Cout, _DT[dtype], in_rows, m_out_cap, pair_cap, int(transposed))
+
+
+def spv_block_conv_kernel(n: int, C: int, dtype: torch.dtype) -> int:
+    return lib().spv_block_conv_kernel(n, C, _DT[dtype])

@@ -157,3 +157,47 @@ def test_host_side_validation_without_gpu():
     # workspace sizing is monotone and covers the block
     assert spv.spv_workspace_bytes(1000, 96) < spv.spv_workspace_bytes(100000, 96)
     assert spv.spv_block_workspace_bytes(121180, 96) > 100 * 1024 * 1024
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="libspv.so not built")
+def test_conv_kernel_choice_at_the_32bit_offset_bound():
+    """The conv's kernel is chosen once on the host: the neighbour-table kernel
+    only while its 32-bit buffer offsets cover the input rows (n * C * 2 bytes),
+    else the pairs path, whose plan builds the tile bounds it reads."""
+    import torch
+    from paper_2007_16100_amd import spv
+    bound = 0xFFFFE000
+    for C in (96, 256):
+        n_max = bound // (2 * C)  # largest row count the neighbour-table kernel addresses
+        assert spv.spv_block_conv_kernel(n_max, C, torch.bfloat16) == 0
+        assert spv.spv_block_conv_kernel(n_max + 1, C, torch.bfloat16) == 2  # 27 n pairs exceed 32 bits too
+        assert spv.spv_conv_kernel(27, C, C, torch.bfloat16, n_max, n_max, 27 * n_max) == 0
+        # too many input rows for either matrix-core kernel's 32-bit offsets: the vector-ALU kernel
+        assert spv.spv_conv_kernel(27, C, C, torch.bfloat16, n_max + 1, 1000, 27 * 1000) == 2
+    # the neighbour table itself: m_out * 27 * 4 bytes
+    m_max = bound // (27 * 4)
+    assert spv.spv_conv_kernel(27, 32, 32, torch.bfloat16, 1000, m_max, 0) == 0
+    assert spv.spv_conv_kernel(27, 32, 32, torch.bfloat16, 1000, m_max + 1, 0) == 1
+    # fp32 and K = 2 never take the table kernel; a sparse transposed map takes the tile kernel
+    assert spv.spv_conv_kernel(27, 32, 32, torch.float32, 1000, 1000, 27000) == 2
+    assert spv.spv_conv_kernel(8, 64, 128, torch.bfloat16, 1000, 600, 1000) == 1
+    assert spv.spv_conv_kernel(8, 128, 64, torch.bfloat16, 600, 1000, 1000, True) == 1
+    assert spv.spv_conv_kernel(27, 96, 96, torch.bfloat16, 1000, 1000, 27000, True) == 0  # dgrad of a submanifold map
+    assert spv.spv_conv_kernel(5, 32, 32, torch.bfloat16, 10, 10, 10) == -1
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="libspv.so not built")
+def test_workspace_alignment_and_voxel_lookup_validation():
+    from paper_2007_16100_amd import spv
+    L = spv.lib()
+    P = ct.c_void_p(16)
+    for ws in (ct.c_void_p(16), ct.c_void_p(256 + 64), None):  # misaligned or null: rejected before any launch
+        assert L.spv_voxel_lookup(None, ws, 1 << 30, 4, P, 4, P) == spv.SPV_ERR_INVALID_ARG
+        assert L.spv_kernel_map_nbr(None, ws, 1 << 30, P, None, 4, P) == spv.SPV_ERR_INVALID_ARG
+        assert L.spv_devoxelize_nbr(None, ws, 1 << 30, P, None, 4, P, P, 0, P, None, 4, ct.c_float(0.1), 0, P, 32,
+                                    None, 0, None, None, None, 0, P, 1) == spv.SPV_ERR_INVALID_ARG
+        assert L.spv_status_check(ws, None) == spv.SPV_ERR_INVALID_ARG
+    ws = ct.c_void_p(512)
+    assert L.spv_voxel_lookup(None, ws, 16, 4, P, 4, P) == spv.SPV_ERR_CAPACITY
+    assert L.spv_voxel_lookup(None, ws, 1 << 30, -1, P, 4, P) == spv.SPV_ERR_INVALID_ARG
+    assert L.spv_voxel_lookup(None, ws, 1 << 30, 4, None, 4, P) == spv.SPV_ERR_INVALID_ARG

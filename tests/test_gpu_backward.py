@@ -14,6 +14,7 @@ import torch
 
 import oracle
 from paper_2007_16100_amd import synth
+from tests import parity
 
 pytestmark = pytest.mark.gpu
 
@@ -81,14 +82,15 @@ def test_conv_dgrad(spv, sweep, kind, cin, cout, dtype, step):
     got = spv.spv_sparse_conv_dgrad(ws, dev(dy, dtype), dev(off), dev(pairs), dev(W, dtype), m_in, transposed=tr)
     ref = oracle.conv_dgrad(dy, off, pairs, W, m_in, dtype, transposed=tr)
     g = synth.from_storage(host(got, dtype)[:m_in], dtype)
-    e = normwise(g, synth.from_storage(ref, dtype))
-    assert e <= TOL[dtype], e
+    parity.check(g, synth.from_storage(ref, dtype), dtype)
 
 
 @pytest.mark.parametrize("kind,cin,cout,dtype,step", [
     ("subm", 32, 32, "bf16", 2), ("subm", 96, 96, "bf16", 4), ("subm", 64, 128, "f16", 4), ("subm", 16, 16, "f32", 8),
     ("subm", 256, 256, "bf16", 16), ("subm", 24, 40, "bf16", 8), ("k2s2", 64, 128, "bf16", 2),
-    ("k3s2", 32, 64, "bf16", 4), ("transposed", 128, 64, "bf16", 2)])
+    ("k3s2", 32, 64, "bf16", 4), ("transposed", 128, 64, "bf16", 2),
+    # pairs wider than 512 channels: past what the MFMA kernel gathers per pair
+    ("subm", 128, 512, "bf16", 16)])
 def test_conv_wgrad(spv, sweep, kind, cin, cout, dtype, step):
     rc, _, _, _ = oracle.voxelize(sweep[::step], 0.05)
     m_in, m_out, K3, tr, off, pairs = _map(rc, kind)
@@ -101,8 +103,8 @@ def test_conv_wgrad(spv, sweep, kind, cin, cout, dtype, step):
     again = host(spv.spv_sparse_conv_wgrad(*args, transposed=tr))
     np.testing.assert_array_equal(got, again)  # deterministic
     ref = oracle.conv_wgrad(x, dy, off, pairs, K3, dtype, transposed=tr)
-    e = normwise(got, ref)
-    assert e <= 1e-3, e
+    # fp32 results of up to ~10^5-term sums: 1e-3 normwise and elementwise
+    parity.check(got, ref, "f32", normwise_tol=1e-3, elemwise_tol=1e-3)
 
 
 @pytest.mark.parametrize("dtype,C", [("bf16", 96), ("f32", 8), ("f16", 5)])
@@ -126,5 +128,4 @@ def test_devoxelize_backward(spv, sweep, mode, stride_log2, C, dtype):
     dout = synth.normal((len(pts), C), 1107, dtype=dtype)
     got = host(spv.spv_devoxelize_backward(dev(ci), dev(cw), dev(dout, dtype), len(rc)))[: len(rc)]
     ref = oracle.devoxelize_backward(ci, cw, dout, len(rc), dtype)
-    e = normwise(got, ref)
-    assert e <= 1e-5, e
+    parity.check(got, ref, "f32")

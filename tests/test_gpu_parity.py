@@ -12,6 +12,8 @@ import torch
 import oracle
 from paper_2007_16100_amd import synth
 
+from tests import parity
+
 pytestmark = pytest.mark.gpu
 
 TOL = {"f32": 1e-5, "bf16": 2e-2, "f16": 2e-2}
@@ -49,18 +51,12 @@ def host(t, dtype=None):
 
 
 def normwise(g, r, dtype):
-    g = synth.from_storage(g, dtype).astype(np.float64)
-    r = synth.from_storage(r, dtype).astype(np.float64)
-    assert g.shape == r.shape
-    if r.size == 0:
-        return 0.0
-    return float(np.max(np.abs(g - r)) / max(np.max(np.abs(r)), 1e-30))
+    return parity.errors(synth.from_storage(g, dtype), synth.from_storage(r, dtype))[0]
 
 
-def check_close(g, r, dtype):
-    e = normwise(g, r, dtype)
-    assert e <= TOL[dtype], f"normwise error {e:.3e} > {TOL[dtype]}"
-    return e
+def check_close(g, r, dtype, kind="op"):
+    """Normwise and elementwise (99.9th percentile) bounds, both logged (tests/parity.py)."""
+    return parity.check(synth.from_storage(g, dtype), synth.from_storage(r, dtype), dtype, kind)
 
 
 # ---------------------------------------------------------------------------
@@ -297,6 +293,26 @@ def test_lookup(spv, sweep):
     table = {tuple(r): i for i, r in enumerate(rc)}
     expect = np.array([table.get(tuple(r), -1) for r in q], np.int32)
     np.testing.assert_array_equal(idx, expect)
+
+
+def test_voxel_lookup_on_the_voxelization_table(spv, sweep):
+    """The table spv_voxelize itself built, queried in place (no rebuild): every voxel,
+    neighbours present or absent, points of another batch and far-away coordinates."""
+    batch = (np.arange(len(sweep)) % 3 == 0).astype(np.int32)
+    rc, _, _, _ = oracle.voxelize(sweep, 0.05, batch=batch)
+    ws = spv.Workspace.for_ops(len(sweep), 16)
+    vox = spv.spv_voxelize(ws, dev(sweep), 0.05, None, dev(batch))
+    assert vox.m == len(rc)
+    rng = np.random.default_rng(5)
+    q = np.concatenate([rc, rc[rng.integers(0, len(rc), 30000)]]).copy()
+    q[len(rc)::2, 1:] += rng.integers(-1, 2, size=(15000, 3)).astype(np.int32)
+    q[len(rc) + 1::4, 0] = 2  # a batch with no points
+    q[-5:] = [[0, 32766, 0, 0], [0, -32767, 0, 0], [65534, 0, 0, 0], [0, 40000, 0, 0], [-1, 0, 0, 0]]
+    idx = host(spv.spv_voxel_lookup(ws, len(sweep), dev(q)))
+    table = {tuple(r): i for i, r in enumerate(rc)}
+    expect = np.array([table.get(tuple(r), -1) for r in q], np.int32)
+    np.testing.assert_array_equal(idx, expect)
+    np.testing.assert_array_equal(idx[: len(rc)], np.arange(len(rc), dtype=np.int32))
 
 
 # ---------------------------------------------------------------------------
@@ -627,7 +643,7 @@ def test_block(spv, cfg):
     out, m = spv.spv_block(ws, params, dev(xyz), dev(feat, dtype), sync=True)
     rout, rm = oracle.block(xyz, feat, v, convs, Wp, scp, shp, relu_p=True, dtype=dtype)
     assert m == rm
-    check_close(host(out, dtype)[:len(xyz)], rout, dtype)
+    check_close(host(out, dtype)[:len(xyz)], rout, dtype, kind="block")
 
 
 @pytest.mark.parametrize("mode", ["center", "corner", "nearest"])
@@ -669,7 +685,7 @@ def test_block_equals_stand_alone_ops(spv, sweep, mode, C):
     assert torch.equal(out[:len(xyz)].view(torch.int16), ref[:len(xyz)].view(torch.int16))
     rout, rm = oracle.block(xyz, feat, 0.05, convs, Wp, scp, shp, relu_p=True, dtype=dt, mode=mode)
     assert rm == m
-    check_close(host(out, dt)[:len(xyz)], rout, dt)
+    check_close(host(out, dt)[:len(xyz)], rout, dt, kind="block")
 
 
 @pytest.mark.parametrize("C,dtype,nconv", [(16, "f32", 1), (16, "f32", 2), (48, "bf16", 2), (96, "bf16", 2)])
@@ -692,7 +708,7 @@ def test_block_residual(spv, sweep, C, dtype, nconv):
     rout, rm = oracle.block(xyz, feat, v, convs, Wp, relu_p=True, dtype=dtype, residual=True)
     assert m == rm
     got = host(out, dtype)[:len(xyz)]
-    check_close(got, rout, dtype)
+    check_close(got, rout, dtype, kind="block")
     plain, _ = oracle.block(xyz, feat, v, convs, Wp, relu_p=True, dtype=dtype)
     diff = np.abs(synth.from_storage(rout, dtype) - synth.from_storage(plain, dtype)).max()
     assert diff > 0.05  # the identity branch matters here
@@ -938,6 +954,19 @@ def test_devoxelize_nbr_bad_voxel_index(spv):
     out = spv.spv_devoxelize_nbr(ws, coords, vf, nbr, p2v, xyz, 0.05)
     torch.cuda.synchronize()
     assert float(out[0].float().abs().max()) == 0.0 and float(out[1, 0]) == 1.0
+    # a live row count below the capacity: an entry past it (a row the map did not
+    # write) gives no corners either
+    assert vox.m == 2
+    p2v = vox.pt2vox.clone()
+    m_dev = torch.tensor([1], dtype=torch.int64, device=d)
+    coords_cap = torch.cat([coords, torch.zeros((6, 4), dtype=torch.int32, device=d)]).contiguous()
+    nbr_cap = torch.cat([nbr[: vox.m], torch.full((6, 27), 7, dtype=torch.int32, device=d)]).contiguous()
+    vf_cap = torch.ones((8, 32), dtype=torch.bfloat16, device=d)
+    out = spv.spv_devoxelize_nbr(ws, coords_cap, vf_cap, nbr_cap, p2v, xyz, 0.05, m_dev=m_dev, m_cap=8)
+    torch.cuda.synchronize()
+    row = int(p2v[1])
+    assert row >= 1  # the second point's voxel is past the live count
+    assert float(out[1].float().abs().max()) == 0.0
 
 
 # ---------------------------------------------------------------------------

@@ -13,6 +13,7 @@ import torch
 import oracle
 from oracle import spvcnn as ospvcnn
 from paper_2007_16100_amd import synth
+from tests import parity
 
 pytestmark = pytest.mark.gpu
 
@@ -87,3 +88,58 @@ def test_spvcnn_forward(spv, dtype, n_sweeps, stride):
                  / np.max(np.abs(synth.from_storage(tr["z3"], dtype))))
     print(f"  logits normwise error {err:.3e}; last fusion {zerr:.3e}", flush=True)
     assert err <= NET_TOL[dtype]
+    parity.check(g, r, dtype, kind="network", what=f"spvcnn {dtype} x{n_sweeps}/{stride}")
+
+
+def _golden_4sweeps():
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "spvcnn_4sweeps.txt")
+    g = {"strides": [], "samples": []}
+    with open(path) as f:
+        for line in f:
+            w = line.split()
+            if not w or w[0] == "#":
+                continue
+            if w[0] == "points":
+                g["points"] = int(w[1])
+            elif w[0] == "stride":
+                g["strides"].append((int(w[1]), int(w[3]), w[5]))
+            elif w[0] == "logits_maxabs":
+                g["maxabs"] = float(w[1])
+            elif w[0] in ("logits_sha256", "samples"):
+                continue
+            else:
+                g["samples"].append((int(w[0]), [int(x, 16) for x in w[1:]]))
+    return g
+
+
+def test_spvcnn_4sweeps_full_size(spv):
+    """The benchmarked forward itself: four full sweeps (seeds 1005-1008, batch index in
+    the key, bf16), as bench.py --spvcnn runs it, against the oracle's reference written
+    by tests/golden/make_spvcnn_4sweeps.py (the oracle takes ~20 minutes on one core, so
+    its results are stored): the coordinate sets of all five strides bit-exact (SHA-256 of
+    the whole arrays), and the logits at 1024 sampled points within the network bounds,
+    normalised by the largest logit of the whole oracle output."""
+    import hashlib
+    from paper_2007_16100_amd.spvcnn import SPVCNN
+    from tests.golden.make_spvcnn_4sweeps import inputs
+    g = _golden_4sweeps()
+    xyz, batch, feat, P = inputs()
+    assert len(xyz) == g["points"]
+    print(f"spvcnn 4 full sweeps n={len(xyz)}", flush=True)
+    net = SPVCNN(P, "bf16", 0.05)
+    gtr = {}
+    out = net.forward(torch.from_numpy(xyz).cuda(), _to_dev(feat, "bf16"), torch.from_numpy(batch).cuda(), trace=gtr)
+    torch.cuda.synchronize()
+    plan = gtr["plan"]
+    for s, (stride, m, sha) in enumerate(g["strides"]):
+        assert stride == 2 ** s and plan.m[s] == m, (stride, plan.m[s], m)
+        c = np.ascontiguousarray(plan.coords[s][:m].cpu().numpy(), dtype="<i4")
+        assert hashlib.sha256(c.tobytes()).hexdigest() == sha, f"stride {stride} coordinates differ"
+    got = _to_host(out, "bf16")[: len(xyz)]
+    assert np.isfinite(got).all()
+    idx = np.array([k for k, _ in g["samples"]])
+    ref = synth.from_storage(np.array([v for _, v in g["samples"]], np.uint16), "bf16").astype(np.float64)
+    parity.check(got[idx], ref, "bf16", kind="network", what="spvcnn 4 full sweeps (sampled)", scale=g["maxabs"])
+    # the whole output's scale agrees with the oracle's
+    assert abs(float(np.abs(got).max()) - g["maxabs"]) <= 2e-2 * g["maxabs"]

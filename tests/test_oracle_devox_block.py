@@ -239,3 +239,83 @@ def test_block_config1_dense_residual(oracle_lib):
     np.testing.assert_allclose(out, ref, rtol=1e-5, atol=1e-5)
     plain, _ = oracle_lib.block(xyz, feat, 0.1, [(W, None, None, True)], Wp, relu_p=True)
     assert np.abs(out - plain).max() > 1e-2  # the identity branch changes the result
+
+
+def _dense_block(xyz, feat, v, convs, Wp, scale_p, shift_p, relu_p, mutant=None):
+    """The block of any depth computed densely (Sec. 3.3, Fig. 2): numpy scatter-mean,
+    then per conv torch conv3d -> scale * . + shift -> ReLU on the active sites,
+    trilinear devoxelization as grid_sample ratio, point MLP act(scale_p * (f Wp) + shift_p),
+    sum.  mutant plants a mistake: "conv2_reads_input" feeds the second conv the
+    block's voxel input, "bn_swapped" applies the first conv's scale / shift to the second."""
+    q = dense_ref.quantize(xyz, v)
+    o = q.min(0) - 2
+    shape = q.max(0) - o + 3
+    idx = q - o
+    s = np.zeros((feat.shape[1],) + tuple(shape))
+    cnt = np.zeros(tuple(shape))
+    for k in range(len(q)):
+        s[:, idx[k, 0], idx[k, 1], idx[k, 2]] += feat[k]
+        cnt[idx[k, 0], idx[k, 1], idx[k, 2]] += 1
+    mask = cnt > 0
+    mean = np.where(mask, s / np.maximum(cnt, 1), 0.0)
+    cur = mean
+    for l, (W, sc, sh, relu) in enumerate(convs):
+        src = mean if (mutant == "conv2_reads_input" and l == 1) else cur
+        if mutant == "bn_swapped" and l == 1:
+            sc, sh = convs[0][1], convs[0][2]
+        w = torch.from_numpy(np.ascontiguousarray(W.reshape(3, 3, 3, *W.shape[1:]).transpose(4, 3, 0, 1, 2)))
+        y = F.conv3d(torch.from_numpy(src)[None], w, padding=1)[0].numpy()
+        if sc is not None:
+            y = y * sc.astype(np.float64)[:, None, None, None]
+        if sh is not None:
+            y = y + sh.astype(np.float64)[:, None, None, None]
+        if relu:
+            y = np.maximum(y, 0.0)
+        cur = y * mask  # submanifold: active sites only
+    a = (xyz / np.float32(v)).astype(np.float64) - 0.5 - o
+    gn = 2.0 * a / (np.array(shape, np.float64) - 1.0) - 1.0
+    grid = torch.from_numpy(gn[:, ::-1].copy()).reshape(1, 1, 1, -1, 3)
+    num = F.grid_sample(torch.from_numpy(cur)[None], grid, align_corners=True)[0, :, 0, 0].numpy()
+    den = F.grid_sample(torch.from_numpy(mask.astype(np.float64))[None, None], grid, align_corners=True)[0, 0, 0, 0]
+    devox = (num / den.numpy()[None]).T
+    mlp = feat @ Wp
+    if scale_p is not None:
+        mlp = mlp * scale_p.astype(np.float64)
+    if shift_p is not None:
+        mlp = mlp + shift_p.astype(np.float64)
+    if relu_p:
+        mlp = np.maximum(mlp, 0.0)
+    return devox + mlp
+
+
+def test_block_two_convs_folded_bn_dense(oracle_lib):
+    """The benchmark block's composition (two submanifold convs, each with folded BN and
+    ReLU; point MLP with BN and ReLU; fusion by addition) against the dense pipeline,
+    in fp32 on the tiny cube.  Planted mistakes in the dense pipeline (the second conv
+    reading the block input; the first conv's BN on the second) miss the oracle by far
+    more than the bound, so a slip of either kind in the oracle would fail this test."""
+    xyz = synth.uniform_cube(2000, 1.6, 1001)
+    C = 16
+    feat = synth.normal((2000, C), 1002)
+    convs = []
+    for l in range(2):
+        W = synth.conv_weight(27, C, C, 1010 + l, "f32")
+        sc, sh = synth.folded_bn(C, 1020 + l)
+        convs.append((W, sc, sh, True))
+    Wp = synth.linear_weight(C, C, 1004, "f32")
+    scp, shp = synth.folded_bn(C, 1030)
+    out, m = oracle_lib.block(xyz, feat, 0.1, convs, Wp, scale_p=scp, shift_p=shp, relu_p=True)
+    assert m == 1944
+    c64 = [(W.astype(np.float64), sc, sh, r) for W, sc, sh, r in convs]
+    args = (xyz, feat.astype(np.float64), 0.1, c64, Wp.astype(np.float64), scp, shp, True)
+    ref = _dense_block(*args)
+    np.testing.assert_allclose(out, ref, rtol=1e-5, atol=1e-5)
+    scale = np.abs(ref).max()
+    for mutant in ("conv2_reads_input", "bn_swapped"):
+        bad = _dense_block(*args, mutant=mutant)
+        assert np.abs(out - bad).max() > 100 * 1e-5 * scale, mutant
+    # the dense pipeline at depth one is the config-1 pipeline
+    one = _dense_block(xyz, feat.astype(np.float64), 0.1, [(c64[0][0], None, None, False)],
+                       Wp.astype(np.float64), None, None, True)
+    ref1 = _dense_block_config1(xyz, feat.astype(np.float64), 0.1, c64[0][0], Wp.astype(np.float64))
+    np.testing.assert_allclose(one, ref1, rtol=1e-12, atol=1e-12)
