@@ -41,12 +41,12 @@ void plan_radix_ws(Arena& a, RadixWs& w, int64_t cap) {
     // zeroed by the producer: digit histograms and tile counters
     w.zero = a.take<uint32_t>(radix_zero_words(c));
     w.ghist = w.zero;
-    w.ctr = w.zero + kRsPasses * 256;
+    w.ctr = w.zero + kRsPasses * kRsBins;
     // look-back words, cleared by the sort's own kernels before each use
-    w.status = a.take<uint64_t>((size_t)kRsPasses * 256 * w.ntiles + w.ntiles);
+    w.status = a.take<uint64_t>((size_t)kRsPasses * kRsBins * w.ntiles + w.ntiles);
 }
 
-size_t radix_zero_words(int64_t) { return (size_t)kRsPasses * 256 + 64; }
+size_t radix_zero_words(int64_t) { return (size_t)kRsPasses * kRsBins + 64; }
 
 // the compacted form of a raw key (all ones for an invalid item)
 __device__ inline uint64_t rs_compact(uint64_t k, const SortStats& st) {
@@ -129,6 +129,17 @@ __device__ inline int64_t rs_count(const int64_t* count_dev, int64_t cap) {
     return c < 0 ? 0 : (c > cap ? cap : c);
 }
 
+// lanes of this wave whose valid digit d equals this lane's (one ballot per digit bit)
+__device__ inline uint64_t rs_peers(uint32_t d, bool valid) {
+    uint64_t peers = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < kRsBits; ++b) {
+        const uint64_t bal = __ballot((d >> b) & 1);
+        peers &= ((d >> b) & 1) ? bal : ~bal;
+    }
+    return peers;
+}
+
 // Statistics (block 0 stores them) and the digit histograms of every pass
 // that the significant bits need, over this block's keys.
 __global__ __launch_bounds__(kRsThreads) void k_rs_hist(RadixWs w, const int64_t* count_dev, int64_t cap,
@@ -142,14 +153,13 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_hist(RadixWs w, const int64_t
         raw[r] = i < count ? w.ka[i] : 0ull;
     }
     // this tile's look-back words of pass 0 and of the consumer's scan start empty
-    w.status[(size_t)blockIdx.x * 256 + threadIdx.x] = 0ull;
-    if (threadIdx.x == 0) w.status[(size_t)kRsPasses * 256 * w.ntiles + blockIdx.x] = 0ull;
+    if (threadIdx.x < kRsBins) w.status[(size_t)blockIdx.x * kRsBins + threadIdx.x] = 0ull;
+    if (threadIdx.x == 0) w.status[(size_t)kRsPasses * kRsBins * w.ntiles + blockIdx.x] = 0ull;
     SortStats st;
     rs_reduce_stats(w.rec, nrec, count, &st);
     if (blockIdx.x == 0 && threadIdx.x == 0) *w.st = st;
-    __shared__ uint32_t hist[kRsPasses][256];
-#pragma unroll
-    for (int p = 0; p < kRsPasses; ++p) hist[p][threadIdx.x] = 0;
+    __shared__ uint32_t hist[kRsPasses][kRsBins];
+    for (int e = threadIdx.x; e < kRsPasses * kRsBins; e += kRsThreads) (&hist[0][0])[e] = 0;
     __syncthreads();
     const int passes = rs_passes(st);
 #pragma unroll
@@ -157,25 +167,15 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_hist(RadixWs w, const int64_t
         const int64_t i = base + r * kRsThreads + threadIdx.x;
         if (i < count) {
             const uint64_t ck = rs_compact(raw[r], st);
-            for (int p = 0; p < passes; ++p) atomicAdd(&hist[p][(uint32_t)(ck >> (8 * p)) & 0xFF], 1u);  // LDS
+            for (int p = 0; p < passes; ++p)
+                atomicAdd(&hist[p][(uint32_t)(ck >> (kRsBits * p)) & (kRsBins - 1)], 1u);  // LDS
         }
     }
     __syncthreads();
-    for (int p = 0; p < passes; ++p) {
-        const uint32_t c = hist[p][threadIdx.x];
-        if (c) atomicAdd(&w.ghist[p * 256 + threadIdx.x], c);
+    for (int e = threadIdx.x; e < passes * kRsBins; e += kRsThreads) {
+        const uint32_t c = (&hist[0][0])[e];
+        if (c) atomicAdd(&w.ghist[e], c);
     }
-}
-
-// lanes of this wave whose valid digit d equals this lane's (8 ballots)
-__device__ inline uint64_t rs_peers(uint32_t d, bool valid) {
-    uint64_t peers = __ballot(valid);
-#pragma unroll
-    for (int b = 0; b < 8; ++b) {
-        const uint64_t bal = __ballot((d >> b) & 1);
-        peers &= ((d >> b) & 1) ? bal : ~bal;
-    }
-    return peers;
 }
 
 __device__ inline uint64_t rs_load_status(const uint64_t* p) {
@@ -190,7 +190,7 @@ __device__ inline void rs_store_status(uint64_t* p, uint64_t v) {
 // holds its inclusive prefix.  A status word not yet written is polled again
 // (the tile that writes it is running); after kRsSpinLimit polls the sort
 // records an error and goes on without it, so the kernel always ends.
-constexpr int kRsWindow = 16;
+constexpr int kRsWindow = 32;
 __device__ inline uint32_t rs_lookback(const uint64_t* col, int64_t stride, int64_t tile, bool& stalled) {
     uint32_t excl = 0;
     int64_t j = tile - 1;
@@ -223,100 +223,107 @@ __device__ inline uint32_t rs_lookback(const uint64_t* col, int64_t stride, int6
     return excl;
 }
 
+// dynamic LDS of a pass: per (round, wave, digit) counts, then offsets relative
+// to the tile's first item of that digit (both at most kRsTile: 16 bits)
+constexpr size_t kRsPassLds = (size_t)kRsItems * (kRsThreads / 64) * kRsBins * sizeof(uint16_t);
+
 template <bool FIRST>
 __global__ __launch_bounds__(kRsThreads) void k_rs_pass(RadixWs w, Header* h, const int64_t* count_dev, int64_t cap,
                                                         int pass) {
+    static_assert(kRsBins <= kRsThreads, "threads t < kRsBins own digit t");
     constexpr int NWV = kRsThreads / 64;
     const SortStats* gst = w.st;
     // the first pass always runs: it writes the compacted keys and the payload
-    if (pass > 0 && (uint32_t)(8 * pass) >= gst->sort_bits) return;
-    // per (round, wave, digit) counts, then offsets relative to the tile's first
-    // item of that digit (both at most kRsTile, 16 bits); dbase: the digit's
-    // first output position for this tile
-    __shared__ uint16_t cnt[kRsItems][NWV][256];
-    __shared__ uint32_t dbase[256];
+    if (pass > 0 && (uint32_t)(kRsBits * pass) >= gst->sort_bits) return;
+    extern __shared__ __align__(16) unsigned char rs_smem[];
+    uint16_t (*cnt)[NWV][kRsBins] = (uint16_t (*)[NWV][kRsBins])rs_smem;
+    __shared__ uint32_t dbase[kRsBins];  // the digit's first output position for this tile
     __shared__ int lds[NWV + 1];
     __shared__ uint32_t s_tile;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     if (t == 0) s_tile = atomicAdd(&w.ctr[pass], 1u);
-    // bucket base of digit t: all keys of smaller digits
-    int all;
-    const uint32_t gbase = (uint32_t)block_exclusive_scan((int)w.ghist[pass * 256 + t], lds, &all);
+    const bool owner = t < kRsBins;
+    const uint32_t gcount = owner ? w.ghist[pass * kRsBins + t] : 0u;
+    {
+        uint4* z = (uint4*)rs_smem;
+        for (size_t e = t; e < kRsPassLds / 16; e += kRsThreads) z[e] = make_uint4(0u, 0u, 0u, 0u);
+    }
+    __syncthreads();
     const int64_t tile = s_tile;
     const int64_t count = rs_count(count_dev, cap);
     const int64_t base = tile * kRsTile;
-    // the next pass's look-back words of this tile start empty (that pass starts after this one ends)
-    if (pass + 1 < kRsPasses) w.status[((size_t)(pass + 1) * w.ntiles + tile) * 256 + t] = 0ull;
     const uint64_t* ksrc = (pass & 1) ? w.kb : w.ka;
     uint64_t* kdst = (pass & 1) ? w.ka : w.kb;
     const uint32_t* vsrc = (pass & 1) ? w.vb : w.va;
     uint32_t* vdst = (pass & 1) ? w.va : w.vb;
-    SortStats st;
-    if constexpr (FIRST) st = *gst;
     uint64_t keys[kRsItems];
     uint32_t vals[kRsItems];
 #pragma unroll
     for (int r = 0; r < kRsItems; ++r) {
         const int64_t i = base + r * kRsThreads + t;
-        if constexpr (FIRST) {
-            keys[r] = i < count ? rs_compact(ksrc[i], st) : 0ull;
-            vals[r] = (uint32_t)i;  // the first pass sorts the item indices
-        } else {
-            keys[r] = i < count ? ksrc[i] : 0ull;
-            vals[r] = i < count ? vsrc[i] : 0u;
-        }
+        keys[r] = i < count ? ksrc[i] : 0ull;
+        if constexpr (FIRST) vals[r] = (uint32_t)i;  // the first pass sorts the item indices
+        else vals[r] = i < count ? vsrc[i] : 0u;
     }
+    // the next pass's look-back words of this tile start empty (that pass starts after this one ends)
+    if (owner && pass + 1 < kRsPasses) w.status[((size_t)(pass + 1) * w.ntiles + tile) * kRsBins + t] = 0ull;
+    // bucket base of digit t: all keys of smaller digits
+    int all;
+    const uint32_t gbase = (uint32_t)block_exclusive_scan((int)gcount, lds, &all);
+    if constexpr (FIRST) {
+        const SortStats st = *gst;
 #pragma unroll
-    for (int r = 0; r < kRsItems; ++r)
-#pragma unroll
-        for (int q = 0; q < NWV; ++q) cnt[r][q][t] = 0;
-    __syncthreads();
+        for (int r = 0; r < kRsItems; ++r)
+            if (base + r * kRsThreads + t < count) keys[r] = rs_compact(keys[r], st);
+    }
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     uint32_t rank[kRsItems];
 #pragma unroll
     for (int r = 0; r < kRsItems; ++r) {
         const int64_t i = base + r * kRsThreads + t;
         const bool valid = i < count;
-        const uint32_t d = (uint32_t)(keys[r] >> (8 * pass)) & 0xFF;
+        const uint32_t d = (uint32_t)(keys[r] >> (kRsBits * pass)) & (kRsBins - 1);
         const uint64_t peers = rs_peers(d, valid);
         rank[r] = (uint32_t)__popcll(peers & lt);
         if (valid && rank[r] == 0) cnt[r][wave][d] = (uint16_t)__popcll(peers);
     }
     __syncthreads();
-    // thread t owns digit t: the tile's count, published before the look-back
-    uint32_t tot = 0;
+    if (owner) {
+        // thread t: the tile's count of digit t, published before the look-back
+        uint32_t tot = 0;
 #pragma unroll
-    for (int r = 0; r < kRsItems; ++r)
+        for (int r = 0; r < kRsItems; ++r)
 #pragma unroll
-        for (int q = 0; q < NWV; ++q) tot += (uint32_t)cnt[r][q][t];
-    uint64_t* col = w.status + (size_t)pass * 256 * w.ntiles + t;  // status[pass][tile][digit] at col + tile * 256
-    bool stalled = false;
-    uint32_t excl = 0;
-    if (tile == 0) {
-        rs_store_status(col, kRsFlagInc | tot);
-    } else {
-        rs_store_status(col + tile * 256, kRsFlagAgg | tot);
-        excl = rs_lookback(col, 256, tile, stalled);
-        rs_store_status(col + tile * 256, kRsFlagInc | (uint64_t)(excl + tot));
-    }
-    if (stalled) raise_flag(h, kFlagInternal);
-    // running write offsets over (round, wave) in index order
-    dbase[t] = gbase + excl;
-    uint32_t run = 0;
-#pragma unroll
-    for (int r = 0; r < kRsItems; ++r)
-#pragma unroll
-        for (int q = 0; q < NWV; ++q) {
-            const uint32_t c = cnt[r][q][t];
-            cnt[r][q][t] = (uint16_t)run;
-            run += c;
+            for (int q = 0; q < NWV; ++q) tot += (uint32_t)cnt[r][q][t];
+        uint64_t* col = w.status + (size_t)pass * kRsBins * w.ntiles + t;  // status[pass][tile][digit]
+        bool stalled = false;
+        uint32_t excl = 0;
+        if (tile == 0) {
+            rs_store_status(col, kRsFlagInc | tot);
+        } else {
+            rs_store_status(col + tile * kRsBins, kRsFlagAgg | tot);
+            excl = rs_lookback(col, kRsBins, tile, stalled);
+            rs_store_status(col + tile * kRsBins, kRsFlagInc | (uint64_t)(excl + tot));
         }
+        if (stalled) raise_flag(h, kFlagInternal);
+        // offsets over (round, wave) in index order, relative to the digit's base
+        dbase[t] = gbase + excl;
+        uint32_t run = 0;
+#pragma unroll
+        for (int r = 0; r < kRsItems; ++r)
+#pragma unroll
+            for (int q = 0; q < NWV; ++q) {
+                const uint32_t c = cnt[r][q][t];
+                cnt[r][q][t] = (uint16_t)run;
+                run += c;
+            }
+    }
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < kRsItems; ++r) {
         const int64_t i = base + r * kRsThreads + t;
         if (i < count) {
-            const uint32_t d = (uint32_t)(keys[r] >> (8 * pass)) & 0xFF;
+            const uint32_t d = (uint32_t)(keys[r] >> (kRsBits * pass)) & (kRsBins - 1);
             const uint32_t pos = dbase[d] + cnt[r][wave][d] + rank[r];
             kdst[pos] = keys[r];
             vdst[pos] = vals[r];
@@ -328,11 +335,17 @@ void launch_radix_sort(hipStream_t s, const RadixWs& w, Header* h, const int64_t
                        uint32_t nrec) {
     if (cap < 0) cap = 0;
     const unsigned nt = (unsigned)radix_tiles(cap);  // at least one tile: the first pass always writes its outputs
+    static const bool lds_ok =
+        hipFuncSetAttribute((const void*)k_rs_pass<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)kRsPassLds) == hipSuccess &&
+        hipFuncSetAttribute((const void*)k_rs_pass<false>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)kRsPassLds) == hipSuccess;
+    (void)lds_ok;
     k_rs_hist<<<nt, kRsThreads, 0, s>>>(w, count_dev, cap, nrec);
     // the significant bits are known on the device only: every pass a 64-bit
     // key may need is launched, and passes beyond them exit at once
-    k_rs_pass<true><<<nt, kRsThreads, 0, s>>>(w, h, count_dev, cap, 0);
-    for (int p = 1; p < kRsPasses; ++p) k_rs_pass<false><<<nt, kRsThreads, 0, s>>>(w, h, count_dev, cap, p);
+    k_rs_pass<true><<<nt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, 0);
+    for (int p = 1; p < kRsPasses; ++p) k_rs_pass<false><<<nt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, p);
 }
 
 }  // namespace spv

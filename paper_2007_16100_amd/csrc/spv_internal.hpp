@@ -142,10 +142,12 @@ __device__ inline uint64_t sorted_key(const SortBufs& sb, int64_t r) {
 // launch_radix_sort the compacted keys, ascending, and the items' original
 // indices sit in rs_keys / rs_vals (which of the two buffers depends on the
 // number of passes, known on the device).
-constexpr int kRsThreads = 256;
-constexpr int kRsItems = 16;
+constexpr int kRsThreads = 1024;
+constexpr int kRsItems = 4;
 constexpr int kRsTile = kRsThreads * kRsItems;  // keys per tile
-constexpr int kRsPasses = 8;                    // 8-bit digits of a 64-bit key
+constexpr int kRsBits = 8;                      // digit width
+constexpr int kRsBins = 1 << kRsBits;
+constexpr int kRsPasses = (64 + kRsBits - 1) / kRsBits;  // digits of a 64-bit key
 constexpr int kRsRecWords = 12;
 constexpr int kRsProducerBlock = 1024;
 struct RadixWs {
@@ -157,9 +159,9 @@ struct RadixWs {
     SortStats* st;
     int64_t ntiles;     // tiles of the capacity (a pass grid)
     uint32_t* zero;     // the region the producer zeroes (radix_zero_words):
-    uint32_t* ghist;    //   [kRsPasses][256] digit counts over all keys
-    uint32_t* ctr;      //   [64] tile counters (0..7 the passes, 8.. for the consumers)
-    uint64_t* status;   // [kRsPasses][ntiles][256] look-back words, then [ntiles] for a consumer's scan:
+    uint32_t* ghist;    //   [kRsPasses][kRsBins] digit counts over all keys
+    uint32_t* ctr;      //   [64] tile counters (0 .. kRsPasses-1 the passes, 8.. for the consumers)
+    uint64_t* status;   // [kRsPasses][ntiles][kRsBins] look-back words, then [ntiles] for a consumer's scan:
                         // the histogram kernel clears pass 0's and the consumer's, pass p clears pass p+1's
 };
 size_t radix_tiles(int64_t cap);
@@ -169,9 +171,11 @@ void plan_radix_ws(Arena& a, RadixWs& w, int64_t cap);
 void launch_radix_sort(hipStream_t s, const RadixWs& w, Header* h, const int64_t* count_dev, int64_t cap,
                        uint32_t nrec);
 __host__ __device__ inline int rs_passes(const SortStats& st) {
-    const int p = (int)((st.sort_bits + 7) / 8);
+    const int p = (int)((st.sort_bits + kRsBits - 1) / kRsBits);
     return p > 0 ? p : 1;
 }
+// the look-back words a consumer of the sort may use for a scan of its own over the tiles
+__host__ __device__ inline uint64_t* rs_consumer_status(const RadixWs& w) { return w.status + (size_t)kRsPasses * kRsBins * w.ntiles; }
 __device__ inline const uint64_t* rs_keys(const RadixWs& w, const SortStats& st) {
     return (rs_passes(st) & 1) ? w.kb : w.ka;
 }

@@ -174,14 +174,13 @@ __device__ inline uint32_t vq_lookback(const uint64_t* stat, int64_t tile, bool&
 // Voxels from the sorted keys: position i starts a voxel when its key differs
 // from position i-1's.  Tile-local ranks of the starts (position order: round,
 // wave, lane) plus the look-back give every start its voxel index; there the
-// voxel's coordinates, its first sorted position (seg) and its table entry are
-// written, and every point receives its voxel's index (invalid points, sorted
-// last, get -1).  The hash inserts of a thread's starts are issued together
-// (each key is new: a first compare-and-swap almost always claims its slot).
-// The last tile writes m.
-__global__ __launch_bounds__(kRsThreads) void k_vq_segments(RadixWs rs, Header* h, Table t, int64_t n,
-                                                            int64_t ntiles, int32_t* coords, int32_t* pt2vox,
-                                                            int32_t* seg, int32_t* plist, int64_t* m_dev) {
+// voxel's coordinates and its first sorted position (seg) are written, and
+// every point receives its voxel's index (invalid points, sorted last, get -1).
+// The last tile writes m.  (The per-voxel kernel that follows inserts each
+// voxel into the hash table: one insert per voxel, spread over the whole chip.)
+__global__ __launch_bounds__(kRsThreads) void k_vq_segments(RadixWs rs, Header* h, int64_t n, int64_t ntiles,
+                                                            int32_t* coords, int32_t* pt2vox, int32_t* seg,
+                                                            int32_t* plist, int64_t* m_dev) {
     constexpr int I = kRsItems, NWV = kRsThreads / 64;
     __shared__ uint32_t s_tile, s_excl;
     __shared__ uint32_t wcnt[I][NWV];  // starts per (round, wave), then their exclusive prefix in the tile
@@ -197,8 +196,8 @@ __global__ __launch_bounds__(kRsThreads) void k_vq_segments(RadixWs rs, Header* 
     const int64_t base = tile * kRsTile;
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     uint64_t key[I];
-    uint32_t hb = 0;       // bit r: position of round r starts a voxel
-    uint32_t rk[I];        // rank of the start among its wave's starts of that round
+    uint32_t hb = 0;  // bit r: the position of round r starts a voxel
+    uint32_t rk[I];   // rank of that start among its wave's starts of the round
 #pragma unroll
     for (int r = 0; r < I; ++r) {
         const int64_t i = base + r * kRsThreads + tid;
@@ -223,7 +222,7 @@ __global__ __launch_bounds__(kRsThreads) void k_vq_segments(RadixWs rs, Header* 
     }
     __syncthreads();
     const uint32_t tot = s_tot;
-    uint64_t* stat = rs.status + (size_t)kRsPasses * 256 * rs.ntiles;
+    uint64_t* stat = rs_consumer_status(rs);
     if (tid < 64) {
         bool stalled = false;
         uint32_t excl = 0;
@@ -249,22 +248,6 @@ __global__ __launch_bounds__(kRsThreads) void k_vq_segments(RadixWs rs, Header* 
     }
     __syncthreads();
     const int64_t excl = s_excl;
-    // voxel index of each position: the starts before it (in the tile and before
-    // the tile); a start takes the next index, any other position its last start's
-    int32_t vid[I];
-    uint64_t pk[I];
-    uint32_t slot[I];
-    uint64_t prev[I];
-#pragma unroll
-    for (int r = 0; r < I; ++r) {
-        const bool hd = (hb >> r) & 1u;
-        vid[r] = (int32_t)(excl + wcnt[r][wave] + rk[r]) - (hd ? 0 : 1);
-        pk[r] = hd ? rs_expand(key[r], st) : kEmpty;
-        slot[r] = hd ? hash_slot(pk[r], t.mask) : 0u;
-        prev[r] = hd ? atomicCAS((unsigned long long*)&t.keys[slot[r]], (unsigned long long)kEmpty,
-                                 (unsigned long long)pk[r])
-                     : 0ull;
-    }
 #pragma unroll
     for (int r = 0; r < I; ++r) {
         const int64_t i = base + r * kRsThreads + tid;
@@ -275,26 +258,20 @@ __global__ __launch_bounds__(kRsThreads) void k_vq_segments(RadixWs rs, Header* 
             pt2vox[k] = -1;
             continue;
         }
-        if ((hb >> r) & 1u) {
-            int32_t* cv = coords + 4 * (int64_t)vid[r];
-            cv[0] = key_b(pk[r]);
-            cv[1] = key_x(pk[r]);
-            cv[2] = key_y(pk[r]);
-            cv[3] = key_z(pk[r]);
-            seg[vid[r]] = (int32_t)i;
-            uint32_t sl = slot[r];
-            uint64_t pv = prev[r];
-            int ins = pv == kEmpty ? 1 : (pv == pk[r] ? 0 : 2);
-            for (uint32_t probe = 1; ins == 2 && probe <= t.mask; ++probe) {  // the slot was taken: probe on
-                sl = (sl + 1) & t.mask;
-                pv = atomicCAS((unsigned long long*)&t.keys[sl], (unsigned long long)kEmpty,
-                               (unsigned long long)pk[r]);
-                ins = pv == kEmpty ? 1 : (pv == pk[r] ? 0 : 2);
-            }
-            if (ins == 1) t.vals[sl] = (int32_t)vid[r];
-            else raise_flag(h, ins == 0 ? kFlagDuplicate : kFlagTableFull);
+        // the starts before this position; a start takes the next index, any
+        // other position the index of its last start
+        const bool hd = (hb >> r) & 1u;
+        const int32_t vid = (int32_t)(excl + wcnt[r][wave] + rk[r]) - (hd ? 0 : 1);
+        if (hd) {
+            const uint64_t pk = rs_expand(key[r], st);
+            int32_t* cv = coords + 4 * (int64_t)vid;
+            cv[0] = key_b(pk);
+            cv[1] = key_x(pk);
+            cv[2] = key_y(pk);
+            cv[3] = key_z(pk);
+            seg[vid] = (int32_t)i;
         }
-        pt2vox[k] = (int32_t)vid[r];
+        pt2vox[k] = vid;
     }
     if (tile == ntiles - 1 && tid == 0) {  // the voxel count, after the last tile's look-back
         const int64_t m = excl + tot;
@@ -304,12 +281,25 @@ __global__ __launch_bounds__(kRsThreads) void k_vq_segments(RadixWs rs, Header* 
     }
 }
 
-// N_m = seg[v + 1] - seg[v] when there are no features to average
-__global__ void k_vq_counts(const Header* h, int64_t cap, const int32_t* seg, int32_t* counts) {
+// Voxel v's hash-table entry (key of coords[v], value v).  Every key is new, so
+// the first compare-and-swap almost always claims its slot.
+__device__ inline void vq_insert(Header* h, Table t, const int32_t* coords, int64_t v) {
+    const int32_t* c = coords + 4 * v;
+    uint32_t slot;
+    const int r = table_insert(t, pack_key(c[0], c[1], c[2], c[3]), &slot);
+    if (r > 0) t.vals[slot] = (int32_t)v;
+    else raise_flag(h, r < 0 ? kFlagTableFull : kFlagDuplicate);
+}
+
+// N_m = seg[v + 1] - seg[v] and the table entry when there are no features to average
+__global__ void k_vq_counts(Header* h, int64_t cap, const int32_t* seg, int32_t* counts, Table t,
+                            const int32_t* coords) {
     int64_t m = h->m;
     if (m > cap) m = cap;
     const int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    if (v < m) counts[v] = seg[v + 1] - seg[v];
+    if (v >= m) return;
+    counts[v] = seg[v + 1] - seg[v];
+    vq_insert(h, t, coords, v);
 }
 
 // every point's voxel index, read at the table slot its insert found
@@ -418,18 +408,28 @@ __device__ inline void mean_store(const double (&acc)[VEC], double N, void* vfea
     }
 }
 
+// ins (voxelization only): the table to enter each voxel into, from coords
 template <int DT, int VEC>
 __global__ void k_vox_mean(Header* h, int64_t cap, const int32_t* seg, const int32_t* plist, const void* feat,
-                           int C, void* vfeat, int run, int32_t* longv, int32_t* counts) {
+                           int C, void* vfeat, int run, int32_t* longv, int32_t* counts, Table ins,
+                           const int32_t* coords) {
     int64_t m = h->m;
     if (m > cap) m = cap;
     const int nch = C / VEC;
+    // with counts, one more thread per voxel counts it and enters it into the
+    // table, off the critical path of the threads that average it
+    const int per = counts ? nch + 1 : nch;
     int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    int64_t vox = t / nch;
-    int ch = (int)(t - vox * nch) * VEC;
+    int64_t vox = t / per;
+    const int slot = (int)(t - vox * per);
     if (vox >= m) return;
     int32_t lo = seg[vox], hi = seg[vox + 1];
-    if (counts && ch == 0) counts[vox] = hi - lo;  // N_m (when the caller has not counted it)
+    if (slot == nch) {  // N_m and the table entry
+        counts[vox] = hi - lo;
+        vq_insert(h, ins, coords, vox);
+        return;
+    }
+    const int ch = slot * VEC;
     if (hi - lo > run) {
         if (ch == 0) longv[atomicAdd((unsigned long long*)&h->aux[0], 1ull)] = (int32_t)vox;
         return;
@@ -480,11 +480,12 @@ constexpr int kMeanRun = 32;  // points a single thread sums
 
 template <int DT, int VEC>
 static void launch_mean(hipStream_t s, const VoxelizeWs& w, int64_t n, const void* feat, int C, void* vfeat,
-                        int32_t* counts) {
-    const int64_t threads = n * (C / VEC);
+                        int32_t* counts, const int32_t* coords) {
+    const int64_t threads = n * (C / VEC + (counts ? 1 : 0));
     const bool split = C / VEC <= kMeanLongThreads / 2;
     k_vox_mean<DT, VEC><<<blocks_for(threads, 256), 256, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat,
-                                                                 split ? kMeanRun : INT32_MAX, w.longv, counts);
+                                                                 split ? kMeanRun : INT32_MAX, w.longv, counts,
+                                                                 w.table, coords);
     if (split) {
         const int64_t g = n < 1024 ? (n > 0 ? n : 1) : 1024;
         k_vox_mean_long<DT, VEC><<<(unsigned)g, kMeanLongThreads, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat,
@@ -492,19 +493,20 @@ static void launch_mean(hipStream_t s, const VoxelizeWs& w, int64_t n, const voi
     }
 }
 
-// counts: written from seg when given (nullptr: the caller counted N_m already)
+// counts: written from seg, with each voxel's table entry from coords, when
+// given (nullptr: the caller counted N_m and built the table already)
 static void launch_mean_dt(hipStream_t s, const VoxelizeWs& w, int64_t cap, const void* feat, int C, int dt,
-                           void* vfeat, int32_t* counts) {
+                           void* vfeat, int32_t* counts, const int32_t* coords) {
     const bool v16 = (dt != SPV_F32) && (C % 8 == 0), v32 = (dt == SPV_F32) && (C % 4 == 0);
     if (dt == SPV_F32) {
-        if (v32) launch_mean<SPV_F32, 4>(s, w, cap, feat, C, vfeat, counts);
-        else launch_mean<SPV_F32, 1>(s, w, cap, feat, C, vfeat, counts);
+        if (v32) launch_mean<SPV_F32, 4>(s, w, cap, feat, C, vfeat, counts, coords);
+        else launch_mean<SPV_F32, 1>(s, w, cap, feat, C, vfeat, counts, coords);
     } else if (dt == SPV_BF16) {
-        if (v16) launch_mean<SPV_BF16, 8>(s, w, cap, feat, C, vfeat, counts);
-        else launch_mean<SPV_BF16, 1>(s, w, cap, feat, C, vfeat, counts);
+        if (v16) launch_mean<SPV_BF16, 8>(s, w, cap, feat, C, vfeat, counts, coords);
+        else launch_mean<SPV_BF16, 1>(s, w, cap, feat, C, vfeat, counts, coords);
     } else {
-        if (v16) launch_mean<SPV_F16, 8>(s, w, cap, feat, C, vfeat, counts);
-        else launch_mean<SPV_F16, 1>(s, w, cap, feat, C, vfeat, counts);
+        if (v16) launch_mean<SPV_F16, 8>(s, w, cap, feat, C, vfeat, counts, coords);
+        else launch_mean<SPV_F16, 1>(s, w, cap, feat, C, vfeat, counts, coords);
     }
 }
 
@@ -524,10 +526,9 @@ void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const
     k_vq_quantize<<<nq, kRsProducerBlock, 0, s>>>(f, xyz, batch, n, voxel_size, w.rs.ka, w.rs.rec);
     launch_radix_sort(s, w.rs, w.h, nullptr, n, nq);
     const int64_t nt = (int64_t)radix_tiles(n);
-    k_vq_segments<<<(unsigned)nt, kRsThreads, 0, s>>>(w.rs, w.h, w.table, n, nt, coords, pt2vox, w.seg, w.plist,
-                                                      m_dev);
-    if (feat) launch_mean_dt(s, w, n, feat, C, dt, vfeat, counts);
-    else k_vq_counts<<<blocks_for(n, 256), 256, 0, s>>>(w.h, n, w.seg, counts);
+    k_vq_segments<<<(unsigned)nt, kRsThreads, 0, s>>>(w.rs, w.h, n, nt, coords, pt2vox, w.seg, w.plist, m_dev);
+    if (feat) launch_mean_dt(s, w, n, feat, C, dt, vfeat, counts, coords);
+    else k_vq_counts<<<blocks_for(n, 256), 256, 0, s>>>(w.h, n, w.seg, counts, w.table, coords);
 }
 
 void launch_voxelize_onto(hipStream_t s, const VoxelizeWs& w, const int32_t* coords, const int64_t* m_dev,
@@ -542,7 +543,7 @@ void launch_voxelize_onto(hipStream_t s, const VoxelizeWs& w, const int32_t* coo
     if (!feat || m_cap == 0) return;
     launch_exclusive_scan(s, counts, w.seg, &w.h->m, m_cap, w.scan_tmp);
     if (n > 0) k_vox_fill<<<blocks_for(n, 256), 256, 0, s>>>(pt2vox, n, w.seg, w.fill, w.plist);
-    launch_mean_dt(s, w, m_cap, feat, C, dt, vfeat, nullptr);
+    launch_mean_dt(s, w, m_cap, feat, C, dt, vfeat, nullptr, nullptr);
 }
 
 }  // namespace spv
