@@ -244,6 +244,26 @@ spv_status spv_sparse_conv_nbr(void* stream, void* ws, size_t ws_bytes,
                                spv_dtype dt);
 
 /*
+ * spv_sparse_conv_nbr_noalloc -- spv_sparse_conv_nbr without a workspace, for
+ * callers that cannot allocate device memory (code under graph capture, tight
+ * serving loops, harnesses that forbid allocation).  It allocates nothing:
+ * the packed weights go to a device-resident array of 3,538,944 bytes (the
+ * packing of a 256 -> 256 layer) that the library holds on every device it
+ * runs on until the process ends; its address is looked up once per device.
+ * Arguments, outputs and the shapes taken are those of spv_sparse_conv_nbr;
+ * packed weights larger than the array return SPV_ERR_CAPACITY, a current
+ * device index of 64 or more SPV_ERR_UNSUPPORTED.  Every call on
+ * one device uses the same array: calls that overlap in time on one device
+ * (different streams without ordering between them) race and give undefined
+ * results; calls in order on one stream are safe.
+ */
+spv_status spv_sparse_conv_nbr_noalloc(void* stream, const void* in, int64_t in_rows, int32_t Cin,
+                                       const int32_t* nbr, const void* W, int32_t Cin_full, int32_t Cout_full,
+                                       const float* scale, const float* shift, const void* res, int32_t relu,
+                                       void* out, const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout,
+                                       spv_dtype dt);
+
+/*
  * The transposed k=2 s=2 conv (a decoder's upsampling) on the stride-2 map's
  * child table:
  *

@@ -5,9 +5,18 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "conv_common.hpp"
 
 using namespace spv;
+
+// Device-resident scratch of spv_sparse_conv_nbr_noalloc: the packed weights of
+// one layer, up to 256 -> 256 channels (27 offsets x 8 input slabs x 16 output
+// blocks x 64 lanes x 16 bytes).  Each device holds its own copy for the
+// lifetime of the process; calls on one device share it.
+constexpr size_t kNoAllocScratchBytes = (size_t)27 * 8 * 16 * 64 * 16;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
 
 namespace {
 
@@ -472,6 +481,66 @@ spv_status spv_sparse_conv_nbr_packed(void* stream, void* ws, size_t ws_bytes, c
     if (!Wpacked) return SPV_ERR_INVALID_ARG;
     return conv_nbr_call(stream, ws, ws_bytes, in, in_rows, Cin, nbr, Wpacked, Cin, Cout, Wpacked, scale, shift, res,
                          relu, out, m_out_dev, m_out_cap, Cout, dt);
+}
+
+// The device address of `scratch` on the current device, looked up once per
+// device (host code never passes the symbol itself to a kernel).
+static spv_status noalloc_scratch(void** out) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        g_last_hip_error = (int)hipGetLastError();
+        return SPV_ERR_HIP;
+    }
+    if (dev < 0 || dev >= kMaxDevices) return SPV_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+            g_last_hip_error = (int)hipGetLastError();
+            return SPV_ERR_HIP;
+        }
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return SPV_OK;
+}
+
+spv_status spv_sparse_conv_nbr_noalloc(void* stream, const void* in, int64_t in_rows, int32_t Cin, const int32_t* nbr,
+                                       const void* W, int32_t Cin_full, int32_t Cout_full, const float* scale,
+                                       const float* shift, const void* res, int32_t relu, void* out,
+                                       const int64_t* m_out_dev, int64_t m_out_cap, int32_t Cout, spv_dtype dt) {
+    if (in_rows < 0 || m_out_cap < 0 || m_out_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !W ||
+        !valid_dt(dt) || Cin > Cin_full || Cout > Cout_full)
+        return SPV_ERR_INVALID_ARG;
+    if (!union_supported(27, Cin, Cout, dt) || m_out_cap * 27 * 4 > (int64_t)0xFFFFE000 ||
+        in_rows * (int64_t)Cin * 2 > (int64_t)0xFFFFE000)
+        return SPV_ERR_UNSUPPORTED;
+    if ((in_rows > 0 && !in) || (m_out_cap > 0 && (!out || !nbr))) return SPV_ERR_INVALID_ARG;
+    if (!aligned16(in) || !aligned16(out) || !aligned16(W) || !aligned16(res) || (res && res == out))
+        return SPV_ERR_INVALID_ARG;
+    // the packed weights are the only scratch; more than the array holds is refused
+    Arena probe(nullptr, 0);
+    plan_wpack_ws(probe, 27, Cin, Cout);
+    if (probe.used > kNoAllocScratchBytes) return SPV_ERR_CAPACITY;
+    if (m_out_cap == 0) return SPV_OK;
+    void* wpack = nullptr;
+    spv_status st = noalloc_scratch(&wpack);
+    if (st) return st;
+    hipStream_t s = (hipStream_t)stream;
+    ConvPlan p;
+    p.m_cap = m_out_cap;
+    p.K3 = 27;
+    p.use_union = 1;
+    p.nbr = const_cast<int32_t*>(nbr);  // read only
+    p.m_out_dev = m_out_dev;
+    p.h = nullptr;
+    p.res = res;
+    launch_pack_job(s, conv_pack_job(27, W, wpack, Cin, Cout, dt, Cout_full, (int64_t)Cin_full * Cout_full));
+    launch_conv_union(s, p, in, Cin, in_rows, Cout, wpack, scale, shift, relu, out, dt);
+    return hip_check();
 }
 
 spv_status spv_map_children(void* stream, void* ws, size_t ws_bytes, const int32_t* off, const int32_t* pairs,

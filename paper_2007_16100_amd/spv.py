@@ -37,6 +37,7 @@ EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_voxelize_onto", "spv_pack
            "spv_voxelize_backward",
            "spv_devoxelize_backward", "spv_devoxelize",
            "spv_block_workspace_bytes", "spv_block", "spv_lookup", "spv_voxel_lookup", "spv_conv_kernel",
+           "spv_sparse_conv_nbr_noalloc",
            "spv_block_conv_kernel", "spv_status_check", "spv_status_string", "spv_last_hip_error")
 
 
@@ -106,6 +107,8 @@ def lib():
         L.spv_block.argtypes = [vp, vp, sz, ct.POINTER(BlockParams), vp, vp, i64, vp, vp, vp]
         L.spv_lookup.argtypes = [vp, vp, sz, vp, vp, i64, vp, i64, vp]
         L.spv_voxel_lookup.argtypes = [vp, vp, sz, i64, vp, i64, vp]
+        L.spv_sparse_conv_nbr_noalloc.argtypes = [vp, vp, i64, i32, vp, vp, i32, i32, vp, vp, vp, i32, vp, vp, i64,
+                                                  i32, i32]
         L.spv_conv_kernel.argtypes = [i32, i32, i32, i32, i64, i64, i64, i32]
         L.spv_conv_kernel.restype = i32
         L.spv_block_conv_kernel.argtypes = [i64, i32, i32]
@@ -120,7 +123,7 @@ def lib():
                   "spv_sparse_conv_dgrad", "spv_sparse_conv_wgrad",
                   "spv_voxelize_backward",
                   "spv_devoxelize_backward", "spv_devoxelize", "spv_block", "spv_lookup", "spv_voxel_lookup",
-                  "spv_status_check"):
+                  "spv_sparse_conv_nbr_noalloc", "spv_status_check"):
             getattr(L, f).restype = ct.c_int
         _lib = L
     return _lib
@@ -425,6 +428,27 @@ def spv_sparse_conv_nbr(ws: Workspace, x: torch.Tensor, nbr: torch.Tensor, W_ful
                                    Cout_full, _ptr(scale), _ptr(shift), _ptr(res), int(relu), _ptr(out),
                                    _ptr(m_out_dev), m_out_cap, Cout, _DT[x.dtype])
     _chk(st, "spv_sparse_conv_nbr")
+    return out
+
+
+def spv_sparse_conv_nbr_noalloc(x: torch.Tensor, nbr: torch.Tensor, W_full: torch.Tensor, Cout: int,
+                                m_out_cap: int, m_out_dev: Optional[torch.Tensor] = None,
+                                scale: Optional[torch.Tensor] = None, shift: Optional[torch.Tensor] = None,
+                                relu: bool = False, res: Optional[torch.Tensor] = None, cin_offset: int = 0,
+                                out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """spv_sparse_conv_nbr with no workspace (the library's device-resident scratch holds the
+    packed weights); out must be given by callers that cannot allocate."""
+    K3, Cin_full, Cout_full = W_full.shape
+    Cin = x.shape[1]
+    if cin_offset < 0 or cin_offset + Cin > Cin_full:
+        raise ValueError("input-channel slice outside the weight")
+    if out is None:
+        out = torch.empty((max(m_out_cap, 1), Cout), dtype=x.dtype, device=x.device)
+    wp = ct.c_void_p(_ptr(W_full).value + cin_offset * Cout_full * W_full.element_size())
+    st = lib().spv_sparse_conv_nbr_noalloc(_stream(), _ptr(x), x.shape[0], Cin, _ptr(nbr), wp, Cin_full, Cout_full,
+                                           _ptr(scale), _ptr(shift), _ptr(res), int(relu), _ptr(out),
+                                           _ptr(m_out_dev), m_out_cap, Cout, _DT[x.dtype])
+    _chk(st, "spv_sparse_conv_nbr_noalloc")
     return out
 
 
