@@ -125,9 +125,7 @@ size_t layout_devox(void* ws, size_t bytes, int64_t m_cap, int64_t n, int C, int
     Arena a(ws, bytes);
     L.h = a.take<Header>(1);
     uint32_t S = table_capacity(m_cap > 0 ? m_cap : 1);
-    L.t.keys = a.take<uint64_t>(S);
-    L.t.vals = a.take<int32_t>(S);
-    L.t.mask = S - 1;
+    L.t = take_table(a, S);
     L.wpack = plan_devox_ws(a, C, Cp);
     int64_t nn = n > 0 ? n : 1;
     L.cidx = a.take<int32_t>(8 * nn);
@@ -306,12 +304,11 @@ spv_status spv_lookup(void* stream, void* ws, size_t ws_bytes, const int32_t* ta
     Arena probe(nullptr, 0);
     probe.take<Header>(1);
     uint32_t S = table_capacity(m_cap > 0 ? m_cap : 1);
-    probe.take<uint64_t>(S);
-    probe.take<int32_t>(S);
+    take_table(probe, S);
     if (need(probe.used, ws_bytes)) return SPV_ERR_CAPACITY;
     Arena a(ws, ws_bytes);
     Header* h = a.take<Header>(1);
-    Table t{a.take<uint64_t>(S), a.take<int32_t>(S), S - 1};
+    Table t = take_table(a, S);
     hipStream_t s = (hipStream_t)stream;
     launch_clear(s, h, t, true);
     if (m_cap > 0) launch_table_build(s, h, t, table_coords, m_dev, m_cap);
@@ -782,8 +779,7 @@ spv_status spv_devoxelize_nbr(void* stream, void* ws, size_t ws_bytes, const int
     if (!devox_mfma_supported(C, cp, dt)) return SPV_ERR_UNSUPPORTED;
     Arena probe(nullptr, 0);
     probe.take<Header>(1);
-    probe.take<uint64_t>(4);
-    probe.take<int32_t>(4);
+    take_table(probe, 4);
     void* wp_probe = plan_devox_ws(probe, C, cp);
     (void)wp_probe;
     if (need(probe.used, ws_bytes)) return SPV_ERR_CAPACITY;
@@ -791,7 +787,7 @@ spv_status spv_devoxelize_nbr(void* stream, void* ws, size_t ws_bytes, const int
     Header* h = ar.take<Header>(1);
     // an empty 4-slot table: the kernel's probe for a corner outside the point's
     // 3x3x3 neighbourhood (not reached when pt2vox is the grid's own) finds nothing
-    Table t{ar.take<uint64_t>(4), ar.take<int32_t>(4), 3};
+    Table t = take_table(ar, 4);
     void* wpack = plan_devox_ws(ar, C, cp);
     hipStream_t s = (hipStream_t)stream;
     launch_clear(s, h, t, true);

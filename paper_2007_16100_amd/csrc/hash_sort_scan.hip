@@ -8,7 +8,7 @@ namespace spv {
 // ---------------------------------------------------------------------------
 // table clear / build / lookup
 // ---------------------------------------------------------------------------
-__global__ void k_clear(Header* h, uint64_t* keys, uint32_t nslots, int clear_header, int64_t* zero64) {
+__global__ void k_clear(Header* h, Table t, int clear_header, int64_t* zero64) {
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         if (clear_header) {
             h->status = 0;
@@ -17,16 +17,18 @@ __global__ void k_clear(Header* h, uint64_t* keys, uint32_t nslots, int clear_he
         }
         if (zero64) *zero64 = 0;
     }
-    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < nslots; i += gridDim.x * blockDim.x) keys[i] = kEmpty;
+    const uint32_t nkw = t.keys ? (t.mask + 1) / 2 : 0;  // 16-byte runs of keys: 2 per bucket
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < nkw; i += gridDim.x * blockDim.x)
+        *(u64x2*)(t.keys + 8 * (size_t)(i >> 1) + 2 * (i & 1)) = u64x2{kEmpty, kEmpty};
 }
 
 void launch_clear(hipStream_t s, Header* h, Table t, bool clear_header, int64_t* zero64) {
     uint32_t n = t.mask + 1;
     unsigned g = blocks_for(n, 256 * 4);
-    k_clear<<<g, 256, 0, s>>>(h, t.keys, n, clear_header ? 1 : 0, zero64);
+    k_clear<<<g, 256, 0, s>>>(h, t, clear_header ? 1 : 0, zero64);
 }
 
-void launch_clear_header(hipStream_t s, Header* h) { k_clear<<<1, 64, 0, s>>>(h, nullptr, 0, 1, nullptr); }
+void launch_clear_header(hipStream_t s, Header* h) { k_clear<<<1, 64, 0, s>>>(h, Table{nullptr, 0}, 1, nullptr); }
 
 __device__ inline bool coord_ok(const int32_t* c) {
     return c[0] >= 0 && c[0] <= kBatchMax && c[1] >= kCoordMin && c[1] <= kCoordMax && c[2] >= kCoordMin &&
@@ -54,7 +56,7 @@ __global__ void k_table_build(Header* h, Table t, const int32_t* coords, const i
         } else if (r == 0) {
             raise_flag(h, kFlagDuplicate);
         } else {
-            t.vals[slot] = (int32_t)i;
+            *slot_val(t, slot) = (int32_t)i;
         }
     }
 }

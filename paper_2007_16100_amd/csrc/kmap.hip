@@ -28,26 +28,23 @@
 namespace spv {
 
 constexpr int kMapThreads = 256;
-constexpr int kNbrVox = 64;  // output voxels per block of the 3x3x3 passes (one per lane)
-constexpr int kNbrProbes = 7;  // offsets per wave: wave w takes k = w, w + 4, ..., < 27
+constexpr int kNbrVox = 64;    // output voxels per block of the 3x3x3 passes (one per lane)
+constexpr int kNbrWaves = 8;   // waves per block of the 3x3x3 passes
+constexpr int kNbrProbes = 4;  // offsets per wave: wave w takes k = w, w + 8, ..., < 27
 
 void plan_kmap_ws(Arena& a, KmapWs& w, int64_t m_cap, int K, int stride, bool own_fine_table, bool own_nbr) {
     int64_t mc = m_cap > 0 ? m_cap : 1;
     const int K3 = K * K * K;
     if (own_fine_table) {
         uint32_t S = table_capacity(mc);
-        w.fine.keys = a.take<uint64_t>(S);
-        w.fine.vals = a.take<int32_t>(S);
-        w.fine.mask = S - 1;
+        w.fine = take_table(a, S);
     }
     if (stride == 2) {
         uint32_t S = table_capacity(mc);
-        w.coarse.keys = a.take<uint64_t>(S);
-        w.coarse.vals = a.take<int32_t>(S);
-        w.coarse.mask = S - 1;
+        w.coarse = take_table(a, S);
         plan_sort_ws(a, w.sort, mc);
     } else {
-        w.coarse = Table{nullptr, nullptr, 0};
+        w.coarse = Table{nullptr, 0};
     }
     size_t nblk = blocks_for(mc, K == 3 ? kNbrVox : kMapThreads);
     w.bcnt = a.take<uint32_t>(K3 * nblk);
@@ -132,7 +129,7 @@ __global__ void k_map_coarse_rank(SortBufs sb, Table coarse, const int64_t* cnt,
     if (r >= m) return;
     uint64_t key = sorted_key(sb, r);
     int64_t slot = table_slot(coarse, key);
-    if (slot >= 0) coarse.vals[slot] = (int32_t)r;
+    if (slot >= 0) *slot_val(coarse, (uint32_t)slot) = (int32_t)r;
     out_coords[4 * r + 0] = key_b(key);
     out_coords[4 * r + 1] = key_x(key);
     out_coords[4 * r + 2] = key_y(key);
@@ -211,7 +208,7 @@ __global__ __launch_bounds__(kMapThreads) void k_s2_write(Header* h, Table coars
 // The block's 64 rows of the table are assembled in LDS and written out as one
 // contiguous run.
 template <bool S2>
-__global__ __launch_bounds__(256) void k_map_nbr3(Table fine, const int32_t* coords, const int64_t* m_out,
+__global__ __launch_bounds__(64 * kNbrWaves) void k_map_nbr3(Table fine, const int32_t* coords, const int64_t* m_out,
                                                   int64_t cap, int32_t* nbr, uint32_t* bcnt) {
     __shared__ int32_t tile[kNbrVox * 27];  // row stride 27 words: conflict-free per-lane writes
     const int lane = threadIdx.x & 63;
@@ -229,7 +226,7 @@ __global__ __launch_bounds__(256) void k_map_nbr3(Table fine, const int32_t* coo
     int32_t res[kNbrProbes];
 #pragma unroll
     for (int q = 0; q < kNbrProbes; ++q) {
-        const int k = wave + 4 * q;
+        const int k = wave + kNbrWaves * q;
         int dx, dy, dz;
         offset_delta<3>(k, dx, dy, dz);
         if constexpr (S2) {
@@ -246,7 +243,7 @@ __global__ __launch_bounds__(256) void k_map_nbr3(Table fine, const int32_t* coo
     const uint32_t nblk = gridDim.x;
 #pragma unroll
     for (int q = 0; q < kNbrProbes; ++q) {
-        const int k = wave + 4 * q;
+        const int k = wave + kNbrWaves * q;
         if (k >= 27) break;
         const int32_t i = (!S2 && k == 13) ? (int32_t)j : res[q];
         const bool present = valid && i >= 0;
@@ -263,7 +260,7 @@ __global__ __launch_bounds__(256) void k_map_nbr3(Table fine, const int32_t* coo
 }
 
 // pass 2 of a submanifold 3x3x3 map: pairs from the neighbour table
-__global__ __launch_bounds__(256) void k_map_pairs3(Header* h, const int32_t* nbr, const int64_t* m_out, int64_t cap,
+__global__ __launch_bounds__(64 * kNbrWaves) void k_map_pairs3(Header* h, const int32_t* nbr, const int64_t* m_out, int64_t cap,
                                                     const uint32_t* bbase, int32_t* off, int32_t* pairs,
                                                     int64_t pair_cap) {
     const int lane = threadIdx.x & 63;
@@ -278,7 +275,7 @@ __global__ __launch_bounds__(256) void k_map_pairs3(Header* h, const int32_t* nb
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 #pragma unroll
     for (int q = 0; q < kNbrProbes; ++q) {
-        const int k = wave + 4 * q;
+        const int k = wave + kNbrWaves * q;
         if (k >= 27) break;
         const int32_t e = valid ? nbr[j * 27 + k] : 0;
         const uint64_t bal = __ballot(e != 0);
@@ -297,7 +294,7 @@ __global__ __launch_bounds__(256) void k_map_pairs3(Header* h, const int32_t* nb
 void launch_kernel_map_nbr(hipStream_t s, const KmapWs& w, const int32_t* coords, const int64_t* m_dev,
                            int64_t m_cap, int32_t* nbr) {
     const int64_t mc = m_cap > 0 ? m_cap : 1;
-    k_map_nbr3<false><<<blocks_for(mc, kNbrVox), 256, 0, s>>>(w.fine, coords, m_dev, mc, nbr, nullptr);
+    k_map_nbr3<false><<<blocks_for(mc, kNbrVox), 64 * kNbrWaves, 0, s>>>(w.fine, coords, m_dev, mc, nbr, nullptr);
 }
 
 void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const int32_t* in_coords,
@@ -330,13 +327,13 @@ void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const in
     if (K == 3) {
         const unsigned nb3 = blocks_for(mc, kNbrVox);
         if (stride == 2) {
-            k_map_nbr3<true><<<nb3, 256, 0, s>>>(w.fine, out_coords, w.m_out, mc, w.nbr, w.bcnt);
+            k_map_nbr3<true><<<nb3, 64 * kNbrWaves, 0, s>>>(w.fine, out_coords, w.m_out, mc, w.nbr, w.bcnt);
         } else {
             if (!fine) k_map_same_count<<<1, 1, 0, s>>>(m_in_dev, m_cap, w.m_out, m_out_dev);
-            k_map_nbr3<false><<<nb3, 256, 0, s>>>(w.fine, in_coords, w.m_out, mc, w.nbr, w.bcnt);
+            k_map_nbr3<false><<<nb3, 64 * kNbrWaves, 0, s>>>(w.fine, in_coords, w.m_out, mc, w.nbr, w.bcnt);
         }
         launch_exclusive_scan(s, (const int32_t*)w.bcnt, (int32_t*)w.bbase, nullptr, (int64_t)27 * nb3, w.scan_tmp);
-        k_map_pairs3<<<nb3, 256, 0, s>>>(w.h, w.nbr, w.m_out, mc, w.bbase, off, pairs, pair_cap);
+        k_map_pairs3<<<nb3, 64 * kNbrWaves, 0, s>>>(w.h, w.nbr, w.m_out, mc, w.bbase, off, pairs, pair_cap);
     } else {
         k_s2_count<<<nblk, kMapThreads, 0, s>>>(in_coords, m_in_dev, mc, w.bcnt);
         launch_exclusive_scan(s, (const int32_t*)w.bcnt, (int32_t*)w.bbase, nullptr, (int64_t)K3 * nblk, w.scan_tmp);

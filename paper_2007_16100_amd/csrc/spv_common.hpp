@@ -56,10 +56,11 @@ __device__ inline void raise_flag(Header* h, uint32_t f) { atomicOr(&h->status, 
 
 // ---------------------------------------------------------------------------
 // open-addressing hash with linear probing over 64-bit keys.  A probe sequence
-// starts at the first slot of a 4-slot bucket (a 32-byte aligned run of keys)
-// and continues linearly, wrapping at the end of the table; lookups read one
-// whole bucket (4 keys + 4 values) per round, so almost every lookup costs a
-// single memory round trip.
+// starts at the first slot of a 4-slot bucket and continues linearly, wrapping
+// at the end of the table; lookups read one whole bucket (4 keys + 4 values)
+// per round, so almost every lookup costs a single memory round trip.  A
+// bucket is one 64-byte block -- its 4 keys, its 4 values, 16 bytes unused --
+// so a probe touches a single cache line.
 // ---------------------------------------------------------------------------
 typedef unsigned long long u64x2 __attribute__((ext_vector_type(2)));
 typedef int i32x4v __attribute__((ext_vector_type(4)));
@@ -77,10 +78,16 @@ __host__ __device__ inline uint32_t hash_slot(uint64_t k, uint32_t mask) {
 constexpr uint32_t kNoSlot = 0xFFFFFFFFu;  // "no table slot"
 
 struct Table {
-    uint64_t* keys;  // [capacity], 256-byte aligned
-    int32_t* vals;   // [capacity], 256-byte aligned
-    uint32_t mask;   // capacity - 1 (capacity is a power of two, >= 1024)
+    uint64_t* keys;  // bucket-major storage, 16 bytes per slot, 256-byte aligned (see table_words)
+    uint32_t mask;   // capacity - 1 (capacity is a power of two, >= 4)
 };
+// 64-bit words of a table of S slots: S / 4 buckets of 8 words
+__host__ __device__ inline size_t table_words(uint32_t S) { return (size_t)2 * S; }
+// the key and the value of slot s
+__device__ inline uint64_t* slot_key(Table t, uint32_t s) { return t.keys + 8 * (size_t)(s >> 2) + (s & 3); }
+__device__ inline int32_t* slot_val(Table t, uint32_t s) {
+    return (int32_t*)(t.keys + 8 * (size_t)(s >> 2) + 4) + (s & 3);
+}
 
 // Insert; returns 1 if this call created the entry, 0 if the key was present,
 // -1 if the table is full.  *slot receives the entry's slot.  Slots are claimed
@@ -91,7 +98,7 @@ struct Table {
 __device__ inline int table_insert(Table t, uint64_t key, uint32_t* slot) {
     uint32_t s = hash_slot(key, t.mask);
     for (uint32_t i = 0; i <= t.mask; ++i) {
-        const uint64_t prev = atomicCAS((unsigned long long*)&t.keys[s], (unsigned long long)kEmpty,
+        const uint64_t prev = atomicCAS((unsigned long long*)slot_key(t, s), (unsigned long long)kEmpty,
                                         (unsigned long long)key);
         if (prev == kEmpty) {
             *slot = s;
@@ -112,10 +119,11 @@ struct Bucket {
     i32x4v v;
 };
 __device__ inline Bucket load_bucket(Table t, uint32_t s) {
+    const uint64_t* q = t.keys + 8 * (size_t)(s >> 2);
     Bucket b;
-    b.k01 = *(const u64x2*)(t.keys + s);
-    b.k23 = *(const u64x2*)(t.keys + s + 2);
-    b.v = *(const i32x4v*)(t.vals + s);
+    b.k01 = *(const u64x2*)q;
+    b.k23 = *(const u64x2*)(q + 2);
+    b.v = *(const i32x4v*)(q + 4);
     return b;
 }
 // settle a lookup from one bucket: 1 = found (*pos = slot offset 0..3),
@@ -166,43 +174,54 @@ __device__ inline int32_t table_find(Table t, uint64_t key) {
 // slot of a present key (used to set values); -1 if absent
 __device__ inline int64_t table_slot(Table t, uint64_t key) { return table_slot_from(t, key, hash_slot(key, t.mask)); }
 
-// NP lookups whose first buckets are read together (one round trip for all of
-// them), then the second buckets of the ones not yet settled (one more round);
-// the rare key settled by neither continues on its own.  Inactive entries
-// (act[p] false) read bucket 0 and return -1.
+// NP lookups whose first buckets are read together, keys only (two 16-byte
+// loads per probe, one round trip for all of them); the values of the keys
+// found there are read next, one 4-byte load each.  A probe settles in its
+// first bucket when the key is there or a slot of the bucket is empty (an
+// insert would have stopped at that slot); the rare other one continues
+// bucket by bucket on its own.  Inactive entries (act[p] false) read bucket 0
+// and return -1.
 template <int NP>
 __device__ inline void table_find_n(Table t, const uint64_t (&key)[NP], const bool (&act)[NP], int32_t (&res)[NP]) {
     uint32_t s[NP];
-    int st[NP];  // 1 found, 0 absent, -1 open
-    Bucket b[NP];
+    u64x2 a[NP], b[NP];
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
         s[p] = act[p] ? hash_slot(key[p], t.mask) : 0u;
-        b[p] = load_bucket(t, s[p]);
+        const uint64_t* q = t.keys + 8 * (size_t)(s[p] >> 2);
+        a[p] = *(const u64x2*)q;
+        b[p] = *(const u64x2*)(q + 2);
+    }
+    int e[NP];  // slot of the key in the bucket (0..3), -1 absent, -2 continue
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+        const uint64_t k4[4] = {a[p].x, a[p].y, b[p].x, b[p].y};
+        bool empty = false;
+        e[p] = -1;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            if (k4[u] == key[p]) e[p] = u;  // a key is stored at most once
+            empty = empty || k4[u] == kEmpty;
+        }
+        if (!act[p]) e[p] = -1;
+        else if (e[p] < 0 && !empty) e[p] = -2;
     }
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
-        int e = 0;
-        st[p] = act[p] ? bucket_match(b[p], key[p], &e) : 0;
-        res[p] = st[p] > 0 ? bucket_val(b[p], e) : -1;
-        if (st[p] < 0) s[p] = (s[p] + 4) & t.mask;
-    }
-#pragma unroll
-    for (int p = 0; p < NP; ++p)
-        if (st[p] < 0) b[p] = load_bucket(t, s[p]);
-#pragma unroll
-    for (int p = 0; p < NP; ++p) {
-        if (st[p] < 0) {
-            int e = 0;
-            const int r = bucket_match(b[p], key[p], &e);
-            if (r > 0) {
-                res[p] = bucket_val(b[p], e);
-            } else if (r < 0) {
-                const int64_t sl = table_slot_from(t, key[p], (s[p] + 4) & t.mask);
-                res[p] = sl >= 0 ? t.vals[sl] : -1;
-            }
+        res[p] = -1;
+        if (e[p] >= 0) {
+            res[p] = *((const int32_t*)(t.keys + 8 * (size_t)(s[p] >> 2) + 4) + e[p]);
+        } else if (e[p] == -2) {
+            const int64_t sl = table_slot_from(t, key[p], (s[p] + 4) & t.mask);
+            res[p] = sl >= 0 ? *slot_val(t, (uint32_t)sl) : -1;
         }
     }
+}
+
+// a table of S slots (a power of two, >= 4) carved from an arena
+template <class A>
+inline Table take_table(A& a, uint32_t S) {
+    return Table{a.template take<uint64_t>(table_words(S)), S - 1};
 }
 
 inline uint32_t table_capacity(int64_t max_keys) {

@@ -22,9 +22,7 @@ namespace spv {
 void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n) {
     int64_t nn = n > 0 ? n : 1;
     uint32_t S = table_capacity(nn);
-    w.table.keys = a.take<uint64_t>(S);
-    w.table.vals = a.take<int32_t>(S);
-    w.table.mask = S - 1;
+    w.table = take_table(a, S);
     plan_radix_ws(a, w.rs, nn);
     w.seg = a.take<int32_t>(nn + 1);
     w.fill = a.take<int32_t>(nn);
@@ -81,8 +79,7 @@ __device__ inline uint64_t point_key_of(const float* xyz, const int32_t* batch, 
 // What the first launch of a voxelization clears and packs besides Eq. 1.
 struct VoxFirst {
     Header* h;
-    uint64_t* tkeys;  // the hash table's key slots -> empty
-    uint32_t nslots;
+    Table table;      // the hash table -> empty
     uint32_t* zero;   // the sort's counters and look-back words -> 0
     int64_t nzero;
     int njobs;
@@ -102,7 +99,9 @@ __global__ __launch_bounds__(kRsProducerBlock) void k_vq_quantize(VoxFirst f, co
     }
     const int64_t t0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = t0; i < (int64_t)f.nslots; i += stride) f.tkeys[i] = kEmpty;
+    const int64_t nkw = (int64_t)(f.table.mask + 1) / 2;  // 16-byte runs of keys: 2 per bucket
+    for (int64_t i = t0; i < nkw; i += stride)
+        *(u64x2*)(f.table.keys + 8 * (i >> 1) + 2 * (i & 1)) = u64x2{kEmpty, kEmpty};
     for (int64_t i = t0; i < f.nzero; i += stride) f.zero[i] = 0u;
     for (int j = 0; j < f.njobs; ++j) pack_job_run(f.job[j]);
 
@@ -287,7 +286,7 @@ __device__ inline void vq_insert(Header* h, Table t, const int32_t* coords, int6
     const int32_t* c = coords + 4 * v;
     uint32_t slot;
     const int r = table_insert(t, pack_key(c[0], c[1], c[2], c[3]), &slot);
-    if (r > 0) t.vals[slot] = (int32_t)v;
+    if (r > 0) *slot_val(t, slot) = (int32_t)v;
     else raise_flag(h, r < 0 ? kFlagTableFull : kFlagDuplicate);
 }
 
@@ -515,8 +514,7 @@ void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const
                      int32_t* counts, int32_t* pt2vox, int64_t* m_dev, const PackJob* jobs, int njobs) {
     VoxFirst f;
     f.h = w.h;
-    f.tkeys = w.table.keys;
-    f.nslots = w.table.mask + 1;
+    f.table = w.table;
     f.zero = w.rs.zero;  // the sort's histograms and tile counters
     f.nzero = (int64_t)radix_zero_words(n);
     f.njobs = 0;
