@@ -114,18 +114,32 @@ def table_slots(n):
 
 def phase_bytes(n, m, pairs, C, nconv=2):
     """Algorithmic bytes per phase of the block: compulsory reads of inputs plus writes of
-    outputs, each gathered row counted once, plus one write of the hash table (12 B/slot)."""
+    outputs, each gathered row counted once.  The hash table has 16 B per slot (64-byte
+    buckets of 4 keys and 4 values); clearing it writes the 8-byte keys of every slot."""
     S = table_slots(n)
     return {
-        # xyz + features in; coords, counts, pt2vox, voxel features out; table written once
-        "voxelize": 12 * n + 2 * C * n + 16 * m + 4 * m + 4 * n + 2 * C * m + 12 * S,
+        # xyz + features in; coords, counts, pt2vox, voxel features out; the table's keys
+        # cleared and one key + value written per voxel
+        "voxelize": 12 * n + 2 * C * n + 16 * m + 4 * m + 4 * n + 2 * C * m + 8 * S + 12 * m,
         # coords in, table read once, 27-entry neighbour table out
-        "kernel_map": 16 * m + 12 * S + 108 * m,
+        "kernel_map": 16 * m + 16 * S + 108 * m,
         # input rows + output rows + the map (8 B per pair) + weights, per conv
         "conv": 2 * C * m + 2 * C * m + 8 * pairs + 27 * C * C * 2,
-        # xyz + point features + voxel features + table + output
-        "devox_mlp_add": 12 * n + 2 * C * n + 2 * C * m + 12 * S + 2 * C * n,
+        # xyz + point features + pt2vox + neighbour rows + voxel features + output
+        "devox_mlp_add": 12 * n + 2 * C * n + 4 * n + 108 * m + 2 * C * m + 2 * C * n,
     }
+
+
+def phase_roofline(n, m, pairs, C, med):
+    """Each phase's algorithmic bytes over its median event time, against 8 TB/s."""
+    pb = phase_bytes(n, m, pairs, C)
+    res = {}
+    for k, key in (("voxelize", "voxelize"), ("kernel_map", "kernel_map"), ("conv1", "conv"),
+                   ("conv2", "conv"), ("devox_mlp_add", "devox_mlp_add")):
+        gbps = pb[key] / (med[k] * 1e-3) / 1e9
+        res[k] = {"bound": "hbm", "alg_bytes": pb[key], "ms": med[k], "achieved": gbps, "peak": PEAK_HBM_GBPS,
+                  "unit": "GB/s", "frac": gbps / PEAK_HBM_GBPS}
+    return res
 
 
 def time_block(spv, ws, params, d_xyz, d_feat, out, steps, warm, batch=None):
@@ -455,7 +469,16 @@ def cpu_baseline(xyz, convs, C, v=0.05):
     oracle.sparse_conv(x, off, pairs, W, len(coords), "bf16", sc, sh, r)
     dt = time.perf_counter() - t0
     flops = 2.0 * C * C * int(off[-1])
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
+            "nproc": os.cpu_count(), "cpu_model": model,
             "sample": f"one submanifold 3x3x3 conv {C}->{C} (bf16 storage, fp64 accumulation) over the full "
                       f"{len(coords)}-voxel sweep, {int(off[-1])} kernel-map pairs; {dt:.2f} s"}
 
@@ -602,6 +625,7 @@ def main():
         "phases_ms_p10": p10,
         "phases_ms_p90": p90,
         "roofline": roof,
+        "phase_roofline": phase_roofline(n, m, pairs_total, C, med),
     }
     if not args.no_cpu:
         res["cpu_baseline"] = cpu_baseline(xyz, convs, C)
