@@ -415,19 +415,24 @@ __global__ void k_vox_mean(Header* h, int64_t cap, const int32_t* seg, const int
     int64_t m = h->m;
     if (m > cap) m = cap;
     const int nch = C / VEC;
-    // with counts, one more thread per voxel counts it and enters it into the
-    // table, off the critical path of the threads that average it
-    const int per = counts ? nch + 1 : nch;
+    // With counts, the first cap threads count the voxels and enter them into
+    // the table: whole waves of their own, launched first, so that their
+    // compare-and-swap round trips overlap the averaging waves instead of
+    // holding them up.
     int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    int64_t vox = t / per;
-    const int slot = (int)(t - vox * per);
+    if (counts) {
+        if (t < cap) {
+            if (t >= m) return;
+            counts[t] = seg[t + 1] - seg[t];  // N_m
+            vq_insert(h, ins, coords, t);
+            return;
+        }
+        t -= cap;
+    }
+    const int64_t vox = t / nch;
+    const int slot = (int)(t - vox * nch);
     if (vox >= m) return;
     int32_t lo = seg[vox], hi = seg[vox + 1];
-    if (slot == nch) {  // N_m and the table entry
-        counts[vox] = hi - lo;
-        vq_insert(h, ins, coords, vox);
-        return;
-    }
     const int ch = slot * VEC;
     if (hi - lo > run) {
         if (ch == 0) longv[atomicAdd((unsigned long long*)&h->aux[0], 1ull)] = (int32_t)vox;
@@ -480,7 +485,7 @@ constexpr int kMeanRun = 32;  // points a single thread sums
 template <int DT, int VEC>
 static void launch_mean(hipStream_t s, const VoxelizeWs& w, int64_t n, const void* feat, int C, void* vfeat,
                         int32_t* counts, const int32_t* coords) {
-    const int64_t threads = n * (C / VEC + (counts ? 1 : 0));
+    const int64_t threads = n * (C / VEC) + (counts ? n : 0);
     const bool split = C / VEC <= kMeanLongThreads / 2;
     k_vox_mean<DT, VEC><<<blocks_for(threads, 256), 256, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat,
                                                                  split ? kMeanRun : INT32_MAX, w.longv, counts,
