@@ -149,7 +149,7 @@ constexpr int kRsBits = 8;                      // digit width
 constexpr int kRsBins = 1 << kRsBits;
 constexpr int kRsPasses = (64 + kRsBits - 1) / kRsBits;  // digits of a 64-bit key
 constexpr int kRsRecWords = 12;
-constexpr int kRsProducerBlock = 1024;
+constexpr int kRsProducerBlock = 256;
 struct RadixWs {
     uint64_t* ka;
     uint64_t* kb;
