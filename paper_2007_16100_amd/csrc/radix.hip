@@ -26,6 +26,9 @@ namespace spv {
 constexpr uint64_t kRsFlagAgg = 1ull << 62;  // status word: the tile's own count
 constexpr uint64_t kRsFlagInc = 2ull << 62;  // ... the inclusive prefix (counts of this tile and all before)
 constexpr uint32_t kRsSpinLimit = 1u << 22;  // polls of one status word before the sort gives up (flags an error)
+constexpr int kRsHeadPasses = 4;    // passes launched one by one (enough for 32 significant bits)
+constexpr unsigned kRsTailGrid = 64;  // workgroups of the launch that runs the passes after them
+constexpr int kRsBarrierCtr = 16;   // ctr[16 + pass]: arrivals at the grid barrier before pass
 
 size_t radix_tiles(int64_t cap) { return blocks_for(cap > 0 ? cap : 1, kRsTile); }
 
@@ -227,15 +230,15 @@ __device__ inline uint32_t rs_lookback(const uint64_t* col, int64_t stride, int6
 // to the tile's first item of that digit (both at most kRsTile: 16 bits)
 constexpr size_t kRsPassLds = (size_t)kRsItems * (kRsThreads / 64) * kRsBins * sizeof(uint16_t);
 
+// One tile of one pass: the tile is taken from the pass's counter (tiles get
+// their place in the order they start, so every tile a reader waits for is
+// already running).  Returns false, with no work done, once the pass's tiles
+// are all taken.
 template <bool FIRST>
-__global__ __launch_bounds__(kRsThreads) void k_rs_pass(RadixWs w, Header* h, const int64_t* count_dev, int64_t cap,
-                                                        int pass) {
+__device__ inline bool rs_pass_tile(const RadixWs& w, Header* h, int64_t count, int64_t ntiles, int pass,
+                                    unsigned char* rs_smem) {
     static_assert(kRsBins <= kRsThreads, "threads t < kRsBins own digit t");
     constexpr int NWV = kRsThreads / 64;
-    const SortStats* gst = w.st;
-    // the first pass always runs: it writes the compacted keys and the payload
-    if (pass > 0 && (uint32_t)(kRsBits * pass) >= gst->sort_bits) return;
-    extern __shared__ __align__(16) unsigned char rs_smem[];
     uint16_t (*cnt)[NWV][kRsBins] = (uint16_t (*)[NWV][kRsBins])rs_smem;
     __shared__ uint32_t dbase[kRsBins];  // the digit's first output position for this tile
     __shared__ int lds[NWV + 1];
@@ -250,7 +253,7 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_pass(RadixWs w, Header* h, co
     }
     __syncthreads();
     const int64_t tile = s_tile;
-    const int64_t count = rs_count(count_dev, cap);
+    if (tile >= ntiles) return false;
     const int64_t base = tile * kRsTile;
     const uint64_t* ksrc = (pass & 1) ? w.kb : w.ka;
     uint64_t* kdst = (pass & 1) ? w.ka : w.kb;
@@ -271,7 +274,7 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_pass(RadixWs w, Header* h, co
     int all;
     const uint32_t gbase = (uint32_t)block_exclusive_scan((int)gcount, lds, &all);
     if constexpr (FIRST) {
-        const SortStats st = *gst;
+        const SortStats st = *w.st;
 #pragma unroll
         for (int r = 0; r < kRsItems; ++r)
             if (base + r * kRsThreads + t < count) keys[r] = rs_compact(keys[r], st);
@@ -329,6 +332,56 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_pass(RadixWs w, Header* h, co
             vdst[pos] = vals[r];
         }
     }
+    return true;
+}
+
+// dynamic LDS of a pass is declared by the kernels: per (round, wave, digit)
+// counts, then offsets relative to the tile's first item of that digit
+template <bool FIRST>
+__global__ __launch_bounds__(kRsThreads) void k_rs_pass(RadixWs w, Header* h, const int64_t* count_dev, int64_t cap,
+                                                        int pass) {
+    // the first pass always runs: it writes the compacted keys and the payload
+    if (pass > 0 && (uint32_t)(kRsBits * pass) >= w.st->sort_bits) return;
+    extern __shared__ __align__(16) unsigned char rs_smem[];
+    rs_pass_tile<FIRST>(w, h, rs_count(count_dev, cap), (int64_t)gridDim.x, pass, rs_smem);
+}
+
+// The passes from `first` on, in one launch of G co-resident workgroups that
+// loop over the tiles; a grid barrier separates two passes.  A key of at most
+// 8 * first significant bits (the usual case) makes it exit at once, so the
+// passes that are not needed cost one launch, not one each.  The barrier
+// publishes each pass's scatter (device-scope fences) before the next reads
+// it; a wait past kRsSpinLimit polls records an error and goes on, so every
+// workgroup ends.
+__global__ __launch_bounds__(kRsThreads) void k_rs_tail(RadixWs w, Header* h, const int64_t* count_dev, int64_t cap,
+                                                        int first, int64_t ntiles) {
+    const uint32_t bits = w.st->sort_bits;
+    if ((uint32_t)(kRsBits * first) >= bits) return;
+    extern __shared__ __align__(16) unsigned char rs_smem[];
+    const int64_t count = rs_count(count_dev, cap);
+    for (int pass = first; pass < kRsPasses && (uint32_t)(kRsBits * pass) < bits; ++pass) {
+        if (pass > first) {
+            // grid barrier: every workgroup has finished pass - 1 (each wave
+            // releases its scatter before the arrival, and acquires after it)
+            __threadfence();
+            __syncthreads();
+            if (threadIdx.x == 0) {
+                uint32_t* bar = &w.ctr[kRsBarrierCtr + pass];
+                atomicAdd(bar, 1u);
+                uint32_t spins = 0;
+                while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < gridDim.x) {
+                    if (++spins > kRsSpinLimit) {
+                        raise_flag(h, kFlagInternal);
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
+            }
+            __syncthreads();
+            __threadfence();
+        }
+        while (rs_pass_tile<false>(w, h, count, ntiles, pass, rs_smem)) __syncthreads();
+    }
 }
 
 void launch_radix_sort(hipStream_t s, const RadixWs& w, Header* h, const int64_t* count_dev, int64_t cap,
@@ -339,13 +392,19 @@ void launch_radix_sort(hipStream_t s, const RadixWs& w, Header* h, const int64_t
         hipFuncSetAttribute((const void*)k_rs_pass<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)kRsPassLds) == hipSuccess &&
         hipFuncSetAttribute((const void*)k_rs_pass<false>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)kRsPassLds) == hipSuccess &&
+        hipFuncSetAttribute((const void*)k_rs_tail, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)kRsPassLds) == hipSuccess;
     (void)lds_ok;
     k_rs_hist<<<nt, kRsThreads, 0, s>>>(w, count_dev, cap, nrec);
-    // the significant bits are known on the device only: every pass a 64-bit
-    // key may need is launched, and passes beyond them exit at once
+    // the significant bits are known on the device only: the first kRsHeadPasses
+    // passes are a launch each (a pass past the bits exits at once), and the
+    // passes after them share one launch
     k_rs_pass<true><<<nt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, 0);
-    for (int p = 1; p < kRsPasses; ++p) k_rs_pass<false><<<nt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, p);
+    for (int p = 1; p < kRsHeadPasses; ++p)
+        k_rs_pass<false><<<nt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, p);
+    const unsigned gt = nt < kRsTailGrid ? nt : kRsTailGrid;
+    k_rs_tail<<<gt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, kRsHeadPasses, (int64_t)nt);
 }
 
 }  // namespace spv
