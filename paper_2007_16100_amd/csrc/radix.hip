@@ -145,29 +145,37 @@ __device__ inline uint64_t rs_peers(uint32_t d, bool valid) {
 
 // Statistics (block 0 stores them) and the digit histograms of every pass
 // that the significant bits need, over this block's keys.
-__global__ __launch_bounds__(kRsThreads) void k_rs_hist(RadixWs w, const int64_t* count_dev, int64_t cap,
-                                                        uint32_t nrec) {
+// Blocks of kRhThreads threads over kRhTile keys: four times as many blocks
+// as pass tiles, so that the whole chip counts (the counting is short, and
+// its time goes into waiting for loads).  Block b also clears pass tile b's
+// look-back words of pass 0 and of the consumer's scan (b < ntiles).
+constexpr int kRhThreads = 256;
+constexpr int kRhTile = kRhThreads * kRsItems;
+__global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t* count_dev, int64_t cap,
+                                                         uint32_t nrec, int64_t ntiles) {
+    static_assert(kRsBins == kRhThreads, "thread t clears digit t's look-back word");
     const int64_t count = rs_count(count_dev, cap);
-    const int64_t base = (int64_t)blockIdx.x * kRsTile;
+    const int64_t base = (int64_t)blockIdx.x * kRhTile;
     uint64_t raw[kRsItems];  // loaded before the statistics are reduced (no dependence between the two)
 #pragma unroll
     for (int r = 0; r < kRsItems; ++r) {
-        const int64_t i = base + r * kRsThreads + threadIdx.x;
+        const int64_t i = base + r * kRhThreads + threadIdx.x;
         raw[r] = i < count ? w.ka[i] : 0ull;
     }
-    // this tile's look-back words of pass 0 and of the consumer's scan start empty
-    if (threadIdx.x < kRsBins) w.status[(size_t)blockIdx.x * kRsBins + threadIdx.x] = 0ull;
-    if (threadIdx.x == 0) w.status[(size_t)kRsPasses * kRsBins * w.ntiles + blockIdx.x] = 0ull;
+    if (blockIdx.x < ntiles) {
+        w.status[(size_t)blockIdx.x * kRsBins + threadIdx.x] = 0ull;
+        if (threadIdx.x == 0) w.status[(size_t)kRsPasses * kRsBins * w.ntiles + blockIdx.x] = 0ull;
+    }
     SortStats st;
     rs_reduce_stats(w.rec, nrec, count, &st);
     if (blockIdx.x == 0 && threadIdx.x == 0) *w.st = st;
     __shared__ uint32_t hist[kRsPasses][kRsBins];
-    for (int e = threadIdx.x; e < kRsPasses * kRsBins; e += kRsThreads) (&hist[0][0])[e] = 0;
+    for (int e = threadIdx.x; e < kRsPasses * kRsBins; e += kRhThreads) (&hist[0][0])[e] = 0;
     __syncthreads();
     const int passes = rs_passes(st);
 #pragma unroll
     for (int r = 0; r < kRsItems; ++r) {
-        const int64_t i = base + r * kRsThreads + threadIdx.x;
+        const int64_t i = base + r * kRhThreads + threadIdx.x;
         if (i < count) {
             const uint64_t ck = rs_compact(raw[r], st);
             for (int p = 0; p < passes; ++p)
@@ -175,7 +183,7 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_hist(RadixWs w, const int64_t
         }
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < passes * kRsBins; e += kRsThreads) {
+    for (int e = threadIdx.x; e < passes * kRsBins; e += kRhThreads) {
         const uint32_t c = (&hist[0][0])[e];
         if (c) atomicAdd(&w.ghist[e], c);
     }
@@ -396,7 +404,8 @@ void launch_radix_sort(hipStream_t s, const RadixWs& w, Header* h, const int64_t
         hipFuncSetAttribute((const void*)k_rs_tail, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)kRsPassLds) == hipSuccess;
     (void)lds_ok;
-    k_rs_hist<<<nt, kRsThreads, 0, s>>>(w, count_dev, cap, nrec);
+    const unsigned nh = (unsigned)blocks_for(cap > 0 ? cap : 1, kRhTile);  // >= nt
+    k_rs_hist<<<nh, kRhThreads, 0, s>>>(w, count_dev, cap, nrec, (int64_t)nt);
     // the significant bits are known on the device only: the first kRsHeadPasses
     // passes are a launch each (a pass past the bits exits at once), and the
     // passes after them share one launch
