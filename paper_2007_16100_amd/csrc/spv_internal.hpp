@@ -142,7 +142,7 @@ __device__ inline uint64_t sorted_key(const SortBufs& sb, int64_t r) {
 // launch_radix_sort the compacted keys, ascending, and the items' original
 // indices sit in rs_keys / rs_vals (which of the two buffers depends on the
 // number of passes, known on the device).
-constexpr int kRsThreads = 1024;
+constexpr int kRsThreads = 512;
 constexpr int kRsItems = 4;
 constexpr int kRsTile = kRsThreads * kRsItems;  // keys per tile
 constexpr int kRsBits = 8;                      // digit width
