@@ -27,7 +27,7 @@ constexpr uint64_t kRsFlagAgg = 1ull << 62;  // status word: the tile's own coun
 constexpr uint64_t kRsFlagInc = 2ull << 62;  // ... the inclusive prefix (counts of this tile and all before)
 constexpr uint32_t kRsSpinLimit = 1u << 22;  // polls of one status word before the sort gives up (flags an error)
 constexpr int kRsHeadPasses = 4;    // passes launched one by one (enough for 32 significant bits)
-constexpr unsigned kRsTailGrid = 64;  // workgroups of the launch that runs the passes after them
+constexpr unsigned kRsTailTiles = 256;  // most tiles for which those passes share one launch
 constexpr int kRsBarrierCtr = 16;   // ctr[16 + pass]: arrivals at the grid barrier before pass
 
 size_t radix_tiles(int64_t cap) { return blocks_for(cap > 0 ? cap : 1, kRsTile); }
@@ -354,7 +354,7 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_pass(RadixWs w, Header* h, co
     rs_pass_tile<FIRST>(w, h, rs_count(count_dev, cap), (int64_t)gridDim.x, pass, rs_smem);
 }
 
-// The passes from `first` on, in one launch of G co-resident workgroups that
+// The passes from `first` on, in one launch of co-resident workgroups that
 // loop over the tiles; a grid barrier separates two passes.  A key of at most
 // 8 * first significant bits (the usual case) makes it exit at once, so the
 // passes that are not needed cost one launch, not one each.  The barrier
@@ -410,10 +410,13 @@ void launch_radix_sort(hipStream_t s, const RadixWs& w, Header* h, const int64_t
     // passes are a launch each (a pass past the bits exits at once), and the
     // passes after them share one launch
     k_rs_pass<true><<<nt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, 0);
-    for (int p = 1; p < kRsHeadPasses; ++p)
-        k_rs_pass<false><<<nt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, p);
-    const unsigned gt = nt < kRsTailGrid ? nt : kRsTailGrid;
-    k_rs_tail<<<gt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, kRsHeadPasses, (int64_t)nt);
+    // up to kRsTailTiles tiles, the passes after the head share one launch
+    // (one workgroup per tile, all resident for the grid barrier); a larger
+    // sort launches them one by one, where a launch that exits at once is
+    // cheap against the passes themselves
+    const int head = nt <= kRsTailTiles ? kRsHeadPasses : kRsPasses;
+    for (int p = 1; p < head; ++p) k_rs_pass<false><<<nt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, p);
+    if (head < kRsPasses) k_rs_tail<<<nt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, head, (int64_t)nt);
 }
 
 }  // namespace spv
