@@ -147,10 +147,12 @@ __device__ inline uint64_t rs_peers(uint32_t d, bool valid) {
 // that the significant bits need, over this block's keys.
 // Blocks of kRhThreads threads over kRhTile keys: four times as many blocks
 // as pass tiles, so that the whole chip counts (the counting is short, and
-// its time goes into waiting for loads).  Block b also clears pass tile b's
-// look-back words of pass 0 and of the consumer's scan (b < ntiles).
+// its time goes into waiting for loads), up to kRhMaxBlocks that stride over
+// the rest.  Block b also clears the look-back words of pass 0 and of the
+// consumer's scan of pass tiles b, b + grid, ...
 constexpr int kRhThreads = 256;
 constexpr int kRhTile = kRhThreads * kRsItems;
+constexpr unsigned kRhMaxBlocks = 1024;
 __global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t* count_dev, int64_t cap,
                                                          uint32_t nrec, int64_t ntiles) {
     static_assert(kRsBins == kRhThreads, "thread t clears digit t's look-back word");
@@ -162,9 +164,9 @@ __global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t
         const int64_t i = base + r * kRhThreads + threadIdx.x;
         raw[r] = i < count ? w.ka[i] : 0ull;
     }
-    if (blockIdx.x < ntiles) {
-        w.status[(size_t)blockIdx.x * kRsBins + threadIdx.x] = 0ull;
-        if (threadIdx.x == 0) w.status[(size_t)kRsPasses * kRsBins * w.ntiles + blockIdx.x] = 0ull;
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        w.status[(size_t)tile * kRsBins + threadIdx.x] = 0ull;
+        if (threadIdx.x == 0) w.status[(size_t)kRsPasses * kRsBins * w.ntiles + tile] = 0ull;
     }
     SortStats st;
     rs_reduce_stats(w.rec, nrec, count, &st);
@@ -173,13 +175,23 @@ __global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t
     for (int e = threadIdx.x; e < kRsPasses * kRsBins; e += kRhThreads) (&hist[0][0])[e] = 0;
     __syncthreads();
     const int passes = rs_passes(st);
+    // grid-stride over blocks of kRhTile keys (the first one's keys are loaded above)
+    for (int64_t b0 = base; b0 < count; b0 += (int64_t)gridDim.x * kRhTile) {
+        if (b0 != base) {
 #pragma unroll
-    for (int r = 0; r < kRsItems; ++r) {
-        const int64_t i = base + r * kRhThreads + threadIdx.x;
-        if (i < count) {
-            const uint64_t ck = rs_compact(raw[r], st);
-            for (int p = 0; p < passes; ++p)
-                atomicAdd(&hist[p][(uint32_t)(ck >> (kRsBits * p)) & (kRsBins - 1)], 1u);  // LDS
+            for (int r = 0; r < kRsItems; ++r) {
+                const int64_t i = b0 + r * kRhThreads + threadIdx.x;
+                raw[r] = i < count ? w.ka[i] : 0ull;
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < kRsItems; ++r) {
+            const int64_t i = b0 + r * kRhThreads + threadIdx.x;
+            if (i < count) {
+                const uint64_t ck = rs_compact(raw[r], st);
+                for (int p = 0; p < passes; ++p)
+                    atomicAdd(&hist[p][(uint32_t)(ck >> (kRsBits * p)) & (kRsBins - 1)], 1u);  // LDS
+            }
         }
     }
     __syncthreads();
@@ -404,7 +416,9 @@ void launch_radix_sort(hipStream_t s, const RadixWs& w, Header* h, const int64_t
         hipFuncSetAttribute((const void*)k_rs_tail, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)kRsPassLds) == hipSuccess;
     (void)lds_ok;
-    const unsigned nh = (unsigned)blocks_for(cap > 0 ? cap : 1, kRhTile);  // >= nt
+    // at most kRhMaxBlocks blocks (each adds its counts with global atomics)
+    unsigned nh = (unsigned)blocks_for(cap > 0 ? cap : 1, kRhTile);
+    if (nh > kRhMaxBlocks) nh = kRhMaxBlocks;
     k_rs_hist<<<nh, kRhThreads, 0, s>>>(w, count_dev, cap, nrec, (int64_t)nt);
     // the significant bits are known on the device only: the first kRsHeadPasses
     // passes are a launch each (a pass past the bits exits at once), and the

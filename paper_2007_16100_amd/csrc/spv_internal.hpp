@@ -150,6 +150,7 @@ constexpr int kRsBins = 1 << kRsBits;
 constexpr int kRsPasses = (64 + kRsBits - 1) / kRsBits;  // digits of a 64-bit key
 constexpr int kRsRecWords = 12;
 constexpr int kRsProducerBlock = 256;
+constexpr unsigned kRsMaxRecords = 1024;  // producer records (blocks) at most
 struct RadixWs {
     uint64_t* ka;
     uint64_t* kb;

@@ -107,17 +107,27 @@ __global__ __launch_bounds__(kRsProducerBlock) void k_vq_quantize(VoxFirst f, co
 
     int mn[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
     int mx[4] = {(int)0x80000000, (int)0x80000000, (int)0x80000000, (int)0x80000000};
-    int why = 0;
-    if (t0 < n) {
-        const uint64_t key = point_key_of(xyz, batch, t0, v, why);
-        keys[t0] = key;
+    uint32_t nonfin = 0, range = 0;
+    for (int64_t k = t0; k < n; k += stride) {  // grid-stride: one record per block, however large n
+        int why = 0;
+        const uint64_t key = point_key_of(xyz, batch, k, v, why);
+        keys[k] = key;
         if (!why) {
             const int fl[4] = {key_b(key), key_x(key), key_y(key), key_z(key)};
 #pragma unroll
-            for (int d = 0; d < 4; ++d) mn[d] = mx[d] = fl[d];
+            for (int d = 0; d < 4; ++d) {
+                mn[d] = min(mn[d], fl[d]);
+                mx[d] = max(mx[d], fl[d]);
+            }
         }
+        nonfin += why == 1 ? 1u : 0u;
+        range += why == 2 ? 1u : 0u;
     }
-    uint32_t nonfin = __popcll(__ballot(why == 1)), range = __popcll(__ballot(why == 2));
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        nonfin += __shfl_xor(nonfin, o, 64);
+        range += __shfl_xor(range, o, 64);
+    }
     __shared__ uint32_t bad[2];
     if (threadIdx.x < 2) bad[threadIdx.x] = 0;
     block_minmax_record(mn, mx, rec + (size_t)kRsRecWords * blockIdx.x);  // synchronizes the block
@@ -411,23 +421,34 @@ __device__ inline void mean_store(const double (&acc)[VEC], double N, void* vfea
 template <int DT, int VEC>
 __global__ void k_vox_mean(Header* h, int64_t cap, const int32_t* seg, const int32_t* plist, const void* feat,
                            int C, void* vfeat, int run, int32_t* longv, int32_t* counts, Table ins,
-                           const int32_t* coords) {
+                           const int32_t* coords, int ins_first) {
     int64_t m = h->m;
     if (m > cap) m = cap;
     const int nch = C / VEC;
-    // With counts, the first cap threads count the voxels and enter them into
-    // the table: whole waves of their own, launched first, so that their
-    // compare-and-swap round trips overlap the averaging waves instead of
-    // holding them up.
+    // With counts, blocks of their own count voxels and enter them into the
+    // table, so that their compare-and-swap round trips overlap the averaging
+    // blocks instead of holding them up: with ins_first the first nb blocks
+    // (a grid that fits the chip at once), otherwise one block in every
+    // nch + 1, spread evenly through a grid that runs in rounds.
     int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
     if (counts) {
-        if (t < cap) {
-            if (t >= m) return;
-            counts[t] = seg[t + 1] - seg[t];  // N_m
-            vq_insert(h, ins, coords, t);
+        const int64_t nb = (int64_t)gridDim.x / (nch + 1);
+        int64_t grp, r;
+        if (ins_first) {
+            grp = blockIdx.x < nb ? blockIdx.x : (blockIdx.x - nb) / nch;
+            r = blockIdx.x < nb ? 0 : (blockIdx.x - nb) - grp * nch + 1;
+        } else {
+            grp = blockIdx.x / (nch + 1);
+            r = blockIdx.x - grp * (nch + 1);
+        }
+        if (r == 0) {
+            const int64_t vox = grp * blockDim.x + threadIdx.x;
+            if (vox >= m) return;
+            counts[vox] = seg[vox + 1] - seg[vox];  // N_m
+            vq_insert(h, ins, coords, vox);
             return;
         }
-        t -= cap;
+        t = (grp * nch + r - 1) * blockDim.x + threadIdx.x;
     }
     const int64_t vox = t / nch;
     const int slot = (int)(t - vox * nch);
@@ -481,15 +502,18 @@ __global__ __launch_bounds__(kMeanLongThreads) void k_vox_mean_long(const Header
 }
 
 constexpr int kMeanRun = 32;  // points a single thread sums
+constexpr int64_t kMeanInsFirst = 1 << 18;  // up to this many points the insert blocks go first
 
 template <int DT, int VEC>
 static void launch_mean(hipStream_t s, const VoxelizeWs& w, int64_t n, const void* feat, int C, void* vfeat,
                         int32_t* counts, const int32_t* coords) {
-    const int64_t threads = n * (C / VEC) + (counts ? n : 0);
-    const bool split = C / VEC <= kMeanLongThreads / 2;
-    k_vox_mean<DT, VEC><<<blocks_for(threads, 256), 256, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat,
+    const int nch = C / VEC;
+    // with counts: per group of nch + 1 blocks, one of inserts and nch of averaging
+    const int64_t nblk = counts ? blocks_for(n, 256) * (nch + 1) : blocks_for(n * nch, 256);
+    const bool split = nch <= kMeanLongThreads / 2;
+    k_vox_mean<DT, VEC><<<nblk, 256, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat,
                                                                  split ? kMeanRun : INT32_MAX, w.longv, counts,
-                                                                 w.table, coords);
+                                                                 w.table, coords, n <= kMeanInsFirst ? 1 : 0);
     if (split) {
         const int64_t g = n < 1024 ? (n > 0 ? n : 1) : 1024;
         k_vox_mean_long<DT, VEC><<<(unsigned)g, kMeanLongThreads, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat,
@@ -525,7 +549,9 @@ void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const
     f.njobs = 0;
     for (int j = 0; j < njobs && f.njobs < kMaxPackJobs; ++j)
         if (jobs[j].total > 0) f.job[f.njobs++] = jobs[j];
-    const unsigned nq = blocks_for(n, kRsProducerBlock);
+    // at most kRsMaxRecords blocks: every histogram block reduces all their records
+    unsigned nq = blocks_for(n, kRsProducerBlock);
+    if (nq > kRsMaxRecords) nq = kRsMaxRecords;
     k_vq_quantize<<<nq, kRsProducerBlock, 0, s>>>(f, xyz, batch, n, voxel_size, w.rs.ka, w.rs.rec);
     launch_radix_sort(s, w.rs, w.h, nullptr, n, nq);
     const int64_t nt = (int64_t)radix_tiles(n);
