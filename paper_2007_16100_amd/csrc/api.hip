@@ -427,7 +427,7 @@ spv_status spv_kernel_map_nbr(void* stream, void* ws, size_t ws_bytes, const int
     hipStream_t s = (hipStream_t)stream;
     if (m_cap == 0) return clear_status_only(s, ws);
     launch_clear(s, L.h, L.w.fine, true);
-    launch_table_build(s, L.h, L.w.fine, in_coords, m_in_dev, m_cap);
+    launch_table_build(s, L.h, L.w.fine, in_coords, m_in_dev, m_cap, nullptr, nullptr, nbr);
     launch_kernel_map_nbr(s, L.w, in_coords, m_in_dev, m_cap, nbr);
     return hip_check();
 }
@@ -879,6 +879,9 @@ spv_status spv_block(void* stream, void* ws, size_t ws_bytes, const spv_block_pa
     int njobs = 0;
     for (int l = 0; l < p->n_convs; ++l) jobs[njobs++] = conv_pack_job(27, p->W[l], L.wpack_conv[l], C, C, dt);
     jobs[njobs++] = devox_pack_job(a, L.wpack_mlp);
+    // the neighbour-table map expects entries 14..26 of every row zeroed: the
+    // voxelization's inserts do it
+    if (L.plan.use_union) L.vox.nbr_upper = L.plan.nbr;
     launch_voxelize(s, L.vox, xyz, batch, n, p->voxel_size, feat, C, dt, L.coords, L.va, L.counts, L.pt2vox, L.m_dev,
                     jobs, njobs);
     mark(1);

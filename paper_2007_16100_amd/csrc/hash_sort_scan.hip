@@ -36,7 +36,7 @@ __device__ inline bool coord_ok(const int32_t* c) {
 }
 
 __global__ void k_table_build(Header* h, Table t, const int32_t* coords, const int64_t* count_dev, int64_t cap,
-                              int64_t* count_out, int64_t* count_out2) {
+                              int64_t* count_out, int64_t* count_out2, int32_t* nbr_upper) {
     int64_t count = count_dev ? *count_dev : cap;
     if (count > cap) count = cap;
     if (blockIdx.x == 0 && threadIdx.x == 0) {  // the count, for kernels that take it from here
@@ -45,6 +45,7 @@ __global__ void k_table_build(Header* h, Table t, const int32_t* coords, const i
     }
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count; i += (int64_t)gridDim.x * blockDim.x) {
         const int32_t* c = coords + 4 * i;
+        if (nbr_upper) clear_nbr_upper(nbr_upper, i);
         if (!coord_ok(c)) {
             raise_flag(h, kFlagRange);
             continue;
@@ -62,8 +63,9 @@ __global__ void k_table_build(Header* h, Table t, const int32_t* coords, const i
 }
 
 void launch_table_build(hipStream_t s, Header* h, Table t, const int32_t* coords, const int64_t* count_dev,
-                        int64_t cap, int64_t* count_out, int64_t* count_out2) {
-    k_table_build<<<blocks_for(cap, 256), 256, 0, s>>>(h, t, coords, count_dev, cap, count_out, count_out2);
+                        int64_t cap, int64_t* count_out, int64_t* count_out2, int32_t* nbr_upper) {
+    k_table_build<<<blocks_for(cap, 256), 256, 0, s>>>(h, t, coords, count_dev, cap, count_out, count_out2,
+                                                        nbr_upper);
 }
 
 __global__ void k_table_lookup(Table t, const int32_t* q, int64_t nq, int32_t* idx) {

@@ -291,10 +291,63 @@ __global__ __launch_bounds__(64 * kNbrWaves) void k_map_pairs3(Header* h, const 
     }
 }
 
+// The neighbour table alone, from half the probes: offset k of voxel j holds i
+// exactly when offset 26 - k of voxel i holds j (the map of a set onto itself
+// is symmetric), so only the 13 offsets below the centre are probed.  A block
+// writes entries 0..13 of its 64 rows (the centre is the voxel itself) through
+// an LDS tile, and every pair it finds also into entry 26 - k of the partner's
+// row; entries 14..26 start at zero (the table build or the voxelization's
+// inserts clear them), and the two kinds of write never touch the same entry.
+constexpr int kSymWaves = 7;  // wave w probes k = w and w + 7 (< 13)
+__global__ __launch_bounds__(64 * kSymWaves) void k_map_nbr3_sym(Table fine, const int32_t* coords,
+                                                                 const int64_t* m_out, int64_t cap, int32_t* nbr) {
+    constexpr int KL = 14;  // entries 0..13 of a row: the probed offsets and the centre
+    __shared__ int32_t tile[kNbrVox * KL];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t m = count_or_cap(m_out, cap);
+    const int64_t j = (int64_t)blockIdx.x * kNbrVox + lane;
+    const bool valid = j < m;
+    int c[4] = {0, 0, 0, 0};
+    if (valid) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) c[d] = coords[4 * j + d];
+    }
+    uint64_t key[2];
+    bool act[2];
+    int32_t res[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int k = wave + kSymWaves * q;
+        int dx, dy, dz;
+        offset_delta<3>(k, dx, dy, dz);
+        act[q] = valid && k < 13;
+        key[q] = pack_key(c[0], c[1] + dx, c[2] + dy, c[3] + dz);
+    }
+    table_find_n<2>(fine, key, act, res);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int k = wave + kSymWaves * q;
+        if (k >= 13) break;
+        const int32_t i = res[q];
+        const bool present = valid && i >= 0;
+        tile[lane * KL + k] = present ? i + 1 : 0;
+        if (present) nbr[(int64_t)i * 27 + (26 - k)] = (int32_t)j + 1;
+    }
+    if (wave == 0) tile[lane * KL + 13] = valid ? (int32_t)j + 1 : 0;
+    __syncthreads();
+    const int64_t j0 = (int64_t)blockIdx.x * kNbrVox;
+    const int rows = m - j0 < kNbrVox ? (int)(m - j0) : kNbrVox;
+    for (int e = threadIdx.x; e < rows * KL; e += blockDim.x) {
+        const int r = e / KL, k = e - r * KL;
+        nbr[(j0 + r) * 27 + k] = tile[e];
+    }
+}
+
 void launch_kernel_map_nbr(hipStream_t s, const KmapWs& w, const int32_t* coords, const int64_t* m_dev,
                            int64_t m_cap, int32_t* nbr) {
     const int64_t mc = m_cap > 0 ? m_cap : 1;
-    k_map_nbr3<false><<<blocks_for(mc, kNbrVox), 64 * kNbrWaves, 0, s>>>(w.fine, coords, m_dev, mc, nbr, nullptr);
+    k_map_nbr3_sym<<<blocks_for(mc, kNbrVox), 64 * kSymWaves, 0, s>>>(w.fine, coords, m_dev, mc, nbr);
 }
 
 void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const int32_t* in_coords,

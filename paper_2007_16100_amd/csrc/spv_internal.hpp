@@ -86,8 +86,10 @@ void launch_clear_header(hipStream_t s, Header* h);
 // raises kFlagDuplicate on a repeated coordinate, kFlagRange on a coordinate
 // outside the key range.
 // count_out / count_out2 (when given) receive the clamped count in the same launch
+// nbr_upper (optional): entries 14..26 of each inserted row's neighbour-table row -> 0
 void launch_table_build(hipStream_t s, Header* h, Table t, const int32_t* coords, const int64_t* count_dev,
-                        int64_t cap, int64_t* count_out = nullptr, int64_t* count_out2 = nullptr);
+                        int64_t cap, int64_t* count_out = nullptr, int64_t* count_out2 = nullptr,
+                        int32_t* nbr_upper = nullptr);
 void launch_table_lookup(hipStream_t s, Table t, const int32_t* q, int64_t nq, int32_t* idx);
 
 // --- radix sort of packed voxel keys (hash_sort_scan.hip) ---------------------
@@ -215,6 +217,8 @@ struct VoxelizeWs {
     int32_t* plist;     // [n] point ids grouped by voxel
     int32_t* longv;     // [n] voxels whose mean takes a whole workgroup (count in h->aux[0])
     int32_t* scan_tmp;  // [scan_tmp_entries(n)]
+    int32_t* nbr_upper = nullptr;  // optional [m][27] neighbour table: entries 14..26 of each voxel's row
+                                   // are zeroed where the voxel is entered into the table
 };
 void plan_voxelize_ws(Arena& a, VoxelizeWs& w, int64_t n);
 // coords/counts/pt2vox and (if feat) vfeat; m into h->m and *m_dev.  The first
@@ -251,9 +255,17 @@ void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const in
                        const int64_t* m_in_dev, int64_t m_cap, int K, int stride, int32_t* out_coords,
                        int64_t* m_out_dev, int32_t* off, int32_t* pairs, int64_t pair_cap, bool clear_header = false);
 // submanifold 3x3x3 neighbour table only (pass 1, no pairs): nbr[j][k] = i + 1,
-// 0 where offset k of voxel j holds no voxel; w.fine must map every coordinate
+// 0 where offset k of voxel j holds no voxel; w.fine must map every coordinate,
+// and entries 14..26 of rows 0 .. m-1 must be zero already (the table build or
+// the voxelization's inserts clear them): offsets below the centre are probed,
+// and each pair found fills both rows (offset k of j, offset 26 - k of i)
 void launch_kernel_map_nbr(hipStream_t s, const KmapWs& w, const int32_t* coords, const int64_t* m_dev,
                            int64_t m_cap, int32_t* nbr);
+// entries 14..26 of neighbour-table row v -> 0
+__device__ inline void clear_nbr_upper(int32_t* nbr, int64_t v) {
+#pragma unroll
+    for (int k = 14; k < 27; ++k) nbr[v * 27 + k] = 0;
+}
 
 // --- sparse conv (conv.hip) ----------------------------------------------------
 // Two MFMA kernels share one plan.

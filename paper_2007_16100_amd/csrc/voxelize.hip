@@ -302,13 +302,14 @@ __device__ inline void vq_insert(Header* h, Table t, const int32_t* coords, int6
 
 // N_m = seg[v + 1] - seg[v] and the table entry when there are no features to average
 __global__ void k_vq_counts(Header* h, int64_t cap, const int32_t* seg, int32_t* counts, Table t,
-                            const int32_t* coords) {
+                            const int32_t* coords, int32_t* nbr_upper) {
     int64_t m = h->m;
     if (m > cap) m = cap;
     const int64_t v = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
     if (v >= m) return;
     counts[v] = seg[v + 1] - seg[v];
     vq_insert(h, t, coords, v);
+    if (nbr_upper) clear_nbr_upper(nbr_upper, v);
 }
 
 // every point's voxel index, read at the table slot its insert found
@@ -421,7 +422,7 @@ __device__ inline void mean_store(const double (&acc)[VEC], double N, void* vfea
 template <int DT, int VEC>
 __global__ void k_vox_mean(Header* h, int64_t cap, const int32_t* seg, const int32_t* plist, const void* feat,
                            int C, void* vfeat, int run, int32_t* longv, int32_t* counts, Table ins,
-                           const int32_t* coords, int ins_first) {
+                           const int32_t* coords, int ins_first, int32_t* nbr_upper) {
     int64_t m = h->m;
     if (m > cap) m = cap;
     const int nch = C / VEC;
@@ -446,6 +447,7 @@ __global__ void k_vox_mean(Header* h, int64_t cap, const int32_t* seg, const int
             if (vox >= m) return;
             counts[vox] = seg[vox + 1] - seg[vox];  // N_m
             vq_insert(h, ins, coords, vox);
+            if (nbr_upper) clear_nbr_upper(nbr_upper, vox);
             return;
         }
         t = (grp * nch + r - 1) * blockDim.x + threadIdx.x;
@@ -513,7 +515,8 @@ static void launch_mean(hipStream_t s, const VoxelizeWs& w, int64_t n, const voi
     const bool split = nch <= kMeanLongThreads / 2;
     k_vox_mean<DT, VEC><<<nblk, 256, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat,
                                                                  split ? kMeanRun : INT32_MAX, w.longv, counts,
-                                                                 w.table, coords, n <= kMeanInsFirst ? 1 : 0);
+                                                                 w.table, coords, n <= kMeanInsFirst ? 1 : 0,
+                                                                 w.nbr_upper);
     if (split) {
         const int64_t g = n < 1024 ? (n > 0 ? n : 1) : 1024;
         k_vox_mean_long<DT, VEC><<<(unsigned)g, kMeanLongThreads, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat,
@@ -557,7 +560,7 @@ void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const
     const int64_t nt = (int64_t)radix_tiles(n);
     k_vq_segments<<<(unsigned)nt, kRsThreads, 0, s>>>(w.rs, w.h, n, nt, coords, pt2vox, w.seg, w.plist, m_dev);
     if (feat) launch_mean_dt(s, w, n, feat, C, dt, vfeat, counts, coords);
-    else k_vq_counts<<<blocks_for(n, 256), 256, 0, s>>>(w.h, n, w.seg, counts, w.table, coords);
+    else k_vq_counts<<<blocks_for(n, 256), 256, 0, s>>>(w.h, n, w.seg, counts, w.table, coords, w.nbr_upper);
 }
 
 void launch_voxelize_onto(hipStream_t s, const VoxelizeWs& w, const int32_t* coords, const int64_t* m_dev,
