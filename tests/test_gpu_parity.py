@@ -828,6 +828,27 @@ def test_kernel_map_nbr_matches_pairs(spv, sweep):
     np.testing.assert_array_equal(got, want)
 
 
+def test_kernel_map_nbr_shuffled_into_a_dirty_buffer(spv, sweep):
+    """The table from half the probes (each pair found fills both rows) on coordinates in a
+    shuffled order, a device count below the capacity, and an output buffer full of garbage:
+    every entry of the live rows is written, rows past the count are left alone."""
+    rc, _, _, _ = oracle.voxelize(sweep[::3], 0.05)
+    perm = np.random.default_rng(77).permutation(len(rc))
+    sc = np.ascontiguousarray(rc[perm])
+    m = len(sc) - 123
+    _, off, pairs = oracle.kernel_map(sc[:m])
+    want = np.zeros((m, 27), np.int32)
+    for k in range(27):
+        p = pairs[off[k]:off[k + 1]]
+        want[p[:, 1], k] = p[:, 0] + 1
+    ws = spv.Workspace.for_ops(len(sc), 16)
+    out = torch.full((len(sc), 27), -5, dtype=torch.int32, device="cuda")
+    spv.spv_kernel_map_nbr(ws, dev(sc), m_dev=torch.tensor([m], dtype=torch.int64, device="cuda"), out=out)
+    got = host(out)
+    np.testing.assert_array_equal(got[:m], want)
+    assert (got[m:] == -5).all()
+
+
 @pytest.mark.parametrize("cin,cout,dtype,res", [(32, 32, "bf16", False), (96, 96, "bf16", True),
                                                 (64, 128, "f16", True), (256, 256, "bf16", False)])
 def test_conv_on_neighbour_table(spv, sweep, cin, cout, dtype, res):
