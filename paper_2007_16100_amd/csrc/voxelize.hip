@@ -7,11 +7,12 @@
 // 2. the points are radix-sorted by key (radix.hip): the canonical (b, x, y, z)
 //    order of the voxels and the grouping of the points by voxel in one step;
 // 3. k_vq_segments: a voxel starts wherever the sorted key changes.  A scan of
-//    those starts numbers the voxels; each voxel's coordinates, its first point
-//    and its hash-table entry (value = its index: one insert per voxel, no
-//    contention) are written at its start, and every point gets its voxel index;
-// 4. k_vox_mean: each voxel sums its own points (fp64) and writes its mean and
-//    count once -- no float atomics.
+//    those starts numbers the voxels; each voxel's coordinates and its first
+//    point are written at its start, and every point gets its voxel index;
+// 4. k_vox_mean: each voxel sums its own points (fp64) and writes its mean once
+//    -- no float atomics; blocks of their own write the counts and enter each
+//    voxel into the hash table (value = its index: one insert per voxel), and
+//    k_vox_mean_long sums the voxels of over 32 points with a workgroup each.
 // The scatter-mean onto a given voxel set (launch_voxelize_onto) finds each
 // point's voxel in the set's table instead and groups the points by a counting
 // sort.
