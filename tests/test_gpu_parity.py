@@ -259,6 +259,23 @@ def test_voxelize_wide_keys_many_tiles(spv):
     np.testing.assert_array_equal(vf, rvf)
 
 
+def test_voxelize_over_a_million_points(spv):
+    """2.2M points (a sixth of them sharing voxels) over +-900 m: the quantize and histogram
+    kernels stride with their largest grids (1024 blocks), the sort launches every pass
+    (over 256 tiles), and the scatter-mean interleaves its insert blocks."""
+    rng = np.random.default_rng(5555)
+    xyz = rng.uniform(-900.0, 900.0, size=(2_200_000, 3)).astype(np.float32)
+    xyz[::6] = xyz[1::6][: len(xyz[::6])]
+    feat = synth.normal((len(xyz), 8), 5556, dtype="bf16")
+    c, vf, cnt, p2v, _ = run_voxelize(spv, xyz, 0.05, feat, "bf16")
+    rc, rvf, rcnt, rp2v = oracle.voxelize(xyz, 0.05, feat, "bf16")
+    assert len(xyz) > 1024 * 1024  # beyond 1024 histogram blocks of 1024 keys: they stride
+    np.testing.assert_array_equal(c, rc)
+    np.testing.assert_array_equal(cnt, rcnt)
+    np.testing.assert_array_equal(p2v, rp2v)
+    np.testing.assert_array_equal(vf, rvf)
+
+
 def test_voxelize_device_errors(spv):
     xyz = np.zeros((100, 3), np.float32)
     xyz[17, 1] = np.nan
