@@ -400,6 +400,54 @@ __device__ inline void mean_add(double (&acc)[VEC], const void* feat, int64_t ro
     }
 }
 
+// The points lo, lo + step, ... < hi of a voxel's list into acc, in list
+// order; U rows' indices, then their features, are loaded before any is
+// added, so a long voxel costs 1/U of the dependent round trips.
+constexpr int kMeanAhead = 4;
+template <int DT, int VEC>
+__device__ inline void mean_add_range(double (&acc)[VEC], const void* feat, const int32_t* plist, int C, int ch,
+                                      int32_t lo, int32_t hi, int32_t step) {
+    constexpr int U = kMeanAhead;
+    int32_t p = lo;
+    for (; p + (U - 1) * step < hi; p += U * step) {
+        int64_t row[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) row[u] = (int64_t)plist[p + u * step] * C + ch;
+        if constexpr (VEC == 8) {
+            uint4 v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) v[u] = *(const uint4*)((const uint16_t*)feat + row[u]);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    acc[2 * j] += (double)from16<DT>(w[j] & 0xFFFF);
+                    acc[2 * j + 1] += (double)from16<DT>(w[j] >> 16);
+                }
+            }
+        } else if constexpr (VEC == 4) {
+            float4 v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) v[u] = *(const float4*)((const float*)feat + row[u]);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                acc[0] += (double)v[u].x;
+                acc[1] += (double)v[u].y;
+                acc[2] += (double)v[u].z;
+                acc[3] += (double)v[u].w;
+            }
+        } else {
+            float v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) v[u] = ld_feat<DT>(feat, row[u]);
+#pragma unroll
+            for (int u = 0; u < U; ++u) acc[0] += (double)v[u];
+        }
+    }
+    for (; p < hi; p += step) mean_add<DT, VEC>(acc, feat, (int64_t)plist[p] * C + ch);
+}
+
 template <int DT, int VEC>
 __device__ inline void mean_store(const double (&acc)[VEC], double N, void* vfeat, int64_t orow) {
     if (N < 1.0) N = 1.0;  // a given voxel no point falls into (scatter-mean onto a set): mean 0
@@ -465,7 +513,7 @@ __global__ void k_vox_mean(Header* h, int64_t cap, const int32_t* seg, const int
     double acc[VEC];
 #pragma unroll
     for (int j = 0; j < VEC; ++j) acc[j] = 0.0;
-    for (int32_t p = lo; p < hi; ++p) mean_add<DT, VEC>(acc, feat, (int64_t)plist[p] * C + ch);
+    mean_add_range<DT, VEC>(acc, feat, plist, C, ch, lo, hi, 1);
     mean_store<DT, VEC>(acc, (double)(hi - lo), vfeat, vox * C + ch);
 }
 
@@ -490,7 +538,7 @@ __global__ __launch_bounds__(kMeanLongThreads) void k_vox_mean_long(const Header
 #pragma unroll
         for (int j = 0; j < VEC; ++j) acc[j] = 0.0;
         if (sl < slices)
-            for (int32_t p = lo + sl; p < hi; p += slices) mean_add<DT, VEC>(acc, feat, (int64_t)plist[p] * C + tch * VEC);
+            mean_add_range<DT, VEC>(acc, feat, plist, C, tch * VEC, lo + sl, hi, slices);
 #pragma unroll
         for (int j = 0; j < VEC; ++j) red[threadIdx.x][j] = acc[j];
         __syncthreads();
