@@ -402,12 +402,12 @@ __device__ inline void mean_add(double (&acc)[VEC], const void* feat, int64_t ro
 
 // The points lo, lo + step, ... < hi of a voxel's list into acc, in list
 // order; U rows' indices, then their features, are loaded before any is
-// added, so a long voxel costs 1/U of the dependent round trips.
-constexpr int kMeanAhead = 4;
-template <int DT, int VEC>
+// added, so a long voxel costs 1/U of the dependent round trips.  (The
+// per-voxel kernel takes U = 2: its voxels are short, and U = 4 cost it two
+// waves per SIMD of occupancy.)
+template <int DT, int VEC, int U>
 __device__ inline void mean_add_range(double (&acc)[VEC], const void* feat, const int32_t* plist, int C, int ch,
                                       int32_t lo, int32_t hi, int32_t step) {
-    constexpr int U = kMeanAhead;
     int32_t p = lo;
     for (; p + (U - 1) * step < hi; p += U * step) {
         int64_t row[U];
@@ -513,7 +513,7 @@ __global__ void k_vox_mean(Header* h, int64_t cap, const int32_t* seg, const int
     double acc[VEC];
 #pragma unroll
     for (int j = 0; j < VEC; ++j) acc[j] = 0.0;
-    mean_add_range<DT, VEC>(acc, feat, plist, C, ch, lo, hi, 1);
+    mean_add_range<DT, VEC, 2>(acc, feat, plist, C, ch, lo, hi, 1);
     mean_store<DT, VEC>(acc, (double)(hi - lo), vfeat, vox * C + ch);
 }
 
@@ -538,7 +538,7 @@ __global__ __launch_bounds__(kMeanLongThreads) void k_vox_mean_long(const Header
 #pragma unroll
         for (int j = 0; j < VEC; ++j) acc[j] = 0.0;
         if (sl < slices)
-            mean_add_range<DT, VEC>(acc, feat, plist, C, tch * VEC, lo + sl, hi, slices);
+            mean_add_range<DT, VEC, 4>(acc, feat, plist, C, tch * VEC, lo + sl, hi, slices);
 #pragma unroll
         for (int j = 0; j < VEC; ++j) red[threadIdx.x][j] = acc[j];
         __syncthreads();
