@@ -257,9 +257,68 @@ __global__ void k_vox_backward(const void* __restrict__ dv, int C, const int32_t
     }
 }
 
+// The same, one thread per (point, 16-byte chunk): the point's voxel and count
+// are read once per chunk instead of once per channel, and the chunk moves in
+// one load and one store.  VEC = 8 (16-bit storage) or 4 (fp32).
+template <int DT, int VEC>
+__global__ void k_vox_backward_vec(const void* __restrict__ dv, int C, const int32_t* __restrict__ counts,
+                                   const int32_t* __restrict__ pt2vox, int64_t n, int64_t m,
+                                   void* __restrict__ dfeat) {
+    const int nch = C / VEC;
+    const int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (t >= n * nch) return;
+    const int64_t k = t / nch;
+    const int c0 = (int)(t - k * nch) * VEC;
+    const int32_t v = pt2vox[k];
+    const int32_t N = (v >= 0 && v < m) ? counts[v] : 0;
+    double q[VEC];
+    if (N > 0) {
+        if constexpr (VEC == 8) {
+            const uint4 u = *(const uint4*)((const uint16_t*)dv + (int64_t)v * C + c0);
+            const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                q[2 * j] = (double)from16<DT>(w[j] & 0xFFFF) / (double)N;
+                q[2 * j + 1] = (double)from16<DT>(w[j] >> 16) / (double)N;
+            }
+        } else {
+            const float4 f = *(const float4*)((const float*)dv + (int64_t)v * C + c0);
+            q[0] = (double)f.x / (double)N;
+            q[1] = (double)f.y / (double)N;
+            q[2] = (double)f.z / (double)N;
+            q[3] = (double)f.w / (double)N;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) q[j] = 0.0;
+    }
+    if constexpr (VEC == 8) {
+        uint32_t w[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            w[j] = (uint32_t)to16<DT>(f64_to_f32_odd(q[2 * j])) | ((uint32_t)to16<DT>(f64_to_f32_odd(q[2 * j + 1])) << 16);
+        *(uint4*)((uint16_t*)dfeat + k * C + c0) = make_uint4(w[0], w[1], w[2], w[3]);
+    } else {
+        *(float4*)((float*)dfeat + k * C + c0) = make_float4((float)q[0], (float)q[1], (float)q[2], (float)q[3]);
+    }
+}
+
 void launch_voxelize_backward(hipStream_t s, const void* dv, int C, const int32_t* counts, const int32_t* pt2vox,
                               int64_t n, int64_t m, void* dfeat, int dt) {
     if (n <= 0) return;
+    // 16-byte chunks when the buffers and the rows allow them
+    const bool a16 = (((uintptr_t)dv | (uintptr_t)dfeat) & 15u) == 0;
+    if (a16 && dt != SPV_F32 && C % 8 == 0) {
+        const unsigned g = (unsigned)blocks_for(n * (C / 8), 256);
+        if (dt == SPV_BF16) k_vox_backward_vec<SPV_BF16, 8><<<g, 256, 0, s>>>(dv, C, counts, pt2vox, n, m, dfeat);
+        else k_vox_backward_vec<SPV_F16, 8><<<g, 256, 0, s>>>(dv, C, counts, pt2vox, n, m, dfeat);
+        return;
+    }
+    if (a16 && dt == SPV_F32 && C % 4 == 0) {
+        const unsigned g = (unsigned)blocks_for(n * (C / 4), 256);
+        k_vox_backward_vec<SPV_F32, 4><<<g, 256, 0, s>>>(dv, C, counts, pt2vox, n, m, dfeat);
+        return;
+    }
     int64_t g = blocks_for(n * C, 256);
     if (g > 8192) g = 8192;
     if (dt == SPV_F32) k_vox_backward<SPV_F32><<<(unsigned)g, 256, 0, s>>>(dv, C, counts, pt2vox, n, m, dfeat);
