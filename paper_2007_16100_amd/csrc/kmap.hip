@@ -344,6 +344,25 @@ __global__ __launch_bounds__(64 * kSymWaves) void k_map_nbr3_sym(Table fine, con
     }
 }
 
+// per-(offset, block) pair counts of a finished neighbour table (the pairs
+// pass's layout: offset-major, one count per block of kNbrVox rows)
+__global__ __launch_bounds__(64 * kNbrWaves) void k_map_count3(const int32_t* nbr, const int64_t* m_out, int64_t cap,
+                                                               uint32_t* bcnt) {
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t m = count_or_cap(m_out, cap);
+    const int64_t j = (int64_t)blockIdx.x * kNbrVox + lane;
+    const bool valid = j < m;
+#pragma unroll
+    for (int q = 0; q < kNbrProbes; ++q) {
+        const int k = wave + kNbrWaves * q;
+        if (k >= 27) break;
+        const bool present = valid && nbr[j * 27 + k] != 0;
+        const uint64_t bal = __ballot(present);
+        if (lane == 0) bcnt[k * gridDim.x + blockIdx.x] = (uint32_t)__popcll(bal);
+    }
+}
+
 void launch_kernel_map_nbr(hipStream_t s, const KmapWs& w, const int32_t* coords, const int64_t* m_dev,
                            int64_t m_cap, int32_t* nbr) {
     const int64_t mc = m_cap > 0 ? m_cap : 1;
@@ -361,8 +380,10 @@ void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const in
         // a submanifold map's table build also hands the output count (= the
         // input count) on
         launch_clear(s, w.h, w.fine, clear_header);
+        // a submanifold map clears entries 14..26 of its neighbour rows here
+        // for the half-probe table
         launch_table_build(s, w.h, w.fine, in_coords, m_in_dev, m_cap, stride == 1 ? w.m_out : nullptr,
-                           stride == 1 ? m_out_dev : nullptr);
+                           stride == 1 ? m_out_dev : nullptr, stride == 1 ? w.nbr : nullptr);
     } else if (clear_header && stride != 2) {
         launch_clear_header(s, w.h);
     }
@@ -382,8 +403,14 @@ void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const in
         if (stride == 2) {
             k_map_nbr3<true><<<nb3, 64 * kNbrWaves, 0, s>>>(w.fine, out_coords, w.m_out, mc, w.nbr, w.bcnt);
         } else {
-            if (!fine) k_map_same_count<<<1, 1, 0, s>>>(m_in_dev, m_cap, w.m_out, m_out_dev);
-            k_map_nbr3<false><<<nb3, 64 * kNbrWaves, 0, s>>>(w.fine, in_coords, w.m_out, mc, w.nbr, w.bcnt);
+            if (fine && w.nbr) {
+                // the table from half the probes, then the per-block counts from it
+                k_map_nbr3_sym<<<nb3, 64 * kSymWaves, 0, s>>>(w.fine, in_coords, w.m_out, mc, w.nbr);
+                k_map_count3<<<nb3, 64 * kNbrWaves, 0, s>>>(w.nbr, w.m_out, mc, w.bcnt);
+            } else {
+                k_map_same_count<<<1, 1, 0, s>>>(m_in_dev, m_cap, w.m_out, m_out_dev);
+                k_map_nbr3<false><<<nb3, 64 * kNbrWaves, 0, s>>>(w.fine, in_coords, w.m_out, mc, w.nbr, w.bcnt);
+            }
         }
         launch_exclusive_scan(s, (const int32_t*)w.bcnt, (int32_t*)w.bbase, nullptr, (int64_t)27 * nb3, w.scan_tmp);
         k_map_pairs3<<<nb3, 64 * kNbrWaves, 0, s>>>(w.h, w.nbr, w.m_out, mc, w.bbase, off, pairs, pair_cap);
