@@ -19,6 +19,20 @@
 // the significant bits of the compacted key exit at once.  Invalid items get
 // the all-ones key, which no valid compacted key reaches; their presence makes
 // the sort cover all 64 bits so that they end up last.
+//
+// Up to kMsMaxBlocks histogram blocks of keys, a bucket sort takes the place of
+// the passes when it can (every item valid, at most 32 significant bits, and no
+// bucket over kMsCap items):
+//   k_rs_hist    also counts, per block, the top 8 significant bits (the
+//                bucket) of its keys;
+//   k_ms_scatter moves every item into its bucket, stable: the bucket's base
+//                plus the counts of the blocks before (a plain sum, no
+//                look-back) plus its rank in the block;
+//   k_ms_bucket  one workgroup per bucket sorts the remaining bits in LDS (an
+//                LSD sort of 8-bit digits whose passes never leave the
+//                workgroup) and writes the result in place of the keys.
+// Otherwise both exit at once and k_rs_tail runs every pass in one launch.
+// Either way the order is the same stable ascending order.
 #include "spv_internal.hpp"
 
 namespace spv {
@@ -31,6 +45,17 @@ constexpr unsigned kRsTailTiles = 256;  // most tiles for which those passes sha
 constexpr int kRsBarrierCtr = 16;   // ctr[16 + pass]: arrivals at the grid barrier before pass
 
 size_t radix_tiles(int64_t cap) { return blocks_for(cap > 0 ? cap : 1, kRsTile); }
+
+// histogram blocks: kRhThreads threads over kRhTile keys
+constexpr int kRhThreads = 256;
+constexpr int kRhTile = kRhThreads * kRsItems;
+constexpr unsigned kRhMaxBlocks = 1024;
+// the bucket sort: at most kMsMaxBlocks histogram blocks (one tile each), at
+// most kMsCap items per bucket, sorted by kMsThreads threads
+constexpr unsigned kMsMaxBlocks = 256;
+constexpr int kMsThreads = 1024;
+constexpr int kMsRounds = 16;
+constexpr int kMsCap = kMsThreads * kMsRounds;
 
 void plan_radix_ws(Arena& a, RadixWs& w, int64_t cap) {
     const int64_t c = cap > 0 ? cap : 1;
@@ -45,11 +70,13 @@ void plan_radix_ws(Arena& a, RadixWs& w, int64_t cap) {
     w.zero = a.take<uint32_t>(radix_zero_words(c));
     w.ghist = w.zero;
     w.ctr = w.zero + kRsPasses * kRsBins;
+    w.mhist = w.ctr + 64;
+    w.tcnt = a.take<uint32_t>((size_t)kRsBins * (kMsMaxBlocks + 1));
     // look-back words, cleared by the sort's own kernels before each use
     w.status = a.take<uint64_t>((size_t)kRsPasses * kRsBins * w.ntiles + w.ntiles);
 }
 
-size_t radix_zero_words(int64_t) { return (size_t)kRsPasses * kRsBins + 64; }
+size_t radix_zero_words(int64_t) { return (size_t)kRsPasses * kRsBins + 64 + kRsBins; }
 
 // the compacted form of a raw key (all ones for an invalid item)
 __device__ inline uint64_t rs_compact(uint64_t k, const SortStats& st) {
@@ -121,6 +148,7 @@ __device__ inline void rs_reduce_stats(const int32_t* rec, uint32_t nrec, int64_
         res.n_invalid = sinv;
         res.invalid_kinds = sflags;
         res.sort_bits = sinv ? 64u : bits;
+        res.msd = 0;
     }
     __syncthreads();
     *out = res;
@@ -132,16 +160,30 @@ __device__ inline int64_t rs_count(const int64_t* count_dev, int64_t cap) {
     return c < 0 ? 0 : (c > cap ? cap : c);
 }
 
-// lanes of this wave whose valid digit d equals this lane's (one ballot per digit bit)
-__device__ inline uint64_t rs_peers(uint32_t d, bool valid) {
-    uint64_t peers = __ballot(valid);
+// lanes of this wave whose valid digit d equals this lane's, on the digit's
+// low nbits bits: one ballot per bit, and per bit the ballot or its complement
+// (XNOR with the lane's bit, sign-extended) on both halves of the mask.
+__device__ inline uint64_t rs_peers(uint32_t d, bool valid, int nbits = kRsBits) {
+    if (nbits < kRsBits) d &= (1u << nbits) - 1u;  // bits above are equal in every lane
+    const uint64_t v = __ballot(valid);
+    int32_t m[kRsBits];
+    uint64_t bal[kRsBits];
 #pragma unroll
     for (int b = 0; b < kRsBits; ++b) {
-        const uint64_t bal = __ballot((d >> b) & 1);
-        peers &= ((d >> b) & 1) ? bal : ~bal;
+        m[b] = (int32_t)(d << (31 - b)) >> 31;
+        bal[b] = __ballot(m[b] < 0);
     }
-    return peers;
+    uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+#pragma unroll
+    for (int b = 0; b < kRsBits; ++b) {
+        lo &= ~((uint32_t)bal[b] ^ (uint32_t)m[b]);
+        hi &= ~((uint32_t)(bal[b] >> 32) ^ (uint32_t)m[b]);
+    }
+    return ((uint64_t)hi << 32) | lo;
 }
+
+// the bucket of a compacted key: its top 8 significant bits
+__device__ inline uint32_t ms_shift(const SortStats& st) { return st.sort_bits > kRsBits ? st.sort_bits - kRsBits : 0u; }
 
 // Statistics (block 0 stores them) and the digit histograms of every pass
 // that the significant bits need, over this block's keys.
@@ -150,11 +192,10 @@ __device__ inline uint64_t rs_peers(uint32_t d, bool valid) {
 // its time goes into waiting for loads), up to kRhMaxBlocks that stride over
 // the rest.  Block b also clears the look-back words of pass 0 and of the
 // consumer's scan of pass tiles b, b + grid, ...
-constexpr int kRhThreads = 256;
-constexpr int kRhTile = kRhThreads * kRsItems;
-constexpr unsigned kRhMaxBlocks = 1024;
+// With `msd` (one block per kRhTile keys) each block also stores its bucket
+// counts in tcnt[bucket][block] and adds them to mhist.
 __global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t* count_dev, int64_t cap,
-                                                         uint32_t nrec, int64_t ntiles) {
+                                                         uint32_t nrec, int64_t ntiles, int msd) {
     static_assert(kRsBins == kRhThreads, "thread t clears digit t's look-back word");
     const int64_t count = rs_count(count_dev, cap);
     const int64_t base = (int64_t)blockIdx.x * kRhTile;
@@ -172,9 +213,12 @@ __global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t
     rs_reduce_stats(w.rec, nrec, count, &st);
     if (blockIdx.x == 0 && threadIdx.x == 0) *w.st = st;
     __shared__ uint32_t hist[kRsPasses][kRsBins];
+    __shared__ uint32_t mh[kRsBins];
     for (int e = threadIdx.x; e < kRsPasses * kRsBins; e += kRhThreads) (&hist[0][0])[e] = 0;
+    mh[threadIdx.x] = 0;
     __syncthreads();
     const int passes = rs_passes(st);
+    const uint32_t sh = ms_shift(st);
     // grid-stride over blocks of kRhTile keys (the first one's keys are loaded above)
     for (int64_t b0 = base; b0 < count; b0 += (int64_t)gridDim.x * kRhTile) {
         if (b0 != base) {
@@ -191,6 +235,7 @@ __global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t
                 const uint64_t ck = rs_compact(raw[r], st);
                 for (int p = 0; p < passes; ++p)
                     atomicAdd(&hist[p][(uint32_t)(ck >> (kRsBits * p)) & (kRsBins - 1)], 1u);  // LDS
+                if (msd) atomicAdd(&mh[(uint32_t)(ck >> sh)], 1u);  // LDS
             }
         }
     }
@@ -198,6 +243,213 @@ __global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t
     for (int e = threadIdx.x; e < passes * kRsBins; e += kRhThreads) {
         const uint32_t c = (&hist[0][0])[e];
         if (c) atomicAdd(&w.ghist[e], c);
+    }
+    if (msd) {
+        const uint32_t c = mh[threadIdx.x];
+        w.tcnt[(size_t)threadIdx.x * kMsMaxBlocks + blockIdx.x] = c;
+        if (c) atomicAdd(&w.mhist[threadIdx.x], c);
+    }
+}
+
+// Whether the bucket sort can order the keys (the same answer in every block:
+// it depends on the statistics and the bucket sizes only).  Every thread of the
+// block takes part; threads t < kRsBins read bucket t's size.
+__device__ inline bool ms_fits(const RadixWs& w, const SortStats& st) {
+    const bool over = threadIdx.x < kRsBins && w.mhist[threadIdx.x] > (uint32_t)kMsCap;
+    const bool bad = over || st.n_invalid != 0 || st.sort_bits > 32;
+    return !__syncthreads_or(bad);
+}
+// bucket bases (exclusive prefix of the sizes), published by the scatter's block 0
+__device__ inline uint32_t* ms_bases(const RadixWs& w) { return w.tcnt + (size_t)kRsBins * kMsMaxBlocks; }
+
+// Every item into its bucket, stable: bucket base (sizes of the buckets below)
+// + the bucket's counts in the blocks before this one + the item's rank among
+// the block's items of that bucket (index order).  Blocks of kRhTile keys, as
+// the histogram's.  An item leaves as one word: its original index above the
+// key bits below the bucket's.  Block 0 records that the bucket sort runs
+// (st.msd) and publishes the bucket bases.
+__global__ __launch_bounds__(kRhThreads) void k_ms_scatter(RadixWs w, const int64_t* count_dev, int64_t cap) {
+    constexpr int NWV = kRhThreads / 64;
+    constexpr int kChunk = 16;  // column loads in flight per thread (4 counts each)
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const SortStats st = *w.st;
+    if (!ms_fits(w, st)) return;
+    const int64_t count = rs_count(count_dev, cap);
+    const int64_t base = (int64_t)blockIdx.x * kRhTile;
+    uint64_t raw[kRsItems];
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r) {
+        const int64_t i = base + r * kRhThreads + t;
+        raw[r] = i < count ? w.ka[i] : 0ull;
+    }
+    // thread t: bucket t's first position for this block
+    const uint32_t size = w.mhist[t];
+    uint32_t pre = 0;
+    {
+        const uint4* col = (const uint4*)(w.tcnt + (size_t)t * kMsMaxBlocks);
+        const uint32_t nb = blockIdx.x;
+        for (uint32_t c0 = 0; c0 * 4 < nb; c0 += kChunk) {
+            uint4 v[kChunk];
+#pragma unroll
+            for (int c = 0; c < kChunk; ++c) v[c] = (4 * (c0 + c) < nb) ? col[c0 + c] : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+            for (int c = 0; c < kChunk; ++c) {
+                const uint32_t q = 4 * (c0 + c);
+                pre += (q < nb ? v[c].x : 0u) + (q + 1 < nb ? v[c].y : 0u) + (q + 2 < nb ? v[c].z : 0u) +
+                       (q + 3 < nb ? v[c].w : 0u);
+            }
+        }
+    }
+    __shared__ int lds[NWV + 1];
+    __shared__ uint32_t dbase[kRsBins];
+    __shared__ uint16_t cnt[kRsItems][NWV][kRsBins];
+    for (int e = t; e < kRsItems * NWV * kRsBins; e += kRhThreads) (&cnt[0][0][0])[e] = 0;
+    int all;
+    const uint32_t bb = (uint32_t)block_exclusive_scan((int)size, lds, &all);  // syncs: cnt is clear after it
+    if (blockIdx.x == 0) {
+        ms_bases(w)[t] = bb;
+        if (t == 0) w.st->msd = 1u;
+    }
+    if (base >= count) return;
+    dbase[t] = bb + pre;
+    const uint32_t sh = ms_shift(st);
+    const uint64_t lowmask = (1ull << sh) - 1;
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    uint64_t ck[kRsItems];
+    uint32_t dg[kRsItems], rank[kRsItems];
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r) {
+        const bool valid = base + r * kRhThreads + t < count;
+        ck[r] = valid ? rs_compact(raw[r], st) : 0ull;
+        dg[r] = (uint32_t)(ck[r] >> sh);
+        const uint64_t peers = rs_peers(dg[r], valid);
+        rank[r] = (uint32_t)__popcll(peers & lt);
+        if (valid && rank[r] == 0) cnt[r][wave][dg[r]] = (uint16_t)__popcll(peers);
+    }
+    __syncthreads();
+    {
+        // bucket t: offsets over (round, wave) in index order
+        uint32_t run = 0;
+#pragma unroll
+        for (int r = 0; r < kRsItems; ++r)
+#pragma unroll
+            for (int q = 0; q < NWV; ++q) {
+                const uint32_t c = cnt[r][q][t];
+                cnt[r][q][t] = (uint16_t)run;
+                run += c;
+            }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r) {
+        const int64_t i = base + r * kRhThreads + t;
+        if (i < count) {
+            const uint32_t pos = dbase[dg[r]] + cnt[r][wave][dg[r]] + rank[r];
+            w.kb[pos] = ((uint64_t)(uint32_t)i << 32) | (ck[r] & lowmask);
+        }
+    }
+}
+
+// One workgroup per bucket: its items (in kb, stable) sorted by the bits below
+// the bucket's, 8 at a time, in LDS.  Wave q holds the items
+// [q * R * 64, (q + 1) * R * 64) of the current order, R = ceil(size / 1024)
+// rounds of 64; an item's new place is the count of items of smaller digit
+// plus those of its digit in the waves before plus the wave's running count of
+// that digit (in LDS, read by every lane and advanced by the digit's first
+// lane, round by round).  The sorted bucket goes to ka / va at the same
+// positions.
+__global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w) {
+    constexpr int NWV = kMsThreads / 64;
+    static_assert(kRsBins * 4 == kMsThreads, "thread t scans digit t / 4 over waves 4 (t % 4) ..");
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const SortStats st = *w.st;
+    const uint32_t b = blockIdx.x;
+    const uint32_t size = w.mhist[b];
+    const uint32_t base = ms_bases(w)[b];
+    if (!st.msd || size == 0) return;
+    const uint32_t sh = ms_shift(st);
+    const uint32_t R = (size + kMsThreads - 1) / kMsThreads;
+    uint32_t key[kMsRounds], val[kMsRounds], rk[kMsRounds];
+#pragma unroll
+    for (int r = 0; r < kMsRounds; ++r) {
+        const uint32_t e = (wave * R + r) * 64 + lane;
+        const uint64_t x = ((uint32_t)r < R && e < size) ? w.kb[base + e] : 0ull;
+        key[r] = (uint32_t)x;
+        val[r] = (uint32_t)(x >> 32);
+    }
+    __shared__ uint64_t buf[kMsCap];
+    __shared__ uint32_t wc[NWV][kRsBins];
+    __shared__ int lds[NWV + 1];
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int passes = (int)((sh + kRsBits - 1) / kRsBits);
+    for (int p = 0; p < passes; ++p) {
+        // the wave's counts start at zero (the last pass's readers have passed
+        // the barrier after the scatter)
+        for (int e = lane; e < kRsBins; e += 64) wc[wave][e] = 0u;
+        const int nb = (int)sh - kRsBits * p < kRsBits ? (int)sh - kRsBits * p : kRsBits;  // bits of this digit
+#pragma unroll
+        for (int r = 0; r < kMsRounds; ++r) {
+            if ((uint32_t)r >= R) continue;
+            const uint32_t e = (wave * R + r) * 64 + lane;
+            const bool valid = e < size;
+            const uint32_t d = (key[r] >> (kRsBits * p)) & (kRsBins - 1);
+            const uint64_t peers = rs_peers(d, valid, nb);
+            const uint32_t lr = (uint32_t)__popcll(peers & lt);
+            // every lane reads the count before the digit's first lane adds this
+            // round's (one wave's LDS accesses take effect in program order)
+            const uint32_t prev = wc[wave][d];
+            rk[r] = prev + lr;
+            if (valid && lr == 0) wc[wave][d] = prev + (uint32_t)__popcll(peers);
+        }
+        __syncthreads();
+        {
+            // offsets in (digit, wave) order
+            const int d = t >> 2, q0 = (t & 3) * 4;
+            uint32_t c[4], sum = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                c[j] = wc[q0 + j][d];
+                sum += c[j];
+            }
+            int tot;
+            uint32_t run = (uint32_t)block_exclusive_scan((int)sum, lds, &tot);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                wc[q0 + j][d] = run;
+                run += c[j];
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < kMsRounds; ++r) {
+            if ((uint32_t)r >= R) continue;
+            const uint32_t e = (wave * R + r) * 64 + lane;
+            if (e < size) {
+                const uint32_t d = (key[r] >> (kRsBits * p)) & (kRsBins - 1);
+                buf[wc[wave][d] + rk[r]] = ((uint64_t)val[r] << 32) | key[r];
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < kMsRounds; ++r) {
+            if ((uint32_t)r >= R) continue;
+            const uint32_t e = (wave * R + r) * 64 + lane;
+            if (e < size) {
+                const uint64_t x = buf[e];
+                key[r] = (uint32_t)x;
+                val[r] = (uint32_t)(x >> 32);
+            }
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int r = 0; r < kMsRounds; ++r) {
+        if ((uint32_t)r >= R) continue;
+        const uint32_t e = (wave * R + r) * 64 + lane;
+        if (e < size) {
+            w.ka[base + e] = ((uint64_t)b << sh) | key[r];
+            w.va[base + e] = val[r];
+        }
     }
 }
 
@@ -373,13 +625,17 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_pass(RadixWs w, Header* h, co
 // publishes each pass's scatter (device-scope fences) before the next reads
 // it; a wait past kRsSpinLimit polls records an error and goes on, so every
 // workgroup ends.
+// With first = 0 it is the bucket sort's fallback: it exits at once when the
+// bucket sort has ordered the keys.
 __global__ __launch_bounds__(kRsThreads) void k_rs_tail(RadixWs w, Header* h, const int64_t* count_dev, int64_t cap,
                                                         int first, int64_t ntiles) {
     const uint32_t bits = w.st->sort_bits;
-    if ((uint32_t)(kRsBits * first) >= bits) return;
+    if (first > 0 && (uint32_t)(kRsBits * first) >= bits) return;
+    if (first == 0 && w.st->msd) return;
     extern __shared__ __align__(16) unsigned char rs_smem[];
     const int64_t count = rs_count(count_dev, cap);
-    for (int pass = first; pass < kRsPasses && (uint32_t)(kRsBits * pass) < bits; ++pass) {
+    // pass 0 always runs: it writes the compacted keys and the payload
+    for (int pass = first; pass < kRsPasses && (pass == 0 || (uint32_t)(kRsBits * pass) < bits); ++pass) {
         if (pass > first) {
             // grid barrier: every workgroup has finished pass - 1 (each wave
             // releases its scatter before the arrival, and acquires after it)
@@ -400,7 +656,11 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_tail(RadixWs w, Header* h, co
             __syncthreads();
             __threadfence();
         }
-        while (rs_pass_tile<false>(w, h, count, ntiles, pass, rs_smem)) __syncthreads();
+        if (pass == 0) {
+            while (rs_pass_tile<true>(w, h, count, ntiles, pass, rs_smem)) __syncthreads();
+        } else {
+            while (rs_pass_tile<false>(w, h, count, ntiles, pass, rs_smem)) __syncthreads();
+        }
     }
 }
 
@@ -418,8 +678,17 @@ void launch_radix_sort(hipStream_t s, const RadixWs& w, Header* h, const int64_t
     (void)lds_ok;
     // at most kRhMaxBlocks blocks (each adds its counts with global atomics)
     unsigned nh = (unsigned)blocks_for(cap > 0 ? cap : 1, kRhTile);
+    if (nh <= kMsMaxBlocks) {
+        // the bucket sort; when it cannot order the keys, the passes in one
+        // launch (one workgroup per tile, all resident for the grid barrier)
+        k_rs_hist<<<nh, kRhThreads, 0, s>>>(w, count_dev, cap, nrec, (int64_t)nt, 1);
+        k_ms_scatter<<<nh, kRhThreads, 0, s>>>(w, count_dev, cap);
+        k_ms_bucket<<<kRsBins, kMsThreads, 0, s>>>(w);
+        k_rs_tail<<<nt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, 0, (int64_t)nt);
+        return;
+    }
     if (nh > kRhMaxBlocks) nh = kRhMaxBlocks;
-    k_rs_hist<<<nh, kRhThreads, 0, s>>>(w, count_dev, cap, nrec, (int64_t)nt);
+    k_rs_hist<<<nh, kRhThreads, 0, s>>>(w, count_dev, cap, nrec, (int64_t)nt, 0);
     // the significant bits are known on the device only: the first kRsHeadPasses
     // passes are a launch each (a pass past the bits exits at once), and the
     // passes after them share one launch

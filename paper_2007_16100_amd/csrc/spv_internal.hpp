@@ -19,14 +19,16 @@ __device__ inline int block_exclusive_scan(int v, int* lds, int* total) {
     }
     if (lane == 63) lds[wave] = x;
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int run = 0;
-        for (int w = 0; w < nw; ++w) {
-            int t = lds[w];
-            lds[w] = run;
-            run += t;
+    if (wave == 0) {
+        // the wave totals scanned by wave 0
+        const int t = lane < nw ? lds[lane] : 0;
+        int y = t;
+        for (int d = 1; d < nw; d <<= 1) {
+            const int u = __shfl_up(y, d, 64);
+            if (lane >= d) y += u;
         }
-        lds[nw] = run;
+        if (lane < nw) lds[lane] = y - t;
+        if (lane == nw - 1) lds[nw] = y;
     }
     __syncthreads();
     int r = lds[wave] + x - v;
@@ -106,6 +108,7 @@ struct SortStats {
     uint32_t sort_bits; // significant bits of the compacted key (64 when any item is invalid)
     uint32_t n_invalid; // items with an invalid key (radix sort of pairs only)
     uint32_t invalid_kinds;  // bit 0: a non-finite item, bit 1: an item out of the key range
+    uint32_t msd;       // radix sort of pairs: 1 when the bucket sort ordered the keys (result in ka / va)
 };
 struct SortBufs {
     uint64_t* a;       // [cap] input keys / ping
@@ -143,7 +146,7 @@ __device__ inline uint64_t sorted_key(const SortBufs& sb, int64_t r) {
 // out-of-range item counts.  It also zeroes zero[0..radix_zero_words).  After
 // launch_radix_sort the compacted keys, ascending, and the items' original
 // indices sit in rs_keys / rs_vals (which of the two buffers depends on the
-// number of passes, known on the device).
+// path taken and the number of passes, both known on the device only).
 constexpr int kRsThreads = 512;
 constexpr int kRsItems = 4;
 constexpr int kRsTile = kRsThreads * kRsItems;  // keys per tile
@@ -164,6 +167,8 @@ struct RadixWs {
     uint32_t* zero;     // the region the producer zeroes (radix_zero_words):
     uint32_t* ghist;    //   [kRsPasses][kRsBins] digit counts over all keys
     uint32_t* ctr;      //   [64] tile counters (0 .. kRsPasses-1 the passes, 8.. for the consumers)
+    uint32_t* mhist;    //   [kRsBins] bucket sizes (the top digit) of the bucket sort
+    uint32_t* tcnt;     // [histogram blocks][kRsBins] per-block bucket counts of the bucket sort
     uint64_t* status;   // [kRsPasses][ntiles][kRsBins] look-back words, then [ntiles] for a consumer's scan:
                         // the histogram kernel clears pass 0's and the consumer's, pass p clears pass p+1's
 };
@@ -180,10 +185,10 @@ __host__ __device__ inline int rs_passes(const SortStats& st) {
 // the look-back words a consumer of the sort may use for a scan of its own over the tiles
 __host__ __device__ inline uint64_t* rs_consumer_status(const RadixWs& w) { return w.status + (size_t)kRsPasses * kRsBins * w.ntiles; }
 __device__ inline const uint64_t* rs_keys(const RadixWs& w, const SortStats& st) {
-    return (rs_passes(st) & 1) ? w.kb : w.ka;
+    return (!st.msd && (rs_passes(st) & 1)) ? w.kb : w.ka;
 }
 __device__ inline const uint32_t* rs_vals(const RadixWs& w, const SortStats& st) {
-    return (rs_passes(st) & 1) ? w.vb : w.va;
+    return (!st.msd && (rs_passes(st) & 1)) ? w.vb : w.va;
 }
 // the packed key of a compacted key
 __device__ inline uint64_t rs_expand(uint64_t ck, const SortStats& st) {

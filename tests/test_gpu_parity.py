@@ -259,6 +259,41 @@ def test_voxelize_wide_keys_many_tiles(spv):
     np.testing.assert_array_equal(vf, rvf)
 
 
+def _bucket_case(case):
+    """Points on a 1 m grid (v = 1): x spans 0..4095 voxels, y 0..63, z 0..31, so
+    the compacted key has 12 + 6 + 5 bits and its top 8 bits (the sort's bucket)
+    are x // 16."""
+    rng = np.random.default_rng(6161)
+    if case == "narrow":  # 6 significant bits: the buckets alone order the keys
+        vox = rng.integers(0, 3, size=(9000, 3))
+    elif case == "most_blocks":  # 256 histogram blocks of 1024 keys exactly
+        vox = np.stack([rng.integers(0, 4096, 262_144), rng.integers(0, 64, 262_144),
+                        rng.integers(0, 32, 262_144)], 1)
+    else:  # bucket 0 holds 16384 items (the bucket sort's capacity) or one more
+        k = 16_384 if case == "cap" else 16_385
+        a = np.stack([rng.integers(0, 16, k), rng.integers(0, 64, k), rng.integers(0, 32, k)], 1)
+        b = np.stack([rng.integers(16, 4096, 30_000), rng.integers(0, 64, 30_000), rng.integers(0, 32, 30_000)], 1)
+        a[0] = (0, 0, 0)
+        b[0] = (4095, 63, 31)
+        vox = np.concatenate([b[: 20_000], a, b[20_000:]])
+    return (vox + rng.uniform(0.1, 0.9, size=vox.shape)).astype(np.float32)
+
+
+@pytest.mark.parametrize("case", ["narrow", "cap", "over", "most_blocks"])
+def test_voxelize_bucket_sort_bounds(spv, case):
+    """The sort's bucket path at its limits: keys the buckets alone order, a bucket
+    at the in-LDS capacity, one item over it (the passes run instead), and the
+    most histogram blocks the bucket path takes."""
+    xyz = _bucket_case(case)
+    feat = synth.normal((len(xyz), 8), 6162, dtype="bf16")
+    c, vf, cnt, p2v, _ = run_voxelize(spv, xyz, 1.0, feat, "bf16")
+    rc, rvf, rcnt, rp2v = oracle.voxelize(xyz, 1.0, feat, "bf16")
+    np.testing.assert_array_equal(c, rc)
+    np.testing.assert_array_equal(cnt, rcnt)
+    np.testing.assert_array_equal(p2v, rp2v)
+    np.testing.assert_array_equal(vf, rvf)
+
+
 def test_voxelize_over_a_million_points(spv):
     """2.2M points (a sixth of them sharing voxels) over +-900 m: the quantize and histogram
     kernels stride with their largest grids (1024 blocks), the sort launches every pass
