@@ -42,7 +42,7 @@ void plan_kmap_ws(Arena& a, KmapWs& w, int64_t m_cap, int K, int stride, bool ow
     if (stride == 2) {
         uint32_t S = table_capacity(mc);
         w.coarse = take_table(a, S);
-        plan_sort_ws(a, w.sort, mc);
+        plan_radix_ws(a, w.rs, mc);
     } else {
         w.coarse = Table{nullptr, 0};
     }
@@ -82,43 +82,60 @@ __global__ void k_map_same_count(const int64_t* m_in_dev, int64_t cap, int64_t* 
 
 // stride 2: coarse keys into the coarse table; each block appends the keys it
 // created to the key list and records their per-field min / max for the sort
-__global__ __launch_bounds__(kAppendThreads) void k_map_coarse_insert(Header* h, Table coarse, SortBufs sb,
-                                                                      int64_t* cnt, const int32_t* in_coords,
+// Every input's coarse key floor(c / 2) into the coarse table; each key the
+// table did not hold yet is appended to the sort's key list (rs.ka, counter
+// cnt).  Grid-stride over the inputs, one sort record per block (per-field
+// minima / maxima of the block's new keys, no invalid items); the same launch
+// zeroes the sort's counters and histograms.
+__global__ __launch_bounds__(kAppendThreads) void k_map_coarse_insert(Header* h, Table coarse, RadixWs rs,
+                                                                      int64_t nzero, int64_t* cnt,
+                                                                      const int32_t* in_coords,
                                                                       const int64_t* m_in_dev, int64_t cap) {
     const int64_t m = count_or_cap(m_in_dev, cap);
-    const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    bool created = false;
-    uint64_t key = kEmpty;
-    int f[4] = {0, 0, 0, 0};
-    if (i < m) {
-        const int32_t* c = in_coords + 4 * i;
-        // floor(c / 2) via arithmetic shift
-        f[0] = c[0];
-        f[1] = c[1] >> 1;
-        f[2] = c[2] >> 1;
-        f[3] = c[3] >> 1;
-        key = pack_key(f[0], f[1], f[2], f[3]);
-    }
-    // sorted fine voxels: neighbours in z often share a coarse voxel, and a lane
-    // whose key equals the previous lane's leaves the insert to its run's head
-    const uint64_t prev_key = __shfl_up(key, 1, 64);
-    if (key != kEmpty && ((threadIdx.x & 63) == 0 || prev_key != key)) {
-        uint32_t slot;
-        const int r = table_insert(coarse, key, &slot);
-        created = r > 0;
-        if (r < 0) raise_flag(h, kFlagTableFull);
-    }
+    const int64_t stride = (int64_t)gridDim.x * kAppendThreads;
+    for (int64_t i = blockIdx.x * (int64_t)kAppendThreads + threadIdx.x; i < nzero; i += stride) rs.zero[i] = 0u;
     int mn[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
     int mx[4] = {(int)0x80000000, (int)0x80000000, (int)0x80000000, (int)0x80000000};
-    if (created) {
+    for (int64_t b0 = blockIdx.x * (int64_t)kAppendThreads; b0 < m; b0 += stride) {  // the same trip count in the block
+        const int64_t i = b0 + threadIdx.x;
+        bool created = false;
+        uint64_t key = kEmpty;
+        int f[4] = {0, 0, 0, 0};
+        if (i < m) {
+            const int32_t* c = in_coords + 4 * i;
+            // floor(c / 2) via arithmetic shift
+            f[0] = c[0];
+            f[1] = c[1] >> 1;
+            f[2] = c[2] >> 1;
+            f[3] = c[3] >> 1;
+            key = pack_key(f[0], f[1], f[2], f[3]);
+        }
+        // sorted fine voxels: neighbours in z often share a coarse voxel, and a lane
+        // whose key equals the previous lane's leaves the insert to its run's head
+        const uint64_t prev_key = __shfl_up(key, 1, 64);
+        if (key != kEmpty && ((threadIdx.x & 63) == 0 || prev_key != key)) {
+            uint32_t slot;
+            const int r = table_insert(coarse, key, &slot);
+            created = r > 0;
+            if (r < 0) raise_flag(h, kFlagTableFull);
+        }
+        if (created) {
 #pragma unroll
-        for (int d = 0; d < 4; ++d) mn[d] = mx[d] = f[d];
+            for (int d = 0; d < 4; ++d) {
+                mn[d] = min(mn[d], f[d]);
+                mx[d] = max(mx[d], f[d]);
+            }
+        }
+        block_append(created, key, rs.ka, cnt);
     }
-    block_append(created, key, sb.a, cnt);
-    block_minmax_record(mn, mx, sb.part + 8 * blockIdx.x);
+    int32_t* rec = rs.rec + (size_t)kRsRecWords * blockIdx.x;
+    block_minmax_record(mn, mx, rec);
+    if (threadIdx.x == 0) rec[8] = rec[9] = 0;  // no invalid keys
 }
 
-__global__ void k_map_coarse_rank(SortBufs sb, Table coarse, const int64_t* cnt, int64_t cap, int32_t* out_coords,
+// The sorted coarse keys in order: output r's coordinates, and r as its
+// coarse-table value.
+__global__ void k_map_coarse_rank(RadixWs rs, Table coarse, const int64_t* cnt, int64_t cap, int32_t* out_coords,
                                   int64_t* m_out, int64_t* m_out_user) {
     int64_t m = count_or_cap(cnt, cap);
     int64_t r = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
@@ -127,7 +144,8 @@ __global__ void k_map_coarse_rank(SortBufs sb, Table coarse, const int64_t* cnt,
         if (m_out_user) *m_out_user = m;
     }
     if (r >= m) return;
-    uint64_t key = sorted_key(sb, r);
+    const SortStats st = *rs.st;
+    const uint64_t key = rs_expand(rs_keys(rs, st)[r], st);
     int64_t slot = table_slot(coarse, key);
     if (slot >= 0) *slot_val(coarse, (uint32_t)slot) = (int32_t)r;
     out_coords[4 * r + 0] = key_b(key);
@@ -391,11 +409,13 @@ void launch_kernel_map(hipStream_t s, const KmapWs& w, bool build_fine, const in
         // coarse table, status header (unless cleared above) and the coarse key
         // counter in one launch
         launch_clear(s, w.h, w.coarse, clear_header && !fine, w.m_out + 1);
-        const unsigned nins = blocks_for(mc, kAppendThreads);
-        k_map_coarse_insert<<<nins, kAppendThreads, 0, s>>>(w.h, w.coarse, w.sort, w.m_out + 1, in_coords, m_in_dev,
-                                                            mc);
-        launch_sort_keys(s, w.sort, w.m_out + 1, mc, nins);
-        k_map_coarse_rank<<<nblk, kMapThreads, 0, s>>>(w.sort, w.coarse, w.m_out + 1, mc, out_coords, w.m_out,
+        // at most kRsMaxRecords insert blocks: every histogram block reduces their records
+        unsigned nins = blocks_for(mc, kAppendThreads);
+        if (nins > kRsMaxRecords) nins = kRsMaxRecords;
+        k_map_coarse_insert<<<nins, kAppendThreads, 0, s>>>(w.h, w.coarse, w.rs, (int64_t)radix_zero_words(mc),
+                                                            w.m_out + 1, in_coords, m_in_dev, mc);
+        launch_radix_sort(s, w.rs, w.h, w.m_out + 1, mc, nins);
+        k_map_coarse_rank<<<nblk, kMapThreads, 0, s>>>(w.rs, w.coarse, w.m_out + 1, mc, out_coords, w.m_out,
                                                        m_out_dev);
     }
     if (K == 3) {

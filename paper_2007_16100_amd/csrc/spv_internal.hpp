@@ -94,52 +94,19 @@ void launch_table_build(hipStream_t s, Header* h, Table t, const int32_t* coords
                         int32_t* nbr_upper = nullptr);
 void launch_table_lookup(hipStream_t s, Table t, const int32_t* q, int64_t nq, int32_t* idx);
 
-// --- radix sort of packed voxel keys (hash_sort_scan.hip) ---------------------
-// Sorts keys a[0..*count) ascending.  The per-field minima and maxima come from
-// partial records (4 minima + 4 maxima each) written by the producer of the keys
-// (nparts of them) or, with nparts = 0, by the sort itself; the keys are then
-// compacted (minimum subtracted, fields packed into the fewest bits) and sorted
-// with stable 8-bit LSD passes; passes beyond the significant bits do nothing.
-// The result is read back with sorted_key() from whichever buffer holds it.
+// --- statistics of the keys being sorted (radix.hip) -------------------------
+// The per-field minima and maxima of the keys; a key is sorted in compacted form
+// (minimum subtracted, fields packed into the fewest bits).
 struct SortStats {
     int32_t fmin[4];    // per-field minimum of the keys being sorted (b, x, y, z)
     int32_t fmax[4];
     uint32_t fbits[4];  // bit width of each compacted field
     uint32_t sort_bits; // significant bits of the compacted key (64 when any item is invalid)
-    uint32_t n_invalid; // items with an invalid key (radix sort of pairs only)
+    uint32_t n_invalid; // items with an invalid key
     uint32_t invalid_kinds;  // bit 0: a non-finite item, bit 1: an item out of the key range
-    uint32_t msd;       // radix sort of pairs: 1 when the bucket sort ordered the keys (result in ka / va)
+    uint32_t msd;       // 1 when the bucket sort ordered the keys (result in ka / va)
 };
-struct SortBufs {
-    uint64_t* a;       // [cap] input keys / ping
-    uint64_t* b;       // [cap] pong
-    uint32_t* hist;    // [256 * nblocks(cap)]
-    int32_t* part;     // [sort_part_records(cap)][8] partial min / max records
-    SortStats* st;
-    int32_t* scan_tmp; // scan partials for the many-tile offsets
-};
-void plan_sort_ws(Arena& a, SortBufs& sb, int64_t cap);
-size_t sort_hist_entries(int64_t cap);
-// records a producer with blocks of kAppendThreads over cap items may write
-size_t sort_part_records(int64_t cap);
-void launch_sort_keys(hipStream_t s, SortBufs bufs, const int64_t* count_dev, int64_t cap, uint32_t nparts);
-// the sorted key of rank r (decompacted), valid after launch_sort_keys
-__device__ inline uint64_t sorted_key(const SortBufs& sb, int64_t r) {
-    const SortStats* st = sb.st;
-    int passes = (int)((st->sort_bits + 7) / 8);
-    uint64_t ck = (passes & 1) ? sb.b[r] : sb.a[r];
-    uint32_t bz = st->fbits[3], by = st->fbits[2], bx = st->fbits[1];
-    int z = (int)(ck & ((1ull << bz) - 1)) + st->fmin[3];
-    ck >>= bz;
-    int y = (int)(ck & ((1ull << by) - 1)) + st->fmin[2];
-    ck >>= by;
-    int x = (int)(ck & ((1ull << bx) - 1)) + st->fmin[1];
-    ck >>= bx;
-    int b = (int)ck + st->fmin[0];
-    return pack_key(b, x, y, z);
-}
-
-// --- radix sort of (key, payload) pairs, one launch per digit (radix.hip) -------
+// --- radix sort of (key, payload) pairs (radix.hip) ---------------------------
 // The producer writes raw packed keys (kEmpty: invalid item) to ka[0..count) and,
 // per block of kRsProducerBlock items, a record of kRsRecWords ints: per-field
 // minima (4) and maxima (4) of its valid keys, then its non-finite and
@@ -244,7 +211,7 @@ struct KmapWs {
     Header* h;          // assigned by the caller
     Table fine;         // table of the input coords (assigned by the caller when shared)
     Table coarse;       // stride 2: table of the output coords
-    SortBufs sort;      // stride 2: coarse key sort
+    RadixWs rs;         // stride 2: coarse key sort
     uint32_t* bcnt;     // [K3 * nblk] per-block per-offset counts (k-major)
     uint32_t* bbase;    // [K3 * nblk + 1]
     int32_t* scan_tmp;  // [scan_tmp_entries(K3 * nblk)]
