@@ -369,6 +369,9 @@ __global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w) {
     if (!st.msd || size == 0) return;
     const uint32_t sh = ms_shift(st);
     const uint32_t R = (size + kMsThreads - 1) / kMsThreads;
+    // this wave's rounds that hold items (rounds past the bucket are skipped)
+    const uint32_t first = wave * R * 64;
+    const uint32_t Rw = first >= size ? 0u : ((size - first + 63) / 64 < R ? (size - first + 63) / 64 : R);
     uint32_t key[kMsRounds], val[kMsRounds], rk[kMsRounds];
 #pragma unroll
     for (int r = 0; r < kMsRounds; ++r) {
@@ -389,7 +392,7 @@ __global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w) {
         const int nb = (int)sh - kRsBits * p < kRsBits ? (int)sh - kRsBits * p : kRsBits;  // bits of this digit
 #pragma unroll
         for (int r = 0; r < kMsRounds; ++r) {
-            if ((uint32_t)r >= R) continue;
+            if ((uint32_t)r >= Rw) continue;
             const uint32_t e = (wave * R + r) * 64 + lane;
             const bool valid = e < size;
             const uint32_t d = (key[r] >> (kRsBits * p)) & (kRsBins - 1);
@@ -422,7 +425,7 @@ __global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w) {
         __syncthreads();
 #pragma unroll
         for (int r = 0; r < kMsRounds; ++r) {
-            if ((uint32_t)r >= R) continue;
+            if ((uint32_t)r >= Rw) continue;
             const uint32_t e = (wave * R + r) * 64 + lane;
             if (e < size) {
                 const uint32_t d = (key[r] >> (kRsBits * p)) & (kRsBins - 1);
@@ -432,7 +435,7 @@ __global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w) {
         __syncthreads();
 #pragma unroll
         for (int r = 0; r < kMsRounds; ++r) {
-            if ((uint32_t)r >= R) continue;
+            if ((uint32_t)r >= Rw) continue;
             const uint32_t e = (wave * R + r) * 64 + lane;
             if (e < size) {
                 const uint64_t x = buf[e];
@@ -444,7 +447,7 @@ __global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w) {
     }
 #pragma unroll
     for (int r = 0; r < kMsRounds; ++r) {
-        if ((uint32_t)r >= R) continue;
+        if ((uint32_t)r >= Rw) continue;
         const uint32_t e = (wave * R + r) * 64 + lane;
         if (e < size) {
             w.ka[base + e] = ((uint64_t)b << sh) | key[r];
