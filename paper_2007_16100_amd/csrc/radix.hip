@@ -23,14 +23,19 @@
 // Up to kMsMaxBlocks histogram blocks of keys, a bucket sort takes the place of
 // the passes when it can (every item valid, at most 32 significant bits, and no
 // bucket over kMsCap items):
-//   k_rs_hist    also counts, per block, the top 8 significant bits (the
-//                bucket) of its keys;
-//   k_ms_scatter moves every item into its bucket, stable: the bucket's base
-//                plus the counts of the blocks before (a plain sum, no
-//                look-back) plus its rank in the block;
-//   k_ms_bucket  one workgroup per bucket sorts the remaining bits in LDS (an
-//                LSD sort of 8-bit digits whose passes never leave the
-//                workgroup) and writes the result in place of the keys.
+//   k_rs_hist    also counts the keys of each fine bin (their top 12
+//                significant bits) over all keys;
+//   k_ms_scatter groups consecutive fine bins into buckets of about equal
+//                item counts (order-preserving: a bucket is a range of fine
+//                bins) and moves every item into its fine bin: the bin's
+//                base, plus the block's share of the bin claimed with one
+//                atomic per bin and block, plus its rank among the block's
+//                items of that bin (index order);
+//   k_ms_bucket  one workgroup per bucket sorts it in LDS by the key bits
+//                below the bucket's first bin and then by the item's block
+//                (an LSD sort of 8-bit digits whose passes never leave the
+//                workgroup), which restores index order between blocks, and
+//                writes the result in place of the keys.
 // Otherwise both exit at once and k_rs_tail runs every pass in one launch.
 // Either way the order is the same stable ascending order.
 #include "spv_internal.hpp"
@@ -50,10 +55,15 @@ size_t radix_tiles(int64_t cap) { return blocks_for(cap > 0 ? cap : 1, kRsTile);
 constexpr int kRhThreads = 256;
 constexpr int kRhTile = kRhThreads * kRsItems;
 constexpr unsigned kRhMaxBlocks = 1024;
-// the bucket sort: at most kMsMaxBlocks histogram blocks (one tile each), at
-// most kMsCap items per bucket, sorted by kMsThreads threads
+// the bucket sort: at most kMsMaxBlocks histogram blocks (one tile of kRhTile
+// keys each, so an item's block fits 8 bits), kMsFine fine bins, at most
+// kMsMaxBuckets buckets of at most kMsCap items, each sorted by kMsThreads
+// threads (two workgroups fit a CU)
 constexpr unsigned kMsMaxBlocks = 256;
-constexpr int kMsThreads = 1024;
+constexpr int kMsFineBits = 12;
+constexpr int kMsFine = 1 << kMsFineBits;
+constexpr int kMsMaxBuckets = 512;
+constexpr int kMsThreads = 512;
 constexpr int kMsRounds = 16;
 constexpr int kMsCap = kMsThreads * kMsRounds;
 
@@ -70,13 +80,14 @@ void plan_radix_ws(Arena& a, RadixWs& w, int64_t cap) {
     w.zero = a.take<uint32_t>(radix_zero_words(c));
     w.ghist = w.zero;
     w.ctr = w.zero + kRsPasses * kRsBins;
-    w.mhist = w.ctr + 64;
-    w.tcnt = a.take<uint32_t>((size_t)kRsBins * (kMsMaxBlocks + 1));
+    w.fhist = w.ctr + 64;
+    w.fcur = w.fhist + kMsFine;
+    w.sb = a.take<uint32_t>(2 * (kMsMaxBuckets + 1) + 1);
     // look-back words, cleared by the sort's own kernels before each use
     w.status = a.take<uint64_t>((size_t)kRsPasses * kRsBins * w.ntiles + w.ntiles);
 }
 
-size_t radix_zero_words(int64_t) { return (size_t)kRsPasses * kRsBins + 64 + kRsBins; }
+size_t radix_zero_words(int64_t) { return (size_t)kRsPasses * kRsBins + 64 + 2 * kMsFine; }
 
 // the compacted form of a raw key (all ones for an invalid item)
 __device__ inline uint64_t rs_compact(uint64_t k, const SortStats& st) {
@@ -163,27 +174,48 @@ __device__ inline int64_t rs_count(const int64_t* count_dev, int64_t cap) {
 // lanes of this wave whose valid digit d equals this lane's, on the digit's
 // low nbits bits: one ballot per bit, and per bit the ballot or its complement
 // (XNOR with the lane's bit, sign-extended) on both halves of the mask.
-__device__ inline uint64_t rs_peers(uint32_t d, bool valid, int nbits = kRsBits) {
-    if (nbits < kRsBits) d &= (1u << nbits) - 1u;  // bits above are equal in every lane
+template <int BITS = kRsBits>
+__device__ inline uint64_t rs_peers(uint32_t d, bool valid, int nbits = BITS) {
+    if (nbits < BITS) d &= (1u << nbits) - 1u;  // bits above are equal in every lane
     const uint64_t v = __ballot(valid);
-    int32_t m[kRsBits];
-    uint64_t bal[kRsBits];
+    int32_t m[BITS];
+    uint64_t bal[BITS];
 #pragma unroll
-    for (int b = 0; b < kRsBits; ++b) {
+    for (int b = 0; b < BITS; ++b) {
         m[b] = (int32_t)(d << (31 - b)) >> 31;
         bal[b] = __ballot(m[b] < 0);
     }
     uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
 #pragma unroll
-    for (int b = 0; b < kRsBits; ++b) {
+    for (int b = 0; b < BITS; ++b) {
         lo &= ~((uint32_t)bal[b] ^ (uint32_t)m[b]);
         hi &= ~((uint32_t)(bal[b] >> 32) ^ (uint32_t)m[b]);
     }
     return ((uint64_t)hi << 32) | lo;
 }
 
-// the bucket of a compacted key: its top 8 significant bits
-__device__ inline uint32_t ms_shift(const SortStats& st) { return st.sort_bits > kRsBits ? st.sort_bits - kRsBits : 0u; }
+// Geometry of the bucket sort for a key of st.sort_bits (at most 32) bits: the
+// fine bin of a compacted key is key >> shF (its top 12 bits, or all of them);
+// a bucket spans at most 2^spanlog fine bins (so the key bits below its first
+// bin fit 24), and A buckets share the items out by count, the bins'
+// spans adding at most kMsFine >> spanlog more.
+struct MsGeom {
+    uint32_t shF, spanlog, A;
+};
+__device__ inline MsGeom ms_geom(const SortStats& st) {
+    MsGeom g;
+    const uint32_t F = st.sort_bits < (uint32_t)kMsFineBits ? st.sort_bits : (uint32_t)kMsFineBits;
+    g.shF = st.sort_bits - F;
+    g.spanlog = 24 - g.shF;
+    g.A = kMsMaxBuckets - 1 - (kMsFine >> (g.spanlog < 31 ? g.spanlog : 31));
+    return g;
+}
+// the bucket of fine bin f, whose items start at excl of total: non-decreasing in f
+__device__ inline uint32_t ms_bucket_of(const MsGeom& g, uint32_t f, uint32_t excl, uint32_t total) {
+    uint32_t a = total ? (uint32_t)((uint64_t)excl * g.A / total) : 0u;
+    if (a > g.A - 1) a = g.A - 1;
+    return a + (f >> g.spanlog);
+}
 
 // Statistics (block 0 stores them) and the digit histograms of every pass
 // that the significant bits need, over this block's keys.
@@ -192,8 +224,8 @@ __device__ inline uint32_t ms_shift(const SortStats& st) { return st.sort_bits >
 // its time goes into waiting for loads), up to kRhMaxBlocks that stride over
 // the rest.  Block b also clears the look-back words of pass 0 and of the
 // consumer's scan of pass tiles b, b + grid, ...
-// With `msd` (one block per kRhTile keys) each block also stores its bucket
-// counts in tcnt[bucket][block] and adds them to mhist.
+// With `msd` (one block per kRhTile keys) each block also adds its fine-bin
+// counts to fhist.
 __global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t* count_dev, int64_t cap,
                                                          uint32_t nrec, int64_t ntiles, int msd) {
     static_assert(kRsBins == kRhThreads, "thread t clears digit t's look-back word");
@@ -213,12 +245,13 @@ __global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t
     rs_reduce_stats(w.rec, nrec, count, &st);
     if (blockIdx.x == 0 && threadIdx.x == 0) *w.st = st;
     __shared__ uint32_t hist[kRsPasses][kRsBins];
-    __shared__ uint32_t mh[kRsBins];
+    __shared__ uint32_t fh[kMsFine];
     for (int e = threadIdx.x; e < kRsPasses * kRsBins; e += kRhThreads) (&hist[0][0])[e] = 0;
-    mh[threadIdx.x] = 0;
+    if (msd)
+        for (int e = threadIdx.x; e < kMsFine; e += kRhThreads) fh[e] = 0;
     __syncthreads();
     const int passes = rs_passes(st);
-    const uint32_t sh = ms_shift(st);
+    const uint32_t shF = ms_geom(st).shF;
     // grid-stride over blocks of kRhTile keys (the first one's keys are loaded above)
     for (int64_t b0 = base; b0 < count; b0 += (int64_t)gridDim.x * kRhTile) {
         if (b0 != base) {
@@ -235,7 +268,7 @@ __global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t
                 const uint64_t ck = rs_compact(raw[r], st);
                 for (int p = 0; p < passes; ++p)
                     atomicAdd(&hist[p][(uint32_t)(ck >> (kRsBits * p)) & (kRsBins - 1)], 1u);  // LDS
-                if (msd) atomicAdd(&mh[(uint32_t)(ck >> sh)], 1u);  // LDS
+                if (msd && st.sort_bits <= 32) atomicAdd(&fh[(uint32_t)(ck >> shF)], 1u);  // LDS
             }
         }
     }
@@ -244,115 +277,172 @@ __global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t
         const uint32_t c = (&hist[0][0])[e];
         if (c) atomicAdd(&w.ghist[e], c);
     }
-    if (msd) {
-        const uint32_t c = mh[threadIdx.x];
-        w.tcnt[(size_t)threadIdx.x * kMsMaxBlocks + blockIdx.x] = c;
-        if (c) atomicAdd(&w.mhist[threadIdx.x], c);
-    }
+    if (msd)
+        for (int e = threadIdx.x; e < kMsFine; e += kRhThreads) {
+            const uint32_t c = fh[e];
+            if (c) atomicAdd(&w.fhist[e], c);
+        }
 }
 
-// Whether the bucket sort can order the keys (the same answer in every block:
-// it depends on the statistics and the bucket sizes only).  Every thread of the
-// block takes part; threads t < kRsBins read bucket t's size.
-__device__ inline bool ms_fits(const RadixWs& w, const SortStats& st) {
-    const bool over = threadIdx.x < kRsBins && w.mhist[threadIdx.x] > (uint32_t)kMsCap;
-    const bool bad = over || st.n_invalid != 0 || st.sort_bits > 32;
-    return !__syncthreads_or(bad);
-}
-// bucket bases (exclusive prefix of the sizes), published by the scatter's block 0
-__device__ inline uint32_t* ms_bases(const RadixWs& w) { return w.tcnt + (size_t)kRsBins * kMsMaxBlocks; }
+// The bucket table the scatter's block 0 publishes: starts[kMsMaxBuckets + 1]
+// (positions), first fine bins[kMsMaxBuckets + 1], then the bucket count.
+__device__ inline uint32_t* ms_starts(const RadixWs& w) { return w.sb; }
+__device__ inline uint32_t* ms_firsts(const RadixWs& w) { return w.sb + kMsMaxBuckets + 1; }
+__device__ inline uint32_t* ms_count(const RadixWs& w) { return w.sb + 2 * (kMsMaxBuckets + 1); }
 
-// Every item into its bucket, stable: bucket base (sizes of the buckets below)
-// + the bucket's counts in the blocks before this one + the item's rank among
-// the block's items of that bucket (index order).  Blocks of kRhTile keys, as
-// the histogram's.  An item leaves as one word: its original index above the
-// key bits below the bucket's.  Block 0 records that the bucket sort runs
-// (st.msd) and publishes the bucket bases.
+// Every item into its fine bin, stable within the block: the bin's base (items
+// of smaller bins), plus the block's share of the bin (claimed with one atomic
+// per bin and block, in whatever order the blocks come), plus the item's rank
+// among the block's items of that bin.  Wave q holds the block's keys
+// [q * 256, (q + 1) * 256) in four rounds of 64, so its running count of a bin
+// (in LDS, read by every lane and advanced by the bin's first lane) and the
+// counts of the waves before give the rank in index order.  Every block also
+// groups the fine bins into buckets from the global counts (the same table in
+// every block), and takes the bucket sort only if no bucket is over kMsCap;
+// block 0 publishes the table and records that the bucket sort runs (st.msd).
+// An item leaves as one word: its original index above its compacted key.
 __global__ __launch_bounds__(kRhThreads) void k_ms_scatter(RadixWs w, const int64_t* count_dev, int64_t cap) {
     constexpr int NWV = kRhThreads / 64;
-    constexpr int kChunk = 16;  // column loads in flight per thread (4 counts each)
+    constexpr int BPT = kMsFine / kRhThreads;  // fine bins per thread
+    static_assert(kRsItems * 64 * NWV == kRhTile, "a wave holds kRsItems rounds of 64 keys");
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const SortStats st = *w.st;
-    if (!ms_fits(w, st)) return;
+    if (st.n_invalid != 0 || st.sort_bits > 32) return;
+    const MsGeom g = ms_geom(st);
     const int64_t count = rs_count(count_dev, cap);
     const int64_t base = (int64_t)blockIdx.x * kRhTile;
     uint64_t raw[kRsItems];
 #pragma unroll
     for (int r = 0; r < kRsItems; ++r) {
-        const int64_t i = base + r * kRhThreads + t;
+        const int64_t i = base + wave * (kRsItems * 64) + r * 64 + lane;
         raw[r] = i < count ? w.ka[i] : 0ull;
     }
-    // thread t: bucket t's first position for this block
-    const uint32_t size = w.mhist[t];
-    uint32_t pre = 0;
+    __shared__ uint16_t wcnt[NWV][kMsFine];  // per-wave running counts, then the waves' offsets in the block's share
+    __shared__ uint32_t fbase[kMsFine];      // each fine bin's first position, then the block's in it
+    __shared__ uint32_t sbs[kMsMaxBuckets + 1], sbf[kMsMaxBuckets + 1];
+    __shared__ int lds[NWV + 1];
+    __shared__ uint32_t s_nb;
+    // thread t: fine bins [t * BPT, (t + 1) * BPT) and their first positions
+    uint32_t h[BPT];
     {
-        const uint4* col = (const uint4*)(w.tcnt + (size_t)t * kMsMaxBlocks);
-        const uint32_t nb = blockIdx.x;
-        for (uint32_t c0 = 0; c0 * 4 < nb; c0 += kChunk) {
-            uint4 v[kChunk];
+        const uint4* src = (const uint4*)(w.fhist + t * BPT);
 #pragma unroll
-            for (int c = 0; c < kChunk; ++c) v[c] = (4 * (c0 + c) < nb) ? col[c0 + c] : make_uint4(0u, 0u, 0u, 0u);
-#pragma unroll
-            for (int c = 0; c < kChunk; ++c) {
-                const uint32_t q = 4 * (c0 + c);
-                pre += (q < nb ? v[c].x : 0u) + (q + 1 < nb ? v[c].y : 0u) + (q + 2 < nb ? v[c].z : 0u) +
-                       (q + 3 < nb ? v[c].w : 0u);
-            }
+        for (int q = 0; q < BPT / 4; ++q) {
+            const uint4 v = src[q];
+            h[4 * q] = v.x;
+            h[4 * q + 1] = v.y;
+            h[4 * q + 2] = v.z;
+            h[4 * q + 3] = v.w;
         }
     }
-    __shared__ int lds[NWV + 1];
-    __shared__ uint32_t dbase[kRsBins];
-    __shared__ uint16_t cnt[kRsItems][NWV][kRsBins];
-    for (int e = t; e < kRsItems * NWV * kRsBins; e += kRhThreads) (&cnt[0][0][0])[e] = 0;
-    int all;
-    const uint32_t bb = (uint32_t)block_exclusive_scan((int)size, lds, &all);  // syncs: cnt is clear after it
+    const uint32_t hprev = t > 0 ? w.fhist[t * BPT - 1] : 0u;
+    uint32_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < BPT; ++j) sum += h[j];
+    int total_i;
+    uint32_t e[BPT];
+    e[0] = (uint32_t)block_exclusive_scan((int)sum, lds, &total_i);
+#pragma unroll
+    for (int j = 1; j < BPT; ++j) e[j] = e[j - 1] + h[j - 1];
+    const uint32_t total = (uint32_t)total_i;
+    // bucket table: bucket b starts at the first fine bin whose bucket is b
+    // (buckets left empty by a jump start where the next one does)
+    {
+        int64_t bp = -1;
+        if (t > 0) bp = ms_bucket_of(g, (uint32_t)(t * BPT - 1), e[0] - hprev, total);
+#pragma unroll
+        for (int j = 0; j < BPT; ++j) {
+            const uint32_t f = (uint32_t)(t * BPT + j);
+            const uint32_t b = ms_bucket_of(g, f, e[j], total);
+            for (int64_t q = bp + 1; q <= (int64_t)b; ++q) {
+                sbs[q] = e[j];
+                sbf[q] = f;
+            }
+            bp = b;
+        }
+        if (t == kRhThreads - 1) {
+            sbs[bp + 1] = total;
+            sbf[bp + 1] = kMsFine;
+            s_nb = (uint32_t)(bp + 1);
+        }
+    }
+    __syncthreads();
+    const uint32_t nb = s_nb;
+    bool over = false;
+    for (uint32_t q = t; q < nb; q += kRhThreads) over |= sbs[q + 1] - sbs[q] > (uint32_t)kMsCap;
+    if (__syncthreads_or(over)) return;
     if (blockIdx.x == 0) {
-        ms_bases(w)[t] = bb;
-        if (t == 0) w.st->msd = 1u;
+        for (uint32_t q = t; q <= nb; q += kRhThreads) {
+            ms_starts(w)[q] = sbs[q];
+            ms_firsts(w)[q] = sbf[q];
+        }
+        if (t == 0) {
+            *ms_count(w) = nb;
+            w.st->msd = 1u;
+        }
     }
     if (base >= count) return;
-    dbase[t] = bb + pre;
-    const uint32_t sh = ms_shift(st);
-    const uint64_t lowmask = (1ull << sh) - 1;
+    {
+        uint4* z = (uint4*)&wcnt[0][0];
+        for (int q = t; q < (int)(sizeof(wcnt) / 16); q += kRhThreads) z[q] = make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int j = 0; j < BPT; ++j) fbase[t * BPT + j] = e[j];
+    __syncthreads();
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    uint64_t ck[kRsItems];
-    uint32_t dg[kRsItems], rank[kRsItems];
+    uint32_t ck[kRsItems], fb[kRsItems], rk[kRsItems];
 #pragma unroll
     for (int r = 0; r < kRsItems; ++r) {
-        const bool valid = base + r * kRhThreads + t < count;
-        ck[r] = valid ? rs_compact(raw[r], st) : 0ull;
-        dg[r] = (uint32_t)(ck[r] >> sh);
-        const uint64_t peers = rs_peers(dg[r], valid);
-        rank[r] = (uint32_t)__popcll(peers & lt);
-        if (valid && rank[r] == 0) cnt[r][wave][dg[r]] = (uint16_t)__popcll(peers);
+        const bool valid = base + wave * (kRsItems * 64) + r * 64 + lane < count;
+        ck[r] = valid ? (uint32_t)rs_compact(raw[r], st) : 0u;
+        fb[r] = ck[r] >> g.shF;
+        const uint64_t peers = rs_peers<kMsFineBits>(fb[r], valid);
+        const uint32_t lr = (uint32_t)__popcll(peers & lt);
+        const uint32_t prev = wcnt[wave][fb[r]];
+        rk[r] = prev + lr;
+        if (valid && lr == 0) wcnt[wave][fb[r]] = (uint16_t)(prev + __popcll(peers));
     }
     __syncthreads();
-    {
-        // bucket t: offsets over (round, wave) in index order
+    // claim the block's share of each fine bin it holds: thread t takes bins
+    // t, t + 256, ... (a block's keys fill few, nearby bins: spread over the
+    // threads, their atomics go out together instead of one after another)
+    uint32_t claim[BPT];
+#pragma unroll
+    for (int j = 0; j < BPT; ++j) {
+        const int f = t + kRhThreads * j;
+        uint32_t tot = 0;
+#pragma unroll
+        for (int q = 0; q < NWV; ++q) tot += wcnt[q][f];
+        claim[j] = tot ? atomicAdd(&w.fcur[f], tot) : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < BPT; ++j) {
+        const int f = t + kRhThreads * j;
         uint32_t run = 0;
 #pragma unroll
-        for (int r = 0; r < kRsItems; ++r)
-#pragma unroll
-            for (int q = 0; q < NWV; ++q) {
-                const uint32_t c = cnt[r][q][t];
-                cnt[r][q][t] = (uint16_t)run;
-                run += c;
-            }
+        for (int q = 0; q < NWV; ++q) {
+            const uint32_t c = wcnt[q][f];
+            wcnt[q][f] = (uint16_t)run;
+            run += c;
+        }
+        if (run) fbase[f] += claim[j];
     }
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < kRsItems; ++r) {
-        const int64_t i = base + r * kRhThreads + t;
+        const int64_t i = base + wave * (kRsItems * 64) + r * 64 + lane;
         if (i < count) {
-            const uint32_t pos = dbase[dg[r]] + cnt[r][wave][dg[r]] + rank[r];
-            w.kb[pos] = ((uint64_t)(uint32_t)i << 32) | (ck[r] & lowmask);
+            const uint32_t pos = fbase[fb[r]] + wcnt[wave][fb[r]] + rk[r];
+            w.kb[pos] = ((uint64_t)(uint32_t)i << 32) | ck[r];
         }
     }
 }
 
-// One workgroup per bucket: its items (in kb, stable) sorted by the bits below
-// the bucket's, 8 at a time, in LDS.  Wave q holds the items
-// [q * R * 64, (q + 1) * R * 64) of the current order, R = ceil(size / 1024)
+// One workgroup per bucket: its items (in kb, grouped by fine bin, each
+// block's share of a bin in index order) sorted by the key bits below the
+// bucket's first fine bin and then by the item's block, 8 bits at a time, in
+// LDS -- which leaves equal keys in index order.  Wave q holds the items
+// [q * R * 64, (q + 1) * R * 64) of the current order, R = ceil(size / 512)
 // rounds of 64; an item's new place is the count of items of smaller digit
 // plus those of its digit in the waves before plus the wave's running count of
 // that digit (in LDS, read by every lane and advanced by the digit's first
@@ -360,14 +450,21 @@ __global__ __launch_bounds__(kRhThreads) void k_ms_scatter(RadixWs w, const int6
 // positions.
 __global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w) {
     constexpr int NWV = kMsThreads / 64;
-    static_assert(kRsBins * 4 == kMsThreads, "thread t scans digit t / 4 over waves 4 (t % 4) ..");
+    static_assert(kRsBins * 2 == kMsThreads, "thread t scans digit t / 2 over waves 4 (t % 2) ..");
+    static_assert(kMsMaxBlocks <= 256 && kRhTile == 1024, "an item's block is its index >> 10, 8 bits");
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const SortStats st = *w.st;
+    if (!st.msd) return;
     const uint32_t b = blockIdx.x;
-    const uint32_t size = w.mhist[b];
-    const uint32_t base = ms_bases(w)[b];
-    if (!st.msd || size == 0) return;
-    const uint32_t sh = ms_shift(st);
+    if (b >= *ms_count(w)) return;
+    const uint32_t start = ms_starts(w)[b];
+    const uint32_t size = ms_starts(w)[b + 1] - start;
+    if (size == 0) return;
+    const MsGeom g = ms_geom(st);
+    const uint32_t f0 = ms_firsts(w)[b];
+    const uint32_t kbase = f0 << g.shF;  // the bucket's smallest possible key
+    const uint32_t span = (ms_firsts(w)[b + 1] - f0) << g.shF;  // at most 2^24
+    const int bits = (span > 1 ? 32 - __clz(span - 1) : 0) + 8;  // key below kbase, then the block
     const uint32_t R = (size + kMsThreads - 1) / kMsThreads;
     // this wave's rounds that hold items (rounds past the bucket are skipped)
     const uint32_t first = wave * R * 64;
@@ -376,20 +473,20 @@ __global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w) {
 #pragma unroll
     for (int r = 0; r < kMsRounds; ++r) {
         const uint32_t e = (wave * R + r) * 64 + lane;
-        const uint64_t x = ((uint32_t)r < R && e < size) ? w.kb[base + e] : 0ull;
-        key[r] = (uint32_t)x;
+        const uint64_t x = ((uint32_t)r < R && e < size) ? w.kb[start + e] : 0ull;
         val[r] = (uint32_t)(x >> 32);
+        key[r] = (((uint32_t)x - kbase) << 8) | (val[r] >> 10);
     }
     __shared__ uint64_t buf[kMsCap];
     __shared__ uint32_t wc[NWV][kRsBins];
     __shared__ int lds[NWV + 1];
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    const int passes = (int)((sh + kRsBits - 1) / kRsBits);
+    const int passes = (bits + kRsBits - 1) / kRsBits;
     for (int p = 0; p < passes; ++p) {
         // the wave's counts start at zero (the last pass's readers have passed
         // the barrier after the scatter)
         for (int e = lane; e < kRsBins; e += 64) wc[wave][e] = 0u;
-        const int nb = (int)sh - kRsBits * p < kRsBits ? (int)sh - kRsBits * p : kRsBits;  // bits of this digit
+        const int nb = bits - kRsBits * p < kRsBits ? bits - kRsBits * p : kRsBits;  // bits of this digit
 #pragma unroll
         for (int r = 0; r < kMsRounds; ++r) {
             if ((uint32_t)r >= Rw) continue;
@@ -407,7 +504,7 @@ __global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w) {
         __syncthreads();
         {
             // offsets in (digit, wave) order
-            const int d = t >> 2, q0 = (t & 3) * 4;
+            const int d = t >> 1, q0 = (t & 1) * 4;
             uint32_t c[4], sum = 0;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -450,8 +547,8 @@ __global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w) {
         if ((uint32_t)r >= Rw) continue;
         const uint32_t e = (wave * R + r) * 64 + lane;
         if (e < size) {
-            w.ka[base + e] = ((uint64_t)b << sh) | key[r];
-            w.va[base + e] = val[r];
+            w.ka[start + e] = (uint64_t)(kbase + (key[r] >> 8));
+            w.va[start + e] = val[r];
         }
     }
 }
@@ -686,7 +783,7 @@ void launch_radix_sort(hipStream_t s, const RadixWs& w, Header* h, const int64_t
         // launch (one workgroup per tile, all resident for the grid barrier)
         k_rs_hist<<<nh, kRhThreads, 0, s>>>(w, count_dev, cap, nrec, (int64_t)nt, 1);
         k_ms_scatter<<<nh, kRhThreads, 0, s>>>(w, count_dev, cap);
-        k_ms_bucket<<<kRsBins, kMsThreads, 0, s>>>(w);
+        k_ms_bucket<<<kMsMaxBuckets, kMsThreads, 0, s>>>(w);
         k_rs_tail<<<nt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, 0, (int64_t)nt);
         return;
     }

@@ -134,8 +134,9 @@ struct RadixWs {
     uint32_t* zero;     // the region the producer zeroes (radix_zero_words):
     uint32_t* ghist;    //   [kRsPasses][kRsBins] digit counts over all keys
     uint32_t* ctr;      //   [64] tile counters (0 .. kRsPasses-1 the passes, 8.. for the consumers)
-    uint32_t* mhist;    //   [kRsBins] bucket sizes (the top digit) of the bucket sort
-    uint32_t* tcnt;     // [histogram blocks][kRsBins] per-block bucket counts of the bucket sort
+    uint32_t* fhist;    //   [4096] the bucket sort's item counts per fine bin (top 12 key bits)
+    uint32_t* fcur;     //   [4096] ... and the items of each fine bin claimed so far
+    uint32_t* sb;       // the bucket sort's bucket table: starts, first fine bins, count
     uint64_t* status;   // [kRsPasses][ntiles][kRsBins] look-back words, then [ntiles] for a consumer's scan:
                         // the histogram kernel clears pass 0's and the consumer's, pass p clears pass p+1's
 };
