@@ -292,6 +292,15 @@ def configs_mode(args):
             out = torch.empty((m, C), dtype=torch.bfloat16, device=dev)
             ms = timed(lambda: spv.spv_sparse_conv(wsm, x, km.off, km.pairs, W, m, out=out))
             report("conv k3 32->32", ms, 2 * C * m * 2 + 8 * P + 27 * C * C * 2, 2.0 * C * C * P, voxels=m, pairs=P)
+            # the neighbour-table route: the map as a [m][27] table, and the conv on it
+            # with weights packed once (no per-call plan)
+            nbr = torch.empty((m, 27), dtype=torch.int32, device=dev)
+            ms = timed(lambda: spv.spv_kernel_map_nbr(wsm, coords, out=nbr))
+            report("kernel_map_nbr k3 s1", ms, 16 * m + 12 * table_slots(m) + 108 * m, voxels=m, pairs=P)
+            Wp = spv.spv_pack_weights(W)
+            ms = timed(lambda: spv.spv_sparse_conv_nbr_packed(wsm, x, nbr, Wp, C, m, out=out))
+            report("conv k3 32->32 on the neighbour table", ms, 2 * C * m * 2 + 108 * m + 27 * C * C * 2,
+                   2.0 * C * C * P, voxels=m, pairs=P)
         else:
             km = spv.spv_kernel_map(wsm, coords, K=2, stride=2)
             mc = int(km.m_out_dev.item())

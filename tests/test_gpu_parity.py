@@ -261,18 +261,20 @@ def test_voxelize_wide_keys_many_tiles(spv):
 
 def _bucket_case(case):
     """Points on a 1 m grid (v = 1): x spans 0..4095 voxels, y 0..63, z 0..31, so
-    the compacted key has 12 + 6 + 5 bits and its top 8 bits (the sort's bucket)
-    are x // 16."""
+    the compacted key has 12 + 6 + 5 bits and its top 12 bits (the sort's fine
+    bin) are x.  The buckets group consecutive fine bins by count, so fine bin 0
+    with k points is a bucket of its own (the next bin's running count already
+    maps past bucket 0) of exactly k items."""
     rng = np.random.default_rng(6161)
-    if case == "narrow":  # 6 significant bits: the buckets alone order the keys
+    if case == "narrow":  # 6 significant bits: every key its own fine bin
         vox = rng.integers(0, 3, size=(9000, 3))
     elif case == "most_blocks":  # 256 histogram blocks of 1024 keys exactly
         vox = np.stack([rng.integers(0, 4096, 262_144), rng.integers(0, 64, 262_144),
                         rng.integers(0, 32, 262_144)], 1)
-    else:  # bucket 0 holds 16384 items (the bucket sort's capacity) or one more
-        k = 16_384 if case == "cap" else 16_385
-        a = np.stack([rng.integers(0, 16, k), rng.integers(0, 64, k), rng.integers(0, 32, k)], 1)
-        b = np.stack([rng.integers(16, 4096, 30_000), rng.integers(0, 64, 30_000), rng.integers(0, 32, 30_000)], 1)
+    else:  # one bucket of 8192 items (the bucket sort's capacity) or one more
+        k = 8_192 if case == "cap" else 8_193
+        a = np.stack([np.zeros(k, np.int64), rng.integers(0, 64, k), rng.integers(0, 32, k)], 1)
+        b = np.stack([rng.integers(1, 4096, 30_000), rng.integers(0, 64, 30_000), rng.integers(0, 32, 30_000)], 1)
         a[0] = (0, 0, 0)
         b[0] = (4095, 63, 31)
         vox = np.concatenate([b[: 20_000], a, b[20_000:]])
@@ -281,9 +283,9 @@ def _bucket_case(case):
 
 @pytest.mark.parametrize("case", ["narrow", "cap", "over", "most_blocks"])
 def test_voxelize_bucket_sort_bounds(spv, case):
-    """The sort's bucket path at its limits: keys the buckets alone order, a bucket
-    at the in-LDS capacity, one item over it (the passes run instead), and the
-    most histogram blocks the bucket path takes."""
+    """The sort's bucket path at its limits: keys of 6 bits, a bucket at the
+    in-LDS capacity, one item over it (the passes run instead), and the most
+    histogram blocks the bucket path takes."""
     xyz = _bucket_case(case)
     feat = synth.normal((len(xyz), 8), 6162, dtype="bf16")
     c, vf, cnt, p2v, _ = run_voxelize(spv, xyz, 1.0, feat, "bf16")
