@@ -224,8 +224,9 @@ __device__ inline uint32_t ms_bucket_of(const MsGeom& g, uint32_t f, uint32_t ex
 // its time goes into waiting for loads), up to kRhMaxBlocks that stride over
 // the rest.  Block b also clears the look-back words of pass 0 and of the
 // consumer's scan of pass tiles b, b + grid, ...
-// With `msd` (one block per kRhTile keys) each block also adds its fine-bin
-// counts to fhist.
+// With `msd` (one block per kRhTile keys) each block adds its fine-bin counts
+// to fhist instead of the digit counts (the bucket sort's fallback counts
+// those itself).
 __global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t* count_dev, int64_t cap,
                                                          uint32_t nrec, int64_t ntiles, int msd) {
     static_assert(kRsBins == kRhThreads, "thread t clears digit t's look-back word");
@@ -266,17 +267,21 @@ __global__ __launch_bounds__(kRhThreads) void k_rs_hist(RadixWs w, const int64_t
             const int64_t i = b0 + r * kRhThreads + threadIdx.x;
             if (i < count) {
                 const uint64_t ck = rs_compact(raw[r], st);
-                for (int p = 0; p < passes; ++p)
-                    atomicAdd(&hist[p][(uint32_t)(ck >> (kRsBits * p)) & (kRsBins - 1)], 1u);  // LDS
-                if (msd && st.sort_bits <= 32) atomicAdd(&fh[(uint32_t)(ck >> shF)], 1u);  // LDS
+                if (msd) {
+                    if (st.sort_bits <= 32) atomicAdd(&fh[(uint32_t)(ck >> shF)], 1u);  // LDS
+                } else {
+                    for (int p = 0; p < passes; ++p)
+                        atomicAdd(&hist[p][(uint32_t)(ck >> (kRsBits * p)) & (kRsBins - 1)], 1u);  // LDS
+                }
             }
         }
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < passes * kRsBins; e += kRhThreads) {
-        const uint32_t c = (&hist[0][0])[e];
-        if (c) atomicAdd(&w.ghist[e], c);
-    }
+    if (!msd)
+        for (int e = threadIdx.x; e < passes * kRsBins; e += kRhThreads) {
+            const uint32_t c = (&hist[0][0])[e];
+            if (c) atomicAdd(&w.ghist[e], c);
+        }
     if (msd)
         for (int e = threadIdx.x; e < kMsFine; e += kRhThreads) {
             const uint32_t c = fh[e];
@@ -726,7 +731,8 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_pass(RadixWs w, Header* h, co
 // it; a wait past kRsSpinLimit polls records an error and goes on, so every
 // workgroup ends.
 // With first = 0 it is the bucket sort's fallback: it exits at once when the
-// bucket sort has ordered the keys.
+// bucket sort has ordered the keys, and otherwise first counts the digits of
+// every pass (the histogram kernel counted only the fine bins).
 __global__ __launch_bounds__(kRsThreads) void k_rs_tail(RadixWs w, Header* h, const int64_t* count_dev, int64_t cap,
                                                         int first, int64_t ntiles) {
     const uint32_t bits = w.st->sort_bits;
@@ -734,6 +740,42 @@ __global__ __launch_bounds__(kRsThreads) void k_rs_tail(RadixWs w, Header* h, co
     if (first == 0 && w.st->msd) return;
     extern __shared__ __align__(16) unsigned char rs_smem[];
     const int64_t count = rs_count(count_dev, cap);
+    if (first == 0) {
+        const SortStats st = *w.st;
+        const int passes = rs_passes(st);
+        uint32_t* hist = (uint32_t*)rs_smem;  // [kRsPasses][kRsBins], 8 KB of the pass's LDS
+        for (int e = threadIdx.x; e < kRsPasses * kRsBins; e += kRsThreads) hist[e] = 0u;
+        __syncthreads();
+        for (int64_t i = blockIdx.x * (int64_t)kRsThreads + threadIdx.x; i < count;
+             i += (int64_t)gridDim.x * kRsThreads) {
+            const uint64_t ck = rs_compact(w.ka[i], st);
+            for (int p = 0; p < passes; ++p)
+                atomicAdd(&hist[p * kRsBins + ((uint32_t)(ck >> (kRsBits * p)) & (kRsBins - 1))], 1u);  // LDS
+        }
+        __syncthreads();
+        for (int e = threadIdx.x; e < passes * kRsBins; e += kRsThreads) {
+            const uint32_t c = hist[e];
+            if (c) atomicAdd(&w.ghist[e], c);
+        }
+        // every workgroup's counts are in before pass 0 reads them (the
+        // barrier slot before pass 0 is otherwise unused)
+        __threadfence();
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint32_t* bar = &w.ctr[kRsBarrierCtr];
+            atomicAdd(bar, 1u);
+            uint32_t spins = 0;
+            while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < gridDim.x) {
+                if (++spins > kRsSpinLimit) {
+                    raise_flag(h, kFlagInternal);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+        }
+        __syncthreads();
+        __threadfence();
+    }
     // pass 0 always runs: it writes the compacted keys and the payload
     for (int pass = first; pass < kRsPasses && (pass == 0 || (uint32_t)(kRsBits * pass) < bits); ++pass) {
         if (pass > first) {
