@@ -36,7 +36,8 @@
 //                (an LSD sort of 8-bit digits whose passes never leave the
 //                workgroup), which restores index order between blocks, and
 //                writes the result in place of the keys.
-// Otherwise both exit at once and k_rs_tail runs every pass in one launch.
+// Otherwise the scatter does nothing and the bucket kernel's first workgroups
+// run every pass instead (one per tile, grid barriers between the passes).
 // Either way the order is the same stable ascending order.
 #include "spv_internal.hpp"
 
@@ -443,6 +444,245 @@ __global__ __launch_bounds__(kRhThreads) void k_ms_scatter(RadixWs w, const int6
     }
 }
 
+
+__device__ inline uint64_t rs_load_status(const uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void rs_store_status(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Exclusive prefix of this tile's count for one digit: the counts of the tiles
+// before it, read WINDOW at a time from the nearest down, until a tile that
+// holds its inclusive prefix.  A status word not yet written is polled again
+// (the tile that writes it is running); after kRsSpinLimit polls the sort
+// records an error and goes on without it, so the kernel always ends.
+constexpr int kRsWindow = 32;
+template <int WINDOW = kRsWindow>
+__device__ inline uint32_t rs_lookback(const uint64_t* col, int64_t stride, int64_t tile, bool& stalled) {
+    uint32_t excl = 0;
+    int64_t j = tile - 1;
+    uint32_t spins = 0;
+    while (j >= 0) {
+        uint64_t s[WINDOW];
+#pragma unroll
+        for (int q = 0; q < WINDOW; ++q) s[q] = (j - q >= 0) ? rs_load_status(col + (j - q) * stride) : kRsFlagInc;
+        int q = 0;
+        bool done = false;
+        for (; q < WINDOW; ++q) {
+            const uint64_t f = s[q] & (3ull << 62);
+            if (f == 0) break;  // not written yet: read it again
+            excl += (uint32_t)s[q];
+            if (f == kRsFlagInc) {
+                done = true;
+                break;
+            }
+        }
+        if (done) break;
+        j -= q;
+        if (q == 0) {
+            if (++spins > kRsSpinLimit) {
+                stalled = true;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+    }
+    return excl;
+}
+
+// dynamic LDS of a pass: per (round, wave, digit) counts, then offsets relative
+// to the tile's first item of that digit (both at most kRsTile: 16 bits)
+constexpr size_t kRsPassLds = (size_t)kRsItems * (kRsThreads / 64) * kRsBins * sizeof(uint16_t);
+
+// One tile of one pass: the tile is taken from the pass's counter (tiles get
+// their place in the order they start, so every tile a reader waits for is
+// already running).  Returns false, with no work done, once the pass's tiles
+// are all taken.
+template <bool FIRST, int WINDOW = kRsWindow>
+__device__ inline bool rs_pass_tile(const RadixWs& w, Header* h, int64_t count, int64_t ntiles, int pass,
+                                    unsigned char* rs_smem) {
+    static_assert(kRsBins <= kRsThreads, "threads t < kRsBins own digit t");
+    constexpr int NWV = kRsThreads / 64;
+    uint16_t (*cnt)[NWV][kRsBins] = (uint16_t (*)[NWV][kRsBins])rs_smem;
+    __shared__ uint32_t dbase[kRsBins];  // the digit's first output position for this tile
+    __shared__ int lds[NWV + 1];
+    __shared__ uint32_t s_tile;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    if (t == 0) s_tile = atomicAdd(&w.ctr[pass], 1u);
+    const bool owner = t < kRsBins;
+    const uint32_t gcount = owner ? w.ghist[pass * kRsBins + t] : 0u;
+    {
+        uint4* z = (uint4*)rs_smem;
+        for (size_t e = t; e < kRsPassLds / 16; e += kRsThreads) z[e] = make_uint4(0u, 0u, 0u, 0u);
+    }
+    __syncthreads();
+    const int64_t tile = s_tile;
+    if (tile >= ntiles) return false;
+    const int64_t base = tile * kRsTile;
+    const uint64_t* ksrc = (pass & 1) ? w.kb : w.ka;
+    uint64_t* kdst = (pass & 1) ? w.ka : w.kb;
+    const uint32_t* vsrc = (pass & 1) ? w.vb : w.va;
+    uint32_t* vdst = (pass & 1) ? w.va : w.vb;
+    uint64_t keys[kRsItems];
+    uint32_t vals[kRsItems];
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r) {
+        const int64_t i = base + r * kRsThreads + t;
+        keys[r] = i < count ? ksrc[i] : 0ull;
+        if constexpr (FIRST) vals[r] = (uint32_t)i;  // the first pass sorts the item indices
+        else vals[r] = i < count ? vsrc[i] : 0u;
+    }
+    // the next pass's look-back words of this tile start empty (that pass starts after this one ends)
+    if (owner && pass + 1 < kRsPasses) w.status[((size_t)(pass + 1) * w.ntiles + tile) * kRsBins + t] = 0ull;
+    // bucket base of digit t: all keys of smaller digits
+    int all;
+    const uint32_t gbase = (uint32_t)block_exclusive_scan((int)gcount, lds, &all);
+    if constexpr (FIRST) {
+        const SortStats st = *w.st;
+#pragma unroll
+        for (int r = 0; r < kRsItems; ++r)
+            if (base + r * kRsThreads + t < count) keys[r] = rs_compact(keys[r], st);
+    }
+    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    uint32_t rank[kRsItems];
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r) {
+        const int64_t i = base + r * kRsThreads + t;
+        const bool valid = i < count;
+        const uint32_t d = (uint32_t)(keys[r] >> (kRsBits * pass)) & (kRsBins - 1);
+        const uint64_t peers = rs_peers(d, valid);
+        rank[r] = (uint32_t)__popcll(peers & lt);
+        if (valid && rank[r] == 0) cnt[r][wave][d] = (uint16_t)__popcll(peers);
+    }
+    __syncthreads();
+    if (owner) {
+        // thread t: the tile's count of digit t, published before the look-back
+        uint32_t tot = 0;
+#pragma unroll
+        for (int r = 0; r < kRsItems; ++r)
+#pragma unroll
+            for (int q = 0; q < NWV; ++q) tot += (uint32_t)cnt[r][q][t];
+        uint64_t* col = w.status + (size_t)pass * kRsBins * w.ntiles + t;  // status[pass][tile][digit]
+        bool stalled = false;
+        uint32_t excl = 0;
+        if (tile == 0) {
+            rs_store_status(col, kRsFlagInc | tot);
+        } else {
+            rs_store_status(col + tile * kRsBins, kRsFlagAgg | tot);
+            excl = rs_lookback<WINDOW>(col, kRsBins, tile, stalled);
+            rs_store_status(col + tile * kRsBins, kRsFlagInc | (uint64_t)(excl + tot));
+        }
+        if (stalled) raise_flag(h, kFlagInternal);
+        // offsets over (round, wave) in index order, relative to the digit's base
+        dbase[t] = gbase + excl;
+        uint32_t run = 0;
+#pragma unroll
+        for (int r = 0; r < kRsItems; ++r)
+#pragma unroll
+            for (int q = 0; q < NWV; ++q) {
+                const uint32_t c = cnt[r][q][t];
+                cnt[r][q][t] = (uint16_t)run;
+                run += c;
+            }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kRsItems; ++r) {
+        const int64_t i = base + r * kRsThreads + t;
+        if (i < count) {
+            const uint32_t d = (uint32_t)(keys[r] >> (kRsBits * pass)) & (kRsBins - 1);
+            const uint32_t pos = dbase[d] + cnt[r][wave][d] + rank[r];
+            kdst[pos] = keys[r];
+            vdst[pos] = vals[r];
+        }
+    }
+    return true;
+}
+
+// dynamic LDS of a pass is declared by the kernels: per (round, wave, digit)
+// counts, then offsets relative to the tile's first item of that digit
+template <bool FIRST>
+__global__ __launch_bounds__(kRsThreads) void k_rs_pass(RadixWs w, Header* h, const int64_t* count_dev, int64_t cap,
+                                                        int pass) {
+    // the first pass always runs: it writes the compacted keys and the payload
+    if (pass > 0 && (uint32_t)(kRsBits * pass) >= w.st->sort_bits) return;
+    extern __shared__ __align__(16) unsigned char rs_smem[];
+    rs_pass_tile<FIRST>(w, h, rs_count(count_dev, cap), (int64_t)gridDim.x, pass, rs_smem);
+}
+
+// Grid barrier (slot `slot` of the counters) of the first `parts` workgroups:
+// each wave releases its writes before the arrival and acquires after it.  A
+// wait past kRsSpinLimit polls records an error and goes on, so every
+// workgroup ends.
+__device__ inline void rs_grid_barrier(const RadixWs& w, Header* h, int slot, uint32_t parts) {
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t* bar = &w.ctr[kRsBarrierCtr + slot];
+        atomicAdd(bar, 1u);
+        uint32_t spins = 0;
+        while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < parts) {
+            if (++spins > kRsSpinLimit) {
+                raise_flag(h, kFlagInternal);
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+    }
+    __syncthreads();
+    __threadfence();
+}
+
+// The passes from `first` on by `parts` co-resident workgroups that loop over
+// the tiles, a grid barrier between two passes (pass 0 always runs: it writes
+// the compacted keys and the payload).  With first = 0 the workgroups first
+// count the digits of every pass (the histogram kernel of the bucket sort
+// counted only its fine bins).  smem: kRsPassLds bytes.  WINDOW: status words
+// a look-back reads at a time (fewer where registers are scarcer).
+template <int WINDOW = kRsWindow>
+__device__ inline void rs_tail_run(const RadixWs& w, Header* h, int64_t count, int64_t ntiles, int first,
+                                   uint32_t parts, unsigned char* smem) {
+    const uint32_t bits = w.st->sort_bits;
+    if (first == 0) {
+        const SortStats st = *w.st;
+        const int passes = rs_passes(st);
+        uint32_t* hist = (uint32_t*)smem;  // [kRsPasses][kRsBins], 8 KB of the pass's LDS
+        for (int e = threadIdx.x; e < kRsPasses * kRsBins; e += kRsThreads) hist[e] = 0u;
+        __syncthreads();
+        for (int64_t i = blockIdx.x * (int64_t)kRsThreads + threadIdx.x; i < count; i += (int64_t)parts * kRsThreads) {
+            const uint64_t ck = rs_compact(w.ka[i], st);
+            for (int p = 0; p < passes; ++p)
+                atomicAdd(&hist[p * kRsBins + ((uint32_t)(ck >> (kRsBits * p)) & (kRsBins - 1))], 1u);  // LDS
+        }
+        __syncthreads();
+        for (int e = threadIdx.x; e < passes * kRsBins; e += kRsThreads) {
+            const uint32_t c = hist[e];
+            if (c) atomicAdd(&w.ghist[e], c);
+        }
+        rs_grid_barrier(w, h, 0, parts);  // every count is in before pass 0 reads them
+    }
+    for (int pass = first; pass < kRsPasses && (pass == 0 || (uint32_t)(kRsBits * pass) < bits); ++pass) {
+        if (pass > first) rs_grid_barrier(w, h, pass, parts);
+        if (pass == 0) {
+            while (rs_pass_tile<true, WINDOW>(w, h, count, ntiles, pass, smem)) __syncthreads();
+        } else {
+            while (rs_pass_tile<false, WINDOW>(w, h, count, ntiles, pass, smem)) __syncthreads();
+        }
+    }
+}
+
+// The passes from `first` on in one launch, one workgroup per tile, all
+// resident.  A key of at most 8 * first significant bits (the usual case)
+// makes it exit at once, so the passes that are not needed cost one launch,
+// not one each.
+__global__ __launch_bounds__(kRsThreads) void k_rs_tail(RadixWs w, Header* h, const int64_t* count_dev, int64_t cap,
+                                                        int first, int64_t ntiles) {
+    if ((uint32_t)(kRsBits * first) >= w.st->sort_bits) return;
+    extern __shared__ __align__(16) unsigned char rs_smem[];
+    rs_tail_run(w, h, rs_count(count_dev, cap), ntiles, first, gridDim.x, rs_smem);
+}
+
 // One workgroup per bucket: its items (in kb, grouped by fine bin, each
 // block's share of a bin in index order) sorted by the key bits below the
 // bucket's first fine bin and then by the item's block, 8 bits at a time, in
@@ -452,14 +692,23 @@ __global__ __launch_bounds__(kRhThreads) void k_ms_scatter(RadixWs w, const int6
 // plus those of its digit in the waves before plus the wave's running count of
 // that digit (in LDS, read by every lane and advanced by the digit's first
 // lane, round by round).  The sorted bucket goes to ka / va at the same
-// positions.
-__global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w) {
+// positions.  When the bucket sort cannot order the keys, the first ntiles
+// workgroups run every pass instead (one tile each, all resident: two of these
+// workgroups fit a CU) and the others exit.
+__global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w, Header* h, const int64_t* count_dev, int64_t cap,
+                                                          int64_t ntiles) {
+    static_assert(kMsThreads == kRsThreads, "the fallback's pass tiles take the same workgroup");
     constexpr int NWV = kMsThreads / 64;
     static_assert(kRsBins * 2 == kMsThreads, "thread t scans digit t / 2 over waves 4 (t % 2) ..");
     static_assert(kMsMaxBlocks <= 256 && kRhTile == 1024, "an item's block is its index >> 10, 8 bits");
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    __shared__ uint64_t buf[kMsCap];
     const SortStats st = *w.st;
-    if (!st.msd) return;
+    if (!st.msd) {
+        if (blockIdx.x < ntiles)
+            rs_tail_run<8>(w, h, rs_count(count_dev, cap), ntiles, 0, (uint32_t)ntiles, (unsigned char*)buf);
+        return;
+    }
     const uint32_t b = blockIdx.x;
     if (b >= *ms_count(w)) return;
     const uint32_t start = ms_starts(w)[b];
@@ -482,7 +731,6 @@ __global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w) {
         val[r] = (uint32_t)(x >> 32);
         key[r] = (((uint32_t)x - kbase) << 8) | (val[r] >> 10);
     }
-    __shared__ uint64_t buf[kMsCap];
     __shared__ uint32_t wc[NWV][kRsBins];
     __shared__ int lds[NWV + 1];
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -558,254 +806,6 @@ __global__ __launch_bounds__(kMsThreads) void k_ms_bucket(RadixWs w) {
     }
 }
 
-__device__ inline uint64_t rs_load_status(const uint64_t* p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ inline void rs_store_status(uint64_t* p, uint64_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Exclusive prefix of this tile's count for one digit: the counts of the tiles
-// before it, read kRsWindow at a time from the nearest down, until a tile that
-// holds its inclusive prefix.  A status word not yet written is polled again
-// (the tile that writes it is running); after kRsSpinLimit polls the sort
-// records an error and goes on without it, so the kernel always ends.
-constexpr int kRsWindow = 32;
-__device__ inline uint32_t rs_lookback(const uint64_t* col, int64_t stride, int64_t tile, bool& stalled) {
-    uint32_t excl = 0;
-    int64_t j = tile - 1;
-    uint32_t spins = 0;
-    while (j >= 0) {
-        uint64_t s[kRsWindow];
-#pragma unroll
-        for (int q = 0; q < kRsWindow; ++q) s[q] = (j - q >= 0) ? rs_load_status(col + (j - q) * stride) : kRsFlagInc;
-        int q = 0;
-        bool done = false;
-        for (; q < kRsWindow; ++q) {
-            const uint64_t f = s[q] & (3ull << 62);
-            if (f == 0) break;  // not written yet: read it again
-            excl += (uint32_t)s[q];
-            if (f == kRsFlagInc) {
-                done = true;
-                break;
-            }
-        }
-        if (done) break;
-        j -= q;
-        if (q == 0) {
-            if (++spins > kRsSpinLimit) {
-                stalled = true;
-                break;
-            }
-            __builtin_amdgcn_s_sleep(1);
-        }
-    }
-    return excl;
-}
-
-// dynamic LDS of a pass: per (round, wave, digit) counts, then offsets relative
-// to the tile's first item of that digit (both at most kRsTile: 16 bits)
-constexpr size_t kRsPassLds = (size_t)kRsItems * (kRsThreads / 64) * kRsBins * sizeof(uint16_t);
-
-// One tile of one pass: the tile is taken from the pass's counter (tiles get
-// their place in the order they start, so every tile a reader waits for is
-// already running).  Returns false, with no work done, once the pass's tiles
-// are all taken.
-template <bool FIRST>
-__device__ inline bool rs_pass_tile(const RadixWs& w, Header* h, int64_t count, int64_t ntiles, int pass,
-                                    unsigned char* rs_smem) {
-    static_assert(kRsBins <= kRsThreads, "threads t < kRsBins own digit t");
-    constexpr int NWV = kRsThreads / 64;
-    uint16_t (*cnt)[NWV][kRsBins] = (uint16_t (*)[NWV][kRsBins])rs_smem;
-    __shared__ uint32_t dbase[kRsBins];  // the digit's first output position for this tile
-    __shared__ int lds[NWV + 1];
-    __shared__ uint32_t s_tile;
-    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    if (t == 0) s_tile = atomicAdd(&w.ctr[pass], 1u);
-    const bool owner = t < kRsBins;
-    const uint32_t gcount = owner ? w.ghist[pass * kRsBins + t] : 0u;
-    {
-        uint4* z = (uint4*)rs_smem;
-        for (size_t e = t; e < kRsPassLds / 16; e += kRsThreads) z[e] = make_uint4(0u, 0u, 0u, 0u);
-    }
-    __syncthreads();
-    const int64_t tile = s_tile;
-    if (tile >= ntiles) return false;
-    const int64_t base = tile * kRsTile;
-    const uint64_t* ksrc = (pass & 1) ? w.kb : w.ka;
-    uint64_t* kdst = (pass & 1) ? w.ka : w.kb;
-    const uint32_t* vsrc = (pass & 1) ? w.vb : w.va;
-    uint32_t* vdst = (pass & 1) ? w.va : w.vb;
-    uint64_t keys[kRsItems];
-    uint32_t vals[kRsItems];
-#pragma unroll
-    for (int r = 0; r < kRsItems; ++r) {
-        const int64_t i = base + r * kRsThreads + t;
-        keys[r] = i < count ? ksrc[i] : 0ull;
-        if constexpr (FIRST) vals[r] = (uint32_t)i;  // the first pass sorts the item indices
-        else vals[r] = i < count ? vsrc[i] : 0u;
-    }
-    // the next pass's look-back words of this tile start empty (that pass starts after this one ends)
-    if (owner && pass + 1 < kRsPasses) w.status[((size_t)(pass + 1) * w.ntiles + tile) * kRsBins + t] = 0ull;
-    // bucket base of digit t: all keys of smaller digits
-    int all;
-    const uint32_t gbase = (uint32_t)block_exclusive_scan((int)gcount, lds, &all);
-    if constexpr (FIRST) {
-        const SortStats st = *w.st;
-#pragma unroll
-        for (int r = 0; r < kRsItems; ++r)
-            if (base + r * kRsThreads + t < count) keys[r] = rs_compact(keys[r], st);
-    }
-    const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    uint32_t rank[kRsItems];
-#pragma unroll
-    for (int r = 0; r < kRsItems; ++r) {
-        const int64_t i = base + r * kRsThreads + t;
-        const bool valid = i < count;
-        const uint32_t d = (uint32_t)(keys[r] >> (kRsBits * pass)) & (kRsBins - 1);
-        const uint64_t peers = rs_peers(d, valid);
-        rank[r] = (uint32_t)__popcll(peers & lt);
-        if (valid && rank[r] == 0) cnt[r][wave][d] = (uint16_t)__popcll(peers);
-    }
-    __syncthreads();
-    if (owner) {
-        // thread t: the tile's count of digit t, published before the look-back
-        uint32_t tot = 0;
-#pragma unroll
-        for (int r = 0; r < kRsItems; ++r)
-#pragma unroll
-            for (int q = 0; q < NWV; ++q) tot += (uint32_t)cnt[r][q][t];
-        uint64_t* col = w.status + (size_t)pass * kRsBins * w.ntiles + t;  // status[pass][tile][digit]
-        bool stalled = false;
-        uint32_t excl = 0;
-        if (tile == 0) {
-            rs_store_status(col, kRsFlagInc | tot);
-        } else {
-            rs_store_status(col + tile * kRsBins, kRsFlagAgg | tot);
-            excl = rs_lookback(col, kRsBins, tile, stalled);
-            rs_store_status(col + tile * kRsBins, kRsFlagInc | (uint64_t)(excl + tot));
-        }
-        if (stalled) raise_flag(h, kFlagInternal);
-        // offsets over (round, wave) in index order, relative to the digit's base
-        dbase[t] = gbase + excl;
-        uint32_t run = 0;
-#pragma unroll
-        for (int r = 0; r < kRsItems; ++r)
-#pragma unroll
-            for (int q = 0; q < NWV; ++q) {
-                const uint32_t c = cnt[r][q][t];
-                cnt[r][q][t] = (uint16_t)run;
-                run += c;
-            }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < kRsItems; ++r) {
-        const int64_t i = base + r * kRsThreads + t;
-        if (i < count) {
-            const uint32_t d = (uint32_t)(keys[r] >> (kRsBits * pass)) & (kRsBins - 1);
-            const uint32_t pos = dbase[d] + cnt[r][wave][d] + rank[r];
-            kdst[pos] = keys[r];
-            vdst[pos] = vals[r];
-        }
-    }
-    return true;
-}
-
-// dynamic LDS of a pass is declared by the kernels: per (round, wave, digit)
-// counts, then offsets relative to the tile's first item of that digit
-template <bool FIRST>
-__global__ __launch_bounds__(kRsThreads) void k_rs_pass(RadixWs w, Header* h, const int64_t* count_dev, int64_t cap,
-                                                        int pass) {
-    // the first pass always runs: it writes the compacted keys and the payload
-    if (pass > 0 && (uint32_t)(kRsBits * pass) >= w.st->sort_bits) return;
-    extern __shared__ __align__(16) unsigned char rs_smem[];
-    rs_pass_tile<FIRST>(w, h, rs_count(count_dev, cap), (int64_t)gridDim.x, pass, rs_smem);
-}
-
-// The passes from `first` on, in one launch of co-resident workgroups that
-// loop over the tiles; a grid barrier separates two passes.  A key of at most
-// 8 * first significant bits (the usual case) makes it exit at once, so the
-// passes that are not needed cost one launch, not one each.  The barrier
-// publishes each pass's scatter (device-scope fences) before the next reads
-// it; a wait past kRsSpinLimit polls records an error and goes on, so every
-// workgroup ends.
-// With first = 0 it is the bucket sort's fallback: it exits at once when the
-// bucket sort has ordered the keys, and otherwise first counts the digits of
-// every pass (the histogram kernel counted only the fine bins).
-__global__ __launch_bounds__(kRsThreads) void k_rs_tail(RadixWs w, Header* h, const int64_t* count_dev, int64_t cap,
-                                                        int first, int64_t ntiles) {
-    const uint32_t bits = w.st->sort_bits;
-    if (first > 0 && (uint32_t)(kRsBits * first) >= bits) return;
-    if (first == 0 && w.st->msd) return;
-    extern __shared__ __align__(16) unsigned char rs_smem[];
-    const int64_t count = rs_count(count_dev, cap);
-    if (first == 0) {
-        const SortStats st = *w.st;
-        const int passes = rs_passes(st);
-        uint32_t* hist = (uint32_t*)rs_smem;  // [kRsPasses][kRsBins], 8 KB of the pass's LDS
-        for (int e = threadIdx.x; e < kRsPasses * kRsBins; e += kRsThreads) hist[e] = 0u;
-        __syncthreads();
-        for (int64_t i = blockIdx.x * (int64_t)kRsThreads + threadIdx.x; i < count;
-             i += (int64_t)gridDim.x * kRsThreads) {
-            const uint64_t ck = rs_compact(w.ka[i], st);
-            for (int p = 0; p < passes; ++p)
-                atomicAdd(&hist[p * kRsBins + ((uint32_t)(ck >> (kRsBits * p)) & (kRsBins - 1))], 1u);  // LDS
-        }
-        __syncthreads();
-        for (int e = threadIdx.x; e < passes * kRsBins; e += kRsThreads) {
-            const uint32_t c = hist[e];
-            if (c) atomicAdd(&w.ghist[e], c);
-        }
-        // every workgroup's counts are in before pass 0 reads them (the
-        // barrier slot before pass 0 is otherwise unused)
-        __threadfence();
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            uint32_t* bar = &w.ctr[kRsBarrierCtr];
-            atomicAdd(bar, 1u);
-            uint32_t spins = 0;
-            while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < gridDim.x) {
-                if (++spins > kRsSpinLimit) {
-                    raise_flag(h, kFlagInternal);
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(1);
-            }
-        }
-        __syncthreads();
-        __threadfence();
-    }
-    // pass 0 always runs: it writes the compacted keys and the payload
-    for (int pass = first; pass < kRsPasses && (pass == 0 || (uint32_t)(kRsBits * pass) < bits); ++pass) {
-        if (pass > first) {
-            // grid barrier: every workgroup has finished pass - 1 (each wave
-            // releases its scatter before the arrival, and acquires after it)
-            __threadfence();
-            __syncthreads();
-            if (threadIdx.x == 0) {
-                uint32_t* bar = &w.ctr[kRsBarrierCtr + pass];
-                atomicAdd(bar, 1u);
-                uint32_t spins = 0;
-                while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < gridDim.x) {
-                    if (++spins > kRsSpinLimit) {
-                        raise_flag(h, kFlagInternal);
-                        break;
-                    }
-                    __builtin_amdgcn_s_sleep(1);
-                }
-            }
-            __syncthreads();
-            __threadfence();
-        }
-        if (pass == 0) {
-            while (rs_pass_tile<true>(w, h, count, ntiles, pass, rs_smem)) __syncthreads();
-        } else {
-            while (rs_pass_tile<false>(w, h, count, ntiles, pass, rs_smem)) __syncthreads();
-        }
-    }
-}
-
 void launch_radix_sort(hipStream_t s, const RadixWs& w, Header* h, const int64_t* count_dev, int64_t cap,
                        uint32_t nrec) {
     if (cap < 0) cap = 0;
@@ -821,12 +821,11 @@ void launch_radix_sort(hipStream_t s, const RadixWs& w, Header* h, const int64_t
     // at most kRhMaxBlocks blocks (each adds its counts with global atomics)
     unsigned nh = (unsigned)blocks_for(cap > 0 ? cap : 1, kRhTile);
     if (nh <= kMsMaxBlocks) {
-        // the bucket sort; when it cannot order the keys, the passes in one
-        // launch (one workgroup per tile, all resident for the grid barrier)
+        // the bucket sort; when it cannot order the keys, the bucket kernel's
+        // first workgroups run the passes instead
         k_rs_hist<<<nh, kRhThreads, 0, s>>>(w, count_dev, cap, nrec, (int64_t)nt, 1);
         k_ms_scatter<<<nh, kRhThreads, 0, s>>>(w, count_dev, cap);
-        k_ms_bucket<<<kMsMaxBuckets, kMsThreads, 0, s>>>(w);
-        k_rs_tail<<<nt, kRsThreads, kRsPassLds, s>>>(w, h, count_dev, cap, 0, (int64_t)nt);
+        k_ms_bucket<<<kMsMaxBuckets, kMsThreads, 0, s>>>(w, h, count_dev, cap, (int64_t)nt);
         return;
     }
     if (nh > kRhMaxBlocks) nh = kRhMaxBlocks;
