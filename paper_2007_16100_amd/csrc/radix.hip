@@ -211,9 +211,12 @@ __device__ inline MsGeom ms_geom(const SortStats& st) {
     g.A = kMsMaxBuckets - 1 - (kMsFine >> (g.spanlog < 31 ? g.spanlog : 31));
     return g;
 }
-// the bucket of fine bin f, whose items start at excl of total: non-decreasing in f
-__device__ inline uint32_t ms_bucket_of(const MsGeom& g, uint32_t f, uint32_t excl, uint32_t total) {
-    uint32_t a = total ? (uint32_t)((uint64_t)excl * g.A / total) : 0u;
+// the bucket of fine bin f, whose items start at excl; sc = A / total (0 with no
+// items).  A product with a rounded scale rather than a 64-bit division: still
+// non-decreasing in f (a correctly rounded product is monotone), and the same
+// in every block.
+__device__ inline uint32_t ms_bucket_of(const MsGeom& g, uint32_t f, uint32_t excl, double sc) {
+    uint32_t a = (uint32_t)((double)excl * sc);
     if (a > g.A - 1) a = g.A - 1;
     return a + (f >> g.spanlog);
 }
@@ -351,15 +354,16 @@ __global__ __launch_bounds__(kRhThreads) void k_ms_scatter(RadixWs w, const int6
 #pragma unroll
     for (int j = 1; j < BPT; ++j) e[j] = e[j - 1] + h[j - 1];
     const uint32_t total = (uint32_t)total_i;
+    const double sc = total ? (double)g.A / (double)total : 0.0;
     // bucket table: bucket b starts at the first fine bin whose bucket is b
     // (buckets left empty by a jump start where the next one does)
     {
         int64_t bp = -1;
-        if (t > 0) bp = ms_bucket_of(g, (uint32_t)(t * BPT - 1), e[0] - hprev, total);
+        if (t > 0) bp = ms_bucket_of(g, (uint32_t)(t * BPT - 1), e[0] - hprev, sc);
 #pragma unroll
         for (int j = 0; j < BPT; ++j) {
             const uint32_t f = (uint32_t)(t * BPT + j);
-            const uint32_t b = ms_bucket_of(g, f, e[j], total);
+            const uint32_t b = ms_bucket_of(g, f, e[j], sc);
             for (int64_t q = bp + 1; q <= (int64_t)b; ++q) {
                 sbs[q] = e[j];
                 sbf[q] = f;
