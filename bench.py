@@ -461,7 +461,8 @@ def backward_mode(args):
     _, ci, cw = spv.spv_devoxelize(ws, coords, x, d_xyz, 0.05, want_corners=True)
     dout = bf(synth.normal((n, C), 6, dtype="bf16"))
     dv = torch.empty((m, C), dtype=torch.float32, device=dev)
-    ms = timed(lambda: spv.spv_devoxelize_backward(ci, cw, dout, m, out=dv))
+    wsd = spv.Workspace.for_devox_backward(n, m)
+    ms = timed(lambda: spv.spv_devoxelize_backward(wsd, ci, cw, dout, m, out=dv))
     line("devoxelize backward C=96", ms, 0.0, 64 * n + 2 * C * n + 4 * C * m)
 
 

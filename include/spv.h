@@ -429,16 +429,24 @@ spv_status spv_voxelize_backward(void* stream, const void* dvfeat, int64_t m, in
 
 /*
  * spv_devoxelize_backward -- backward of the trilinear devoxelization w.r.t.
- * the voxel features (Sec. 3.3 "Sparse Devoxelization"): point k adds
- * dout[k] * w_c / sum of the present corners' w to voxel corner_idx[k][c] for
- * each present corner c (w = the raw trilinear weights).  dvfeat is zeroed
- * first.  fp32 atomic accumulation: the last bits depend on the order of the
- * additions.  No workspace.
- * In:  corner_idx [n][8], corner_w [n][8] as spv_devoxelize reports them;
- *      dout [n][C] (dt).
+ * the voxel features (Sec. 3.3 "Sparse Devoxelization"):
+ *   dvfeat[v] = sum over the points k and corners c with corner_idx[k][c] = v
+ *               of a_kc * dout[k],   a_kc = w_kc / (sum of k's present w)
+ * (w = the raw trilinear weights; a corner is present when 0 <= index < m; a
+ * point whose present weights sum to <= 0 adds nothing).  Deterministic: each
+ * voxel sums its terms in ascending (k, c) order with fp32 fmas, so repeated
+ * calls give the same bits; every row v < m is written (0 without terms).
+ * In:  ws: spv_devoxelize_backward_workspace_bytes(n, m) bytes, 256-byte
+ *      aligned; corner_idx [n][8] i32, corner_w [n][8] f32 as spv_devoxelize
+ *      reports them; dout [n][C] (dt).
  * Out: dvfeat [m][C] float32.
+ * Errors: SPV_ERR_INVALID_ARG (null pointers, negative sizes, n >= 2^28,
+ *      m >= 2^31 - 1), SPV_ERR_CAPACITY (ws too small); a corner index >= m is
+ *      skipped and reported as SPV_ERR_RANGE through spv_status_check(ws).
  */
-spv_status spv_devoxelize_backward(void* stream, const int32_t* corner_idx, const float* corner_w,
+size_t spv_devoxelize_backward_workspace_bytes(int64_t n, int64_t m);
+spv_status spv_devoxelize_backward(void* stream, void* ws, size_t ws_bytes,
+                                   const int32_t* corner_idx, const float* corner_w,
                                    const void* dout, int64_t n, int32_t C, float* dvfeat, int64_t m,
                                    spv_dtype dt);
 

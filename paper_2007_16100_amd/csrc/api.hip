@@ -640,11 +640,24 @@ spv_status spv_voxelize_backward(void* stream, const void* dvfeat, int64_t m, in
     return hip_check();
 }
 
-spv_status spv_devoxelize_backward(void* stream, const int32_t* corner_idx, const float* corner_w, const void* dout,
-                                   int64_t n, int32_t C, float* dvfeat, int64_t m, spv_dtype dt) {
-    if (m < 0 || n < 0 || C <= 0 || !valid_dt(dt) || (m > 0 && !dvfeat)) return SPV_ERR_INVALID_ARG;
+size_t spv_devoxelize_backward_workspace_bytes(int64_t n, int64_t m) {
+    if (n < 0 || m < 0) return 0;
+    Arena a(nullptr, 0);
+    plan_devox_backward_ws(a, n, m);
+    return a.used;
+}
+
+spv_status spv_devoxelize_backward(void* stream, void* ws, size_t ws_bytes, const int32_t* corner_idx,
+                                   const float* corner_w, const void* dout, int64_t n, int32_t C, float* dvfeat,
+                                   int64_t m, spv_dtype dt) {
+    if (!ws_ok(ws) || m < 0 || n < 0 || C <= 0 || !valid_dt(dt) || (m > 0 && !dvfeat)) return SPV_ERR_INVALID_ARG;
     if (n > 0 && (!corner_idx || !corner_w || !dout)) return SPV_ERR_INVALID_ARG;
-    launch_devoxelize_backward((hipStream_t)stream, corner_idx, corner_w, dout, n, C, dvfeat, m, (int)dt);
+    // entry numbers 8n and voxel positions fit int32
+    if (n >= ((int64_t)1 << 28) || m >= ((int64_t)1 << 31) - 1) return SPV_ERR_INVALID_ARG;
+    if (need(spv_devoxelize_backward_workspace_bytes(n, m), ws_bytes)) return SPV_ERR_CAPACITY;
+    Arena a(ws, ws_bytes);
+    const DvbWs w = plan_devox_backward_ws(a, n, m);
+    launch_devoxelize_backward((hipStream_t)stream, w, corner_idx, corner_w, dout, n, C, dvfeat, m, (int)dt);
     return hip_check();
 }
 

@@ -14,9 +14,9 @@
 //   over the same map with the pairs' roles swapped and W read transposed.
 // * backward of the scatter-mean (Eq. 2): dfeat[k] = dv[v(k)] / N_v(k);
 // * backward of the trilinear devoxelization w.r.t. the voxel features (Sec.
-//   3.3): each point scatters its gradient to its present corners with the
-//   weights the forward used (fp32 atomics: the order of the additions, and so
-//   the last bits, vary from run to run).
+//   3.3): every voxel gathers the gradients of the points that have it as a
+//   corner, weighted as the forward weighed them, in a fixed order (the same
+//   bits on every run).
 #include "conv_common.hpp"
 
 namespace spv {
@@ -327,50 +327,269 @@ void launch_voxelize_backward(hipStream_t s, const void* dv, int C, const int32_
 }
 
 // ---------------------------------------------------------------------------
-// devoxelization backward: zero dv, then thread per (point, channel) scatters
-// to the point's present corners with the renormalized forward weights
+// devoxelization backward, deterministic.  An entry is one present corner c of
+// one point k, numbered e = 8k + c, with the coefficient a = w_c / (sum of the
+// point's present corner weights).  A counting sort groups the entries by
+// voxel (count, scan, fill: inside a voxel the order is whatever the atomics
+// of the count gave); every entry then takes its place in ascending e among its
+// voxel's entries (it counts the smaller ones, so a voxel of L entries costs
+// L^2 comparisons spread over L threads); the gather sums a voxel's entries
+// a * dout[k] in that order, one fp32 fma after another, so the result is the
+// same bit for bit on every run.  Every voxel row is written, the empty ones
+// with zeros.
 // ---------------------------------------------------------------------------
-__global__ void k_fill_zero_f32(float* p, int64_t n) {
-    for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < n; t += (int64_t)gridDim.x * blockDim.x)
-        p[t] = 0.f;
+DvbWs plan_devox_backward_ws(Arena& a, int64_t n, int64_t m) {
+    DvbWs w;
+    w.h = a.take<Header>(1);
+    w.cnt = a.take<int32_t>((size_t)m + 1);
+    w.off = a.take<int32_t>((size_t)m + 1);
+    w.tmp = a.take<int32_t>(scan_tmp_entries(m));
+    const size_t E = 8 * (size_t)n;
+    w.slot = a.take<int32_t>(E);
+    w.ent = a.take<int32_t>(E);
+    w.coef = a.take<float>(E);
+    w.vox = a.take<int32_t>(E);
+    w.rec = a.take<int2>(E);
+    return w;
 }
 
-template <int DT>
-__global__ void k_devox_backward(const int32_t* __restrict__ cidx, const float* __restrict__ cw,
-                                 const void* __restrict__ dout, int64_t n, int C, float* __restrict__ dv, int64_t m) {
-    for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < n * C; t += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t k = t / C;
-        const int c = (int)(t - k * C);
+__global__ void k_dvb_zero(Header* h, int32_t* cnt, int64_t len) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        h->status = 0;
+        h->m = 0;
+        for (int i = 0; i < 4; ++i) h->aux[i] = 0;
+    }
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < len; i += (int64_t)gridDim.x * blockDim.x)
+        cnt[i] = 0;
+}
+
+// point k's present corners (0 <= idx < m; an index past m is reported and
+// skipped) and their coefficients; false when the weights sum to <= 0
+__device__ inline bool dvb_corners(const int32_t* cidx, const float* cw, int64_t k, int64_t m, Header* h,
+                                   int32_t idx[8], float a[8]) {
+    float den = 0.f;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        idx[q] = cidx[8 * k + q];
+        a[q] = cw[8 * k + q];
+        if (idx[q] >= m) {
+            if (h) raise_flag(h, kFlagRange);
+            idx[q] = -1;
+        }
+        if (idx[q] >= 0) den += a[q];
+    }
+    if (den <= 0.f) return false;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) a[q] = a[q] / den;
+    return true;
+}
+
+// Count every voxel's entries and give each entry its slot among them.  A
+// workgroup first groups its points' entries by voxel in an LDS hash table
+// (the points of a workgroup lie close together and share most corners), then
+// claims each voxel's share with one global atomic; an entry's slot is the
+// claimed base plus its rank in the workgroup.  slot[8k + c] = -1 marks an
+// absent corner.
+constexpr int kDvbThreads = 256;
+constexpr int kDvbHash = 4096;  // at most 8 * kDvbThreads keys: the table stays at most half full
+
+__global__ __launch_bounds__(kDvbThreads) void k_dvb_count(const int32_t* __restrict__ cidx,
+                                                           const float* __restrict__ cw, int64_t n, int64_t m,
+                                                           Header* h, int32_t* cnt, int32_t* __restrict__ slot) {
+    __shared__ int32_t hkey[kDvbHash];
+    __shared__ int32_t hval[kDvbHash];  // the workgroup's count of the key's entries, then the claimed base
+    const int t = threadIdx.x;
+    for (int i = t; i < kDvbHash; i += kDvbThreads) {
+        hkey[i] = -1;
+        hval[i] = 0;
+    }
+    __syncthreads();
+    const int64_t k = (int64_t)blockIdx.x * kDvbThreads + t;
+    int32_t idx[8];
+    float a[8];
+    const bool live = k < n && dvb_corners(cidx, cw, k, m, h, idx, a);
+    int hs[8], lr[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        hs[q] = -1;
+        lr[q] = 0;
+        if (!live || idx[q] < 0) continue;
+        uint32_t p = ((uint32_t)idx[q] * 2654435761u) >> 20;  // 12 bits
+        while (true) {
+            const int32_t old = atomicCAS(&hkey[p], -1, idx[q]);
+            if (old == -1 || old == idx[q]) break;
+            p = (p + 1) & (kDvbHash - 1);
+        }
+        hs[q] = (int)p;
+        lr[q] = atomicAdd(&hval[p], 1);
+    }
+    __syncthreads();
+    for (int i = t; i < kDvbHash; i += kDvbThreads) {
+        const int32_t v = hkey[i];
+        if (v >= 0) hval[i] = atomicAdd(cnt + v, hval[i]);
+    }
+    __syncthreads();
+    if (k < n) {
+        int32_t sl[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) sl[q] = hs[q] >= 0 ? hval[hs[q]] + lr[q] : -1;
+        int4* o = (int4*)(slot + 8 * k);
+        o[0] = make_int4(sl[0], sl[1], sl[2], sl[3]);
+        o[1] = make_int4(sl[4], sl[5], sl[6], sl[7]);
+    }
+}
+
+// every entry to its place in its voxel's range (no atomics: the count kernel
+// gave the slots)
+__global__ void k_dvb_fill(const int32_t* __restrict__ cidx, const float* __restrict__ cw, int64_t n, int64_t m,
+                           Header* h, const int32_t* __restrict__ slot, const int32_t* __restrict__ off, int32_t* ent,
+                           float* coef, int32_t* vox) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < n; k += (int64_t)gridDim.x * blockDim.x) {
         int32_t idx[8];
-        float w[8];
-        float den = 0.f;
+        float a[8];
+        if (!dvb_corners(cidx, cw, k, m, nullptr, idx, a)) continue;
+        const int4* sp = (const int4*)(slot + 8 * k);
+        const int4 s0 = sp[0], s1 = sp[1];
+        const int32_t sl[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            idx[q] = cidx[8 * k + q];
-            w[q] = cw[8 * k + q];
-            if (idx[q] >= 0 && idx[q] < m) den += w[q];
+            const int32_t v = idx[q];
+            if (v < 0) continue;
+            const int32_t lo = off[v];
+            if (sl[q] < 0 || sl[q] >= off[v + 1] - lo) {  // cannot happen: the count kernel saw the same corners
+                raise_flag(h, kFlagInternal);
+                continue;
+            }
+            const int64_t pos = lo + sl[q];
+            ent[pos] = (int32_t)(8 * k + q);
+            coef[pos] = a[q];
+            vox[pos] = v;
         }
-        if (den <= 0.f) continue;
-        const float g = ld_feat<DT>(dout, t) / den;
-#pragma unroll
-        for (int q = 0; q < 8; ++q)
-            if (idx[q] >= 0 && idx[q] < m) atomicAdd(dv + (int64_t)idx[q] * C + c, w[q] * g);
     }
 }
 
-void launch_devoxelize_backward(hipStream_t s, const int32_t* cidx, const float* cw, const void* dout, int64_t n, int C,
-                                float* dv, int64_t m, int dt) {
-    if (m > 0) {
-        int64_t gz = blocks_for(m * C, 256);
-        if (gz > 8192) gz = 8192;
-        k_fill_zero_f32<<<(unsigned)gz, 256, 0, s>>>(dv, m * C);
+// entry i of voxel v goes to position off[v] + (the entries of v smaller than
+// it): entries are distinct, so the positions are too
+__global__ void k_dvb_rank(const int32_t* __restrict__ off, int64_t m, int64_t cap, const int32_t* __restrict__ ent,
+                           const float* __restrict__ coef, const int32_t* __restrict__ vox, int2* __restrict__ rec) {
+    int64_t E = off[m];
+    if (E > cap) E = cap;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < E; i += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t v = vox[i], key = ent[i];
+        if ((uint64_t)(uint32_t)v >= (uint64_t)m) continue;  // only after a fill that raised kFlagInternal
+        const int32_t lo = off[v], hi = off[v + 1];
+        int32_t r = 0;
+        for (int32_t j = lo; j < hi; ++j) r += ent[j] < key ? 1 : 0;
+        rec[lo + r] = make_int2(key, __float_as_int(coef[i]));
     }
-    if (n <= 0) return;
-    int64_t g = blocks_for(n * C, 256);
-    if (g > 8192) g = 8192;
-    if (dt == SPV_F32) k_devox_backward<SPV_F32><<<(unsigned)g, 256, 0, s>>>(cidx, cw, dout, n, C, dv, m);
-    else if (dt == SPV_BF16) k_devox_backward<SPV_BF16><<<(unsigned)g, 256, 0, s>>>(cidx, cw, dout, n, C, dv, m);
-    else k_devox_backward<SPV_F16><<<(unsigned)g, 256, 0, s>>>(cidx, cw, dout, n, C, dv, m);
+}
+
+template <int DT, int VEC>
+__device__ inline void dvb_load(const void* p, int64_t i, float x[VEC]) {
+    if constexpr (VEC == 1) {
+        x[0] = ld_feat<DT>(p, i);
+    } else if constexpr (DT == SPV_F32) {
+        static_assert(VEC == 4, "four fp32 channels per 16 bytes");
+        const float4 v = *(const float4*)((const float*)p + i);
+        x[0] = v.x;
+        x[1] = v.y;
+        x[2] = v.z;
+        x[3] = v.w;
+    } else {
+        static_assert(VEC == 8, "eight 16-bit channels per 16 bytes");
+        const uint4 v = *(const uint4*)((const uint16_t*)p + i);
+        const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            x[2 * j] = from16<DT>(u[j] & 0xffffu);
+            x[2 * j + 1] = from16<DT>(u[j] >> 16);
+        }
+    }
+}
+
+// thread per (voxel, VEC consecutive channels): its entries four at a time
+// (the loads first, then the fmas in entry order).  An entry past the points
+// (left only by a fill that raised kFlagInternal) reads point 0 with weight 0.
+template <int DT, int VEC>
+__global__ void k_dvb_gather(const int32_t* __restrict__ off, const int2* __restrict__ rec, const void* __restrict__ dout,
+                             int64_t n, int C, int64_t m, float* __restrict__ dv) {
+    const int G = C / VEC;
+    for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < m * G; t += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t v = t / G;
+        const int c0 = (int)(t - v * G) * VEC;
+        const int32_t lo = off[v], hi = off[v + 1];
+        float acc[VEC];
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) acc[c] = 0.f;
+        int32_t i = lo;
+        for (; i + 4 <= hi; i += 4) {
+            int2 r[4];
+            float x[4][VEC];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                r[u] = rec[i + u];
+                if ((uint64_t)(uint32_t)(r[u].x >> 3) >= (uint64_t)n) r[u] = make_int2(0, 0);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) dvb_load<DT, VEC>(dout, (int64_t)(r[u].x >> 3) * C + c0, x[u]);
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int c = 0; c < VEC; ++c) acc[c] = fmaf(__int_as_float(r[u].y), x[u][c], acc[c]);
+        }
+        for (; i < hi; ++i) {
+            int2 r = rec[i];
+            if ((uint64_t)(uint32_t)(r.x >> 3) >= (uint64_t)n) r = make_int2(0, 0);
+            float x[VEC];
+            dvb_load<DT, VEC>(dout, (int64_t)(r.x >> 3) * C + c0, x);
+#pragma unroll
+            for (int c = 0; c < VEC; ++c) acc[c] = fmaf(__int_as_float(r.y), x[c], acc[c]);
+        }
+        float* o = dv + v * C + c0;
+        if constexpr (VEC == 1) {
+            o[0] = acc[0];
+        } else {
+#pragma unroll
+            for (int c = 0; c < VEC; c += 4) *(float4*)(o + c) = make_float4(acc[c], acc[c + 1], acc[c + 2], acc[c + 3]);
+        }
+    }
+}
+
+template <int DT, int VEC>
+static void launch_dvb_gather(hipStream_t s, const DvbWs& w, const void* dout, int64_t n, int C, int64_t m,
+                              float* dv) {
+    int64_t g = blocks_for(m * (C / VEC), 256);
+    if (g > 16384) g = 16384;
+    k_dvb_gather<DT, VEC><<<(unsigned)g, 256, 0, s>>>(w.off, w.rec, dout, n, C, m, dv);
+}
+
+void launch_devoxelize_backward(hipStream_t s, const DvbWs& w, const int32_t* cidx, const float* cw, const void* dout,
+                                int64_t n, int C, float* dv, int64_t m, int dt) {
+    int64_t gz = blocks_for(m + 1, 256 * 4);
+    if (gz > 4096) gz = 4096;
+    k_dvb_zero<<<(unsigned)gz, 256, 0, s>>>(w.h, w.cnt, m + 1);
+    if (m == 0) return;
+    if (n > 0) k_dvb_count<<<blocks_for(n, kDvbThreads), kDvbThreads, 0, s>>>(cidx, cw, n, m, w.h, w.cnt, w.slot);
+    launch_exclusive_scan(s, w.cnt, w.off, nullptr, m, w.tmp);
+    if (n > 0) {
+        int64_t gp = blocks_for(n, 256);
+        if (gp > 8192) gp = 8192;
+        k_dvb_fill<<<(unsigned)gp, 256, 0, s>>>(cidx, cw, n, m, w.h, w.slot, w.off, w.ent, w.coef, w.vox);
+        int64_t gr = blocks_for(8 * n, 256);
+        if (gr > 16384) gr = 16384;
+        k_dvb_rank<<<(unsigned)gr, 256, 0, s>>>(w.off, m, 8 * n, w.ent, w.coef, w.vox, w.rec);
+    }
+    const bool vec = (((uintptr_t)dout | (uintptr_t)dv) & 15u) == 0;
+    if (dt == SPV_F32) {
+        if (vec && C % 4 == 0) launch_dvb_gather<SPV_F32, 4>(s, w, dout, n, C, m, dv);
+        else launch_dvb_gather<SPV_F32, 1>(s, w, dout, n, C, m, dv);
+    } else if (dt == SPV_BF16) {
+        if (vec && C % 8 == 0) launch_dvb_gather<SPV_BF16, 8>(s, w, dout, n, C, m, dv);
+        else launch_dvb_gather<SPV_BF16, 1>(s, w, dout, n, C, m, dv);
+    } else {
+        if (vec && C % 8 == 0) launch_dvb_gather<SPV_F16, 8>(s, w, dout, n, C, m, dv);
+        else launch_dvb_gather<SPV_F16, 1>(s, w, dout, n, C, m, dv);
+    }
 }
 
 }  // namespace spv

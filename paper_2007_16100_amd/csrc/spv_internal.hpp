@@ -400,8 +400,23 @@ void* plan_wgrad_ws(Arena& a, int K3, int Cin, int Cout);
 void launch_wgrad(hipStream_t s, const WgradArgs& a, float* partial, float* dW);
 void launch_voxelize_backward(hipStream_t s, const void* dv, int C, const int32_t* counts, const int32_t* pt2vox,
                               int64_t n, int64_t m, void* dfeat, int dt);
-void launch_devoxelize_backward(hipStream_t s, const int32_t* cidx, const float* cw, const void* dout, int64_t n, int C,
-                                float* dv, int64_t m, int dt);
+// devoxelization backward: the counting sort of the (point, corner) entries by
+// voxel; entries hold 8 * point + corner, rec the (entry, coefficient) pairs of
+// every voxel in ascending entry order
+struct DvbWs {
+    Header* h;
+    int32_t* cnt;   // [m + 1] entries per voxel
+    int32_t* off;   // [m + 1] exclusive scan of cnt
+    int32_t* tmp;   // [scan_tmp_entries(m)]
+    int32_t* slot;  // [8n] each entry's slot in its voxel's range (-1: corner absent)
+    int32_t* ent;   // [8n] entry numbers in fill order
+    float* coef;    // [8n] their coefficients
+    int32_t* vox;   // [8n] their voxels
+    int2* rec;      // [8n] (entry, coefficient bits), sorted within each voxel
+};
+DvbWs plan_devox_backward_ws(Arena& a, int64_t n, int64_t m);
+void launch_devoxelize_backward(hipStream_t s, const DvbWs& w, const int32_t* cidx, const float* cw, const void* dout,
+                                int64_t n, int C, float* dv, int64_t m, int dt);
 
 // weight packings a block call runs inside its voxelization's first launch
 constexpr int kMaxPackJobs = 3;

@@ -35,7 +35,7 @@ EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_voxelize_onto", "spv_pack
            "spv_linear", "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_map_children", "spv_sparse_conv_up",
            "spv_sparse_conv_dgrad", "spv_wgrad_workspace_bytes", "spv_sparse_conv_wgrad",
            "spv_voxelize_backward",
-           "spv_devoxelize_backward", "spv_devoxelize",
+           "spv_devoxelize_backward_workspace_bytes", "spv_devoxelize_backward", "spv_devoxelize",
            "spv_block_workspace_bytes", "spv_block", "spv_lookup", "spv_voxel_lookup", "spv_conv_kernel",
            "spv_sparse_conv_nbr_noalloc",
            "spv_block_conv_kernel", "spv_status_check", "spv_status_string", "spv_last_hip_error")
@@ -99,7 +99,9 @@ def lib():
         L.spv_wgrad_workspace_bytes.argtypes = [i32, i32, i32]
         L.spv_wgrad_workspace_bytes.restype = sz
         L.spv_voxelize_backward.argtypes = [vp, vp, i64, i32, vp, vp, i64, vp, i32]
-        L.spv_devoxelize_backward.argtypes = [vp, vp, vp, vp, i64, i32, vp, i64, i32]
+        L.spv_devoxelize_backward.argtypes = [vp, vp, sz, vp, vp, vp, i64, i32, vp, i64, i32]
+        L.spv_devoxelize_backward_workspace_bytes.argtypes = [i64, i64]
+        L.spv_devoxelize_backward_workspace_bytes.restype = sz
         L.spv_devoxelize.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, vp, i64, f32, i32, vp, i32, vp, i32, vp, vp,
                                      vp, i32, vp, i32, vp, vp]
         L.spv_devoxelize_nbr.argtypes = [vp, vp, sz, vp, vp, i64, vp, vp, i32, vp, vp, i64, f32, i32, vp, i32, vp,
@@ -164,6 +166,10 @@ class Workspace:
     @classmethod
     def for_wgrad(cls, K3: int, Cin: int, Cout: int, device="cuda"):
         return cls(lib().spv_wgrad_workspace_bytes(K3, Cin, Cout), device)
+
+    @classmethod
+    def for_devox_backward(cls, n: int, m: int, device="cuda"):
+        return cls(lib().spv_devoxelize_backward_workspace_bytes(n, m), device)
 
     @classmethod
     def for_block(cls, max_points: int, C: int, device="cuda"):
@@ -520,13 +526,13 @@ def spv_voxelize_backward(dvfeat: torch.Tensor, counts: torch.Tensor, pt2vox: to
     return out
 
 
-def spv_devoxelize_backward(corner_idx: torch.Tensor, corner_w: torch.Tensor, dout: torch.Tensor, m: int,
-                            out: Optional[torch.Tensor] = None) -> torch.Tensor:
+def spv_devoxelize_backward(ws: Workspace, corner_idx: torch.Tensor, corner_w: torch.Tensor, dout: torch.Tensor,
+                            m: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     n, C = dout.shape
     if out is None:
         out = torch.empty((max(m, 1), C), dtype=torch.float32, device=dout.device)
-    st = lib().spv_devoxelize_backward(_stream(), _ptr(corner_idx), _ptr(corner_w), _ptr(dout), n, C, _ptr(out), m,
-                                       _DT[dout.dtype])
+    st = lib().spv_devoxelize_backward(_stream(), ws.ptr, ws.nbytes, _ptr(corner_idx), _ptr(corner_w), _ptr(dout), n,
+                                       C, _ptr(out), m, _DT[dout.dtype])
     _chk(st, "spv_devoxelize_backward")
     return out
 

@@ -135,7 +135,16 @@ def test_host_side_validation_without_gpu():
     assert L.spv_wgrad_workspace_bytes(27, 0, 32) == 0
     # backward of the scatter-mean / devox: negative sizes
     assert L.spv_voxelize_backward(None, None, -1, 4, None, None, 0, None, 1) == spv.SPV_ERR_INVALID_ARG
-    assert L.spv_devoxelize_backward(None, None, None, None, 4, 8, None, 4, 1) == spv.SPV_ERR_INVALID_ARG
+    assert L.spv_devoxelize_backward(None, ws, 1 << 30, None, None, None, 4, 8, None, 4, 1) == spv.SPV_ERR_INVALID_ARG
+    # devox backward: no workspace; a small one; sizes past the int32 entry numbers
+    dvb = (ct.c_void_p(16), ct.c_void_p(16), ct.c_void_p(16), 4, 8, ct.c_void_p(16), 4, 1)
+    assert L.spv_devoxelize_backward(None, None, 1 << 30, *dvb) == spv.SPV_ERR_INVALID_ARG
+    assert L.spv_devoxelize_backward(None, ws, 64, *dvb) == spv.SPV_ERR_CAPACITY
+    assert L.spv_devoxelize_backward(None, ws, 1 << 40, ct.c_void_p(16), ct.c_void_p(16), ct.c_void_p(16), 1 << 28, 8,
+                                     ct.c_void_p(16), 4, 1) == spv.SPV_ERR_INVALID_ARG
+    need = L.spv_devoxelize_backward_workspace_bytes(1000, 700)
+    assert need >= 1000 * 8 * 20 + 700 * 8
+    assert L.spv_devoxelize_backward_workspace_bytes(-1, 700) == 0
     # misaligned feature pointer
     st = L.spv_sparse_conv(None, ws, 1 << 30, ct.c_void_p(18), 4, 8, ct.c_void_p(16), ct.c_void_p(16), 4, 27, 0,
                            ct.c_void_p(16), None, None, 0, ct.c_void_p(16), None, 4, 16, 1)

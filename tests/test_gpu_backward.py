@@ -126,6 +126,48 @@ def test_devoxelize_backward(spv, sweep, mode, stride_log2, C, dtype):
     vf = synth.normal((len(rc), C), 1106, dtype=dtype)
     _, ci, cw = oracle.devoxelize(rc, vf, pts, 0.05, stride_log2, mode, dtype=dtype, want_corners=True)
     dout = synth.normal((len(pts), C), 1107, dtype=dtype)
-    got = host(spv.spv_devoxelize_backward(dev(ci), dev(cw), dev(dout, dtype), len(rc)))[: len(rc)]
+    ws = spv.Workspace.for_devox_backward(len(pts), len(rc))
+    args = (ws, dev(ci), dev(cw), dev(dout, dtype), len(rc))
+    got = host(spv.spv_devoxelize_backward(*args))[: len(rc)]
+    again = host(spv.spv_devoxelize_backward(*args))[: len(rc)]
+    np.testing.assert_array_equal(got, again)  # deterministic
+    assert spv.spv_status_check(ws) == spv.SPV_OK
     ref = oracle.devoxelize_backward(ci, cw, dout, len(rc), dtype)
     parity.check(got, ref, "f32")
+
+
+def test_devoxelize_backward_edges(spv):
+    """Voxels with 0 to ~80 terms (over 64 and under), three voxels with none, absent corners, weights summing
+    to 0, odd C (one channel per thread), a misaligned gradient (no vector loads) and a corner index past m."""
+    rng = np.random.default_rng(1108)
+    lengths = np.arange(71)
+    m = len(lengths) + 3  # the last three voxels get no terms: their rows must be zeros
+    # point k has corner 0 on voxel owner[k]; each other corner on a random voxel below len(lengths) with
+    # probability 1/20, else absent
+    owner = np.repeat(np.arange(len(lengths)), lengths)
+    n = len(owner)
+    ci = rng.integers(0, len(lengths), size=(n, 8)).astype(np.int32)
+    ci[rng.random((n, 8)) >= 0.05] = -1
+    ci[:, 0] = owner
+    cw = rng.random((n, 8)).astype(np.float32)
+    cw[::7] = 0.0  # present weights summing to 0: the point adds nothing
+    for C, dtype in ((5, "f32"), (16, "bf16")):
+        dout = synth.normal((n, C), 1109, dtype=dtype)
+        ref = oracle.devoxelize_backward(ci, cw, dout, m, dtype)
+        ws = spv.Workspace.for_devox_backward(n, m)
+        got = host(spv.spv_devoxelize_backward(ws, dev(ci), dev(cw), dev(dout, dtype), m))[:m]
+        assert spv.spv_status_check(ws) == spv.SPV_OK
+        assert not got[len(lengths):].any()
+        parity.check(got, ref, "f32")
+        if dtype == "bf16":  # a gradient 2 bytes off a 16-byte boundary
+            buf = torch.empty(n * C + 1, dtype=torch.bfloat16, device="cuda")
+            shifted = buf[1:].view(n, C)
+            shifted.copy_(dev(dout, dtype))
+            got2 = host(spv.spv_devoxelize_backward(ws, dev(ci), dev(cw), shifted, m))[:m]
+            parity.check(got2, ref, "f32")
+    # a corner index past m: skipped, reported as a range error
+    bad = ci.copy()
+    bad[3, 5] = m + 2
+    ws = spv.Workspace.for_devox_backward(n, m)
+    spv.spv_devoxelize_backward(ws, dev(bad), dev(cw), dev(synth.normal((n, 8), 1110, dtype="f32"), "f32"), m)
+    assert spv.spv_status_check(ws) == spv.SPV_ERR_RANGE

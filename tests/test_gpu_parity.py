@@ -1138,7 +1138,8 @@ def test_empty_inputs_of_network_entry_points(spv):
     dW = spv.spv_sparse_conv_wgrad(wsw, torch.zeros((4, 32), dtype=torch.bfloat16, device=d),
                                    torch.zeros((4, 32), dtype=torch.bfloat16, device=d), off, pairs, 27)
     assert torch.count_nonzero(dW).item() == 0
-    dv = spv.spv_devoxelize_backward(torch.zeros((0, 8), dtype=torch.int32, device=d),
+    dv = spv.spv_devoxelize_backward(spv.Workspace.for_devox_backward(0, 5),
+                                     torch.zeros((0, 8), dtype=torch.int32, device=d),
                                      torch.zeros((0, 8), dtype=torch.float32, device=d),
                                      torch.zeros((0, 16), dtype=torch.bfloat16, device=d), 5,
                                      out=torch.full((5, 16), 3.0, dtype=torch.float32, device=d))
