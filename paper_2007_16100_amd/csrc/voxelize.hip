@@ -567,9 +567,7 @@ static void launch_mean(hipStream_t s, const VoxelizeWs& w, int64_t n, const voi
                                                                  w.table, coords, n <= kMeanInsFirst ? 1 : 0,
                                                                  w.nbr_upper);
     if (split) {
-        // a workgroup per CU: the long voxels are few (at most n / (kMeanRun + 1)),
-        // and a larger grid costs its dispatch even when there are none
-        const int64_t g = n < 256 ? (n > 0 ? n : 1) : 256;
+        const int64_t g = n < 1024 ? (n > 0 ? n : 1) : 1024;
         k_vox_mean_long<DT, VEC><<<(unsigned)g, kMeanLongThreads, 0, s>>>(w.h, n, w.seg, w.plist, feat, C, vfeat,
                                                                           w.longv);
     }
