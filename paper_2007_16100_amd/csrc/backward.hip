@@ -26,9 +26,10 @@ constexpr int kWgChunk = 64;  // pairs per LDS fill: two MFMA K-steps of 32
 constexpr int kWgLd = kWgChunk + 8;  // LDS row length in 16-bit elements (padded)
 constexpr int kWgMaxRowPair = 512;    // Cin + Cout the MFMA kernel takes (8 pieces per thread)
 
-// slices per offset: as many as a 64 MB partial-sum buffer holds (the centre
-// offset of a submanifold map has ~15% of the pairs: more slices spread it
-// over more compute units), a power of two in [8, 64]
+// slices per offset of the vector-ALU kernel: as many as a 64 MB partial-sum
+// buffer holds (the centre offset of a submanifold map has ~15% of the pairs:
+// more slices spread it over more compute units), a power of two in [8, 64];
+// the buffer is sized by it for both kernels
 static int wgrad_slices(int Cin, int Cout) {
     const int64_t per = (int64_t)27 * Cin * Cout * 4;
     int S = 64;
@@ -37,6 +38,24 @@ static int wgrad_slices(int Cin, int Cout) {
 }
 
 bool wgrad_supported(int Cin, int Cout) { return (int64_t)Cin * Cout <= 256 * 256; }
+
+// The MFMA kernel splits the chunks of all offsets (64 pairs each, never
+// across offsets; offset-major, as the map stores them) into G equal
+// contiguous ranges, one per workgroup, so the centre offset's many pairs
+// spread over as many workgroups as the rest.  A workgroup writes one
+// partial sum per offset its range touches, to slot w + k: G + K3 - 1 slots
+// at most, which the slice buffer holds when G <= K3 * (S - 1).
+constexpr int kWgMaxK3 = 27;
+constexpr int kWgMaxGroups = 1024;
+__host__ __device__ inline int64_t wgrad_chunks_per_wg(int64_t chunks, int G) { return (chunks + G - 1) / G; }
+// LDS of the MFMA kernel: the transposed chunk tiles, then 3 * 28 int64 of offset data
+__host__ __device__ inline size_t wgrad_tiles_bytes(int Cin, int Cout) {
+    return ((size_t)(Cin + Cout) * kWgLd * 2 + 15) & ~(size_t)15;
+}
+static int wgrad_groups(int K3, int S) {
+    const int g = K3 * (S - 1);
+    return g < kWgMaxGroups ? g : kWgMaxGroups;
+}
 
 void* plan_wgrad_ws(Arena& a, int K3, int Cin, int Cout) {
     return a.take<float>((size_t)K3 * wgrad_slices(Cin, Cout) * Cin * Cout);
@@ -54,13 +73,28 @@ template <int DT, int TPW, int PPT>
 __global__ __launch_bounds__(64 * kWgWaves) void k_conv_wgrad_mfma(
     const uint16_t* __restrict__ x, int64_t x_rows, int Cin, const uint16_t* __restrict__ dy, int64_t dy_rows,
     int Cout, const int32_t* __restrict__ off, const int32_t* __restrict__ pairs, int64_t pair_bound, int transposed,
-    float* __restrict__ partial) {
+    int K3, float* __restrict__ partial) {
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t* xt = (uint16_t*)smem;             // [Cin][kWgLd]
     uint16_t* gt = xt + (size_t)Cin * kWgLd;    // [Cout][kWgLd]
-    const int k = blockIdx.y, S = gridDim.x, sl = blockIdx.x;
-    int64_t lo, hi;
-    pair_range(off, k, pair_bound, lo, hi);
+    // then the offsets' pair ranges and chunk prefix (all LDS is dynamic: the
+    // launch raises the dynamic limit to the whole 160 KB)
+    int64_t* s_lo = (int64_t*)(smem + wgrad_tiles_bytes(Cin, Cout));
+    int64_t* s_hi = s_lo + kWgMaxK3;
+    int64_t* s_cpre = s_hi + kWgMaxK3;
+    const int G = gridDim.x, w = blockIdx.x;
+    if (threadIdx.x == 0) {
+        int64_t c = 0;
+        for (int k = 0; k < K3; ++k) {
+            pair_range(off, k, pair_bound, s_lo[k], s_hi[k]);
+            s_cpre[k] = c;
+            c += (s_hi[k] - s_lo[k] + kWgChunk - 1) / kWgChunk;
+        }
+        s_cpre[K3] = c;
+    }
+    __syncthreads();
+    const int64_t T = wgrad_chunks_per_wg(s_cpre[K3], G);
+    const int64_t g0 = (int64_t)w * T, g1 = g0 + T < s_cpre[K3] ? g0 + T : s_cpre[K3];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r16 = lane & 15, g = lane >> 4;
@@ -78,30 +112,76 @@ __global__ __launch_bounds__(64 * kWgWaves) void k_conv_wgrad_mfma(
     // zeros past the chunk's pairs and the rows
     static_assert(kWgChunk == 64, "one pair per lane");
     uint4 pv[PPT];
-    auto gather = [&](int64_t c0) {
-        const int np = (hi - c0) < kWgChunk ? (int)(hi - c0) : kWgChunk;
+    // global chunk gc: its offset (from kc upwards) and first pair
+    auto locate = [&](int64_t gc, int& kc, int64_t& c0, int& np) {
+        while (kc + 1 < K3 && gc >= s_cpre[kc + 1]) ++kc;
+        c0 = s_lo[kc] + (gc - s_cpre[kc]) * kWgChunk;
+        const int64_t left = s_hi[kc] - c0;
+        np = left < kWgChunk ? (int)left : kWgChunk;
+    };
+    // a thread's pieces all belong to pair threadIdx.x % 64 of the chunk: its
+    // two row indices are loaded one chunk before its rows (-1: no pair)
+    auto load_idx = [&](int64_t c0, int np, int64_t& ii, int64_t& jj) {
+        const int p = threadIdx.x & (kWgChunk - 1);
+        ii = -1;
+        jj = -1;
+        if (p < np) {
+            ii = pairs[2 * (c0 + p) + isel];
+            jj = pairs[2 * (c0 + p) + 1 - isel];
+        }
+    };
+    auto gather = [&](int64_t ii, int64_t jj) {
 #pragma unroll
         for (int r = 0; r < PPT; ++r) {
-            const int e = threadIdx.x + r * 64 * kWgWaves;
-            const int p = e & (kWgChunk - 1), q = e / kWgChunk;
+            const int q = (threadIdx.x + r * 64 * kWgWaves) / kWgChunk;
             uint4 v = make_uint4(0u, 0u, 0u, 0u);
-            if (q < qq && p < np && c0 < hi) {
-                const int64_t pp = c0 + p;
-                if (q < qx) {
-                    const int64_t i = pairs[2 * pp + isel];
-                    if (i >= 0 && i < x_rows) v = *(const uint4*)(x + i * Cin + q * 8);
-                } else {
-                    const int64_t j = pairs[2 * pp + 1 - isel];
-                    if (j >= 0 && j < dy_rows) v = *(const uint4*)(dy + j * Cout + (q - qx) * 8);
-                }
+            if (q < qx) {
+                if (ii >= 0 && ii < x_rows) v = *(const uint4*)(x + ii * Cin + q * 8);
+            } else if (q < qq) {
+                if (jj >= 0 && jj < dy_rows) v = *(const uint4*)(dy + jj * Cout + (q - qx) * 8);
             }
             pv[r] = v;
         }
     };
-    const int64_t step = (int64_t)S * kWgChunk;
-    int64_t c0 = lo + (int64_t)sl * kWgChunk;
-    if (c0 < hi) gather(c0);
-    for (; c0 < hi; c0 += step) {
+    // lane (r16, g) of tile (ci0, co0) holds dW[ci0 + 4g + e][co0 + r16]: the
+    // workgroup's sums for offset k go to slot w + k (the offsets a workgroup
+    // covers only grow with w, so the slots are distinct)
+    auto flush = [&](int k) {
+        float* pk = partial + ((int64_t)w + k) * Cin * Cout;
+#pragma unroll
+        for (int u = 0; u < TPW; ++u) {
+            const int t = wave + u * kWgWaves;
+            if (t < NT) {
+                const int ci0 = (t / NTc) * 16, co0 = (t - (t / NTc) * NTc) * 16;
+                // Cout through an opaque copy: left visible, the compiler hoists
+                // all TPW * 4 store addresses out of the chunk loop (66 more
+                // registers, half the waves per SIMD)
+                int cv;
+                asm volatile("s_mov_b32 %0, %1" : "=s"(cv) : "s"(Cout));
+                float* q = pk + (int64_t)(ci0 + 4 * g) * cv + co0 + r16;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) q[(int64_t)e * cv] = acc[u][e];
+            }
+            acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+    };
+    // chunk gc's rows are in pv; chunk gc + 1's offset k1 and row indices
+    // (i1, j1) are known
+    int kcur = 0, k1 = 0;
+    int64_t i1 = -1, j1 = -1;
+    if (g0 < g1) {
+        int64_t c0, ii, jj;
+        int np;
+        locate(g0, kcur, c0, np);
+        load_idx(c0, np, ii, jj);
+        gather(ii, jj);
+        k1 = kcur;
+        if (g0 + 1 < g1) {
+            locate(g0 + 1, k1, c0, np);
+            load_idx(c0, np, i1, j1);
+        }
+    }
+    for (int64_t gc = g0; gc < g1; ++gc) {
         // the pieces in registers -> LDS, channel-major
 #pragma unroll
         for (int r = 0; r < PPT; ++r) {
@@ -109,22 +189,37 @@ __global__ __launch_bounds__(64 * kWgWaves) void k_conv_wgrad_mfma(
             const int p = e & (kWgChunk - 1), q = e / kWgChunk;
             if (q < qq) {
                 uint16_t* dst = (q < qx ? xt + (size_t)(q * 8) * kWgLd : gt + (size_t)((q - qx) * 8) * kWgLd) + p;
-                const uint32_t w[4] = {pv[r].x, pv[r].y, pv[r].z, pv[r].w};
+                const uint32_t wd[4] = {pv[r].x, pv[r].y, pv[r].z, pv[r].w};
 #pragma unroll
                 for (int h = 0; h < 4; ++h) {
-                    dst[(2 * h) * kWgLd] = (uint16_t)(w[h] & 0xFFFF);
-                    dst[(2 * h + 1) * kWgLd] = (uint16_t)(w[h] >> 16);
+                    dst[(2 * h) * kWgLd] = (uint16_t)(wd[h] & 0xFFFF);
+                    dst[(2 * h + 1) * kWgLd] = (uint16_t)(wd[h] >> 16);
                 }
             }
         }
         __syncthreads();
-        // the next chunk's gathers are in flight while this one is multiplied
-        gather(c0 + step);
+        // the next chunk's rows and the indices of the one after are in flight
+        // while this one is multiplied
+        gather(i1, j1);
+        int k2 = k1;
+        int64_t i2 = -1, j2 = -1;
+        if (gc + 2 < g1) {
+            int64_t c2;
+            int n2;
+            locate(gc + 2, k2, c2, n2);
+            load_idx(c2, n2, i2, j2);
+        }
 #pragma unroll
         for (int ks = 0; ks < kWgChunk / 32; ++ks) {
 #pragma unroll
             for (int u = 0; u < TPW; ++u) {
-                const int t = wave + u * kWgWaves;  // wave-uniform
+                // wave-uniform.  With 16 or more tiles per wave it goes through an
+                // opaque copy, as Cout in flush: the LDS addresses of all tiles
+                // would otherwise be hoisted out of the chunk loop and held,
+                // and the wave would spill (with fewer tiles, recomputing them
+                // every chunk costs more than holding them)
+                int t = wave + u * kWgWaves;
+                if constexpr (TPW >= 16) asm volatile("s_mov_b32 %0, %1" : "=s"(t) : "s"(wave + u * kWgWaves));
                 if (t < NT) {
                     const int ci0 = (t / NTc) * 16, co0 = (t - (t / NTc) * NTc) * 16;
                     const uint4 a = *(const uint4*)(xt + (size_t)(ci0 + r16) * kWgLd + ks * 32 + 8 * g);
@@ -134,17 +229,11 @@ __global__ __launch_bounds__(64 * kWgWaves) void k_conv_wgrad_mfma(
             }
         }
         __syncthreads();
-    }
-    // lane (r16, g) of tile (ci0, co0) holds dW[ci0 + 4g + e][co0 + r16]
-    float* pk = partial + ((int64_t)k * S + sl) * Cin * Cout;
-#pragma unroll
-    for (int u = 0; u < TPW; ++u) {
-        const int t = wave + u * kWgWaves;
-        if (t < NT) {
-            const int ci0 = (t / NTc) * 16, co0 = (t - (t / NTc) * NTc) * 16;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) pk[(int64_t)(ci0 + 4 * g + e) * Cout + co0 + r16] = acc[u][e];
-        }
+        if (gc + 1 == g1 || k1 != kcur) flush(kcur);
+        kcur = k1;
+        k1 = k2;
+        i1 = i2;
+        j1 = j2;
     }
 }
 
@@ -182,6 +271,67 @@ __global__ void k_wgrad_reduce(const float* __restrict__ partial, int S, int64_t
     dW[t] = s;
 }
 
+__device__ inline void acc_add(float& s, float v) { s += v; }
+__device__ inline void acc_add(float4& s, const float4& v) {
+    s.x += v.x;
+    s.y += v.y;
+    s.z += v.z;
+    s.w += v.w;
+}
+
+// dW[k][e] = the sum of slots w + k over the workgroups w whose chunk ranges
+// touch offset k (zero when offset k has no pairs).  V = float4 (four elements
+// per lane) or float.  A workgroup of 4 waves takes 64 element groups of one
+// offset: wave q sums the q-th quarter of the workgroups in order, and the
+// four quarter sums are added in quarter order -- a fixed association, so the
+// result does not depend on scheduling, with a quarter of the dependent loads
+// per lane.  The chunk bounds of offset k are recomputed from off as the MFMA
+// kernel computed them.
+constexpr int kWgRedParts = 4;
+template <class V>
+__global__ __launch_bounds__(64 * kWgRedParts) void k_wgrad_reduce_bal(const V* __restrict__ partial, int G,
+                                                                       int64_t per_kv, const int32_t* off,
+                                                                       int64_t pair_bound, V* __restrict__ dW) {
+    __shared__ V red[kWgRedParts][64];
+    const int k = blockIdx.y, K3 = gridDim.y;
+    const int lane = threadIdx.x & 63, part = threadIdx.x >> 6;
+    const int64_t e = blockIdx.x * (int64_t)64 + lane;
+    int64_t c = 0, ck = 0, nk = 0;
+    for (int q = 0; q < K3; ++q) {
+        int64_t lo, hi;
+        pair_range(off, q, pair_bound, lo, hi);
+        const int64_t n = (hi - lo + kWgChunk - 1) / kWgChunk;
+        if (q == k) {
+            ck = c;
+            nk = n;
+        }
+        c += n;
+    }
+    V s{};
+    if (nk > 0 && e < per_kv) {
+        const int64_t T = wgrad_chunks_per_wg(c, G);
+        const int64_t wlo = ck / T, nw = (ck + nk - 1) / T - wlo + 1;
+        const int64_t pw = (nw + kWgRedParts - 1) / kWgRedParts;
+        const int64_t wa = wlo + part * pw, wb = wa + pw < wlo + nw ? wa + pw : wlo + nw;
+        int64_t w = wa;
+        for (; w + 8 <= wb; w += 8) {  // the loads together, the additions in order
+            V v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = partial[(w + u + k) * per_kv + e];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) acc_add(s, v[u]);
+        }
+        for (; w < wb; ++w) acc_add(s, partial[(w + k) * per_kv + e]);
+    }
+    red[part][lane] = s;
+    __syncthreads();
+    if (part == 0 && e < per_kv) {
+#pragma unroll
+        for (int q = 1; q < kWgRedParts; ++q) acc_add(s, red[q][lane]);
+        dW[(int64_t)k * per_kv + e] = s;
+    }
+}
+
 // The same sums four elements per thread, the slices eight at a time (their
 // loads issued together, then added in slice order: the same bits as above).
 // Needs per_k % 4 == 0, S % 8 == 0 and a 16-byte aligned dW.
@@ -209,14 +359,15 @@ __global__ void k_wgrad_reduce4(const float4* __restrict__ partial, int S, int64
 
 template <int DT, int TPW, int PPT>
 static void launch_wgrad_mfma3(hipStream_t s, dim3 grid, const WgradArgs& a, float* partial) {
-    const size_t lds = (size_t)(a.Cin + a.Cout) * kWgLd * 2;
+    const size_t lds = wgrad_tiles_bytes(a.Cin, a.Cout) + (3 * kWgMaxK3 + 1) * sizeof(int64_t);
     static const bool lds_ok = hipFuncSetAttribute((const void*)k_conv_wgrad_mfma<DT, TPW, PPT>,
                                                    hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) ==
                                hipSuccess;
     (void)lds_ok;
     k_conv_wgrad_mfma<DT, TPW, PPT><<<grid, 64 * kWgWaves, lds, s>>>((const uint16_t*)a.x, a.x_rows, a.Cin,
                                                                      (const uint16_t*)a.dy, a.dy_rows, a.Cout, a.off,
-                                                                     a.pairs, a.pair_bound, a.transposed, partial);
+                                                                     a.pairs, a.pair_bound, a.transposed, a.K3,
+                                                                     partial);
 }
 
 template <int DT, int TPW>
@@ -244,13 +395,26 @@ static void launch_wgrad_tpw(hipStream_t s, dim3 grid, const WgradArgs& a, float
 void launch_wgrad(hipStream_t s, const WgradArgs& a, float* partial, float* dW) {
     const int S = wgrad_slices(a.Cin, a.Cout);
     const dim3 grid((unsigned)S, (unsigned)a.K3);
+    const int G = wgrad_groups(a.K3, S);
     // the MFMA kernel gathers at most 8 pieces of 16 bytes per thread, i.e. 64
     // pieces (512 channels) of a pair's two rows, and holds both rows of 64
     // pairs in LDS: wider pairs run on the vector-ALU kernel
     const bool mfma = a.dt != SPV_F32 && a.Cin % 16 == 0 && a.Cout % 16 == 0 && a.Cin + a.Cout <= kWgMaxRowPair;
+    const int64_t per_k = (int64_t)a.Cin * a.Cout;
     if (mfma) {
-        if (a.dt == SPV_BF16) launch_wgrad_tpw<SPV_BF16>(s, grid, a, partial);
-        else launch_wgrad_tpw<SPV_F16>(s, grid, a, partial);
+        const dim3 gb((unsigned)G, 1);
+        if (a.dt == SPV_BF16) launch_wgrad_tpw<SPV_BF16>(s, gb, a, partial);
+        else launch_wgrad_tpw<SPV_F16>(s, gb, a, partial);
+        // per_k is a multiple of 256 here (16-channel multiples)
+        if (((uintptr_t)dW & 15u) == 0) {
+            const dim3 gr(blocks_for(per_k / 4, 64), (unsigned)a.K3);
+            k_wgrad_reduce_bal<float4><<<gr, 64 * kWgRedParts, 0, s>>>((const float4*)partial, G, per_k / 4, a.off,
+                                                                       a.pair_bound, (float4*)dW);
+        } else {
+            const dim3 gr(blocks_for(per_k, 64), (unsigned)a.K3);
+            k_wgrad_reduce_bal<float><<<gr, 64 * kWgRedParts, 0, s>>>(partial, G, per_k, a.off, a.pair_bound, dW);
+        }
+        return;
     } else if (a.dt == SPV_F32) {
         k_conv_wgrad_valu<SPV_F32><<<grid, 256, 0, s>>>(a.x, a.x_rows, a.Cin, a.dy, a.dy_rows, a.Cout, a.off, a.pairs,
                                                         a.pair_bound, a.transposed, partial);
@@ -261,7 +425,6 @@ void launch_wgrad(hipStream_t s, const WgradArgs& a, float* partial, float* dW) 
         k_conv_wgrad_valu<SPV_F16><<<grid, 256, 0, s>>>(a.x, a.x_rows, a.Cin, a.dy, a.dy_rows, a.Cout, a.off, a.pairs,
                                                         a.pair_bound, a.transposed, partial);
     }
-    const int64_t per_k = (int64_t)a.Cin * a.Cout;
     if (per_k % 4 == 0 && S % 8 == 0 && ((uintptr_t)dW & 15u) == 0)
         k_wgrad_reduce4<<<blocks_for((int64_t)a.K3 * per_k / 4, 256), 256, 0, s>>>((const float4*)partial, S,
                                                                                     per_k / 4, a.K3, (float4*)dW);
