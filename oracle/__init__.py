@@ -57,12 +57,14 @@ def lib():
         L.spvo_sparse_conv_wgrad.argtypes = [vp, i64, i32, vp, i64, i32, vp, vp, i32, i32, vp, i32]
         L.spvo_voxelize_backward.argtypes = [vp, i64, i32, vp, vp, i64, vp, i32]
         L.spvo_devoxelize_backward.argtypes = [vp, vp, vp, i64, i32, vp, i64, i32]
+        L.spvo_epilogue_backward.argtypes = [vp, vp, vp, vp, i32, vp, i32, i64, i32, vp, vp, vp, vp, i32]
+        L.spvo_linear_backward.argtypes = [vp, i64, i32, vp, i32, vp, vp, vp, i32]
         L.spvo_decode.argtypes = [vp, i64, i32]
         L.spvo_decode.restype = ct.c_double
         L.spvo_round_store.argtypes = [ct.c_double, vp, i64, i32]
         for f in ("spvo_voxelize", "spvo_kernel_map", "spvo_sparse_conv", "spvo_sparse_conv_res", "spvo_devoxelize",
                   "spvo_block", "spvo_linear", "spvo_sparse_conv_wgrad", "spvo_voxelize_backward",
-                  "spvo_devoxelize_backward"):
+                  "spvo_devoxelize_backward", "spvo_epilogue_backward", "spvo_linear_backward"):
             getattr(L, f).restype = ct.c_int
         _lib = L
     return _lib
@@ -238,6 +240,39 @@ def linear(x, W, dtype="f32", scale=None, shift=None, relu=False, res=None, res_
                            Cout, DT[dtype])
     _chk(st, "linear")
     return out[:m]
+
+
+def epilogue_backward(dy, a, scale=None, shift=None, relu=False, res=None, res_after_act=False, dtype="f32"):
+    """Backward of act(scale * a + shift + res) (or act(...) + res with res_after_act) w.r.t.
+    a, res, scale and shift, given the raw product a: (da, dres, dscale, dshift)."""
+    dy = np.ascontiguousarray(dy, dtype=_sdt(dtype))
+    m, C = dy.shape
+    a = np.ascontiguousarray(a, dtype=_sdt(dtype)).reshape(m, C)
+    scale = None if scale is None else np.ascontiguousarray(scale, dtype=np.float32)
+    shift = None if shift is None else np.ascontiguousarray(shift, dtype=np.float32)
+    res = None if res is None else np.ascontiguousarray(res, dtype=_sdt(dtype)).reshape(m, C)
+    da = np.zeros((max(m, 1), C), _sdt(dtype))
+    dres = np.zeros((max(m, 1), C), _sdt(dtype))
+    dscale = np.zeros(C, np.float32)
+    dshift = np.zeros(C, np.float32)
+    st = lib().spvo_epilogue_backward(_p(dy), _p(a), _p(scale), _p(shift), int(relu), _p(res), int(res_after_act), m,
+                                      C, _p(da), _p(dres), _p(dscale), _p(dshift), DT[dtype])
+    _chk(st, "epilogue_backward")
+    return da[:m], dres[:m], dscale, dshift
+
+
+def linear_backward(x, W, da, dtype="f32"):
+    """Gradients of x @ W: (dx = da @ W^T in dtype, dW = x^T @ da in float32)."""
+    x = np.ascontiguousarray(x, dtype=_sdt(dtype))
+    W = np.ascontiguousarray(W, dtype=_sdt(dtype))
+    m, Cin = x.shape
+    Cout = W.shape[1]
+    da = np.ascontiguousarray(da, dtype=_sdt(dtype)).reshape(m, Cout)
+    dx = np.zeros((max(m, 1), Cin), _sdt(dtype))
+    dW = np.zeros((Cin, Cout), np.float32)
+    st = lib().spvo_linear_backward(_p(x), m, Cin, _p(W), Cout, _p(da), _p(dx), _p(dW), DT[dtype])
+    _chk(st, "linear_backward")
+    return dx[:m], dW
 
 
 def devoxelize(grid_coords, vfeat, xyz, voxel_size, stride_log2=0, mode="center", batch=None, pfeat=None,

@@ -580,6 +580,69 @@ int spvo_linear(const void* in, int64_t m, int32_t Cin, const void* W, const flo
     return SPVO_OK;
 }
 
+/* backward of the epilogue: the activation's input is formed in float32 the
+ * way the kernels form it, so that both take the ReLU's decision on the same
+ * value; everything after it is fp64 */
+int spvo_epilogue_backward(const void* dy, const void* a, const float* scale, const float* shift, int32_t relu,
+                           const void* res, int32_t res_after_act, int64_t m, int32_t C, void* da, void* dres,
+                           float* dscale, float* dshift, int32_t dtype) {
+    if (m < 0 || C <= 0 || !valid_dtype(dtype)) return SPVO_ERR_INVALID_ARG;
+    if (m > 0 && (!dy || !a)) return SPVO_ERR_INVALID_ARG;
+    double* ss = (double*)calloc((size_t)C, sizeof(double));
+    double* sb = (double*)calloc((size_t)C, sizeof(double));
+    if (!ss || !sb) {
+        free(ss);
+        free(sb);
+        return SPVO_ERR_CAPACITY;
+    }
+    for (int64_t i = 0; i < m; ++i) {
+        for (int32_t c = 0; c < C; ++c) {
+            const int64_t t = i * C + c;
+            const float av = (float)spvo_decode(a, t, dtype);
+            const float s = scale ? scale[c] : 1.0f, b = shift ? shift[c] : 0.0f;
+            float z = fmaf(av, s, b);
+            if (res && !res_after_act) z = z + (float)spvo_decode(res, t, dtype);
+            const double g = spvo_decode(dy, t, dtype);
+            const double gz = (!relu || z > 0.0f) ? g : 0.0;
+            if (da) spvo_round_store(gz * (double)s, da, t, dtype);
+            if (dres) spvo_round_store(res_after_act ? g : gz, dres, t, dtype);
+            ss[c] += gz * (double)av;
+            sb[c] += gz;
+        }
+    }
+    for (int32_t c = 0; c < C; ++c) {
+        if (dscale) dscale[c] = (float)ss[c];
+        if (dshift) dshift[c] = (float)sb[c];
+    }
+    free(ss);
+    free(sb);
+    return SPVO_OK;
+}
+
+int spvo_linear_backward(const void* in, int64_t m, int32_t Cin, const void* W, int32_t Cout, const void* da,
+                         void* din, float* dW, int32_t dtype) {
+    if (m < 0 || Cin <= 0 || Cout <= 0 || !W || !valid_dtype(dtype)) return SPVO_ERR_INVALID_ARG;
+    if (m > 0 && (!in || !da)) return SPVO_ERR_INVALID_ARG;
+    double* acc = (double*)calloc((size_t)Cin * Cout, sizeof(double));
+    if (!acc) return SPVO_ERR_CAPACITY;
+    for (int64_t i = 0; i < m; ++i) {
+        for (int32_t ci = 0; ci < Cin; ++ci) {
+            const double x = spvo_decode(in, i * Cin + ci, dtype);
+            double s = 0.0;
+            for (int32_t co = 0; co < Cout; ++co) {
+                const double g = spvo_decode(da, i * Cout + co, dtype);
+                s += g * spvo_decode(W, (int64_t)ci * Cout + co, dtype);
+                acc[(int64_t)ci * Cout + co] += x * g;
+            }
+            if (din) spvo_round_store(s, din, i * Cin + ci, dtype);
+        }
+    }
+    if (dW)
+        for (int64_t t = 0; t < (int64_t)Cin * Cout; ++t) dW[t] = (float)acc[t];
+    free(acc);
+    return SPVO_OK;
+}
+
 /* ------------------------------------------------------------------------- */
 /* devoxelize (trilinear over 8 neighbour voxels) + point MLP + add           */
 /* ------------------------------------------------------------------------- */

@@ -105,6 +105,23 @@ int spvo_devoxelize_backward(const int32_t* cidx, const float* cw, const void* d
 int spvo_linear(const void* in, int64_t m, int32_t Cin, const void* W, const float* scale, const float* shift,
                 const void* res, int32_t res_after_act, int32_t relu, void* out, int32_t Cout, int32_t dtype);
 
+/* Backward of the epilogue the convolutions and linear layers apply to their
+ * raw product a (Sec. 3.3's BN folded into scale / shift, then ReLU, with the
+ * residual before or after it):
+ *   z = fmaf(a, scale, shift) (+ res when res_after_act = 0), in float32;
+ *   gz = dy where relu = 0 or z > 0, else 0;
+ *   da = gz * scale (one rounding to dtype); dres = dy (res_after_act = 1) or gz;
+ *   dscale[c] = sum_i gz * a, dshift[c] = sum_i gz (fp64 sums, one rounding).
+ * scale / shift / res may be NULL (1, 0, 0); any output may be NULL. */
+int spvo_epilogue_backward(const void* dy, const void* a, const float* scale, const float* shift, int32_t relu,
+                           const void* res, int32_t res_after_act, int64_t m, int32_t C, void* da, void* dres,
+                           float* dscale, float* dshift, int32_t dtype);
+
+/* Gradients of the product out = in @ W: din = da @ W^T (one rounding to dtype),
+ * dW = in^T @ da (float32); fp64 sums. */
+int spvo_linear_backward(const void* in, int64_t m, int32_t Cin, const void* W, int32_t Cout, const void* da,
+                         void* din, float* dW, int32_t dtype);
+
 /* Devoxelize from a grid of voxel size voxel_size * 2^stride_log2 (coords in
  * that grid's units), optionally add the point MLP act(scale*(pfeat @ Wp)+shift).
  * corner_idx [n][8] / corner_w [n][8] (optional) receive the corner voxel index
