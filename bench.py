@@ -464,6 +464,20 @@ def backward_mode(args):
     wsd = spv.Workspace.for_devox_backward(n, m)
     ms = timed(lambda: spv.spv_devoxelize_backward(wsd, ci, cw, dout, m, out=dv))
     line("devoxelize backward C=96", ms, 0.0, 64 * n + 2 * C * n + 4 * C * m)
+    # the point branch's layer ReLU(scale * (x @ W) + shift) + res over the n points
+    pf = bf(synth.normal((n, C), 7, dtype="bf16"))
+    Wl = bf(synth.linear_weight(C, C, 8, "bf16"))
+    wsl = spv.Workspace.for_ops(n, C)
+    a = spv.spv_linear(wsl, pf, Wl)
+    sc = torch.from_numpy(0.5 + synth.uniform_cube(C, 1.0, 9)[:, 0] ** 2).to(dev)  # seeded, in [0.5, 1.5)
+    sh = torch.from_numpy(synth.normal((C,), 10, std=0.1)).to(dev)
+    wse = spv.Workspace.for_epilogue_backward(n, C)
+    ms = timed(lambda: spv.spv_epilogue_backward(wse, dout, a, sc, sh, True, dout, True))
+    line("epilogue backward C=96 (BN + ReLU + residual, n points)", ms, 0.0, 2 * C * n * 4)
+    wlb = spv.Workspace.for_linear_backward(C, C)
+    da = spv.spv_epilogue_backward(wse, dout, a, sc, sh, True)[0]
+    ms = timed(lambda: spv.spv_linear_backward(wlb, pf, Wl, da))
+    line("linear backward 96->96 (dx and dW, n points)", ms, 2 * 2.0 * n * C * C, 2 * C * n * 3 + 4 * C * C)
 
 
 def cpu_baseline(xyz, convs, C, v=0.05):

@@ -428,6 +428,50 @@ spv_status spv_voxelize_backward(void* stream, const void* dvfeat, int64_t m, in
                                  void* dfeat, spv_dtype dt);
 
 /*
+ * spv_epilogue_backward -- backward of the epilogue the convolutions, the
+ * linear layers and spv_block apply to their raw product a (Sec. 3.3: BN folded
+ * into a per-channel scale and shift, ReLU, and the residual of a ResNet block
+ * before the activation or the fusion by addition after it):
+ *   forward  y = act(scale * a + shift + res)   (res_after_act = 0)
+ *            y = act(scale * a + shift) + res   (res_after_act = 1)
+ *   z = fmaf(a, scale, shift) (+ res when res_after_act = 0), in float32;
+ *   gz = dy where relu = 0 or z > 0, else 0;
+ *   da = gz * scale (one rounding to dt), dres = dy (res_after_act = 1) or gz;
+ *   dscale[c] = sum_i gz * a, dshift[c] = sum_i gz (fp64 in a fixed order, one
+ *   rounding: the same bits on every call).
+ * a is the op's output with scale = shift = res = NULL and relu = 0 (the same
+ * call without its epilogue).
+ * In:  dy, a, res [m][C] (dt; res may be NULL); scale, shift [C] f32 or NULL
+ *      (1, 0).
+ * Out: da, dres [m][C] (dt), dscale, dshift [C] f32; any may be NULL.
+ *      ws: spv_epilogue_backward_workspace_bytes(m, C) bytes, 256-byte aligned,
+ *      needed only with dscale or dshift.
+ * Errors: SPV_ERR_INVALID_ARG, SPV_ERR_CAPACITY.
+ */
+size_t spv_epilogue_backward_workspace_bytes(int64_t m, int32_t C);
+spv_status spv_epilogue_backward(void* stream, void* ws, size_t ws_bytes,
+                                 const void* dy, const void* a, const float* scale, const float* shift,
+                                 int32_t relu, const void* res, int32_t res_after_act, int64_t m, int32_t C,
+                                 void* da, void* dres, float* dscale, float* dshift, spv_dtype dt);
+
+/*
+ * spv_linear_backward -- gradients of the linear layer's product out = in @ W
+ * (the point branch's MLP of Sec. 3.3, a 1x1 shortcut):
+ *   din = da @ W^T  (fp32 accumulation, one rounding to dt)
+ *   dW  = in^T @ da (float32; deterministic: fixed partial sums in a fixed order)
+ * da is the gradient of the product (spv_epilogue_backward's da).
+ * In:  in [m][Cin], W [Cin][Cout], da [m][Cout] (dt); in, da, din 16-byte aligned.
+ * Out: din [m][Cin] (dt) and / or dW [Cin][Cout] f32 (either may be NULL).
+ *      ws: spv_linear_backward_workspace_bytes(Cin, Cout) bytes, 256-byte aligned.
+ * Errors: SPV_ERR_INVALID_ARG, SPV_ERR_CAPACITY, SPV_ERR_UNSUPPORTED (dW with
+ *      Cin * Cout > 65536).
+ */
+size_t spv_linear_backward_workspace_bytes(int32_t Cin, int32_t Cout);
+spv_status spv_linear_backward(void* stream, void* ws, size_t ws_bytes,
+                               const void* in, int64_t m, int32_t Cin, const void* W, int32_t Cout,
+                               const void* da, void* din, float* dW, spv_dtype dt);
+
+/*
  * spv_devoxelize_backward -- backward of the trilinear devoxelization w.r.t.
  * the voxel features (Sec. 3.3 "Sparse Devoxelization"):
  *   dvfeat[v] = sum over the points k and corners c with corner_idx[k][c] = v

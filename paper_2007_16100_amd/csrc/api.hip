@@ -640,6 +640,76 @@ spv_status spv_voxelize_backward(void* stream, const void* dvfeat, int64_t m, in
     return hip_check();
 }
 
+size_t spv_epilogue_backward_workspace_bytes(int64_t m, int32_t C) {
+    if (m < 0 || C <= 0) return 0;
+    Arena a(nullptr, 0);
+    a.take<double>(epilogue_backward_part_entries(m, C));
+    return a.used;
+}
+
+spv_status spv_epilogue_backward(void* stream, void* ws, size_t ws_bytes, const void* dy, const void* a,
+                                 const float* scale, const float* shift, int32_t relu, const void* res,
+                                 int32_t res_after_act, int64_t m, int32_t C, void* da, void* dres, float* dscale,
+                                 float* dshift, spv_dtype dt) {
+    if (m < 0 || C <= 0 || !valid_dt(dt)) return SPV_ERR_INVALID_ARG;
+    if (m > 0 && (!dy || !a)) return SPV_ERR_INVALID_ARG;
+    const bool sums = dscale || dshift;
+    if (sums) {
+        if (!ws_ok(ws)) return SPV_ERR_INVALID_ARG;
+        if (need(spv_epilogue_backward_workspace_bytes(m, C), ws_bytes)) return SPV_ERR_CAPACITY;
+    }
+    if (m == 0 && !sums) return SPV_OK;
+    EpiBwdArgs e{dy, a, scale, shift, relu ? 1 : 0, res, res_after_act ? 1 : 0, m, C, (int)dt, da, dres, dscale, dshift};
+    launch_epilogue_backward((hipStream_t)stream, e, sums ? (double*)ws : nullptr);
+    return hip_check();
+}
+
+// the packed transposed W (the input gradient runs on the linear kernel), then
+// the weight gradient's partial sums (sized as a 27-offset map's: the
+// workgroups of the identity map's one offset take as many slots)
+static size_t layout_linear_backward(void* ws, size_t bytes, int Cin, int Cout, void** wpack, float** partial) {
+    Arena a(ws, bytes);
+    a.take<Header>(1);
+    *wpack = plan_linear_ws(a, Cout, Cin);
+    *partial = (float*)plan_wgrad_ws(a, 27, Cin, Cout);
+    return a.used;
+}
+
+size_t spv_linear_backward_workspace_bytes(int32_t Cin, int32_t Cout) {
+    if (Cin <= 0 || Cout <= 0) return 0;
+    void* wp;
+    float* part;
+    return layout_linear_backward(nullptr, 0, Cin, Cout, &wp, &part);
+}
+
+spv_status spv_linear_backward(void* stream, void* ws, size_t ws_bytes, const void* in, int64_t m, int32_t Cin,
+                               const void* W, int32_t Cout, const void* da, void* din, float* dW, spv_dtype dt) {
+    if (!ws_ok(ws) || m < 0 || m >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !W || !valid_dt(dt))
+        return SPV_ERR_INVALID_ARG;
+    if (m > 0 && (!in || !da || (!din && !dW))) return SPV_ERR_INVALID_ARG;
+    if (!aligned16(in) || !aligned16(da) || !aligned16(din) || (din && (din == da || din == in)))
+        return SPV_ERR_INVALID_ARG;
+    if (dW && !wgrad_supported(Cin, Cout)) return SPV_ERR_UNSUPPORTED;
+    void* wpack;
+    float* partial;
+    if (need(layout_linear_backward(nullptr, 0, Cin, Cout, &wpack, &partial), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_linear_backward(ws, ws_bytes, Cin, Cout, &wpack, &partial);
+    const hipStream_t s = (hipStream_t)stream;
+    if (din && m > 0) {
+        // din = da @ W^T: the linear layer with Cout inputs, Cin outputs, W read transposed
+        LinearArgs l{da, nullptr, m, Cout, Cin, (int)dt, W, Cout, nullptr, nullptr, 0, nullptr, 0, din};
+        l.wt = 1;
+        launch_linear(s, l, wpack, false);
+    }
+    if (dW) {
+        // dW = in^T da: the weight gradient over the identity map (pair p = (p, p))
+        WgradArgs w{in, m, Cin, da, m, Cout, nullptr, nullptr, m, 1, 0, (int)dt};
+        w.slot_k3 = 27;
+        launch_wgrad(s, w, partial, dW);
+    }
+    return hip_check();
+}
+
 size_t spv_devoxelize_backward_workspace_bytes(int64_t n, int64_t m) {
     if (n < 0 || m < 0) return 0;
     Arena a(nullptr, 0);

@@ -61,7 +61,15 @@ void* plan_wgrad_ws(Arena& a, int K3, int Cin, int Cout) {
     return a.take<float>((size_t)K3 * wgrad_slices(Cin, Cout) * Cin * Cout);
 }
 
+// The pairs of offset k, clamped to the pair buffer.  Without off and pairs
+// the "map" is the identity on pair_bound rows, one offset: pair p = (p, p)
+// (the weight gradient of a linear layer, x^T dy).
 __device__ inline void pair_range(const int32_t* off, int k, int64_t pair_bound, int64_t& lo, int64_t& hi) {
+    if (!off) {
+        lo = 0;
+        hi = k == 0 ? pair_bound : 0;
+        return;
+    }
     lo = off[k];
     hi = off[k + 1];
     lo = lo < 0 ? 0 : (lo > pair_bound ? pair_bound : lo);
@@ -126,8 +134,12 @@ __global__ __launch_bounds__(64 * kWgWaves) void k_conv_wgrad_mfma(
         ii = -1;
         jj = -1;
         if (p < np) {
-            ii = pairs[2 * (c0 + p) + isel];
-            jj = pairs[2 * (c0 + p) + 1 - isel];
+            if (pairs) {
+                ii = pairs[2 * (c0 + p) + isel];
+                jj = pairs[2 * (c0 + p) + 1 - isel];
+            } else {
+                ii = jj = c0 + p;
+            }
         }
     };
     auto gather = [&](int64_t ii, int64_t jj) {
@@ -253,7 +265,7 @@ __global__ __launch_bounds__(256) void k_conv_wgrad_valu(const void* __restrict_
         const int ci = e / Cout, co = e - ci * Cout;
         float s = 0.f;
         for (int64_t p = lo + sl; p < hi; p += S) {
-            const int64_t i = pairs[2 * p + isel], j = pairs[2 * p + 1 - isel];
+            const int64_t i = pairs ? pairs[2 * p + isel] : p, j = pairs ? pairs[2 * p + 1 - isel] : p;
             if (i >= 0 && i < x_rows && j >= 0 && j < dy_rows)
                 s += ld_feat<DT>(x, i * Cin + ci) * ld_feat<DT>(dy, j * Cout + co);
         }
@@ -395,7 +407,10 @@ static void launch_wgrad_tpw(hipStream_t s, dim3 grid, const WgradArgs& a, float
 void launch_wgrad(hipStream_t s, const WgradArgs& a, float* partial, float* dW) {
     const int S = wgrad_slices(a.Cin, a.Cout);
     const dim3 grid((unsigned)S, (unsigned)a.K3);
-    const int G = wgrad_groups(a.K3, S);
+    // the buffer holds slot_k3 * S slots: G + K3 - 1 <= slot_k3 * S
+    const int sk = a.slot_k3 > a.K3 ? a.slot_k3 : a.K3;
+    int G = wgrad_groups(sk, S);
+    if (G > sk * S - a.K3 + 1) G = sk * S - a.K3 + 1;
     // the MFMA kernel gathers at most 8 pieces of 16 bytes per thread, i.e. 64
     // pieces (512 channels) of a pair's two rows, and holds both rows of 64
     // pairs in LDS: wider pairs run on the vector-ALU kernel
@@ -430,6 +445,114 @@ void launch_wgrad(hipStream_t s, const WgradArgs& a, float* partial, float* dW) 
                                                                                     per_k / 4, a.K3, (float4*)dW);
     else
         k_wgrad_reduce<<<blocks_for((int64_t)a.K3 * per_k, 256), 256, 0, s>>>(partial, S, per_k, a.K3, dW);
+}
+
+// ---------------------------------------------------------------------------
+// backward of the epilogue act(scale * a + shift (+ res)) (+ res) the convs and
+// linear layers apply to their raw product a.  The activation's input is formed
+// in float32 as fmaf(a, scale, shift) (+ res), the ReLU passes the gradient
+// where it is > 0; da = gz * scale rounds once (an exact fp64 product), dres is
+// dy or gz unchanged.  The per-channel sums dscale = sum gz * a and dshift =
+// sum gz run in fp64 in a fixed association: within a workgroup of kEbRows
+// rows, row lane q sums rows q, q + 4, ... in order and the four lanes are
+// added in order; a second kernel adds the workgroups' sums in contiguous
+// runs of the 256 threads, then the runs in order.
+// ---------------------------------------------------------------------------
+constexpr int kEbRows = 128;
+constexpr int kEbLanes = 4;
+
+size_t epilogue_backward_part_entries(int64_t m, int C) { return (size_t)blocks_for(m, kEbRows) * 2 * (size_t)C; }
+
+template <int DT>
+__global__ __launch_bounds__(64 * kEbLanes) void k_epi_backward(EpiBwdArgs a, double* part) {
+    __shared__ double red[kEbLanes][2][64];
+    const int cl = threadIdx.x & 63, rl = threadIdx.x >> 6;
+    const int c = blockIdx.y * 64 + cl;
+    const int64_t r0 = (int64_t)blockIdx.x * kEbRows;
+    const int64_t r1 = r0 + kEbRows < a.m ? r0 + kEbRows : a.m;
+    double ss = 0.0, sb = 0.0;
+    if (c < a.C) {
+        const float sc = a.scale ? a.scale[c] : 1.f, sh = a.shift ? a.shift[c] : 0.f;
+        const bool rb = a.res && !a.res_after;
+        // U rows per round: their loads first, then the rows in order
+        constexpr int U = 4;
+        for (int64_t i0 = r0 + rl; i0 < r1; i0 += U * kEbLanes) {
+            float av[U], g[U], rv[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t i = i0 + u * kEbLanes;
+                const int64_t t = i * a.C + c;
+                const bool in = i < r1;
+                av[u] = in ? ld_feat<DT>(a.a, t) : 0.f;
+                g[u] = in ? ld_feat<DT>(a.dy, t) : 0.f;
+                rv[u] = (in && rb) ? ld_feat<DT>(a.res, t) : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t i = i0 + u * kEbLanes;
+                if (i >= r1) break;
+                const int64_t t = i * a.C + c;
+                float z = fmaf(av[u], sc, sh);
+                if (rb) z = z + rv[u];
+                const float gz = (!a.relu || z > 0.f) ? g[u] : 0.f;
+                if (a.da) {
+                    const double d = (double)gz * (double)sc;
+                    if constexpr (DT == SPV_F32) ((float*)a.da)[t] = (float)d;
+                    else ((uint16_t*)a.da)[t] = to16<DT>(f64_to_f32_odd(d));
+                }
+                if (a.dres) st_feat<DT>(a.dres, t, a.res_after ? g[u] : gz);
+                ss += (double)gz * (double)av[u];
+                sb += (double)gz;
+            }
+        }
+    }
+    if (!part) return;  // the whole workgroup
+    red[rl][0][cl] = ss;
+    red[rl][1][cl] = sb;
+    __syncthreads();
+    if (rl == 0 && c < a.C) {
+        for (int q = 1; q < kEbLanes; ++q) {
+            ss += red[q][0][cl];
+            sb += red[q][1][cl];
+        }
+        part[((int64_t)blockIdx.x * 2) * a.C + c] = ss;
+        part[((int64_t)blockIdx.x * 2 + 1) * a.C + c] = sb;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_epi_reduce(const double* __restrict__ part, int64_t nblk, int C,
+                                                    float* __restrict__ dscale, float* __restrict__ dshift) {
+    __shared__ double rs[256], rb[256];
+    const int c = blockIdx.x;
+    const int64_t L = (nblk + 255) / 256;
+    const int64_t b0 = threadIdx.x * L, b1 = b0 + L < nblk ? b0 + L : nblk;
+    double ss = 0.0, sb = 0.0;
+    for (int64_t b = b0; b < b1; ++b) {
+        ss += part[(b * 2) * C + c];
+        sb += part[(b * 2 + 1) * C + c];
+    }
+    rs[threadIdx.x] = ss;
+    rb[threadIdx.x] = sb;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double s0 = 0.0, s1 = 0.0;
+        for (int q = 0; q < 256; ++q) {
+            s0 += rs[q];
+            s1 += rb[q];
+        }
+        if (dscale) dscale[c] = (float)s0;
+        if (dshift) dshift[c] = (float)s1;
+    }
+}
+
+void launch_epilogue_backward(hipStream_t s, const EpiBwdArgs& a, double* part) {
+    const bool sums = a.dscale || a.dshift;
+    const dim3 g(blocks_for(a.m, kEbRows), (unsigned)((a.C + 63) / 64));
+    double* p = sums ? part : nullptr;
+    if (a.dt == SPV_F32) k_epi_backward<SPV_F32><<<g, 64 * kEbLanes, 0, s>>>(a, p);
+    else if (a.dt == SPV_BF16) k_epi_backward<SPV_BF16><<<g, 64 * kEbLanes, 0, s>>>(a, p);
+    else k_epi_backward<SPV_F16><<<g, 64 * kEbLanes, 0, s>>>(a, p);
+    if (sums) k_epi_reduce<<<(unsigned)a.C, 256, 0, s>>>(part, (int64_t)g.x, a.C, a.dscale, a.dshift);
 }
 
 // ---------------------------------------------------------------------------

@@ -105,7 +105,7 @@ __global__ __launch_bounds__(64 * kLinWaves) void k_linear_mfma(
 template <int DT>
 __global__ __launch_bounds__(256) void k_linear_valu(const void* __restrict__ in, int Cin,
                                                      const int64_t* __restrict__ m_dev, int64_t m_cap,
-                                                     const void* __restrict__ W, int ldw,
+                                                     const void* __restrict__ W, int ldc, int ldcol,
                                                      const float* __restrict__ scale, const float* __restrict__ shift,
                                                      int relu, const void* __restrict__ res, int res_after,
                                                      void* __restrict__ out, int Cout) {
@@ -115,7 +115,8 @@ __global__ __launch_bounds__(256) void k_linear_valu(const void* __restrict__ in
         const int64_t i = t / Cout;
         const int co = (int)(t - i * Cout);
         float s = 0.f;
-        for (int ci = 0; ci < Cin; ++ci) s += ld_feat<DT>(in, i * Cin + ci) * ld_feat<DT>(W, (int64_t)ci * ldw + co);
+        for (int ci = 0; ci < Cin; ++ci)
+            s += ld_feat<DT>(in, i * Cin + ci) * ld_feat<DT>(W, (int64_t)ci * ldc + (int64_t)co * ldcol);
         float y = s * (scale ? scale[co] : 1.f) + (shift ? shift[co] : 0.f);
         const float r = res ? ld_feat<DT>(res, t) : 0.f;
         if (!res_after) y += r;
@@ -184,24 +185,25 @@ void launch_linear(hipStream_t s, const LinearArgs& a, void* wpack, bool prepack
     if (a.m_cap <= 0) return;
     if (linear_mfma_supported(a.Cin, a.Cout, a.dt)) {
         const int KCH = linear_kch(a.Cin), NB = (a.Cout + 15) / 16;
-        PackJob q{(const uint16_t*)a.W, (uint4*)wpack, 1, a.Cin, a.Cout, KCH, NB, (int64_t)KCH * NB * 64, a.ldw,
-                  (int64_t)a.Cin * a.ldw, 1};
+        PackJob q{(const uint16_t*)a.W, (uint4*)wpack, 1, a.Cin, a.Cout, KCH, NB, (int64_t)KCH * NB * 64,
+                  a.wt ? 1 : a.ldw, (int64_t)a.Cin * a.ldw, a.wt ? a.ldw : 1};
         if (!prepacked) launch_pack_job(s, q);
         if (a.dt == SPV_BF16) launch_lin_dt<SPV_BF16>(s, a, wpack);
         else launch_lin_dt<SPV_F16>(s, a, wpack);
         return;
     }
+    const int ldc = a.wt ? 1 : a.ldw, ldcol = a.wt ? a.ldw : 1;
     int64_t grid = (a.m_cap * a.Cout + 255) / 256;
     if (grid > 4096) grid = 4096;
     if (grid < 1) grid = 1;
     if (a.dt == SPV_F32)
-        k_linear_valu<SPV_F32><<<(unsigned)grid, 256, 0, s>>>(a.in, a.Cin, a.m_dev, a.m_cap, a.W, a.ldw, a.scale,
+        k_linear_valu<SPV_F32><<<(unsigned)grid, 256, 0, s>>>(a.in, a.Cin, a.m_dev, a.m_cap, a.W, ldc, ldcol, a.scale,
                                                               a.shift, a.relu, a.res, a.res_after, a.out, a.Cout);
     else if (a.dt == SPV_BF16)
-        k_linear_valu<SPV_BF16><<<(unsigned)grid, 256, 0, s>>>(a.in, a.Cin, a.m_dev, a.m_cap, a.W, a.ldw, a.scale,
+        k_linear_valu<SPV_BF16><<<(unsigned)grid, 256, 0, s>>>(a.in, a.Cin, a.m_dev, a.m_cap, a.W, ldc, ldcol, a.scale,
                                                                a.shift, a.relu, a.res, a.res_after, a.out, a.Cout);
     else
-        k_linear_valu<SPV_F16><<<(unsigned)grid, 256, 0, s>>>(a.in, a.Cin, a.m_dev, a.m_cap, a.W, a.ldw, a.scale,
+        k_linear_valu<SPV_F16><<<(unsigned)grid, 256, 0, s>>>(a.in, a.Cin, a.m_dev, a.m_cap, a.W, ldc, ldcol, a.scale,
                                                               a.shift, a.relu, a.res, a.res_after, a.out, a.Cout);
 }
 

@@ -353,6 +353,7 @@ struct LinearArgs {
     const void* res;         // [m][Cout] or nullptr
     int res_after;           // 1: res added after the activation
     void* out;               // [m][Cout]
+    int wt = 0;              // 1: W read transposed, W[ci][co] at W[co * ldw + ci]
 };
 bool linear_mfma_supported(int Cin, int Cout, int dt);
 void* plan_linear_ws(Arena& a, int Cin, int Cout);
@@ -393,6 +394,7 @@ struct WgradArgs {
     const int32_t* pairs;    // [pair_bound][2]
     int64_t pair_bound;
     int K3, transposed, dt;
+    int slot_k3 = 0;         // K3 the partial buffer was sized for (0: K3)
 };
 bool wgrad_supported(int Cin, int Cout);
 void* plan_wgrad_ws(Arena& a, int K3, int Cin, int Cout);
@@ -400,6 +402,26 @@ void* plan_wgrad_ws(Arena& a, int K3, int Cin, int Cout);
 void launch_wgrad(hipStream_t s, const WgradArgs& a, float* partial, float* dW);
 void launch_voxelize_backward(hipStream_t s, const void* dv, int C, const int32_t* counts, const int32_t* pt2vox,
                               int64_t n, int64_t m, void* dfeat, int dt);
+// backward of the conv / linear epilogue (scale, shift, ReLU, residual)
+struct EpiBwdArgs {
+    const void* dy;          // [m][C] gradient of the epilogue's output
+    const void* a;           // [m][C] the raw product the epilogue was applied to
+    const float* scale;      // [C] or nullptr (1)
+    const float* shift;      // [C] or nullptr (0)
+    int relu;
+    const void* res;         // [m][C] or nullptr
+    int res_after;
+    int64_t m;
+    int C, dt;
+    void* da;                // [m][C] or nullptr
+    void* dres;              // [m][C] or nullptr
+    float* dscale;           // [C] or nullptr
+    float* dshift;           // [C] or nullptr
+};
+// fp64 entries of the per-workgroup sums
+size_t epilogue_backward_part_entries(int64_t m, int C);
+void launch_epilogue_backward(hipStream_t s, const EpiBwdArgs& a, double* part);
+
 // devoxelization backward: the counting sort of the (point, corner) entries by
 // voxel; entries hold 8 * point + corner, rec the (entry, coefficient) pairs of
 // every voxel in ascending entry order

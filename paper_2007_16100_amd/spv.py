@@ -36,6 +36,8 @@ EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_voxelize_onto", "spv_pack
            "spv_sparse_conv_dgrad", "spv_wgrad_workspace_bytes", "spv_sparse_conv_wgrad",
            "spv_voxelize_backward",
            "spv_devoxelize_backward_workspace_bytes", "spv_devoxelize_backward", "spv_devoxelize",
+           "spv_epilogue_backward_workspace_bytes", "spv_epilogue_backward",
+           "spv_linear_backward_workspace_bytes", "spv_linear_backward",
            "spv_block_workspace_bytes", "spv_block", "spv_lookup", "spv_voxel_lookup", "spv_conv_kernel",
            "spv_sparse_conv_nbr_noalloc",
            "spv_block_conv_kernel", "spv_status_check", "spv_status_string", "spv_last_hip_error")
@@ -101,6 +103,12 @@ def lib():
         L.spv_voxelize_backward.argtypes = [vp, vp, i64, i32, vp, vp, i64, vp, i32]
         L.spv_devoxelize_backward.argtypes = [vp, vp, sz, vp, vp, vp, i64, i32, vp, i64, i32]
         L.spv_devoxelize_backward_workspace_bytes.argtypes = [i64, i64]
+        L.spv_epilogue_backward_workspace_bytes.argtypes = [i64, i32]
+        L.spv_epilogue_backward_workspace_bytes.restype = sz
+        L.spv_epilogue_backward.argtypes = [vp, vp, sz, vp, vp, vp, vp, i32, vp, i32, i64, i32, vp, vp, vp, vp, i32]
+        L.spv_linear_backward_workspace_bytes.argtypes = [i32, i32]
+        L.spv_linear_backward_workspace_bytes.restype = sz
+        L.spv_linear_backward.argtypes = [vp, vp, sz, vp, i64, i32, vp, i32, vp, vp, vp, i32]
         L.spv_devoxelize_backward_workspace_bytes.restype = sz
         L.spv_devoxelize.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, vp, i64, f32, i32, vp, i32, vp, i32, vp, vp,
                                      vp, i32, vp, i32, vp, vp]
@@ -124,7 +132,8 @@ def lib():
                   "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_map_children", "spv_sparse_conv_up",
                   "spv_sparse_conv_dgrad", "spv_sparse_conv_wgrad",
                   "spv_voxelize_backward",
-                  "spv_devoxelize_backward", "spv_devoxelize", "spv_block", "spv_lookup", "spv_voxel_lookup",
+                  "spv_devoxelize_backward", "spv_epilogue_backward", "spv_linear_backward", "spv_devoxelize",
+                  "spv_block", "spv_lookup", "spv_voxel_lookup",
                   "spv_sparse_conv_nbr_noalloc", "spv_status_check"):
             getattr(L, f).restype = ct.c_int
         _lib = L
@@ -170,6 +179,14 @@ class Workspace:
     @classmethod
     def for_devox_backward(cls, n: int, m: int, device="cuda"):
         return cls(lib().spv_devoxelize_backward_workspace_bytes(n, m), device)
+
+    @classmethod
+    def for_epilogue_backward(cls, m: int, C: int, device="cuda"):
+        return cls(max(lib().spv_epilogue_backward_workspace_bytes(m, C), 256), device)
+
+    @classmethod
+    def for_linear_backward(cls, Cin: int, Cout: int, device="cuda"):
+        return cls(lib().spv_linear_backward_workspace_bytes(Cin, Cout), device)
 
     @classmethod
     def for_block(cls, max_points: int, C: int, device="cuda"):
@@ -535,6 +552,35 @@ def spv_devoxelize_backward(ws: Workspace, corner_idx: torch.Tensor, corner_w: t
                                        C, _ptr(out), m, _DT[dout.dtype])
     _chk(st, "spv_devoxelize_backward")
     return out
+
+
+def spv_epilogue_backward(ws: Workspace, dy: torch.Tensor, a: torch.Tensor, scale: Optional[torch.Tensor] = None,
+                          shift: Optional[torch.Tensor] = None, relu: bool = False,
+                          res: Optional[torch.Tensor] = None, res_after_act: bool = False):
+    """(da, dres, dscale, dshift) of the epilogue act(scale * a + shift (+ res)) (+ res)."""
+    m, C = dy.shape
+    d = dy.device
+    da = torch.empty((max(m, 1), C), dtype=dy.dtype, device=d)
+    dres = torch.empty((max(m, 1), C), dtype=dy.dtype, device=d) if res is not None else None
+    dscale = torch.empty(C, dtype=torch.float32, device=d)
+    dshift = torch.empty(C, dtype=torch.float32, device=d)
+    st = lib().spv_epilogue_backward(_stream(), ws.ptr, ws.nbytes, _ptr(dy), _ptr(a), _ptr(scale), _ptr(shift),
+                                     int(relu), _ptr(res), int(res_after_act), m, C, _ptr(da), _ptr(dres),
+                                     _ptr(dscale), _ptr(dshift), _DT[dy.dtype])
+    _chk(st, "spv_epilogue_backward")
+    return da, dres, dscale, dshift
+
+
+def spv_linear_backward(ws: Workspace, x: torch.Tensor, W: torch.Tensor, da: torch.Tensor):
+    """(dx, dW) of the product x @ W, given its gradient da."""
+    m, Cin = x.shape
+    Cout = W.shape[1]
+    dx = torch.empty((max(m, 1), Cin), dtype=x.dtype, device=x.device)
+    dW = torch.empty((Cin, Cout), dtype=torch.float32, device=x.device)
+    st = lib().spv_linear_backward(_stream(), ws.ptr, ws.nbytes, _ptr(x), m, Cin, _ptr(W), Cout, _ptr(da), _ptr(dx),
+                                   _ptr(dW), _DT[x.dtype])
+    _chk(st, "spv_linear_backward")
+    return dx, dW
 
 
 def spv_devoxelize(ws: Workspace, grid_coords: torch.Tensor, vfeat: torch.Tensor, xyz: torch.Tensor,

@@ -145,6 +145,22 @@ def test_host_side_validation_without_gpu():
     need = L.spv_devoxelize_backward_workspace_bytes(1000, 700)
     assert need >= 1000 * 8 * 20 + 700 * 8
     assert L.spv_devoxelize_backward_workspace_bytes(-1, 700) == 0
+    # epilogue backward: sums without a workspace; a small one; negative sizes
+    epi = (ct.c_void_p(16), ct.c_void_p(16), None, None, 1, None, 0, 4, 8, ct.c_void_p(16), None, ct.c_void_p(16),
+           None, 1)
+    assert L.spv_epilogue_backward(None, None, 0, *epi) == spv.SPV_ERR_INVALID_ARG
+    assert L.spv_epilogue_backward(None, ws, 8, *epi) == spv.SPV_ERR_CAPACITY
+    assert L.spv_epilogue_backward(None, ws, 1 << 30, ct.c_void_p(16), ct.c_void_p(16), None, None, 1, None, 0, -1, 8,
+                                   None, None, None, None, 1) == spv.SPV_ERR_INVALID_ARG
+    assert L.spv_epilogue_backward_workspace_bytes(1000, 96) >= 4 * 2 * 96 * 8
+    # linear backward: misaligned rows, output aliasing the gradient, too wide for dW, small workspace
+    lin = lambda ws_, nb, x_, da_, din_, cin=32, cout=32: L.spv_linear_backward(
+        None, ws_, nb, x_, 4, cin, ct.c_void_p(16), cout, da_, din_, ct.c_void_p(16), 1)
+    assert lin(ws, 1 << 30, ct.c_void_p(18), ct.c_void_p(16), ct.c_void_p(32)) == spv.SPV_ERR_INVALID_ARG
+    assert lin(ws, 1 << 30, ct.c_void_p(16), ct.c_void_p(32), ct.c_void_p(32)) == spv.SPV_ERR_INVALID_ARG
+    assert lin(ws, 1 << 30, ct.c_void_p(16), ct.c_void_p(32), ct.c_void_p(48), 512, 256) == spv.SPV_ERR_UNSUPPORTED
+    assert lin(ws, 1024, ct.c_void_p(16), ct.c_void_p(32), ct.c_void_p(48)) == spv.SPV_ERR_CAPACITY
+    assert L.spv_linear_backward_workspace_bytes(32, 32) >= 27 * 32 * 32 * 4
     # misaligned feature pointer
     st = L.spv_sparse_conv(None, ws, 1 << 30, ct.c_void_p(18), 4, 8, ct.c_void_p(16), ct.c_void_p(16), 4, 27, 0,
                            ct.c_void_p(16), None, None, 0, ct.c_void_p(16), None, 4, 16, 1)

@@ -171,3 +171,99 @@ def test_devoxelize_backward_edges(spv):
     ws = spv.Workspace.for_devox_backward(n, m)
     spv.spv_devoxelize_backward(ws, dev(bad), dev(cw), dev(synth.normal((n, 8), 1110, dtype="f32"), "f32"), m)
     assert spv.spv_status_check(ws) == spv.SPV_ERR_RANGE
+
+
+def _epi_inputs(m, C, dtype, seed):
+    rng = np.random.default_rng(seed)
+    a = synth.normal((m, C), seed, dtype=dtype)
+    dy = synth.normal((m, C), seed + 1, dtype=dtype)
+    res = synth.normal((m, C), seed + 2, dtype=dtype)
+    s = (0.5 + rng.random(C)).astype(np.float32)
+    s[1] = -s[1]
+    b = (0.3 * rng.standard_normal(C)).astype(np.float32)
+    b[0] = 0.0  # rows 0..3 of channel 0: the activation's input is exactly 0
+    zero = synth.to_storage(np.zeros(4, np.float32), dtype)
+    a[:4, 0] = zero
+    res[:4, 0] = zero
+    return a, dy, res, s, b
+
+
+@pytest.mark.parametrize("dtype,C,m", [("bf16", 96, 20000), ("f32", 19, 3001), ("f16", 64, 777)])
+@pytest.mark.parametrize("relu,res_after_act", [(True, False), (True, True), (False, False)])
+def test_epilogue_backward(spv, dtype, C, m, relu, res_after_act):
+    a, dy, res, s, b = _epi_inputs(m, C, dtype, 1210)
+    ref = oracle.epilogue_backward(dy, a, s, b, relu, res, res_after_act, dtype)
+    ws = spv.Workspace.for_epilogue_backward(m, C)
+    args = (ws, dev(dy, dtype), dev(a, dtype), dev(s), dev(b), relu, dev(res, dtype), res_after_act)
+    got = spv.spv_epilogue_backward(*args)
+    again = spv.spv_epilogue_backward(*args)
+    da, dres, dscale, dshift = (host(got[0], dtype)[:m], host(got[1], dtype)[:m], host(got[2]), host(got[3]))
+    np.testing.assert_array_equal(da, ref[0])      # one rounding of an exact product: bit-exact
+    np.testing.assert_array_equal(dres, ref[1])    # dy or 0, unchanged
+    np.testing.assert_array_equal(host(again[2]), dscale)  # deterministic sums
+    np.testing.assert_array_equal(host(again[3]), dshift)
+    # fp64 sums in another order, one rounding to float32
+    np.testing.assert_allclose(dscale, ref[2], rtol=1e-6, atol=1e-6)
+    np.testing.assert_allclose(dshift, ref[3], rtol=1e-6, atol=1e-6)
+
+
+def test_epilogue_backward_empty_and_partial_outputs(spv):
+    d = "cuda"
+    ws = spv.Workspace.for_epilogue_backward(0, 8)
+    e = torch.zeros((0, 8), dtype=torch.bfloat16, device=d)
+    da, _, dscale, dshift = spv.spv_epilogue_backward(ws, e, e)
+    assert not dscale.any() and not dshift.any()
+    # no sums asked for: no workspace needed
+    L = spv.lib()
+    m, C = 100, 16
+    a, dy, _, s, b = _epi_inputs(m, C, "bf16", 1211)
+    out = torch.empty((m, C), dtype=torch.bfloat16, device=d)
+    dyt, at, st_, bt = dev(dy, "bf16"), dev(a, "bf16"), dev(s), dev(b)  # held until the call has run
+    st = L.spv_epilogue_backward(None, None, 0, spv._ptr(dyt), spv._ptr(at), spv._ptr(st_), spv._ptr(bt), 1, None, 0,
+                                 m, C, spv._ptr(out), None, None, None, spv.SPV_BF16)
+    assert st == spv.SPV_OK
+    torch.cuda.synchronize()
+    ref = oracle.epilogue_backward(dy, a, s, b, True, dtype="bf16")
+    np.testing.assert_array_equal(host(out, "bf16"), ref[0])
+
+
+@pytest.mark.parametrize("dtype,cin,cout,m", [("bf16", 96, 96, 30011), ("f16", 32, 64, 5000), ("f32", 24, 40, 2003),
+                                              ("bf16", 256, 19, 1500), ("bf16", 40, 24, 999)])
+def test_linear_backward(spv, dtype, cin, cout, m):
+    x = synth.normal((m, cin), 1212, dtype=dtype)
+    W = synth.linear_weight(cin, cout, 1213, dtype)
+    da = synth.normal((m, cout), 1214, dtype=dtype)
+    ws = spv.Workspace.for_linear_backward(cin, cout)
+    args = (ws, dev(x, dtype), dev(W, dtype), dev(da, dtype))
+    dx, dW = spv.spv_linear_backward(*args)
+    _, dW2 = spv.spv_linear_backward(*args)
+    np.testing.assert_array_equal(host(dW2), host(dW))  # deterministic
+    rdx, rdW = oracle.linear_backward(x, W, da, dtype)
+    parity.check(host(dx, dtype)[:m], rdx, dtype)
+    # fp32 sums of m terms: 1e-3 normwise and elementwise, as the conv weight gradient
+    parity.check(host(dW), rdW, "f32", normwise_tol=1e-3, elemwise_tol=1e-3)
+
+
+def test_point_branch_layer_backward_chain(spv):
+    """out = ReLU(scale * (x @ W) + shift) + res on the GPU: the raw product by spv_linear without
+    its epilogue, spv_epilogue_backward, spv_linear_backward, against the oracle's same chain."""
+    m, cin, cout, dtype = 12000, 64, 96, "bf16"
+    x = synth.normal((m, cin), 1215, dtype=dtype)
+    W = synth.linear_weight(cin, cout, 1216, dtype)
+    _, dy, res, s, b = _epi_inputs(m, cout, dtype, 1217)
+    wsl = spv.Workspace.for_ops(m, max(cin, cout))
+    a = spv.spv_linear(wsl, dev(x, dtype), dev(W, dtype))
+    a_ref = host(a, dtype)[:m]  # both chains start from the same raw product
+    parity.check(a_ref, oracle.linear(x, W, dtype), dtype)
+    wse = spv.Workspace.for_epilogue_backward(m, cout)
+    da, dres, dscale, dshift = spv.spv_epilogue_backward(wse, dev(dy, dtype), a, dev(s), dev(b), True,
+                                                         dev(res, dtype), True)
+    dx, dW = spv.spv_linear_backward(spv.Workspace.for_linear_backward(cin, cout), dev(x, dtype), dev(W, dtype), da)
+    rda, rdres, rdscale, rdshift = oracle.epilogue_backward(dy, a_ref, s, b, True, res, True, dtype)
+    rdx, rdW = oracle.linear_backward(x, W, rda, dtype)
+    np.testing.assert_array_equal(host(da, dtype)[:m], rda)
+    np.testing.assert_array_equal(host(dres, dtype)[:m], rdres)
+    np.testing.assert_allclose(host(dscale), rdscale, rtol=1e-6, atol=1e-6)
+    np.testing.assert_allclose(host(dshift), rdshift, rtol=1e-6, atol=1e-6)
+    parity.check(host(dx, dtype)[:m], rdx, dtype)
+    parity.check(host(dW), rdW, "f32", normwise_tol=1e-3, elemwise_tol=1e-3)
