@@ -464,6 +464,19 @@ def backward_mode(args):
     wsd = spv.Workspace.for_devox_backward(n, m)
     ms = timed(lambda: spv.spv_devoxelize_backward(wsd, ci, cw, dout, m, out=dv))
     line("devoxelize backward C=96", ms, 0.0, 64 * n + 2 * C * n + 4 * C * m)
+    # the same at stride 16 (the network's second devoxelization: 0.8 m voxels, thousands of corner
+    # entries on the densest)
+    cs = coords
+    for _ in range(4):
+        k2 = spv.spv_kernel_map(ws, cs, K=2, stride=2)
+        cs = k2.out_coords[: int(k2.m_out_dev.item())].contiguous()
+    m16 = cs.shape[0]
+    v16 = bf(synth.normal((m16, C), 11, dtype="bf16"))
+    _, ci16, cw16 = spv.spv_devoxelize(ws, cs, v16, d_xyz, 0.05, stride_log2=4, want_corners=True)
+    dv16 = torch.empty((m16, C), dtype=torch.float32, device=dev)
+    wsd16 = spv.Workspace.for_devox_backward(n, m16)
+    ms = timed(lambda: spv.spv_devoxelize_backward(wsd16, ci16, cw16, dout, m16, out=dv16))
+    line("devoxelize backward C=96, stride 16", ms, 0.0, 64 * n + 2 * C * n + 4 * C * m16)
     # the point branch's layer ReLU(scale * (x @ W) + shift) + res over the n points
     pf = bf(synth.normal((n, C), 7, dtype="bf16"))
     Wl = bf(synth.linear_weight(C, C, 8, "bf16"))

@@ -647,8 +647,8 @@ void launch_voxelize_backward(hipStream_t s, const void* dv, int C, const int32_
 // point's present corner weights).  A counting sort groups the entries by
 // voxel (count, scan, fill: inside a voxel the order is whatever the atomics
 // of the count gave); every entry then takes its place in ascending e among its
-// voxel's entries (it counts the smaller ones, so a voxel of L entries costs
-// L^2 comparisons spread over L threads); the gather sums a voxel's entries
+// voxel's entries (it counts the smaller ones of its chunk of 256, then finds
+// those of the other chunks by binary search); the gather sums a voxel's entries
 // a * dout[k] in that order, one fp32 fma after another, so the result is the
 // same bit for bit on every run.  Every voxel row is written, the empty ones
 // with zeros.
@@ -665,6 +665,8 @@ DvbWs plan_devox_backward_ws(Arena& a, int64_t n, int64_t m) {
     w.coef = a.take<float>(E);
     w.vox = a.take<int32_t>(E);
     w.rec = a.take<int2>(E);
+    w.chk = a.take<int2>(E);
+    w.longv = a.take<int32_t>((size_t)m + 1);
     return w;
 }
 
@@ -783,19 +785,64 @@ __global__ void k_dvb_fill(const int32_t* __restrict__ cidx, const float* __rest
     }
 }
 
-// entry i of voxel v goes to position off[v] + (the entries of v smaller than
-// it): entries are distinct, so the positions are too
+// Entry i of voxel v goes to position off[v] + (the entries of v smaller than
+// it); entries are distinct, so the positions are too.  A voxel's range (in
+// fill order) is cut into chunks of kDvbChunk: every entry first counts the
+// smaller entries of its own chunk.  A voxel of one chunk is then done (its
+// entry goes straight to its place in rec); in a longer one the entry goes to
+// that rank inside its chunk of chk (each chunk sorted), and the merge kernel
+// adds, by a binary search of every other chunk, the smaller entries there --
+// L * (kDvbChunk + (L / kDvbChunk) log kDvbChunk) comparisons for a voxel of L
+// entries instead of L^2.
+constexpr int kDvbChunk = 256;
+constexpr int kDvbLong = 64;  // longer voxels are gathered by a workgroup each
+
 __global__ void k_dvb_rank(const int32_t* __restrict__ off, int64_t m, int64_t cap, const int32_t* __restrict__ ent,
-                           const float* __restrict__ coef, const int32_t* __restrict__ vox, int2* __restrict__ rec) {
+                           const float* __restrict__ coef, const int32_t* __restrict__ vox, int2* __restrict__ rec,
+                           int2* __restrict__ chk, Header* h, int32_t* longv) {
     int64_t E = off[m];
     if (E > cap) E = cap;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < E; i += (int64_t)gridDim.x * blockDim.x) {
         const int32_t v = vox[i], key = ent[i];
         if ((uint64_t)(uint32_t)v >= (uint64_t)m) continue;  // only after a fill that raised kFlagInternal
         const int32_t lo = off[v], hi = off[v + 1];
+        const int32_t c0 = lo + ((int32_t)(i - lo) / kDvbChunk) * kDvbChunk;
+        const int32_t c1 = c0 + kDvbChunk < hi ? c0 + kDvbChunk : hi;
         int32_t r = 0;
-        for (int32_t j = lo; j < hi; ++j) r += ent[j] < key ? 1 : 0;
-        rec[lo + r] = make_int2(key, __float_as_int(coef[i]));
+        for (int32_t j = c0; j < c1; ++j) r += ent[j] < key ? 1 : 0;
+        const int2 e = make_int2(key, __float_as_int(coef[i]));
+        if (hi - lo <= kDvbChunk) rec[lo + r] = e;
+        else chk[c0 + r] = e;
+        // the voxels whose gather takes a workgroup, once each (by the first entry in fill order)
+        if (i == lo && hi - lo > kDvbLong)
+            longv[atomicAdd((unsigned long long*)&h->aux[0], 1ull)] = v;
+    }
+}
+
+__global__ void k_dvb_merge(const int32_t* __restrict__ off, int64_t m, int64_t cap, const int32_t* __restrict__ vox,
+                            const int2* __restrict__ chk, int2* __restrict__ rec) {
+    int64_t E = off[m];
+    if (E > cap) E = cap;
+    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < E; p += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t v = vox[p];  // any position of a voxel's range holds that voxel
+        if ((uint64_t)(uint32_t)v >= (uint64_t)m) continue;
+        const int32_t lo = off[v], hi = off[v + 1];
+        if (hi - lo <= kDvbChunk) continue;  // done by the rank kernel
+        const int2 e = chk[p];
+        const int32_t own = lo + ((int32_t)(p - lo) / kDvbChunk) * kDvbChunk;
+        int32_t r = (int32_t)(p - own);  // the smaller entries of its own chunk
+        for (int32_t c0 = lo; c0 < hi; c0 += kDvbChunk) {
+            if (c0 == own) continue;
+            // the entries of chunk [c0, c1) below e.x: a lower bound in the sorted chunk
+            int32_t a = c0, b = c0 + kDvbChunk < hi ? c0 + kDvbChunk : hi;
+            while (a < b) {
+                const int32_t mid = (a + b) >> 1;
+                if (chk[mid].x < e.x) a = mid + 1;
+                else b = mid;
+            }
+            r += a - c0;
+        }
+        rec[lo + r] = e;
     }
 }
 
@@ -822,9 +869,51 @@ __device__ inline void dvb_load(const void* p, int64_t i, float x[VEC]) {
     }
 }
 
-// thread per (voxel, VEC consecutive channels): its entries four at a time
-// (the loads first, then the fmas in entry order).  An entry past the points
-// (left only by a fill that raised kFlagInternal) reads point 0 with weight 0.
+// the entries [lo, hi) of one voxel into acc for channels c0 .. c0 + VEC - 1,
+// four at a time (the loads first, then the fmas in entry order).  An entry
+// past the points (left only by a fill that raised kFlagInternal) reads point
+// 0 with weight 0.
+template <int DT, int VEC>
+__device__ inline void dvb_sum_range(const int2* __restrict__ rec, const void* __restrict__ dout, int64_t n, int C,
+                                     int c0, int32_t lo, int32_t hi, float (&acc)[VEC]) {
+    int32_t i = lo;
+    for (; i + 4 <= hi; i += 4) {
+        int2 r[4];
+        float x[4][VEC];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            r[u] = rec[i + u];
+            if ((uint64_t)(uint32_t)(r[u].x >> 3) >= (uint64_t)n) r[u] = make_int2(0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) dvb_load<DT, VEC>(dout, (int64_t)(r[u].x >> 3) * C + c0, x[u]);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int c = 0; c < VEC; ++c) acc[c] = fmaf(__int_as_float(r[u].y), x[u][c], acc[c]);
+    }
+    for (; i < hi; ++i) {
+        int2 r = rec[i];
+        if ((uint64_t)(uint32_t)(r.x >> 3) >= (uint64_t)n) r = make_int2(0, 0);
+        float x[VEC];
+        dvb_load<DT, VEC>(dout, (int64_t)(r.x >> 3) * C + c0, x);
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) acc[c] = fmaf(__int_as_float(r.y), x[c], acc[c]);
+    }
+}
+
+template <int VEC>
+__device__ inline void dvb_store(float* o, const float (&acc)[VEC]) {
+    if constexpr (VEC == 1) {
+        o[0] = acc[0];
+    } else {
+#pragma unroll
+        for (int c = 0; c < VEC; c += 4) *(float4*)(o + c) = make_float4(acc[c], acc[c + 1], acc[c + 2], acc[c + 3]);
+    }
+}
+
+// thread per (voxel, VEC consecutive channels) of the voxels of at most
+// kDvbLong entries (the others are the long kernel's)
 template <int DT, int VEC>
 __global__ void k_dvb_gather(const int32_t* __restrict__ off, const int2* __restrict__ rec, const void* __restrict__ dout,
                              int64_t n, int C, int64_t m, float* __restrict__ dv) {
@@ -833,40 +922,62 @@ __global__ void k_dvb_gather(const int32_t* __restrict__ off, const int2* __rest
         const int64_t v = t / G;
         const int c0 = (int)(t - v * G) * VEC;
         const int32_t lo = off[v], hi = off[v + 1];
+        if (hi - lo > kDvbLong) continue;
         float acc[VEC];
 #pragma unroll
         for (int c = 0; c < VEC; ++c) acc[c] = 0.f;
-        int32_t i = lo;
-        for (; i + 4 <= hi; i += 4) {
-            int2 r[4];
-            float x[4][VEC];
+        dvb_sum_range<DT, VEC>(rec, dout, n, C, c0, lo, hi, acc);
+        dvb_store<VEC>(dv + v * C + c0, acc);
+    }
+}
+
+// a workgroup per voxel of more than kDvbLong entries (listed by the rank
+// kernel): with G channel groups, P = 256 / G parts of the entry range are
+// summed by their own threads, each in entry order, and the parts are added
+// in part order -- a fixed association for the voxel's length and C
+template <int DT, int VEC>
+__global__ __launch_bounds__(256) void k_dvb_gather_long(const Header* h, const int32_t* __restrict__ longv, int64_t m,
+                                                         const int32_t* __restrict__ off,
+                                                         const int2* __restrict__ rec, const void* __restrict__ dout,
+                                                         int64_t n, int C, float* __restrict__ dv) {
+    __shared__ float red[256][VEC];
+    int64_t nl = h->aux[0];
+    if (nl > m) nl = m;
+    const int G = C / VEC;
+    const int P = G >= 256 ? 1 : 256 / G;
+    const int q = threadIdx.x / G, g = threadIdx.x - q * G;  // G >= 256: q = 0, g = threadIdx.x
+    for (int64_t e = blockIdx.x; e < nl; e += gridDim.x) {
+        const int32_t v = longv[e];
+        if ((uint64_t)(uint32_t)v >= (uint64_t)m) continue;  // the whole workgroup
+        const int32_t lo = off[v], hi = off[v + 1];
+        if (G >= 256) {
+            for (int gg = threadIdx.x; gg < G; gg += 256) {
+                float acc[VEC];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                r[u] = rec[i + u];
-                if ((uint64_t)(uint32_t)(r[u].x >> 3) >= (uint64_t)n) r[u] = make_int2(0, 0);
+                for (int c = 0; c < VEC; ++c) acc[c] = 0.f;
+                dvb_sum_range<DT, VEC>(rec, dout, n, C, gg * VEC, lo, hi, acc);
+                dvb_store<VEC>(dv + (int64_t)v * C + gg * VEC, acc);
             }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) dvb_load<DT, VEC>(dout, (int64_t)(r[u].x >> 3) * C + c0, x[u]);
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-#pragma unroll
-                for (int c = 0; c < VEC; ++c) acc[c] = fmaf(__int_as_float(r[u].y), x[u][c], acc[c]);
+            continue;
         }
-        for (; i < hi; ++i) {
-            int2 r = rec[i];
-            if ((uint64_t)(uint32_t)(r.x >> 3) >= (uint64_t)n) r = make_int2(0, 0);
-            float x[VEC];
-            dvb_load<DT, VEC>(dout, (int64_t)(r.x >> 3) * C + c0, x);
+        const int32_t len = (hi - lo + P - 1) / P;
+        float acc[VEC];
 #pragma unroll
-            for (int c = 0; c < VEC; ++c) acc[c] = fmaf(__int_as_float(r.y), x[c], acc[c]);
+        for (int c = 0; c < VEC; ++c) acc[c] = 0.f;
+        if (q < P) {
+            const int32_t a = lo + q * len, b = a + len < hi ? a + len : hi;
+            if (a < b) dvb_sum_range<DT, VEC>(rec, dout, n, C, g * VEC, a, b, acc);
         }
-        float* o = dv + v * C + c0;
-        if constexpr (VEC == 1) {
-            o[0] = acc[0];
-        } else {
 #pragma unroll
-            for (int c = 0; c < VEC; c += 4) *(float4*)(o + c) = make_float4(acc[c], acc[c + 1], acc[c + 2], acc[c + 3]);
+        for (int c = 0; c < VEC; ++c) red[threadIdx.x][c] = acc[c];
+        __syncthreads();
+        if (q == 0) {
+            for (int qq = 1; qq < P; ++qq)
+#pragma unroll
+                for (int c = 0; c < VEC; ++c) acc[c] += red[qq * G + g][c];
+            dvb_store<VEC>(dv + (int64_t)v * C + g * VEC, acc);
         }
+        __syncthreads();
     }
 }
 
@@ -876,6 +987,8 @@ static void launch_dvb_gather(hipStream_t s, const DvbWs& w, const void* dout, i
     int64_t g = blocks_for(m * (C / VEC), 256);
     if (g > 16384) g = 16384;
     k_dvb_gather<DT, VEC><<<(unsigned)g, 256, 0, s>>>(w.off, w.rec, dout, n, C, m, dv);
+    const int64_t gl = m < 1024 ? m : 1024;
+    k_dvb_gather_long<DT, VEC><<<(unsigned)gl, 256, 0, s>>>(w.h, w.longv, m, w.off, w.rec, dout, n, C, dv);
 }
 
 void launch_devoxelize_backward(hipStream_t s, const DvbWs& w, const int32_t* cidx, const float* cw, const void* dout,
@@ -892,7 +1005,8 @@ void launch_devoxelize_backward(hipStream_t s, const DvbWs& w, const int32_t* ci
         k_dvb_fill<<<(unsigned)gp, 256, 0, s>>>(cidx, cw, n, m, w.h, w.slot, w.off, w.ent, w.coef, w.vox);
         int64_t gr = blocks_for(8 * n, 256);
         if (gr > 16384) gr = 16384;
-        k_dvb_rank<<<(unsigned)gr, 256, 0, s>>>(w.off, m, 8 * n, w.ent, w.coef, w.vox, w.rec);
+        k_dvb_rank<<<(unsigned)gr, 256, 0, s>>>(w.off, m, 8 * n, w.ent, w.coef, w.vox, w.rec, w.chk, w.h, w.longv);
+        k_dvb_merge<<<(unsigned)gr, 256, 0, s>>>(w.off, m, 8 * n, w.vox, w.chk, w.rec);
     }
     const bool vec = (((uintptr_t)dout | (uintptr_t)dv) & 15u) == 0;
     if (dt == SPV_F32) {

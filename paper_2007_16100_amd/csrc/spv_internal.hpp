@@ -435,6 +435,8 @@ struct DvbWs {
     float* coef;    // [8n] their coefficients
     int32_t* vox;   // [8n] their voxels
     int2* rec;      // [8n] (entry, coefficient bits), sorted within each voxel
+    int2* chk;      // [8n] the same, sorted within chunks of a long voxel's range
+    int32_t* longv; // [m + 1] the voxels gathered by a workgroup each (count in h->aux[0])
 };
 DvbWs plan_devox_backward_ws(Arena& a, int64_t n, int64_t m);
 void launch_devoxelize_backward(hipStream_t s, const DvbWs& w, const int32_t* cidx, const float* cw, const void* dout,

@@ -137,10 +137,11 @@ def test_devoxelize_backward(spv, sweep, mode, stride_log2, C, dtype):
 
 
 def test_devoxelize_backward_edges(spv):
-    """Voxels with 0 to ~80 terms (over 64 and under), three voxels with none, absent corners, weights summing
-    to 0, odd C (one channel per thread), a misaligned gradient (no vector loads) and a corner index past m."""
+    """Voxels with 0 to ~80 terms, and of 300 to 1500 (several chunks of 256: the merge by binary search), three
+    voxels with none, absent corners, weights summing to 0, odd C (one channel per thread), a misaligned gradient
+    (no vector loads) and a corner index past m."""
     rng = np.random.default_rng(1108)
-    lengths = np.arange(71)
+    lengths = np.concatenate([np.arange(71), [256, 257, 300, 777, 1500]])
     m = len(lengths) + 3  # the last three voxels get no terms: their rows must be zeros
     # point k has corner 0 on voxel owner[k]; each other corner on a random voxel below len(lengths) with
     # probability 1/20, else absent
