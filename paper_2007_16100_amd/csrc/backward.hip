@@ -520,6 +520,102 @@ __global__ __launch_bounds__(64 * kEbLanes) void k_epi_backward(EpiBwdArgs a, do
     }
 }
 
+// The same, VEC channels per thread (16-byte loads and stores; C % VEC == 0,
+// C / VEC <= 256, 16-byte aligned rows): thread (lane q, group g) of the
+// L = 256 / G lanes takes rows q, q + L, ... of the workgroup's kEbRows; the
+// lanes' sums are added in lane order.
+template <int DT, int VEC>
+__device__ inline void epi_ld(const void* p, int64_t i, float (&x)[VEC]) {
+    if constexpr (DT == SPV_F32) {
+        const float4 v = *(const float4*)((const float*)p + i);
+        x[0] = v.x;
+        x[1] = v.y;
+        x[2] = v.z;
+        x[3] = v.w;
+    } else {
+        const uint4 v = *(const uint4*)((const uint16_t*)p + i);
+        const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            x[2 * j] = from16<DT>(u[j] & 0xffffu);
+            x[2 * j + 1] = from16<DT>(u[j] >> 16);
+        }
+    }
+}
+template <int DT, int VEC>
+__device__ inline void epi_st(void* p, int64_t i, const float (&x)[VEC]) {
+    if constexpr (DT == SPV_F32) {
+        *(float4*)((float*)p + i) = make_float4(x[0], x[1], x[2], x[3]);
+    } else {
+        uint32_t u[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) u[j] = (uint32_t)to16<DT>(x[2 * j]) | ((uint32_t)to16<DT>(x[2 * j + 1]) << 16);
+        *(uint4*)((uint16_t*)p + i) = make_uint4(u[0], u[1], u[2], u[3]);
+    }
+}
+
+template <int DT, int VEC>
+__global__ __launch_bounds__(256) void k_epi_backward_vec(EpiBwdArgs a, double* part) {
+    __shared__ double red[256][2 * VEC];
+    const int G = a.C / VEC, L = 256 / G;
+    const int q = threadIdx.x / G, g = threadIdx.x - q * G;
+    const int64_t r0 = (int64_t)blockIdx.x * kEbRows;
+    const int64_t r1 = r0 + kEbRows < a.m ? r0 + kEbRows : a.m;
+    double ss[VEC], sb[VEC];
+#pragma unroll
+    for (int c = 0; c < VEC; ++c) ss[c] = sb[c] = 0.0;
+    if (q < L) {
+        float sc[VEC], sh[VEC];
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) {
+            sc[c] = a.scale ? a.scale[g * VEC + c] : 1.f;
+            sh[c] = a.shift ? a.shift[g * VEC + c] : 0.f;
+        }
+        const bool rb = a.res && !a.res_after;
+        for (int64_t i = r0 + q; i < r1; i += L) {
+            const int64_t t = i * a.C + g * VEC;
+            float av[VEC], gv[VEC], rv[VEC];
+            epi_ld<DT, VEC>(a.a, t, av);
+            epi_ld<DT, VEC>(a.dy, t, gv);
+            if (rb) epi_ld<DT, VEC>(a.res, t, rv);
+            float dz[VEC], dr[VEC];
+#pragma unroll
+            for (int c = 0; c < VEC; ++c) {
+                float z = fmaf(av[c], sc[c], sh[c]);
+                if (rb) z = z + rv[c];
+                const float gz = (!a.relu || z > 0.f) ? gv[c] : 0.f;
+                const double d = (double)gz * (double)sc[c];
+                dz[c] = (DT == SPV_F32) ? (float)d : f64_to_f32_odd(d);  // one rounding below
+                dr[c] = a.res_after ? gv[c] : gz;
+                ss[c] += (double)gz * (double)av[c];
+                sb[c] += (double)gz;
+            }
+            if (a.da) epi_st<DT, VEC>(a.da, t, dz);
+            if (a.dres) epi_st<DT, VEC>(a.dres, t, dr);
+        }
+    }
+    if (!part) return;  // the whole workgroup
+#pragma unroll
+    for (int c = 0; c < VEC; ++c) {
+        red[threadIdx.x][c] = ss[c];
+        red[threadIdx.x][VEC + c] = sb[c];
+    }
+    __syncthreads();
+    if (q == 0) {
+        for (int qq = 1; qq < L; ++qq)
+#pragma unroll
+            for (int c = 0; c < VEC; ++c) {
+                ss[c] += red[qq * G + g][c];
+                sb[c] += red[qq * G + g][VEC + c];
+            }
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) {
+            part[((int64_t)blockIdx.x * 2) * a.C + g * VEC + c] = ss[c];
+            part[((int64_t)blockIdx.x * 2 + 1) * a.C + g * VEC + c] = sb[c];
+        }
+    }
+}
+
 __global__ __launch_bounds__(256) void k_epi_reduce(const double* __restrict__ part, int64_t nblk, int C,
                                                     float* __restrict__ dscale, float* __restrict__ dshift) {
     __shared__ double rs[256], rb[256];
@@ -549,9 +645,20 @@ void launch_epilogue_backward(hipStream_t s, const EpiBwdArgs& a, double* part) 
     const bool sums = a.dscale || a.dshift;
     const dim3 g(blocks_for(a.m, kEbRows), (unsigned)((a.C + 63) / 64));
     double* p = sums ? part : nullptr;
-    if (a.dt == SPV_F32) k_epi_backward<SPV_F32><<<g, 64 * kEbLanes, 0, s>>>(a, p);
-    else if (a.dt == SPV_BF16) k_epi_backward<SPV_BF16><<<g, 64 * kEbLanes, 0, s>>>(a, p);
-    else k_epi_backward<SPV_F16><<<g, 64 * kEbLanes, 0, s>>>(a, p);
+    const int vec = a.dt == SPV_F32 ? 4 : 8;
+    const bool al = (((uintptr_t)a.dy | (uintptr_t)a.a | (uintptr_t)a.res | (uintptr_t)a.da | (uintptr_t)a.dres) &
+                     15u) == 0;
+    if (al && a.C % vec == 0 && a.C / vec <= 256) {
+        if (a.dt == SPV_F32) k_epi_backward_vec<SPV_F32, 4><<<g.x, 256, 0, s>>>(a, p);
+        else if (a.dt == SPV_BF16) k_epi_backward_vec<SPV_BF16, 8><<<g.x, 256, 0, s>>>(a, p);
+        else k_epi_backward_vec<SPV_F16, 8><<<g.x, 256, 0, s>>>(a, p);
+    } else if (a.dt == SPV_F32) {
+        k_epi_backward<SPV_F32><<<g, 64 * kEbLanes, 0, s>>>(a, p);
+    } else if (a.dt == SPV_BF16) {
+        k_epi_backward<SPV_BF16><<<g, 64 * kEbLanes, 0, s>>>(a, p);
+    } else {
+        k_epi_backward<SPV_F16><<<g, 64 * kEbLanes, 0, s>>>(a, p);
+    }
     if (sums) k_epi_reduce<<<(unsigned)a.C, 256, 0, s>>>(part, (int64_t)g.x, a.C, a.dscale, a.dshift);
 }
 
