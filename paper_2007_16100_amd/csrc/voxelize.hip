@@ -451,19 +451,30 @@ __device__ inline void mean_add_range(double (&acc)[VEC], const void* feat, cons
 template <int DT, int VEC>
 __device__ inline void mean_store(const double (&acc)[VEC], double N, void* vfeat, int64_t orow) {
     if (N < 1.0) N = 1.0;  // a given voxel no point falls into (scatter-mean onto a set): mean 0
+    // the quotients acc / N; for N a power of two (1 for most voxels) the product
+    // with 1 / N, which is exact and so the same value, without the division
+    double q[VEC];
+    const int ni = (int)N;
+    if ((ni & (ni - 1)) == 0) {
+        const double r = 1.0 / N;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) q[j] = acc[j] * r;
+    } else {
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) q[j] = acc[j] / N;
+    }
     if constexpr (VEC == 8) {
         uint32_t w[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            w[j] = (uint32_t)to16<DT>(f64_to_f32_odd(acc[2 * j] / N)) |
-                   ((uint32_t)to16<DT>(f64_to_f32_odd(acc[2 * j + 1] / N)) << 16);
+            w[j] = (uint32_t)to16<DT>(f64_to_f32_odd(q[2 * j])) |
+                   ((uint32_t)to16<DT>(f64_to_f32_odd(q[2 * j + 1])) << 16);
         *(uint4*)((uint16_t*)vfeat + orow) = make_uint4(w[0], w[1], w[2], w[3]);
     } else if constexpr (VEC == 4) {
-        *(float4*)((float*)vfeat + orow) =
-            make_float4((float)(acc[0] / N), (float)(acc[1] / N), (float)(acc[2] / N), (float)(acc[3] / N));
+        *(float4*)((float*)vfeat + orow) = make_float4((float)q[0], (float)q[1], (float)q[2], (float)q[3]);
     } else {
-        if constexpr (DT == SPV_F32) st_feat<DT>(vfeat, orow, (float)(acc[0] / N));
-        else st_feat<DT>(vfeat, orow, f64_to_f32_odd(acc[0] / N));
+        if constexpr (DT == SPV_F32) st_feat<DT>(vfeat, orow, (float)q[0]);
+        else st_feat<DT>(vfeat, orow, f64_to_f32_odd(q[0]));
     }
 }
 
