@@ -85,26 +85,39 @@ struct VoxFirst {
     int64_t nzero;
     int njobs;
     PackJob job[kMaxPackJobs];
+    int npack;        // the grid's last npack blocks run the packings, the others the rest
 };
 
 // Eq. 1 per point into the sort's key buffer, with the block's record (per-field
 // minima / maxima of its valid keys, its non-finite and out-of-range counts).
-// Grid-stride alongside: the header, the table, the sort's scratch, the packings.
+// Grid-stride alongside: the header, the table, the sort's scratch.  The weight
+// packings run in blocks of their own at the end of the grid, so that their
+// gathers' round trip does not delay the quantization.
 __global__ __launch_bounds__(kRsProducerBlock) void k_vq_quantize(VoxFirst f, const float* xyz,
                                                                   const int32_t* batch, int64_t n, float v,
                                                                   uint64_t* keys, int32_t* rec) {
+    const int nqb = (int)gridDim.x - f.npack;  // the quantizing blocks
+    if ((int)blockIdx.x >= nqb) {
+        const int64_t tp = (blockIdx.x - nqb) * (int64_t)blockDim.x + threadIdx.x;
+        const int64_t sp = (int64_t)f.npack * blockDim.x;
+        for (int j = 0; j < f.njobs; ++j) {
+            const PackJob& q = f.job[j];
+            for (int64_t t = tp; t < q.total; t += sp)
+                q.wpack[t] = pack_fragment(q.W, q.Cin, q.Cout, q.ldc, q.ldcol, q.ldk, q.KCH, q.NB, t);
+        }
+        return;
+    }
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         f.h->status = 0;
         f.h->m = 0;
         for (int i = 0; i < 4; ++i) f.h->aux[i] = 0;
     }
     const int64_t t0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t stride = (int64_t)nqb * blockDim.x;
     const int64_t nkw = (int64_t)(f.table.mask + 1) / 2;  // 16-byte runs of keys: 2 per bucket
     for (int64_t i = t0; i < nkw; i += stride)
         *(u64x2*)(f.table.keys + 8 * (i >> 1) + 2 * (i & 1)) = u64x2{kEmpty, kEmpty};
     for (int64_t i = t0; i < f.nzero; i += stride) f.zero[i] = 0u;
-    for (int j = 0; j < f.njobs; ++j) pack_job_run(f.job[j]);
 
     int mn[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
     int mx[4] = {(int)0x80000000, (int)0x80000000, (int)0x80000000, (int)0x80000000};
@@ -610,12 +623,20 @@ void launch_voxelize(hipStream_t s, const VoxelizeWs& w, const float* xyz, const
     f.zero = w.rs.zero;  // the sort's histograms and tile counters
     f.nzero = (int64_t)radix_zero_words(n);
     f.njobs = 0;
+    int64_t frags = 0;
     for (int j = 0; j < njobs && f.njobs < kMaxPackJobs; ++j)
-        if (jobs[j].total > 0) f.job[f.njobs++] = jobs[j];
-    // at most kRsMaxRecords blocks: every histogram block reduces all their records
+        if (jobs[j].total > 0) {
+            f.job[f.njobs++] = jobs[j];
+            frags += jobs[j].total;
+        }
+    // about one fragment per packing thread
+    f.npack = frags > 0 ? (int)blocks_for(frags, kRsProducerBlock) : 0;
+    if (f.npack > 256) f.npack = 256;
+    // at most kRsMaxRecords quantizing blocks: every histogram block reduces all their records
     unsigned nq = blocks_for(n, kRsProducerBlock);
     if (nq > kRsMaxRecords) nq = kRsMaxRecords;
-    k_vq_quantize<<<nq, kRsProducerBlock, 0, s>>>(f, xyz, batch, n, voxel_size, w.rs.ka, w.rs.rec);
+    k_vq_quantize<<<nq + (unsigned)f.npack, kRsProducerBlock, 0, s>>>(f, xyz, batch, n, voxel_size, w.rs.ka,
+                                                                      w.rs.rec);
     launch_radix_sort(s, w.rs, w.h, nullptr, n, nq);
     const int64_t nt = (int64_t)radix_tiles(n);
     k_vq_segments<<<(unsigned)nt, kRsThreads, 0, s>>>(w.rs, w.h, n, nt, coords, pt2vox, w.seg, w.plist, m_dev);
