@@ -411,6 +411,13 @@ void launch_wgrad(hipStream_t s, const WgradArgs& a, float* partial, float* dW) 
     const int sk = a.slot_k3 > a.K3 ? a.slot_k3 : a.K3;
     int G = wgrad_groups(sk, S);
     if (G > sk * S - a.K3 + 1) G = sk * S - a.K3 + 1;
+    if (!a.off) {
+        // the identity map's chunk count is known here: about eight chunks per
+        // workgroup, so that the reduction has fewer partial sums to add
+        const int64_t ch = (a.pair_bound + kWgChunk - 1) / kWgChunk;
+        const int64_t gi = ch / 8 > 1 ? ch / 8 : 1;
+        if (gi < G) G = (int)gi;
+    }
     // the MFMA kernel gathers at most 8 pieces of 16 bytes per thread, i.e. 64
     // pieces (512 channels) of a pair's two rows, and holds both rows of 64
     // pairs in LDS: wider pairs run on the vector-ALU kernel
