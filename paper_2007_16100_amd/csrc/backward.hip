@@ -46,7 +46,7 @@ bool wgrad_supported(int Cin, int Cout) { return (int64_t)Cin * Cout <= 256 * 25
 // partial sum per offset its range touches, to slot w + k: G + K3 - 1 slots
 // at most, which the slice buffer holds when G <= K3 * (S - 1).
 constexpr int kWgMaxK3 = 27;
-constexpr int kWgMaxGroups = 1024;
+constexpr int kWgMaxGroups = 512;
 __host__ __device__ inline int64_t wgrad_chunks_per_wg(int64_t chunks, int G) { return (chunks + G - 1) / G; }
 // LDS of the MFMA kernel: the transposed chunk tiles, then 3 * 28 int64 of offset data
 __host__ __device__ inline size_t wgrad_tiles_bytes(int Cin, int Cout) {
