@@ -450,6 +450,9 @@ def backward_mode(args):
 
     ms = timed(lambda: spv.spv_sparse_conv_dgrad(ws, dy, km.off, km.pairs, W, m, out=dx))
     line("conv dgrad 96->96 (plan included)", ms, F, 2 * 2 * C * m + 8 * P + 27 * C * C * 2)
+    nbr = spv.spv_kernel_map_nbr(ws, coords)
+    ms = timed(lambda: spv.spv_sparse_conv_dgrad_nbr(ws, dy, nbr, W, out=dx))
+    line("conv dgrad 96->96 on the neighbour table", ms, F, 2 * 2 * C * m + 108 * m + 27 * C * C * 2)
     wsw = spv.Workspace.for_wgrad(27, C, C)
     dW = torch.empty((27, C, C), dtype=torch.float32, device=dev)
     ms = timed(lambda: spv.spv_sparse_conv_wgrad(wsw, x, dy, km.off, km.pairs, 27, out=dW))

@@ -391,6 +391,27 @@ spv_status spv_sparse_conv_dgrad(void* stream, void* ws, size_t ws_bytes,
                                  spv_dtype dt);
 
 /*
+ * spv_sparse_conv_dgrad_nbr -- spv_sparse_conv_dgrad for a submanifold 3x3x3
+ * map given as its neighbour table (spv_kernel_map_nbr's [m][27], entry k of
+ * row i = j + 1 for the voxel j at c_i + delta_k), with no per-call plan.  The
+ * map of a set onto itself is symmetric: entry k of row i holds j exactly when
+ * entry 26 - k of row j holds i, so
+ *   dx[i] = sum over k of dy[nbr[i][k] - 1] @ W[26 - k]^T
+ * is the neighbour-table conv with each W[26 - k] read transposed by the
+ * weight packing.
+ * In:  dy [m_cap][Cout] (dt); nbr [m_cap][27]; W [27][Cin][Cout] (dt), the
+ *      forward weights; m_dev: device row count (NULL = m_cap).
+ * Out: dx [m_cap][Cin] (dt); rows < *m_dev are written.
+ * Errors: SPV_ERR_UNSUPPORTED for widths the neighbour-table kernel does not
+ *      take (Cin, Cout in {32, 64, 96, 128, 256}, 16-bit), otherwise as
+ *      spv_sparse_conv_nbr.
+ */
+spv_status spv_sparse_conv_dgrad_nbr(void* stream, void* ws, size_t ws_bytes,
+                                     const void* dy, int32_t Cout, const int32_t* nbr, const void* W,
+                                     void* dx, const int64_t* m_dev, int64_t m_cap, int32_t Cin,
+                                     spv_dtype dt);
+
+/*
  * spv_sparse_conv_wgrad -- weight gradient of spv_sparse_conv:
  *   dW[k] = sum over the pairs (i, j) of offset k of x[i]^T dy[j]
  * (roles of each pair swapped with transposed = 1); fp32 accumulation.  The

@@ -612,6 +612,31 @@ spv_status spv_sparse_conv_dgrad(void* stream, void* ws, size_t ws_bytes, const 
                             m_in_cap, Cin, dt);
 }
 
+spv_status spv_sparse_conv_dgrad_nbr(void* stream, void* ws, size_t ws_bytes, const void* dy, int32_t Cout,
+                                     const int32_t* nbr, const void* W, void* dx, const int64_t* m_dev, int64_t m_cap,
+                                     int32_t Cin, spv_dtype dt) {
+    if (!ws_ok(ws) || m_cap < 0 || m_cap >= ((int64_t)1 << 31) || Cin <= 0 || Cout <= 0 || !W || !valid_dt(dt))
+        return SPV_ERR_INVALID_ARG;
+    // the conv with Cout inputs and Cin outputs on the same table
+    if (!union_supported(27, Cout, Cin, dt) || m_cap * 27 * 4 > (int64_t)0xFFFFE000 ||
+        m_cap * (int64_t)Cout * 2 > (int64_t)0xFFFFE000)
+        return SPV_ERR_UNSUPPORTED;
+    if (m_cap > 0 && (!dy || !dx || !nbr)) return SPV_ERR_INVALID_ARG;
+    if (!aligned16(dy) || !aligned16(dx) || !aligned16(W) || dx == dy) return SPV_ERR_INVALID_ARG;
+    ConvLayout L;
+    if (need(layout_conv(nullptr, 0, m_cap, 27, Cout, Cin, dt, L, m_cap), ws_bytes)) return SPV_ERR_CAPACITY;
+    layout_conv(ws, ws_bytes, m_cap, 27, Cout, Cin, dt, L, m_cap);
+    if (m_cap == 0) return SPV_OK;
+    hipStream_t s = (hipStream_t)stream;
+    ConvPlan p = L.p;
+    p.nbr = const_cast<int32_t*>(nbr);  // read only
+    p.m_out_dev = m_dev;
+    p.res = nullptr;
+    launch_pack_job(s, conv_pack_job_mirrored(W, L.wpack, Cin, Cout, dt));
+    launch_conv_union(s, p, dy, Cout, m_cap, Cin, L.wpack, nullptr, nullptr, 0, dx, dt);
+    return hip_check();
+}
+
 spv_status spv_sparse_conv_wgrad(void* stream, void* ws, size_t ws_bytes, const void* x, int64_t x_rows, int32_t Cin,
                                  const void* dy, int64_t dy_rows, int32_t Cout, const int32_t* off, const int32_t* pairs,
                                  int64_t pair_cap, int32_t K3, int32_t transposed, float* dW, spv_dtype dt) {

@@ -641,6 +641,20 @@ PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int
     return q;
 }
 
+// The packing of W'[k] = W[26 - k]^T ([27][Cout][Cin] from W [27][Cin][Cout]):
+// the input gradient of a submanifold conv as a conv on the same neighbour
+// table.  W'[k][c][col] = W[26 - k][col][c] sits at (W + 26 Cin Cout) +
+// k (-Cin Cout) + c + col Cout.
+PackJob conv_pack_job_mirrored(const void* W, void* wpack, int Cin, int Cout, int dt) {
+    const int64_t per = (int64_t)Cin * Cout;
+    PackJob q{(const uint16_t*)W + 26 * per, (uint4*)wpack, 27, Cout, Cin, 0, 0, 0, 1, -per, Cout};
+    if (!conv_mfma_supported(Cout, Cin, dt)) return q;
+    q.KCH = conv_kch(Cout);
+    q.NB = Cin / 16;
+    q.total = (int64_t)27 * q.KCH * q.NB * 64;
+    return q;
+}
+
 // the MFMA kernels address the input rows, the neighbour table and the pair
 // list with 32-bit buffer offsets
 static bool conv_fits_buffers(int64_t in_rows, int Cin, int64_t pair_bound) {

@@ -334,6 +334,8 @@ __device__ inline void pack_job_run(const PackJob& q) {
 
 // ldc / ldk <= 0: W is a dense [K3][Cin][Cout] tensor; otherwise the leading
 // Cin x Cout block of each offset of a wider tensor (a channel slice)
+// W[26 - k]^T for every offset k of a 3x3x3 W [27][Cin][Cout] (a [27][Cout][Cin] packing)
+PackJob conv_pack_job_mirrored(const void* W, void* wpack, int Cin, int Cout, int dt);
 PackJob conv_pack_job(int K3, const void* W, void* wpack, int Cin, int Cout, int dt, int ldc = 0, int64_t ldk = 0,
                       int ldcol = 0);
 // the weight packing q as a launch of its own

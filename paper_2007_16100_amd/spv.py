@@ -33,7 +33,7 @@ EXPORTS = ("spv_workspace_bytes", "spv_voxelize", "spv_voxelize_onto", "spv_pack
            "spv_pack_weights", "spv_devoxelize_nbr", "spv_sparse_conv_nbr_packed", "spv_sparse_conv_up_packed", "spv_linear_packed",
            "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced",
            "spv_linear", "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_map_children", "spv_sparse_conv_up",
-           "spv_sparse_conv_dgrad", "spv_wgrad_workspace_bytes", "spv_sparse_conv_wgrad",
+           "spv_sparse_conv_dgrad", "spv_sparse_conv_dgrad_nbr", "spv_wgrad_workspace_bytes", "spv_sparse_conv_wgrad",
            "spv_voxelize_backward",
            "spv_devoxelize_backward_workspace_bytes", "spv_devoxelize_backward", "spv_devoxelize",
            "spv_epilogue_backward_workspace_bytes", "spv_epilogue_backward",
@@ -97,6 +97,7 @@ def lib():
         L.spv_sparse_conv_up.argtypes = [vp, vp, sz, vp, vp, i64, i32, vp, vp, i32, i32, vp, vp, vp, i32, vp, i64, i32,
                                          i32]
         L.spv_sparse_conv_dgrad.argtypes = [vp, vp, sz, vp, i64, i32, vp, vp, i64, i32, i32, vp, vp, vp, i64, i32, i32]
+        L.spv_sparse_conv_dgrad_nbr.argtypes = [vp, vp, sz, vp, i32, vp, vp, vp, vp, i64, i32, i32]
         L.spv_sparse_conv_wgrad.argtypes = [vp, vp, sz, vp, i64, i32, vp, i64, i32, vp, vp, i64, i32, i32, vp, i32]
         L.spv_wgrad_workspace_bytes.argtypes = [i32, i32, i32]
         L.spv_wgrad_workspace_bytes.restype = sz
@@ -130,7 +131,7 @@ def lib():
         for f in ("spv_voxelize", "spv_voxelize_onto", "spv_pack_weights", "spv_devoxelize_nbr", "spv_sparse_conv_nbr_packed",
                   "spv_sparse_conv_up_packed", "spv_linear_packed", "spv_kernel_map", "spv_sparse_conv", "spv_sparse_conv_sliced", "spv_linear",
                   "spv_kernel_map_nbr", "spv_sparse_conv_nbr", "spv_map_children", "spv_sparse_conv_up",
-                  "spv_sparse_conv_dgrad", "spv_sparse_conv_wgrad",
+                  "spv_sparse_conv_dgrad", "spv_sparse_conv_dgrad_nbr", "spv_sparse_conv_wgrad",
                   "spv_voxelize_backward",
                   "spv_devoxelize_backward", "spv_epilogue_backward", "spv_linear_backward", "spv_devoxelize",
                   "spv_block", "spv_lookup", "spv_voxel_lookup",
@@ -529,6 +530,19 @@ def spv_sparse_conv_wgrad(ws: Workspace, x: torch.Tensor, dy: torch.Tensor, off:
                                      Cout, _ptr(off), _ptr(pairs), pairs.shape[0], K3, int(transposed), _ptr(out),
                                      _DT[x.dtype])
     _chk(st, "spv_sparse_conv_wgrad")
+    return out
+
+
+def spv_sparse_conv_dgrad_nbr(ws: Workspace, dy: torch.Tensor, nbr: torch.Tensor, W: torch.Tensor,
+                              m_dev: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Input gradient of the 3x3x3 submanifold conv with weights W [27][Cin][Cout] on the neighbour table."""
+    m_cap, Cout = dy.shape
+    Cin = W.shape[1]
+    if out is None:
+        out = torch.empty((max(m_cap, 1), Cin), dtype=dy.dtype, device=dy.device)
+    st = lib().spv_sparse_conv_dgrad_nbr(_stream(), ws.ptr, ws.nbytes, _ptr(dy), Cout, _ptr(nbr), _ptr(W), _ptr(out),
+                                         _ptr(m_dev), m_cap, Cin, _DT[dy.dtype])
+    _chk(st, "spv_sparse_conv_dgrad_nbr")
     return out
 
 

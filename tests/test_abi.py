@@ -161,6 +161,13 @@ def test_host_side_validation_without_gpu():
     assert lin(ws, 1 << 30, ct.c_void_p(16), ct.c_void_p(32), ct.c_void_p(48), 512, 256) == spv.SPV_ERR_UNSUPPORTED
     assert lin(ws, 1024, ct.c_void_p(16), ct.c_void_p(32), ct.c_void_p(48)) == spv.SPV_ERR_CAPACITY
     assert L.spv_linear_backward_workspace_bytes(32, 32) >= 27 * 32 * 32 * 4
+    # input gradient on the neighbour table: a width the kernel does not take; dx aliasing dy
+    st = L.spv_sparse_conv_dgrad_nbr(None, ws, 1 << 30, ct.c_void_p(16), 48, ct.c_void_p(16), ct.c_void_p(16),
+                                     ct.c_void_p(32), None, 4, 48, 1)
+    assert st == spv.SPV_ERR_UNSUPPORTED
+    st = L.spv_sparse_conv_dgrad_nbr(None, ws, 1 << 30, ct.c_void_p(16), 32, ct.c_void_p(16), ct.c_void_p(16),
+                                     ct.c_void_p(16), None, 4, 32, 1)
+    assert st == spv.SPV_ERR_INVALID_ARG
     # misaligned feature pointer
     st = L.spv_sparse_conv(None, ws, 1 << 30, ct.c_void_p(18), 4, 8, ct.c_void_p(16), ct.c_void_p(16), 4, 27, 0,
                            ct.c_void_p(16), None, None, 0, ct.c_void_p(16), None, 4, 16, 1)

@@ -85,6 +85,29 @@ def test_conv_dgrad(spv, sweep, kind, cin, cout, dtype, step):
     parity.check(g, synth.from_storage(ref, dtype), dtype)
 
 
+@pytest.mark.parametrize("cin,cout,dtype,step", [(96, 96, "bf16", 2), (32, 64, "f16", 2), (128, 32, "bf16", 3),
+                                                 (256, 256, "bf16", 8)])
+def test_conv_dgrad_nbr(spv, sweep, cin, cout, dtype, step):
+    """The input gradient on the neighbour table (mirrored, transposed weights, no plan) against the oracle's
+    dgrad over the CSR map; the table has a live row count below its capacity."""
+    rc, _, _, _ = oracle.voxelize(sweep[::step], 0.05)
+    m = len(rc)
+    _, off, pairs = oracle.kernel_map(rc)
+    W = synth.conv_weight(27, cin, cout, 1111, dtype)
+    dy = synth.normal((m, cout), 1112, dtype=dtype)
+    cap = m + 37
+    ws = spv.Workspace.for_ops(cap, max(cin, cout))
+    coords = torch.zeros((cap, 4), dtype=torch.int32, device="cuda")
+    coords[:m] = dev(rc)
+    m_dev = torch.tensor([m], dtype=torch.int64, device="cuda")
+    nbr = spv.spv_kernel_map_nbr(ws, coords, m_dev=m_dev)
+    dyp = torch.zeros((cap, cout), dtype=TD[dtype], device="cuda")
+    dyp[:m] = dev(dy, dtype)
+    got = spv.spv_sparse_conv_dgrad_nbr(ws, dyp, nbr, dev(W, dtype), m_dev=m_dev)
+    ref = oracle.conv_dgrad(dy, off, pairs, W, m, dtype)
+    parity.check(synth.from_storage(host(got, dtype)[:m], dtype), synth.from_storage(ref, dtype), dtype)
+
+
 @pytest.mark.parametrize("kind,cin,cout,dtype,step", [
     ("subm", 32, 32, "bf16", 2), ("subm", 96, 96, "bf16", 4), ("subm", 64, 128, "f16", 4), ("subm", 16, 16, "f32", 8),
     ("subm", 256, 256, "bf16", 16), ("subm", 24, 40, "bf16", 8), ("k2s2", 64, 128, "bf16", 2),
