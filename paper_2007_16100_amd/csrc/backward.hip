@@ -44,11 +44,12 @@ bool wgrad_supported(int Cin, int Cout) { return (int64_t)Cin * Cout <= 256 * 25
 // contiguous ranges, one per workgroup, so the centre offset's many pairs
 // spread over as many workgroups as the rest.  A workgroup writes one
 // partial sum per offset its range touches, to slot w + k: G + K3 - 1 slots
-// at most, which the slice buffer holds when G <= K3 * (S - 1).
+// at most, which the slice buffer (sized for slot_k3 * S slots) must hold.
 constexpr int kWgMaxK3 = 27;
 constexpr int kWgMaxGroups = 512;
 __host__ __device__ inline int64_t wgrad_chunks_per_wg(int64_t chunks, int G) { return (chunks + G - 1) / G; }
-// LDS of the MFMA kernel: the transposed chunk tiles, then 3 * 28 int64 of offset data
+// LDS of the MFMA kernel: the transposed chunk tiles, then the offsets' pair
+// ranges and chunk prefix (27 + 27 + 28 int64)
 __host__ __device__ inline size_t wgrad_tiles_bytes(int Cin, int Cout) {
     return ((size_t)(Cin + Cout) * kWgLd * 2 + 15) & ~(size_t)15;
 }
