@@ -506,7 +506,7 @@ spv_status spv_linear_backward(void* stream, void* ws, size_t ws_bytes,
  *      reports them; dout [n][C] (dt).
  * Out: dvfeat [m][C] float32.
  * Errors: SPV_ERR_INVALID_ARG (null pointers, negative sizes, n >= 2^28,
- *      m >= 2^31 - 1), SPV_ERR_CAPACITY (ws too small); a corner index >= m is
+ *      m >= 2^31 - 1, dvfeat = dout), SPV_ERR_CAPACITY (ws too small); a corner index >= m is
  *      skipped and reported as SPV_ERR_RANGE through spv_status_check(ws).
  */
 size_t spv_devoxelize_backward_workspace_bytes(int64_t n, int64_t m);

@@ -747,6 +747,7 @@ spv_status spv_devoxelize_backward(void* stream, void* ws, size_t ws_bytes, cons
                                    int64_t m, spv_dtype dt) {
     if (!ws_ok(ws) || m < 0 || n < 0 || C <= 0 || !valid_dt(dt) || (m > 0 && !dvfeat)) return SPV_ERR_INVALID_ARG;
     if (n > 0 && (!corner_idx || !corner_w || !dout)) return SPV_ERR_INVALID_ARG;
+    if (dvfeat && (const void*)dvfeat == dout) return SPV_ERR_INVALID_ARG;  // the gather reads dout while writing
     // entry numbers 8n and voxel positions fit int32
     if (n >= ((int64_t)1 << 28) || m >= ((int64_t)1 << 31) - 1) return SPV_ERR_INVALID_ARG;
     if (need(spv_devoxelize_backward_workspace_bytes(n, m), ws_bytes)) return SPV_ERR_CAPACITY;

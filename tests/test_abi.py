@@ -140,6 +140,9 @@ def test_host_side_validation_without_gpu():
     dvb = (ct.c_void_p(16), ct.c_void_p(16), ct.c_void_p(16), 4, 8, ct.c_void_p(16), 4, 1)
     assert L.spv_devoxelize_backward(None, None, 1 << 30, *dvb) == spv.SPV_ERR_INVALID_ARG
     assert L.spv_devoxelize_backward(None, ws, 64, *dvb) == spv.SPV_ERR_CAPACITY
+    # the output aliasing the gradient
+    assert L.spv_devoxelize_backward(None, ws, 1 << 40, ct.c_void_p(16), ct.c_void_p(16), ct.c_void_p(48), 4, 8,
+                                     ct.c_void_p(48), 4, 1) == spv.SPV_ERR_INVALID_ARG
     assert L.spv_devoxelize_backward(None, ws, 1 << 40, ct.c_void_p(16), ct.c_void_p(16), ct.c_void_p(16), 1 << 28, 8,
                                      ct.c_void_p(16), 4, 1) == spv.SPV_ERR_INVALID_ARG
     need = L.spv_devoxelize_backward_workspace_bytes(1000, 700)
