@@ -137,14 +137,14 @@ def test_host_side_validation_without_gpu():
     assert L.spv_voxelize_backward(None, None, -1, 4, None, None, 0, None, 1) == spv.SPV_ERR_INVALID_ARG
     assert L.spv_devoxelize_backward(None, ws, 1 << 30, None, None, None, 4, 8, None, 4, 1) == spv.SPV_ERR_INVALID_ARG
     # devox backward: no workspace; a small one; sizes past the int32 entry numbers
-    dvb = (ct.c_void_p(16), ct.c_void_p(16), ct.c_void_p(16), 4, 8, ct.c_void_p(16), 4, 1)
+    dvb = (ct.c_void_p(16), ct.c_void_p(16), ct.c_void_p(16), 4, 8, ct.c_void_p(64), 4, 1)
     assert L.spv_devoxelize_backward(None, None, 1 << 30, *dvb) == spv.SPV_ERR_INVALID_ARG
     assert L.spv_devoxelize_backward(None, ws, 64, *dvb) == spv.SPV_ERR_CAPACITY
     # the output aliasing the gradient
     assert L.spv_devoxelize_backward(None, ws, 1 << 40, ct.c_void_p(16), ct.c_void_p(16), ct.c_void_p(48), 4, 8,
                                      ct.c_void_p(48), 4, 1) == spv.SPV_ERR_INVALID_ARG
     assert L.spv_devoxelize_backward(None, ws, 1 << 40, ct.c_void_p(16), ct.c_void_p(16), ct.c_void_p(16), 1 << 28, 8,
-                                     ct.c_void_p(16), 4, 1) == spv.SPV_ERR_INVALID_ARG
+                                     ct.c_void_p(64), 4, 1) == spv.SPV_ERR_INVALID_ARG
     need = L.spv_devoxelize_backward_workspace_bytes(1000, 700)
     assert need >= 1000 * 8 * 20 + 700 * 8
     assert L.spv_devoxelize_backward_workspace_bytes(-1, 700) == 0
